@@ -1,0 +1,181 @@
+/*
+ * frac.h -- C ABI of the Frac selective mode-bank scan for MI355X (gfx950).
+ *
+ * The operation ("Fractional State Space Transition for Long Sequence Modeling",
+ * Sec. 3.2 and the Appendix-D algorithm "Frac state transition"), per batch b,
+ * head h (group g = h*G/H) and token t, with M modes of base timescale tau_m:
+ *
+ *   dtt_t      = dt_t * lambda_t^(1/alpha_t)                     eq. tau-eff / rho-beta-def-frac
+ *   rho_{t,m}  = exp(-dtt_t / tau_m)                             eq. rho-beta-def-frac
+ *   beta_{t,m} = 1 - rho_{t,m}                                   Algorithm step 3 (and the remark
+ *                                                                 after it: no 1/lambda factor)
+ *   c_t = softmax_m(-alpha_t ln tau_m + read_logit_{t,m})        eq. read-softmax
+ *   w_t = softmax_m(-alpha_t ln tau_m + write_logit_{t,m})       write weights, same form
+ *   S_{t,m} = rho_{t,m} S_{t-1,m} + beta_{t,m} w_{t,m} B_t x_t^T eq. frac-selective-update, each
+ *                                                                 mode's state widened to N x P
+ *                                                                 by the B/C projections
+ *   y_t = sum_m c_{t,m} S_{t,m}^T C_t + D_h x_t                  eq. frac-readout + feedthrough
+ *                                                                 D (Sec. 3.3)
+ *
+ * The readout uses the state after token t's update.  The prefill/training scan
+ * evaluates this over whole sequences in chunks (the chunked parallel scan of the
+ * remark closing Sec. 3.2, with the log-space intra-chunk mixing of the appendix
+ * on the efficient implementation); the decode step is one token of the same
+ * recurrence on a cached state (same remark).
+ *
+ * Conventions shared by every entry point:
+ *  - Every tensor pointer is a DEVICE pointer owned by the caller.  The library
+ *    never allocates, frees or keeps them after the call returns.  Arrays are
+ *    C-contiguous in the layouts given below, 16-byte aligned.
+ *  - Calls are asynchronous on `stream` (a hipStream_t passed as void*; NULL is
+ *    the default stream).  Results are ready when the stream reaches them.
+ *  - The return value reports host-side validation and launch errors only.  On
+ *    error nothing is launched and frac_last_error() (thread-local) describes it.
+ *    Device data is not inspected: values outside the documented domains
+ *    (alpha outside (0,1], lambda <= 0, dt < 0, tau <= 0) give undefined results,
+ *    NaN/Inf propagate.
+ *  - io_dtype selects x, B, C, y (and dx, dB, dC, dy) as float32 or bfloat16;
+ *    dt, alpha, lambda, logits, tau, D and all states are float32.  Arithmetic
+ *    is float32 (bfloat16 operands of the matrix cores, float32 accumulation);
+ *    bfloat16 outputs are rounded to nearest even.
+ *  - Supported sizes: headdim P and dstate N multiples of 8 with N <= 128 and
+ *    P <= 128; 1 <= nmodes <= 8; H % G == 0; chunk 0 (auto) or 64.  Anything else
+ *    returns FRAC_ERR_UNSUPPORTED.  batch or seqlen 0 is a no-op.
+ *  - The library keeps no state between calls; it is safe to call from several
+ *    host threads on different streams.
+ */
+#ifndef FRAC_H
+#define FRAC_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  FRAC_OK = 0,
+  FRAC_ERR_INVALID_ARG = -1, /* null required pointer, bad size, misaligned pointer, H % G != 0 */
+  FRAC_ERR_UNSUPPORTED = -2, /* a size or option outside the supported set above */
+  FRAC_ERR_WORKSPACE = -3,   /* workspace missing or smaller than frac_scan_workspace_size() */
+  FRAC_ERR_HIP = -4          /* a HIP runtime call or kernel launch failed */
+} frac_status;
+
+typedef enum { FRAC_F32 = 0, FRAC_BF16 = 1 } frac_dtype;
+
+/* Problem sizes.  chunk: tokens per chunk of the parallel scan, 0 = library
+ * default (64).  io_dtype: a frac_dtype value. */
+typedef struct {
+  int64_t batch, seqlen, nheads, headdim, dstate, ngroups, nmodes, chunk;
+  int32_t io_dtype;
+} frac_shape;
+
+/* Inputs and outputs of the prefill / training forward scan.
+ *   x            [B,L,H,P] io_dtype        content input u_t (Algorithm input)
+ *   dt           [B,L,H]   f32             step sizes Delta_t > 0, used verbatim (no clipping)
+ *   Bm, Cm       [B,L,G,N] io_dtype        input / output projections of the widened state
+ *   alpha        f32, element (b,t,h) at alpha[b*s0 + t*s1 + h*s2] with s = alpha_stride;
+ *                strides may be 0 to broadcast (a per-head alpha is strides {0,0,1}).
+ *                Fractional order, 0 < alpha <= 1.  Required.
+ *   lambda       same addressing with lambda_stride; NULL means lambda = 1.
+ *   read_logit,
+ *   write_logit  [B,L,H,M] f32 content logits g_read(u_t), g_write(u_t); NULL = 0.
+ *   tau          [M] f32 base timescales tau_m > 0 (frac_default_tau gives the paper's bank).
+ *   D            [H] f32 feedthrough; NULL = no skip term.
+ *   init_state   [B,H,M,N,P] f32 state before token 0; NULL = zeros.
+ *   y            [B,L,H,P] io_dtype, written.
+ *   final_state  [B,H,M,N,P] f32 state after the last token, written; NULL = not produced. */
+typedef struct {
+  const void *x;
+  const float *dt;
+  const void *Bm, *Cm;
+  const float *alpha;
+  int64_t alpha_stride[3];
+  const float *lambda;
+  int64_t lambda_stride[3];
+  const float *read_logit, *write_logit;
+  const float *tau;
+  const float *D;
+  const float *init_state;
+  void *y;
+  float *final_state;
+} frac_fwd_args;
+
+/* Backward of frac_scan_fwd.  `fwd` holds the same inputs as the forward call
+ * (fwd.y and fwd.final_state are ignored); the backward recomputes everything it
+ * needs from them, nothing is carried between calls.
+ *   dy             [B,L,H,P] io_dtype   gradient of y
+ *   d_final_state  [B,H,M,N,P] f32      gradient of final_state; NULL = zero
+ *   dx             [B,L,H,P] io_dtype   written
+ *   ddt            [B,L,H] f32          written
+ *   dBm, dCm       [B,L,G,N] io_dtype   written, summed over the heads of each group
+ *   dD             [H] f32              written when fwd.D is non-NULL and dD is non-NULL
+ * Gradients with respect to alpha, lambda, the logits, tau and init_state are not
+ * produced. */
+typedef struct {
+  frac_fwd_args fwd;
+  const void *dy;
+  const float *d_final_state;
+  void *dx;
+  float *ddt;
+  void *dBm, *dCm;
+  float *dD;
+} frac_bwd_args;
+
+/* One decode token on a cached state (shape.seqlen must be 1).
+ *   x [B,H,P] io_dtype, dt [B,H] f32, Bm/Cm [B,G,N] io_dtype,
+ *   alpha / lambda addressed as alpha[b*s0 + h*s1] (strides may be 0; lambda NULL = 1),
+ *   read_logit / write_logit [B,H,M] f32 or NULL, tau [M], D [H] or NULL,
+ *   state [B,H,M,N,P] f32: read, then overwritten in place with the updated state,
+ *   y [B,H,P] io_dtype written. */
+typedef struct {
+  const void *x;
+  const float *dt;
+  const void *Bm, *Cm;
+  const float *alpha;
+  int64_t alpha_stride[2];
+  const float *lambda;
+  int64_t lambda_stride[2];
+  const float *read_logit, *write_logit;
+  const float *tau;
+  const float *D;
+  float *state;
+  void *y;
+} frac_step_args;
+
+/* Bytes of device workspace frac_scan_fwd (backward = 0) or frac_scan_bwd
+ * (backward = 1) needs for `shape`; 0 means none.  Returns 0 for an invalid shape
+ * (the scan call then reports the error). */
+size_t frac_scan_workspace_size(const frac_shape *shape, int backward);
+
+/* Chunked parallel scan, forward.  ws/ws_bytes: caller-owned device workspace of
+ * at least frac_scan_workspace_size(shape, 0) bytes (may be NULL when that is 0);
+ * its contents are scratch. */
+frac_status frac_scan_fwd(const frac_shape *shape, const frac_fwd_args *args, void *ws, size_t ws_bytes,
+                          void *stream);
+
+/* Chunked parallel scan, backward (see frac_bwd_args). */
+frac_status frac_scan_bwd(const frac_shape *shape, const frac_bwd_args *args, void *ws, size_t ws_bytes,
+                          void *stream);
+
+/* Bounded-state decode: one token, state updated in place. */
+frac_status frac_decode_step(const frac_shape *shape, const frac_step_args *args, void *stream);
+
+/* The paper's base timescale bank (Appendix E): M geometrically spaced values
+ * from tau_min to tau_max, both included (M = 1 gives tau_min), written to the
+ * HOST array out[M].  Returns FRAC_ERR_INVALID_ARG for M < 1, tau_min <= 0,
+ * tau_max < tau_min or out == NULL. */
+frac_status frac_default_tau(int M, double tau_min, double tau_max, float *out);
+
+/* Static description of a status code. */
+const char *frac_status_string(frac_status status);
+
+/* Message of the last error returned on the calling host thread ("" if none). */
+const char *frac_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* FRAC_H */

@@ -1,0 +1,186 @@
+"""Frac selective mode-bank scan for MI355X (gfx950).
+
+Python face of the C ABI in ``include/frac.h``.  The functions keep the C names
+without the ``frac_`` prefix: ``scan_fwd``, ``scan_bwd``, ``decode_step``,
+``scan_workspace_size``, ``default_tau``.  They take PyTorch tensors (device
+memory), allocate outputs and workspace with PyTorch, and launch on the current
+stream; the arithmetic runs in libfrac.so.
+"""
+from __future__ import annotations
+
+import ctypes
+from typing import Optional
+
+import torch
+
+from . import _lib
+from ._lib import FracError, FracShape, FracFwdArgs, FracBwdArgs, FracStepArgs, FRAC_BF16, FRAC_F32
+
+__all__ = ["scan_fwd", "scan_bwd", "decode_step", "scan_workspace_size", "default_tau", "FracError",
+           "CHUNK"]
+
+CHUNK = 64
+TAU_MIN = 1.0
+TAU_MAX = 2.0 ** 17
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _io_dtype(t: torch.Tensor) -> int:
+    if t.dtype == torch.bfloat16:
+        return FRAC_BF16
+    if t.dtype == torch.float32:
+        return FRAC_F32
+    raise TypeError("x/Bm/Cm must be float32 or bfloat16, got %s" % t.dtype)
+
+
+def _f32(t, name):
+    if t is None:
+        return None
+    if not isinstance(t, torch.Tensor) or t.dtype != torch.float32:
+        raise TypeError("%s must be a float32 tensor" % name)
+    if not t.is_contiguous():
+        raise ValueError("%s must be contiguous" % name)
+    return t
+
+
+def _strided(v, shape, device, name):
+    """float32 scalar / broadcastable tensor -> (tensor, element strides over `shape`)."""
+    if v is None:
+        return None, (0,) * len(shape)
+    if not isinstance(v, torch.Tensor):
+        v = torch.full((1,), float(v), dtype=torch.float32, device=device)
+    if v.dtype != torch.float32:
+        raise TypeError("%s must be float32" % name)
+    e = v.expand(shape)
+    return v, tuple(int(s) for s in e.stride())
+
+
+def _stream():
+    return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+def _shape(x, Bm, nmodes, chunk, seqlen=None):
+    if x.dim() == 4:
+        Bsz, L, H, P = x.shape
+        G, N = Bm.shape[2], Bm.shape[3]
+    else:
+        Bsz, H, P = x.shape
+        L = 1
+        G, N = Bm.shape[1], Bm.shape[2]
+    return FracShape(Bsz, L if seqlen is None else seqlen, H, P, N, G, nmodes, chunk, _io_dtype(x))
+
+
+def scan_workspace_size(shape: FracShape, backward: bool = False) -> int:
+    """Bytes of workspace frac_scan_fwd / frac_scan_bwd need (frac_scan_workspace_size)."""
+    return int(_lib.load().frac_scan_workspace_size(ctypes.byref(shape), int(bool(backward))))
+
+
+def default_tau(M: int, tau_min: float = TAU_MIN, tau_max: float = TAU_MAX, device=None) -> torch.Tensor:
+    """The paper's base timescale bank (frac_default_tau), as a float32 tensor."""
+    out = (ctypes.c_float * M)()
+    _lib.check(_lib.load().frac_default_tau(int(M), float(tau_min), float(tau_max), out))
+    t = torch.tensor(list(out), dtype=torch.float32)
+    return t if device is None else t.to(device)
+
+
+def _fwd_struct(x, dt, Bm, Cm, alpha, tau, lam, read_logit, write_logit, D, init_state, y, final_state):
+    Bsz, L, H, P = x.shape
+    if Bm.dtype != x.dtype or Cm.dtype != x.dtype:
+        raise TypeError("x, Bm and Cm must share one dtype")
+    for t, n in ((x, "x"), (Bm, "Bm"), (Cm, "Cm")):
+        if not t.is_contiguous():
+            raise ValueError("%s must be contiguous" % n)
+    alpha_t, a_str = _strided(alpha, (Bsz, L, H), x.device, "alpha")
+    lam_t, l_str = _strided(lam, (Bsz, L, H), x.device, "lambda")
+    a = FracFwdArgs()
+    a.x, a.dt, a.Bm, a.Cm = _ptr(x), _ptr(_f32(dt, "dt")), _ptr(Bm), _ptr(Cm)
+    a.alpha, a.alpha_stride = _ptr(alpha_t), (ctypes.c_int64 * 3)(*a_str)
+    a.lam, a.lambda_stride = _ptr(lam_t), (ctypes.c_int64 * 3)(*l_str)
+    a.read_logit, a.write_logit = _ptr(_f32(read_logit, "read_logit")), _ptr(_f32(write_logit, "write_logit"))
+    a.tau, a.D = _ptr(_f32(tau, "tau")), _ptr(_f32(D, "D"))
+    a.init_state = _ptr(_f32(init_state, "init_state"))
+    a.y, a.final_state = _ptr(y), _ptr(final_state)
+    keep = (alpha_t, lam_t)
+    return a, keep
+
+
+def scan_fwd(x, dt, Bm, Cm, alpha, tau, *, lam=None, read_logit=None, write_logit=None, D=None,
+             init_state=None, return_final_state=False, chunk=0, y=None, final_state=None, workspace=None):
+    """Chunked parallel scan, forward (frac_scan_fwd).
+
+    x [B,L,H,P], Bm/Cm [B,L,G,N] (float32 or bfloat16, one dtype); dt [B,L,H] f32;
+    alpha, lam: float or f32 tensor broadcastable to [B,L,H]; read/write logits
+    [B,L,H,M] f32; tau [M] f32; D [H] f32; init_state [B,H,M,N,P] f32.
+    Returns y, or (y, final_state) when return_final_state."""
+    M = int(tau.shape[0])
+    shape = _shape(x, Bm, M, chunk)
+    Bsz, L, H, P = x.shape
+    N = Bm.shape[3]
+    if y is None:
+        y = torch.empty_like(x)
+    if return_final_state and final_state is None:
+        final_state = torch.empty((Bsz, H, M, N, P), dtype=torch.float32, device=x.device)
+    args, keep = _fwd_struct(x, dt, Bm, Cm, alpha, tau, lam, read_logit, write_logit, D, init_state, y,
+                             final_state if return_final_state else None)
+    ws_bytes = scan_workspace_size(shape, False)
+    if workspace is None and ws_bytes:
+        workspace = torch.empty(ws_bytes, dtype=torch.uint8, device=x.device)
+    _lib.check(_lib.load().frac_scan_fwd(ctypes.byref(shape), ctypes.byref(args), _ptr(workspace),
+                                         ws_bytes if workspace is not None else 0, _stream()))
+    del keep
+    return (y, final_state) if return_final_state else y
+
+
+def scan_bwd(x, dt, Bm, Cm, alpha, tau, dy, *, lam=None, read_logit=None, write_logit=None, D=None,
+             init_state=None, d_final_state=None, chunk=0, workspace=None):
+    """Chunked parallel scan, backward (frac_scan_bwd).
+
+    Returns dict(dx, ddt, dBm, dCm, dD) with dD None when D is None."""
+    M = int(tau.shape[0])
+    shape = _shape(x, Bm, M, chunk)
+    Bsz, L, H, P = x.shape
+    if dy.dtype != x.dtype or not dy.is_contiguous():
+        raise TypeError("dy must be contiguous with the dtype of x")
+    fwd, keep = _fwd_struct(x, dt, Bm, Cm, alpha, tau, lam, read_logit, write_logit, D, init_state, None, None)
+    out = dict(dx=torch.empty_like(x), ddt=torch.empty_like(dt), dBm=torch.empty_like(Bm),
+               dCm=torch.empty_like(Cm), dD=None if D is None else torch.empty_like(D))
+    a = FracBwdArgs()
+    a.fwd = fwd
+    a.dy, a.d_final_state = _ptr(dy), _ptr(_f32(d_final_state, "d_final_state"))
+    a.dx, a.ddt, a.dBm, a.dCm, a.dD = (_ptr(out["dx"]), _ptr(out["ddt"]), _ptr(out["dBm"]), _ptr(out["dCm"]),
+                                       _ptr(out["dD"]))
+    ws_bytes = scan_workspace_size(shape, True)
+    if workspace is None and ws_bytes:
+        workspace = torch.empty(ws_bytes, dtype=torch.uint8, device=x.device)
+    _lib.check(_lib.load().frac_scan_bwd(ctypes.byref(shape), ctypes.byref(a), _ptr(workspace),
+                                         ws_bytes if workspace is not None else 0, _stream()))
+    del keep
+    return out
+
+
+def decode_step(state, x, dt, Bm, Cm, alpha, tau, *, lam=None, read_logit=None, write_logit=None, D=None,
+                y=None):
+    """One decode token (frac_decode_step): updates `state` [B,H,M,N,P] f32 in place,
+    returns y [B,H,P].  x [B,H,P], dt [B,H], Bm/Cm [B,G,N]."""
+    M = int(tau.shape[0])
+    shape = _shape(x, Bm, M, 0, seqlen=1)
+    Bsz, H, P = x.shape
+    if Bm.dtype != x.dtype or Cm.dtype != x.dtype:
+        raise TypeError("x, Bm and Cm must share one dtype")
+    alpha_t, a_str = _strided(alpha, (Bsz, H), x.device, "alpha")
+    lam_t, l_str = _strided(lam, (Bsz, H), x.device, "lambda")
+    if y is None:
+        y = torch.empty_like(x)
+    a = FracStepArgs()
+    a.x, a.dt, a.Bm, a.Cm = _ptr(x), _ptr(_f32(dt, "dt")), _ptr(Bm), _ptr(Cm)
+    a.alpha, a.alpha_stride = _ptr(alpha_t), (ctypes.c_int64 * 2)(*a_str)
+    a.lam, a.lambda_stride = _ptr(lam_t), (ctypes.c_int64 * 2)(*l_str)
+    a.read_logit, a.write_logit = _ptr(_f32(read_logit, "read_logit")), _ptr(_f32(write_logit, "write_logit"))
+    a.tau, a.D = _ptr(_f32(tau, "tau")), _ptr(_f32(D, "D"))
+    a.state, a.y = _ptr(_f32(state, "state")), _ptr(y)
+    _lib.check(_lib.load().frac_decode_step(ctypes.byref(shape), ctypes.byref(a), _stream()))
+    del alpha_t, lam_t
+    return y

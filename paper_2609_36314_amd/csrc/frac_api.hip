@@ -1,0 +1,242 @@
+// frac_api.hip -- the C ABI declared in include/frac.h: argument validation,
+// error reporting and dispatch to the kernel launchers.
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <string>
+
+#include "frac.h"
+#include "frac_kernels.h"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+frac_status fail(frac_status s, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return s;
+}
+
+frac_status ok() {
+  g_last_error.clear();
+  return FRAC_OK;
+}
+
+bool aligned16(const void* p) { return p == nullptr || (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+int next_tile_n(int64_t n) {
+  int t = 16;
+  while (t < n) t <<= 1;
+  return t;
+}
+
+// Validates the sizes common to every entry point and fills the size fields of p.
+frac_status fill_shape(const frac_shape* sh, frac::ScanParams& p) {
+  if (!sh) return fail(FRAC_ERR_INVALID_ARG, "shape is NULL");
+  if (sh->batch < 0 || sh->seqlen < 0) return fail(FRAC_ERR_INVALID_ARG, "batch and seqlen must be >= 0");
+  if (sh->nheads < 1 || sh->headdim < 1 || sh->dstate < 1 || sh->ngroups < 1 || sh->nmodes < 1)
+    return fail(FRAC_ERR_INVALID_ARG, "nheads, headdim, dstate, ngroups and nmodes must be >= 1");
+  if (sh->nheads % sh->ngroups != 0)
+    return fail(FRAC_ERR_INVALID_ARG, "nheads (%lld) is not a multiple of ngroups (%lld)", (long long)sh->nheads,
+                (long long)sh->ngroups);
+  if (sh->io_dtype != FRAC_F32 && sh->io_dtype != FRAC_BF16)
+    return fail(FRAC_ERR_INVALID_ARG, "io_dtype %d is not a frac_dtype", (int)sh->io_dtype);
+  if (sh->chunk != 0 && sh->chunk != 64) return fail(FRAC_ERR_UNSUPPORTED, "chunk %lld: only 64 (or 0 = auto) is built", (long long)sh->chunk);
+  if (sh->nmodes > 8) return fail(FRAC_ERR_UNSUPPORTED, "nmodes %lld > 8", (long long)sh->nmodes);
+  if (sh->dstate % 8 || sh->dstate > 128)
+    return fail(FRAC_ERR_UNSUPPORTED, "dstate %lld: must be a multiple of 8 and <= 128", (long long)sh->dstate);
+  if (sh->headdim % 8 || sh->headdim > 128)
+    return fail(FRAC_ERR_UNSUPPORTED, "headdim %lld: must be a multiple of 8 and <= 128", (long long)sh->headdim);
+  const int64_t lim = (int64_t)1 << 30;
+  if (sh->batch > lim || sh->seqlen > lim || sh->nheads > lim || sh->batch * sh->nheads > lim)
+    return fail(FRAC_ERR_UNSUPPORTED, "sizes beyond 2^30");
+  p.Bsz = (int)sh->batch;
+  p.L = (int)sh->seqlen;
+  p.H = (int)sh->nheads;
+  p.P = (int)sh->headdim;
+  p.N = (int)sh->dstate;
+  p.G = (int)sh->ngroups;
+  p.M = (int)sh->nmodes;
+  p.PP = (p.P + 15) / 16 * 16;
+  p.NP = next_tile_n(p.N);
+  p.io_bf16 = sh->io_dtype == FRAC_BF16;
+  // the forward scan runs (P/16) x (2 if N > 16 else 1) waves per workgroup, at most 8
+  const int halves = p.NP >= 32 ? 2 : 1;
+  if (p.PP / 16 * halves > 8)
+    return fail(FRAC_ERR_UNSUPPORTED, "headdim %d with dstate %d: headdim must be <= 64 when dstate > 16", p.P, p.N);
+  return FRAC_OK;
+}
+
+frac_status fill_fwd(const frac_fwd_args* a, frac::ScanParams& p, bool need_outputs) {
+  if (!a) return fail(FRAC_ERR_INVALID_ARG, "args is NULL");
+  if (!a->x || !a->dt || !a->Bm || !a->Cm || !a->alpha || !a->tau)
+    return fail(FRAC_ERR_INVALID_ARG, "x, dt, Bm, Cm, alpha and tau are required");
+  if (need_outputs && !a->y) return fail(FRAC_ERR_INVALID_ARG, "y is required");
+  if (!aligned16(a->x) || !aligned16(a->Bm) || !aligned16(a->Cm) || !aligned16(a->init_state) ||
+      (need_outputs && (!aligned16(a->y) || !aligned16(a->final_state))))
+    return fail(FRAC_ERR_INVALID_ARG, "x, Bm, Cm, y and the state arrays must be 16-byte aligned");
+  p.x = a->x;
+  p.dt = a->dt;
+  p.Bm = a->Bm;
+  p.Cm = a->Cm;
+  p.alpha = a->alpha;
+  p.as0 = a->alpha_stride[0];
+  p.as1 = a->alpha_stride[1];
+  p.as2 = a->alpha_stride[2];
+  p.lambda = a->lambda;
+  p.ls0 = a->lambda ? a->lambda_stride[0] : 0;
+  p.ls1 = a->lambda ? a->lambda_stride[1] : 0;
+  p.ls2 = a->lambda ? a->lambda_stride[2] : 0;
+  p.read_logit = a->read_logit;
+  p.write_logit = a->write_logit;
+  p.tau = a->tau;
+  p.D = a->D;
+  p.init_state = a->init_state;
+  p.y = need_outputs ? a->y : nullptr;
+  p.final_state = need_outputs ? a->final_state : nullptr;
+  return FRAC_OK;
+}
+
+// final_state for an empty sequence: the initial state (or zeros).
+__global__ void copy_or_zero_kernel(float* dst, const float* src, int64_t n) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
+    dst[i] = src ? src[i] : 0.0f;
+}
+
+frac_status hip_status(hipError_t e, const char* what) {
+  if (e == hipSuccess) return ok();
+  return fail(FRAC_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* frac_status_string(frac_status s) {
+  switch (s) {
+    case FRAC_OK: return "FRAC_OK";
+    case FRAC_ERR_INVALID_ARG: return "FRAC_ERR_INVALID_ARG: invalid argument";
+    case FRAC_ERR_UNSUPPORTED: return "FRAC_ERR_UNSUPPORTED: size or option not supported";
+    case FRAC_ERR_WORKSPACE: return "FRAC_ERR_WORKSPACE: workspace missing or too small";
+    case FRAC_ERR_HIP: return "FRAC_ERR_HIP: HIP runtime error";
+  }
+  return "unknown frac_status";
+}
+
+const char* frac_last_error(void) { return g_last_error.c_str(); }
+
+frac_status frac_default_tau(int M, double tau_min, double tau_max, float* out) {
+  if (M < 1 || !(tau_min > 0.0) || !(tau_max >= tau_min) || !out)
+    return fail(FRAC_ERR_INVALID_ARG, "frac_default_tau: need M >= 1, 0 < tau_min <= tau_max, out != NULL");
+  if (M == 1) {
+    out[0] = (float)tau_min;
+    return ok();
+  }
+  const double lr = log(tau_max / tau_min);
+  for (int m = 0; m < M; ++m) out[m] = (float)(tau_min * exp(lr * (double)m / (double)(M - 1)));
+  out[M - 1] = (float)tau_max;
+  return ok();
+}
+
+size_t frac_scan_workspace_size(const frac_shape* shape, int backward) {
+  frac::ScanParams p{};
+  if (fill_shape(shape, p) != FRAC_OK) return 0;
+  return backward ? frac::scan_bwd_workspace(p) : frac::scan_fwd_workspace(p);
+}
+
+frac_status frac_scan_fwd(const frac_shape* shape, const frac_fwd_args* args, void* ws, size_t ws_bytes,
+                          void* stream) {
+  frac::ScanParams p{};
+  frac_status s = fill_shape(shape, p);
+  if (s != FRAC_OK) return s;
+  if (p.Bsz == 0) return ok();
+  if (!args) return fail(FRAC_ERR_INVALID_ARG, "args is NULL");
+  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  if (p.L == 0) {
+    if (args->final_state) {
+      const int64_t n = (int64_t)p.Bsz * p.H * p.M * p.N * p.P;
+      hipLaunchKernelGGL(copy_or_zero_kernel, dim3(256), dim3(256), 0, st, args->final_state, args->init_state, n);
+      return hip_status(hipGetLastError(), "frac_scan_fwd (empty sequence)");
+    }
+    return ok();
+  }
+  s = fill_fwd(args, p, true);
+  if (s != FRAC_OK) return s;
+  const size_t need = frac::scan_fwd_workspace(p);
+  if (need && (!ws || ws_bytes < need))
+    return fail(FRAC_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", need, ws ? ws_bytes : (size_t)0);
+  return hip_status(frac::launch_scan_fwd(p, ws, ws_bytes, st), "frac_scan_fwd launch");
+}
+
+frac_status frac_scan_bwd(const frac_shape* shape, const frac_bwd_args* args, void* ws, size_t ws_bytes,
+                          void* stream) {
+  frac::ScanParams p{};
+  frac_status s = fill_shape(shape, p);
+  if (s != FRAC_OK) return s;
+  if (p.Bsz == 0 || p.L == 0) {
+    if (args && args->dD && p.Bsz >= 0) {
+      hipLaunchKernelGGL(copy_or_zero_kernel, dim3(1), dim3(256), 0, reinterpret_cast<hipStream_t>(stream),
+                         args->dD, (const float*)nullptr, (int64_t)p.H);
+      return hip_status(hipGetLastError(), "frac_scan_bwd (empty)");
+    }
+    return ok();
+  }
+  if (!args) return fail(FRAC_ERR_INVALID_ARG, "args is NULL");
+  s = fill_fwd(&args->fwd, p, false);
+  if (s != FRAC_OK) return s;
+  if (!args->dy || !args->dx || !args->ddt || !args->dBm || !args->dCm)
+    return fail(FRAC_ERR_INVALID_ARG, "dy, dx, ddt, dBm and dCm are required");
+  if (!aligned16(args->dy) || !aligned16(args->dx) || !aligned16(args->dBm) || !aligned16(args->dCm) ||
+      !aligned16(args->d_final_state))
+    return fail(FRAC_ERR_INVALID_ARG, "dy, dx, dBm, dCm and d_final_state must be 16-byte aligned");
+  p.dy = args->dy;
+  p.d_final_state = args->d_final_state;
+  p.dx = args->dx;
+  p.ddt = args->ddt;
+  p.dBm = args->dBm;
+  p.dCm = args->dCm;
+  p.dD = args->fwd.D ? args->dD : nullptr;
+  const size_t need = frac::scan_bwd_workspace(p);
+  if (need && (!ws || ws_bytes < need))
+    return fail(FRAC_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", need, ws ? ws_bytes : (size_t)0);
+  return hip_status(frac::launch_scan_bwd(p, ws, ws_bytes, reinterpret_cast<hipStream_t>(stream)),
+                    "frac_scan_bwd launch");
+}
+
+frac_status frac_decode_step(const frac_shape* shape, const frac_step_args* a, void* stream) {
+  frac::ScanParams p{};
+  frac_status s = fill_shape(shape, p);
+  if (s != FRAC_OK) return s;
+  if (shape->seqlen != 1) return fail(FRAC_ERR_INVALID_ARG, "frac_decode_step: shape.seqlen must be 1");
+  if (p.Bsz == 0) return ok();
+  if (!a) return fail(FRAC_ERR_INVALID_ARG, "args is NULL");
+  if (!a->x || !a->dt || !a->Bm || !a->Cm || !a->alpha || !a->tau || !a->state || !a->y)
+    return fail(FRAC_ERR_INVALID_ARG, "x, dt, Bm, Cm, alpha, tau, state and y are required");
+  if (!aligned16(a->state)) return fail(FRAC_ERR_INVALID_ARG, "state must be 16-byte aligned");
+  p.x = a->x;
+  p.dt = a->dt;
+  p.Bm = a->Bm;
+  p.Cm = a->Cm;
+  p.alpha = a->alpha;
+  p.as0 = a->alpha_stride[0];
+  p.as1 = a->alpha_stride[1];
+  p.lambda = a->lambda;
+  p.ls0 = a->lambda ? a->lambda_stride[0] : 0;
+  p.ls1 = a->lambda ? a->lambda_stride[1] : 0;
+  p.read_logit = a->read_logit;
+  p.write_logit = a->write_logit;
+  p.tau = a->tau;
+  p.D = a->D;
+  p.y = a->y;
+  return hip_status(frac::launch_decode_step(p, a->state, reinterpret_cast<hipStream_t>(stream)),
+                    "frac_decode_step launch");
+}
+
+}  // extern "C"

@@ -1,0 +1,143 @@
+// frac_decode.hip -- bounded-state decode: one token of the recurrence on a
+// cached state, updated in place (the one-step recurrent form named in the remark
+// closing Sec. 3.2; steps of the Appendix-D algorithm with the B/C-widened state).
+//
+// Per (batch, head) the step reads and rewrites the whole M x N x P float32 state
+// once; everything else is a few hundred bytes.  The kernel is therefore a
+// streaming kernel: one workgroup per (batch, head), the state walked as rows of P
+// floats with 16-byte loads and stores, the readout reduced over (m, n) in
+// registers and then across row groups through LDS in a fixed order.
+#include "frac_device.h"
+#include "frac_kernels.h"
+
+namespace frac {
+
+namespace {
+
+constexpr int kDecodeThreads = 256;
+constexpr int kDecodeUnroll = 8;
+
+template <typename T, int MP>
+__global__ void __launch_bounds__(kDecodeThreads) frac_decode_kernel(ScanParams p, float* __restrict__ state) {
+  const int tid = threadIdx.x;
+  const int H = p.H, P = p.P, N = p.N, M = p.M;
+  const int bh = blockIdx.x;
+  const int b = bh / H, h = bh - b * H, g = h * p.G / H;
+
+  __shared__ float sB[128], sC[128], sx[128];
+  __shared__ float s_rho[MP], s_kap[MP], s_c[MP];
+  __shared__ float4 red[kDecodeThreads];
+
+  const T* x = reinterpret_cast<const T*>(p.x) + ((int64_t)b * H + h) * P;
+  const T* Bg = reinterpret_cast<const T*>(p.Bm) + ((int64_t)b * p.G + g) * N;
+  const T* Cg = reinterpret_cast<const T*>(p.Cm) + ((int64_t)b * p.G + g) * N;
+
+  if (tid == 0) {
+    // per-token coefficients (eq. tau-eff, eq. rho-beta-def-frac, Algorithm steps 1-6)
+    const int64_t ith = (int64_t)b * H + h;
+    const float dtv = p.dt[ith];
+    const float al = p.alpha[b * p.as0 + h * p.as1];
+    const float lam = p.lambda ? p.lambda[b * p.ls0 + h * p.ls1] : 1.0f;
+    const float dtt = effective_step(dtv, al, p.lambda, lam);
+    float zc[MP], zw[MP];
+#pragma unroll
+    for (int m = 0; m < MP; ++m) {
+      const float prior = (m < M) ? -al * logf(p.tau[m]) : 0.0f;
+      zc[m] = prior + ((p.read_logit && m < M) ? p.read_logit[ith * M + m] : 0.0f);
+      zw[m] = prior + ((p.write_logit && m < M) ? p.write_logit[ith * M + m] : 0.0f);
+    }
+    softmax_modes<MP>(zc, M);
+    softmax_modes<MP>(zw, M);
+#pragma unroll
+    for (int m = 0; m < MP; ++m) {
+      const float arg = (m < M) ? -dtt / p.tau[m] : 0.0f;
+      s_rho[m] = expf(arg);
+      s_kap[m] = -expm1f(arg) * zw[m];
+      s_c[m] = zc[m];
+    }
+  }
+  for (int i = tid; i < N; i += kDecodeThreads) {
+    sB[i] = to_f32(Bg[i]);
+    sC[i] = to_f32(Cg[i]);
+  }
+  for (int i = tid; i < P; i += kDecodeThreads) sx[i] = to_f32(x[i]);
+  __syncthreads();
+
+  const int P4 = P >> 2;             // float4 columns per state row
+  const int RG = kDecodeThreads / P4;  // row groups
+  const int col = tid % P4, rg = tid / P4;
+  const float4 xv = make_float4(sx[4 * col], sx[4 * col + 1], sx[4 * col + 2], sx[4 * col + 3]);
+  float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+  float* base = state + ((int64_t)b * H + h) * (int64_t)M * N * P;
+
+  const int rows = (rg < RG) ? M * N : 0;  // threads beyond the last full row group idle
+  for (int r0 = rg; r0 < rows; r0 += RG * kDecodeUnroll) {
+    float4 s[kDecodeUnroll];
+#pragma unroll
+    for (int u = 0; u < kDecodeUnroll; ++u) {
+      const int row = r0 + u * RG;
+      if (row < rows) s[u] = *reinterpret_cast<const float4*>(base + (int64_t)row * P + 4 * col);
+    }
+#pragma unroll
+    for (int u = 0; u < kDecodeUnroll; ++u) {
+      const int row = r0 + u * RG;
+      if (row < rows) {
+        const int m = row / N, n = row - m * N;
+        const float rho = s_rho[m];
+        const float kb = s_kap[m] * sB[n];
+        float4 v = s[u];
+        v.x = rho * v.x + kb * xv.x;
+        v.y = rho * v.y + kb * xv.y;
+        v.z = rho * v.z + kb * xv.z;
+        v.w = rho * v.w + kb * xv.w;
+        *reinterpret_cast<float4*>(base + (int64_t)row * P + 4 * col) = v;
+        const float cc = s_c[m] * sC[n];
+        acc.x += cc * v.x;
+        acc.y += cc * v.y;
+        acc.z += cc * v.z;
+        acc.w += cc * v.w;
+      }
+    }
+  }
+  red[tid] = acc;
+  __syncthreads();
+  if (tid < P4) {
+    float4 sum = red[tid];
+    for (int j = 1; j < RG; ++j) {
+      const float4 o = red[j * P4 + tid];
+      sum.x += o.x;
+      sum.y += o.y;
+      sum.z += o.z;
+      sum.w += o.w;
+    }
+    const float Dh = p.D ? p.D[h] : 0.0f;
+    T* y = reinterpret_cast<T*>(p.y) + ((int64_t)b * H + h) * P + 4 * tid;
+    y[0] = (T)(sum.x + Dh * sx[4 * tid]);
+    y[1] = (T)(sum.y + Dh * sx[4 * tid + 1]);
+    y[2] = (T)(sum.z + Dh * sx[4 * tid + 2]);
+    y[3] = (T)(sum.w + Dh * sx[4 * tid + 3]);
+  }
+}
+
+template <typename T, int MP>
+hipError_t launch_decode_variant(const ScanParams& p, float* state, hipStream_t stream) {
+  hipLaunchKernelGGL((frac_decode_kernel<T, MP>), dim3(p.Bsz * p.H), dim3(kDecodeThreads), 0, stream, p, state);
+  return hipGetLastError();
+}
+
+template <typename T>
+hipError_t launch_decode_mp(const ScanParams& p, float* state, hipStream_t stream) {
+  if (p.M <= 1) return launch_decode_variant<T, 1>(p, state, stream);
+  if (p.M <= 2) return launch_decode_variant<T, 2>(p, state, stream);
+  if (p.M <= 4) return launch_decode_variant<T, 4>(p, state, stream);
+  return launch_decode_variant<T, 8>(p, state, stream);
+}
+
+}  // namespace
+
+hipError_t launch_decode_step(const ScanParams& p, float* state, hipStream_t stream) {
+  if (p.Bsz == 0) return hipSuccess;
+  return p.io_bf16 ? launch_decode_mp<bf16>(p, state, stream) : launch_decode_mp<float>(p, state, stream);
+}
+
+}  // namespace frac

@@ -1,0 +1,172 @@
+// frac_device.h -- device-side building blocks shared by the Frac scan kernels
+// (gfx950 / CDNA4, wave64).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace frac {
+
+typedef __bf16 bf16;
+typedef bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+
+constexpr int kWave = 64;
+constexpr int kQ = 64;  // tokens per chunk
+
+// ---------------------------------------------------------------- fragments
+//
+// A 16x16x32 matrix-core step consumes, per lane (i = lane % 16, g = lane / 16),
+// eight K-slots of the A row i and eight K-slots of the B column i.  Which K index
+// a slot stands for is free as long as A and B agree; every fragment below is
+// built with an explicit slot -> K map and both operands of a product use the
+// same map.  For float32 operands the step is issued as eight 16x16x4 products,
+// slot s of lane group g going to product s.
+
+template <typename T>
+struct Frag;
+template <>
+struct Frag<bf16> {
+  bf16x8 v;
+};
+template <>
+struct Frag<float> {
+  float v[8];
+};
+
+__device__ __forceinline__ void mma(floatx4& acc, const Frag<bf16>& a, const Frag<bf16>& b) {
+  acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a.v, b.v, acc, 0, 0, 0);
+}
+
+__device__ __forceinline__ void mma(floatx4& acc, const Frag<float>& a, const Frag<float>& b) {
+#pragma unroll
+  for (int s = 0; s < 8; ++s) acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.v[s], b.v[s], acc, 0, 0, 0);
+}
+
+template <typename T>
+__device__ __forceinline__ Frag<T> frag_zero() {
+  Frag<T> f;
+#pragma unroll
+  for (int s = 0; s < 8; ++s) f.v[s] = (T)0.0f;
+  return f;
+}
+
+template <typename T>
+__device__ __forceinline__ void frag_set(Frag<T>& f, int s, float val) {
+  f.v[s] = (T)val;
+}
+
+// Eight consecutive elements at p (16-byte aligned for bf16, 32-byte for float).
+__device__ __forceinline__ Frag<bf16> frag_load8(const bf16* p) {
+  Frag<bf16> f;
+  f.v = *reinterpret_cast<const bf16x8*>(p);
+  return f;
+}
+__device__ __forceinline__ Frag<float> frag_load8(const float* p) {
+  Frag<float> f;
+  const float4 a = *reinterpret_cast<const float4*>(p);
+  const float4 b = *reinterpret_cast<const float4*>(p + 4);
+  f.v[0] = a.x; f.v[1] = a.y; f.v[2] = a.z; f.v[3] = a.w;
+  f.v[4] = b.x; f.v[5] = b.y; f.v[6] = b.z; f.v[7] = b.w;
+  return f;
+}
+
+// Slots 0..3 from p0[0..3], slots 4..7 from p1[0..3] (p1 == nullptr: zeros).
+__device__ __forceinline__ Frag<bf16> frag_load4x2(const bf16* p0, const bf16* p1) {
+  Frag<bf16> f;
+  const bf16x4 a = *reinterpret_cast<const bf16x4*>(p0);
+  bf16x4 b;
+  if (p1) b = *reinterpret_cast<const bf16x4*>(p1);
+  else b = bf16x4{(bf16)0.0f, (bf16)0.0f, (bf16)0.0f, (bf16)0.0f};
+  f.v = bf16x8{a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
+  return f;
+}
+__device__ __forceinline__ Frag<float> frag_load4x2(const float* p0, const float* p1) {
+  Frag<float> f;
+  const float4 a = *reinterpret_cast<const float4*>(p0);
+  float4 b = make_float4(0.f, 0.f, 0.f, 0.f);
+  if (p1) b = *reinterpret_cast<const float4*>(p1);
+  f.v[0] = a.x; f.v[1] = a.y; f.v[2] = a.z; f.v[3] = a.w;
+  f.v[4] = b.x; f.v[5] = b.y; f.v[6] = b.z; f.v[7] = b.w;
+  return f;
+}
+
+// ------------------------------------------------------------ io conversion
+
+__device__ __forceinline__ float to_f32(bf16 v) { return (float)v; }
+__device__ __forceinline__ float to_f32(float v) { return v; }
+
+// Load 8 consecutive io elements from global memory as floats.
+__device__ __forceinline__ void load8(const bf16* p, float* out) {
+  const bf16x8 v = *reinterpret_cast<const bf16x8*>(p);
+#pragma unroll
+  for (int j = 0; j < 8; ++j) out[j] = (float)v[j];
+}
+__device__ __forceinline__ void load8(const float* p, float* out) {
+  const float4 a = *reinterpret_cast<const float4*>(p);
+  const float4 b = *reinterpret_cast<const float4*>(p + 4);
+  out[0] = a.x; out[1] = a.y; out[2] = a.z; out[3] = a.w;
+  out[4] = b.x; out[5] = b.y; out[6] = b.z; out[7] = b.w;
+}
+
+// Raw copy of 8 io elements global -> shared, no conversion.
+__device__ __forceinline__ void copy8(bf16* dst, const bf16* src) {
+  *reinterpret_cast<bf16x8*>(dst) = *reinterpret_cast<const bf16x8*>(src);
+}
+__device__ __forceinline__ void copy8(float* dst, const float* src) {
+  reinterpret_cast<float4*>(dst)[0] = reinterpret_cast<const float4*>(src)[0];
+  reinterpret_cast<float4*>(dst)[1] = reinterpret_cast<const float4*>(src)[1];
+}
+
+template <typename T>
+__device__ __forceinline__ void zero8(T* dst) {
+#pragma unroll
+  for (int j = 0; j < 8; ++j) dst[j] = (T)0.0f;
+}
+
+// ------------------------------------------------------------- wave helpers
+
+// Inclusive prefix sum over the 64 lanes of a wave (Hillis-Steele, fixed order).
+__device__ __forceinline__ float wave_inclusive_sum(float v) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const float o = __shfl_up(v, off, 64);
+    if (lane >= off) v += o;
+  }
+  return v;
+}
+
+// ------------------------------------------------------- per-token controls
+
+// Scalar-broadcast strided load: element (i0,i1,i2) at p[i0*s0 + i1*s1 + i2*s2].
+__device__ __forceinline__ float strided3(const float* p, int64_t s0, int64_t s1, int64_t s2, int64_t i0,
+                                          int64_t i1, int64_t i2) {
+  return p[i0 * s0 + i1 * s1 + i2 * s2];
+}
+
+// softmax over the first M of MP entries (the rest get weight 0), in place.
+template <int MP>
+__device__ __forceinline__ void softmax_modes(float* z, int M) {
+  float mx = z[0];
+#pragma unroll
+  for (int m = 1; m < MP; ++m)
+    if (m < M) mx = fmaxf(mx, z[m]);
+  float sum = 0.f;
+#pragma unroll
+  for (int m = 0; m < MP; ++m) {
+    z[m] = (m < M) ? expf(z[m] - mx) : 0.f;
+    sum += z[m];
+  }
+  const float inv = 1.0f / sum;
+#pragma unroll
+  for (int m = 0; m < MP; ++m) z[m] *= inv;
+}
+
+// Effective step dt * lambda^(1/alpha) (eq. tau-eff).
+__device__ __forceinline__ float effective_step(float dt, float alpha, const float* lam_ptr, float lam) {
+  return lam_ptr ? dt * exp2f(log2f(lam) / alpha) : dt;
+}
+
+}  // namespace frac

@@ -1,0 +1,518 @@
+// frac_fwd.hip -- chunked parallel scan, forward (prefill / training forward).
+//
+// Method: the selective mode-bank recurrence of Sec. 3.2 (eq. frac-selective-update,
+// eq. frac-readout) with a B/C-widened N x P state per mode, evaluated chunk by
+// chunk as in the remark closing Sec. 3.2 and the appendix on the efficient
+// implementation.  Inside a chunk of Q tokens, with A_t the chunk-local inclusive
+// sum of the effective steps dtt and r_m = 1 / tau_m:
+//
+//   y_t = sum_m c_{t,m} e^{-r_m A_t} C_t^T S_m            (state entering the chunk)
+//       + sum_{k<=t} (C_t . B_k) Gamma_{t,k} x_k            (intra-chunk mixing)
+//       + D x_t
+//   Gamma_{t,k} = sum_m c_{t,m} kappa_{k,m} e^{-r_m (A_t - A_k)}
+//   S_m <- e^{-r_m A_Q} S_m + sum_k kappa_{k,m} e^{-r_m (A_Q - A_k)} B_k x_k^T
+//
+// The decay between two tokens is always formed from a difference of chunk-local
+// cumulative steps (the log-space form of the appendix), never from a ratio of
+// sequence-global products.
+//
+// Kernels:
+//   frac_cb_kernel   G_chunk = C B^T (Q x Q, causal 16x16 tiles) once per
+//                    (batch, chunk, group) -- shared by every head of the group --
+//                    stored in the per-lane fragment order the scan reads back.
+//   frac_fwd_kernel  one workgroup per (batch, head).  Wave (pb, nh) owns state
+//                    columns p in [16 pb, 16 pb + 16) and, when N >= 32, one half
+//                    of the N rows, for every mode.  Its share of the float32
+//                    M x N x P state lives in matrix-core accumulator registers
+//                    for the whole sequence and never touches memory.  Per chunk:
+//                    stage x (transposed), B (transposed) and C in LDS; per-token
+//                    controls and weights (lane = token); (G o Gamma) tiles split
+//                    over the waves; readout, intra-chunk product and state update
+//                    as 16x16x32 matrix-core products (bfloat16 operands, float32
+//                    accumulation).  The accumulator tiles of the state are
+//                    converted in registers straight into B operands of the
+//                    readout: their row order becomes the K-slot order, matched by
+//                    the order in which C is read from LDS.
+//
+// Gamma uses the factorised form (c e^{-r A_t}) (kappa e^{r A_k}) through a float32
+// 16x16x4 product with the modes as K, for every mode whose chunk decay r_m A_Q
+// stays below 55 (so e^{r A_k} cannot overflow); other modes fall back to one exp
+// per (t, k) pair.  The per-mode decay of the state is not applied to the
+// accumulators every chunk: the state is held as E_m * S^_m with a float scale E_m
+// that absorbs the chunk decays, and the accumulators are rescaled only when E_m
+// would fall below 2^-60.
+#include "frac_device.h"
+#include "frac_kernels.h"
+
+namespace frac {
+
+namespace {
+
+// lower-triangular 16x16 tiles of the Q x Q matrix: (row block, column block)
+__constant__ int kTileTB[10] = {0, 1, 1, 2, 2, 2, 3, 3, 3, 3};
+__constant__ int kTileKB[10] = {0, 0, 1, 0, 1, 2, 0, 1, 2, 3};
+constexpr int kTiles = 10;
+constexpr int kTileElems = 256;  // one 16x16 tile: 64 lanes x 4 values
+
+constexpr float kSafeExponent = 55.0f;  // e^{r A} <= e^55 ~ 7.7e23
+constexpr float kRescaleFloor = 0x1p-60f;
+
+// Broadcast lane 0's value as a wave-uniform scalar.  The builtin moves 32-bit
+// integers, so the float travels as its bit pattern.
+__device__ __forceinline__ float uniform(float v) {
+  return __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(v)));
+}
+
+// --------------------------------------------------------------- C B^T tiles
+
+template <typename T, int NB>
+__global__ void __launch_bounds__(256) frac_cb_kernel(ScanParams p, T* __restrict__ gtiles) {
+  constexpr int NP = NB * 16;
+  constexpr int LDN = NP + 8;
+  constexpr int KB = (NB + 1) / 2;
+  const int c = blockIdx.x, g = blockIdx.y, b = blockIdx.z;
+  const int nchunks = gridDim.x;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, li = lane & 15, lg = lane >> 4;
+  const int L = p.L, N = p.N, G = p.G;
+  const int t0 = c * kQ, nv = min(kQ, L - t0);
+
+  extern __shared__ __align__(16) unsigned char smem[];
+  T* Cs = reinterpret_cast<T*>(smem);
+  T* Bs = Cs + kQ * LDN;
+  const T* Bg = reinterpret_cast<const T*>(p.Bm);
+  const T* Cg = reinterpret_cast<const T*>(p.Cm);
+  constexpr int ngroups = NP / 8;
+  for (int idx = tid; idx < kQ * ngroups; idx += 256) {
+    const int t = idx / ngroups, n0 = (idx - t * ngroups) * 8;
+    if (t < nv && n0 < N) {
+      const int64_t off = (((int64_t)b * L + t0 + t) * G + g) * N + n0;
+      copy8(Cs + t * LDN + n0, Cg + off);
+      copy8(Bs + t * LDN + n0, Bg + off);
+    } else {
+      zero8(Cs + t * LDN + n0);
+      zero8(Bs + t * LDN + n0);
+    }
+  }
+  __syncthreads();
+  T* out = gtiles + (((int64_t)b * nchunks + c) * G + g) * (kTiles * kTileElems);
+  for (int tile = wave; tile < kTiles; tile += 4) {
+    const int tb = kTileTB[tile], kb = kTileKB[tile];
+    floatx4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int kk = 0; kk < KB; ++kk) {
+      const int n0 = kk * 32 + lg * 8;
+      Frag<T> a = frag_zero<T>(), bb = frag_zero<T>();
+      if (n0 < NP) {
+        a = frag_load8(Cs + (tb * 16 + li) * LDN + n0);
+        bb = frag_load8(Bs + (kb * 16 + li) * LDN + n0);
+      }
+      mma(acc, a, bb);
+    }
+#pragma unroll
+    for (int r = 0; r < 4; ++r) out[tile * kTileElems + lane * 4 + r] = (T)acc[r];
+  }
+}
+
+// ------------------------------------------------------------------- the scan
+
+template <typename T, int NB, int NH>
+struct FwdLayout {
+  static constexpr int NP = NB * 16;
+  static constexpr int LDN = NP + 8;  // row stride of Cs
+  static constexpr int LDQ = kQ + 8;  // row stride of BTs / GG / XTs
+  static size_t bytes(int PP, int MP) {
+    const int NW = PP / 16;
+    return sizeof(T) * (size_t)(kQ * LDN + NP * LDQ + kQ * LDQ + PP * LDQ) +
+           sizeof(float) * (size_t)(6 * MP * kQ + kQ + (NH > 1 ? NW * 2 * 512 : 0));
+  }
+};
+
+template <typename T, int MP, int NB, int NH>
+__global__ void __launch_bounds__(512) frac_fwd_kernel(ScanParams p, const T* __restrict__ gtiles) {
+  using Lay = FwdLayout<T, NB, NH>;
+  constexpr int NP = Lay::NP;
+  constexpr int LDN = Lay::LDN;
+  constexpr int LDQ = Lay::LDQ;
+  constexpr int NBW = NB / NH;            // n-blocks (16 rows) owned by a wave
+  constexpr int KBW = (NBW + 1) / 2;      // 32-row K steps of the readout per wave
+  const int NWT = blockDim.x >> 6;        // waves in the workgroup
+  const int NW = NWT / NH;                // p-blocks
+  const int PP = NW * 16;
+  const int tid = threadIdx.x;
+  const int wave = tid >> 6, lane = tid & 63, li = lane & 15, lg = lane >> 4;
+  const int pb = wave % NW, nh = wave / NW;
+  const int L = p.L, H = p.H, P = p.P, N = p.N, M = p.M;
+  const int nchunks = (L + kQ - 1) / kQ;
+
+  // Blocks are dealt round-robin to the 8 XCDs; give each XCD a contiguous run of
+  // (batch, head) so that heads sharing B and C share one L2.
+  int j = blockIdx.x;
+  const int nblk = gridDim.x;
+  if ((nblk & 7) == 0) j = (blockIdx.x & 7) * (nblk >> 3) + (blockIdx.x >> 3);
+  const int b = j / H, h = j - b * H, g = h * p.G / H;
+
+  extern __shared__ __align__(16) unsigned char smem[];
+  T* Cs = reinterpret_cast<T*>(smem);  // [Q][LDN]   C of the chunk
+  T* BTs = Cs + kQ * LDN;              // [NP][LDQ]  B transposed
+  T* GG = BTs + NP * LDQ;              // [Q][LDQ]   (C B^T) o Gamma, causal
+  T* XTs = GG + kQ * LDQ;              // [PP][LDQ]  x transposed
+  float* P_om = reinterpret_cast<float*>(XTs + PP * LDQ);  // [MP][Q] c e^{-rA_t} E_m  (readout)
+  float* P_v = P_om + MP * kQ;   // [MP][Q] kappa e^{-r(A_Q - A_t)} / E_m'  (update)
+  float* P_O = P_v + MP * kQ;    // [MP][Q] c e^{-r A_t}
+  float* P_Vt = P_O + MP * kQ;   // [MP][Q] kappa e^{r A_t} (safe modes) or 0
+  float* P_c = P_Vt + MP * kQ;   // [MP][Q] c
+  float* P_k = P_c + MP * kQ;    // [MP][Q] kappa
+  float* P_A = P_k + MP * kQ;    // [Q]     A_t
+  float* YX = P_A + kQ;          // [NW][2][2][4][64] partial outputs exchanged between n-halves
+
+  const T* x = reinterpret_cast<const T*>(p.x);
+  const T* Bg = reinterpret_cast<const T*>(p.Bm);
+  const T* Cg = reinterpret_cast<const T*>(p.Cm);
+  T* y = reinterpret_cast<T*>(p.y);
+
+  float rr[MP], lnt[MP];
+#pragma unroll
+  for (int m = 0; m < MP; ++m) {
+    const float tau = (m < M) ? p.tau[m] : 1.0f;
+    rr[m] = (m < M) ? 1.0f / tau : 0.0f;
+    lnt[m] = (m < M) ? logf(tau) : 0.0f;
+  }
+  for (int i = tid; i < kQ * LDQ; i += blockDim.x) GG[i] = (T)0.0f;
+
+  // ---- state: S[m][j] holds rows n = 16 (nh NBW + j) + 4 lg + r, column 16 pb + li
+  const int pc = pb * 16 + li;
+  const int64_t sbase = ((int64_t)b * H + h) * (int64_t)M * N * P;
+  floatx4 S[MP][NBW];
+  float E[MP];
+  {
+    // lane offset kept opaque so that the final store cannot share (and keep
+    // alive across the sequence loop) the per-element offsets of this load
+    int lo = (nh * NBW * 16 + lg * 4) * P + pc;
+    asm volatile("" : "+v"(lo));
+#pragma unroll
+    for (int m = 0; m < MP; ++m) {
+      E[m] = 1.0f;
+#pragma unroll
+      for (int jb = 0; jb < NBW; ++jb)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int n = (nh * NBW + jb) * 16 + lg * 4 + r;
+          float v = 0.0f;
+          if (p.init_state && m < M && n < N && pc < P)
+            v = p.init_state[sbase + lo + ((int64_t)m * N + jb * 16 + r) * P];
+          S[m][jb][r] = v;
+        }
+    }
+  }
+  const float Dh = p.D ? p.D[h] : 0.0f;
+
+  for (int c = 0; c < nchunks; ++c) {
+    const int t0 = c * kQ;
+    const int nv = min(kQ, L - t0);
+    __syncthreads();  // every read of the previous chunk's LDS is done
+
+    // ---- stage x (transposed), B (transposed) and C for this chunk
+    const int xgroups = PP >> 3;
+    for (int idx = tid; idx < kQ * xgroups; idx += blockDim.x) {
+      const int t = idx / xgroups, p0 = (idx - t * xgroups) * 8;
+      float v[8];
+      if (t < nv && p0 < P) load8(x + (((int64_t)b * L + t0 + t) * H + h) * P + p0, v);
+      else {
+#pragma unroll
+        for (int jj = 0; jj < 8; ++jj) v[jj] = 0.0f;
+      }
+#pragma unroll
+      for (int jj = 0; jj < 8; ++jj) XTs[(p0 + jj) * LDQ + t] = (T)v[jj];
+    }
+    constexpr int ngroups = NP / 8;
+    for (int idx = tid; idx < kQ * ngroups; idx += blockDim.x) {
+      const int t = idx / ngroups, n0 = (idx - t * ngroups) * 8;
+      if (t < nv && n0 < N) {
+        const int64_t off = (((int64_t)b * L + t0 + t) * p.G + g) * N + n0;
+        copy8(Cs + t * LDN + n0, Cg + off);
+        float v[8];
+        load8(Bg + off, v);
+#pragma unroll
+        for (int jj = 0; jj < 8; ++jj) BTs[(n0 + jj) * LDQ + t] = (T)v[jj];
+      } else {
+        zero8(Cs + t * LDN + n0);
+#pragma unroll
+        for (int jj = 0; jj < 8; ++jj) BTs[(n0 + jj) * LDQ + t] = (T)0.0f;
+      }
+    }
+
+    // ---- prologue: lane = token.  Every wave derives the controls, the
+    // chunk-local cumulative step and the weights; wave w stores modes m % NWT == w.
+    float vscale[MP], renf[MP];
+    bool ren[MP], safe[MP];
+    {
+      const int t = lane;
+      const bool valid = t < nv;
+      const int64_t tg = t0 + t;
+      const int64_t ith = ((int64_t)b * L + tg) * H + h;
+      const float dtv = valid ? p.dt[ith] : 0.0f;
+      const float al = valid ? strided3(p.alpha, p.as0, p.as1, p.as2, b, tg, h) : 1.0f;
+      const float lam = (valid && p.lambda) ? strided3(p.lambda, p.ls0, p.ls1, p.ls2, b, tg, h) : 1.0f;
+      const float dtt = valid ? effective_step(dtv, al, p.lambda, lam) : 0.0f;
+      const float A = wave_inclusive_sum(dtt);
+      const float Alast = uniform(__shfl(A, 63, 64));
+      float zc[MP], zw[MP];
+#pragma unroll
+      for (int m = 0; m < MP; ++m) {
+        const float prior = -al * lnt[m];
+        zc[m] = prior + ((p.read_logit && valid && m < M) ? p.read_logit[ith * M + m] : 0.0f);
+        zw[m] = prior + ((p.write_logit && valid && m < M) ? p.write_logit[ith * M + m] : 0.0f);
+      }
+      softmax_modes<MP>(zc, M);
+      softmax_modes<MP>(zw, M);
+      if (wave == 0) P_A[t] = A;
+#pragma unroll
+      for (int m = 0; m < MP; ++m) {
+        const float xr = rr[m] * Alast;
+        safe[m] = xr <= kSafeExponent;
+        const float Enew = uniform(E[m] * expf(-xr));
+        ren[m] = !(Enew >= kRescaleFloor);
+        vscale[m] = ren[m] ? 1.0f : 1.0f / Enew;
+        renf[m] = Enew;
+        if ((m % NWT) != wave) continue;
+        const float kap = -expm1f(-dtt * rr[m]) * zw[m];
+        const float om = zc[m] * expf(-rr[m] * A);
+        P_O[m * kQ + t] = om;
+        P_om[m * kQ + t] = om * E[m];
+        P_c[m * kQ + t] = zc[m];
+        P_k[m * kQ + t] = kap;
+        P_v[m * kQ + t] = kap * expf(-rr[m] * (Alast - A)) * vscale[m];
+        P_Vt[m * kQ + t] = safe[m] ? kap * expf(rr[m] * A) : 0.0f;
+      }
+    }
+    __syncthreads();
+
+    // ---- (C B^T) o Gamma, lower-triangular 16x16 tiles split over the waves
+    {
+      const T* gt = gtiles + (((int64_t)b * nchunks + c) * p.G + g) * (kTiles * kTileElems);
+      for (int tile = wave; tile < kTiles; tile += NWT) {
+        const int tb = kTileTB[tile], kb = kTileKB[tile];
+        float Gt[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) Gt[r] = to_f32(gt[tile * kTileElems + lane * 4 + r]);
+        floatx4 Gm = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int q = 0; q < (MP + 3) / 4; ++q) {
+          const int m = q * 4 + lg;
+          const float av = (m < MP) ? P_O[m * kQ + tb * 16 + li] : 0.0f;
+          const float bv = (m < MP) ? P_Vt[m * kQ + kb * 16 + li] : 0.0f;
+          Gm = __builtin_amdgcn_mfma_f32_16x16x4f32(av, bv, Gm, 0, 0, 0);
+        }
+#pragma unroll
+        for (int m = 0; m < MP; ++m) {
+          if (safe[m] || m >= M) continue;
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int t = tb * 16 + lg * 4 + r, k = kb * 16 + li;
+            if (t >= k) Gm[r] += P_c[m * kQ + t] * P_k[m * kQ + k] * expf(-rr[m] * (P_A[t] - P_A[k]));
+          }
+        }
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int t = tb * 16 + lg * 4 + r, k = kb * 16 + li;
+          GG[t * LDQ + k] = (T)((t >= k) ? Gt[r] * Gm[r] : 0.0f);
+        }
+      }
+    }
+
+    // ---- readout of the state entering the chunk (this wave's rows of N)
+    floatx4 Y[4];
+#pragma unroll
+    for (int tb = 0; tb < 4; ++tb) Y[tb] = floatx4{0.f, 0.f, 0.f, 0.f};
+    {
+      Frag<T> Ca[4][KBW];
+#pragma unroll
+      for (int tb = 0; tb < 4; ++tb)
+#pragma unroll
+        for (int kb = 0; kb < KBW; ++kb) {
+          const int n0 = nh * NBW * 16 + kb * 32;
+          const T* row = Cs + (tb * 16 + li) * LDN + n0 + lg * 4;
+          Ca[tb][kb] = frag_load4x2(row, (2 * kb + 1 < NBW) ? row + 16 : nullptr);
+        }
+#pragma unroll
+      for (int m = 0; m < MP; ++m) {
+        if (m >= M) continue;
+        Frag<T> Sf[KBW];
+#pragma unroll
+        for (int kb = 0; kb < KBW; ++kb) {
+#pragma unroll
+          for (int s = 0; s < 4; ++s) frag_set(Sf[kb], s, S[m][2 * kb][s]);
+#pragma unroll
+          for (int s = 0; s < 4; ++s) frag_set(Sf[kb], 4 + s, (2 * kb + 1 < NBW) ? S[m][2 * kb + 1][s] : 0.0f);
+        }
+#pragma unroll
+        for (int tb = 0; tb < 4; ++tb) {
+          floatx4 Z = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+          for (int kb = 0; kb < KBW; ++kb) mma(Z, Ca[tb][kb], Sf[kb]);
+          const float4 om = *reinterpret_cast<const float4*>(P_om + m * kQ + tb * 16 + lg * 4);
+          Y[tb][0] += om.x * Z[0];
+          Y[tb][1] += om.y * Z[1];
+          Y[tb][2] += om.z * Z[2];
+          Y[tb][3] += om.w * Z[3];
+        }
+      }
+    }
+    if (NH > 1) {
+      // hand the row blocks finished by the other n-half over through LDS
+      float* dst = YX + ((pb * 2 + nh) * 2) * 4 * 64;
+#pragma unroll
+      for (int jj = 0; jj < 2; ++jj) {
+        const int tb = (1 - nh) * 2 + jj;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) dst[(jj * 4 + r) * 64 + lane] = Y[tb][r];
+      }
+    }
+    __syncthreads();  // GG and YX complete
+
+    // ---- intra-chunk product, skip term and output for the row blocks this
+    // wave finishes (all four with NH = 1, two with NH = 2)
+#pragma unroll
+    for (int tb = 0; tb < 4; ++tb) {
+      if (NH > 1 && (tb >> 1) != nh) continue;
+      if (NH > 1) {
+        const float* src = YX + ((pb * 2 + (1 - nh)) * 2) * 4 * 64;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) Y[tb][r] += src[((tb & 1) * 4 + r) * 64 + lane];
+      }
+#pragma unroll
+      for (int kk = 0; kk <= tb / 2; ++kk) {
+        const Frag<T> a = frag_load8(GG + (tb * 16 + li) * LDQ + kk * 32 + lg * 8);
+        const Frag<T> bb = frag_load8(XTs + pc * LDQ + kk * 32 + lg * 8);
+        mma(Y[tb], a, bb);
+      }
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int t = tb * 16 + lg * 4 + r;
+        if (t < nv && pc < P) {
+          const float xv = to_f32(XTs[pc * LDQ + t]);
+          y[(((int64_t)b * L + t0 + t) * H + h) * P + pc] = (T)(Y[tb][r] + Dh * xv);
+        }
+      }
+    }
+
+    // ---- state update
+#pragma unroll
+    for (int m = 0; m < MP; ++m) {
+      if (!ren[m]) continue;
+#pragma unroll
+      for (int jb = 0; jb < NBW; ++jb)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) S[m][jb][r] *= renf[m];
+    }
+#pragma unroll
+    for (int kt = 0; kt < 2; ++kt) {
+      float xr8[8];
+#pragma unroll
+      for (int s = 0; s < 8; ++s) xr8[s] = to_f32(XTs[pc * LDQ + kt * 32 + lg * 8 + s]);
+      Frag<T> Xf[MP];
+#pragma unroll
+      for (int m = 0; m < MP; ++m) {
+        const float4 v0 = *reinterpret_cast<const float4*>(P_v + m * kQ + kt * 32 + lg * 8);
+        const float4 v1 = *reinterpret_cast<const float4*>(P_v + m * kQ + kt * 32 + lg * 8 + 4);
+        frag_set(Xf[m], 0, xr8[0] * v0.x);
+        frag_set(Xf[m], 1, xr8[1] * v0.y);
+        frag_set(Xf[m], 2, xr8[2] * v0.z);
+        frag_set(Xf[m], 3, xr8[3] * v0.w);
+        frag_set(Xf[m], 4, xr8[4] * v1.x);
+        frag_set(Xf[m], 5, xr8[5] * v1.y);
+        frag_set(Xf[m], 6, xr8[6] * v1.z);
+        frag_set(Xf[m], 7, xr8[7] * v1.w);
+      }
+#pragma unroll
+      for (int jb = 0; jb < NBW; ++jb) {
+        const Frag<T> a = frag_load8(BTs + ((nh * NBW + jb) * 16 + li) * LDQ + kt * 32 + lg * 8);
+#pragma unroll
+        for (int m = 0; m < MP; ++m)
+          if (m < M) mma(S[m][jb], a, Xf[m]);
+      }
+    }
+#pragma unroll
+    for (int m = 0; m < MP; ++m) E[m] = ren[m] ? 1.0f : renf[m];
+  }
+
+  if (p.final_state) {
+    int lo = (nh * NBW * 16 + lg * 4) * P + pc;
+    asm volatile("" : "+v"(lo));
+#pragma unroll
+    for (int m = 0; m < MP; ++m)
+#pragma unroll
+      for (int jb = 0; jb < NBW; ++jb)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int n = (nh * NBW + jb) * 16 + lg * 4 + r;
+          if (m < M && n < N && pc < P)
+            p.final_state[sbase + lo + ((int64_t)m * N + jb * 16 + r) * P] = S[m][jb][r] * E[m];
+        }
+  }
+}
+
+template <int NB>
+constexpr int halves() {
+  return NB >= 2 ? 2 : 1;
+}
+
+template <typename T>
+size_t gtile_bytes(const ScanParams& p) {
+  const int64_t nchunks = (p.L + kQ - 1) / kQ;
+  return sizeof(T) * (size_t)p.Bsz * nchunks * p.G * kTiles * kTileElems;
+}
+
+template <typename T, int MP, int NB>
+hipError_t launch_fwd_variant(const ScanParams& p, void* ws, hipStream_t stream) {
+  constexpr int NH = halves<NB>();
+  const int nchunks = (p.L + kQ - 1) / kQ;
+  T* gt = reinterpret_cast<T*>(ws);
+  const size_t cb_lds = sizeof(T) * 2 * kQ * (NB * 16 + 8);
+  auto cbk = frac_cb_kernel<T, NB>;
+  hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(cbk), hipFuncAttributeMaxDynamicSharedMemorySize,
+                                     (int)cb_lds);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(cbk, dim3(nchunks, p.G, p.Bsz), dim3(256), cb_lds, stream, p, gt);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const size_t lds = FwdLayout<T, NB, NH>::bytes(p.PP, MP);
+  auto kern = frac_fwd_kernel<T, MP, NB, NH>;
+  e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern), hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(kern, dim3(p.Bsz * p.H), dim3(64 * (p.PP / 16) * NH), lds, stream, p, (const T*)gt);
+  return hipGetLastError();
+}
+
+template <typename T, int MP>
+hipError_t launch_fwd_nb(const ScanParams& p, void* ws, hipStream_t stream) {
+  switch (p.NP / 16) {
+    case 1: return launch_fwd_variant<T, MP, 1>(p, ws, stream);
+    case 2: return launch_fwd_variant<T, MP, 2>(p, ws, stream);
+    case 4: return launch_fwd_variant<T, MP, 4>(p, ws, stream);
+    case 8: return launch_fwd_variant<T, MP, 8>(p, ws, stream);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+template <typename T>
+hipError_t launch_fwd_mp(const ScanParams& p, void* ws, hipStream_t stream) {
+  if (p.M <= 1) return launch_fwd_nb<T, 1>(p, ws, stream);
+  if (p.M <= 2) return launch_fwd_nb<T, 2>(p, ws, stream);
+  if (p.M <= 4) return launch_fwd_nb<T, 4>(p, ws, stream);
+  return launch_fwd_nb<T, 8>(p, ws, stream);
+}
+
+}  // namespace
+
+size_t scan_fwd_workspace(const ScanParams& p) {
+  if (p.Bsz == 0 || p.L == 0) return 0;
+  return p.io_bf16 ? gtile_bytes<bf16>(p) : gtile_bytes<float>(p);
+}
+
+hipError_t launch_scan_fwd(const ScanParams& p, void* ws, size_t, hipStream_t stream) {
+  if (p.Bsz == 0 || p.L == 0) return hipSuccess;
+  return p.io_bf16 ? launch_fwd_mp<bf16>(p, ws, stream) : launch_fwd_mp<float>(p, ws, stream);
+}
+
+}  // namespace frac

@@ -1,0 +1,54 @@
+// frac_kernels.h -- host-side launch interface between the C ABI (frac_api.hip)
+// and the kernel translation units.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace frac {
+
+// Validated problem description handed to the kernel launchers.  Sizes are the
+// caller's; PP and NP are P and N rounded up to the 16-wide matrix-core tile.
+struct ScanParams {
+  int Bsz, L, H, P, N, G, M;
+  int PP, NP;
+  int io_bf16;
+  const void* x;
+  const float* dt;
+  const void* Bm;
+  const void* Cm;
+  const float* alpha;
+  int64_t as0, as1, as2;
+  const float* lambda;
+  int64_t ls0, ls1, ls2;
+  const float* read_logit;
+  const float* write_logit;
+  const float* tau;
+  const float* D;
+  const float* init_state;
+  void* y;
+  float* final_state;
+  // backward only
+  const void* dy;
+  const float* d_final_state;
+  void* dx;
+  float* ddt;
+  void* dBm;
+  void* dCm;
+  float* dD;
+};
+
+// Each launcher returns hipSuccess or the launch error; `stream` may be null.
+hipError_t launch_scan_fwd(const ScanParams& p, void* ws, size_t ws_bytes, hipStream_t stream);
+size_t scan_fwd_workspace(const ScanParams& p);
+
+hipError_t launch_scan_bwd(const ScanParams& p, void* ws, size_t ws_bytes, hipStream_t stream);
+size_t scan_bwd_workspace(const ScanParams& p);
+
+hipError_t launch_decode_step(const ScanParams& p, float* state, hipStream_t stream);
+
+// True when a kernel variant exists for these sizes (M, N, P, dtype).
+bool scan_supported(const ScanParams& p, const char** why);
+
+}  // namespace frac

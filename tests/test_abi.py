@@ -1,0 +1,114 @@
+"""Host-side checks of the C ABI (no GPU needed): the library loads, exports every
+function include/frac.h declares, validates arguments before touching the device,
+and builds the paper's timescale bank like the oracle does."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2609_36314_amd import _lib
+from paper_2609_36314_amd._lib import FracShape, FracFwdArgs, FracBwdArgs, FracStepArgs
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared():
+    src = open(os.path.join(ROOT, "include", "frac.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(frac_[a-z_]+)\s*\(", src)))
+
+
+def test_header_declares_the_bound_symbols():
+    assert _declared() == sorted(_lib.EXPORTS)
+
+
+def test_library_exports_every_declared_symbol():
+    lib = _lib.load()
+    for name in _declared():
+        assert hasattr(lib, name), name
+    out = os.popen("nm -D --defined-only %s" % _lib.LIB_PATH).read()
+    for name in _declared():
+        assert re.search(r"\bT %s\b" % name, out), name
+
+
+def test_status_strings():
+    lib = _lib.load()
+    for s in (0, -1, -2, -3, -4):
+        assert lib.frac_status_string(s).decode().startswith(_lib.STATUS[s])
+
+
+def test_default_tau_matches_oracle_grid():
+    lib = _lib.load()
+    for M in (1, 2, 4, 8, 16, 32):
+        out = (ctypes.c_float * M)()
+        assert lib.frac_default_tau(M, 1.0, 2.0 ** 17, out) == 0
+        assert np.array_equal(np.array(out, np.float32), oracle.default_tau(M).astype(np.float32))
+    assert lib.frac_default_tau(0, 1.0, 2.0, (ctypes.c_float * 1)()) == -1
+    assert lib.frac_default_tau(3, 2.0, 1.0, (ctypes.c_float * 3)()) == -1
+
+
+def _shape(**kw):
+    d = dict(batch=1, seqlen=64, nheads=4, headdim=64, dstate=128, ngroups=1, nmodes=4, chunk=0, io_dtype=1)
+    d.update(kw)
+    return FracShape(**d)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(nheads=6, ngroups=4), -1),
+    (dict(nmodes=0), -1),
+    (dict(batch=-1), -1),
+    (dict(io_dtype=7), -1),
+    (dict(nmodes=9), -2),
+    (dict(dstate=12), -2),
+    (dict(dstate=256), -2),
+    (dict(headdim=20), -2),
+    (dict(headdim=128, dstate=128), -2),
+    (dict(chunk=128), -2),
+])
+def test_invalid_shapes_are_rejected_on_the_host(kw, status):
+    lib = _lib.load()
+    sh = _shape(**kw)
+    a = FracFwdArgs()
+    assert lib.frac_scan_fwd(ctypes.byref(sh), ctypes.byref(a), None, 0, None) == status
+    assert lib.frac_last_error().decode() != ""
+    b = FracBwdArgs()
+    assert lib.frac_scan_bwd(ctypes.byref(sh), ctypes.byref(b), None, 0, None) == status
+    assert lib.frac_scan_workspace_size(ctypes.byref(sh), 0) == 0
+
+
+def test_missing_pointers_are_rejected():
+    lib = _lib.load()
+    sh = _shape()
+    a = FracFwdArgs()
+    assert lib.frac_scan_fwd(ctypes.byref(sh), ctypes.byref(a), None, 0, None) == -1
+    assert lib.frac_scan_fwd(None, ctypes.byref(a), None, 0, None) == -1
+    st = FracStepArgs()
+    sh1 = _shape(seqlen=1)
+    assert lib.frac_decode_step(ctypes.byref(sh1), ctypes.byref(st), None) == -1
+    assert lib.frac_decode_step(ctypes.byref(_shape(seqlen=2)), ctypes.byref(st), None) == -1
+
+
+def test_misaligned_pointer_is_rejected():
+    lib = _lib.load()
+    sh = _shape()
+    a = FracFwdArgs()
+    for f in ("x", "dt", "Bm", "Cm", "alpha", "tau", "y"):
+        setattr(a, f, ctypes.c_void_p(0x10000))
+    a.x = ctypes.c_void_p(0x10002)
+    assert lib.frac_scan_fwd(ctypes.byref(sh), ctypes.byref(a), None, 0, None) == -1
+    assert "aligned" in lib.frac_last_error().decode()
+
+
+def test_workspace_is_required_and_checked():
+    lib = _lib.load()
+    sh = _shape(batch=2, seqlen=200)
+    need = lib.frac_scan_workspace_size(ctypes.byref(sh), 0)
+    assert need > 0
+    a = FracFwdArgs()
+    for f in ("x", "dt", "Bm", "Cm", "alpha", "tau", "y"):
+        setattr(a, f, ctypes.c_void_p(0x10000))
+    assert lib.frac_scan_fwd(ctypes.byref(sh), ctypes.byref(a), None, 0, None) == -3
+    assert lib.frac_scan_fwd(ctypes.byref(sh), ctypes.byref(a), ctypes.c_void_p(0x20000), need - 1, None) == -3
