@@ -1,0 +1,278 @@
+#!/usr/bin/env python3
+"""Benchmark of the Frac scan on one MI355X.
+
+    python bench.py [--steps K] [--warmup W] [--workloads a,b,...] [--no-cpu-baseline]
+
+Prints ONE JSON line.  The headline `value` is the training step of the Frac
+layer at the 1.3B-model layer shape: forward + backward scan (dx, ddt, dB, dC)
+over batch 4 x 4096 tokens, 64 heads of dim 64, state 128, 8 modes, bfloat16
+I/O with float32 state -- tokens per second, inputs resident in HBM.  The
+other workloads (layer forward at L = 2048, long prefill at L = 16384 with
+the final state, decode at batch 256) are reported under "workloads".
+
+Timing: W untimed warmup steps, then K steps bracketed by device
+synchronisation; per-launch durations come from HIP events recorded on the
+stream the library launches on (torch's current stream).
+
+Roofline: algorithmic work of the scan counted per token and head
+    forward   (Q+1) P + 4 M N P + (Q+1) N G/H     flops
+    backward  2 (Q+1) P + 8 M N P + 3 (Q+1) N G/H flops
+against the bf16 dense matrix-core peak (float32 peak for float32 I/O);
+decode counts the float32 state read and written once plus the token I/O,
+against peak HBM bandwidth.  cpu_baseline times the float64 oracle on a bounded
+slice of the same workload on the host cores.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = ("Frac scan tokens/s fwd+bwd (1.3B layer shape, L=2k–16k); decode µs/step; % roofline")
+PEAK_BF16_FLOPS = 2.5e15     # MI355X dense bf16 matrix cores
+PEAK_F32_FLOPS = 157.3e12    # MI355X float32 (matrix and vector)
+PEAK_HBM_BYTES = 8.0e12      # MI355X HBM3E
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workloads", default="train-b4-l4096-m8,layer-fwd-b8-l2048,prefill-b1-l16384,"
+                                           "decode-b256-128steps")
+    ap.add_argument("--main", default="train-b4-l4096-m8")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-sample-heads", type=int, default=64)
+    return ap.parse_args()
+
+
+def fwd_flops_per_token_head(w):
+    Q, P, N, M, G, H = w.chunk, w.headdim, w.dstate, w.nmodes, w.ngroups, w.nheads
+    return (Q + 1) * P + 4 * M * N * P + (Q + 1) * N * G / H
+
+
+def bwd_flops_per_token_head(w):
+    Q, P, N, M, G, H = w.chunk, w.headdim, w.dstate, w.nmodes, w.ngroups, w.nheads
+    return 2 * (Q + 1) * P + 8 * M * N * P + 3 * (Q + 1) * N * G / H
+
+
+def decode_bytes_per_step(w):
+    B, H, P, N, M, G = w.batch, w.nheads, w.headdim, w.dstate, w.nmodes, w.ngroups
+    io = 2 if w.io_dtype == "bf16" else 4
+    state = 2 * B * H * M * N * P * 4
+    tokens = B * H * P * io * 2 + 2 * B * G * N * io + B * H * 4
+    return state + tokens
+
+
+class Timer:
+    """HIP events on the current stream around each timed launch group."""
+
+    def __init__(self, torch):
+        self.torch = torch
+        self.pairs = []
+
+    def __enter__(self):
+        s = self.torch.cuda.Event(enable_timing=True)
+        s.record()
+        self._s = s
+        return self
+
+    def __exit__(self, *a):
+        e = self.torch.cuda.Event(enable_timing=True)
+        e.record()
+        self.pairs.append((self._s, e))
+
+    def ms(self):
+        self.torch.cuda.synchronize()
+        return [s.elapsed_time(e) for s, e in self.pairs]
+
+
+def device_inputs(torch, w, seed=0):
+    from paper_2609_36314_amd.workloads import generate
+    a = generate(w, seed)
+    io = torch.bfloat16 if w.io_dtype == "bf16" else torch.float32
+    out = {}
+    for k, v in a.items():
+        t = torch.as_tensor(np.asarray(v))
+        if k in ("x", "Bm", "Cm", "dy"):
+            t = t.to(io)
+        out[k] = t.cuda().contiguous() if t.dim() else float(t.item())
+    return out
+
+
+def bench_scan(torch, frac, w, steps, warmup):
+    inp = device_inputs(torch, w)
+    tau = frac.default_tau(w.nmodes, device="cuda")
+    alpha = inp["alpha"]
+    x, dt, Bm, Cm = inp["x"], inp["dt"], inp["Bm"], inp["Cm"]
+    y = torch.empty_like(x)
+    fs = torch.empty((w.batch, w.nheads, w.nmodes, w.dstate, w.headdim), dtype=torch.float32,
+                     device="cuda") if w.final_state else None
+    shape = frac._shape(x, Bm, w.nmodes, 0)
+    ws_f = torch.empty(max(1, frac.scan_workspace_size(shape, False)), dtype=torch.uint8, device="cuda")
+    ws_b = torch.empty(max(1, frac.scan_workspace_size(shape, True)), dtype=torch.uint8, device="cuda")
+    dy = inp.get("dy")
+
+    def fwd():
+        frac.scan_fwd(x, dt, Bm, Cm, alpha, tau, y=y, final_state=fs, return_final_state=fs is not None,
+                      workspace=ws_f)
+
+    def bwd():
+        frac.scan_bwd(x, dt, Bm, Cm, alpha, tau, dy, workspace=ws_b)
+
+    for _ in range(warmup):
+        fwd()
+        if w.backward:
+            bwd()
+    torch.cuda.synchronize()
+    tf, tb = Timer(torch), Timer(torch)
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        with tf:
+            fwd()
+        if w.backward:
+            with tb:
+                bwd()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    fms = float(np.mean(tf.ms()))
+    bms = float(np.mean(tb.ms())) if w.backward else 0.0
+    tokens = w.batch * w.seqlen
+    step_ms = wall * 1e3 / steps
+    th = tokens * w.nheads
+    peak = PEAK_BF16_FLOPS if w.io_dtype == "bf16" else PEAK_F32_FLOPS
+    res = {
+        "tokens_per_s": tokens / (step_ms * 1e-3),
+        "ms_per_step": step_ms,
+        "fwd_ms": fms,
+        "fwd_roofline": roofline("mfma", th * fwd_flops_per_token_head(w), fms, peak, "TFLOP/s"),
+    }
+    if w.backward:
+        res["bwd_ms"] = bms
+        res["bwd_roofline"] = roofline("mfma", th * bwd_flops_per_token_head(w), bms, peak, "TFLOP/s")
+        res["fwd_bwd_roofline"] = roofline(
+            "mfma", th * (fwd_flops_per_token_head(w) + bwd_flops_per_token_head(w)), fms + bms, peak, "TFLOP/s")
+    return res
+
+
+def bench_decode(torch, frac, w, steps, warmup):
+    inp = device_inputs(torch, w)
+    tau = frac.default_tau(w.nmodes, device="cuda")
+    state = inp["init_state"]
+    S = w.decode_steps
+    ys = torch.empty((S, w.batch, w.nheads, w.headdim), dtype=inp["x"].dtype, device="cuda")
+
+    def one_pass():
+        for s in range(S):
+            frac.decode_step(state, inp["x"][s], inp["dt"][s], inp["Bm"][s], inp["Cm"][s], inp["alpha"], tau,
+                             y=ys[s])
+
+    for _ in range(warmup):
+        one_pass()
+    torch.cuda.synchronize()
+    t = Timer(torch)
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        with t:
+            one_pass()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    us_step = float(np.mean(t.ms())) * 1e3 / S
+    return {
+        "us_per_step": us_step,
+        "wall_us_per_step": wall * 1e6 / (steps * S),
+        "tokens_per_s": w.batch / (us_step * 1e-6),
+        "roofline": roofline("hbm", decode_bytes_per_step(w), us_step * 1e-3, PEAK_HBM_BYTES, "GB/s"),
+    }
+
+
+def roofline(bound, work, ms, peak, unit):
+    rate = work / (ms * 1e-3)
+    scale = 1e12 if unit == "TFLOP/s" else 1e9
+    return {"bound": bound, "achieved": rate / scale, "peak": peak / scale, "unit": unit, "frac": rate / peak,
+            "work_per_launch": work, "ms_per_launch": ms, "traffic": None}
+
+
+def cpu_baseline(w, heads):
+    """The float64 oracle on a bounded slice: batch element 0, `heads` heads, full length."""
+    import oracle
+    from paper_2609_36314_amd.workloads import generate
+    a = generate(w, 0)
+    H = min(heads, w.nheads)
+    tau = oracle.default_tau(w.nmodes)
+    sl = lambda k: np.asarray(a[k])[0:1].astype(np.float64)
+    x, dt = sl("x")[:, :, :H], sl("dt")[:, :, :H]
+    Bm, Cm = sl("Bm"), sl("Cm")
+    alpha = np.broadcast_to(np.asarray(a["alpha"], np.float64), dt.shape)
+    t0 = time.perf_counter()
+    oracle.forward(x, dt, Bm, Cm, alpha, tau)
+    if w.backward:
+        oracle.backward(x, dt, Bm, Cm, alpha, tau, sl("dy")[:, :, :H])
+    sec = time.perf_counter() - t0
+    tokens = w.seqlen * H / w.nheads  # token-equivalents of the full head count
+    return {"value": tokens / sec, "unit": "tokens/s", "cores": oracle.num_threads(), "kind": "oracle",
+            "sample": "batch element 0, %d of %d heads, %d tokens, %s" % (
+                H, w.nheads, w.seqlen, "forward + backward" if w.backward else "forward"),
+            "seconds": sec}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print("bench.py: this build runs on one GPU; --gpus %d is not supported (the scan shards by batch and "
+              "head without communication; see the design notes)" % args.gpus, file=sys.stderr)
+        sys.exit(2)
+    import torch
+    import paper_2609_36314_amd as frac
+    from paper_2609_36314_amd.workloads import WORKLOADS
+
+    names = [n for n in args.workloads.split(",") if n]
+    results = {}
+    for n in names:
+        w = WORKLOADS[n]
+        if w.decode_steps:
+            results[n] = bench_decode(torch, frac, w, max(1, args.steps // 4), max(1, args.warmup // 2))
+        else:
+            results[n] = bench_scan(torch, frac, w, args.steps, args.warmup)
+        print("# %s: %s" % (n, json.dumps(results[n])), file=sys.stderr, flush=True)
+        torch.cuda.empty_cache()
+
+    main_w = WORKLOADS[args.main]
+    mres = results.get(args.main)
+    line = {
+        "metric": METRIC,
+        "value": mres["tokens_per_s"] if mres else None,
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": mres["ms_per_step"] if mres else None,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": main_w.io_dtype,
+        "data": "synthetic",
+        "config": {"workload": main_w.name, "batch": main_w.batch, "seq_len": main_w.seqlen,
+                   "nheads": main_w.nheads, "headdim": main_w.headdim, "dstate": main_w.dstate,
+                   "nmodes": main_w.nmodes, "ngroups": main_w.ngroups, "chunk": main_w.chunk,
+                   "step": "forward + backward scan" if main_w.backward else "forward scan"},
+    }
+    if mres:
+        rf = mres.get("fwd_bwd_roofline") or mres["fwd_roofline"]
+        line["roofline"] = dict(rf, kernel="frac_scan_fwd + frac_scan_bwd (all launches of one step)")
+    line["workloads"] = results
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = cpu_baseline(main_w, args.cpu_sample_heads)
+    print(json.dumps(line))
+
+
+if __name__ == "__main__":
+    main()

@@ -196,6 +196,7 @@ frac_status frac_scan_bwd(const frac_shape* shape, const frac_bwd_args* args, vo
   if (!aligned16(args->dy) || !aligned16(args->dx) || !aligned16(args->dBm) || !aligned16(args->dCm) ||
       !aligned16(args->d_final_state))
     return fail(FRAC_ERR_INVALID_ARG, "dy, dx, dBm, dCm and d_final_state must be 16-byte aligned");
+  if (p.PP > 64) return fail(FRAC_ERR_UNSUPPORTED, "frac_scan_bwd: headdim %d > 64 is not built", p.P);
   p.dy = args->dy;
   p.d_final_state = args->d_final_state;
   p.dx = args->dx;

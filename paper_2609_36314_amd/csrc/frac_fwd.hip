@@ -463,18 +463,23 @@ size_t gtile_bytes(const ScanParams& p) {
   return sizeof(T) * (size_t)p.Bsz * nchunks * p.G * kTiles * kTileElems;
 }
 
-template <typename T, int MP, int NB>
-hipError_t launch_fwd_variant(const ScanParams& p, void* ws, hipStream_t stream) {
-  constexpr int NH = halves<NB>();
+template <typename T, int NB>
+hipError_t launch_cb_variant(const ScanParams& p, T* gt, hipStream_t stream) {
   const int nchunks = (p.L + kQ - 1) / kQ;
-  T* gt = reinterpret_cast<T*>(ws);
   const size_t cb_lds = sizeof(T) * 2 * kQ * (NB * 16 + 8);
   auto cbk = frac_cb_kernel<T, NB>;
   hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(cbk), hipFuncAttributeMaxDynamicSharedMemorySize,
                                      (int)cb_lds);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(cbk, dim3(nchunks, p.G, p.Bsz), dim3(256), cb_lds, stream, p, gt);
-  e = hipGetLastError();
+  return hipGetLastError();
+}
+
+template <typename T, int MP, int NB>
+hipError_t launch_fwd_variant(const ScanParams& p, void* ws, hipStream_t stream) {
+  constexpr int NH = halves<NB>();
+  T* gt = reinterpret_cast<T*>(ws);
+  hipError_t e = launch_cb_variant<T, NB>(p, gt, stream);
   if (e != hipSuccess) return e;
   const size_t lds = FwdLayout<T, NB, NH>::bytes(p.PP, MP);
   auto kern = frac_fwd_kernel<T, MP, NB, NH>;
@@ -504,6 +509,33 @@ hipError_t launch_fwd_mp(const ScanParams& p, void* ws, hipStream_t stream) {
 }
 
 }  // namespace
+
+size_t cb_tiles_bytes(const ScanParams& p) {
+  if (p.Bsz == 0 || p.L == 0) return 0;
+  return p.io_bf16 ? gtile_bytes<bf16>(p) : gtile_bytes<float>(p);
+}
+
+hipError_t launch_cb_tiles(const ScanParams& p, void* tiles, hipStream_t stream) {
+  const int nb = p.NP / 16;
+  if (p.io_bf16) {
+    bf16* t = reinterpret_cast<bf16*>(tiles);
+    switch (nb) {
+      case 1: return launch_cb_variant<bf16, 1>(p, t, stream);
+      case 2: return launch_cb_variant<bf16, 2>(p, t, stream);
+      case 4: return launch_cb_variant<bf16, 4>(p, t, stream);
+      case 8: return launch_cb_variant<bf16, 8>(p, t, stream);
+    }
+  } else {
+    float* t = reinterpret_cast<float*>(tiles);
+    switch (nb) {
+      case 1: return launch_cb_variant<float, 1>(p, t, stream);
+      case 2: return launch_cb_variant<float, 2>(p, t, stream);
+      case 4: return launch_cb_variant<float, 4>(p, t, stream);
+      case 8: return launch_cb_variant<float, 8>(p, t, stream);
+    }
+  }
+  return hipErrorInvalidValue;
+}
 
 size_t scan_fwd_workspace(const ScanParams& p) {
   if (p.Bsz == 0 || p.L == 0) return 0;

@@ -43,6 +43,11 @@ struct ScanParams {
 hipError_t launch_scan_fwd(const ScanParams& p, void* ws, size_t ws_bytes, hipStream_t stream);
 size_t scan_fwd_workspace(const ScanParams& p);
 
+// C B^T of every chunk (causal 16x16 tiles, per-lane fragment order), shared by
+// the heads of a group; `tiles` holds cb_tiles_bytes(p) bytes.
+size_t cb_tiles_bytes(const ScanParams& p);
+hipError_t launch_cb_tiles(const ScanParams& p, void* tiles, hipStream_t stream);
+
 hipError_t launch_scan_bwd(const ScanParams& p, void* ws, size_t ws_bytes, hipStream_t stream);
 size_t scan_bwd_workspace(const ScanParams& p);
 

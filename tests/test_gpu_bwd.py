@@ -1,0 +1,141 @@
+"""GPU parity of the chunked backward scan (frac_scan_bwd) against the float64 oracle."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2609_36314_amd as frac
+from paper_2609_36314_amd.workloads import TRAIN, Workload
+from harness import TOL, assert_close, device_inputs, f64
+
+pytestmark = pytest.mark.gpu
+
+
+def _tau(M):
+    t32 = oracle.default_tau(M).astype(np.float32)
+    return torch.from_numpy(t32).cuda(), t32.astype(np.float64)
+
+
+def _alpha64(inp, shape):
+    a = inp["alpha"]
+    if isinstance(a, torch.Tensor) and a.dim() == 1:
+        return np.broadcast_to(f64(a)[None, None, :], shape)
+    return np.broadcast_to(f64(a), shape)
+
+
+def _run_bwd(inp, tau_d, dfs=None):
+    kw = {k: inp[k] for k in ("lam", "read_logit", "write_logit", "D", "init_state") if k in inp}
+    return frac.scan_bwd(inp["x"], inp["dt"], inp["Bm"], inp["Cm"], inp["alpha"], tau_d, inp["dy"],
+                         d_final_state=dfs, **kw)
+
+
+def _oracle_bwd(inp, tau64, dfs=None, b=None, h=None):
+    x, dt, Bm, Cm, dy = (f64(inp[k]) for k in ("x", "dt", "Bm", "Cm", "dy"))
+    alpha = _alpha64(inp, dt.shape)
+    kw = {k: f64(inp[k]) for k in ("lam", "read_logit", "write_logit", "D", "init_state") if k in inp}
+    dF = None if dfs is None else f64(dfs)
+    if b is not None:
+        H = x.shape[2]
+        G = Bm.shape[2]
+        hs = slice(h, h + 1) if h is not None else slice(None)
+        x, dt, alpha, dy = x[b:b + 1, :, hs], dt[b:b + 1, :, hs], alpha[b:b + 1, :, hs], dy[b:b + 1, :, hs]
+        if h is not None:
+            gi = h * G // H
+            Bm, Cm = Bm[b:b + 1, :, gi:gi + 1], Cm[b:b + 1, :, gi:gi + 1]
+        else:
+            Bm, Cm = Bm[b:b + 1], Cm[b:b + 1]
+        for k in ("lam",):
+            if k in kw:
+                kw[k] = kw[k][b:b + 1, :, hs]
+        for k in ("read_logit", "write_logit"):
+            if k in kw:
+                kw[k] = kw[k][b:b + 1, :, hs]
+        if "D" in kw:
+            kw["D"] = kw["D"][hs]
+        if "init_state" in kw:
+            kw["init_state"] = kw["init_state"][b:b + 1, hs]
+        if dF is not None:
+            dF = dF[b:b + 1, hs]
+    return oracle.backward(x, dt, Bm, Cm, alpha, tau64, dy, d_final_state=dF, **kw)
+
+
+CASES = {
+    "f32 extras dfinal": Workload("t", 1, 150, 2, 32, 32, 3, io_dtype="f32", extras=True, init_state=True,
+                                  backward=True, final_state=True),
+    "f32 tiny": Workload("t", 1, 256, 2, 16, 16, 4, io_dtype="f32", backward=True),
+    "bf16 ragged": Workload("t", 2, 200, 4, 64, 128, 4, backward=True),
+    "bf16 M8": Workload("t", 1, 130, 2, 64, 128, 8, backward=True, final_state=True),
+    "bf16 groups extras": Workload("t", 2, 100, 4, 64, 64, 4, ngroups=2, extras=True, init_state=True,
+                                   backward=True, final_state=True),
+    "bf16 G=H M2 N32 P48": Workload("t", 1, 80, 2, 48, 32, 2, ngroups=2, backward=True),
+    "bf16 M1 N16 P16": Workload("t", 2, 70, 3, 16, 16, 1, backward=True),
+    "bf16 L1": Workload("t", 2, 1, 2, 64, 128, 4, backward=True, final_state=True, init_state=True),
+}
+
+
+@pytest.mark.parametrize("name", list(CASES))
+def test_bwd_parity_small(name):
+    w = CASES[name]
+    inp = device_inputs(w, seed=1)
+    tau_d, tau64 = _tau(w.nmodes)
+    dfs = inp.get("d_final_state")
+    print("case", name, w, flush=True)
+    g = _run_bwd(inp, tau_d, dfs)
+    torch.cuda.synchronize()
+    ref = _oracle_bwd(inp, tau64, dfs)
+    tol = TOL[w.io_dtype]
+    assert_close("dx", f64(g["dx"]), ref["dx"], tol)
+    assert_close("ddt", f64(g["ddt"]), ref["ddt"], tol)
+    assert_close("dB", f64(g["dBm"]), ref["dBm"], tol)
+    assert_close("dC", f64(g["dCm"]), ref["dCm"], tol)
+    if "D" in inp:
+        assert_close("dD", f64(g["dD"]), ref["dD"], tol)
+
+
+def test_bwd_large_steps_use_direct_decay():
+    """Steps large enough that r A_Q exceeds the factorisation bound for the fast
+    modes (the per-pair exponential path), in float32 and bfloat16."""
+    for io in ("f32", "bf16"):
+        w = Workload("t", 1, 140, 2, 32, 32, 4, io_dtype=io, backward=True)
+        inp = device_inputs(w, seed=3)
+        inp["dt"] = (inp["dt"] * 8.0).contiguous()
+        tau_d, tau64 = _tau(4)
+        g = _run_bwd(inp, tau_d)
+        torch.cuda.synchronize()
+        ref = _oracle_bwd(inp, tau64)
+        for k, rk in (("dx", "dx"), ("ddt", "ddt"), ("dBm", "dBm"), ("dCm", "dCm")):
+            assert_close(io + " " + k, f64(g[k]), ref[rk], TOL[io])
+
+
+def test_bwd_deterministic():
+    w = Workload("t", 2, 192, 4, 64, 128, 4, backward=True)
+    inp = device_inputs(w, seed=4)
+    tau_d, _ = _tau(4)
+    g1 = _run_bwd(inp, tau_d)
+    g2 = _run_bwd(inp, tau_d)
+    torch.cuda.synchronize()
+    for k in ("dx", "ddt", "dBm", "dCm"):
+        assert torch.equal(g1[k], g2[k]), k
+
+
+def test_bwd_full_size_sampled():
+    """The training workload at full size (batch 4, L 4096, 64 heads, M 8), as the
+    benchmark launches it.  dx and ddt are checked on sampled heads (they depend
+    on their own head only); dB and dC, summed over all 64 heads, on batch
+    element 0 recomputed by the oracle for every head."""
+    w = TRAIN
+    inp = device_inputs(w, seed=0)
+    tau_d, tau64 = _tau(w.nmodes)
+    print("full-size", w.name, flush=True)
+    g = _run_bwd(inp, tau_d)
+    torch.cuda.synchronize()
+    for k in ("dx", "ddt", "dBm", "dCm"):
+        assert torch.isfinite(g[k].float()).all(), k
+    for (b, h) in [(1, 5), (3, 60)]:
+        ref = _oracle_bwd(inp, tau64, b=b, h=h)
+        assert_close("dx[%d,:,%d]" % (b, h), f64(g["dx"][b:b + 1, :, h:h + 1]), ref["dx"], TOL["bf16"])
+        assert_close("ddt[%d,:,%d]" % (b, h), f64(g["ddt"][b:b + 1, :, h:h + 1]), ref["ddt"], TOL["bf16"])
+    ref = _oracle_bwd(inp, tau64, b=0)
+    assert_close("dB[0]", f64(g["dBm"][0:1]), ref["dBm"], TOL["bf16"])
+    assert_close("dC[0]", f64(g["dCm"][0:1]), ref["dCm"], TOL["bf16"])
+    assert_close("dx[0]", f64(g["dx"][0:1]), ref["dx"], TOL["bf16"])
