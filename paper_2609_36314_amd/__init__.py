@@ -46,12 +46,27 @@ def _f32(t, name):
     return t
 
 
+_scalars = {}
+
+
+def _scalar_tensor(v: float, device) -> torch.Tensor:
+    """A cached one-element float32 device tensor holding v (read-only by the library)."""
+    key = (float(v), str(device))
+    t = _scalars.get(key)
+    if t is None:
+        if len(_scalars) > 256:
+            _scalars.clear()
+        t = torch.full((1,), float(v), dtype=torch.float32, device=device)
+        _scalars[key] = t
+    return t
+
+
 def _strided(v, shape, device, name):
     """float32 scalar / broadcastable tensor -> (tensor, element strides over `shape`)."""
     if v is None:
         return None, (0,) * len(shape)
     if not isinstance(v, torch.Tensor):
-        v = torch.full((1,), float(v), dtype=torch.float32, device=device)
+        v = _scalar_tensor(v, device)
     if v.dtype != torch.float32:
         raise TypeError("%s must be float32" % name)
     e = v.expand(shape)
