@@ -67,10 +67,12 @@ frac_status fill_shape(const frac_shape* sh, frac::ScanParams& p) {
   p.PP = (p.P + 15) / 16 * 16;
   p.NP = next_tile_n(p.N);
   p.io_bf16 = sh->io_dtype == FRAC_BF16;
-  // the forward scan runs (P/16) x (2 if N > 16 else 1) waves per workgroup, at most 8
-  const int halves = p.NP >= 32 ? 2 : 1;
-  if (p.PP / 16 * halves > 8)
-    return fail(FRAC_ERR_UNSUPPORTED, "headdim %d with dstate %d: headdim must be <= 64 when dstate > 16", p.P, p.N);
+  return FRAC_OK;
+}
+
+// The chunked scan keeps one 64-column tile of x per chunk in LDS: headdim <= 64.
+frac_status check_scan_shape(const frac::ScanParams& p, const char* what) {
+  if (p.PP > 64) return fail(FRAC_ERR_UNSUPPORTED, "%s: headdim %d > 64 is not built", what, p.P);
   return FRAC_OK;
 }
 
@@ -147,7 +149,7 @@ frac_status frac_default_tau(int M, double tau_min, double tau_max, float* out) 
 
 size_t frac_scan_workspace_size(const frac_shape* shape, int backward) {
   frac::ScanParams p{};
-  if (fill_shape(shape, p) != FRAC_OK) return 0;
+  if (fill_shape(shape, p) != FRAC_OK || check_scan_shape(p, "frac_scan_workspace_size") != FRAC_OK) return 0;
   return backward ? frac::scan_bwd_workspace(p) : frac::scan_fwd_workspace(p);
 }
 
@@ -155,6 +157,7 @@ frac_status frac_scan_fwd(const frac_shape* shape, const frac_fwd_args* args, vo
                           void* stream) {
   frac::ScanParams p{};
   frac_status s = fill_shape(shape, p);
+  if (s == FRAC_OK) s = check_scan_shape(p, "frac_scan_fwd");
   if (s != FRAC_OK) return s;
   if (p.Bsz == 0) return ok();
   if (!args) return fail(FRAC_ERR_INVALID_ARG, "args is NULL");
@@ -179,6 +182,7 @@ frac_status frac_scan_bwd(const frac_shape* shape, const frac_bwd_args* args, vo
                           void* stream) {
   frac::ScanParams p{};
   frac_status s = fill_shape(shape, p);
+  if (s == FRAC_OK) s = check_scan_shape(p, "frac_scan_bwd");
   if (s != FRAC_OK) return s;
   if (p.Bsz == 0 || p.L == 0) {
     if (args && args->dD && p.Bsz >= 0) {
@@ -196,7 +200,6 @@ frac_status frac_scan_bwd(const frac_shape* shape, const frac_bwd_args* args, vo
   if (!aligned16(args->dy) || !aligned16(args->dx) || !aligned16(args->dBm) || !aligned16(args->dCm) ||
       !aligned16(args->d_final_state))
     return fail(FRAC_ERR_INVALID_ARG, "dy, dx, dBm, dCm and d_final_state must be 16-byte aligned");
-  if (p.PP > 64) return fail(FRAC_ERR_UNSUPPORTED, "frac_scan_bwd: headdim %d > 64 is not built", p.P);
   p.dy = args->dy;
   p.d_final_state = args->d_final_state;
   p.dx = args->dx;

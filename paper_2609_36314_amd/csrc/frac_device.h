@@ -169,4 +169,119 @@ __device__ __forceinline__ float effective_step(float dt, float alpha, const flo
   return lam_ptr ? dt * exp2f(log2f(lam) / alpha) : dt;
 }
 
+// ------------------------------------------------------- fast scalar math
+
+// e^x through the hardware exp2 (a multiply and one transcendental).
+__device__ __forceinline__ float fexp(float x) { return __expf(x); }
+
+// 1 - e^{-x} for x >= 0 without cancellation: a short Taylor series where the
+// difference is small, the subtraction elsewhere (relative error <= ~4e-6).
+__device__ __forceinline__ float one_minus_exp_neg(float x) {
+  const float series = x * (1.0f - x * (0.5f - x * (1.0f / 6.0f - x * (1.0f / 24.0f - x * (1.0f / 120.0f)))));
+  return x < 0.0625f ? series : 1.0f - __expf(-x);
+}
+
+// softmax over the first M of MP entries with the fast exponential.
+template <int MP>
+__device__ __forceinline__ void softmax_fast(float* z, int M) {
+  float mx = z[0];
+#pragma unroll
+  for (int m = 1; m < MP; ++m)
+    if (m < M) mx = fmaxf(mx, z[m]);
+  float sum = 0.f;
+#pragma unroll
+  for (int m = 0; m < MP; ++m) {
+    z[m] = (m < M) ? __expf(z[m] - mx) : 0.0f;
+    sum += z[m];
+  }
+  const float inv = __frcp_rn(sum);
+#pragma unroll
+  for (int m = 0; m < MP; ++m) z[m] *= inv;
+}
+
+// ------------------------------------------------ LDS fragment reads (K = rows)
+
+typedef short v4i16 __attribute__((ext_vector_type(4)));
+
+// Eight K-slots from a row-major LDS matrix (row stride ld elements): slot s holds
+// row row0 + s of column col0 + (lane % 16).  For bfloat16 this is two transposed
+// 64-bit LDS reads (ds_read_b64_tr_b16): within each 16-lane group, lane i
+// addresses 4 consecutive elements of row row0 + i/4 at column col0 + 4 (i % 4),
+// and lane j receives column col0 + j of the 4 rows.  row0 may differ between
+// the 16-lane groups.
+__device__ __forceinline__ Frag<bf16> frag_load_rows(const bf16* m, int ld, int row0, int col0) {
+  const int li = threadIdx.x & 15;
+  const bf16* p = m + (row0 + (li >> 2)) * ld + col0 + 4 * (li & 3);
+  const v4i16 a = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) v4i16*)(p));
+  const v4i16 b = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) v4i16*)(p + 4 * ld));
+  typedef short v8i16 __attribute__((ext_vector_type(8)));
+  const v8i16 ab = {a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
+  Frag<bf16> f;
+  f.v = __builtin_bit_cast(bf16x8, ab);
+  return f;
+}
+__device__ __forceinline__ Frag<float> frag_load_rows(const float* m, int ld, int row0, int col0) {
+  const int li = threadIdx.x & 15;
+  Frag<float> f;
+#pragma unroll
+  for (int s = 0; s < 8; ++s) f.v[s] = m[(row0 + s) * ld + col0 + li];
+  return f;
+}
+
+// Four consecutive rows row0..row0+3 of column col0 + (lane % 16), as floats
+// (one transposed read for bfloat16).
+__device__ __forceinline__ void col4_rows(const bf16* m, int ld, int row0, int col0, float* out) {
+  const int li = threadIdx.x & 15;
+  const bf16* p = m + (row0 + (li >> 2)) * ld + col0 + 4 * (li & 3);
+  const v4i16 a = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) v4i16*)(p));
+  const bf16x4 v = __builtin_bit_cast(bf16x4, a);
+#pragma unroll
+  for (int s = 0; s < 4; ++s) out[s] = (float)v[s];
+}
+__device__ __forceinline__ void col4_rows(const float* m, int ld, int row0, int col0, float* out) {
+  const int li = threadIdx.x & 15;
+#pragma unroll
+  for (int s = 0; s < 4; ++s) out[s] = m[(row0 + s) * ld + col0 + li];
+}
+
+// -------------------------------------------------- direct global -> LDS tiles
+
+// 16 zero bytes: the source of padded rows and columns of a staged tile.
+static __device__ const int4 kZero16 = {0, 0, 0, 0};
+
+// Copy a 64-row tile into LDS with 16-byte direct-to-LDS loads (no registers):
+// tile row t is `cols` elements at src + t * gstride; the LDS row stride is
+// `lstride` elements (a multiple of 16 bytes, >= cols).  Rows >= nv and columns
+// >= cols are zero-filled.  Each wave copies consecutive 1 KB runs of the tile.
+template <typename T>
+__device__ __forceinline__ void dma_tile(T* lds, const T* src, int64_t gstride, int cols, int lstride, int nv) {
+  constexpr int E = 16 / sizeof(T);
+  const int nwt = blockDim.x >> 6, wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int cpr = lstride / E;
+  const int total = 64 * cpr;
+  for (int base = wave * 64; base < total; base += nwt * 64) {
+    const int pos = base + lane;
+    if (pos < total) {
+      const int row = pos / cpr, ch = pos - row * cpr;
+      const void* g = (row < nv && ch * E < cols) ? (const void*)(src + (int64_t)row * gstride + ch * E)
+                                                  : (const void*)&kZero16;
+      __builtin_amdgcn_global_load_lds(g, (__attribute__((address_space(3))) void*)(lds + base * E), 16, 0, 0);
+    }
+  }
+}
+
+// Wait for this wave's outstanding vector-memory operations (including the
+// direct-to-LDS copies, which the compiler does not count).
+__device__ __forceinline__ void wait_vmem() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+
+// Workgroup barrier for LDS traffic: this wave's LDS accesses complete, then
+// s_barrier.  Unlike __syncthreads it does not wait for outstanding global loads,
+// so direct-to-LDS copies of the next tile stay in flight across it (their
+// completion is awaited with wait_vmem before the barrier that publishes them).
+__device__ __forceinline__ void barrier() {
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
 }  // namespace frac

@@ -115,25 +115,27 @@ __global__ void __launch_bounds__(256) frac_cb_kernel(ScanParams p, T* __restric
 
 // ------------------------------------------------------------------- the scan
 
-template <typename T, int NB, int NH>
-struct FwdLayout {
+// LDS row strides (elements) of the staged tiles; padded so that the transposed
+// fragment reads of 4 consecutive rows and the row reads of 16 rows spread over
+// the LDS banks.  bfloat16 tiles are double-buffered: the next chunk is copied
+// in (direct global -> LDS) while the current one is computed.
+template <typename T, int NB>
+struct FwdCfg {
   static constexpr int NP = NB * 16;
-  static constexpr int LDN = NP + 8;  // row stride of Cs
-  static constexpr int LDQ = kQ + 8;  // row stride of BTs / GG / XTs
-  static size_t bytes(int PP, int MP) {
-    const int NW = PP / 16;
-    return sizeof(T) * (size_t)(kQ * LDN + NP * LDQ + kQ * LDQ + PP * LDQ) +
-           sizeof(float) * (size_t)(6 * MP * kQ + kQ + (NH > 1 ? NW * 2 * 512 : 0));
-  }
+  static constexpr bool kBf16 = sizeof(T) == 2;
+  static constexpr int XS = kBf16 ? 64 + 8 : 64 + 4;    // x tile   [t][p]
+  static constexpr int BS = kBf16 ? NP + 16 : NP + 8;   // B tile   [t][n]
+  static constexpr int CS = kBf16 ? NP + 8 : NP + 4;    // C tile   [t][n]
+  static constexpr int GS = kBf16 ? 64 + 8 : 64 + 4;    // ((C B^T) o Gamma)^T [k][t]
+  static constexpr int NBUF = kBf16 ? 2 : 1;
 };
 
-template <typename T, int MP, int NB, int NH>
+template <typename T, int MP, int NB>
 __global__ void __launch_bounds__(512) frac_fwd_kernel(ScanParams p, const T* __restrict__ gtiles) {
-  using Lay = FwdLayout<T, NB, NH>;
-  constexpr int NP = Lay::NP;
-  constexpr int LDN = Lay::LDN;
-  constexpr int LDQ = Lay::LDQ;
-  constexpr int NBW = NB / NH;            // n-blocks (16 rows) owned by a wave
+  using Cfg = FwdCfg<T, NB>;
+  constexpr int NP = Cfg::NP, XS = Cfg::XS, BS = Cfg::BS, CS = Cfg::CS, GS = Cfg::GS;
+  constexpr int NH = NB >= 2 ? 2 : 1;     // N halves (waves per p-block)
+  constexpr int NBW = NB / NH;            // 16-row blocks of N owned by a wave
   constexpr int KBW = (NBW + 1) / 2;      // 32-row K steps of the readout per wave
   const int NWT = blockDim.x >> 6;        // waves in the workgroup
   const int NW = NWT / NH;                // p-blocks
@@ -141,7 +143,8 @@ __global__ void __launch_bounds__(512) frac_fwd_kernel(ScanParams p, const T* __
   const int tid = threadIdx.x;
   const int wave = tid >> 6, lane = tid & 63, li = lane & 15, lg = lane >> 4;
   const int pb = wave % NW, nh = wave / NW;
-  const int L = p.L, H = p.H, P = p.P, N = p.N, M = p.M;
+  const int pc = pb * 16 + li;
+  const int L = p.L, H = p.H, P = p.P, N = p.N, M = p.M, G = p.G;
   const int nchunks = (L + kQ - 1) / kQ;
 
   // Blocks are dealt round-robin to the 8 XCDs; give each XCD a contiguous run of
@@ -149,44 +152,45 @@ __global__ void __launch_bounds__(512) frac_fwd_kernel(ScanParams p, const T* __
   int j = blockIdx.x;
   const int nblk = gridDim.x;
   if ((nblk & 7) == 0) j = (blockIdx.x & 7) * (nblk >> 3) + (blockIdx.x >> 3);
-  const int b = j / H, h = j - b * H, g = h * p.G / H;
+  const int b = j / H, h = j - b * H, g = h * G / H;
 
-  extern __shared__ __align__(16) unsigned char smem[];
-  T* Cs = reinterpret_cast<T*>(smem);  // [Q][LDN]   C of the chunk
-  T* BTs = Cs + kQ * LDN;              // [NP][LDQ]  B transposed
-  T* GG = BTs + NP * LDQ;              // [Q][LDQ]   (C B^T) o Gamma, causal
-  T* XTs = GG + kQ * LDQ;              // [PP][LDQ]  x transposed
-  float* P_om = reinterpret_cast<float*>(XTs + PP * LDQ);  // [MP][Q] c e^{-rA_t} E_m  (readout)
-  float* P_v = P_om + MP * kQ;   // [MP][Q] kappa e^{-r(A_Q - A_t)} / E_m'  (update)
-  float* P_O = P_v + MP * kQ;    // [MP][Q] c e^{-r A_t}
-  float* P_Vt = P_O + MP * kQ;   // [MP][Q] kappa e^{r A_t} (safe modes) or 0
-  float* P_c = P_Vt + MP * kQ;   // [MP][Q] c
-  float* P_k = P_c + MP * kQ;    // [MP][Q] kappa
-  float* P_A = P_k + MP * kQ;    // [Q]     A_t
-  float* YX = P_A + kQ;          // [NW][2][2][4][64] partial outputs exchanged between n-halves
+  __shared__ __align__(16) T Xb0[64 * XS], Bb0[64 * BS], Cb0[64 * CS];
+  __shared__ __align__(16) T Xb1[Cfg::NBUF == 2 ? 64 * XS : 8], Bb1[Cfg::NBUF == 2 ? 64 * BS : 8],
+      Cb1[Cfg::NBUF == 2 ? 64 * CS : 8];
+  __shared__ __align__(16) T GGT[64 * GS];   // ((C B^T) o Gamma)^T of the chunk, causal
+  __shared__ __align__(16) T Yb[64 * XS];    // output rows of the previous chunk
+  __shared__ __align__(16) float prm[6 * MP * kQ + kQ];
+  __shared__ __align__(16) float YX[NH > 1 ? 4 * 1024 : 4];
+  float* P_om = prm;              // [MP][Q] c e^{-rA_t} E_m        (readout)
+  float* P_v = P_om + MP * kQ;    // [MP][Q] kappa e^{-r(A_Q-A_t)} upd (update)
+  float* P_O = P_v + MP * kQ;     // [MP][Q] c e^{-r A_t}            (Gamma rows)
+  float* P_Vt = P_O + MP * kQ;    // [MP][Q] kappa e^{r A_t}, safe modes (Gamma columns)
+  float* P_c = P_Vt + MP * kQ;    // [MP][Q] c      (modes past the factorisation bound)
+  float* P_k = P_c + MP * kQ;     // [MP][Q] kappa
+  float* P_A = P_k + MP * kQ;     // [Q] A_t
 
-  const T* x = reinterpret_cast<const T*>(p.x);
-  const T* Bg = reinterpret_cast<const T*>(p.Bm);
-  const T* Cg = reinterpret_cast<const T*>(p.Cm);
-  T* y = reinterpret_cast<T*>(p.y);
+  const T* xg = reinterpret_cast<const T*>(p.x) + (((int64_t)b * L) * H + h) * P;
+  const T* Bgp = reinterpret_cast<const T*>(p.Bm) + (((int64_t)b * L) * G + g) * N;
+  const T* Cgp = reinterpret_cast<const T*>(p.Cm) + (((int64_t)b * L) * G + g) * N;
+  T* yg = reinterpret_cast<T*>(p.y) + (((int64_t)b * L) * H + h) * P;
+  const int64_t xstride = (int64_t)H * P, bstride = (int64_t)G * N;
 
-  float rr[MP], lnt[MP];
-#pragma unroll
-  for (int m = 0; m < MP; ++m) {
-    const float tau = (m < M) ? p.tau[m] : 1.0f;
-    rr[m] = (m < M) ? 1.0f / tau : 0.0f;
-    lnt[m] = (m < M) ? logf(tau) : 0.0f;
+  // per-mode rates 1/tau_m and log tau_m, read from LDS where needed
+  __shared__ float s_rr[MP], s_lnt[MP];
+  if (tid < MP) {
+    const float tau = (tid < M) ? p.tau[tid] : 1.0f;
+    s_rr[tid] = (tid < M) ? 1.0f / tau : 0.0f;
+    s_lnt[tid] = (tid < M) ? logf(tau) : 0.0f;
   }
-  for (int i = tid; i < kQ * LDQ; i += blockDim.x) GG[i] = (T)0.0f;
+  for (int i = tid; i < 64 * GS; i += blockDim.x) GGT[i] = (T)0.0f;
 
-  // ---- state: S[m][j] holds rows n = 16 (nh NBW + j) + 4 lg + r, column 16 pb + li
-  const int pc = pb * 16 + li;
+  // ---- state: S[m][jb] holds rows n = 16 (nh NBW + jb) + 4 lg + r, column pc
   const int64_t sbase = ((int64_t)b * H + h) * (int64_t)M * N * P;
   floatx4 S[MP][NBW];
   float E[MP];
   {
-    // lane offset kept opaque so that the final store cannot share (and keep
-    // alive across the sequence loop) the per-element offsets of this load
+    // lane offset kept opaque so that the final store cannot share (and keep alive
+    // across the sequence loop) the per-element offsets of this load
     int lo = (nh * NBW * 16 + lg * 4) * P + pc;
     asm volatile("" : "+v"(lo));
 #pragma unroll
@@ -205,91 +209,121 @@ __global__ void __launch_bounds__(512) frac_fwd_kernel(ScanParams p, const T* __
     }
   }
   const float Dh = p.D ? p.D[h] : 0.0f;
+  const bool w_is_c = p.write_logit == p.read_logit;  // then the write weights equal the read weights
 
-  for (int c = 0; c < nchunks; ++c) {
+  // per-token controls of a chunk, loaded one chunk ahead (lane = token)
+  const float* dt_bh = p.dt + (int64_t)b * L * H + h;
+  const float* al_bh = p.alpha + b * p.as0 + h * p.as2;
+  const int64_t al_st = p.as1;
+  const float* lm_bh = p.lambda ? p.lambda + b * p.ls0 + h * p.ls2 : nullptr;
+  const int64_t lm_st = p.ls1;
+  const float* rl_bh = p.read_logit ? p.read_logit + ((int64_t)b * L * H + h) * M : nullptr;
+  const float* wl_bh = p.write_logit ? p.write_logit + ((int64_t)b * L * H + h) * M : nullptr;
+  const int64_t lg_st = (int64_t)H * M;
+  auto load_controls = [&](int c, float& dtv, float& al, float& lam) {
+    const int tg = c * kQ + lane;
+    const bool valid = tg < L;
+    dtv = valid ? dt_bh[(int64_t)tg * H] : 0.0f;
+    al = valid ? al_bh[tg * al_st] : 1.0f;
+    lam = (valid && lm_bh) ? lm_bh[tg * lm_st] : 1.0f;
+  };
+  auto stage = [&](int c, T* Xd, T* Bd, T* Cd) {
+    const int t0 = c * kQ, nv = min(kQ, L - t0);
+    dma_tile<T>(Xd, xg + (int64_t)t0 * xstride, xstride, P, XS, nv);
+    dma_tile<T>(Bd, Bgp + (int64_t)t0 * bstride, bstride, N, BS, nv);
+    dma_tile<T>(Cd, Cgp + (int64_t)t0 * bstride, bstride, N, CS, nv);
+  };
+  // output rows of chunk c (staged in Yb) -> global, 16 bytes per thread
+  auto store_y = [&](int c) {
+    constexpr int E8 = 16 / sizeof(T);
+    const int t0 = c * kQ, nv = min(kQ, L - t0);
+    const int cpr = P / E8;
+    for (int i = tid; i < nv * cpr; i += blockDim.x) {
+      const int t = i / cpr, ch = i - t * cpr;
+      *reinterpret_cast<int4*>(yg + (int64_t)(t0 + t) * xstride + ch * E8) =
+          *reinterpret_cast<const int4*>(Yb + t * XS + ch * E8);
+    }
+  };
+
+  float dt_n, al_n, lam_n;
+  load_controls(0, dt_n, al_n, lam_n);
+  if (Cfg::NBUF == 2) stage(0, Xb0, Bb0, Cb0);
+
+  // one chunk: Xc/Bc/Cc hold it (or receive it when single-buffered), Xn/Bn/Cn
+  // receive the next one
+  auto step = [&](int c, T* Xc, T* Bc, T* Cc, T* Xn, T* Bn, T* Cn) __attribute__((always_inline)) {
     const int t0 = c * kQ;
     const int nv = min(kQ, L - t0);
-    __syncthreads();  // every read of the previous chunk's LDS is done
-
-    // ---- stage x (transposed), B (transposed) and C for this chunk
-    const int xgroups = PP >> 3;
-    for (int idx = tid; idx < kQ * xgroups; idx += blockDim.x) {
-      const int t = idx / xgroups, p0 = (idx - t * xgroups) * 8;
-      float v[8];
-      if (t < nv && p0 < P) load8(x + (((int64_t)b * L + t0 + t) * H + h) * P + p0, v);
-      else {
-#pragma unroll
-        for (int jj = 0; jj < 8; ++jj) v[jj] = 0.0f;
-      }
-#pragma unroll
-      for (int jj = 0; jj < 8; ++jj) XTs[(p0 + jj) * LDQ + t] = (T)v[jj];
+    wait_vmem();
+    barrier();  // this chunk's tiles have landed; every wave is done with the previous chunk
+    if (c > 0) store_y(c - 1);
+    if (Cfg::NBUF == 2) {
+      if (c + 1 < nchunks) stage(c + 1, Xn, Bn, Cn);
+    } else {
+      stage(c, Xc, Bc, Cc);
+      wait_vmem();
+      barrier();
     }
-    constexpr int ngroups = NP / 8;
-    for (int idx = tid; idx < kQ * ngroups; idx += blockDim.x) {
-      const int t = idx / ngroups, n0 = (idx - t * ngroups) * 8;
-      if (t < nv && n0 < N) {
-        const int64_t off = (((int64_t)b * L + t0 + t) * p.G + g) * N + n0;
-        copy8(Cs + t * LDN + n0, Cg + off);
-        float v[8];
-        load8(Bg + off, v);
-#pragma unroll
-        for (int jj = 0; jj < 8; ++jj) BTs[(n0 + jj) * LDQ + t] = (T)v[jj];
-      } else {
-        zero8(Cs + t * LDN + n0);
-#pragma unroll
-        for (int jj = 0; jj < 8; ++jj) BTs[(n0 + jj) * LDQ + t] = (T)0.0f;
-      }
-    }
+    const float dtv = dt_n, al = al_n, lam = lam_n;
+    if (c + 1 < nchunks) load_controls(c + 1, dt_n, al_n, lam_n);
 
-    // ---- prologue: lane = token.  Every wave derives the controls, the
-    // chunk-local cumulative step and the weights; wave w stores modes m % NWT == w.
-    float vscale[MP], renf[MP];
-    bool ren[MP], safe[MP];
+    // ---- controls and weights, lane = token; wave w stores modes m % NWT == w
+    // per-mode flags as scalar bit masks: bit m of `renbits` set = the state of
+    // mode m is folded back to unit scale after this chunk, bit m of `unsafe` set
+    // = the factorised Gamma would overflow for mode m (direct decay instead)
+    float renf[MP];
+    int renbits = 0, unsafe = 0;
     {
       const int t = lane;
       const bool valid = t < nv;
-      const int64_t tg = t0 + t;
-      const int64_t ith = ((int64_t)b * L + tg) * H + h;
-      const float dtv = valid ? p.dt[ith] : 0.0f;
-      const float al = valid ? strided3(p.alpha, p.as0, p.as1, p.as2, b, tg, h) : 1.0f;
-      const float lam = (valid && p.lambda) ? strided3(p.lambda, p.ls0, p.ls1, p.ls2, b, tg, h) : 1.0f;
-      const float dtt = valid ? effective_step(dtv, al, p.lambda, lam) : 0.0f;
+      const int64_t ith = (int64_t)(t0 + t) * lg_st;
+      const float s_eff = lm_bh ? exp2f(log2f(lam) / al) : 1.0f;
+      const float dtt = valid ? dtv * s_eff : 0.0f;
       const float A = wave_inclusive_sum(dtt);
       const float Alast = uniform(__shfl(A, 63, 64));
       float zc[MP], zw[MP];
 #pragma unroll
       for (int m = 0; m < MP; ++m) {
-        const float prior = -al * lnt[m];
-        zc[m] = prior + ((p.read_logit && valid && m < M) ? p.read_logit[ith * M + m] : 0.0f);
-        zw[m] = prior + ((p.write_logit && valid && m < M) ? p.write_logit[ith * M + m] : 0.0f);
+        const float prior = -al * s_lnt[m];
+        zc[m] = prior + ((rl_bh && valid && m < M) ? rl_bh[ith + m] : 0.0f);
+        zw[m] = prior + ((wl_bh && valid && m < M) ? wl_bh[ith + m] : 0.0f);
       }
-      softmax_modes<MP>(zc, M);
-      softmax_modes<MP>(zw, M);
+      softmax_fast<MP>(zc, M);
+      if (w_is_c) {
+#pragma unroll
+        for (int m = 0; m < MP; ++m) zw[m] = zc[m];
+      } else {
+        softmax_fast<MP>(zw, M);
+      }
       if (wave == 0) P_A[t] = A;
 #pragma unroll
       for (int m = 0; m < MP; ++m) {
-        const float xr = rr[m] * Alast;
-        safe[m] = xr <= kSafeExponent;
-        const float Enew = uniform(E[m] * expf(-xr));
-        ren[m] = !(Enew >= kRescaleFloor);
-        vscale[m] = ren[m] ? 1.0f : 1.0f / Enew;
+        const float r = s_rr[m];
+        // r A_Q and the new scale are wave-uniform and non-negative: compare bit patterns
+        const float xr = uniform(r * Alast);
+        const bool safe = __float_as_int(xr) <= __float_as_int(kSafeExponent);
+        if (m < M && !safe) unsafe |= 1 << m;
+        const float Enew = uniform(E[m] * fexp(-xr));
+        const bool ren = __float_as_int(Enew) < __float_as_int(kRescaleFloor);
+        if (ren) renbits |= 1 << m;
         renf[m] = Enew;
         if ((m % NWT) != wave) continue;
-        const float kap = -expm1f(-dtt * rr[m]) * zw[m];
-        const float om = zc[m] * expf(-rr[m] * A);
+        const float upd = ren ? 1.0f : __frcp_rn(Enew);
+        const float kap = one_minus_exp_neg(dtt * r) * zw[m];
+        const float om = zc[m] * fexp(-r * A);
         P_O[m * kQ + t] = om;
         P_om[m * kQ + t] = om * E[m];
+        P_v[m * kQ + t] = kap * fexp(-r * (Alast - A)) * upd;
+        P_Vt[m * kQ + t] = safe ? kap * fexp(r * A) : 0.0f;
         P_c[m * kQ + t] = zc[m];
         P_k[m * kQ + t] = kap;
-        P_v[m * kQ + t] = kap * expf(-rr[m] * (Alast - A)) * vscale[m];
-        P_Vt[m * kQ + t] = safe[m] ? kap * expf(rr[m] * A) : 0.0f;
       }
     }
-    __syncthreads();
+    barrier();  // controls in LDS
 
-    // ---- (C B^T) o Gamma, lower-triangular 16x16 tiles split over the waves
+    // ---- ((C B^T) o Gamma)^T, lower-triangular 16x16 tiles split over the waves
     {
-      const T* gt = gtiles + (((int64_t)b * nchunks + c) * p.G + g) * (kTiles * kTileElems);
+      const T* gt = gtiles + (((int64_t)b * nchunks + c) * G + g) * (kTiles * kTileElems);
       for (int tile = wave; tile < kTiles; tile += NWT) {
         const int tb = kTileTB[tile], kb = kTileKB[tile];
         float Gt[4];
@@ -303,19 +337,22 @@ __global__ void __launch_bounds__(512) frac_fwd_kernel(ScanParams p, const T* __
           const float bv = (m < MP) ? P_Vt[m * kQ + kb * 16 + li] : 0.0f;
           Gm = __builtin_amdgcn_mfma_f32_16x16x4f32(av, bv, Gm, 0, 0, 0);
         }
+        if (unsafe) {
+          for (int m = 0; m < MP; ++m) {
+            if (!((unsafe >> m) & 1)) continue;
+            const float rm = s_rr[m];
 #pragma unroll
-        for (int m = 0; m < MP; ++m) {
-          if (safe[m] || m >= M) continue;
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const int t = tb * 16 + lg * 4 + r, k = kb * 16 + li;
-            if (t >= k) Gm[r] += P_c[m * kQ + t] * P_k[m * kQ + k] * expf(-rr[m] * (P_A[t] - P_A[k]));
+            for (int r = 0; r < 4; ++r) {
+              const int t = tb * 16 + lg * 4 + r, k = kb * 16 + li;
+              if (t >= k) Gm[r] += P_c[m * kQ + t] * P_k[m * kQ + k] * fexp(-rm * (P_A[t] - P_A[k]));
+            }
           }
         }
+        T* dst = GGT + (kb * 16 + li) * GS + tb * 16 + lg * 4;
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int t = tb * 16 + lg * 4 + r, k = kb * 16 + li;
-          GG[t * LDQ + k] = (T)((t >= k) ? Gt[r] * Gm[r] : 0.0f);
+          dst[r] = (T)((t >= k) ? Gt[r] * Gm[r] : 0.0f);
         }
       }
     }
@@ -330,8 +367,7 @@ __global__ void __launch_bounds__(512) frac_fwd_kernel(ScanParams p, const T* __
       for (int tb = 0; tb < 4; ++tb)
 #pragma unroll
         for (int kb = 0; kb < KBW; ++kb) {
-          const int n0 = nh * NBW * 16 + kb * 32;
-          const T* row = Cs + (tb * 16 + li) * LDN + n0 + lg * 4;
+          const T* row = Cc + (tb * 16 + li) * CS + nh * NBW * 16 + kb * 32 + lg * 4;
           Ca[tb][kb] = frag_load4x2(row, (2 * kb + 1 < NBW) ? row + 16 : nullptr);
         }
 #pragma unroll
@@ -359,7 +395,7 @@ __global__ void __launch_bounds__(512) frac_fwd_kernel(ScanParams p, const T* __
       }
     }
     if (NH > 1) {
-      // hand the row blocks finished by the other n-half over through LDS
+      // hand the row blocks finished by the other N half over through LDS
       float* dst = YX + ((pb * 2 + nh) * 2) * 4 * 64;
 #pragma unroll
       for (int jj = 0; jj < 2; ++jj) {
@@ -368,10 +404,9 @@ __global__ void __launch_bounds__(512) frac_fwd_kernel(ScanParams p, const T* __
         for (int r = 0; r < 4; ++r) dst[(jj * 4 + r) * 64 + lane] = Y[tb][r];
       }
     }
-    __syncthreads();  // GG and YX complete
+    barrier();  // GGT and YX complete
 
-    // ---- intra-chunk product, skip term and output for the row blocks this
-    // wave finishes (all four with NH = 1, two with NH = 2)
+    // ---- intra-chunk product, skip term, output rows into Yb
 #pragma unroll
     for (int tb = 0; tb < 4; ++tb) {
       if (NH > 1 && (tb >> 1) != nh) continue;
@@ -382,24 +417,20 @@ __global__ void __launch_bounds__(512) frac_fwd_kernel(ScanParams p, const T* __
       }
 #pragma unroll
       for (int kk = 0; kk <= tb / 2; ++kk) {
-        const Frag<T> a = frag_load8(GG + (tb * 16 + li) * LDQ + kk * 32 + lg * 8);
-        const Frag<T> bb = frag_load8(XTs + pc * LDQ + kk * 32 + lg * 8);
+        const Frag<T> a = frag_load_rows(GGT, GS, kk * 32 + lg * 8, tb * 16);
+        const Frag<T> bb = frag_load_rows(Xc, XS, kk * 32 + lg * 8, pb * 16);
         mma(Y[tb], a, bb);
       }
+      float xv[4];
+      col4_rows(Xc, XS, tb * 16 + lg * 4, pb * 16, xv);
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int t = tb * 16 + lg * 4 + r;
-        if (t < nv && pc < P) {
-          const float xv = to_f32(XTs[pc * LDQ + t]);
-          y[(((int64_t)b * L + t0 + t) * H + h) * P + pc] = (T)(Y[tb][r] + Dh * xv);
-        }
-      }
+      for (int r = 0; r < 4; ++r) Yb[(tb * 16 + lg * 4 + r) * XS + pc] = (T)(Y[tb][r] + Dh * xv[r]);
     }
 
-    // ---- state update
+    // ---- state update  S_m <- (rescale) + B^T (v_m o X)
 #pragma unroll
     for (int m = 0; m < MP; ++m) {
-      if (!ren[m]) continue;
+      if (!((renbits >> m) & 1)) continue;
 #pragma unroll
       for (int jb = 0; jb < NBW; ++jb)
 #pragma unroll
@@ -407,34 +438,45 @@ __global__ void __launch_bounds__(512) frac_fwd_kernel(ScanParams p, const T* __
     }
 #pragma unroll
     for (int kt = 0; kt < 2; ++kt) {
-      float xr8[8];
+      const Frag<T> xf = frag_load_rows(Xc, XS, kt * 32 + lg * 8, pb * 16);
+      float xs[8];
 #pragma unroll
-      for (int s = 0; s < 8; ++s) xr8[s] = to_f32(XTs[pc * LDQ + kt * 32 + lg * 8 + s]);
-      Frag<T> Xf[MP];
+      for (int s = 0; s < 8; ++s) xs[s] = to_f32(xf.v[s]);
+      Frag<T> a[NBW];
+#pragma unroll
+      for (int jb = 0; jb < NBW; ++jb) a[jb] = frag_load_rows(Bc, BS, kt * 32 + lg * 8, (nh * NBW + jb) * 16);
 #pragma unroll
       for (int m = 0; m < MP; ++m) {
+        if (m >= M) continue;
         const float4 v0 = *reinterpret_cast<const float4*>(P_v + m * kQ + kt * 32 + lg * 8);
         const float4 v1 = *reinterpret_cast<const float4*>(P_v + m * kQ + kt * 32 + lg * 8 + 4);
-        frag_set(Xf[m], 0, xr8[0] * v0.x);
-        frag_set(Xf[m], 1, xr8[1] * v0.y);
-        frag_set(Xf[m], 2, xr8[2] * v0.z);
-        frag_set(Xf[m], 3, xr8[3] * v0.w);
-        frag_set(Xf[m], 4, xr8[4] * v1.x);
-        frag_set(Xf[m], 5, xr8[5] * v1.y);
-        frag_set(Xf[m], 6, xr8[6] * v1.z);
-        frag_set(Xf[m], 7, xr8[7] * v1.w);
-      }
+        Frag<T> Xf;
+        frag_set(Xf, 0, xs[0] * v0.x);
+        frag_set(Xf, 1, xs[1] * v0.y);
+        frag_set(Xf, 2, xs[2] * v0.z);
+        frag_set(Xf, 3, xs[3] * v0.w);
+        frag_set(Xf, 4, xs[4] * v1.x);
+        frag_set(Xf, 5, xs[5] * v1.y);
+        frag_set(Xf, 6, xs[6] * v1.z);
+        frag_set(Xf, 7, xs[7] * v1.w);
 #pragma unroll
-      for (int jb = 0; jb < NBW; ++jb) {
-        const Frag<T> a = frag_load8(BTs + ((nh * NBW + jb) * 16 + li) * LDQ + kt * 32 + lg * 8);
-#pragma unroll
-        for (int m = 0; m < MP; ++m)
-          if (m < M) mma(S[m][jb], a, Xf[m]);
+        for (int jb = 0; jb < NBW; ++jb) mma(S[m][jb], a[jb], Xf);
       }
     }
 #pragma unroll
-    for (int m = 0; m < MP; ++m) E[m] = ren[m] ? 1.0f : renf[m];
+    for (int m = 0; m < MP; ++m) E[m] = ((renbits >> m) & 1) ? 1.0f : renf[m];
+  };
+
+  for (int c = 0; c < nchunks; c += 2) {
+    step(c, Xb0, Bb0, Cb0, Xb1, Bb1, Cb1);
+    if (c + 1 < nchunks) {
+      if (Cfg::NBUF == 2) step(c + 1, Xb1, Bb1, Cb1, Xb0, Bb0, Cb0);
+      else step(c + 1, Xb0, Bb0, Cb0, Xb0, Bb0, Cb0);
+    }
   }
+  wait_vmem();
+  barrier();
+  store_y(nchunks - 1);
 
   if (p.final_state) {
     int lo = (nh * NBW * 16 + lg * 4) * P + pc;
@@ -481,11 +523,8 @@ hipError_t launch_fwd_variant(const ScanParams& p, void* ws, hipStream_t stream)
   T* gt = reinterpret_cast<T*>(ws);
   hipError_t e = launch_cb_variant<T, NB>(p, gt, stream);
   if (e != hipSuccess) return e;
-  const size_t lds = FwdLayout<T, NB, NH>::bytes(p.PP, MP);
-  auto kern = frac_fwd_kernel<T, MP, NB, NH>;
-  e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern), hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-  if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(kern, dim3(p.Bsz * p.H), dim3(64 * (p.PP / 16) * NH), lds, stream, p, (const T*)gt);
+  hipLaunchKernelGGL((frac_fwd_kernel<T, MP, NB>), dim3(p.Bsz * p.H), dim3(64 * (p.PP / 16) * NH), 0, stream, p,
+                     (const T*)gt);
   return hipGetLastError();
 }
 

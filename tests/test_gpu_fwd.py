@@ -78,7 +78,7 @@ SMALL = {
                                 final_state=True),
     "bf16 M1 N16 P16": Workload("t", 2, 70, 3, 16, 16, 1, final_state=True),
     "bf16 M2 N32 P48": Workload("t", 1, 64, 2, 48, 32, 2, final_state=True),
-    "f32 P128 N16": Workload("t", 1, 90, 2, 128, 16, 4, io_dtype="f32", final_state=True),
+    "f32 P64 N16": Workload("t", 1, 90, 2, 64, 16, 4, io_dtype="f32", final_state=True),
     "bf16 L1 init": Workload("t", 2, 1, 2, 64, 128, 4, final_state=True, init_state=True),
     "bf16 per-head alpha": LONG_PREFILL.scaled(seqlen=300, nheads=4),
     "f32 M8 N128": Workload("t", 1, 150, 2, 64, 128, 8, io_dtype="f32", final_state=True, extras=True),
