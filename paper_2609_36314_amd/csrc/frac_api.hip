@@ -71,8 +71,13 @@ frac_status fill_shape(const frac_shape* sh, frac::ScanParams& p) {
 }
 
 // The chunked scan keeps one 64-column tile of x per chunk in LDS: headdim <= 64.
+// The tiles of 64 tokens are addressed with 32-bit byte offsets: 64 rows of x
+// (H P elements apart) and of B, C (G N elements apart) must span < 2 GiB.
 frac_status check_scan_shape(const frac::ScanParams& p, const char* what) {
   if (p.PP > 64) return fail(FRAC_ERR_UNSUPPORTED, "%s: headdim %d > 64 is not built", what, p.P);
+  const int64_t es = p.io_bf16 ? 2 : 4, lim = (int64_t)1 << 31;
+  if (64 * (int64_t)p.H * p.P * es >= lim || 64 * (int64_t)p.G * p.N * es >= lim)
+    return fail(FRAC_ERR_UNSUPPORTED, "%s: nheads * headdim or ngroups * dstate too large", what);
   return FRAC_OK;
 }
 

@@ -199,6 +199,20 @@ __device__ __forceinline__ void softmax_fast(float* z, int M) {
   for (int m = 0; m < MP; ++m) z[m] *= inv;
 }
 
+// softmax across the MP consecutive lanes that hold the modes of one token (MP a
+// power of two dividing 64, lane = token * MP + mode); -inf entries get weight 0.
+template <int MP>
+__device__ __forceinline__ float group_softmax(float z) {
+  float mx = z;
+#pragma unroll
+  for (int o = 1; o < MP; o <<= 1) mx = fmaxf(mx, __shfl_xor(mx, o, 64));
+  const float e = __expf(z - mx);
+  float sum = e;
+#pragma unroll
+  for (int o = 1; o < MP; o <<= 1) sum += __shfl_xor(sum, o, 64);
+  return e * __frcp_rn(sum);
+}
+
 // ------------------------------------------------ LDS fragment reads (K = rows)
 
 typedef short v4i16 __attribute__((ext_vector_type(4)));
@@ -246,29 +260,45 @@ __device__ __forceinline__ void col4_rows(const float* m, int ld, int row0, int 
 
 // -------------------------------------------------- direct global -> LDS tiles
 
-// 16 zero bytes: the source of padded rows and columns of a staged tile.
-static __device__ const int4 kZero16 = {0, 0, 0, 0};
-
-// Copy a 64-row tile into LDS with 16-byte direct-to-LDS loads (no registers):
-// tile row t is `cols` elements at src + t * gstride; the LDS row stride is
-// `lstride` elements (a multiple of 16 bytes, >= cols).  Rows >= nv and columns
-// >= cols are zero-filled.  Each wave copies consecutive 1 KB runs of the tile.
-template <typename T>
-__device__ __forceinline__ void dma_tile(T* lds, const T* src, int64_t gstride, int cols, int lstride, int nv) {
-  constexpr int E = 16 / sizeof(T);
-  const int nwt = blockDim.x >> 6, wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int cpr = lstride / E;
-  const int total = 64 * cpr;
-  for (int base = wave * 64; base < total; base += nwt * 64) {
-    const int pos = base + lane;
-    if (pos < total) {
-      const int row = pos / cpr, ch = pos - row * cpr;
-      const void* g = (row < nv && ch * E < cols) ? (const void*)(src + (int64_t)row * gstride + ch * E)
-                                                  : (const void*)&kZero16;
-      __builtin_amdgcn_global_load_lds(g, (__attribute__((address_space(3))) void*)(lds + base * E), 16, 0, 0);
+// Direct global -> LDS copy of a 64-row tile with a padded LDS row stride LDW
+// (elements; LDW * sizeof(T) a multiple of 16), through a buffer resource.  A
+// block of 8 waves issues KT 16-byte copies per lane; copy k of wave w fills LDS
+// bytes [(8k + w) 1024, +1024), so lane l writes 16-byte chunk
+// q = (8k + w) 64 + l = row * (LDW / E) + chunk of the tile.  The per-lane byte
+// offsets depend on the sizes only and are computed once (init).  Chunks that are
+// padding or lie past `cols`, and rows past the valid ones, get an offset past the
+// resource's range: the hardware returns zeros for them.
+template <typename T, int LDW>
+struct DmaPlan {
+  static constexpr int E = 16 / sizeof(T);
+  static constexpr int CPR = LDW / E;  // 16-byte chunks per LDS row
+  static constexpr int KT = (64 * CPR + 511) / 512;
+  static constexpr unsigned kOut = 0x80000000u;  // >= every range handed to issue()
+  unsigned off[KT];
+  // gstride: elements between consecutive rows; requires 64 gstride sizeof(T) < 2^31
+  __device__ __forceinline__ void init(int64_t gstride, int cols) {
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+#pragma unroll
+    for (int k = 0; k < KT; ++k) {
+      const int q = (k * 8 + wave) * 64 + lane;
+      const int row = q / CPR, ch = q - row * CPR;
+      off[k] = (q < 64 * CPR && ch * E < cols) ? (unsigned)((row * gstride + ch * E) * (int64_t)sizeof(T)) : kOut;
     }
   }
-}
+  // Copy the tile whose first row is at src; only the first nv rows are in range.
+  __device__ __forceinline__ void issue(T* lds, const T* src, int64_t gstride, int nv) const {
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const long long range = (long long)nv * gstride * (long long)sizeof(T);
+    const __amdgpu_buffer_rsrc_t rs =
+        __builtin_amdgcn_make_buffer_rsrc((void*)src, (short)0, (int)(range < kOut ? range : kOut), 0x00020000);
+#pragma unroll
+    for (int k = 0; k < KT; ++k) {
+      if (k * 8 + wave >= CPR) continue;  // past the tile (uniform)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (__attribute__((address_space(3))) void*)(lds + (k * 8 + wave) * 64 * E),
+                                               16, (int)off[k], 0, 0, 0);
+    }
+  }
+};
 
 // Wait for this wave's outstanding vector-memory operations (including the
 // direct-to-LDS copies, which the compiler does not count).

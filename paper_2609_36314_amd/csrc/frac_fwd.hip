@@ -115,11 +115,12 @@ __global__ void __launch_bounds__(256) frac_cb_kernel(ScanParams p, T* __restric
 
 // ------------------------------------------------------------------- the scan
 
-// LDS row strides (elements) of the staged tiles; padded so that the transposed
+// LDS row strides (elements) of the staged tiles, padded so that the transposed
 // fragment reads of 4 consecutive rows and the row reads of 16 rows spread over
 // the LDS banks.  bfloat16 tiles are double-buffered: the next chunk is copied
-// in (direct global -> LDS) while the current one is computed.
-template <typename T, int NB>
+// in (direct global -> LDS) while the current one is computed.  The block is
+// always 8 waves: 4 blocks of 16 columns of P times 2 parts.
+template <typename T, int MP, int NB>
 struct FwdCfg {
   static constexpr int NP = NB * 16;
   static constexpr bool kBf16 = sizeof(T) == 2;
@@ -128,39 +129,68 @@ struct FwdCfg {
   static constexpr int CS = kBf16 ? NP + 8 : NP + 4;    // C tile   [t][n]
   static constexpr int GS = kBf16 ? 64 + 8 : 64 + 4;    // ((C B^T) o Gamma)^T [k][t]
   static constexpr int NBUF = kBf16 ? 2 : 1;
+  // Two waves per 16-column block of P.  With two or more modes they split the
+  // modes (each holds all of N for its modes); with one mode they split N.
+  // With 8 modes the columns of P are split over two workgroups (PS) so that
+  // every wave holds at most 2 modes x all of N of state.  The 8 waves of a
+  // workgroup are NPW blocks of 16 columns of P times NPART parts; the parts
+  // split the modes (2 or more modes) or N (one mode).
+  static constexpr int PS = MP >= 8 ? 2 : 1;
+  static constexpr int NPW = 4 / PS;
+  static constexpr bool kModeSplit = MP >= 2;
+  static constexpr int NPART = kModeSplit ? 8 / NPW : (NB >= 2 ? 2 : 1);
+  static constexpr int MPW = kModeSplit ? MP / NPART : MP;           // modes per wave
+  static constexpr int NBW = (!kModeSplit && NB >= 2) ? NB / 2 : NB;  // 16-row blocks of N per wave
+  static constexpr int KBW = (NBW + 1) / 2;                           // 32-deep K steps of the readout
+  static constexpr int TBO = 4 / NPART;                               // row blocks of y finished per wave
+  // row blocks of the readout whose C fragments are held at once (register budget)
+  static constexpr int TBP = (kBf16 ? MPW * NBW < 16 : MPW * NBW < 8) ? 4 : (kBf16 || MPW * NBW < 16) ? 2 : 1;
 };
 
 template <typename T, int MP, int NB>
 __global__ void __launch_bounds__(512) frac_fwd_kernel(ScanParams p, const T* __restrict__ gtiles) {
-  using Cfg = FwdCfg<T, NB>;
+  using Cfg = FwdCfg<T, MP, NB>;
   constexpr int NP = Cfg::NP, XS = Cfg::XS, BS = Cfg::BS, CS = Cfg::CS, GS = Cfg::GS;
-  constexpr int NH = NB >= 2 ? 2 : 1;     // N halves (waves per p-block)
-  constexpr int NBW = NB / NH;            // 16-row blocks of N owned by a wave
-  constexpr int KBW = (NBW + 1) / 2;      // 32-row K steps of the readout per wave
-  const int NWT = blockDim.x >> 6;        // waves in the workgroup
-  const int NW = NWT / NH;                // p-blocks
-  const int PP = NW * 16;
+  constexpr int NPART = Cfg::NPART, MPW = Cfg::MPW, NBW = Cfg::NBW, KBW = Cfg::KBW, TBP = Cfg::TBP;
+  constexpr int NWT = 8;                  // waves in the workgroup
   const int tid = threadIdx.x;
   const int wave = tid >> 6, lane = tid & 63, li = lane & 15, lg = lane >> 4;
-  const int pb = wave % NW, nh = wave / NW;
+  const int ps = blockIdx.x % Cfg::PS;                  // which columns of P
+  const int pb = ps * Cfg::NPW + wave % Cfg::NPW, part = wave / Cfg::NPW;
+  // waves past the P blocks (or the second part when there is one) only stage
+  // tiles, compute controls and Gamma tiles
+  const bool active = pb * 16 < p.PP && part < NPART;
+  const int mo = Cfg::kModeSplit ? part * MPW : 0;                 // first mode of this wave
+  const int nbo = (!Cfg::kModeSplit && NPART == 2) ? part * NBW : 0;  // first N block of this wave
   const int pc = pb * 16 + li;
   const int L = p.L, H = p.H, P = p.P, N = p.N, M = p.M, G = p.G;
   const int nchunks = (L + kQ - 1) / kQ;
 
   // Blocks are dealt round-robin to the 8 XCDs; give each XCD a contiguous run of
   // (batch, head) so that heads sharing B and C share one L2.
-  int j = blockIdx.x;
-  const int nblk = gridDim.x;
-  if ((nblk & 7) == 0) j = (blockIdx.x & 7) * (nblk >> 3) + (blockIdx.x >> 3);
+  int j = blockIdx.x / Cfg::PS;
+  const int nblk = gridDim.x / Cfg::PS;
+  if ((nblk & 7) == 0) j = (j & 7) * (nblk >> 3) + (j >> 3);
   const int b = j / H, h = j - b * H, g = h * G / H;
 
   __shared__ __align__(16) T Xb0[64 * XS], Bb0[64 * BS], Cb0[64 * CS];
   __shared__ __align__(16) T Xb1[Cfg::NBUF == 2 ? 64 * XS : 8], Bb1[Cfg::NBUF == 2 ? 64 * BS : 8],
       Cb1[Cfg::NBUF == 2 ? 64 * CS : 8];
-  __shared__ __align__(16) T GGT[64 * GS];   // ((C B^T) o Gamma)^T of the chunk, causal
-  __shared__ __align__(16) T Yb[64 * XS];    // output rows of the previous chunk
-  __shared__ __align__(16) float prm[6 * MP * kQ + kQ];
-  __shared__ __align__(16) float YX[NH > 1 ? 4 * 1024 : 4];
+  // everything else in one array, so that its addresses differ by constants
+  constexpr int oGG = 0;                                        // T [64][GS] ((C B^T) o Gamma)^T, causal
+  constexpr int oYb = oGG + 64 * GS * (int)sizeof(T);           // T [64][XS] output rows of the previous chunk
+  constexpr int oPrm = oYb + 64 * XS * (int)sizeof(T);          // float [6 MP + 1][Q] per-token weights
+  constexpr int NSLOT = 4 - Cfg::TBO;                           // row blocks a wave hands over
+  constexpr int oYX = oPrm + (6 * MP * kQ + kQ) * 4;            // float [8 waves][NSLOT][4][64] readout exchange
+  constexpr int oSc = oYX + (NPART > 1 ? 8 * NSLOT * 256 : 4) * 4;  // float rates, log tau, scales
+  __shared__ __align__(16) unsigned char sm[oSc + 4 * MP * 4];
+  T* GGT = reinterpret_cast<T*>(sm + oGG);
+  T* Yb = reinterpret_cast<T*>(sm + oYb);
+  float* prm = reinterpret_cast<float*>(sm + oPrm);
+  float* YX = reinterpret_cast<float*>(sm + oYX);
+  float* s_rr = reinterpret_cast<float*>(sm + oSc);
+  float* s_lnt = s_rr + MP;
+  float* s_E2 = s_lnt + MP;  // [2][MP] by chunk parity
   float* P_om = prm;              // [MP][Q] c e^{-rA_t} E_m        (readout)
   float* P_v = P_om + MP * kQ;    // [MP][Q] kappa e^{-r(A_Q-A_t)} upd (update)
   float* P_O = P_v + MP * kQ;     // [MP][Q] c e^{-r A_t}            (Gamma rows)
@@ -175,41 +205,41 @@ __global__ void __launch_bounds__(512) frac_fwd_kernel(ScanParams p, const T* __
   T* yg = reinterpret_cast<T*>(p.y) + (((int64_t)b * L) * H + h) * P;
   const int64_t xstride = (int64_t)H * P, bstride = (int64_t)G * N;
 
-  // per-mode rates 1/tau_m and log tau_m, read from LDS where needed
-  __shared__ float s_rr[MP], s_lnt[MP];
+  // per-mode rates 1/tau_m, log tau_m and state scales E_m (by chunk parity) in LDS
   if (tid < MP) {
     const float tau = (tid < M) ? p.tau[tid] : 1.0f;
     s_rr[tid] = (tid < M) ? 1.0f / tau : 0.0f;
     s_lnt[tid] = (tid < M) ? logf(tau) : 0.0f;
+    s_E2[tid] = 1.0f;
   }
-  for (int i = tid; i < 64 * GS; i += blockDim.x) GGT[i] = (T)0.0f;
+  // tiles start zeroed: columns past P or N are never copied into
+  for (int i = tid; i < 64 * GS; i += 512) GGT[i] = (T)0.0f;
+  for (int i = tid; i < 64 * XS; i += 512) Xb0[i] = Xb1[Cfg::NBUF == 2 ? i : 0] = (T)0.0f;
+  for (int i = tid; i < 64 * BS; i += 512) Bb0[i] = Bb1[Cfg::NBUF == 2 ? i : 0] = (T)0.0f;
+  for (int i = tid; i < 64 * CS; i += 512) Cb0[i] = Cb1[Cfg::NBUF == 2 ? i : 0] = (T)0.0f;
 
-  // ---- state: S[m][jb] holds rows n = 16 (nh NBW + jb) + 4 lg + r, column pc
+  // ---- state: S[m][jb] holds mode mo + m, rows n = 16 (nbo + jb) + 4 lg + r, column pc
   const int64_t sbase = ((int64_t)b * H + h) * (int64_t)M * N * P;
-  floatx4 S[MP][NBW];
-  float E[MP];
+  floatx4 S[MPW][NBW];
   {
     // lane offset kept opaque so that the final store cannot share (and keep alive
     // across the sequence loop) the per-element offsets of this load
-    int lo = (nh * NBW * 16 + lg * 4) * P + pc;
+    int lo = (mo * N + nbo * 16 + lg * 4) * P + pc;
     asm volatile("" : "+v"(lo));
 #pragma unroll
-    for (int m = 0; m < MP; ++m) {
-      E[m] = 1.0f;
+    for (int m = 0; m < MPW; ++m)
 #pragma unroll
       for (int jb = 0; jb < NBW; ++jb)
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          const int n = (nh * NBW + jb) * 16 + lg * 4 + r;
+          const int n = (nbo + jb) * 16 + lg * 4 + r;
           float v = 0.0f;
-          if (p.init_state && m < M && n < N && pc < P)
+          if (p.init_state && active && mo + m < M && n < N && pc < P)
             v = p.init_state[sbase + lo + ((int64_t)m * N + jb * 16 + r) * P];
           S[m][jb][r] = v;
         }
-    }
   }
   const float Dh = p.D ? p.D[h] : 0.0f;
-  const bool w_is_c = p.write_logit == p.read_logit;  // then the write weights equal the read weights
 
   // per-token controls of a chunk, loaded one chunk ahead (lane = token)
   const float* dt_bh = p.dt + (int64_t)b * L * H + h;
@@ -219,6 +249,7 @@ __global__ void __launch_bounds__(512) frac_fwd_kernel(ScanParams p, const T* __
   const int64_t lm_st = p.ls1;
   const float* rl_bh = p.read_logit ? p.read_logit + ((int64_t)b * L * H + h) * M : nullptr;
   const float* wl_bh = p.write_logit ? p.write_logit + ((int64_t)b * L * H + h) * M : nullptr;
+  const bool w_is_c = wl_bh == rl_bh;  // then the write weights equal the read weights
   const int64_t lg_st = (int64_t)H * M;
   auto load_controls = [&](int c, float& dtv, float& al, float& lam) {
     const int tg = c * kQ + lane;
@@ -227,21 +258,30 @@ __global__ void __launch_bounds__(512) frac_fwd_kernel(ScanParams p, const T* __
     al = valid ? al_bh[tg * al_st] : 1.0f;
     lam = (valid && lm_bh) ? lm_bh[tg * lm_st] : 1.0f;
   };
+  DmaPlan<T, XS> planX;
+  DmaPlan<T, BS> planB;
+  DmaPlan<T, CS> planC;
+  planX.init(xstride, P);
+  planB.init(bstride, N);
+  planC.init(bstride, N);
   auto stage = [&](int c, T* Xd, T* Bd, T* Cd) {
     const int t0 = c * kQ, nv = min(kQ, L - t0);
-    dma_tile<T>(Xd, xg + (int64_t)t0 * xstride, xstride, P, XS, nv);
-    dma_tile<T>(Bd, Bgp + (int64_t)t0 * bstride, bstride, N, BS, nv);
-    dma_tile<T>(Cd, Cgp + (int64_t)t0 * bstride, bstride, N, CS, nv);
+    planX.issue(Xd, xg + (int64_t)t0 * xstride, xstride, nv);
+    planB.issue(Bd, Bgp + (int64_t)t0 * bstride, bstride, nv);
+    planC.issue(Cd, Cgp + (int64_t)t0 * bstride, bstride, nv);
   };
   // output rows of chunk c (staged in Yb) -> global, 16 bytes per thread
   auto store_y = [&](int c) {
     constexpr int E8 = 16 / sizeof(T);
     const int t0 = c * kQ, nv = min(kQ, L - t0);
-    const int cpr = P / E8;
-    for (int i = tid; i < nv * cpr; i += blockDim.x) {
-      const int t = i / cpr, ch = i - t * cpr;
-      *reinterpret_cast<int4*>(yg + (int64_t)(t0 + t) * xstride + ch * E8) =
-          *reinterpret_cast<const int4*>(Yb + t * XS + ch * E8);
+    constexpr int CY = 64 / E8;  // 16-byte chunks of a 64-column row
+#pragma unroll
+    for (int i0 = 0; i0 < 64 * CY; i0 += 512) {
+      const int i = i0 + tid, t = i / CY, ch = i & (CY - 1);
+      const int col = ch * E8;  // only this workgroup's columns of P
+      if (t < nv && col < P && col >= ps * Cfg::NPW * 16 && col < (ps + 1) * Cfg::NPW * 16)
+        *reinterpret_cast<int4*>(yg + (int64_t)(t0 + t) * xstride + ch * E8) =
+            *reinterpret_cast<const int4*>(Yb + t * XS + ch * E8);
     }
   };
 
@@ -254,6 +294,8 @@ __global__ void __launch_bounds__(512) frac_fwd_kernel(ScanParams p, const T* __
   auto step = [&](int c, T* Xc, T* Bc, T* Cc, T* Xn, T* Bn, T* Cn) __attribute__((always_inline)) {
     const int t0 = c * kQ;
     const int nv = min(kQ, L - t0);
+    const float* Ecur = s_E2 + (c & 1) * MP;
+    float* Enext = s_E2 + ((c + 1) & 1) * MP;
     wait_vmem();
     barrier();  // this chunk's tiles have landed; every wave is done with the previous chunk
     if (c > 0) store_y(c - 1);
@@ -264,63 +306,58 @@ __global__ void __launch_bounds__(512) frac_fwd_kernel(ScanParams p, const T* __
       wait_vmem();
       barrier();
     }
-    const float dtv = dt_n, al = al_n, lam = lam_n;
+    const float dtv = dt_n, al_l = al_n, lam_l = lam_n;
     if (c + 1 < nchunks) load_controls(c + 1, dt_n, al_n, lam_n);
 
-    // ---- controls and weights, lane = token; wave w stores modes m % NWT == w
-    // per-mode flags as scalar bit masks: bit m of `renbits` set = the state of
-    // mode m is folded back to unit scale after this chunk, bit m of `unsafe` set
-    // = the factorised Gamma would overflow for mode m (direct decay instead)
-    float renf[MP];
-    int renbits = 0, unsafe = 0;
-    {
-      const int t = lane;
+    // ---- per-token step and its chunk-local cumulative sum (lane = token, every wave)
+    const float s_eff_l = lm_bh ? exp2f(log2f(lam_l) / al_l) : 1.0f;
+    const float dtt_l = (lane < nv) ? dtv * s_eff_l : 0.0f;
+    const float A_l = wave_inclusive_sum(dtt_l);
+    const float Alast = uniform(__shfl(A_l, 63, 64));
+    if (wave == 0) P_A[lane] = A_l;
+
+    // ---- per (token, mode) controls and weights: thread pair = t MP + m
+    int unsafe = 0;  // bit m: the factorised Gamma would overflow for mode m (direct decay)
+    for (int pr = tid; pr < kQ * MP; pr += 512) {
+      const int t = pr / MP, m = pr - t * MP;
+      const float A = __shfl(A_l, t, 64), dtt = __shfl(dtt_l, t, 64), al = __shfl(al_l, t, 64);
       const bool valid = t < nv;
-      const int64_t ith = (int64_t)(t0 + t) * lg_st;
-      const float s_eff = lm_bh ? exp2f(log2f(lam) / al) : 1.0f;
-      const float dtt = valid ? dtv * s_eff : 0.0f;
-      const float A = wave_inclusive_sum(dtt);
-      const float Alast = uniform(__shfl(A, 63, 64));
-      float zc[MP], zw[MP];
+      const int64_t ith = (int64_t)(t0 + t) * lg_st + m;
+      const float r = s_rr[m], prior = -al * s_lnt[m];
+      float zc = (m < M) ? prior + ((rl_bh && valid) ? rl_bh[ith] : 0.0f) : -INFINITY;
+      float zw = (m < M) ? prior + ((wl_bh && valid) ? wl_bh[ith] : 0.0f) : -INFINITY;
+      const float cw = group_softmax<MP>(zc);
+      const float ww = w_is_c ? cw : group_softmax<MP>(zw);
+      const float xr = r * Alast;
+      const bool safe = xr <= kSafeExponent;
+      const float Enew = Ecur[m] * fexp(-xr);
+      const bool ren = !(Enew >= kRescaleFloor);
+      const float upd = ren ? 1.0f : __frcp_rn(Enew);
+      const float kap = one_minus_exp_neg(dtt * r) * ww;
+      const float om = cw * fexp(-r * A);
+      P_O[m * kQ + t] = om;
+      P_om[m * kQ + t] = om * Ecur[m];
+      P_v[m * kQ + t] = kap * fexp(-r * (Alast - A)) * upd;
+      P_Vt[m * kQ + t] = safe ? kap * fexp(r * A) : 0.0f;
+      P_c[m * kQ + t] = cw;
+      P_k[m * kQ + t] = kap;
+      if (pr < MP) Enext[m] = ren ? 1.0f : Enew;
+      // lanes 0..MP-1 of every wave hold modes 0..MP-1 of one token
+      unsafe = (int)(__ballot(m < M && !safe) & ((1ull << MP) - 1));
+    }
+    unsafe = __builtin_amdgcn_readfirstlane(unsafe);
+    // this wave's modes: rescale flags and factors (wave-uniform)
+    float renf[MPW];
+    int renbits = 0;
 #pragma unroll
-      for (int m = 0; m < MP; ++m) {
-        const float prior = -al * s_lnt[m];
-        zc[m] = prior + ((rl_bh && valid && m < M) ? rl_bh[ith + m] : 0.0f);
-        zw[m] = prior + ((wl_bh && valid && m < M) ? wl_bh[ith + m] : 0.0f);
-      }
-      softmax_fast<MP>(zc, M);
-      if (w_is_c) {
-#pragma unroll
-        for (int m = 0; m < MP; ++m) zw[m] = zc[m];
-      } else {
-        softmax_fast<MP>(zw, M);
-      }
-      if (wave == 0) P_A[t] = A;
-#pragma unroll
-      for (int m = 0; m < MP; ++m) {
-        const float r = s_rr[m];
-        // r A_Q and the new scale are wave-uniform and non-negative: compare bit patterns
-        const float xr = uniform(r * Alast);
-        const bool safe = __float_as_int(xr) <= __float_as_int(kSafeExponent);
-        if (m < M && !safe) unsafe |= 1 << m;
-        const float Enew = uniform(E[m] * fexp(-xr));
-        const bool ren = __float_as_int(Enew) < __float_as_int(kRescaleFloor);
-        if (ren) renbits |= 1 << m;
-        renf[m] = Enew;
-        if ((m % NWT) != wave) continue;
-        const float upd = ren ? 1.0f : __frcp_rn(Enew);
-        const float kap = one_minus_exp_neg(dtt * r) * zw[m];
-        const float om = zc[m] * fexp(-r * A);
-        P_O[m * kQ + t] = om;
-        P_om[m * kQ + t] = om * E[m];
-        P_v[m * kQ + t] = kap * fexp(-r * (Alast - A)) * upd;
-        P_Vt[m * kQ + t] = safe ? kap * fexp(r * A) : 0.0f;
-        P_c[m * kQ + t] = zc[m];
-        P_k[m * kQ + t] = kap;
-      }
+    for (int m = 0; m < MPW; ++m) {
+      const float Enew = uniform(Ecur[mo + m] * fexp(-s_rr[mo + m] * Alast));
+      renf[m] = Enew;
+      if (__float_as_int(Enew) < __float_as_int(kRescaleFloor)) renbits |= 1 << m;
     }
     barrier();  // controls in LDS
 
+    __builtin_amdgcn_sched_barrier(0);
     // ---- ((C B^T) o Gamma)^T, lower-triangular 16x16 tiles split over the waves
     {
       const T* gt = gtiles + (((int64_t)b * nchunks + c) * G + g) * (kTiles * kTileElems);
@@ -348,32 +385,37 @@ __global__ void __launch_bounds__(512) frac_fwd_kernel(ScanParams p, const T* __
             }
           }
         }
-        T* dst = GGT + (kb * 16 + li) * GS + tb * 16 + lg * 4;
+        float gv[4];
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int t = tb * 16 + lg * 4 + r, k = kb * 16 + li;
-          dst[r] = (T)((t >= k) ? Gt[r] * Gm[r] : 0.0f);
+          gv[r] = (t >= k) ? Gt[r] * Gm[r] : 0.0f;
         }
+        T* dst = GGT + (kb * 16 + li) * GS + tb * 16 + lg * 4;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) dst[r] = (T)gv[r];
       }
     }
 
-    // ---- readout of the state entering the chunk (this wave's rows of N)
+    __builtin_amdgcn_sched_barrier(0);
+    // ---- readout of the state entering the chunk, this wave's modes
     floatx4 Y[4];
 #pragma unroll
     for (int tb = 0; tb < 4; ++tb) Y[tb] = floatx4{0.f, 0.f, 0.f, 0.f};
-    {
-      Frag<T> Ca[4][KBW];
+    if (active) {
 #pragma unroll
-      for (int tb = 0; tb < 4; ++tb)
+    for (int tp = 0; tp < 4 / TBP; ++tp) {
+      Frag<T> Ca[TBP][KBW];
+#pragma unroll
+      for (int i = 0; i < TBP; ++i)
 #pragma unroll
         for (int kb = 0; kb < KBW; ++kb) {
-          const T* row = Cc + (tb * 16 + li) * CS + nh * NBW * 16 + kb * 32 + lg * 4;
-          Ca[tb][kb] = frag_load4x2(row, (2 * kb + 1 < NBW) ? row + 16 : nullptr);
+          const T* row = Cc + ((tp * TBP + i) * 16 + li) * CS + nbo * 16 + kb * 32 + lg * 4;
+          Ca[i][kb] = frag_load4x2(row, (2 * kb + 1 < NBW) ? row + 16 : nullptr);
         }
 #pragma unroll
-      for (int m = 0; m < MP; ++m) {
-        if (m >= M) continue;
-        Frag<T> Sf[KBW];
+      for (int m = 0; m < MPW; ++m) {
+        Frag<T> Sf[KBW];  // modes >= M hold a zero state and zero weights
 #pragma unroll
         for (int kb = 0; kb < KBW; ++kb) {
 #pragma unroll
@@ -382,11 +424,12 @@ __global__ void __launch_bounds__(512) frac_fwd_kernel(ScanParams p, const T* __
           for (int s = 0; s < 4; ++s) frag_set(Sf[kb], 4 + s, (2 * kb + 1 < NBW) ? S[m][2 * kb + 1][s] : 0.0f);
         }
 #pragma unroll
-        for (int tb = 0; tb < 4; ++tb) {
+        for (int i = 0; i < TBP; ++i) {
+          const int tb = tp * TBP + i;
           floatx4 Z = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-          for (int kb = 0; kb < KBW; ++kb) mma(Z, Ca[tb][kb], Sf[kb]);
-          const float4 om = *reinterpret_cast<const float4*>(P_om + m * kQ + tb * 16 + lg * 4);
+          for (int kb = 0; kb < KBW; ++kb) mma(Z, Ca[i][kb], Sf[kb]);
+          const float4 om = *reinterpret_cast<const float4*>(P_om + (mo + m) * kQ + tb * 16 + lg * 4);
           Y[tb][0] += om.x * Z[0];
           Y[tb][1] += om.y * Z[1];
           Y[tb][2] += om.z * Z[2];
@@ -394,26 +437,34 @@ __global__ void __launch_bounds__(512) frac_fwd_kernel(ScanParams p, const T* __
         }
       }
     }
-    if (NH > 1) {
-      // hand the row blocks finished by the other N half over through LDS
-      float* dst = YX + ((pb * 2 + nh) * 2) * 4 * 64;
+    if (NPART > 1) {
+      // hand the row blocks the other parts of this P block finish over through LDS
+      float* dst = YX + wave * NSLOT * 256;
 #pragma unroll
-      for (int jj = 0; jj < 2; ++jj) {
-        const int tb = (1 - nh) * 2 + jj;
+      for (int tb = 0; tb < 4; ++tb) {
+        if (tb / Cfg::TBO == part) continue;
+        const int slot = tb < part * Cfg::TBO ? tb : tb - Cfg::TBO;
 #pragma unroll
-        for (int r = 0; r < 4; ++r) dst[(jj * 4 + r) * 64 + lane] = Y[tb][r];
+        for (int r = 0; r < 4; ++r) dst[(slot * 4 + r) * 64 + lane] = Y[tb][r];
       }
     }
+    }  // active
     barrier();  // GGT and YX complete
+    if (!active) return;
 
+    __builtin_amdgcn_sched_barrier(0);
     // ---- intra-chunk product, skip term, output rows into Yb
 #pragma unroll
     for (int tb = 0; tb < 4; ++tb) {
-      if (NH > 1 && (tb >> 1) != nh) continue;
-      if (NH > 1) {
-        const float* src = YX + ((pb * 2 + (1 - nh)) * 2) * 4 * 64;
+      if (NPART > 1 && tb / Cfg::TBO != part) continue;
+      // partial sums of the other parts, added in part order
 #pragma unroll
-        for (int r = 0; r < 4; ++r) Y[tb][r] += src[((tb & 1) * 4 + r) * 64 + lane];
+      for (int q = 0; q < NPART; ++q) {
+        if (q == part) continue;
+        const int slot = tb < q * Cfg::TBO ? tb : tb - Cfg::TBO;
+        const float* src = YX + (q * Cfg::NPW + wave % Cfg::NPW) * NSLOT * 256;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) Y[tb][r] += src[(slot * 4 + r) * 64 + lane];
       }
 #pragma unroll
       for (int kk = 0; kk <= tb / 2; ++kk) {
@@ -427,9 +478,10 @@ __global__ void __launch_bounds__(512) frac_fwd_kernel(ScanParams p, const T* __
       for (int r = 0; r < 4; ++r) Yb[(tb * 16 + lg * 4 + r) * XS + pc] = (T)(Y[tb][r] + Dh * xv[r]);
     }
 
-    // ---- state update  S_m <- (rescale) + B^T (v_m o X)
+    __builtin_amdgcn_sched_barrier(0);
+    // ---- state update  S_m <- (rescale) + B^T (v_m o X), this wave's modes
 #pragma unroll
-    for (int m = 0; m < MP; ++m) {
+    for (int m = 0; m < MPW; ++m) {
       if (!((renbits >> m) & 1)) continue;
 #pragma unroll
       for (int jb = 0; jb < NBW; ++jb)
@@ -439,32 +491,29 @@ __global__ void __launch_bounds__(512) frac_fwd_kernel(ScanParams p, const T* __
 #pragma unroll
     for (int kt = 0; kt < 2; ++kt) {
       const Frag<T> xf = frag_load_rows(Xc, XS, kt * 32 + lg * 8, pb * 16);
-      float xs[8];
+      Frag<T> Xf[MPW];
 #pragma unroll
-      for (int s = 0; s < 8; ++s) xs[s] = to_f32(xf.v[s]);
-      Frag<T> a[NBW];
+      for (int m = 0; m < MPW; ++m) {
+        const float* pv = P_v + (mo + m) * kQ + kt * 32 + lg * 8;
+        const float4 v0 = *reinterpret_cast<const float4*>(pv);
+        const float4 v1 = *reinterpret_cast<const float4*>(pv + 4);
+        frag_set(Xf[m], 0, to_f32(xf.v[0]) * v0.x);
+        frag_set(Xf[m], 1, to_f32(xf.v[1]) * v0.y);
+        frag_set(Xf[m], 2, to_f32(xf.v[2]) * v0.z);
+        frag_set(Xf[m], 3, to_f32(xf.v[3]) * v0.w);
+        frag_set(Xf[m], 4, to_f32(xf.v[4]) * v1.x);
+        frag_set(Xf[m], 5, to_f32(xf.v[5]) * v1.y);
+        frag_set(Xf[m], 6, to_f32(xf.v[6]) * v1.z);
+        frag_set(Xf[m], 7, to_f32(xf.v[7]) * v1.w);
+      }
 #pragma unroll
-      for (int jb = 0; jb < NBW; ++jb) a[jb] = frag_load_rows(Bc, BS, kt * 32 + lg * 8, (nh * NBW + jb) * 16);
+      for (int jb = 0; jb < NBW; ++jb) {
+        const Frag<T> a = frag_load_rows(Bc, BS, kt * 32 + lg * 8, (nbo + jb) * 16);
 #pragma unroll
-      for (int m = 0; m < MP; ++m) {
-        if (m >= M) continue;
-        const float4 v0 = *reinterpret_cast<const float4*>(P_v + m * kQ + kt * 32 + lg * 8);
-        const float4 v1 = *reinterpret_cast<const float4*>(P_v + m * kQ + kt * 32 + lg * 8 + 4);
-        Frag<T> Xf;
-        frag_set(Xf, 0, xs[0] * v0.x);
-        frag_set(Xf, 1, xs[1] * v0.y);
-        frag_set(Xf, 2, xs[2] * v0.z);
-        frag_set(Xf, 3, xs[3] * v0.w);
-        frag_set(Xf, 4, xs[4] * v1.x);
-        frag_set(Xf, 5, xs[5] * v1.y);
-        frag_set(Xf, 6, xs[6] * v1.z);
-        frag_set(Xf, 7, xs[7] * v1.w);
-#pragma unroll
-        for (int jb = 0; jb < NBW; ++jb) mma(S[m][jb], a[jb], Xf);
+        for (int m = 0; m < MPW; ++m)
+          mma(S[m][jb], a, Xf[m]);  // modes >= M carry zero weights
       }
     }
-#pragma unroll
-    for (int m = 0; m < MP; ++m) E[m] = ((renbits >> m) & 1) ? 1.0f : renf[m];
   };
 
   for (int c = 0; c < nchunks; c += 2) {
@@ -478,25 +527,23 @@ __global__ void __launch_bounds__(512) frac_fwd_kernel(ScanParams p, const T* __
   barrier();
   store_y(nchunks - 1);
 
-  if (p.final_state) {
-    int lo = (nh * NBW * 16 + lg * 4) * P + pc;
+  if (p.final_state && active) {
+    const float* Ef = s_E2 + (nchunks & 1) * MP;
+    int lo = (mo * N + nbo * 16 + lg * 4) * P + pc;
     asm volatile("" : "+v"(lo));
 #pragma unroll
-    for (int m = 0; m < MP; ++m)
+    for (int m = 0; m < MPW; ++m) {
+      const float Em = (mo + m < M) ? Ef[mo + m] : 0.0f;
 #pragma unroll
       for (int jb = 0; jb < NBW; ++jb)
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          const int n = (nh * NBW + jb) * 16 + lg * 4 + r;
-          if (m < M && n < N && pc < P)
-            p.final_state[sbase + lo + ((int64_t)m * N + jb * 16 + r) * P] = S[m][jb][r] * E[m];
+          const int n = (nbo + jb) * 16 + lg * 4 + r;
+          if (mo + m < M && n < N && pc < P)
+            p.final_state[sbase + lo + ((int64_t)m * N + jb * 16 + r) * P] = S[m][jb][r] * Em;
         }
+    }
   }
-}
-
-template <int NB>
-constexpr int halves() {
-  return NB >= 2 ? 2 : 1;
 }
 
 template <typename T>
@@ -519,11 +566,10 @@ hipError_t launch_cb_variant(const ScanParams& p, T* gt, hipStream_t stream) {
 
 template <typename T, int MP, int NB>
 hipError_t launch_fwd_variant(const ScanParams& p, void* ws, hipStream_t stream) {
-  constexpr int NH = halves<NB>();
   T* gt = reinterpret_cast<T*>(ws);
   hipError_t e = launch_cb_variant<T, NB>(p, gt, stream);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((frac_fwd_kernel<T, MP, NB>), dim3(p.Bsz * p.H), dim3(64 * (p.PP / 16) * NH), 0, stream, p,
+  hipLaunchKernelGGL((frac_fwd_kernel<T, MP, NB>), dim3(p.Bsz * p.H * FwdCfg<T, MP, NB>::PS), dim3(512), 0, stream, p,
                      (const T*)gt);
   return hipGetLastError();
 }

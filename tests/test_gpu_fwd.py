@@ -82,6 +82,9 @@ SMALL = {
     "bf16 L1 init": Workload("t", 2, 1, 2, 64, 128, 4, final_state=True, init_state=True),
     "bf16 per-head alpha": LONG_PREFILL.scaled(seqlen=300, nheads=4),
     "f32 M8 N128": Workload("t", 1, 150, 2, 64, 128, 8, io_dtype="f32", final_state=True, extras=True),
+    # 8 modes split P over two workgroups: a partly filled second half, an empty one
+    "bf16 M8 P48 groups": Workload("t", 2, 190, 4, 48, 64, 8, ngroups=2, final_state=True, init_state=True),
+    "bf16 M6 P16 N32": Workload("t", 1, 129, 2, 16, 32, 6, final_state=True, extras=True),
 }
 
 
