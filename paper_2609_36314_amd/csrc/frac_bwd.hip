@@ -4,38 +4,42 @@
 // (eq. frac-selective-update, eq. frac-readout, the Appendix-D algorithm), with
 // the B/C-widened state, evaluated chunk by chunk like the forward.  Per mode
 // (r = 1/tau_m), chunk-local inclusive cumulative step A_t, chunk total A_Q,
-// state entering the chunk S0 and adjoint of the chunk's last state G_out:
+// state entering the chunk S0 and adjoint of the chunk's last state G:
 //
-//   dC_t  = sum_m c e^{-rA_t} S0^T-contraction: sum_m c_{t,m} e^{-r A_t} S0_m dy_t
-//           + sum_{k<=t} Gamma_{t,k} (dy_t . x_k) B_k
-//   dx_t  = sum_m kappa_{t,m} e^{-r(A_Q - A_t)} G_out,m^T B_t
+//   dC_t  = sum_m c_{t,m} e^{-r A_t} S0_m dy_t + sum_{k<=t} Gamma_{t,k} (dy_t . x_k) B_k
+//   dx_t  = sum_m kappa_{t,m} e^{-r(A_Q - A_t)} B_t G_m
 //           + sum_{t'>=t} Gamma_{t',t} (C_t' . B_t) dy_t' + D dy_t
-//   dB_t  = sum_m kappa_{t,m} e^{-r(A_Q - A_t)} G_out,m x_t
+//   dB_t  = sum_m kappa_{t,m} e^{-r(A_Q - A_t)} G_m x_t
 //           + sum_{t'>=t} Gamma_{t',t} (dy_t' . x_t) C_t'
-//   G_out(previous chunk) = e^{-r A_Q} G_out + sum_t c_{t,m} e^{-r A_t} C_t dy_t^T
+//   G (entering the previous chunk) = e^{-r A_Q} G + sum_t c_{t,m} e^{-r A_t} C_t dy_t^T
 //
-// and for the step sizes (with dc = C^T S dy, dkappa = B^T G x per token and mode):
+// and for the step sizes (dc = C^T S dy, dkappa = B^T G x per token and mode):
 //   ddtt_t = -sum_m r_m <dS_final, S_final>_m - sum_{t'>=t} e_t' + f_t
 //   e_t = sum_m r_m (c dc - kappa dkappa)_{t,m},  f_t = sum_m r_m w rho dkappa_{t,m}
 //   ddt_t = ddtt_t * lambda_t^(1/alpha_t)
 // (the gradient of the cumulative log-retention telescopes into the suffix sum of
-// e; derived from the recurrence, checked against the float64 oracle).  Inside a
-// chunk the e/f terms reduce to row and column sums of
+// e).  Inside a chunk the e/f terms reduce to row and column sums of
 //   H o Phi and H o Psi,  H = (C B^T) o (dY X^T),
 //   Phi_{t,k} = sum_m r_m c_{t,m} kappa_{k,m} e^{-r(A_t - A_k)},
 //   Psi_{t,k} = sum_m r_m c_{t,m} w_{k,m} rho_{k,m} e^{-r(A_t - A_k)},
 // rank-M products like Gamma.
 //
-// Three independent sweeps run in one launch (blockIdx.y), one workgroup per
-// (batch, head) each; a state or adjoint share lives in matrix-core accumulators:
-//   0  forward sweep, state held transposed (wave = 16 columns of N, all of P):
-//      recomputes S, gives dC (per head), the readout and intra-chunk parts of
-//      e, f, the final-state term and sum(dy . x) for dD;
-//   1  reverse sweep, adjoint in row layout (waves = P blocks x N halves): dx and
-//      the state-adjoint parts of e and f;
-//   2  reverse sweep, adjoint transposed (wave = 16 columns of N): dB (per head).
-// A finishing kernel forms ddt from the suffix sums, and a reduction kernel sums
-// dB and dC over the heads of each group in a fixed order.
+// Three sweeps, each its own kernel; every wave keeps its share of a state or
+// adjoint (at most 2 x 4 16x16 float32 tiles per mode group) in matrix-core
+// accumulators for the whole sequence:
+//   state  forward in time, state transposed (lane = column n of N, rows p): dC
+//          (per head), the readout and intra-chunk parts of e and f, the
+//          final-state term and sum(dy . x) for dD;
+//   rows   reverse, adjoint in row layout (lane = column p of P, rows n): dx and
+//          the adjoint parts of e and f;
+//   cols   reverse, adjoint transposed (lane = column n): dB (per head).
+// With many modes and a wide state the state and cols sweeps split N, and the
+// rows sweep splits P, over two workgroups per (batch, head), so that no
+// per-head output gets a second partial sum.  Tiles are copied straight into
+// LDS (natural layout, padded rows) and read back as matrix-core fragments with
+// row reads or transposed 64-bit reads.  A finishing kernel forms ddt from the
+// suffix sums, and a reduction kernel sums dB and dC over the heads of each group
+// in a fixed order.
 #include "frac_device.h"
 #include "frac_kernels.h"
 
@@ -47,49 +51,11 @@ __constant__ int kTB[10] = {0, 1, 1, 2, 2, 2, 3, 3, 3, 3};
 __constant__ int kKB[10] = {0, 0, 1, 0, 1, 2, 0, 1, 2, 3};
 constexpr int kTiles = 10;
 constexpr int kTileElems = 256;
-// row block of lower-triangular tile `tile` (0..9, row-major over tb >= kb)
-__host__ __device__ constexpr int tile_tb(int tile) { return tile < 1 ? 0 : tile < 3 ? 1 : tile < 6 ? 2 : 3; }
 constexpr float kSafeExponent = 55.0f;
 constexpr float kRescaleFloor = 0x1p-60f;
-constexpr int kPBM = 4;  // p-blocks of 16 held per wave in the transposed layouts (P <= 64)
-constexpr int LDQ = kQ + 8;
-constexpr int LDP = 64 + 8;
 
 __device__ __forceinline__ float uniform(float v) {
   return __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(v)));
-}
-
-// Sum over the 16 lanes of a lane group of v[j], returned in the lane whose
-// index within the group is j (8 + 4 + 2 + 1 exchanges).
-__device__ __forceinline__ float transpose_reduce16(float v[16], int li) {
-#pragma unroll
-  for (int j = 0; j < 8; ++j) {
-    const bool hi = li & 8;
-    const float send = hi ? v[j] : v[j + 8];
-    const float keep = hi ? v[j + 8] : v[j];
-    v[j] = keep + __shfl_xor(send, 8, 64);
-  }
-#pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const bool hi = li & 4;
-    const float send = hi ? v[j] : v[j + 4];
-    const float keep = hi ? v[j + 4] : v[j];
-    v[j] = keep + __shfl_xor(send, 4, 64);
-  }
-#pragma unroll
-  for (int j = 0; j < 2; ++j) {
-    const bool hi = li & 2;
-    const float send = hi ? v[j] : v[j + 2];
-    const float keep = hi ? v[j + 2] : v[j];
-    v[j] = keep + __shfl_xor(send, 2, 64);
-  }
-  {
-    const bool hi = li & 1;
-    const float send = hi ? v[0] : v[1];
-    const float keep = hi ? v[1] : v[0];
-    v[0] = keep + __shfl_xor(send, 1, 64);
-  }
-  return v[0];
 }
 
 // Sum over the 16 lanes of a lane group of v[r] (r = 0..3); returned in every
@@ -113,78 +79,125 @@ __device__ __forceinline__ float reduce16_4(float v[4], int li) {
   return v[0];
 }
 
-// token of value index j = 4 tb + r held by lane group lg
-__device__ __forceinline__ int tok_of(int j, int lg) { return (j >> 2) * 16 + lg * 4 + (j & 3); }
+// ------------------------------------------------------------ shared pieces
 
-// Stage 64 rows (tokens) of `ncols` io elements, row t at g + t * stride, into
-// LDS: natural [t][ldn] and/or transposed [col][LDQ]; rows >= nv and columns
-// >= ncols (up to ncols_pad) are zero.
 template <typename T>
-__device__ __forceinline__ void stage(const T* g, int64_t stride, int ncols, int ncols_pad, int nv, T* nat, int ldn, T* tr) {
-  const int groups = ncols_pad >> 3;
-  for (int idx = threadIdx.x; idx < kQ * groups; idx += blockDim.x) {
-    const int t = idx / groups, c0 = (idx - t * groups) * 8;
-    float v[8];
-    if (t < nv && c0 < ncols) load8(g + t * stride + c0, v);
-    else {
-#pragma unroll
-      for (int j = 0; j < 8; ++j) v[j] = 0.0f;
-    }
-    if (nat) {
-#pragma unroll
-      for (int j = 0; j < 8; ++j) nat[t * ldn + c0 + j] = (T)v[j];
-    }
-    if (tr) {
-#pragma unroll
-      for (int j = 0; j < 8; ++j) tr[(c0 + j) * LDQ + t] = (T)v[j];
-    }
-  }
-}
-
-// Controls of the lane's token: effective step and the read / write weights.
-template <int MP>
-__device__ __forceinline__ void token_controls(const ScanParams& p, int b, int h, int64_t tg, bool valid,
-                                               const float* lnt, float& dtt, float& s_eff, float* c, float* w) {
-  const int64_t ith = ((int64_t)b * p.L + tg) * p.H + h;
-  const float dtv = valid ? p.dt[ith] : 0.0f;
-  const float al = valid ? strided3(p.alpha, p.as0, p.as1, p.as2, b, tg, h) : 1.0f;
-  const float lam = (valid && p.lambda) ? strided3(p.lambda, p.ls0, p.ls1, p.ls2, b, tg, h) : 1.0f;
-  s_eff = p.lambda ? exp2f(log2f(lam) / al) : 1.0f;
-  dtt = valid ? dtv * s_eff : 0.0f;
-#pragma unroll
-  for (int m = 0; m < MP; ++m) {
-    const float prior = -al * lnt[m];
-    c[m] = prior + ((p.read_logit && valid && m < p.M) ? p.read_logit[ith * p.M + m] : 0.0f);
-    w[m] = prior + ((p.write_logit && valid && m < p.M) ? p.write_logit[ith * p.M + m] : 0.0f);
-  }
-  softmax_modes<MP>(c, p.M);
-  softmax_modes<MP>(w, p.M);
-}
-
-// Per-mode chunk scalars of the lazily rescaled state / adjoint S = E S^:
-// this chunk's decay folds into E unless E would drop below the floor, in which
-// case the accumulators are rescaled (ren) and E restarts at 1.
-struct ModeScale {
-  float E;       // scale of the state entering the chunk
-  float Enew;    // E * e^{-r A_Q}
-  bool ren;      // rescale the accumulators by Enew before adding this chunk
-  float upd;     // factor on this chunk's additions (1/Enew or 1)
-  bool safe;     // r A_Q small enough for the factorised decay
+struct Pad {
+  static constexpr bool kBf16 = sizeof(T) == 2;
+  static constexpr int XS = kBf16 ? 64 + 8 : 64 + 4;  // [t][p] tiles and [t][t'] tiles
+  template <int NP>
+  static constexpr int BS = kBf16 ? NP + 16 : NP + 8;  // [t][n] tiles read transposed
+  template <int NP>
+  static constexpr int CS = kBf16 ? NP + 8 : NP + 4;  // [t][n] tiles read along rows
 };
 
-__device__ __forceinline__ void mode_scale(ModeScale& s, float r, float Alast) {
-  const float xr = r * Alast;
-  s.safe = xr <= kSafeExponent;
-  s.Enew = uniform(s.E * expf(-xr));
-  s.ren = !(s.Enew >= kRescaleFloor);
-  s.upd = s.ren ? 1.0f : 1.0f / s.Enew;
+// Which sweep computes a chunk's per-(token, mode) weights, and which of them.
+enum Role { kState = 0, kRows = 1, kCols = 2 };
+
+// Number of [MP][Q] weight arrays a role keeps in LDS (plus one [Q] array for A_t).
+template <int ROLE>
+constexpr int n_weight_arrays() {
+  return ROLE == kState ? 9 : ROLE == kRows ? 7 : 6;
 }
 
-__device__ __forceinline__ void mode_scale_advance(ModeScale& s) { s.E = s.ren ? 1.0f : s.Enew; }
+// Per-wave chunk controls (lane = token): effective step, its chunk-local
+// inclusive sum and the chunk total.
+struct ChunkCtl {
+  float dtt, A, al, Alast;
+};
 
-// Rank-M product sum_m a[m][row] b[m][col] over a 16x16 tile (float32 matrix cores).
+__device__ __forceinline__ ChunkCtl chunk_controls(float dtv, float al, float lam, bool has_lambda, int nv) {
+  const int lane = threadIdx.x & 63;
+  ChunkCtl k;
+  const float s_eff = has_lambda ? exp2f(log2f(lam) / al) : 1.0f;
+  k.dtt = (lane < nv) ? dtv * s_eff : 0.0f;
+  k.A = wave_inclusive_sum(k.dtt);
+  k.Alast = uniform(__shfl(k.A, 63, 64));
+  k.al = al;
+  return k;
+}
+
+// Per-(token, mode) weights of one chunk, pair = t * MP + m, written to the
+// role's LDS arrays w[i * MP * Q + m * Q + t].  Returns the modes whose chunk
+// decay exceeds the factorisation bound (bit m).
+//   state: 0 c e^{-rA}, 1 kappa e^{rA} (safe), 2 r c e^{-rA}, 3 r w rho e^{rA} (safe),
+//          4 c e^{-rA} E, 5 kappa e^{-r(A_Q-A)} upd, 6 c, 7 kappa, 8 r w rho
+//   rows:  0 c e^{-rA}, 1 kappa e^{rA} (safe), 2 c, 3 kappa, 4 kappa e^{-r(A_Q-A)} E,
+//          5 r w rho e^{-r(A_Q-A)} E, 6 c e^{-rA} upd
+//   cols:  0 c e^{-rA}, 1 kappa e^{rA} (safe), 2 c, 3 kappa, 4 kappa e^{-r(A_Q-A)} E,
+//          5 c e^{-rA} upd
+// E is the scale of the state (or adjoint) before this chunk's update, upd the
+// factor on the update (1/E_new, or 1 when the accumulators are folded back).
+template <int MP, int ROLE>
+__device__ __forceinline__ int pair_weights(const ChunkCtl& k, int t0, int nv, int M, const float* rl, const float* wl,
+                                            int64_t lg_st, const float* s_rr, const float* s_lnt, const float* Ecur,
+                                            float* Enext, float* w) {
+  const int tid = threadIdx.x;
+  const bool w_is_c = rl == wl;
+  for (int pr = tid; pr < kQ * MP; pr += 512) {
+    const int t = pr / MP, m = pr - t * MP;
+    const float A = __shfl(k.A, t, 64), dtt = __shfl(k.dtt, t, 64), al = __shfl(k.al, t, 64);
+    const bool valid = t < nv;
+    const int64_t ith = (int64_t)(t0 + t) * lg_st + m;
+    const float r = s_rr[m], prior = -al * s_lnt[m];
+    const float zc = (m < M) ? prior + ((rl && valid) ? rl[ith] : 0.0f) : -INFINITY;
+    const float zw = (m < M) ? prior + ((wl && valid) ? wl[ith] : 0.0f) : -INFINITY;
+    // tokens past the sequence get zero weights (their tile rows may hold anything finite)
+    const float cw = valid ? group_softmax<MP>(zc) : 0.0f;
+    const float ww = w_is_c ? cw : (valid ? group_softmax<MP>(zw) : 0.0f);
+    const float xr = r * k.Alast;
+    const bool safe = xr <= kSafeExponent;
+    const float E = Ecur[m];
+    const float Enew = E * fexp(-xr);
+    const bool ren = !(Enew >= kRescaleFloor);
+    const float upd = ren ? 1.0f : __frcp_rn(Enew);
+    const float beta = one_minus_exp_neg(dtt * r);
+    const float kap = beta * ww;
+    const float ea = fexp(-r * A);
+    const float ep = safe ? fexp(r * A) : 0.0f;
+    const float dec = fexp(-r * (k.Alast - A));
+    float* o = w + m * kQ + t;
+    constexpr int SW = MP * kQ;  // stride of the weight arrays
+    if constexpr (ROLE == kState) {
+      const float rwr = r * ww * (1.0f - beta);
+      o[0 * SW] = cw * ea;
+      o[1 * SW] = kap * ep;
+      o[2 * SW] = r * cw * ea;
+      o[3 * SW] = rwr * ep;
+      o[4 * SW] = cw * ea * E;
+      o[5 * SW] = kap * dec * upd;
+      o[6 * SW] = cw;
+      o[7 * SW] = kap;
+      o[8 * SW] = rwr;
+    } else if constexpr (ROLE == kRows) {
+      o[0 * SW] = cw * ea;
+      o[1 * SW] = kap * ep;
+      o[2 * SW] = cw;
+      o[3 * SW] = kap;
+      o[4 * SW] = kap * dec * E;
+      o[5 * SW] = r * ww * (1.0f - beta) * dec * E;
+      o[6 * SW] = cw * ea * upd;
+    } else {
+      o[0 * SW] = cw * ea;
+      o[1 * SW] = kap * ep;
+      o[2 * SW] = cw;
+      o[3 * SW] = kap;
+      o[4 * SW] = kap * dec * E;
+      o[5 * SW] = cw * ea * upd;
+    }
+    if (pr < MP) Enext[m] = ren ? 1.0f : Enew;
+  }
+  // the same flags in every wave: lane m < MP tests mode m
+  const int lane = tid & 63;
+  const bool over = lane < MP && lane < M && !(s_rr[lane < MP ? lane : 0] * k.Alast <= kSafeExponent);
+  return (int)(__ballot(over) & ((1ull << MP) - 1));
+}
+
+// Rank-M product sum_m a[m][row0 + i] b[m][col0 + j] over a 16x16 tile
+// (float32 matrix cores, modes as K), in the accumulator layout.
 template <int MP>
-__device__ __forceinline__ floatx4 rank_m_tile(const float* a, const float* bm, int row0, int col0, int li, int lg) {
+__device__ __forceinline__ floatx4 rank_m_tile(const float* a, const float* bm, int row0, int col0) {
+  const int li = threadIdx.x & 15, lg = (threadIdx.x >> 4) & 3;
   floatx4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
   for (int q = 0; q < (MP + 3) / 4; ++q) {
@@ -196,926 +209,1169 @@ __device__ __forceinline__ floatx4 rank_m_tile(const float* a, const float* bm, 
   return acc;
 }
 
-// dY X^T tile (rows tb, cols kb), K over P (<= 64) from natural-layout LDS.
-template <typename T>
-__device__ __forceinline__ floatx4 dyx_tile(const T* dYs, const T* Xs, int tb, int kb, int PP, int li, int lg) {
+// Modes past the factorisation bound: add the pairwise-decay terms of
+// sum_m a_m[t] b_m[k] s_m e^{-r_m (A_t - A_k)} (t >= k) to a 16x16 tile.
+template <int MP>
+__device__ __forceinline__ void unsafe_terms(floatx4& acc, int unsafe, const float* a, const float* bm, const float* A,
+                                             const float* s_rr, int tb, int kb, bool scale_r) {
+  const int li = threadIdx.x & 15, lg = (threadIdx.x >> 4) & 3;
+  for (int m = 0; m < MP; ++m) {
+    if (!((unsafe >> m) & 1)) continue;
+    const float rm = s_rr[m];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int t = tb * 16 + lg * 4 + r, k = kb * 16 + li;
+      if (t >= k) acc[r] += (scale_r ? rm : 1.0f) * a[m * kQ + t] * bm[m * kQ + k] * fexp(-rm * (A[t] - A[k]));
+    }
+  }
+}
+
+// dY X^T tile (rows tb, cols kb), K over the 64 columns of P, from natural tiles.
+template <typename T, int XS>
+__device__ __forceinline__ floatx4 dyx_tile(const T* Ys, const T* Xs, int tb, int kb) {
+  const int li = threadIdx.x & 15, lg = (threadIdx.x >> 4) & 3;
   floatx4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-  for (int kk = 0; kk < 2; ++kk) {
-    const int p0 = kk * 32 + lg * 8;
-    Frag<T> a = frag_zero<T>(), bb = frag_zero<T>();
-    if (p0 < PP) {
-      a = frag_load8(dYs + (tb * 16 + li) * LDP + p0);
-      bb = frag_load8(Xs + (kb * 16 + li) * LDP + p0);
-    }
-    mma(acc, a, bb);
+  for (int kp = 0; kp < 2; ++kp) {
+    const T* ra = Ys + (tb * 16 + li) * XS + kp * 32 + lg * 4;
+    const T* rb = Xs + (kb * 16 + li) * XS + kp * 32 + lg * 4;
+    mma(acc, frag_load4x2(ra, ra + 16), frag_load4x2(rb, rb + 16));
   }
   return acc;
 }
 
-template <typename T>
-__device__ __forceinline__ void load_gtile(const T* gt, int tile, int lane, float* Gt) {
+// Hand-over of partial 16x16 row blocks between the NPART waves that share a
+// block of columns: part q finishes the row blocks tb with tb % OW == q (OW =
+// min(NPART, 4)); every other part writes its partial of that block to a slot.
+template <int NPART>
+struct Exchange {
+  static constexpr int OW = NPART < 4 ? NPART : 4;
+  static constexpr int NSLOT = NPART > 4 ? 4 : 4 - 4 / NPART;
+  static constexpr int kFloats = NPART > 1 ? 8 * NSLOT * 256 : 4;
+  static __device__ __forceinline__ bool owns(int tb, int part) { return tb % OW == part; }
+  static __device__ __forceinline__ int slot(int tb, int part) {
+    int s = 0;
 #pragma unroll
-  for (int r = 0; r < 4; ++r) Gt[r] = to_f32(gt[tile * kTileElems + lane * 4 + r]);
+    for (int j = 0; j < 4; ++j)
+      if (j < tb && !owns(j, part)) ++s;
+    return s;
+  }
+  // wave `wave` (part `part`) publishes its non-owned partial blocks
+  static __device__ __forceinline__ void put(float* X, int wave, int part, const floatx4* acc) {
+    const int lane = threadIdx.x & 63;
+#pragma unroll
+    for (int tb = 0; tb < 4; ++tb) {
+      if (owns(tb, part)) continue;
+      float* dst = X + (wave * NSLOT + slot(tb, part)) * 256;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) dst[r * 64 + lane] = acc[tb][r];
+    }
+  }
+  // the owner adds the other parts' partials of row block tb, in part order;
+  // wave_of(q) is the wave of part q with the same columns
+  template <typename F>
+  static __device__ __forceinline__ void gather(const float* X, int part, int tb, floatx4& acc, F wave_of) {
+    const int lane = threadIdx.x & 63;
+#pragma unroll
+    for (int q = 0; q < NPART; ++q) {
+      if (q == part) continue;
+      const float* src = X + (wave_of(q) * NSLOT + slot(tb, q)) * 256;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) acc[r] += src[r * 64 + lane];
+    }
+  }
+};
+
+// XCD-aware (batch, head) of a block with PS blocks per head: heads dealt to
+// the 8 XCDs in contiguous runs so that heads sharing B and C share an L2.
+__device__ __forceinline__ void block_head(int PS, int H, int& b, int& h, int& ps) {
+  ps = blockIdx.x % PS;
+  int j = blockIdx.x / PS;
+  const int nblk = gridDim.x / PS;
+  if ((nblk & 7) == 0) j = (j & 7) * (nblk >> 3) + (j >> 3);
+  b = j / H;
+  h = j - b * H;
 }
 
-// --------------------------------------------------------------------------
-// sweep 0: forward direction, state transposed (rows p, columns n)
+struct BwdWork {
+  const void* tiles;  // C B^T tiles
+  void* dBp;          // per-head dB, [B, L, H, N]
+  void* dCp;          // per-head dC
+  float* eA;          // [2][B L H] readout / intra part of e (per N half)
+  float* fA;          // [B L H] intra part of f
+  float* eB;          // [2][B L H] adjoint part of e (per P half)
+  float* fB;          // [2][B L H] adjoint part of f
+  float* F;           // [2][B H] final-state term (per N half)
+  float* dDp;         // [B H] sum(dy . x)
+};
+
+// ------------------------------------------------ state / cols sweep layout
+
+// Transposed layout (lane = column n): the workgroup holds NBF 16-column blocks
+// of N (all of N, or half when MP * NB > 32); its 8 waves are those blocks times
+// FPART parts, the parts splitting the modes.
+template <typename T, int MP, int NB>
+struct ColCfg {
+  static constexpr int NP = NB * 16;
+  static constexpr int XS = Pad<T>::XS;
+  static constexpr int BS = Pad<T>::template BS<NP>;
+  static constexpr int CS = Pad<T>::template CS<NP>;
+  static constexpr int PS = MP * NB > 32 ? 2 : 1;
+  static constexpr int NBF = NB / PS;
+  static constexpr int FPART = 8 / NBF;
+  static constexpr int MPF = MP >= FPART ? MP / FPART : 1;
+  static constexpr int NACT = MP >= FPART ? FPART : MP;  // parts holding modes (the rest idle)
+  static constexpr int NBUF = Pad<T>::kBf16 ? 2 : 1;
+};
+
+// ------------------------------------------------------------ state sweep
 
 template <typename T, int MP, int NB>
-__device__ __forceinline__ void sweep_state(const ScanParams& p, int b, int h, int g, const T* __restrict__ gtiles,
-                            T* __restrict__ dCp, float* __restrict__ eA, float* __restrict__ fA,
-                            float* __restrict__ Fw, float* __restrict__ dDp, unsigned char* smem) {
-  constexpr int NP = NB * 16;
-  const int PP = p.PP, PB = PP / 16, KP = (PB + 1) / 2;
-  const int NWT = blockDim.x >> 6;
+__global__ void __launch_bounds__(512) frac_bwd_state_kernel(ScanParams p, BwdWork wk) {
+  using Cfg = ColCfg<T, MP, NB>;
+  constexpr int NP = Cfg::NP, XS = Cfg::XS, BS = Cfg::BS, CS = Cfg::CS;
+  constexpr int NBF = Cfg::NBF, FPART = Cfg::FPART, MPF = Cfg::MPF;
+  using Ex = Exchange<Cfg::NACT>;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, li = lane & 15, lg = lane >> 4;
-  const bool active = wave < NB;
-  const int ncol = wave * 16 + li;  // state column n of this lane
-  const int L = p.L, H = p.H, P = p.P, N = p.N, M = p.M;
+  const int L = p.L, H = p.H, P = p.P, N = p.N, M = p.M, G = p.G;
   const int nchunks = (L + kQ - 1) / kQ;
+  int b, h, ps;
+  block_head(Cfg::PS, H, b, h, ps);
+  const int g = h * G / H;
+  const int nbl = wave % NBF, part = wave / NBF, nb = ps * NBF + nbl, ncol = nb * 16 + li;
+  const int mo = part * MPF;
+  const bool active = mo < MP;
 
-  T* Xs = reinterpret_cast<T*>(smem);  // [Q][LDP]
-  T* XT = Xs + kQ * LDP;               // [64][LDQ]
-  T* dYs = XT + 64 * LDQ;              // [Q][LDP]
-  T* BT = dYs + kQ * LDP;              // [NP][LDQ]
-  T* CT = BT + NP * LDQ;               // [NP][LDQ]
-  T* HG = CT + NP * LDQ;               // [Q][LDQ]  Gamma o dY X^T (natural)
-  float* P_O = reinterpret_cast<float*>(HG + kQ * LDQ);  // [MP][Q] c e^{-rA}
-  float* P_Vt = P_O + MP * kQ;    // kappa e^{rA} (safe)
-  float* P_rO = P_Vt + MP * kQ;   // r c e^{-rA}
-  float* P_Y = P_rO + MP * kQ;    // r w rho e^{rA} (safe)
-  float* P_wdc = P_Y + MP * kQ;   // c e^{-rA} E
-  float* P_wec = P_wdc + MP * kQ; // r c e^{-rA} E
-  float* P_v = P_wec + MP * kQ;   // kappa e^{-r(A_Q - A)} * upd
-  float* P_c = P_v + MP * kQ;     // c
-  float* P_k = P_c + MP * kQ;     // kappa
-  float* P_wr = P_k + MP * kQ;    // r w rho
-  float* P_A = P_wr + MP * kQ;    // [Q]
-  float* redR = P_A + kQ;         // [8][Q]  per-wave readout-side partials (also the final reduce)
-  float* redC = redR + 8 * kQ;    // [8][Q]  final reduce
-  float* slotR = redC + 8 * kQ;   // [10 tiles][16] row sums of H o Phi
-  float* slotC = slotR + kTiles * 16;  // column sums of H o Phi
-  float* slotF = slotC + kTiles * 16;  // column sums of H o Psi
+  __shared__ __align__(16) T Xb0[64 * XS], Yb0[64 * XS], Bb0[64 * BS];
+  __shared__ __align__(16) T Xb1[Cfg::NBUF == 2 ? 64 * XS : 8], Yb1[Cfg::NBUF == 2 ? 64 * XS : 8],
+      Bb1[Cfg::NBUF == 2 ? 64 * BS : 8];
+  __shared__ __align__(16) T Cb[64 * CS];
+  constexpr int NWA = n_weight_arrays<kState>();
+  constexpr int oHG = 0;                                         // T [k][t] (Gamma o dY X^T)^T, causal
+  constexpr int oW = oHG + 64 * XS * (int)sizeof(T);             // float weights [NWA][MP][Q], A [Q]
+  constexpr int oSl = oW + (NWA * MP * kQ + kQ) * 4;             // float slots R, C, F [10][16] each
+  constexpr int oRd = oSl + 3 * kTiles * 16 * 4;                 // float [8][Q] per-wave token partials
+  constexpr int oEx = oRd + 8 * kQ * 4;                          // float exchange
+  constexpr int oSc = oEx + Ex::kFloats * 4;                     // float rates, log tau, scales
+  __shared__ __align__(16) unsigned char sm[oSc + 4 * MP * 4];
+  T* HGT = reinterpret_cast<T*>(sm + oHG);
+  float* W = reinterpret_cast<float*>(sm + oW);
+  float* P_A = W + NWA * MP * kQ;
+  float* slotR = reinterpret_cast<float*>(sm + oSl);
+  float* slotC = slotR + kTiles * 16;
+  float* slotF = slotC + kTiles * 16;
+  float* redR = reinterpret_cast<float*>(sm + oRd);
+  float* XCH = reinterpret_cast<float*>(sm + oEx);
+  float* s_rr = reinterpret_cast<float*>(sm + oSc);
+  float* s_lnt = s_rr + MP;
+  float* s_E2 = s_lnt + MP;
+  constexpr int SW = MP * kQ;  // stride of the weight arrays
+  const float* P_O = W;
+  const float* P_Vt = W + 1 * SW;
+  const float* P_rO = W + 2 * SW;
+  const float* P_Y = W + 3 * SW;
+  const float* P_wdc = W + 4 * SW;  // times r_m: the readout weight of e
+  const float* P_v = W + 5 * SW;
+  const float* P_c = W + 6 * SW;
+  const float* P_k = W + 7 * SW;
+  const float* P_wr = W + 8 * SW;
 
-  float rr[MP], lnt[MP];
-#pragma unroll
-  for (int m = 0; m < MP; ++m) {
-    const float tau = (m < M) ? p.tau[m] : 1.0f;
-    rr[m] = (m < M) ? 1.0f / tau : 0.0f;
-    lnt[m] = (m < M) ? logf(tau) : 0.0f;
+  if (tid < MP) {
+    const float tau = (tid < M) ? p.tau[tid] : 1.0f;
+    s_rr[tid] = (tid < M) ? 1.0f / tau : 0.0f;
+    s_lnt[tid] = (tid < M) ? logf(tau) : 0.0f;
+    s_E2[tid] = 1.0f;
   }
-  for (int i = tid; i < kQ * LDQ; i += blockDim.x) HG[i] = (T)0.0f;
+  for (int i = tid; i < 64 * XS; i += 512) {
+    HGT[i] = (T)0.0f;
+    Xb0[i] = Yb0[i] = (T)0.0f;
+    Xb1[Cfg::NBUF == 2 ? i : 0] = Yb1[Cfg::NBUF == 2 ? i : 0] = (T)0.0f;
+  }
+  for (int i = tid; i < 64 * BS; i += 512) Bb0[i] = Bb1[Cfg::NBUF == 2 ? i : 0] = (T)0.0f;
+  for (int i = tid; i < 64 * CS; i += 512) Cb[i] = (T)0.0f;
 
+  // ---- state S^T: S[m][pb] holds mode mo + m, rows p = 16 pb + 4 lg + r, column ncol
   const int64_t sbase = ((int64_t)b * H + h) * (int64_t)M * N * P;
-  floatx4 S[MP][kPBM];
-  ModeScale ms[MP];
+  floatx4 S[MPF][4];
   {
-    int lo = (lg * 4) * 1 + ncol * P;  // element (n = ncol, p = 16 pb + 4 lg + r) at sbase + m N P + lo + 16 pb + r
+    int lo = ncol * P + lg * 4;
     asm volatile("" : "+v"(lo));
 #pragma unroll
-    for (int m = 0; m < MP; ++m) {
-      ms[m].E = 1.0f;
+    for (int m = 0; m < MPF; ++m)
 #pragma unroll
-      for (int pb = 0; pb < kPBM; ++pb)
+      for (int pb = 0; pb < 4; ++pb)
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int pr = pb * 16 + lg * 4 + r;
           float v = 0.0f;
-          if (p.init_state && active && m < M && ncol < N && pr < P)
-            v = p.init_state[sbase + (int64_t)m * N * P + lo + pb * 16 + r];
+          if (p.init_state && active && mo + m < M && ncol < N && pr < P)
+            v = p.init_state[sbase + (int64_t)(mo + m) * N * P + lo + pb * 16 + r];
           S[m][pb][r] = v;
         }
-    }
+  }
+
+  const T* xg = reinterpret_cast<const T*>(p.x) + (((int64_t)b * L) * H + h) * P;
+  const T* yg = reinterpret_cast<const T*>(p.dy) + (((int64_t)b * L) * H + h) * P;
+  const T* Bgp = reinterpret_cast<const T*>(p.Bm) + (((int64_t)b * L) * G + g) * N;
+  const T* Cgp = reinterpret_cast<const T*>(p.Cm) + (((int64_t)b * L) * G + g) * N;
+  const int64_t xstride = (int64_t)H * P, bstride = (int64_t)G * N;
+  const float* dt_bh = p.dt + (int64_t)b * L * H + h;
+  const float* al_bh = p.alpha + b * p.as0 + h * p.as2;
+  const float* lm_bh = p.lambda ? p.lambda + b * p.ls0 + h * p.ls2 : nullptr;
+  const float* rl_bh = p.read_logit ? p.read_logit + ((int64_t)b * L * H + h) * M : nullptr;
+  const float* wl_bh = p.write_logit ? p.write_logit + ((int64_t)b * L * H + h) * M : nullptr;
+  const int64_t lg_st = (int64_t)H * M;
+  auto load_controls = [&](int c, float& dtv, float& al, float& lam) {
+    const int tg = c * kQ + lane;
+    const bool valid = tg < L;
+    dtv = valid ? dt_bh[(int64_t)tg * H] : 0.0f;
+    al = valid ? al_bh[tg * p.as1] : 1.0f;
+    lam = (valid && lm_bh) ? lm_bh[tg * p.ls1] : 1.0f;
+  };
+  DmaPlan<T, XS> planX;
+  DmaPlan<T, BS> planB;
+  DmaPlan<T, CS> planC;
+  planX.init(xstride, P);
+  planB.init(bstride, N);
+  planC.init(bstride, N);
+  auto stage = [&](int c, T* Xd, T* Yd, T* Bd) {
+    const int t0 = c * kQ, nv = min(kQ, L - t0);
+    planX.template issue<Cfg::NBUF == 1>(Xd, xg + (int64_t)t0 * xstride, xstride, nv);
+    planX.template issue<Cfg::NBUF == 1>(Yd, yg + (int64_t)t0 * xstride, xstride, nv);
+    planB.template issue<Cfg::NBUF == 1>(Bd, Bgp + (int64_t)t0 * bstride, bstride, nv);
+  };
+  auto stageC = [&](int c) {
+    const int t0 = c * kQ, nv = min(kQ, L - t0);
+    planC.template issue<Cfg::NBUF == 1>(Cb, Cgp + (int64_t)t0 * bstride, bstride, nv);
+  };
+
+  float dt_n, al_n, lam_n;
+  load_controls(0, dt_n, al_n, lam_n);
+  if (Cfg::NBUF == 2) {
+    stage(0, Xb0, Yb0, Bb0);
+    stageC(0);
   }
   float dd_acc = 0.0f;
+  const T* gtiles = reinterpret_cast<const T*>(wk.tiles);
+  T* dCp = reinterpret_cast<T*>(wk.dCp);
+  const int64_t bl_h = (int64_t)p.Bsz * L * H;
 
-  for (int c = 0; c < nchunks; ++c) {
+  auto step = [&](int c, T* Xc, T* Yc, T* Bc, T* Xn, T* Yn, T* Bn) __attribute__((always_inline)) {
     const int t0 = c * kQ, nv = min(kQ, L - t0);
-    __syncthreads();
-    const int64_t xrow0 = (((int64_t)b * L + t0) * H + h) * P;
-    const int64_t brow0 = (((int64_t)b * L + t0) * p.G + g) * N;
-    stage<T>(reinterpret_cast<const T*>(p.x) + xrow0, (int64_t)H * P, P, PP, nv, Xs, LDP, XT);
-    stage<T>(reinterpret_cast<const T*>(p.dy) + xrow0, (int64_t)H * P, P, PP, nv, dYs, LDP, nullptr);
-    stage<T>(reinterpret_cast<const T*>(p.Bm) + brow0, (int64_t)p.G * N, N, NP, nv, nullptr, 0, BT);
-    stage<T>(reinterpret_cast<const T*>(p.Cm) + brow0, (int64_t)p.G * N, N, NP, nv, nullptr, 0, CT);
-    {
-      const int t = lane;
-      const bool valid = t < nv;
-      float dtt, s_eff, cw[MP], ww[MP];
-      token_controls<MP>(p, b, h, t0 + t, valid, lnt, dtt, s_eff, cw, ww);
-      const float A = wave_inclusive_sum(dtt);
-      const float Alast = uniform(__shfl(A, 63, 64));
-      if (wave == 0) P_A[t] = A;
-#pragma unroll
-      for (int m = 0; m < MP; ++m) {
-        mode_scale(ms[m], rr[m], Alast);
-        if ((m % NWT) != wave) continue;
-        const float rho = expf(-dtt * rr[m]);
-        const float kap = -expm1f(-dtt * rr[m]) * ww[m];
-        const float ea = expf(-rr[m] * A);
-        const float ep = ms[m].safe ? expf(rr[m] * A) : 0.0f;
-        P_O[m * kQ + t] = cw[m] * ea;
-        P_Vt[m * kQ + t] = kap * ep;
-        P_rO[m * kQ + t] = rr[m] * cw[m] * ea;
-        P_Y[m * kQ + t] = rr[m] * ww[m] * rho * ep;
-        P_wdc[m * kQ + t] = cw[m] * ea * ms[m].E;
-        P_wec[m * kQ + t] = rr[m] * cw[m] * ea * ms[m].E;
-        P_v[m * kQ + t] = kap * expf(-rr[m] * (Alast - A)) * ms[m].upd;
-        P_c[m * kQ + t] = cw[m];
-        P_k[m * kQ + t] = kap;
-        P_wr[m * kQ + t] = rr[m] * ww[m] * rho;
-      }
+    const float* Ecur = s_E2 + (c & 1) * MP;
+    float* Enext = s_E2 + ((c + 1) & 1) * MP;
+    wait_vmem();
+    barrier();  // this chunk's tiles have landed; the previous chunk is done
+    if (Cfg::NBUF == 2) {
+      if (c + 1 < nchunks) stage(c + 1, Xn, Yn, Bn);
+    } else {
+      stage(c, Xc, Yc, Bc);
+      stageC(c);
+      wait_vmem();
+      barrier();
     }
-    __syncthreads();
+    const float dtv = dt_n, al_l = al_n, lam_l = lam_n;
+    if (c + 1 < nchunks) load_controls(c + 1, dt_n, al_n, lam_n);
+    const ChunkCtl k = chunk_controls(dtv, al_l, lam_l, lm_bh != nullptr, nv);
+    if (wave == 0) P_A[lane] = k.A;
+    const int unsafe = pair_weights<MP, kState>(k, t0, nv, M, rl_bh, wl_bh, lg_st, s_rr, s_lnt, Ecur, Enext, W);
+    float renf[MPF];
+    int renbits = 0;
+#pragma unroll
+    for (int m = 0; m < MPF; ++m) {
+      const float Enew = uniform(Ecur[mo + m] * fexp(-s_rr[mo + m] * k.Alast));
+      renf[m] = Enew;
+      if (__float_as_int(Enew) < __float_as_int(kRescaleFloor)) renbits |= 1 << m;
+    }
+    barrier();  // weights in LDS
 
-    // sum(dy . x) of the chunk for dD (fixed element assignment per thread)
-    for (int i = tid; i < kQ * PP; i += blockDim.x) {
-      const int t = i / PP, pc = i - t * PP;
-      dd_acc += to_f32(Xs[t * LDP + pc]) * to_f32(dYs[t * LDP + pc]);
-    }
-
-    float rowacc[16];
-#pragma unroll
-    for (int j = 0; j < 16; ++j) rowacc[j] = 0.0f;
-    // ---- readout-side terms from the state entering the chunk: dC (inter) and e (inter)
-    floatx4 dCacc[4];
-#pragma unroll
-    for (int tb = 0; tb < 4; ++tb) dCacc[tb] = floatx4{0.f, 0.f, 0.f, 0.f};
-    if (active) {
-      Frag<T> Af[4][2];
-#pragma unroll
-      for (int tb = 0; tb < 4; ++tb)
-#pragma unroll
-        for (int kp = 0; kp < 2; ++kp) {
-          Af[tb][kp] = frag_zero<T>();
-          if (kp < KP) {
-            const T* row = dYs + (tb * 16 + li) * LDP + kp * 32 + lg * 4;
-            Af[tb][kp] = frag_load4x2(row, (2 * kp + 1 < PB) ? row + 16 : nullptr);
-          }
-        }
-#pragma unroll
-      for (int m = 0; m < MP; ++m) {
-        if (m >= M) continue;
-        Frag<T> Sf[2];
-#pragma unroll
-        for (int kp = 0; kp < 2; ++kp) {
-#pragma unroll
-          for (int s = 0; s < 4; ++s) frag_set(Sf[kp], s, S[m][2 * kp][s]);
-#pragma unroll
-          for (int s = 0; s < 4; ++s) frag_set(Sf[kp], 4 + s, S[m][2 * kp + 1][s]);
-        }
-#pragma unroll
-        for (int tb = 0; tb < 4; ++tb) {
-          floatx4 U = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-          for (int kp = 0; kp < 2; ++kp)
-            if (kp < KP) mma(U, Af[tb][kp], Sf[kp]);
-          const float4 wd = *reinterpret_cast<const float4*>(P_wdc + m * kQ + tb * 16 + lg * 4);
-          const float4 we = *reinterpret_cast<const float4*>(P_wec + m * kQ + tb * 16 + lg * 4);
-          dCacc[tb][0] += wd.x * U[0];
-          dCacc[tb][1] += wd.y * U[1];
-          dCacc[tb][2] += wd.z * U[2];
-          dCacc[tb][3] += wd.w * U[3];
-          const T* cr = CT + ncol * LDQ + tb * 16 + lg * 4;
-          rowacc[tb * 4 + 0] += we.x * U[0] * to_f32(cr[0]);
-          rowacc[tb * 4 + 1] += we.y * U[1] * to_f32(cr[1]);
-          rowacc[tb * 4 + 2] += we.z * U[2] * to_f32(cr[2]);
-          rowacc[tb * 4 + 3] += we.w * U[3] * to_f32(cr[3]);
-        }
-        __builtin_amdgcn_sched_barrier(0);
-      }
-    }
-    // ---- intra-chunk tiles: HG = Gamma o D (LDS), H o Phi row / column sums, H o Psi column sums
+    __builtin_amdgcn_sched_barrier(0);
+    // ---- intra-chunk tiles: HG = Gamma o D (LDS, transposed), row / column sums of
+    // H o Phi and column sums of H o Psi (first workgroup of the head only)
     {
-      const T* gt = gtiles + (((int64_t)b * nchunks + c) * p.G + g) * (kTiles * kTileElems);
-      for (int tile = wave; tile < kTiles; tile += NWT) {
+      const T* gt = gtiles + (((int64_t)b * nchunks + c) * G + g) * (kTiles * kTileElems);
+      for (int tile = wave; tile < kTiles; tile += 8) {
         const int tb = kTB[tile], kb = kKB[tile];
-        float Gt[4];
-        load_gtile(gt, tile, lane, Gt);
-        const floatx4 D = dyx_tile<T>(dYs, Xs, tb, kb, PP, li, lg);
-        floatx4 Gm = rank_m_tile<MP>(P_O, P_Vt, tb * 16, kb * 16, li, lg);
-        floatx4 Ph = rank_m_tile<MP>(P_rO, P_Vt, tb * 16, kb * 16, li, lg);
-        floatx4 Ps = rank_m_tile<MP>(P_O, P_Y, tb * 16, kb * 16, li, lg);
-#pragma unroll
-        for (int m = 0; m < MP; ++m) {
-          if (ms[m].safe || m >= M) continue;
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const int t = tb * 16 + lg * 4 + r, k = kb * 16 + li;
-            if (t >= k) {
-              const float d = P_c[m * kQ + t] * expf(-rr[m] * (P_A[t] - P_A[k]));
-              Gm[r] += d * P_k[m * kQ + k];
-              Ph[r] += rr[m] * d * P_k[m * kQ + k];
-              Ps[r] += d * P_wr[m * kQ + k];
-            }
-          }
-        }
-        float rv[4], ce = 0.f, cf = 0.f;
+        const floatx4 D = dyx_tile<T, XS>(Yc, Xc, tb, kb);
+        floatx4 Gm = rank_m_tile<MP>(P_O, P_Vt, tb * 16, kb * 16);
+        if (unsafe) unsafe_terms<MP>(Gm, unsafe, P_c, P_k, P_A, s_rr, tb, kb, false);
+        float hv[4];
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          const int t = tb * 16 + lg * 4 + r, k = kb * 16 + li;
-          const bool ok = t >= k;
-          const float hm = ok ? Gt[r] * D[r] : 0.0f;
-          HG[t * LDQ + k] = (T)(ok ? Gm[r] * D[r] : 0.0f);
-          rv[r] = hm * Ph[r];
-          ce += hm * Ph[r];
-          cf += hm * Ps[r];
+          const int t = tb * 16 + lg * 4 + r, kk = kb * 16 + li;
+          hv[r] = (t >= kk) ? Gm[r] * D[r] : 0.0f;
         }
-        const float rs = reduce16_4(rv, li);
-        if ((li & 3) == 0) slotR[tile * 16 + lg * 4 + ((li >> 2) & 3)] = rs;
-        ce += __shfl_xor(ce, 16, 64);
-        ce += __shfl_xor(ce, 32, 64);
-        cf += __shfl_xor(cf, 16, 64);
-        cf += __shfl_xor(cf, 32, 64);
-        if (lg == 0) {
-          slotC[tile * 16 + li] = ce;
-          slotF[tile * 16 + li] = cf;
+        T* dst = HGT + (kb * 16 + li) * XS + tb * 16 + lg * 4;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) dst[r] = (T)hv[r];
+        if (ps == 0) {
+          floatx4 Ph = rank_m_tile<MP>(P_rO, P_Vt, tb * 16, kb * 16);
+          floatx4 Ps = rank_m_tile<MP>(P_O, P_Y, tb * 16, kb * 16);
+          if (unsafe) {
+            unsafe_terms<MP>(Ph, unsafe, P_c, P_k, P_A, s_rr, tb, kb, true);
+            unsafe_terms<MP>(Ps, unsafe, P_c, P_wr, P_A, s_rr, tb, kb, false);
+          }
+          float rv[4], ce = 0.f, cf = 0.f;
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int t = tb * 16 + lg * 4 + r, kk = kb * 16 + li;
+            const float hm = (t >= kk) ? to_f32(gt[tile * kTileElems + lane * 4 + r]) * D[r] : 0.0f;
+            rv[r] = hm * Ph[r];
+            ce += hm * Ph[r];
+            cf += hm * Ps[r];
+          }
+          const float rs = reduce16_4(rv, li);
+          if ((li & 3) == 0) slotR[tile * 16 + lg * 4 + ((li >> 2) & 3)] = rs;
+          ce += __shfl_xor(ce, 16, 64);
+          ce += __shfl_xor(ce, 32, 64);
+          cf += __shfl_xor(cf, 16, 64);
+          cf += __shfl_xor(cf, 32, 64);
+          if (lg == 0) {
+            slotC[tile * 16 + li] = ce;
+            slotF[tile * 16 + li] = cf;
+          }
         }
       }
     }
 
-    // per-token partials of this wave (readout side) -> LDS
-    redR[wave * kQ + tok_of(li, lg)] = transpose_reduce16(rowacc, li);
-    __syncthreads();  // HG and the per-wave partials are complete
+    __builtin_amdgcn_sched_barrier(0);
+    // ---- readout side of the state entering the chunk, transposed: U^T_m = S_m dY^T
+    // (rows n of this wave's block, columns t), dC^T (inter) and the readout part of e
+    floatx4 dCa[4];  // dC^T: rows n = 16 nb + 4 lg + r, column t = 16 tb + li
+#pragma unroll
+    for (int tb = 0; tb < 4; ++tb) dCa[tb] = floatx4{0.f, 0.f, 0.f, 0.f};
+    {
+      float racc[4] = {0.f, 0.f, 0.f, 0.f};  // per row block: this lane's token
+      if (active) {
+        Frag<T> Sa[MPF][2];
+#pragma unroll
+        for (int m = 0; m < MPF; ++m)
+#pragma unroll
+          for (int kp = 0; kp < 2; ++kp) {
+#pragma unroll
+            for (int s = 0; s < 4; ++s) frag_set(Sa[m][kp], s, S[m][2 * kp][s]);
+#pragma unroll
+            for (int s = 0; s < 4; ++s) frag_set(Sa[m][kp], 4 + s, S[m][2 * kp + 1][s]);
+          }
+#pragma unroll
+        for (int tb = 0; tb < 4; ++tb) {
+          const T* row = Yc + (tb * 16 + li) * XS + lg * 4;
+          const Frag<T> y0 = frag_load4x2(row, row + 16), y1 = frag_load4x2(row + 32, row + 48);
+          floatx4 ws = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+          for (int m = 0; m < MPF; ++m) {
+            floatx4 U = {0.f, 0.f, 0.f, 0.f};
+            mma(U, Sa[m][0], y0);
+            mma(U, Sa[m][1], y1);
+            const float wd = P_wdc[(mo + m) * kQ + tb * 16 + li];
+            const float rm = s_rr[mo + m];
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+              const float v = wd * U[r];
+              dCa[tb][r] += v;
+              ws[r] += rm * v;
+            }
+          }
+          // sum over n of C_t[n] ws[n]: this lane's 4 values, then the 4 lane groups
+          const T* crow = Cb + (tb * 16 + li) * CS + nb * 16 + lg * 4;
+          float cv[4];
+          load4(crow, cv);
+          racc[tb] = ws[0] * cv[0] + ws[1] * cv[1] + ws[2] * cv[2] + ws[3] * cv[3];
+        }
+        if (Cfg::NACT > 1) Ex::put(XCH, wave, part, dCa);
+      }
+#pragma unroll
+      for (int tb = 0; tb < 4; ++tb) {
+        float v = racc[tb];
+        v += __shfl_xor(v, 16, 64);
+        v += __shfl_xor(v, 32, 64);
+        if (lg == 0) redR[wave * kQ + tb * 16 + li] = v;
+      }
+    }
+    barrier();  // HG, slots, token partials and exchange complete; C is free
+    if (Cfg::NBUF == 2 && c + 1 < nchunks) stageC(c + 1);
 
     if (wave == 0) {
-      // token t: readout side (all waves) + row sums of its row-block tiles - column
-      // sums of its column-block tiles, in a fixed order
+      // token t: readout part (all waves) [+ row sums of its row-block tiles - column
+      // sums of its column-block tiles], fixed order
       const int t = lane, tbt = t >> 4, tr = t & 15;
       float er = 0.f, ec = 0.f, ef = 0.f;
-      for (int w2 = 0; w2 < NWT; ++w2) er += redR[w2 * kQ + t];
-      for (int kb2 = 0; kb2 <= tbt; ++kb2) er += slotR[(tbt * (tbt + 1) / 2 + kb2) * 16 + tr];
-      for (int tb2 = tbt; tb2 < 4; ++tb2) {
-        ec += slotC[(tb2 * (tb2 + 1) / 2 + tbt) * 16 + tr];
-        ef += slotF[(tb2 * (tb2 + 1) / 2 + tbt) * 16 + tr];
+      for (int w2 = 0; w2 < 8; ++w2) er += redR[w2 * kQ + t];
+      if (ps == 0) {
+        for (int kb2 = 0; kb2 <= tbt; ++kb2) er += slotR[(tbt * (tbt + 1) / 2 + kb2) * 16 + tr];
+        for (int tb2 = tbt; tb2 < 4; ++tb2) {
+          ec += slotC[(tb2 * (tb2 + 1) / 2 + tbt) * 16 + tr];
+          ef += slotF[(tb2 * (tb2 + 1) / 2 + tbt) * 16 + tr];
+        }
       }
       if (t < nv) {
         const int64_t ith = ((int64_t)b * L + t0 + t) * H + h;
-        eA[ith] = er - ec;
-        fA[ith] = ef;
+        wk.eA[ps * bl_h + ith] = er - ec;
+        if (ps == 0) wk.fA[ith] = ef;
       }
     }
-
-    if (active) {
-      // ---- dC intra: (Gamma o dY X^T) B, causal
-#pragma unroll
-      for (int tb = 0; tb < 4; ++tb)
-#pragma unroll
-        for (int kk = 0; kk <= tb / 2; ++kk) {
-          const Frag<T> a = frag_load8(HG + (tb * 16 + li) * LDQ + kk * 32 + lg * 8);
-          const Frag<T> bb = frag_load8(BT + ncol * LDQ + kk * 32 + lg * 8);
-          mma(dCacc[tb], a, bb);
-        }
-#pragma unroll
-      for (int tb = 0; tb < 4; ++tb)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int t = tb * 16 + lg * 4 + r;
-          if (t < nv && ncol < N) dCp[(((int64_t)b * L + t0 + t) * H + h) * N + ncol] = (T)dCacc[tb][r];
-        }
-
-      // ---- state update S^T += X^T (v o B), rows p, columns n
-#pragma unroll
-      for (int m = 0; m < MP; ++m) {
-        if (!ms[m].ren) continue;
-#pragma unroll
-        for (int pb = 0; pb < kPBM; ++pb)
-#pragma unroll
-          for (int r = 0; r < 4; ++r) S[m][pb][r] *= ms[m].Enew;
-      }
-#pragma unroll
-      for (int kt = 0; kt < 2; ++kt) {
-        float br8[8];
-#pragma unroll
-        for (int s = 0; s < 8; ++s) br8[s] = to_f32(BT[ncol * LDQ + kt * 32 + lg * 8 + s]);
-        Frag<T> Bf[MP];
-#pragma unroll
-        for (int m = 0; m < MP; ++m) {
-          const float4 v0 = *reinterpret_cast<const float4*>(P_v + m * kQ + kt * 32 + lg * 8);
-          const float4 v1 = *reinterpret_cast<const float4*>(P_v + m * kQ + kt * 32 + lg * 8 + 4);
-          frag_set(Bf[m], 0, br8[0] * v0.x);
-          frag_set(Bf[m], 1, br8[1] * v0.y);
-          frag_set(Bf[m], 2, br8[2] * v0.z);
-          frag_set(Bf[m], 3, br8[3] * v0.w);
-          frag_set(Bf[m], 4, br8[4] * v1.x);
-          frag_set(Bf[m], 5, br8[5] * v1.y);
-          frag_set(Bf[m], 6, br8[6] * v1.z);
-          frag_set(Bf[m], 7, br8[7] * v1.w);
-        }
-#pragma unroll
-        for (int pb = 0; pb < kPBM; ++pb) {
-          if (pb >= PB) continue;
-          const Frag<T> a = frag_load8(XT + (pb * 16 + li) * LDQ + kt * 32 + lg * 8);
-#pragma unroll
-          for (int m = 0; m < MP; ++m)
-            if (m < M) mma(S[m][pb], a, Bf[m]);
-        }
+    if (ps == 0) {
+      // sum(dy . x) of the chunk for dD (fixed element assignment per thread)
+      for (int i = tid; i < kQ * 64; i += 512) {
+        const int t = i >> 6, pc = i & 63;
+        if (t < nv) dd_acc += to_f32(Xc[t * XS + pc]) * to_f32(Yc[t * XS + pc]);
       }
     }
+    if (!active) return;
+
+    __builtin_amdgcn_sched_barrier(0);
+    // ---- dC^T blocks this wave finishes: other parts + intra B^T (Gamma o dY X^T)^T, causal
 #pragma unroll
-    for (int m = 0; m < MP; ++m) mode_scale_advance(ms[m]);
+    for (int tb = 0; tb < 4; ++tb) {
+      if (!Ex::owns(tb, part)) continue;
+      if (Cfg::NACT > 1) Ex::gather(XCH, part, tb, dCa[tb], [&](int q) { return q * NBF + nbl; });
+#pragma unroll
+      for (int kk = 0; kk <= tb / 2; ++kk) {
+        const Frag<T> a = frag_load_rows(Bc, BS, kk * 32 + lg * 8, nb * 16);
+        const Frag<T> bb = frag_load_rows(HGT, XS, kk * 32 + lg * 8, tb * 16);
+        mma(dCa[tb], a, bb);
+      }
+      // per-head partial: token t = 16 tb + li, columns n .. n+3 (32-bit offsets from the chunk)
+      const int t = tb * 16 + li, n = nb * 16 + lg * 4;
+      if (t < nv && n < N) store4(dCp + (((int64_t)b * L + t0) * H + h) * N + t * (H * N) + n, dCa[tb]);
+    }
+
+    __builtin_amdgcn_sched_barrier(0);
+    // ---- state update S^T += X^T (v o B), rows p, column ncol
+#pragma unroll
+    for (int m = 0; m < MPF; ++m) {
+      if (!((renbits >> m) & 1)) continue;
+#pragma unroll
+      for (int pb = 0; pb < 4; ++pb)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) S[m][pb][r] *= renf[m];
+    }
+#pragma unroll
+    for (int kt = 0; kt < 2; ++kt) {
+      Frag<T> Xa[4];
+#pragma unroll
+      for (int pb = 0; pb < 4; ++pb) Xa[pb] = frag_load_rows(Xc, XS, kt * 32 + lg * 8, pb * 16);
+      const Frag<T> bf = frag_load_rows(Bc, BS, kt * 32 + lg * 8, nb * 16);
+      float b8[8];
+#pragma unroll
+      for (int s = 0; s < 8; ++s) b8[s] = to_f32(bf.v[s]);
+#pragma unroll
+      for (int m = 0; m < MPF; ++m) {
+        const float* pv = P_v + (mo + m) * kQ + kt * 32 + lg * 8;
+        const float4 v0 = *reinterpret_cast<const float4*>(pv);
+        const float4 v1 = *reinterpret_cast<const float4*>(pv + 4);
+        Frag<T> Bv;
+        frag_set(Bv, 0, b8[0] * v0.x);
+        frag_set(Bv, 1, b8[1] * v0.y);
+        frag_set(Bv, 2, b8[2] * v0.z);
+        frag_set(Bv, 3, b8[3] * v0.w);
+        frag_set(Bv, 4, b8[4] * v1.x);
+        frag_set(Bv, 5, b8[5] * v1.y);
+        frag_set(Bv, 6, b8[6] * v1.z);
+        frag_set(Bv, 7, b8[7] * v1.w);
+#pragma unroll
+        for (int pb = 0; pb < 4; ++pb) mma(S[m][pb], Xa[pb], Bv);
+      }
+    }
+  };
+
+  for (int c = 0; c < nchunks; c += 2) {
+    step(c, Xb0, Yb0, Bb0, Xb1, Yb1, Bb1);
+    if (c + 1 < nchunks) {
+      if (Cfg::NBUF == 2) step(c + 1, Xb1, Yb1, Bb1, Xb0, Yb0, Bb0);
+      else step(c + 1, Xb0, Yb0, Bb0, Xb0, Yb0, Bb0);
+    }
   }
+  wait_vmem();
+  barrier();
 
   // ---- final-state term sum_m r_m <dS_final_m, S_final_m> and sum(dy . x)
   float fpart = 0.0f;
   if (p.d_final_state && active) {
+    const float* Ef = s_E2 + (nchunks & 1) * MP;
     int lo = ncol * P + lg * 4;
     asm volatile("" : "+v"(lo));
 #pragma unroll
-    for (int m = 0; m < MP; ++m)
+    for (int m = 0; m < MPF; ++m) {
+      const float scale = (mo + m < M) ? s_rr[mo + m] * Ef[mo + m] : 0.0f;
 #pragma unroll
-      for (int pb = 0; pb < kPBM; ++pb)
+      for (int pb = 0; pb < 4; ++pb)
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int pr = pb * 16 + lg * 4 + r;
-          if (m < M && ncol < N && pr < P)
-            fpart += rr[m] * ms[m].E * S[m][pb][r] *
-                     p.d_final_state[sbase + (int64_t)m * N * P + lo + pb * 16 + r];
+          if (mo + m < M && ncol < N && pr < P)
+            fpart += scale * S[m][pb][r] * p.d_final_state[sbase + (int64_t)(mo + m) * N * P + lo + pb * 16 + r];
         }
+    }
   }
-  __syncthreads();
-  redR[tid] = fpart;
-  redC[tid] = dd_acc;
-  __syncthreads();
+  float* red = reinterpret_cast<float*>(sm + oW);  // the weights are no longer needed
+  red[tid] = fpart;
+  red[512 + tid] = dd_acc;
+  barrier();
   if (tid == 0) {
     float fs = 0.f, ds = 0.f;
-    for (int i = 0; i < (int)blockDim.x; ++i) {
-      fs += redR[i];
-      ds += redC[i];
+    for (int i = 0; i < 512; ++i) {
+      fs += red[i];
+      ds += red[512 + i];
     }
-    Fw[(int64_t)b * H + h] = fs;
-    dDp[(int64_t)b * H + h] = ds;
+    wk.F[(int64_t)ps * p.Bsz * H + (int64_t)b * H + h] = fs;
+    if (ps == 0) wk.dDp[(int64_t)b * H + h] = ds;
   }
 }
 
-// --------------------------------------------------------------------------
-// sweep 1: reverse direction, adjoint in row layout (rows n, columns p): dx, e/f adjoint parts
+// ------------------------------------------------------------- cols sweep
 
 template <typename T, int MP, int NB>
-__device__ __forceinline__ void sweep_adj_rows(const ScanParams& p, int b, int h, int g, const T* __restrict__ gtiles,
-                               float* __restrict__ eB, float* __restrict__ fB, unsigned char* smem) {
-  constexpr int NP = NB * 16;
-  constexpr int NH = NB >= 2 ? 2 : 1;
-  constexpr int NBW = NB / NH;
-  constexpr int KBW = (NBW + 1) / 2;
-  constexpr int LDN = NP + 8;
-  const int PP = p.PP, NW = PP / 16;
-  const int NWT = blockDim.x >> 6;
+__global__ void __launch_bounds__(512) frac_bwd_cols_kernel(ScanParams p, BwdWork wk) {
+  using Cfg = ColCfg<T, MP, NB>;
+  constexpr int NP = Cfg::NP, XS = Cfg::XS, CS = Cfg::BS;  // C is read transposed here
+  constexpr int NBF = Cfg::NBF, FPART = Cfg::FPART, MPF = Cfg::MPF;
+  using Ex = Exchange<Cfg::NACT>;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, li = lane & 15, lg = lane >> 4;
-  const bool active = wave < NW * NH;
-  const int pb = wave % NW, nh = active ? wave / NW : 0;
-  const int pc = pb * 16 + li;
-  const int L = p.L, H = p.H, P = p.P, N = p.N, M = p.M;
+  const int L = p.L, H = p.H, P = p.P, N = p.N, M = p.M, G = p.G;
   const int nchunks = (L + kQ - 1) / kQ;
+  int b, h, ps;
+  block_head(Cfg::PS, H, b, h, ps);
+  const int g = h * G / H;
+  const int nbl = wave % NBF, part = wave / NBF, nb = ps * NBF + nbl, ncol = nb * 16 + li;
+  const int mo = part * MPF;
+  const bool active = mo < MP;
 
-  T* Bs = reinterpret_cast<T*>(smem);  // [Q][LDN]
-  T* CT = Bs + kQ * LDN;               // [NP][LDQ]
-  T* dYT = CT + NP * LDQ;              // [64][LDQ]
-  T* XT = dYT + 64 * LDQ;              // [64][LDQ]
-  T* GGT = XT + 64 * LDQ;              // [Q][LDQ]  ((C B^T) o Gamma)^T
-  float* P_O = reinterpret_cast<float*>(GGT + kQ * LDQ);
-  float* P_Vt = P_O + MP * kQ;
-  float* P_c = P_Vt + MP * kQ;
-  float* P_k = P_c + MP * kQ;
-  float* P_wdx = P_k + MP * kQ;   // kappa e^{-r(A_Q - A)} E
-  float* P_wek = P_wdx + MP * kQ; // r kappa e^{-r(A_Q - A)} E
-  float* P_wfk = P_wek + MP * kQ; // r w rho e^{-r(A_Q - A)} E
-  float* P_om = P_wfk + MP * kQ;  // c e^{-rA} * upd
-  float* P_A = P_om + MP * kQ;
-  float* YX = P_A + kQ;           // [4 p-blocks][2][2][4][64]
-  float* redE = YX + 4 * 1024;    // [NWT][Q]
-  float* redF = redE + 8 * kQ;    // [NWT][Q]
+  __shared__ __align__(16) T Xb0[64 * XS], Yb0[64 * XS], Cb0[64 * CS];
+  __shared__ __align__(16) T Xb1[Cfg::NBUF == 2 ? 64 * XS : 8], Yb1[Cfg::NBUF == 2 ? 64 * XS : 8],
+      Cb1[Cfg::NBUF == 2 ? 64 * CS : 8];
+  constexpr int NWA = n_weight_arrays<kCols>();
+  constexpr int oHG = 0;                                         // T [t][k] Gamma o dY X^T, causal
+  constexpr int oW = oHG + 64 * XS * (int)sizeof(T);
+  constexpr int oEx = oW + (NWA * MP * kQ + kQ) * 4;
+  constexpr int oSc = oEx + Ex::kFloats * 4;
+  __shared__ __align__(16) unsigned char sm[oSc + 4 * MP * 4];
+  T* HG = reinterpret_cast<T*>(sm + oHG);
+  float* W = reinterpret_cast<float*>(sm + oW);
+  float* P_A = W + NWA * MP * kQ;
+  float* XCH = reinterpret_cast<float*>(sm + oEx);
+  float* s_rr = reinterpret_cast<float*>(sm + oSc);
+  float* s_lnt = s_rr + MP;
+  float* s_E2 = s_lnt + MP;
+  constexpr int SW = MP * kQ;  // stride of the weight arrays
+  const float* P_O = W;
+  const float* P_Vt = W + 1 * SW;
+  const float* P_c = W + 2 * SW;
+  const float* P_k = W + 3 * SW;
+  const float* P_wdb = W + 4 * SW;
+  const float* P_om = W + 5 * SW;
 
-  float rr[MP], lnt[MP];
-#pragma unroll
-  for (int m = 0; m < MP; ++m) {
-    const float tau = (m < M) ? p.tau[m] : 1.0f;
-    rr[m] = (m < M) ? 1.0f / tau : 0.0f;
-    lnt[m] = (m < M) ? logf(tau) : 0.0f;
+  if (tid < MP) {
+    const float tau = (tid < M) ? p.tau[tid] : 1.0f;
+    s_rr[tid] = (tid < M) ? 1.0f / tau : 0.0f;
+    s_lnt[tid] = (tid < M) ? logf(tau) : 0.0f;
+    s_E2[tid] = 1.0f;
   }
-  for (int i = tid; i < kQ * LDQ; i += blockDim.x) GGT[i] = (T)0.0f;
+  for (int i = tid; i < 64 * XS; i += 512) {
+    HG[i] = (T)0.0f;
+    Xb0[i] = Yb0[i] = (T)0.0f;
+    Xb1[Cfg::NBUF == 2 ? i : 0] = Yb1[Cfg::NBUF == 2 ? i : 0] = (T)0.0f;
+  }
+  for (int i = tid; i < 64 * CS; i += 512) Cb0[i] = Cb1[Cfg::NBUF == 2 ? i : 0] = (T)0.0f;
 
+  // ---- adjoint G^T: Gs[m][pb] holds mode mo + m, rows p = 16 pb + 4 lg + r, column ncol
   const int64_t sbase = ((int64_t)b * H + h) * (int64_t)M * N * P;
-  floatx4 Gs[MP][NBW];
-  ModeScale ms[MP];
+  floatx4 Gs[MPF][4];
   {
-    int lo = (nh * NBW * 16 + lg * 4) * P + pc;
+    int lo = ncol * P + lg * 4;
     asm volatile("" : "+v"(lo));
 #pragma unroll
-    for (int m = 0; m < MP; ++m) {
-      ms[m].E = 1.0f;
+    for (int m = 0; m < MPF; ++m)
+#pragma unroll
+      for (int pb = 0; pb < 4; ++pb)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int pr = pb * 16 + lg * 4 + r;
+          float v = 0.0f;
+          if (p.d_final_state && active && mo + m < M && ncol < N && pr < P)
+            v = p.d_final_state[sbase + (int64_t)(mo + m) * N * P + lo + pb * 16 + r];
+          Gs[m][pb][r] = v;
+        }
+  }
+
+  const T* xg = reinterpret_cast<const T*>(p.x) + (((int64_t)b * L) * H + h) * P;
+  const T* yg = reinterpret_cast<const T*>(p.dy) + (((int64_t)b * L) * H + h) * P;
+  const T* Cgp = reinterpret_cast<const T*>(p.Cm) + (((int64_t)b * L) * G + g) * N;
+  const int64_t xstride = (int64_t)H * P, bstride = (int64_t)G * N;
+  const float* dt_bh = p.dt + (int64_t)b * L * H + h;
+  const float* al_bh = p.alpha + b * p.as0 + h * p.as2;
+  const float* lm_bh = p.lambda ? p.lambda + b * p.ls0 + h * p.ls2 : nullptr;
+  const float* rl_bh = p.read_logit ? p.read_logit + ((int64_t)b * L * H + h) * M : nullptr;
+  const float* wl_bh = p.write_logit ? p.write_logit + ((int64_t)b * L * H + h) * M : nullptr;
+  const int64_t lg_st = (int64_t)H * M;
+  auto load_controls = [&](int c, float& dtv, float& al, float& lam) {
+    const int tg = c * kQ + lane;
+    const bool valid = tg < L;
+    dtv = valid ? dt_bh[(int64_t)tg * H] : 0.0f;
+    al = valid ? al_bh[tg * p.as1] : 1.0f;
+    lam = (valid && lm_bh) ? lm_bh[tg * p.ls1] : 1.0f;
+  };
+  DmaPlan<T, XS> planX;
+  DmaPlan<T, CS> planC;
+  planX.init(xstride, P);
+  planC.init(bstride, N);
+  auto stage = [&](int c, T* Xd, T* Yd, T* Cd) {
+    const int t0 = c * kQ, nv = min(kQ, L - t0);
+    planX.template issue<Cfg::NBUF == 1>(Xd, xg + (int64_t)t0 * xstride, xstride, nv);
+    planX.template issue<Cfg::NBUF == 1>(Yd, yg + (int64_t)t0 * xstride, xstride, nv);
+    planC.template issue<Cfg::NBUF == 1>(Cd, Cgp + (int64_t)t0 * bstride, bstride, nv);
+  };
+
+  float dt_n, al_n, lam_n;
+  load_controls(nchunks - 1, dt_n, al_n, lam_n);
+  if (Cfg::NBUF == 2) stage(nchunks - 1, Xb0, Yb0, Cb0);
+  T* dBp = reinterpret_cast<T*>(wk.dBp);
+
+  // chunks in reverse order; i counts processed chunks (buffer parity)
+  auto step = [&](int c, int i, T* Xc, T* Yc, T* Cc, T* Xn, T* Yn, T* Cn) __attribute__((always_inline)) {
+    const int t0 = c * kQ, nv = min(kQ, L - t0);
+    const float* Ecur = s_E2 + (i & 1) * MP;
+    float* Enext = s_E2 + ((i + 1) & 1) * MP;
+    wait_vmem();
+    barrier();
+    if (Cfg::NBUF == 2) {
+      if (c > 0) stage(c - 1, Xn, Yn, Cn);
+    } else {
+      stage(c, Xc, Yc, Cc);
+      wait_vmem();
+      barrier();
+    }
+    const float dtv = dt_n, al_l = al_n, lam_l = lam_n;
+    if (c > 0) load_controls(c - 1, dt_n, al_n, lam_n);
+    const ChunkCtl k = chunk_controls(dtv, al_l, lam_l, lm_bh != nullptr, nv);
+    if (wave == 0) P_A[lane] = k.A;
+    const int unsafe = pair_weights<MP, kCols>(k, t0, nv, M, rl_bh, wl_bh, lg_st, s_rr, s_lnt, Ecur, Enext, W);
+    float renf[MPF];
+    int renbits = 0;
+#pragma unroll
+    for (int m = 0; m < MPF; ++m) {
+      const float Enew = uniform(Ecur[mo + m] * fexp(-s_rr[mo + m] * k.Alast));
+      renf[m] = Enew;
+      if (__float_as_int(Enew) < __float_as_int(kRescaleFloor)) renbits |= 1 << m;
+    }
+    barrier();  // weights in LDS
+
+    __builtin_amdgcn_sched_barrier(0);
+    // ---- HG = Gamma o dY X^T (natural [t][k], causal)
+    for (int tile = wave; tile < kTiles; tile += 8) {
+      const int tb = kTB[tile], kb = kKB[tile];
+      const floatx4 D = dyx_tile<T, XS>(Yc, Xc, tb, kb);
+      floatx4 Gm = rank_m_tile<MP>(P_O, P_Vt, tb * 16, kb * 16);
+      if (unsafe) unsafe_terms<MP>(Gm, unsafe, P_c, P_k, P_A, s_rr, tb, kb, false);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int t = tb * 16 + lg * 4 + r, kk = kb * 16 + li;
+        HG[t * XS + kk] = (T)((t >= kk) ? Gm[r] * D[r] : 0.0f);
+      }
+    }
+
+    __builtin_amdgcn_sched_barrier(0);
+    // ---- V^T_m = G_m X^T (rows n of this wave's block, columns k) -> dB^T (inter)
+    floatx4 dBa[4];  // dB^T: rows n = 16 nb + 4 lg + r, column k = 16 tb + li
+#pragma unroll
+    for (int tb = 0; tb < 4; ++tb) dBa[tb] = floatx4{0.f, 0.f, 0.f, 0.f};
+    if (active) {
+      Frag<T> Ga[MPF][2];
+#pragma unroll
+      for (int m = 0; m < MPF; ++m)
+#pragma unroll
+        for (int kp = 0; kp < 2; ++kp) {
+#pragma unroll
+          for (int s = 0; s < 4; ++s) frag_set(Ga[m][kp], s, Gs[m][2 * kp][s]);
+#pragma unroll
+          for (int s = 0; s < 4; ++s) frag_set(Ga[m][kp], 4 + s, Gs[m][2 * kp + 1][s]);
+        }
+#pragma unroll
+      for (int tb = 0; tb < 4; ++tb) {
+        const T* row = Xc + (tb * 16 + li) * XS + lg * 4;
+        const Frag<T> x0 = frag_load4x2(row, row + 16), x1 = frag_load4x2(row + 32, row + 48);
+#pragma unroll
+        for (int m = 0; m < MPF; ++m) {
+          floatx4 V = {0.f, 0.f, 0.f, 0.f};
+          mma(V, Ga[m][0], x0);
+          mma(V, Ga[m][1], x1);
+          const float wb = P_wdb[(mo + m) * kQ + tb * 16 + li];
+#pragma unroll
+          for (int r = 0; r < 4; ++r) dBa[tb][r] += wb * V[r];
+        }
+      }
+      if (Cfg::NACT > 1) Ex::put(XCH, wave, part, dBa);
+    }
+    barrier();  // HG and exchange complete
+    if (!active) return;
+
+    __builtin_amdgcn_sched_barrier(0);
+    // ---- dB^T blocks this wave finishes: other parts + intra C^T (Gamma o dY X^T), t >= k
+#pragma unroll
+    for (int tb = 0; tb < 4; ++tb) {
+      if (!Ex::owns(tb, part)) continue;
+      if (Cfg::NACT > 1) Ex::gather(XCH, part, tb, dBa[tb], [&](int q) { return q * NBF + nbl; });
+#pragma unroll
+      for (int kk = tb / 2; kk < 2; ++kk) {
+        const Frag<T> a = frag_load_rows(Cc, CS, kk * 32 + lg * 8, nb * 16);
+        const Frag<T> bb = frag_load_rows(HG, XS, kk * 32 + lg * 8, tb * 16);
+        mma(dBa[tb], a, bb);
+      }
+      const int k = tb * 16 + li, n = nb * 16 + lg * 4;
+      if (k < nv && n < N) store4(dBp + (((int64_t)b * L + t0) * H + h) * N + k * (H * N) + n, dBa[tb]);
+    }
+
+    __builtin_amdgcn_sched_barrier(0);
+    // ---- adjoint update G^T += dY^T (omega o C), rows p, column ncol
+#pragma unroll
+    for (int m = 0; m < MPF; ++m) {
+      if (!((renbits >> m) & 1)) continue;
+#pragma unroll
+      for (int pb = 0; pb < 4; ++pb)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) Gs[m][pb][r] *= renf[m];
+    }
+#pragma unroll
+    for (int kt = 0; kt < 2; ++kt) {
+      Frag<T> Ya[4];
+#pragma unroll
+      for (int pb = 0; pb < 4; ++pb) Ya[pb] = frag_load_rows(Yc, XS, kt * 32 + lg * 8, pb * 16);
+      const Frag<T> cf = frag_load_rows(Cc, CS, kt * 32 + lg * 8, nb * 16);
+      float c8[8];
+#pragma unroll
+      for (int s = 0; s < 8; ++s) c8[s] = to_f32(cf.v[s]);
+#pragma unroll
+      for (int m = 0; m < MPF; ++m) {
+        const float* pv = P_om + (mo + m) * kQ + kt * 32 + lg * 8;
+        const float4 v0 = *reinterpret_cast<const float4*>(pv);
+        const float4 v1 = *reinterpret_cast<const float4*>(pv + 4);
+        Frag<T> Cv;
+        frag_set(Cv, 0, c8[0] * v0.x);
+        frag_set(Cv, 1, c8[1] * v0.y);
+        frag_set(Cv, 2, c8[2] * v0.z);
+        frag_set(Cv, 3, c8[3] * v0.w);
+        frag_set(Cv, 4, c8[4] * v1.x);
+        frag_set(Cv, 5, c8[5] * v1.y);
+        frag_set(Cv, 6, c8[6] * v1.z);
+        frag_set(Cv, 7, c8[7] * v1.w);
+#pragma unroll
+        for (int pb = 0; pb < 4; ++pb) mma(Gs[m][pb], Ya[pb], Cv);
+      }
+    }
+  };
+
+  for (int i = 0; i < nchunks; i += 2) {
+    const int c = nchunks - 1 - i;
+    step(c, i, Xb0, Yb0, Cb0, Xb1, Yb1, Cb1);
+    if (c > 0) {
+      if (Cfg::NBUF == 2) step(c - 1, i + 1, Xb1, Yb1, Cb1, Xb0, Yb0, Cb0);
+      else step(c - 1, i + 1, Xb0, Yb0, Cb0, Xb0, Yb0, Cb0);
+    }
+  }
+}
+
+// ------------------------------------------------------------- rows sweep
+
+// Row layout (lane = column p), as in the forward: with 8 modes the columns of P
+// are split over two workgroups; the 8 waves are NPW blocks of 16 columns times
+// NPART parts splitting the modes (or N, with one mode).
+template <typename T, int MP, int NB>
+struct RowCfg {
+  static constexpr int NP = NB * 16;
+  static constexpr bool kBf16 = sizeof(T) == 2;
+  static constexpr int XS = Pad<T>::XS;
+  static constexpr int BS = Pad<T>::template CS<NP>;  // B read along rows (readout A operand)
+  static constexpr int CS = Pad<T>::template BS<NP>;  // C read transposed (update A operand)
+  static constexpr int NBUF = kBf16 ? 2 : 1;
+  // (float32 tiles take twice the LDS: no P split there, the exchange would not fit)
+  static constexpr int PS = (MP >= 8 && kBf16) ? 2 : 1;
+  static constexpr int NPW = 4 / PS;
+  static constexpr bool kModeSplit = MP >= 2;
+  static constexpr int NPART = kModeSplit ? 8 / NPW : (NB >= 2 ? 2 : 1);
+  static constexpr int MPW = kModeSplit ? MP / NPART : MP;
+  static constexpr int NBW = (!kModeSplit && NB >= 2) ? NB / 2 : NB;
+  static constexpr int KBW = (NBW + 1) / 2;
+  static constexpr int TBP = (kBf16 ? MPW * NBW < 16 : MPW * NBW < 8) ? 4 : (kBf16 || MPW * NBW < 16) ? 2 : 1;
+};
+
+template <typename T, int MP, int NB>
+__global__ void __launch_bounds__(512) frac_bwd_rows_kernel(ScanParams p, BwdWork wk) {
+  using Cfg = RowCfg<T, MP, NB>;
+  constexpr int NP = Cfg::NP, XS = Cfg::XS, BS = Cfg::BS, CS = Cfg::CS;
+  constexpr int NPART = Cfg::NPART, MPW = Cfg::MPW, NBW = Cfg::NBW, KBW = Cfg::KBW, TBP = Cfg::TBP;
+  using Ex = Exchange<NPART>;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, li = lane & 15, lg = lane >> 4;
+  const int L = p.L, H = p.H, P = p.P, N = p.N, M = p.M, G = p.G;
+  const int nchunks = (L + kQ - 1) / kQ;
+  int b, h, ps;
+  block_head(Cfg::PS, H, b, h, ps);
+  const int g = h * G / H;
+  const int pbl = wave % Cfg::NPW, part = wave / Cfg::NPW;
+  const int pb = ps * Cfg::NPW + pbl;
+  const bool active = pb * 16 < p.PP && part < NPART;
+  const int mo = Cfg::kModeSplit ? part * MPW : 0;
+  const int nbo = (!Cfg::kModeSplit && NPART == 2) ? part * NBW : 0;
+  const int pc = pb * 16 + li;
+
+  // B and x are needed early in a chunk only: single buffers refilled mid-chunk
+  __shared__ __align__(16) T Bb[64 * BS], Xb[64 * XS];
+  __shared__ __align__(16) T Cb0[64 * CS], Yb0[64 * XS];
+  __shared__ __align__(16) T Cb1[Cfg::NBUF == 2 ? 64 * CS : 8], Yb1[Cfg::NBUF == 2 ? 64 * XS : 8];
+  constexpr int NWA = n_weight_arrays<kRows>();
+  constexpr int oGG = 0;                                         // T [t'][k] (C B^T) o Gamma, causal
+  constexpr int oDx = oGG + 64 * XS * (int)sizeof(T);            // T [t][p] dx rows of the previous chunk (bf16)
+  constexpr int oW = oDx + (Cfg::kBf16 ? 64 * XS * (int)sizeof(T) : 0);
+  constexpr int oRd = oW + (NWA * MP * kQ + kQ) * 4;             // float [2][8][Q] token partials of e, f
+  constexpr int oEx = oRd + 2 * 8 * kQ * 4;
+  constexpr int oSc = oEx + Ex::kFloats * 4;
+  __shared__ __align__(16) unsigned char sm[oSc + 4 * MP * 4];
+  T* GG = reinterpret_cast<T*>(sm + oGG);
+  T* Dxb = reinterpret_cast<T*>(sm + oDx);
+  float* W = reinterpret_cast<float*>(sm + oW);
+  float* P_A = W + NWA * MP * kQ;
+  float* redE = reinterpret_cast<float*>(sm + oRd);
+  float* redF = redE + 8 * kQ;
+  float* XCH = reinterpret_cast<float*>(sm + oEx);
+  float* s_rr = reinterpret_cast<float*>(sm + oSc);
+  float* s_lnt = s_rr + MP;
+  float* s_E2 = s_lnt + MP;
+  constexpr int SW = MP * kQ;  // stride of the weight arrays
+  const float* P_O = W;
+  const float* P_Vt = W + 1 * SW;
+  const float* P_c = W + 2 * SW;
+  const float* P_k = W + 3 * SW;
+  const float* P_wdx = W + 4 * SW;  // times r_m: the adjoint weight of e
+  const float* P_wfk = W + 5 * SW;
+  const float* P_om = W + 6 * SW;
+
+  if (tid < MP) {
+    const float tau = (tid < M) ? p.tau[tid] : 1.0f;
+    s_rr[tid] = (tid < M) ? 1.0f / tau : 0.0f;
+    s_lnt[tid] = (tid < M) ? logf(tau) : 0.0f;
+    s_E2[tid] = 1.0f;
+  }
+  for (int i = tid; i < 64 * XS; i += 512) {
+    GG[i] = (T)0.0f;
+    Xb[i] = Yb0[i] = (T)0.0f;
+    Yb1[Cfg::NBUF == 2 ? i : 0] = (T)0.0f;
+  }
+  for (int i = tid; i < 64 * BS; i += 512) Bb[i] = (T)0.0f;
+  for (int i = tid; i < 64 * CS; i += 512) Cb0[i] = Cb1[Cfg::NBUF == 2 ? i : 0] = (T)0.0f;
+
+  // ---- adjoint G: Gs[m][jb] holds mode mo + m, rows n = 16 (nbo + jb) + 4 lg + r, column pc
+  const int64_t sbase = ((int64_t)b * H + h) * (int64_t)M * N * P;
+  floatx4 Gs[MPW][NBW];
+  {
+    int lo = (mo * N + nbo * 16 + lg * 4) * P + pc;
+    asm volatile("" : "+v"(lo));
+#pragma unroll
+    for (int m = 0; m < MPW; ++m)
 #pragma unroll
       for (int jb = 0; jb < NBW; ++jb)
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          const int n = (nh * NBW + jb) * 16 + lg * 4 + r;
+          const int n = (nbo + jb) * 16 + lg * 4 + r;
           float v = 0.0f;
-          if (p.d_final_state && active && m < M && n < N && pc < P)
+          if (p.d_final_state && active && mo + m < M && n < N && pc < P)
             v = p.d_final_state[sbase + lo + ((int64_t)m * N + jb * 16 + r) * P];
           Gs[m][jb][r] = v;
         }
-    }
   }
   const float Dh = p.D ? p.D[h] : 0.0f;
 
-  for (int c = nchunks - 1; c >= 0; --c) {
+  const T* xg = reinterpret_cast<const T*>(p.x) + (((int64_t)b * L) * H + h) * P;
+  const T* yg = reinterpret_cast<const T*>(p.dy) + (((int64_t)b * L) * H + h) * P;
+  T* dxg = reinterpret_cast<T*>(p.dx) + (((int64_t)b * L) * H + h) * P;
+  const T* Bgp = reinterpret_cast<const T*>(p.Bm) + (((int64_t)b * L) * G + g) * N;
+  const T* Cgp = reinterpret_cast<const T*>(p.Cm) + (((int64_t)b * L) * G + g) * N;
+  const int64_t xstride = (int64_t)H * P, bstride = (int64_t)G * N;
+  const float* dt_bh = p.dt + (int64_t)b * L * H + h;
+  const float* al_bh = p.alpha + b * p.as0 + h * p.as2;
+  const float* lm_bh = p.lambda ? p.lambda + b * p.ls0 + h * p.ls2 : nullptr;
+  const float* rl_bh = p.read_logit ? p.read_logit + ((int64_t)b * L * H + h) * M : nullptr;
+  const float* wl_bh = p.write_logit ? p.write_logit + ((int64_t)b * L * H + h) * M : nullptr;
+  const int64_t lg_st = (int64_t)H * M;
+  auto load_controls = [&](int c, float& dtv, float& al, float& lam) {
+    const int tg = c * kQ + lane;
+    const bool valid = tg < L;
+    dtv = valid ? dt_bh[(int64_t)tg * H] : 0.0f;
+    al = valid ? al_bh[tg * p.as1] : 1.0f;
+    lam = (valid && lm_bh) ? lm_bh[tg * p.ls1] : 1.0f;
+  };
+  DmaPlan<T, XS> planX;
+  DmaPlan<T, BS> planB;
+  DmaPlan<T, CS> planC;
+  planX.init(xstride, P);
+  planB.init(bstride, N);
+  planC.init(bstride, N);
+  auto stage_late = [&](int c, T* Cd, T* Yd) {  // used through the whole chunk
     const int t0 = c * kQ, nv = min(kQ, L - t0);
-    __syncthreads();
-    const int64_t xrow0 = (((int64_t)b * L + t0) * H + h) * P;
-    const int64_t brow0 = (((int64_t)b * L + t0) * p.G + g) * N;
-    stage<T>(reinterpret_cast<const T*>(p.Bm) + brow0, (int64_t)p.G * N, N, NP, nv, Bs, LDN, nullptr);
-    stage<T>(reinterpret_cast<const T*>(p.Cm) + brow0, (int64_t)p.G * N, N, NP, nv, nullptr, 0, CT);
-    stage<T>(reinterpret_cast<const T*>(p.dy) + xrow0, (int64_t)H * P, P, PP, nv, nullptr, 0, dYT);
-    stage<T>(reinterpret_cast<const T*>(p.x) + xrow0, (int64_t)H * P, P, PP, nv, nullptr, 0, XT);
-    {
-      const int t = lane;
-      const bool valid = t < nv;
-      float dtt, s_eff, cw[MP], ww[MP];
-      token_controls<MP>(p, b, h, t0 + t, valid, lnt, dtt, s_eff, cw, ww);
-      const float A = wave_inclusive_sum(dtt);
-      const float Alast = uniform(__shfl(A, 63, 64));
-      if (wave == 0) P_A[t] = A;
+    planC.template issue<Cfg::NBUF == 1>(Cd, Cgp + (int64_t)t0 * bstride, bstride, nv);
+    planX.template issue<Cfg::NBUF == 1>(Yd, yg + (int64_t)t0 * xstride, xstride, nv);
+  };
+  auto stage_early = [&](int c) {  // read before the mid-chunk barrier only
+    const int t0 = c * kQ, nv = min(kQ, L - t0);
+    planB.template issue<Cfg::NBUF == 1>(Bb, Bgp + (int64_t)t0 * bstride, bstride, nv);
+    planX.template issue<Cfg::NBUF == 1>(Xb, xg + (int64_t)t0 * xstride, xstride, nv);
+  };
+  // dx rows of chunk c (staged in Dxb) -> global, this workgroup's columns
+  auto store_dx = [&](int c) {
+    constexpr int E8 = 16 / sizeof(T);
+    constexpr int CY = 64 / E8;
+    const int t0 = c * kQ, nv = min(kQ, L - t0);
 #pragma unroll
-      for (int m = 0; m < MP; ++m) {
-        mode_scale(ms[m], rr[m], Alast);
-        if ((m % NWT) != wave) continue;
-        const float rho = expf(-dtt * rr[m]);
-        const float kap = -expm1f(-dtt * rr[m]) * ww[m];
-        const float ea = expf(-rr[m] * A);
-        const float dec = expf(-rr[m] * (Alast - A)) * ms[m].E;
-        P_O[m * kQ + t] = cw[m] * ea;
-        P_Vt[m * kQ + t] = ms[m].safe ? kap * expf(rr[m] * A) : 0.0f;
-        P_c[m * kQ + t] = cw[m];
-        P_k[m * kQ + t] = kap;
-        P_wdx[m * kQ + t] = kap * dec;
-        P_wek[m * kQ + t] = rr[m] * kap * dec;
-        P_wfk[m * kQ + t] = rr[m] * ww[m] * rho * dec;
-        P_om[m * kQ + t] = cw[m] * ea * ms[m].upd;
+    for (int i0 = 0; i0 < 64 * CY; i0 += 512) {
+      const int i = i0 + tid, t = i / CY, ch = i & (CY - 1);
+      const int col = ch * E8;
+      if (t < nv && col < P && col >= ps * Cfg::NPW * 16 && col < (ps + 1) * Cfg::NPW * 16)
+        *reinterpret_cast<int4*>(dxg + (int64_t)(t0 + t) * xstride + col) =
+            *reinterpret_cast<const int4*>(Dxb + t * XS + col);
+    }
+  };
+
+  float dt_n, al_n, lam_n;
+  load_controls(nchunks - 1, dt_n, al_n, lam_n);
+  if (Cfg::NBUF == 2) {
+    stage_late(nchunks - 1, Cb0, Yb0);
+    stage_early(nchunks - 1);
+  }
+  const T* gtiles = reinterpret_cast<const T*>(wk.tiles);
+  const int64_t bl_h = (int64_t)p.Bsz * L * H;
+
+  auto step = [&](int c, int i, T* Cc, T* Yc, T* Cn, T* Yn) __attribute__((always_inline)) {
+    const int t0 = c * kQ, nv = min(kQ, L - t0);
+    const float* Ecur = s_E2 + (i & 1) * MP;
+    float* Enext = s_E2 + ((i + 1) & 1) * MP;
+    wait_vmem();
+    barrier();
+    if (Cfg::kBf16 && i > 0) store_dx(c + 1);
+    if (Cfg::NBUF == 2) {
+      if (c > 0) stage_late(c - 1, Cn, Yn);
+    } else {
+      stage_late(c, Cc, Yc);
+      stage_early(c);
+      wait_vmem();
+      barrier();
+    }
+    const float dtv = dt_n, al_l = al_n, lam_l = lam_n;
+    if (c > 0) load_controls(c - 1, dt_n, al_n, lam_n);
+    const ChunkCtl k = chunk_controls(dtv, al_l, lam_l, lm_bh != nullptr, nv);
+    if (wave == 0) P_A[lane] = k.A;
+    const int unsafe = pair_weights<MP, kRows>(k, t0, nv, M, rl_bh, wl_bh, lg_st, s_rr, s_lnt, Ecur, Enext, W);
+    float renf[MPW];
+    int renbits = 0;
+#pragma unroll
+    for (int m = 0; m < MPW; ++m) {
+      const float Enew = uniform(Ecur[mo + m] * fexp(-s_rr[mo + m] * k.Alast));
+      renf[m] = Enew;
+      if (__float_as_int(Enew) < __float_as_int(kRescaleFloor)) renbits |= 1 << m;
+    }
+    barrier();  // weights in LDS
+
+    __builtin_amdgcn_sched_barrier(0);
+    // ---- GG = (C B^T) o Gamma, natural [t'][k], causal
+    {
+      const T* gt = gtiles + (((int64_t)b * nchunks + c) * G + g) * (kTiles * kTileElems);
+      for (int tile = wave; tile < kTiles; tile += 8) {
+        const int tb = kTB[tile], kb = kKB[tile];
+        floatx4 Gm = rank_m_tile<MP>(P_O, P_Vt, tb * 16, kb * 16);
+        if (unsafe) unsafe_terms<MP>(Gm, unsafe, P_c, P_k, P_A, s_rr, tb, kb, false);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int t = tb * 16 + lg * 4 + r, kk = kb * 16 + li;
+          GG[t * XS + kk] = (T)((t >= kk) ? to_f32(gt[tile * kTileElems + lane * 4 + r]) * Gm[r] : 0.0f);
+        }
       }
     }
-    __syncthreads();
 
-    // ---- adjoint-side terms: W_m = B G_m  ->  dx (inter), e / f (inter)
-    floatx4 dxa[4];
-    float ekf[16], fkf[16];
+    __builtin_amdgcn_sched_barrier(0);
+    // ---- Z^T_m = G_m^T B^T (rows p of this wave's block, columns t) -> dx^T (inter)
+    // and the adjoint parts of e, f
+    floatx4 dxa[4];  // dx^T: rows p = 16 pb + 4 lg + r, column t = 16 tb + li
 #pragma unroll
     for (int tb = 0; tb < 4; ++tb) dxa[tb] = floatx4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int j = 0; j < 16; ++j) ekf[j] = fkf[j] = 0.0f;
-    if (active) {
-      Frag<T> Bf[4][KBW];
-#pragma unroll
-      for (int tb = 0; tb < 4; ++tb)
-#pragma unroll
-        for (int kb = 0; kb < KBW; ++kb) {
-          const int n0 = nh * NBW * 16 + kb * 32;
-          const T* row = Bs + (tb * 16 + li) * LDN + n0 + lg * 4;
-          Bf[tb][kb] = frag_load4x2(row, (2 * kb + 1 < NBW) ? row + 16 : nullptr);
-        }
-#pragma unroll
-      for (int m = 0; m < MP; ++m) {
-        if (m >= M) continue;
-        Frag<T> Gf[KBW];
-#pragma unroll
-        for (int kb = 0; kb < KBW; ++kb) {
-#pragma unroll
-          for (int s = 0; s < 4; ++s) frag_set(Gf[kb], s, Gs[m][2 * kb][s]);
-#pragma unroll
-          for (int s = 0; s < 4; ++s) frag_set(Gf[kb], 4 + s, (2 * kb + 1 < NBW) ? Gs[m][2 * kb + 1][s] : 0.0f);
-        }
-#pragma unroll
-        for (int tb = 0; tb < 4; ++tb) {
-          floatx4 W = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-          for (int kb = 0; kb < KBW; ++kb) mma(W, Bf[tb][kb], Gf[kb]);
-          const float4 wx = *reinterpret_cast<const float4*>(P_wdx + m * kQ + tb * 16 + lg * 4);
-          const float4 we = *reinterpret_cast<const float4*>(P_wek + m * kQ + tb * 16 + lg * 4);
-          const float4 wf = *reinterpret_cast<const float4*>(P_wfk + m * kQ + tb * 16 + lg * 4);
-          dxa[tb][0] += wx.x * W[0];
-          dxa[tb][1] += wx.y * W[1];
-          dxa[tb][2] += wx.z * W[2];
-          dxa[tb][3] += wx.w * W[3];
-          ekf[tb * 4 + 0] += we.x * W[0];
-          ekf[tb * 4 + 1] += we.y * W[1];
-          ekf[tb * 4 + 2] += we.z * W[2];
-          ekf[tb * 4 + 3] += we.w * W[3];
-          fkf[tb * 4 + 0] += wf.x * W[0];
-          fkf[tb * 4 + 1] += wf.y * W[1];
-          fkf[tb * 4 + 2] += wf.z * W[2];
-          fkf[tb * 4 + 3] += wf.w * W[3];
-        }
-        __builtin_amdgcn_sched_barrier(0);
-      }
-#pragma unroll
-      for (int tb = 0; tb < 4; ++tb)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const float xv = to_f32(XT[pc * LDQ + tb * 16 + lg * 4 + r]);
-          ekf[tb * 4 + r] *= xv;
-          fkf[tb * 4 + r] *= xv;
-        }
-      if (NH > 1) {
-        float* dst = YX + ((pb * 2 + nh) * 2) * 4 * 64;
-#pragma unroll
-        for (int jj = 0; jj < 2; ++jj) {
-          const int tb = (1 - nh) * 2 + jj;
-#pragma unroll
-          for (int r = 0; r < 4; ++r) dst[(jj * 4 + r) * 64 + lane] = dxa[tb][r];
-        }
-      }
-    }
     {
-      const float ve = transpose_reduce16(ekf, li);
-      const float vf = transpose_reduce16(fkf, li);
-      redE[wave * kQ + tok_of(li, lg)] = ve;
-      redF[wave * kQ + tok_of(li, lg)] = vf;
-    }
-    // ---- ((C B^T) o Gamma)^T tiles
-    {
-      const T* gt = gtiles + (((int64_t)b * nchunks + c) * p.G + g) * (kTiles * kTileElems);
-      for (int tile = wave; tile < kTiles; tile += NWT) {
-        const int tb = kTB[tile], kb = kKB[tile];
-        float Gt[4];
-        load_gtile(gt, tile, lane, Gt);
-        floatx4 Gm = rank_m_tile<MP>(P_O, P_Vt, tb * 16, kb * 16, li, lg);
+      float ekf[4] = {0.f, 0.f, 0.f, 0.f}, fkf[4] = {0.f, 0.f, 0.f, 0.f};  // this lane's token, per row block
+      if (active) {
 #pragma unroll
-        for (int m = 0; m < MP; ++m) {
-          if (ms[m].safe || m >= M) continue;
+        for (int tp = 0; tp < 4 / TBP; ++tp) {
+          Frag<T> Ba[TBP][KBW];
 #pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const int t = tb * 16 + lg * 4 + r, k = kb * 16 + li;
-            if (t >= k) Gm[r] += P_c[m * kQ + t] * P_k[m * kQ + k] * expf(-rr[m] * (P_A[t] - P_A[k]));
+          for (int q = 0; q < TBP; ++q)
+#pragma unroll
+            for (int kb = 0; kb < KBW; ++kb) {
+              const T* row = Bb + ((tp * TBP + q) * 16 + li) * BS + nbo * 16 + kb * 32 + lg * 4;
+              Ba[q][kb] = frag_load4x2(row, row + 16, 2 * kb + 1 < NBW);
+            }
+          floatx4 We[TBP], Wf[TBP];
+#pragma unroll
+          for (int q = 0; q < TBP; ++q) We[q] = Wf[q] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+          for (int m = 0; m < MPW; ++m) {
+            Frag<T> Gf[KBW];
+#pragma unroll
+            for (int kb = 0; kb < KBW; ++kb) {
+#pragma unroll
+              for (int s = 0; s < 4; ++s) frag_set(Gf[kb], s, Gs[m][2 * kb][s]);
+#pragma unroll
+              for (int s = 0; s < 4; ++s) frag_set(Gf[kb], 4 + s, (2 * kb + 1 < NBW) ? Gs[m][2 * kb + 1][s] : 0.0f);
+            }
+            const float rm = s_rr[mo + m];
+#pragma unroll
+            for (int q = 0; q < TBP; ++q) {
+              const int tb = tp * TBP + q;
+              floatx4 Z = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+              for (int kb = 0; kb < KBW; ++kb) mma(Z, Gf[kb], Ba[q][kb]);
+              const int o = (mo + m) * kQ + tb * 16 + li;
+              const float wx = P_wdx[o], wf = P_wfk[o];
+#pragma unroll
+              for (int r = 0; r < 4; ++r) {
+                const float v = wx * Z[r];
+                dxa[tb][r] += v;
+                We[q][r] += rm * v;
+                Wf[q][r] += wf * Z[r];
+              }
+            }
+          }
+#pragma unroll
+          for (int q = 0; q < TBP; ++q) {
+            const int tb = tp * TBP + q;
+            float xv[4];
+            load4(Xb + (tb * 16 + li) * XS + pb * 16 + lg * 4, xv);
+            ekf[tb] = We[q][0] * xv[0] + We[q][1] * xv[1] + We[q][2] * xv[2] + We[q][3] * xv[3];
+            fkf[tb] = Wf[q][0] * xv[0] + Wf[q][1] * xv[1] + Wf[q][2] * xv[2] + Wf[q][3] * xv[3];
           }
         }
+        if (NPART > 1) Ex::put(XCH, wave, part, dxa);
+      }
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int t = tb * 16 + lg * 4 + r, k = kb * 16 + li;
-          GGT[k * LDQ + t] = (T)((t >= k) ? Gt[r] * Gm[r] : 0.0f);
+      for (int tb = 0; tb < 4; ++tb) {
+        float e = ekf[tb], f = fkf[tb];
+        e += __shfl_xor(e, 16, 64);
+        e += __shfl_xor(e, 32, 64);
+        f += __shfl_xor(f, 16, 64);
+        f += __shfl_xor(f, 32, 64);
+        if (lg == 0) {
+          redE[wave * kQ + tb * 16 + li] = e;
+          redF[wave * kQ + tb * 16 + li] = f;
         }
       }
     }
-
-    __syncthreads();  // GGT, YX and the partials are complete
+    barrier();  // GG, exchange and token partials complete; B and x are free
+    if (Cfg::NBUF == 2 && c > 0) stage_early(c - 1);
 
     if (wave == 0) {
       const int t = lane;
       float e = 0.f, f = 0.f;
-      for (int w2 = 0; w2 < NWT; ++w2) {
+      for (int w2 = 0; w2 < 8; ++w2) {
         e += redE[w2 * kQ + t];
         f += redF[w2 * kQ + t];
       }
       if (t < nv) {
         const int64_t ith = ((int64_t)b * L + t0 + t) * H + h;
-        eB[ith] = e;
-        fB[ith] = f;
+        wk.eB[ps * bl_h + ith] = e;
+        wk.fB[ps * bl_h + ith] = f;
       }
     }
+    if (!active) return;
 
-    if (active) {
-      // ---- dx rows finished by this wave: other half + intra ((C B^T) o Gamma)^T dY + D dy
-      T* dx = reinterpret_cast<T*>(p.dx);
+    __builtin_amdgcn_sched_barrier(0);
+    // ---- dx^T blocks this wave finishes: other parts + intra dY^T GG (t' >= t) + D dy
 #pragma unroll
-      for (int tb = 0; tb < 4; ++tb) {
-        if (NH > 1 && (tb >> 1) != nh) continue;
-        if (NH > 1) {
-          const float* src = YX + ((pb * 2 + (1 - nh)) * 2) * 4 * 64;
+    for (int tb = 0; tb < 4; ++tb) {
+      if (!Ex::owns(tb, part)) continue;
+      if (NPART > 1) Ex::gather(XCH, part, tb, dxa[tb], [&](int q) { return q * Cfg::NPW + pbl; });
 #pragma unroll
-          for (int r = 0; r < 4; ++r) dxa[tb][r] += src[((tb & 1) * 4 + r) * 64 + lane];
-        }
-#pragma unroll
-        for (int kk = tb / 2; kk < 2; ++kk) {
-          const Frag<T> a = frag_load8(GGT + (tb * 16 + li) * LDQ + kk * 32 + lg * 8);
-          const Frag<T> bb = frag_load8(dYT + pc * LDQ + kk * 32 + lg * 8);
-          mma(dxa[tb], a, bb);
-        }
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int t = tb * 16 + lg * 4 + r;
-          if (t < nv && pc < P) {
-            const float dyv = to_f32(dYT[pc * LDQ + t]);
-            dx[(((int64_t)b * L + t0 + t) * H + h) * P + pc] = (T)(dxa[tb][r] + Dh * dyv);
-          }
-        }
+      for (int kk = tb / 2; kk < 2; ++kk) {
+        const Frag<T> a = frag_load_rows(Yc, XS, kk * 32 + lg * 8, pb * 16);
+        const Frag<T> bb = frag_load_rows(GG, XS, kk * 32 + lg * 8, tb * 16);
+        mma(dxa[tb], a, bb);
       }
+      const int t = tb * 16 + li, pr = pb * 16 + lg * 4;
+      float yv[4];
+      load4(Yc + t * XS + pr, yv);
+      floatx4 v;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) v[r] = dxa[tb][r] + Dh * yv[r];
+      if (Cfg::kBf16) store4(Dxb + t * XS + pr, v);  // staged, stored 16 bytes at a time
+      else if (t < nv && pr < P) store4(dxg + (int64_t)t0 * xstride + t * (H * P) + pr, v);
+    }
 
-      // ---- adjoint update G += C^T (omega o dY), rows n, columns p
+    __builtin_amdgcn_sched_barrier(0);
+    // ---- adjoint update G += C^T (omega o dY), rows n, column pc
 #pragma unroll
-      for (int m = 0; m < MP; ++m) {
-        if (!ms[m].ren) continue;
+    for (int m = 0; m < MPW; ++m) {
+      if (!((renbits >> m) & 1)) continue;
 #pragma unroll
-        for (int jb = 0; jb < NBW; ++jb)
+      for (int jb = 0; jb < NBW; ++jb)
 #pragma unroll
-          for (int r = 0; r < 4; ++r) Gs[m][jb][r] *= ms[m].Enew;
-      }
-#pragma unroll
-      for (int kt = 0; kt < 2; ++kt) {
-        float y8[8];
-#pragma unroll
-        for (int s = 0; s < 8; ++s) y8[s] = to_f32(dYT[pc * LDQ + kt * 32 + lg * 8 + s]);
-        Frag<T> Yf[MP];
-#pragma unroll
-        for (int m = 0; m < MP; ++m) {
-          const float4 v0 = *reinterpret_cast<const float4*>(P_om + m * kQ + kt * 32 + lg * 8);
-          const float4 v1 = *reinterpret_cast<const float4*>(P_om + m * kQ + kt * 32 + lg * 8 + 4);
-          frag_set(Yf[m], 0, y8[0] * v0.x);
-          frag_set(Yf[m], 1, y8[1] * v0.y);
-          frag_set(Yf[m], 2, y8[2] * v0.z);
-          frag_set(Yf[m], 3, y8[3] * v0.w);
-          frag_set(Yf[m], 4, y8[4] * v1.x);
-          frag_set(Yf[m], 5, y8[5] * v1.y);
-          frag_set(Yf[m], 6, y8[6] * v1.z);
-          frag_set(Yf[m], 7, y8[7] * v1.w);
-        }
-#pragma unroll
-        for (int jb = 0; jb < NBW; ++jb) {
-          const Frag<T> a = frag_load8(CT + ((nh * NBW + jb) * 16 + li) * LDQ + kt * 32 + lg * 8);
-#pragma unroll
-          for (int m = 0; m < MP; ++m)
-            if (m < M) mma(Gs[m][jb], a, Yf[m]);
-        }
-      }
+        for (int r = 0; r < 4; ++r) Gs[m][jb][r] *= renf[m];
     }
 #pragma unroll
-    for (int m = 0; m < MP; ++m) mode_scale_advance(ms[m]);
-  }
-}
-
-// --------------------------------------------------------------------------
-// sweep 2: reverse direction, adjoint transposed (rows p, columns n): dB
-
-template <typename T, int MP, int NB>
-__device__ __forceinline__ void sweep_adj_cols(const ScanParams& p, int b, int h, int g, T* __restrict__ dBp, unsigned char* smem) {
-  constexpr int NP = NB * 16;
-  const int PP = p.PP, PB = PP / 16, KP = (PB + 1) / 2;
-  const int NWT = blockDim.x >> 6;
-  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, li = lane & 15, lg = lane >> 4;
-  const bool active = wave < NB;
-  const int ncol = wave * 16 + li;
-  const int L = p.L, H = p.H, P = p.P, N = p.N, M = p.M;
-  const int nchunks = (L + kQ - 1) / kQ;
-
-  T* Xs = reinterpret_cast<T*>(smem);  // [Q][LDP]
-  T* dYs = Xs + kQ * LDP;              // [Q][LDP]
-  T* dYT = dYs + kQ * LDP;             // [64][LDQ]
-  T* CT = dYT + 64 * LDQ;              // [NP][LDQ]
-  T* HGT = CT + NP * LDQ;              // [Q][LDQ]  (Gamma o dY X^T)^T
-  float* P_O = reinterpret_cast<float*>(HGT + kQ * LDQ);
-  float* P_Vt = P_O + MP * kQ;
-  float* P_c = P_Vt + MP * kQ;
-  float* P_k = P_c + MP * kQ;
-  float* P_wdb = P_k + MP * kQ;  // kappa e^{-r(A_Q - A)} E
-  float* P_om = P_wdb + MP * kQ; // c e^{-rA} * upd
-  float* P_A = P_om + MP * kQ;
-
-  float rr[MP], lnt[MP];
+    for (int kt = 0; kt < 2; ++kt) {
+      const Frag<T> yf = frag_load_rows(Yc, XS, kt * 32 + lg * 8, pb * 16);
+      Frag<T> Yf[MPW];
 #pragma unroll
-  for (int m = 0; m < MP; ++m) {
-    const float tau = (m < M) ? p.tau[m] : 1.0f;
-    rr[m] = (m < M) ? 1.0f / tau : 0.0f;
-    lnt[m] = (m < M) ? logf(tau) : 0.0f;
-  }
-  for (int i = tid; i < kQ * LDQ; i += blockDim.x) HGT[i] = (T)0.0f;
+      for (int m = 0; m < MPW; ++m) {
+        const float* pv = P_om + (mo + m) * kQ + kt * 32 + lg * 8;
+        const float4 v0 = *reinterpret_cast<const float4*>(pv);
+        const float4 v1 = *reinterpret_cast<const float4*>(pv + 4);
+        frag_set(Yf[m], 0, to_f32(yf.v[0]) * v0.x);
+        frag_set(Yf[m], 1, to_f32(yf.v[1]) * v0.y);
+        frag_set(Yf[m], 2, to_f32(yf.v[2]) * v0.z);
+        frag_set(Yf[m], 3, to_f32(yf.v[3]) * v0.w);
+        frag_set(Yf[m], 4, to_f32(yf.v[4]) * v1.x);
+        frag_set(Yf[m], 5, to_f32(yf.v[5]) * v1.y);
+        frag_set(Yf[m], 6, to_f32(yf.v[6]) * v1.z);
+        frag_set(Yf[m], 7, to_f32(yf.v[7]) * v1.w);
+      }
+#pragma unroll
+      for (int jb = 0; jb < NBW; ++jb) {
+        const Frag<T> a = frag_load_rows(Cc, CS, kt * 32 + lg * 8, (nbo + jb) * 16);
+#pragma unroll
+        for (int m = 0; m < MPW; ++m) mma(Gs[m][jb], a, Yf[m]);  // modes >= M carry zero weights
+      }
+    }
+  };
 
-  const int64_t sbase = ((int64_t)b * H + h) * (int64_t)M * N * P;
-  floatx4 Gs[MP][kPBM];
-  ModeScale ms[MP];
-  {
-    int lo = ncol * P + lg * 4;
-    asm volatile("" : "+v"(lo));
-#pragma unroll
-    for (int m = 0; m < MP; ++m) {
-      ms[m].E = 1.0f;
-#pragma unroll
-      for (int pb = 0; pb < kPBM; ++pb)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int pr = pb * 16 + lg * 4 + r;
-          float v = 0.0f;
-          if (p.d_final_state && active && m < M && ncol < N && pr < P)
-            v = p.d_final_state[sbase + (int64_t)m * N * P + lo + pb * 16 + r];
-          Gs[m][pb][r] = v;
-        }
+  for (int i = 0; i < nchunks; i += 2) {
+    const int c = nchunks - 1 - i;
+    step(c, i, Cb0, Yb0, Cb1, Yb1);
+    if (c > 0) {
+      if (Cfg::NBUF == 2) step(c - 1, i + 1, Cb1, Yb1, Cb0, Yb0);
+      else step(c - 1, i + 1, Cb0, Yb0, Cb0, Yb0);
     }
   }
-
-  for (int c = nchunks - 1; c >= 0; --c) {
-    const int t0 = c * kQ, nv = min(kQ, L - t0);
-    __syncthreads();
-    const int64_t xrow0 = (((int64_t)b * L + t0) * H + h) * P;
-    const int64_t brow0 = (((int64_t)b * L + t0) * p.G + g) * N;
-    stage<T>(reinterpret_cast<const T*>(p.x) + xrow0, (int64_t)H * P, P, PP, nv, Xs, LDP, nullptr);
-    stage<T>(reinterpret_cast<const T*>(p.dy) + xrow0, (int64_t)H * P, P, PP, nv, dYs, LDP, dYT);
-    stage<T>(reinterpret_cast<const T*>(p.Cm) + brow0, (int64_t)p.G * N, N, NP, nv, nullptr, 0, CT);
-    {
-      const int t = lane;
-      const bool valid = t < nv;
-      float dtt, s_eff, cw[MP], ww[MP];
-      token_controls<MP>(p, b, h, t0 + t, valid, lnt, dtt, s_eff, cw, ww);
-      const float A = wave_inclusive_sum(dtt);
-      const float Alast = uniform(__shfl(A, 63, 64));
-      if (wave == 0) P_A[t] = A;
-#pragma unroll
-      for (int m = 0; m < MP; ++m) {
-        mode_scale(ms[m], rr[m], Alast);
-        if ((m % NWT) != wave) continue;
-        const float kap = -expm1f(-dtt * rr[m]) * ww[m];
-        const float ea = expf(-rr[m] * A);
-        P_O[m * kQ + t] = cw[m] * ea;
-        P_Vt[m * kQ + t] = ms[m].safe ? kap * expf(rr[m] * A) : 0.0f;
-        P_c[m * kQ + t] = cw[m];
-        P_k[m * kQ + t] = kap;
-        P_wdb[m * kQ + t] = kap * expf(-rr[m] * (Alast - A)) * ms[m].E;
-        P_om[m * kQ + t] = cw[m] * ea * ms[m].upd;
-      }
-    }
-    __syncthreads();
-
-    // ---- V_m = X G_m^T  ->  dB (inter)
-    floatx4 dBa[4];
-#pragma unroll
-    for (int tb = 0; tb < 4; ++tb) dBa[tb] = floatx4{0.f, 0.f, 0.f, 0.f};
-    if (active) {
-      Frag<T> Af[4][2];
-#pragma unroll
-      for (int tb = 0; tb < 4; ++tb)
-#pragma unroll
-        for (int kp = 0; kp < 2; ++kp) {
-          Af[tb][kp] = frag_zero<T>();
-          if (kp < KP) {
-            const T* row = Xs + (tb * 16 + li) * LDP + kp * 32 + lg * 4;
-            Af[tb][kp] = frag_load4x2(row, (2 * kp + 1 < PB) ? row + 16 : nullptr);
-          }
-        }
-#pragma unroll
-      for (int m = 0; m < MP; ++m) {
-        if (m >= M) continue;
-        Frag<T> Gf[2];
-#pragma unroll
-        for (int kp = 0; kp < 2; ++kp) {
-#pragma unroll
-          for (int s = 0; s < 4; ++s) frag_set(Gf[kp], s, Gs[m][2 * kp][s]);
-#pragma unroll
-          for (int s = 0; s < 4; ++s) frag_set(Gf[kp], 4 + s, Gs[m][2 * kp + 1][s]);
-        }
-#pragma unroll
-        for (int tb = 0; tb < 4; ++tb) {
-          floatx4 V = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-          for (int kp = 0; kp < 2; ++kp)
-            if (kp < KP) mma(V, Af[tb][kp], Gf[kp]);
-          const float4 wb = *reinterpret_cast<const float4*>(P_wdb + m * kQ + tb * 16 + lg * 4);
-          dBa[tb][0] += wb.x * V[0];
-          dBa[tb][1] += wb.y * V[1];
-          dBa[tb][2] += wb.z * V[2];
-          dBa[tb][3] += wb.w * V[3];
-        }
-        __builtin_amdgcn_sched_barrier(0);
-      }
-    }
-    // ---- (Gamma o dY X^T)^T tiles
-    for (int tile = wave; tile < kTiles; tile += NWT) {
-      const int tb = kTB[tile], kb = kKB[tile];
-      const floatx4 D = dyx_tile<T>(dYs, Xs, tb, kb, PP, li, lg);
-      floatx4 Gm = rank_m_tile<MP>(P_O, P_Vt, tb * 16, kb * 16, li, lg);
-#pragma unroll
-      for (int m = 0; m < MP; ++m) {
-        if (ms[m].safe || m >= M) continue;
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int t = tb * 16 + lg * 4 + r, k = kb * 16 + li;
-          if (t >= k) Gm[r] += P_c[m * kQ + t] * P_k[m * kQ + k] * expf(-rr[m] * (P_A[t] - P_A[k]));
-        }
-      }
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int t = tb * 16 + lg * 4 + r, k = kb * 16 + li;
-        HGT[k * LDQ + t] = (T)((t >= k) ? Gm[r] * D[r] : 0.0f);
-      }
-    }
-
-    __syncthreads();  // HGT complete
-
-    if (active) {
-      // ---- dB intra: (Gamma o dY X^T)^T C, rows k, contraction over t >= k
-#pragma unroll
-      for (int tb = 0; tb < 4; ++tb)
-#pragma unroll
-        for (int kk = tb / 2; kk < 2; ++kk) {
-          const Frag<T> a = frag_load8(HGT + (tb * 16 + li) * LDQ + kk * 32 + lg * 8);
-          const Frag<T> bb = frag_load8(CT + ncol * LDQ + kk * 32 + lg * 8);
-          mma(dBa[tb], a, bb);
-        }
-#pragma unroll
-      for (int tb = 0; tb < 4; ++tb)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int t = tb * 16 + lg * 4 + r;
-          if (t < nv && ncol < N) dBp[(((int64_t)b * L + t0 + t) * H + h) * N + ncol] = (T)dBa[tb][r];
-        }
-
-      // ---- adjoint update G^T += dY^T (omega o C), rows p, columns n
-#pragma unroll
-      for (int m = 0; m < MP; ++m) {
-        if (!ms[m].ren) continue;
-#pragma unroll
-        for (int pb = 0; pb < kPBM; ++pb)
-#pragma unroll
-          for (int r = 0; r < 4; ++r) Gs[m][pb][r] *= ms[m].Enew;
-      }
-#pragma unroll
-      for (int kt = 0; kt < 2; ++kt) {
-        float c8[8];
-#pragma unroll
-        for (int s = 0; s < 8; ++s) c8[s] = to_f32(CT[ncol * LDQ + kt * 32 + lg * 8 + s]);
-        Frag<T> Cf[MP];
-#pragma unroll
-        for (int m = 0; m < MP; ++m) {
-          const float4 v0 = *reinterpret_cast<const float4*>(P_om + m * kQ + kt * 32 + lg * 8);
-          const float4 v1 = *reinterpret_cast<const float4*>(P_om + m * kQ + kt * 32 + lg * 8 + 4);
-          frag_set(Cf[m], 0, c8[0] * v0.x);
-          frag_set(Cf[m], 1, c8[1] * v0.y);
-          frag_set(Cf[m], 2, c8[2] * v0.z);
-          frag_set(Cf[m], 3, c8[3] * v0.w);
-          frag_set(Cf[m], 4, c8[4] * v1.x);
-          frag_set(Cf[m], 5, c8[5] * v1.y);
-          frag_set(Cf[m], 6, c8[6] * v1.z);
-          frag_set(Cf[m], 7, c8[7] * v1.w);
-        }
-#pragma unroll
-        for (int pb = 0; pb < kPBM; ++pb) {
-          if (pb >= PB) continue;
-          const Frag<T> a = frag_load8(dYT + (pb * 16 + li) * LDQ + kt * 32 + lg * 8);
-#pragma unroll
-          for (int m = 0; m < MP; ++m)
-            if (m < M) mma(Gs[m][pb], a, Cf[m]);
-        }
-      }
-    }
-#pragma unroll
-    for (int m = 0; m < MP; ++m) mode_scale_advance(ms[m]);
-  }
+  wait_vmem();
+  barrier();
+  if (Cfg::kBf16) store_dx(0);
 }
 
-// --------------------------------------------------------------------------
-
-struct BwdWork {
-  void* tiles;
-  void* dBp;
-  void* dCp;
-  float* eA;
-  float* fA;
-  float* eB;
-  float* fB;
-  float* F;
-  float* dDp;
-};
-
-template <typename T, int MP, int NB>
-__global__ void __launch_bounds__(512) frac_bwd_kernel(ScanParams p, BwdWork wk) {
-  extern __shared__ __align__(16) unsigned char smem[];
-  // XCD-aware (batch, head) order as in the forward
-  int j = blockIdx.x;
-  const int nblk = gridDim.x;
-  if ((nblk & 7) == 0) j = (blockIdx.x & 7) * (nblk >> 3) + (blockIdx.x >> 3);
-  const int b = j / p.H, h = j - b * p.H, g = h * p.G / p.H;
-  const T* tiles = reinterpret_cast<const T*>(wk.tiles);
-  if (blockIdx.y == 0)
-    sweep_state<T, MP, NB>(p, b, h, g, tiles, reinterpret_cast<T*>(wk.dCp), wk.eA, wk.fA, wk.F, wk.dDp, smem);
-  else if (blockIdx.y == 1)
-    sweep_adj_rows<T, MP, NB>(p, b, h, g, tiles, wk.eB, wk.fB, smem);
-  else
-    sweep_adj_cols<T, MP, NB>(p, b, h, g, reinterpret_cast<T*>(wk.dBp), smem);
-}
-
-template <typename T, int MP, int NB>
-size_t bwd_lds_bytes(int PP) {
-  constexpr int NP = NB * 16;
-  const size_t s0 = sizeof(T) * (size_t)(kQ * LDP + 64 * LDQ + kQ * LDP + 2 * NP * LDQ + kQ * LDQ) +
-                    sizeof(float) * (size_t)(10 * MP * kQ + kQ + 2 * 8 * kQ + 3 * kTiles * 16);
-  const size_t s1 = sizeof(T) * (size_t)(kQ * (NP + 8) + NP * LDQ + 2 * 64 * LDQ + kQ * LDQ) +
-                    sizeof(float) * (size_t)(8 * MP * kQ + kQ + 4 * 1024 + 2 * 8 * kQ);
-  const size_t s2 = sizeof(T) * (size_t)(2 * kQ * LDP + 64 * LDQ + NP * LDQ + kQ * LDQ) +
-                    sizeof(float) * (size_t)(6 * MP * kQ + kQ);
-  (void)PP;
-  return s0 > s1 ? (s0 > s2 ? s0 : s2) : (s1 > s2 ? s1 : s2);
-}
+// ---------------------------------------------------------- finishing kernels
 
 // ddt from the per-token terms: suffix sums over the sequence, one wave per (batch, head).
-__global__ void __launch_bounds__(64) frac_bwd_ddt_kernel(ScanParams p, const float* __restrict__ eA,
-                                                         const float* __restrict__ fA, const float* __restrict__ eB,
-                                                         const float* __restrict__ fB, const float* __restrict__ F,
-                                                         const float* __restrict__ dDp) {
+__global__ void __launch_bounds__(64) frac_bwd_ddt_kernel(ScanParams p, BwdWork wk, int nA, int nB) {
   const int bh = blockIdx.x, b = bh / p.H, h = bh - b * p.H;
   const int lane = threadIdx.x;
   const int L = p.L, H = p.H;
+  const int64_t blh = (int64_t)p.Bsz * L * H, bhn = (int64_t)p.Bsz * H;
   float carry = 0.0f;  // sum of e over the tokens after the current chunk
-  const float Fv = F[bh];
+  float Fv = 0.0f;
+  for (int q = 0; q < nA; ++q) Fv += wk.F[q * bhn + bh];
   for (int c = (L + kQ - 1) / kQ - 1; c >= 0; --c) {
     const int t0 = c * kQ, t = t0 + lane;
     const bool valid = t < L;
     const int64_t ith = ((int64_t)b * L + t) * H + h;
-    const float e = valid ? eA[ith] - eB[ith] : 0.0f;
+    float e = 0.0f, f = 0.0f;
+    if (valid) {
+      for (int q = 0; q < nA; ++q) e += wk.eA[q * blh + ith];
+      for (int q = 0; q < nB; ++q) {
+        e -= wk.eB[q * blh + ith];
+        f += wk.fB[q * blh + ith];
+      }
+      f += wk.fA[ith];
+    }
     // inclusive suffix sum within the chunk (lane order reversed)
     float s = e;
 #pragma unroll
@@ -1127,14 +1383,14 @@ __global__ void __launch_bounds__(64) frac_bwd_ddt_kernel(ScanParams p, const fl
       const float al = strided3(p.alpha, p.as0, p.as1, p.as2, b, t, h);
       const float lam = p.lambda ? strided3(p.lambda, p.ls0, p.ls1, p.ls2, b, t, h) : 1.0f;
       const float s_eff = p.lambda ? exp2f(log2f(lam) / al) : 1.0f;
-      const float ddtt = -Fv - (carry + s) + fA[ith] + fB[ith];
+      const float ddtt = -Fv - (carry + s) + f;
       p.ddt[ith] = ddtt * s_eff;
     }
     carry += __shfl(s, 0, 64);
   }
   if (p.dD && b == 0 && lane == 0) {
     float acc = 0.0f;
-    for (int bb = 0; bb < p.Bsz; ++bb) acc += dDp[(int64_t)bb * H + h];
+    for (int bb = 0; bb < p.Bsz; ++bb) acc += wk.dDp[(int64_t)bb * H + h];
     p.dD[h] = acc;
   }
 }
@@ -1174,7 +1430,8 @@ BwdLayout bwd_layout(const ScanParams& p) {
   l.dBp = up(cb_tiles_bytes(p));
   l.dCp = l.dBp + up(bl * p.H * p.N * es);
   l.scal = l.dCp + up(bl * p.H * p.N * es);
-  l.total = l.scal + up(sizeof(float) * (4 * bl * p.H + 2 * (size_t)p.Bsz * p.H));
+  // eA[2], fA, eB[2], fB[2] per token and head; F[2], dDp per head
+  l.total = l.scal + up(sizeof(float) * (7 * bl * p.H + 3 * (size_t)p.Bsz * p.H));
   return l;
 }
 
@@ -1189,27 +1446,27 @@ hipError_t launch_bwd_variant(const ScanParams& p, void* ws, hipStream_t stream)
   float* sc = reinterpret_cast<float*>(base + l.scal);
   const size_t blh = (size_t)p.Bsz * p.L * p.H;
   wk.eA = sc;
-  wk.fA = sc + blh;
-  wk.eB = sc + 2 * blh;
-  wk.fB = sc + 3 * blh;
-  wk.F = sc + 4 * blh;
-  wk.dDp = wk.F + (size_t)p.Bsz * p.H;
+  wk.fA = sc + 2 * blh;
+  wk.eB = sc + 3 * blh;
+  wk.fB = sc + 5 * blh;
+  wk.F = sc + 7 * blh;
+  wk.dDp = wk.F + 2 * (size_t)p.Bsz * p.H;
 
-  hipError_t e = launch_cb_tiles(p, wk.tiles, stream);
+  hipError_t e = launch_cb_tiles(p, base + l.tiles, stream);
   if (e != hipSuccess) return e;
-  const int nw_state = NB, nw_rows = (p.PP / 16) * (NB >= 2 ? 2 : 1);
-  const int nwt = nw_state > nw_rows ? nw_state : nw_rows;
-  const size_t lds = bwd_lds_bytes<T, MP, NB>(p.PP);
-  auto kern = frac_bwd_kernel<T, MP, NB>;
-  e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern), hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-  if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(kern, dim3(p.Bsz * p.H, 3), dim3(64 * nwt), lds, stream, p, wk);
-  e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(frac_bwd_ddt_kernel, dim3(p.Bsz * p.H), dim3(64), 0, stream, p, wk.eA, wk.fA, wk.eB, wk.fB,
-                     wk.F, wk.dDp);
-  e = hipGetLastError();
-  if (e != hipSuccess) return e;
+  const int bh = p.Bsz * p.H;
+  hipLaunchKernelGGL((frac_bwd_state_kernel<T, MP, NB>), dim3(bh * ColCfg<T, MP, NB>::PS), dim3(512), 0, stream, p,
+                     wk);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  hipLaunchKernelGGL((frac_bwd_rows_kernel<T, MP, NB>), dim3(bh * RowCfg<T, MP, NB>::PS), dim3(512), 0, stream, p,
+                     wk);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  hipLaunchKernelGGL((frac_bwd_cols_kernel<T, MP, NB>), dim3(bh * ColCfg<T, MP, NB>::PS), dim3(512), 0, stream, p,
+                     wk);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  hipLaunchKernelGGL(frac_bwd_ddt_kernel, dim3(bh), dim3(64), 0, stream, p, wk, ColCfg<T, MP, NB>::PS,
+                     RowCfg<T, MP, NB>::PS);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
   hipLaunchKernelGGL((frac_bwd_group_sum_kernel<T>), dim3((unsigned)(p.Bsz * p.L), p.G), dim3(128), 0, stream, p,
                      reinterpret_cast<const T*>(wk.dBp), reinterpret_cast<const T*>(wk.dCp));
   return hipGetLastError();

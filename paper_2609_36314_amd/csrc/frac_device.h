@@ -72,21 +72,22 @@ __device__ __forceinline__ Frag<float> frag_load8(const float* p) {
   return f;
 }
 
-// Slots 0..3 from p0[0..3], slots 4..7 from p1[0..3] (p1 == nullptr: zeros).
-__device__ __forceinline__ Frag<bf16> frag_load4x2(const bf16* p0, const bf16* p1) {
+// Slots 0..3 from p0[0..3], slots 4..7 from p1[0..3]; with two = false slots
+// 4..7 are zero and p1 is not read.  (No null-pointer test: comparing an LDS
+// address against null miscompiles on this target.)
+__device__ __forceinline__ Frag<bf16> frag_load4x2(const bf16* p0, const bf16* p1, bool two = true) {
   Frag<bf16> f;
   const bf16x4 a = *reinterpret_cast<const bf16x4*>(p0);
-  bf16x4 b;
-  if (p1) b = *reinterpret_cast<const bf16x4*>(p1);
-  else b = bf16x4{(bf16)0.0f, (bf16)0.0f, (bf16)0.0f, (bf16)0.0f};
+  bf16x4 b = bf16x4{(bf16)0.0f, (bf16)0.0f, (bf16)0.0f, (bf16)0.0f};
+  if (two) b = *reinterpret_cast<const bf16x4*>(p1);
   f.v = bf16x8{a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
   return f;
 }
-__device__ __forceinline__ Frag<float> frag_load4x2(const float* p0, const float* p1) {
+__device__ __forceinline__ Frag<float> frag_load4x2(const float* p0, const float* p1, bool two = true) {
   Frag<float> f;
   const float4 a = *reinterpret_cast<const float4*>(p0);
   float4 b = make_float4(0.f, 0.f, 0.f, 0.f);
-  if (p1) b = *reinterpret_cast<const float4*>(p1);
+  if (two) b = *reinterpret_cast<const float4*>(p1);
   f.v[0] = a.x; f.v[1] = a.y; f.v[2] = a.z; f.v[3] = a.w;
   f.v[4] = b.x; f.v[5] = b.y; f.v[6] = b.z; f.v[7] = b.w;
   return f;
@@ -108,6 +109,25 @@ __device__ __forceinline__ void load8(const float* p, float* out) {
   const float4 b = *reinterpret_cast<const float4*>(p + 4);
   out[0] = a.x; out[1] = a.y; out[2] = a.z; out[3] = a.w;
   out[4] = b.x; out[5] = b.y; out[6] = b.z; out[7] = b.w;
+}
+
+// Four consecutive io elements as floats (8-byte aligned for bf16, 16 for float).
+__device__ __forceinline__ void load4(const bf16* p, float* out) {
+  const bf16x4 v = *reinterpret_cast<const bf16x4*>(p);
+#pragma unroll
+  for (int j = 0; j < 4; ++j) out[j] = (float)v[j];
+}
+__device__ __forceinline__ void load4(const float* p, float* out) {
+  const float4 v = *reinterpret_cast<const float4*>(p);
+  out[0] = v.x; out[1] = v.y; out[2] = v.z; out[3] = v.w;
+}
+
+// Store four floats as four consecutive io elements.
+__device__ __forceinline__ void store4(bf16* p, const floatx4& v) {
+  *reinterpret_cast<bf16x4*>(p) = bf16x4{(bf16)v[0], (bf16)v[1], (bf16)v[2], (bf16)v[3]};
+}
+__device__ __forceinline__ void store4(float* p, const floatx4& v) {
+  *reinterpret_cast<float4*>(p) = make_float4(v[0], v[1], v[2], v[3]);
 }
 
 // Raw copy of 8 io elements global -> shared, no conversion.
@@ -286,6 +306,10 @@ struct DmaPlan {
     }
   }
   // Copy the tile whose first row is at src; only the first nv rows are in range.
+  // OPAQUE: pass the LDS address as a plain 32-bit offset instead of an address
+  // space cast (for single-buffered tiles; some constant-folded casts of LDS
+  // addresses do not compile on this target).
+  template <bool OPAQUE = false>
   __device__ __forceinline__ void issue(T* lds, const T* src, int64_t gstride, int nv) const {
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const long long range = (long long)nv * gstride * (long long)sizeof(T);
@@ -294,8 +318,11 @@ struct DmaPlan {
 #pragma unroll
     for (int k = 0; k < KT; ++k) {
       if (k * 8 + wave >= CPR) continue;  // past the tile (uniform)
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (__attribute__((address_space(3))) void*)(lds + (k * 8 + wave) * 64 * E),
-                                               16, (int)off[k], 0, 0, 0);
+      T* dst = lds + (k * 8 + wave) * 64 * E;
+      __attribute__((address_space(3))) void* l3;
+      if constexpr (OPAQUE) l3 = (__attribute__((address_space(3))) void*)(uintptr_t)(uint32_t)(uintptr_t)dst;
+      else l3 = (__attribute__((address_space(3))) void*)dst;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, l3, 16, (int)off[k], 0, 0, 0);
     }
   }
 };

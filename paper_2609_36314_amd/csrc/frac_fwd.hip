@@ -266,9 +266,9 @@ __global__ void __launch_bounds__(512) frac_fwd_kernel(ScanParams p, const T* __
   planC.init(bstride, N);
   auto stage = [&](int c, T* Xd, T* Bd, T* Cd) {
     const int t0 = c * kQ, nv = min(kQ, L - t0);
-    planX.issue(Xd, xg + (int64_t)t0 * xstride, xstride, nv);
-    planB.issue(Bd, Bgp + (int64_t)t0 * bstride, bstride, nv);
-    planC.issue(Cd, Cgp + (int64_t)t0 * bstride, bstride, nv);
+    planX.template issue<Cfg::NBUF == 1>(Xd, xg + (int64_t)t0 * xstride, xstride, nv);
+    planB.template issue<Cfg::NBUF == 1>(Bd, Bgp + (int64_t)t0 * bstride, bstride, nv);
+    planC.template issue<Cfg::NBUF == 1>(Cd, Cgp + (int64_t)t0 * bstride, bstride, nv);
   };
   // output rows of chunk c (staged in Yb) -> global, 16 bytes per thread
   auto store_y = [&](int c) {
@@ -317,7 +317,10 @@ __global__ void __launch_bounds__(512) frac_fwd_kernel(ScanParams p, const T* __
     if (wave == 0) P_A[lane] = A_l;
 
     // ---- per (token, mode) controls and weights: thread pair = t MP + m
-    int unsafe = 0;  // bit m: the factorised Gamma would overflow for mode m (direct decay)
+    // bit m of unsafe: the factorised Gamma would overflow for mode m (direct decay);
+    // the same flags in every wave, lane m < MP testing mode m
+    const bool over = lane < MP && lane < M && !(s_rr[lane < MP ? lane : 0] * Alast <= kSafeExponent);
+    const int unsafe = (int)(__ballot(over) & ((1ull << MP) - 1));
     for (int pr = tid; pr < kQ * MP; pr += 512) {
       const int t = pr / MP, m = pr - t * MP;
       const float A = __shfl(A_l, t, 64), dtt = __shfl(dtt_l, t, 64), al = __shfl(al_l, t, 64);
@@ -326,8 +329,9 @@ __global__ void __launch_bounds__(512) frac_fwd_kernel(ScanParams p, const T* __
       const float r = s_rr[m], prior = -al * s_lnt[m];
       float zc = (m < M) ? prior + ((rl_bh && valid) ? rl_bh[ith] : 0.0f) : -INFINITY;
       float zw = (m < M) ? prior + ((wl_bh && valid) ? wl_bh[ith] : 0.0f) : -INFINITY;
-      const float cw = group_softmax<MP>(zc);
-      const float ww = w_is_c ? cw : group_softmax<MP>(zw);
+      // tokens past the sequence get zero weights (their tile rows may hold anything finite)
+      const float cw = valid ? group_softmax<MP>(zc) : 0.0f;
+      const float ww = w_is_c ? cw : (valid ? group_softmax<MP>(zw) : 0.0f);
       const float xr = r * Alast;
       const bool safe = xr <= kSafeExponent;
       const float Enew = Ecur[m] * fexp(-xr);
@@ -342,10 +346,7 @@ __global__ void __launch_bounds__(512) frac_fwd_kernel(ScanParams p, const T* __
       P_c[m * kQ + t] = cw;
       P_k[m * kQ + t] = kap;
       if (pr < MP) Enext[m] = ren ? 1.0f : Enew;
-      // lanes 0..MP-1 of every wave hold modes 0..MP-1 of one token
-      unsafe = (int)(__ballot(m < M && !safe) & ((1ull << MP) - 1));
     }
-    unsafe = __builtin_amdgcn_readfirstlane(unsafe);
     // this wave's modes: rescale flags and factors (wave-uniform)
     float renf[MPW];
     int renbits = 0;
@@ -411,7 +412,7 @@ __global__ void __launch_bounds__(512) frac_fwd_kernel(ScanParams p, const T* __
 #pragma unroll
         for (int kb = 0; kb < KBW; ++kb) {
           const T* row = Cc + ((tp * TBP + i) * 16 + li) * CS + nbo * 16 + kb * 32 + lg * 4;
-          Ca[i][kb] = frag_load4x2(row, (2 * kb + 1 < NBW) ? row + 16 : nullptr);
+          Ca[i][kb] = frag_load4x2(row, row + 16, 2 * kb + 1 < NBW);
         }
 #pragma unroll
       for (int m = 0; m < MPW; ++m) {

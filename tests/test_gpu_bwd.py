@@ -92,19 +92,20 @@ def test_bwd_parity_small(name):
         assert_close("dD", f64(g["dD"]), ref["dD"], tol)
 
 
-def test_bwd_large_steps_use_direct_decay():
+@pytest.mark.parametrize("io,M,N", [("f32", 4, 32), ("bf16", 4, 32), ("bf16", 8, 128)])
+def test_bwd_large_steps_use_direct_decay(io, M, N):
     """Steps large enough that r A_Q exceeds the factorisation bound for the fast
     modes (the per-pair exponential path), in float32 and bfloat16."""
-    for io in ("f32", "bf16"):
-        w = Workload("t", 1, 140, 2, 32, 32, 4, io_dtype=io, backward=True)
-        inp = device_inputs(w, seed=3)
-        inp["dt"] = (inp["dt"] * 8.0).contiguous()
-        tau_d, tau64 = _tau(4)
-        g = _run_bwd(inp, tau_d)
-        torch.cuda.synchronize()
-        ref = _oracle_bwd(inp, tau64)
-        for k, rk in (("dx", "dx"), ("ddt", "ddt"), ("dBm", "dBm"), ("dCm", "dCm")):
-            assert_close(io + " " + k, f64(g[k]), ref[rk], TOL[io])
+    w = Workload("t", 1, 140, 2, 32, N, M, io_dtype=io, backward=True)
+    inp = device_inputs(w, seed=3)
+    inp["dt"] = (inp["dt"] * 8.0).contiguous()
+    tau_d, tau64 = _tau(M)
+    print("case", io, M, N, flush=True)
+    g = _run_bwd(inp, tau_d)
+    torch.cuda.synchronize()
+    ref = _oracle_bwd(inp, tau64)
+    for k, rk in (("dx", "dx"), ("ddt", "ddt"), ("dBm", "dBm"), ("dCm", "dCm")):
+        assert_close(io + " " + k, f64(g[k]), ref[rk], TOL[io])
 
 
 def test_bwd_deterministic():

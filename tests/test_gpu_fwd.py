@@ -120,6 +120,23 @@ def test_fwd_mode_isolation(mode):
     assert_close("state of mode %d" % mode, f64(fs)[:, :, mode], fsr[:, :, mode], TOL["bf16"])
 
 
+@pytest.mark.parametrize("io,M,N", [("f32", 4, 32), ("bf16", 4, 32), ("bf16", 8, 64), ("bf16", 8, 128)])
+def test_fwd_large_steps_use_direct_decay(io, M, N):
+    """Steps large enough that r A_Q exceeds the factorisation bound for the fast
+    modes (the per-pair exponential path) and the state scale is folded back into
+    the accumulators every chunk."""
+    w = Workload("t", 1, 140, 2, 32, N, M, io_dtype=io, final_state=True)
+    inp = device_inputs(w, seed=3)
+    inp["dt"] = (inp["dt"] * 8.0).contiguous()
+    tau_d, tau64 = _tau(M)
+    print("case", io, M, N, flush=True)
+    y, fs = _run(w, inp, tau_d)
+    torch.cuda.synchronize()
+    yr, fsr = _oracle(inp, tau64)
+    assert_close("y", f64(y), yr, TOL[io])
+    _check_state(f64(fs), fsr, TOL[io], M)
+
+
 def test_fwd_chunk_split_invariance():
     """Prefill of L tokens == prefill of 128 then L-128 more from the returned state."""
     w = Workload("t", 2, 300, 4, 64, 128, 4, final_state=True)
