@@ -51,6 +51,8 @@ def parse():
     ap.add_argument("--main", default="train-b4-l4096-m8")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample-heads", type=int, default=64)
+    ap.add_argument("--cpu-sample-batch", type=int, default=4,
+                    help="batch elements of the main workload the oracle runs (bounded CPU sample)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run one plain 1 GiB device copy (reference for the HBM byte counters)")
     return ap.parse_args()
@@ -203,14 +205,15 @@ def roofline(bound, work, ms, peak, unit):
             "work_per_launch": work, "ms_per_launch": ms, "traffic": None}
 
 
-def cpu_baseline(w, heads):
-    """The float64 oracle on a bounded slice: batch element 0, `heads` heads, full length."""
+def cpu_baseline(w, heads, batch):
+    """The float64 oracle on a bounded slice: the first `batch` batch elements, `heads` heads, full length."""
     import oracle
     from paper_2609_36314_amd.workloads import generate
     a = generate(w, 0)
     H = min(heads, w.nheads)
+    nb = max(1, min(batch, w.batch))
     tau = oracle.default_tau(w.nmodes)
-    sl = lambda k: np.asarray(a[k])[0:1].astype(np.float64)
+    sl = lambda k: np.asarray(a[k])[0:nb].astype(np.float64)
     x, dt = sl("x")[:, :, :H], sl("dt")[:, :, :H]
     Bm, Cm = sl("Bm"), sl("Cm")
     alpha = np.broadcast_to(np.asarray(a["alpha"], np.float64), dt.shape)
@@ -219,10 +222,10 @@ def cpu_baseline(w, heads):
     if w.backward:
         oracle.backward(x, dt, Bm, Cm, alpha, tau, sl("dy")[:, :, :H])
     sec = time.perf_counter() - t0
-    tokens = w.seqlen * H / w.nheads  # token-equivalents of the full head count
+    tokens = nb * w.seqlen * H / w.nheads  # token-equivalents of the full head count
     return {"value": tokens / sec, "unit": "tokens/s", "cores": oracle.num_threads(), "kind": "oracle",
-            "sample": "batch element 0, %d of %d heads, %d tokens, %s" % (
-                H, w.nheads, w.seqlen, "forward + backward" if w.backward else "forward"),
+            "sample": "%d of %d batch elements, %d of %d heads, %d tokens, %s" % (
+                nb, w.batch, H, w.nheads, w.seqlen, "forward + backward" if w.backward else "forward"),
             "seconds": sec}
 
 
@@ -275,11 +278,16 @@ def main():
                    "step": "forward + backward scan" if main_w.backward else "forward scan"},
     }
     if mres:
-        rf = mres.get("fwd_bwd_roofline") or mres["fwd_roofline"]
-        line["roofline"] = dict(rf, kernel="frac_scan_fwd + frac_scan_bwd (all launches of one step)")
+        if "bwd_roofline" in mres:
+            # the dominant entry point of the step: frac_scan_bwd (C B^T tiles, state / row / column
+            # sweeps, ddt suffix sums, group sum of dB and dC), one launch per step
+            line["roofline"] = dict(mres["bwd_roofline"], kernel="frac_scan_bwd")
+            line["step_roofline"] = dict(mres["fwd_bwd_roofline"], kernel="frac_scan_fwd + frac_scan_bwd")
+        else:
+            line["roofline"] = dict(mres["fwd_roofline"], kernel="frac_scan_fwd")
     line["workloads"] = results
     if not args.no_cpu_baseline:
-        line["cpu_baseline"] = cpu_baseline(main_w, args.cpu_sample_heads)
+        line["cpu_baseline"] = cpu_baseline(main_w, args.cpu_sample_heads, args.cpu_sample_batch)
     print(json.dumps(line))
 
 

@@ -297,10 +297,10 @@ struct BwdWork {
   const void* tiles;  // C B^T tiles
   void* dBp;          // per-head dB, [B, L, H, N]
   void* dCp;          // per-head dC
-  float* eA;          // [2][B L H] readout / intra part of e (per N half)
-  float* fA;          // [B L H] intra part of f
-  float* eB;          // [2][B L H] adjoint part of e (per P half)
-  float* fB;          // [2][B L H] adjoint part of f
+  float* eA;          // [2][B H L] readout / intra part of e (per N half)
+  float* fA;          // [B H L] intra part of f
+  float* eB;          // [2][B H L] adjoint part of e (per P half)
+  float* fB;          // [2][B H L] adjoint part of f
   float* F;           // [2][B H] final-state term (per N half)
   float* dDp;         // [B H] sum(dy . x)
 };
@@ -605,7 +605,7 @@ __global__ void __launch_bounds__(512) frac_bwd_state_kernel(ScanParams p, BwdWo
         }
       }
       if (t < nv) {
-        const int64_t ith = ((int64_t)b * L + t0 + t) * H + h;
+        const int64_t ith = ((int64_t)b * H + h) * L + t0 + t;  // [B, H, L]: one head's tokens contiguous
         wk.eA[ps * bl_h + ith] = er - ec;
         if (ps == 0) wk.fA[ith] = ef;
       }
@@ -1269,7 +1269,7 @@ __global__ void __launch_bounds__(512) frac_bwd_rows_kernel(ScanParams p, BwdWor
         f += redF[w2 * kQ + t];
       }
       if (t < nv) {
-        const int64_t ith = ((int64_t)b * L + t0 + t) * H + h;
+        const int64_t ith = ((int64_t)b * H + h) * L + t0 + t;  // [B, H, L]
         wk.eB[ps * bl_h + ith] = e;
         wk.fB[ps * bl_h + ith] = f;
       }
@@ -1350,70 +1350,99 @@ __global__ void __launch_bounds__(512) frac_bwd_rows_kernel(ScanParams p, BwdWor
 
 // ---------------------------------------------------------- finishing kernels
 
-// ddt from the per-token terms: suffix sums over the sequence, one wave per (batch, head).
-__global__ void __launch_bounds__(64) frac_bwd_ddt_kernel(ScanParams p, BwdWork wk, int nA, int nB) {
+// ddt from the per-token terms: suffix sums over the sequence.  One block of 256
+// threads per (batch, head) walks the sequence backwards in tiles of 256 tokens
+// (coalesced reads of the [B, H, L] partials); fixed summation order.
+__global__ void __launch_bounds__(256) frac_bwd_ddt_kernel(ScanParams p, BwdWork wk, int nA, int nB) {
+  __shared__ float wsum[4];
   const int bh = blockIdx.x, b = bh / p.H, h = bh - b * p.H;
-  const int lane = threadIdx.x;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int L = p.L, H = p.H;
   const int64_t blh = (int64_t)p.Bsz * L * H, bhn = (int64_t)p.Bsz * H;
-  float carry = 0.0f;  // sum of e over the tokens after the current chunk
+  const int64_t row = (int64_t)bh * L;  // this head's tokens in the partials
   float Fv = 0.0f;
   for (int q = 0; q < nA; ++q) Fv += wk.F[q * bhn + bh];
-  for (int c = (L + kQ - 1) / kQ - 1; c >= 0; --c) {
-    const int t0 = c * kQ, t = t0 + lane;
+  float carry = 0.0f;  // sum of e over the tokens after the current tile
+  for (int t0 = ((L - 1) / 256) * 256; t0 >= 0; t0 -= 256) {
+    const int t = t0 + tid;
     const bool valid = t < L;
-    const int64_t ith = ((int64_t)b * L + t) * H + h;
     float e = 0.0f, f = 0.0f;
     if (valid) {
-      for (int q = 0; q < nA; ++q) e += wk.eA[q * blh + ith];
+      for (int q = 0; q < nA; ++q) e += wk.eA[q * blh + row + t];
       for (int q = 0; q < nB; ++q) {
-        e -= wk.eB[q * blh + ith];
-        f += wk.fB[q * blh + ith];
+        e -= wk.eB[q * blh + row + t];
+        f += wk.fB[q * blh + row + t];
       }
-      f += wk.fA[ith];
+      f += wk.fA[row + t];
     }
-    // inclusive suffix sum within the chunk (lane order reversed)
+    // inclusive suffix sum within the wave (lane order reversed), then across the 4 waves
     float s = e;
 #pragma unroll
     for (int off = 1; off < 64; off <<= 1) {
       const float o = __shfl_down(s, off, 64);
       if (lane + off < 64) s += o;
     }
+    if (lane == 0) wsum[wave] = s;
+    __syncthreads();
+    float later = carry;  // waves after this one within the tile, in wave order
+    for (int w2 = 3; w2 > wave; --w2) later += wsum[w2];
+    float tile_total = 0.0f;
+    for (int w2 = 3; w2 >= 0; --w2) tile_total += wsum[w2];
+    __syncthreads();
     if (valid) {
       const float al = strided3(p.alpha, p.as0, p.as1, p.as2, b, t, h);
       const float lam = p.lambda ? strided3(p.lambda, p.ls0, p.ls1, p.ls2, b, t, h) : 1.0f;
       const float s_eff = p.lambda ? exp2f(log2f(lam) / al) : 1.0f;
-      const float ddtt = -Fv - (carry + s) + f;
-      p.ddt[ith] = ddtt * s_eff;
+      const float ddtt = -Fv - (later + s) + f;
+      p.ddt[((int64_t)b * L + t) * H + h] = ddtt * s_eff;
     }
-    carry += __shfl(s, 0, 64);
+    carry += tile_total;
   }
-  if (p.dD && b == 0 && lane == 0) {
+  if (p.dD && b == 0 && tid == 0) {
     float acc = 0.0f;
     for (int bb = 0; bb < p.Bsz; ++bb) acc += wk.dDp[(int64_t)bb * H + h];
     p.dD[h] = acc;
   }
 }
 
-// dB, dC of each group: fixed-order sum of the per-head partials.
+// dB, dC of each group: fixed-order sum of the per-head partials; each thread
+// sums 16 bytes of a (token, group) row over the group's heads.
 template <typename T>
-__global__ void __launch_bounds__(128) frac_bwd_group_sum_kernel(ScanParams p, const T* __restrict__ dBp,
-                                                                 const T* __restrict__ dCp) {
-  const int64_t bt = blockIdx.x;  // b * L + t
-  const int g = blockIdx.y;
-  const int H = p.H, N = p.N, hpg = H / p.G;
-  T* dB = reinterpret_cast<T*>(p.dBm);
-  T* dC = reinterpret_cast<T*>(p.dCm);
-  for (int n = threadIdx.x; n < N; n += blockDim.x) {
-    float sb = 0.f, sc = 0.f;
-    for (int j = 0; j < hpg; ++j) {
-      const int64_t off = (bt * H + g * hpg + j) * N + n;
-      sb += to_f32(dBp[off]);
-      sc += to_f32(dCp[off]);
+__global__ void __launch_bounds__(256) frac_bwd_group_sum_kernel(ScanParams p, const T* __restrict__ dBp,
+                                                                 const T* __restrict__ dCp, int64_t nrows) {
+  constexpr int E = 16 / sizeof(T);
+  const int H = p.H, N = p.N, G = p.G, hpg = H / G, cpr = N / E;  // 16-byte chunks per row
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= nrows * G * cpr) return;
+  const int ch = (int)(i % cpr);
+  const int64_t rg = i / cpr;  // (b * L + t) * G + g
+  const int g = (int)(rg % G);
+  const int64_t bt = rg / G;
+  float sb[E], sc[E];
+#pragma unroll
+  for (int k = 0; k < E; ++k) sb[k] = sc[k] = 0.0f;
+  for (int j = 0; j < hpg; ++j) {
+    const int64_t off = (bt * H + g * hpg + j) * N + ch * E;
+    float vb[E], vc[E];
+    if constexpr (E == 8) {
+      load8(dBp + off, vb);
+      load8(dCp + off, vc);
+    } else {
+      load4(dBp + off, vb);
+      load4(dCp + off, vc);
     }
-    const int64_t o = (bt * p.G + g) * N + n;
-    dB[o] = (T)sb;
-    dC[o] = (T)sc;
+#pragma unroll
+    for (int k = 0; k < E; ++k) {
+      sb[k] += vb[k];
+      sc[k] += vc[k];
+    }
+  }
+  T* dB = reinterpret_cast<T*>(p.dBm) + rg * N + ch * E;
+  T* dC = reinterpret_cast<T*>(p.dCm) + rg * N + ch * E;
+#pragma unroll
+  for (int k = 0; k < E; ++k) {
+    dB[k] = (T)sb[k];
+    dC[k] = (T)sc[k];
   }
 }
 
@@ -1464,11 +1493,13 @@ hipError_t launch_bwd_variant(const ScanParams& p, void* ws, hipStream_t stream)
   hipLaunchKernelGGL((frac_bwd_cols_kernel<T, MP, NB>), dim3(bh * ColCfg<T, MP, NB>::PS), dim3(512), 0, stream, p,
                      wk);
   if ((e = hipGetLastError()) != hipSuccess) return e;
-  hipLaunchKernelGGL(frac_bwd_ddt_kernel, dim3(bh), dim3(64), 0, stream, p, wk, ColCfg<T, MP, NB>::PS,
+  hipLaunchKernelGGL(frac_bwd_ddt_kernel, dim3(bh), dim3(256), 0, stream, p, wk, ColCfg<T, MP, NB>::PS,
                      RowCfg<T, MP, NB>::PS);
   if ((e = hipGetLastError()) != hipSuccess) return e;
-  hipLaunchKernelGGL((frac_bwd_group_sum_kernel<T>), dim3((unsigned)(p.Bsz * p.L), p.G), dim3(128), 0, stream, p,
-                     reinterpret_cast<const T*>(wk.dBp), reinterpret_cast<const T*>(wk.dCp));
+  const int64_t nrows = (int64_t)p.Bsz * p.L;
+  const int64_t nthr = nrows * p.G * (p.N / (16 / (int)sizeof(T)));
+  hipLaunchKernelGGL((frac_bwd_group_sum_kernel<T>), dim3((unsigned)((nthr + 255) / 256)), dim3(256), 0, stream, p,
+                     reinterpret_cast<const T*>(wk.dBp), reinterpret_cast<const T*>(wk.dCp), nrows);
   return hipGetLastError();
 }
 
