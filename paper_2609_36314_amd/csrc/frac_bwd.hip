@@ -298,7 +298,7 @@ struct BwdWork {
   void* dBp;          // per-head dB, [B, L, H, N]
   void* dCp;          // per-head dC
   float* eA;          // [2][B H L] readout / intra part of e (per N half)
-  float* fA;          // [B H L] intra part of f
+  float* fA;          // [2][B H L] intra part of f (per N half)
   float* eB;          // [2][B H L] adjoint part of e (per P half)
   float* fB;          // [2][B H L] adjoint part of f
   float* F;           // [2][B H] final-state term (per N half)
@@ -453,6 +453,8 @@ __global__ void __launch_bounds__(512) frac_bwd_state_kernel(ScanParams p, BwdWo
   }
   float dd_acc = 0.0f;
   const T* gtiles = reinterpret_cast<const T*>(wk.tiles);
+  TilePrefetch<T> gtile;  // C B^T tile values, loaded one chunk ahead
+  gtile.load(gtiles + ((int64_t)b * nchunks * G + g) * (kTiles * kTileElems), wave, lane);
   T* dCp = reinterpret_cast<T*>(wk.dCp);
   const int64_t bl_h = (int64_t)p.Bsz * L * H;
 
@@ -489,8 +491,10 @@ __global__ void __launch_bounds__(512) frac_bwd_state_kernel(ScanParams p, BwdWo
     // ---- intra-chunk tiles: HG = Gamma o D (LDS, transposed), row / column sums of
     // H o Phi and column sums of H o Psi (first workgroup of the head only)
     {
-      const T* gt = gtiles + (((int64_t)b * nchunks + c) * G + g) * (kTiles * kTileElems);
-      for (int tile = wave; tile < kTiles; tile += 8) {
+#pragma unroll
+      for (int jt = 0; jt < 2; ++jt) {
+        const int tile = wave + 8 * jt;
+        if (tile >= kTiles) break;
         const int tb = kTB[tile], kb = kKB[tile];
         const floatx4 D = dyx_tile<T, XS>(Yc, Xc, tb, kb);
         floatx4 Gm = rank_m_tile<MP>(P_O, P_Vt, tb * 16, kb * 16);
@@ -504,7 +508,7 @@ __global__ void __launch_bounds__(512) frac_bwd_state_kernel(ScanParams p, BwdWo
         T* dst = HGT + (kb * 16 + li) * XS + tb * 16 + lg * 4;
 #pragma unroll
         for (int r = 0; r < 4; ++r) dst[r] = (T)hv[r];
-        if (ps == 0) {
+        if (tile % Cfg::PS == ps) {  // the two halves of N share the tile sums
           floatx4 Ph = rank_m_tile<MP>(P_rO, P_Vt, tb * 16, kb * 16);
           floatx4 Ps = rank_m_tile<MP>(P_O, P_Y, tb * 16, kb * 16);
           if (unsafe) {
@@ -515,7 +519,7 @@ __global__ void __launch_bounds__(512) frac_bwd_state_kernel(ScanParams p, BwdWo
 #pragma unroll
           for (int r = 0; r < 4; ++r) {
             const int t = tb * 16 + lg * 4 + r, kk = kb * 16 + li;
-            const float hm = (t >= kk) ? to_f32(gt[tile * kTileElems + lane * 4 + r]) * D[r] : 0.0f;
+            const float hm = (t >= kk) ? gtile.get(jt, r) * D[r] : 0.0f;
             rv[r] = hm * Ph[r];
             ce += hm * Ph[r];
             cf += hm * Ps[r];
@@ -533,6 +537,8 @@ __global__ void __launch_bounds__(512) frac_bwd_state_kernel(ScanParams p, BwdWo
         }
       }
     }
+
+    if (c + 1 < nchunks) gtile.load(gtiles + (((int64_t)b * nchunks + c + 1) * G + g) * (kTiles * kTileElems), wave, lane);
 
     __builtin_amdgcn_sched_barrier(0);
     // ---- readout side of the state entering the chunk, transposed: U^T_m = S_m dY^T
@@ -597,17 +603,21 @@ __global__ void __launch_bounds__(512) frac_bwd_state_kernel(ScanParams p, BwdWo
       const int t = lane, tbt = t >> 4, tr = t & 15;
       float er = 0.f, ec = 0.f, ef = 0.f;
       for (int w2 = 0; w2 < 8; ++w2) er += redR[w2 * kQ + t];
-      if (ps == 0) {
-        for (int kb2 = 0; kb2 <= tbt; ++kb2) er += slotR[(tbt * (tbt + 1) / 2 + kb2) * 16 + tr];
-        for (int tb2 = tbt; tb2 < 4; ++tb2) {
-          ec += slotC[(tb2 * (tb2 + 1) / 2 + tbt) * 16 + tr];
-          ef += slotF[(tb2 * (tb2 + 1) / 2 + tbt) * 16 + tr];
+      for (int kb2 = 0; kb2 <= tbt; ++kb2) {
+        const int tile = tbt * (tbt + 1) / 2 + kb2;
+        if (tile % Cfg::PS == ps) er += slotR[tile * 16 + tr];
+      }
+      for (int tb2 = tbt; tb2 < 4; ++tb2) {
+        const int tile = tb2 * (tb2 + 1) / 2 + tbt;
+        if (tile % Cfg::PS == ps) {
+          ec += slotC[tile * 16 + tr];
+          ef += slotF[tile * 16 + tr];
         }
       }
       if (t < nv) {
         const int64_t ith = ((int64_t)b * H + h) * L + t0 + t;  // [B, H, L]: one head's tokens contiguous
         wk.eA[ps * bl_h + ith] = er - ec;
-        if (ps == 0) wk.fA[ith] = ef;
+        wk.fA[ps * bl_h + ith] = ef;
       }
     }
     if (ps == 0) {
@@ -1137,6 +1147,8 @@ __global__ void __launch_bounds__(512) frac_bwd_rows_kernel(ScanParams p, BwdWor
   }
   const T* gtiles = reinterpret_cast<const T*>(wk.tiles);
   const int64_t bl_h = (int64_t)p.Bsz * L * H;
+  TilePrefetch<T> gtile;  // C B^T tile values, loaded one chunk ahead (in processing order)
+  gtile.load(gtiles + (((int64_t)b * nchunks + nchunks - 1) * G + g) * (kTiles * kTileElems), wave, lane);
 
   auto step = [&](int c, int i, T* Cc, T* Yc, T* Cn, T* Yn) __attribute__((always_inline)) {
     const int t0 = c * kQ, nv = min(kQ, L - t0);
@@ -1171,18 +1183,22 @@ __global__ void __launch_bounds__(512) frac_bwd_rows_kernel(ScanParams p, BwdWor
     __builtin_amdgcn_sched_barrier(0);
     // ---- GG = (C B^T) o Gamma, natural [t'][k], causal
     {
-      const T* gt = gtiles + (((int64_t)b * nchunks + c) * G + g) * (kTiles * kTileElems);
-      for (int tile = wave; tile < kTiles; tile += 8) {
+#pragma unroll
+      for (int jt = 0; jt < 2; ++jt) {
+        const int tile = wave + 8 * jt;
+        if (tile >= kTiles) break;
         const int tb = kTB[tile], kb = kKB[tile];
         floatx4 Gm = rank_m_tile<MP>(P_O, P_Vt, tb * 16, kb * 16);
         if (unsafe) unsafe_terms<MP>(Gm, unsafe, P_c, P_k, P_A, s_rr, tb, kb, false);
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int t = tb * 16 + lg * 4 + r, kk = kb * 16 + li;
-          GG[t * XS + kk] = (T)((t >= kk) ? to_f32(gt[tile * kTileElems + lane * 4 + r]) * Gm[r] : 0.0f);
+          GG[t * XS + kk] = (T)((t >= kk) ? gtile.get(jt, r) * Gm[r] : 0.0f);
         }
       }
     }
+
+    if (c > 0) gtile.load(gtiles + (((int64_t)b * nchunks + c - 1) * G + g) * (kTiles * kTileElems), wave, lane);
 
     __builtin_amdgcn_sched_barrier(0);
     // ---- Z^T_m = G_m^T B^T (rows p of this wave's block, columns t) -> dx^T (inter)
@@ -1373,7 +1389,7 @@ __global__ void __launch_bounds__(256) frac_bwd_ddt_kernel(ScanParams p, BwdWork
         e -= wk.eB[q * blh + row + t];
         f += wk.fB[q * blh + row + t];
       }
-      f += wk.fA[row + t];
+      for (int q = 0; q < nA; ++q) f += wk.fA[q * blh + row + t];
     }
     // inclusive suffix sum within the wave (lane order reversed), then across the 4 waves
     float s = e;
@@ -1459,8 +1475,8 @@ BwdLayout bwd_layout(const ScanParams& p) {
   l.dBp = up(cb_tiles_bytes(p));
   l.dCp = l.dBp + up(bl * p.H * p.N * es);
   l.scal = l.dCp + up(bl * p.H * p.N * es);
-  // eA[2], fA, eB[2], fB[2] per token and head; F[2], dDp per head
-  l.total = l.scal + up(sizeof(float) * (7 * bl * p.H + 3 * (size_t)p.Bsz * p.H));
+  // eA[2], fA[2], eB[2], fB[2] per token and head; F[2], dDp per head
+  l.total = l.scal + up(sizeof(float) * (8 * bl * p.H + 3 * (size_t)p.Bsz * p.H));
   return l;
 }
 
@@ -1476,9 +1492,9 @@ hipError_t launch_bwd_variant(const ScanParams& p, void* ws, hipStream_t stream)
   const size_t blh = (size_t)p.Bsz * p.L * p.H;
   wk.eA = sc;
   wk.fA = sc + 2 * blh;
-  wk.eB = sc + 3 * blh;
-  wk.fB = sc + 5 * blh;
-  wk.F = sc + 7 * blh;
+  wk.eB = sc + 4 * blh;
+  wk.fB = sc + 6 * blh;
+  wk.F = sc + 8 * blh;
   wk.dDp = wk.F + 2 * (size_t)p.Bsz * p.H;
 
   hipError_t e = launch_cb_tiles(p, base + l.tiles, stream);

@@ -32,28 +32,26 @@ __global__ void __launch_bounds__(kDecodeThreads) frac_decode_kernel(ScanParams 
   const T* Bg = reinterpret_cast<const T*>(p.Bm) + ((int64_t)b * p.G + g) * N;
   const T* Cg = reinterpret_cast<const T*>(p.Cm) + ((int64_t)b * p.G + g) * N;
 
-  if (tid == 0) {
-    // per-token coefficients (eq. tau-eff, eq. rho-beta-def-frac, Algorithm steps 1-6)
+  if (tid < 64) {
+    // per-token coefficients (eq. tau-eff, eq. rho-beta-def-frac, Algorithm steps 1-6):
+    // lane m < MP handles mode m, the softmax runs across those lanes
+    const int m = tid < MP ? tid : MP - 1;
     const int64_t ith = (int64_t)b * H + h;
     const float dtv = p.dt[ith];
     const float al = p.alpha[b * p.as0 + h * p.as1];
     const float lam = p.lambda ? p.lambda[b * p.ls0 + h * p.ls1] : 1.0f;
     const float dtt = effective_step(dtv, al, p.lambda, lam);
-    float zc[MP], zw[MP];
-#pragma unroll
-    for (int m = 0; m < MP; ++m) {
-      const float prior = (m < M) ? -al * logf(p.tau[m]) : 0.0f;
-      zc[m] = prior + ((p.read_logit && m < M) ? p.read_logit[ith * M + m] : 0.0f);
-      zw[m] = prior + ((p.write_logit && m < M) ? p.write_logit[ith * M + m] : 0.0f);
-    }
-    softmax_modes<MP>(zc, M);
-    softmax_modes<MP>(zw, M);
-#pragma unroll
-    for (int m = 0; m < MP; ++m) {
-      const float arg = (m < M) ? -dtt / p.tau[m] : 0.0f;
+    const float tau = (m < M) ? p.tau[m] : 1.0f;
+    const float prior = -al * logf(tau);
+    const float zc = (m < M) ? prior + (p.read_logit ? p.read_logit[ith * M + m] : 0.0f) : -INFINITY;
+    const float zw = (m < M) ? prior + (p.write_logit ? p.write_logit[ith * M + m] : 0.0f) : -INFINITY;
+    const float cw = group_softmax<MP>(zc);
+    const float ww = group_softmax<MP>(zw);
+    if (tid < MP) {
+      const float arg = (m < M) ? -dtt / tau : 0.0f;
       s_rho[m] = expf(arg);
-      s_kap[m] = -expm1f(arg) * zw[m];
-      s_c[m] = zc[m];
+      s_kap[m] = -expm1f(arg) * ww;
+      s_c[m] = cw;
     }
   }
   for (int i = tid; i < N; i += kDecodeThreads) {
@@ -67,39 +65,50 @@ __global__ void __launch_bounds__(kDecodeThreads) frac_decode_kernel(ScanParams 
   const int RG = kDecodeThreads / P4;  // row groups
   const int col = tid % P4, rg = tid / P4;
   const float4 xv = make_float4(sx[4 * col], sx[4 * col + 1], sx[4 * col + 2], sx[4 * col + 3]);
-  float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-  float* base = state + ((int64_t)b * H + h) * (int64_t)M * N * P;
+  floatx4 acc = {0.f, 0.f, 0.f, 0.f};
+  float* base = state + ((int64_t)b * H + h) * (int64_t)M * N * P + 4 * col;
 
+  // rows rg, rg + RG, ... of the (m, n) row space; (m, n) of a row kept incrementally
   const int rows = (rg < RG) ? M * N : 0;  // threads beyond the last full row group idle
+  int m0 = 0, n0 = rg;
+  while (n0 >= N) {
+    n0 -= N;
+    ++m0;
+  }
   for (int r0 = rg; r0 < rows; r0 += RG * kDecodeUnroll) {
-    float4 s[kDecodeUnroll];
+    // the state is touched once per step: stream it past the caches
+    floatx4 s[kDecodeUnroll];
 #pragma unroll
     for (int u = 0; u < kDecodeUnroll; ++u) {
       const int row = r0 + u * RG;
-      if (row < rows) s[u] = *reinterpret_cast<const float4*>(base + (int64_t)row * P + 4 * col);
+      if (row < rows) s[u] = __builtin_nontemporal_load(reinterpret_cast<const floatx4*>(base + (int64_t)row * P));
     }
 #pragma unroll
     for (int u = 0; u < kDecodeUnroll; ++u) {
       const int row = r0 + u * RG;
       if (row < rows) {
-        const int m = row / N, n = row - m * N;
-        const float rho = s_rho[m];
-        const float kb = s_kap[m] * sB[n];
-        float4 v = s[u];
-        v.x = rho * v.x + kb * xv.x;
-        v.y = rho * v.y + kb * xv.y;
-        v.z = rho * v.z + kb * xv.z;
-        v.w = rho * v.w + kb * xv.w;
-        *reinterpret_cast<float4*>(base + (int64_t)row * P + 4 * col) = v;
-        const float cc = s_c[m] * sC[n];
-        acc.x += cc * v.x;
-        acc.y += cc * v.y;
-        acc.z += cc * v.z;
-        acc.w += cc * v.w;
+        const float rho = s_rho[m0];
+        const float kb = s_kap[m0] * sB[n0];
+        floatx4 v = s[u];
+        v[0] = rho * v[0] + kb * xv.x;
+        v[1] = rho * v[1] + kb * xv.y;
+        v[2] = rho * v[2] + kb * xv.z;
+        v[3] = rho * v[3] + kb * xv.w;
+        __builtin_nontemporal_store(v, reinterpret_cast<floatx4*>(base + (int64_t)row * P));
+        const float cc = s_c[m0] * sC[n0];
+        acc[0] += cc * v[0];
+        acc[1] += cc * v[1];
+        acc[2] += cc * v[2];
+        acc[3] += cc * v[3];
+      }
+      n0 += RG;
+      while (n0 >= N) {
+        n0 -= N;
+        ++m0;
       }
     }
   }
-  red[tid] = acc;
+  red[tid] = make_float4(acc[0], acc[1], acc[2], acc[3]);
   __syncthreads();
   if (tid < P4) {
     float4 sum = red[tid];

@@ -327,6 +327,25 @@ struct DmaPlan {
   }
 };
 
+// This lane's 4 io values of the C B^T tiles `wave` and `wave + 8` of one chunk
+// (10 lower-triangular 16x16 tiles of 256 values, lane-major), loaded one chunk
+// ahead of their use.
+template <typename T>
+struct TilePrefetch {
+  struct alignas(4 * sizeof(T)) V {
+    T e[4];
+  };
+  V v[2];
+  __device__ __forceinline__ void load(const T* chunk_tiles, int wave, int lane) {
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const int tile = wave + 8 * j;
+      if (tile < 10) v[j] = *reinterpret_cast<const V*>(chunk_tiles + tile * 256 + lane * 4);
+    }
+  }
+  __device__ __forceinline__ float get(int j, int r) const { return to_f32(v[j].e[r]); }
+};
+
 // Wait for this wave's outstanding vector-memory operations (including the
 // direct-to-LDS copies, which the compiler does not count).
 __device__ __forceinline__ void wait_vmem() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }

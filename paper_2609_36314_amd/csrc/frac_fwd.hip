@@ -120,7 +120,7 @@ __global__ void __launch_bounds__(256) frac_cb_kernel(ScanParams p, T* __restric
 // the LDS banks.  bfloat16 tiles are double-buffered: the next chunk is copied
 // in (direct global -> LDS) while the current one is computed.  The block is
 // always 8 waves: 4 blocks of 16 columns of P times 2 parts.
-template <typename T, int MP, int NB>
+template <typename T, int MP, int NB, int PS_ = (MP >= 8 ? 2 : 1)>
 struct FwdCfg {
   static constexpr int NP = NB * 16;
   static constexpr bool kBf16 = sizeof(T) == 2;
@@ -135,7 +135,7 @@ struct FwdCfg {
   // every wave holds at most 2 modes x all of N of state.  The 8 waves of a
   // workgroup are NPW blocks of 16 columns of P times NPART parts; the parts
   // split the modes (2 or more modes) or N (one mode).
-  static constexpr int PS = MP >= 8 ? 2 : 1;
+  static constexpr int PS = PS_;
   static constexpr int NPW = 4 / PS;
   static constexpr bool kModeSplit = MP >= 2;
   static constexpr int NPART = kModeSplit ? 8 / NPW : (NB >= 2 ? 2 : 1);
@@ -147,9 +147,9 @@ struct FwdCfg {
   static constexpr int TBP = (kBf16 ? MPW * NBW < 16 : MPW * NBW < 8) ? 4 : (kBf16 || MPW * NBW < 16) ? 2 : 1;
 };
 
-template <typename T, int MP, int NB>
+template <typename T, int MP, int NB, int PS>
 __global__ void __launch_bounds__(512) frac_fwd_kernel(ScanParams p, const T* __restrict__ gtiles) {
-  using Cfg = FwdCfg<T, MP, NB>;
+  using Cfg = FwdCfg<T, MP, NB, PS>;
   constexpr int NP = Cfg::NP, XS = Cfg::XS, BS = Cfg::BS, CS = Cfg::CS, GS = Cfg::GS;
   constexpr int NPART = Cfg::NPART, MPW = Cfg::MPW, NBW = Cfg::NBW, KBW = Cfg::KBW, TBP = Cfg::TBP;
   constexpr int NWT = 8;                  // waves in the workgroup
@@ -287,6 +287,8 @@ __global__ void __launch_bounds__(512) frac_fwd_kernel(ScanParams p, const T* __
 
   float dt_n, al_n, lam_n;
   load_controls(0, dt_n, al_n, lam_n);
+  TilePrefetch<T> gtile;  // C B^T tile values, loaded one chunk ahead
+  gtile.load(gtiles + ((int64_t)b * nchunks * G + g) * (kTiles * kTileElems), wave, lane);
   if (Cfg::NBUF == 2) stage(0, Xb0, Bb0, Cb0);
 
   // one chunk: Xc/Bc/Cc hold it (or receive it when single-buffered), Xn/Bn/Cn
@@ -361,12 +363,14 @@ __global__ void __launch_bounds__(512) frac_fwd_kernel(ScanParams p, const T* __
     __builtin_amdgcn_sched_barrier(0);
     // ---- ((C B^T) o Gamma)^T, lower-triangular 16x16 tiles split over the waves
     {
-      const T* gt = gtiles + (((int64_t)b * nchunks + c) * G + g) * (kTiles * kTileElems);
-      for (int tile = wave; tile < kTiles; tile += NWT) {
+#pragma unroll
+      for (int jt = 0; jt < 2; ++jt) {
+        const int tile = wave + NWT * jt;
+        if (tile >= kTiles) break;
         const int tb = kTileTB[tile], kb = kTileKB[tile];
         float Gt[4];
 #pragma unroll
-        for (int r = 0; r < 4; ++r) Gt[r] = to_f32(gt[tile * kTileElems + lane * 4 + r]);
+        for (int r = 0; r < 4; ++r) Gt[r] = gtile.get(jt, r);
         floatx4 Gm = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int q = 0; q < (MP + 3) / 4; ++q) {
@@ -397,6 +401,8 @@ __global__ void __launch_bounds__(512) frac_fwd_kernel(ScanParams p, const T* __
         for (int r = 0; r < 4; ++r) dst[r] = (T)gv[r];
       }
     }
+
+    if (c + 1 < nchunks) gtile.load(gtiles + (((int64_t)b * nchunks + c + 1) * G + g) * (kTiles * kTileElems), wave, lane);
 
     __builtin_amdgcn_sched_barrier(0);
     // ---- readout of the state entering the chunk, this wave's modes
@@ -570,8 +576,18 @@ hipError_t launch_fwd_variant(const ScanParams& p, void* ws, hipStream_t stream)
   T* gt = reinterpret_cast<T*>(ws);
   hipError_t e = launch_cb_variant<T, NB>(p, gt, stream);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((frac_fwd_kernel<T, MP, NB>), dim3(p.Bsz * p.H * FwdCfg<T, MP, NB>::PS), dim3(512), 0, stream, p,
-                     (const T*)gt);
+  // Few (batch, head) pairs (long single-sequence prefill): split the columns of P
+  // over two workgroups per head so that more of the 256 compute units have work.
+  const bool split = MP >= 8 || (MP >= 4 && p.Bsz * p.H < 192);
+  if (split) {
+    constexpr int PS = MP >= 4 ? 2 : 1;
+    hipLaunchKernelGGL((frac_fwd_kernel<T, MP, NB, PS>), dim3(p.Bsz * p.H * PS), dim3(512), 0, stream, p,
+                       (const T*)gt);
+  } else {
+    constexpr int PS = MP >= 8 ? 2 : 1;
+    hipLaunchKernelGGL((frac_fwd_kernel<T, MP, NB, PS>), dim3(p.Bsz * p.H * PS), dim3(512), 0, stream, p,
+                       (const T*)gt);
+  }
   return hipGetLastError();
 }
 
