@@ -25,8 +25,11 @@ slice of the same workload on the host cores.
 from __future__ import annotations
 
 import argparse
+import glob
+import hashlib
 import json
 import os
+import re
 import sys
 import time
 
@@ -198,6 +201,37 @@ def bench_decode(torch, frac, w, steps, warmup):
     }
 
 
+def kernel_source_digest():
+    """sha256 over the code (comments and blank lines stripped) of the HIP sources
+    and headers the library is built from."""
+    h = hashlib.sha256()
+    files = sorted(glob.glob(os.path.join(ROOT, "paper_2609_36314_amd", "csrc", "*")))
+    files += sorted(glob.glob(os.path.join(ROOT, "include", "*.h")))
+    for f in files:
+        with open(f, encoding="utf-8") as fh:
+            src = re.sub(r"/\*.*?\*/", "", fh.read(), flags=re.S)
+        code = [ln.split("//")[0].rstrip() for ln in src.splitlines()]
+        h.update(os.path.basename(f).encode())
+        h.update("\n".join(ln for ln in code if ln).encode())
+    return h.hexdigest()
+
+
+def measured_traffic(entry, workload):
+    """HBM bytes per launch of `entry` on `workload` from the committed counter summary
+    (FETCH_SIZE scaled by the copy calibration, plus WRITE_SIZE), or None when the
+    kernels have changed since the counters were taken."""
+    path = os.path.join(ROOT, "profiles", "hbm_traffic_%s_%s.md" % (entry, workload))
+    if not os.path.exists(path):
+        return None
+    m = re.search(r"^traffic: (\{.*\})\s*$", open(path).read(), re.M)
+    if not m:
+        return None
+    rec = json.loads(m.group(1))
+    if rec.get("source_sha256") != kernel_source_digest():
+        return None
+    return float(rec["bytes_per_launch"])
+
+
 def roofline(bound, work, ms, peak, unit):
     rate = work / (ms * 1e-3)
     scale = 1e12 if unit == "TFLOP/s" else 1e9
@@ -266,7 +300,7 @@ def main():
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": mres["ms_per_step"] if mres else None,
+        "ms_per_step": (mres.get("ms_per_step", mres.get("us_per_step", 0.0) * 1e-3)) if mres else None,
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -281,10 +315,15 @@ def main():
         if "bwd_roofline" in mres:
             # the dominant entry point of the step: frac_scan_bwd (C B^T tiles, state / row / column
             # sweeps, ddt suffix sums, group sum of dB and dC), one launch per step
-            line["roofline"] = dict(mres["bwd_roofline"], kernel="frac_scan_bwd")
+            line["roofline"] = dict(mres["bwd_roofline"], kernel="frac_scan_bwd",
+                                    traffic=measured_traffic("frac_scan_bwd", main_w.name))
             line["step_roofline"] = dict(mres["fwd_bwd_roofline"], kernel="frac_scan_fwd + frac_scan_bwd")
+        elif "roofline" in mres:
+            line["roofline"] = dict(mres["roofline"], kernel="frac_decode_step",
+                                    traffic=measured_traffic("frac_decode_step", main_w.name))
         else:
-            line["roofline"] = dict(mres["fwd_roofline"], kernel="frac_scan_fwd")
+            line["roofline"] = dict(mres["fwd_roofline"], kernel="frac_scan_fwd",
+                                    traffic=measured_traffic("frac_scan_fwd", main_w.name))
     line["workloads"] = results
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(main_w, args.cpu_sample_heads, args.cpu_sample_batch)

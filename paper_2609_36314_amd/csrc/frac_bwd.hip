@@ -620,11 +620,16 @@ __global__ void __launch_bounds__(512) frac_bwd_state_kernel(ScanParams p, BwdWo
         wk.fA[ps * bl_h + ith] = ef;
       }
     }
-    if (ps == 0) {
-      // sum(dy . x) of the chunk for dD (fixed element assignment per thread)
-      for (int i = tid; i < kQ * 64; i += 512) {
-        const int t = i >> 6, pc = i & 63;
-        if (t < nv) dd_acc += to_f32(Xc[t * XS + pc]) * to_f32(Yc[t * XS + pc]);
+    if (ps == 0 && p.dD) {
+      // sum(dy . x) of the chunk for dD: 8 consecutive columns of one token per
+      // thread (columns past P hold zeros)
+      const int t = tid >> 3, c8 = (tid & 7) * 8;
+      if (t < nv) {
+        float xv[8], yv[8];
+        load8(Xc + t * XS + c8, xv);
+        load8(Yc + t * XS + c8, yv);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) dd_acc += xv[j] * yv[j];
       }
     }
     if (!active) return;

@@ -219,17 +219,36 @@ __device__ __forceinline__ void softmax_fast(float* z, int M) {
   for (int m = 0; m < MP; ++m) z[m] *= inv;
 }
 
+// One DPP row permutation of a float (every lane of the wave active).
+template <int CTRL>
+__device__ __forceinline__ float dpp_move(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xF, 0xF, true));
+}
+
+// op over each aligned group of G consecutive lanes (G a power of two <= 64),
+// returned in every lane of the group, bit-identical across the group.  Groups
+// up to 16 lanes use DPP: swap neighbours, swap pairs (quad permutations), then
+// pair each lane with its mirror in the 8- and 16-lane rows, which at that point
+// belongs to the other half and already holds that half's result.
+template <int G, typename Op>
+__device__ __forceinline__ float group_allreduce(float v, Op op) {
+  if constexpr (G >= 2) v = op(v, dpp_move<0xB1>(v));   // quad_perm [1, 0, 3, 2]
+  if constexpr (G >= 4) v = op(v, dpp_move<0x4E>(v));   // quad_perm [2, 3, 0, 1]
+  if constexpr (G >= 8) v = op(v, dpp_move<0x141>(v));  // row_half_mirror
+  if constexpr (G >= 16) v = op(v, dpp_move<0x140>(v)); // row_mirror
+  if constexpr (G >= 32) v = op(v, __shfl_xor(v, 16, 64));
+  if constexpr (G >= 64) v = op(v, __shfl_xor(v, 32, 64));
+  return v;
+}
+
 // softmax across the MP consecutive lanes that hold the modes of one token (MP a
-// power of two dividing 64, lane = token * MP + mode); -inf entries get weight 0.
+// power of two dividing 64, lane = token * MP + mode, the whole wave active);
+// -inf entries get weight 0.
 template <int MP>
 __device__ __forceinline__ float group_softmax(float z) {
-  float mx = z;
-#pragma unroll
-  for (int o = 1; o < MP; o <<= 1) mx = fmaxf(mx, __shfl_xor(mx, o, 64));
+  const float mx = group_allreduce<MP>(z, [](float a, float b) { return fmaxf(a, b); });
   const float e = __expf(z - mx);
-  float sum = e;
-#pragma unroll
-  for (int o = 1; o < MP; o <<= 1) sum += __shfl_xor(sum, o, 64);
+  const float sum = group_allreduce<MP>(e, [](float a, float b) { return a + b; });
   return e * __frcp_rn(sum);
 }
 

@@ -20,19 +20,25 @@
 //   frac_cb_kernel   G_chunk = C B^T (Q x Q, causal 16x16 tiles) once per
 //                    (batch, chunk, group) -- shared by every head of the group --
 //                    stored in the per-lane fragment order the scan reads back.
-//   frac_fwd_kernel  one workgroup per (batch, head).  Wave (pb, nh) owns state
-//                    columns p in [16 pb, 16 pb + 16) and, when N >= 32, one half
-//                    of the N rows, for every mode.  Its share of the float32
-//                    M x N x P state lives in matrix-core accumulator registers
-//                    for the whole sequence and never touches memory.  Per chunk:
-//                    stage x (transposed), B (transposed) and C in LDS; per-token
-//                    controls and weights (lane = token); (G o Gamma) tiles split
-//                    over the waves; readout, intra-chunk product and state update
-//                    as 16x16x32 matrix-core products (bfloat16 operands, float32
-//                    accumulation).  The accumulator tiles of the state are
-//                    converted in registers straight into B operands of the
-//                    readout: their row order becomes the K-slot order, matched by
-//                    the order in which C is read from LDS.
+//   frac_fwd_kernel  one workgroup of 8 waves per (batch, head), or two per
+//                    (batch, head) splitting the columns of P when there are 8
+//                    modes or too few heads to fill the chip.  Each wave owns a
+//                    16-column block of P and either a share of the modes (two or
+//                    more modes; it then holds all N rows of its modes) or half of
+//                    N (one mode).  Its share of the float32 M x N x P state lives
+//                    in matrix-core accumulator registers for the whole sequence
+//                    and never touches memory.  Per chunk: x, B and C are copied
+//                    straight into LDS (double-buffered for bfloat16, the next
+//                    chunk's copy in flight during this chunk's products);
+//                    per-token controls and per-(token, mode) weights (lane =
+//                    token); (G o Gamma) tiles split over the waves; readout,
+//                    intra-chunk product and state update as 16x16x32 matrix-core
+//                    products (bfloat16 operands, float32 accumulation).  The
+//                    accumulator tiles of the state are converted in registers
+//                    straight into B operands of the readout: their row order
+//                    becomes the K-slot order, matched by the order in which C is
+//                    read from LDS.  Waves that split the modes add their partial
+//                    outputs through LDS exchange slots before y is stored.
 //
 // Gamma uses the factorised form (c e^{-r A_t}) (kappa e^{r A_k}) through a float32
 // 16x16x4 product with the modes as K, for every mode whose chunk decay r_m A_Q
