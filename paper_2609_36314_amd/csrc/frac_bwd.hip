@@ -196,8 +196,8 @@ __device__ __forceinline__ int pair_weights(const ChunkCtl& k, int t0, int nv, i
 // Rank-M product sum_m a[m][row0 + i] b[m][col0 + j] over a 16x16 tile
 // (float32 matrix cores, modes as K), in the accumulator layout.
 template <int MP>
-__device__ __forceinline__ floatx4 rank_m_tile(const float* a, const float* bm, int row0, int col0) {
-  const int li = threadIdx.x & 15, lg = (threadIdx.x >> 4) & 3;
+__device__ __forceinline__ floatx4 rank_m_tile(const float* a, const float* bm, int row0, int col0, int tid = threadIdx.x) {
+  const int li = tid & 15, lg = (tid >> 4) & 3;
   floatx4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
   for (int q = 0; q < (MP + 3) / 4; ++q) {
@@ -213,8 +213,8 @@ __device__ __forceinline__ floatx4 rank_m_tile(const float* a, const float* bm, 
 // sum_m a_m[t] b_m[k] s_m e^{-r_m (A_t - A_k)} (t >= k) to a 16x16 tile.
 template <int MP>
 __device__ __forceinline__ void unsafe_terms(floatx4& acc, int unsafe, const float* a, const float* bm, const float* A,
-                                             const float* s_rr, int tb, int kb, bool scale_r) {
-  const int li = threadIdx.x & 15, lg = (threadIdx.x >> 4) & 3;
+                                             const float* s_rr, int tb, int kb, bool scale_r, int tid = threadIdx.x) {
+  const int li = tid & 15, lg = (tid >> 4) & 3;
   for (int m = 0; m < MP; ++m) {
     if (!((unsafe >> m) & 1)) continue;
     const float rm = s_rr[m];
@@ -228,8 +228,8 @@ __device__ __forceinline__ void unsafe_terms(floatx4& acc, int unsafe, const flo
 
 // dY X^T tile (rows tb, cols kb), K over the 64 columns of P, from natural tiles.
 template <typename T, int XS>
-__device__ __forceinline__ floatx4 dyx_tile(const T* Ys, const T* Xs, int tb, int kb) {
-  const int li = threadIdx.x & 15, lg = (threadIdx.x >> 4) & 3;
+__device__ __forceinline__ floatx4 dyx_tile(const T* Ys, const T* Xs, int tb, int kb, int tid = threadIdx.x) {
+  const int li = tid & 15, lg = (tid >> 4) & 3;
   floatx4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
   for (int kp = 0; kp < 2; ++kp) {
@@ -460,6 +460,8 @@ __global__ void __launch_bounds__(512) frac_bwd_state_kernel(ScanParams p, BwdWo
 
   auto step = [&](int c, T* Xc, T* Yc, T* Bc, T* Xn, T* Yn, T* Bn) __attribute__((always_inline)) {
     const int t0 = c * kQ, nv = min(kQ, L - t0);
+    // lane-derived addresses recomputed per chunk rather than held across the loop
+    const int tid = fresh_tid(), lane = tid & 63, li = lane & 15, lg = lane >> 4;
     const float* Ecur = s_E2 + (c & 1) * MP;
     float* Enext = s_E2 + ((c + 1) & 1) * MP;
     wait_vmem();
@@ -496,9 +498,9 @@ __global__ void __launch_bounds__(512) frac_bwd_state_kernel(ScanParams p, BwdWo
         const int tile = wave + 8 * jt;
         if (tile >= kTiles) break;
         const int tb = kTB[tile], kb = kKB[tile];
-        const floatx4 D = dyx_tile<T, XS>(Yc, Xc, tb, kb);
-        floatx4 Gm = rank_m_tile<MP>(P_O, P_Vt, tb * 16, kb * 16);
-        if (unsafe) unsafe_terms<MP>(Gm, unsafe, P_c, P_k, P_A, s_rr, tb, kb, false);
+        const floatx4 D = dyx_tile<T, XS>(Yc, Xc, tb, kb, tid);
+        floatx4 Gm = rank_m_tile<MP>(P_O, P_Vt, tb * 16, kb * 16, tid);
+        if (unsafe) unsafe_terms<MP>(Gm, unsafe, P_c, P_k, P_A, s_rr, tb, kb, false, tid);
         float hv[4];
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
@@ -509,11 +511,11 @@ __global__ void __launch_bounds__(512) frac_bwd_state_kernel(ScanParams p, BwdWo
 #pragma unroll
         for (int r = 0; r < 4; ++r) dst[r] = (T)hv[r];
         if (tile % Cfg::PS == ps) {  // the two halves of N share the tile sums
-          floatx4 Ph = rank_m_tile<MP>(P_rO, P_Vt, tb * 16, kb * 16);
-          floatx4 Ps = rank_m_tile<MP>(P_O, P_Y, tb * 16, kb * 16);
+          floatx4 Ph = rank_m_tile<MP>(P_rO, P_Vt, tb * 16, kb * 16, tid);
+          floatx4 Ps = rank_m_tile<MP>(P_O, P_Y, tb * 16, kb * 16, tid);
           if (unsafe) {
-            unsafe_terms<MP>(Ph, unsafe, P_c, P_k, P_A, s_rr, tb, kb, true);
-            unsafe_terms<MP>(Ps, unsafe, P_c, P_wr, P_A, s_rr, tb, kb, false);
+            unsafe_terms<MP>(Ph, unsafe, P_c, P_k, P_A, s_rr, tb, kb, true, tid);
+            unsafe_terms<MP>(Ps, unsafe, P_c, P_wr, P_A, s_rr, tb, kb, false, tid);
           }
           float rv[4], ce = 0.f, cf = 0.f;
 #pragma unroll
@@ -642,8 +644,8 @@ __global__ void __launch_bounds__(512) frac_bwd_state_kernel(ScanParams p, BwdWo
       if (Cfg::NACT > 1) Ex::gather(XCH, part, tb, dCa[tb], [&](int q) { return q * NBF + nbl; });
 #pragma unroll
       for (int kk = 0; kk <= tb / 2; ++kk) {
-        const Frag<T> a = frag_load_rows(Bc, BS, kk * 32 + lg * 8, nb * 16);
-        const Frag<T> bb = frag_load_rows(HGT, XS, kk * 32 + lg * 8, tb * 16);
+        const Frag<T> a = frag_load_rows(Bc, BS, kk * 32 + lg * 8, nb * 16, tid);
+        const Frag<T> bb = frag_load_rows(HGT, XS, kk * 32 + lg * 8, tb * 16, tid);
         mma(dCa[tb], a, bb);
       }
       // per-head partial: token t = 16 tb + li, columns n .. n+3 (32-bit offsets from the chunk)
@@ -665,8 +667,8 @@ __global__ void __launch_bounds__(512) frac_bwd_state_kernel(ScanParams p, BwdWo
     for (int kt = 0; kt < 2; ++kt) {
       Frag<T> Xa[4];
 #pragma unroll
-      for (int pb = 0; pb < 4; ++pb) Xa[pb] = frag_load_rows(Xc, XS, kt * 32 + lg * 8, pb * 16);
-      const Frag<T> bf = frag_load_rows(Bc, BS, kt * 32 + lg * 8, nb * 16);
+      for (int pb = 0; pb < 4; ++pb) Xa[pb] = frag_load_rows(Xc, XS, kt * 32 + lg * 8, pb * 16, tid);
+      const Frag<T> bf = frag_load_rows(Bc, BS, kt * 32 + lg * 8, nb * 16, tid);
       float b8[8];
 #pragma unroll
       for (int s = 0; s < 8; ++s) b8[s] = to_f32(bf.v[s]);

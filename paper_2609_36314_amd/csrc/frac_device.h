@@ -252,6 +252,15 @@ __device__ __forceinline__ float group_softmax(float z) {
   return e * __frcp_rn(sum);
 }
 
+// The thread index behind an empty asm statement: values derived from it inside
+// a loop body are recomputed there instead of being hoisted out of the loop and
+// held (or spilled) for its whole duration.
+__device__ __forceinline__ int fresh_tid() {
+  int t = threadIdx.x;
+  asm volatile("" : "+v"(t));
+  return t;
+}
+
 // ------------------------------------------------ LDS fragment reads (K = rows)
 
 typedef short v4i16 __attribute__((ext_vector_type(4)));
@@ -262,8 +271,8 @@ typedef short v4i16 __attribute__((ext_vector_type(4)));
 // addresses 4 consecutive elements of row row0 + i/4 at column col0 + 4 (i % 4),
 // and lane j receives column col0 + j of the 4 rows.  row0 may differ between
 // the 16-lane groups.
-__device__ __forceinline__ Frag<bf16> frag_load_rows(const bf16* m, int ld, int row0, int col0) {
-  const int li = threadIdx.x & 15;
+__device__ __forceinline__ Frag<bf16> frag_load_rows(const bf16* m, int ld, int row0, int col0, int tid = threadIdx.x) {
+  const int li = tid & 15;
   const bf16* p = m + (row0 + (li >> 2)) * ld + col0 + 4 * (li & 3);
   const v4i16 a = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) v4i16*)(p));
   const v4i16 b = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) v4i16*)(p + 4 * ld));
@@ -273,8 +282,8 @@ __device__ __forceinline__ Frag<bf16> frag_load_rows(const bf16* m, int ld, int 
   f.v = __builtin_bit_cast(bf16x8, ab);
   return f;
 }
-__device__ __forceinline__ Frag<float> frag_load_rows(const float* m, int ld, int row0, int col0) {
-  const int li = threadIdx.x & 15;
+__device__ __forceinline__ Frag<float> frag_load_rows(const float* m, int ld, int row0, int col0, int tid = threadIdx.x) {
+  const int li = tid & 15;
   Frag<float> f;
 #pragma unroll
   for (int s = 0; s < 8; ++s) f.v[s] = m[(row0 + s) * ld + col0 + li];
@@ -283,16 +292,16 @@ __device__ __forceinline__ Frag<float> frag_load_rows(const float* m, int ld, in
 
 // Four consecutive rows row0..row0+3 of column col0 + (lane % 16), as floats
 // (one transposed read for bfloat16).
-__device__ __forceinline__ void col4_rows(const bf16* m, int ld, int row0, int col0, float* out) {
-  const int li = threadIdx.x & 15;
+__device__ __forceinline__ void col4_rows(const bf16* m, int ld, int row0, int col0, float* out, int tid = threadIdx.x) {
+  const int li = tid & 15;
   const bf16* p = m + (row0 + (li >> 2)) * ld + col0 + 4 * (li & 3);
   const v4i16 a = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) v4i16*)(p));
   const bf16x4 v = __builtin_bit_cast(bf16x4, a);
 #pragma unroll
   for (int s = 0; s < 4; ++s) out[s] = (float)v[s];
 }
-__device__ __forceinline__ void col4_rows(const float* m, int ld, int row0, int col0, float* out) {
-  const int li = threadIdx.x & 15;
+__device__ __forceinline__ void col4_rows(const float* m, int ld, int row0, int col0, float* out, int tid = threadIdx.x) {
+  const int li = tid & 15;
 #pragma unroll
   for (int s = 0; s < 4; ++s) out[s] = m[(row0 + s) * ld + col0 + li];
 }
