@@ -348,15 +348,20 @@ __global__ void __launch_bounds__(512) frac_bwd_state_kernel(ScanParams p, BwdWo
   __shared__ __align__(16) T Cb[64 * CS];
   constexpr int NWA = n_weight_arrays<kState>();
   constexpr int oHG = 0;                                         // T [k][t] (Gamma o dY X^T)^T, causal
-  constexpr int oW = oHG + 64 * XS * (int)sizeof(T);             // float weights [NWA][MP][Q], A [Q]
-  constexpr int oSl = oW + (NWA * MP * kQ + kQ) * 4;             // float slots R, C, F [10][16] each
+  constexpr int WSZ = NWA * MP * kQ + kQ;                        // one chunk's weights [NWA][MP][Q], A [Q]
+  // two chunks' weights (the next one formed during this one's update) when LDS allows
+  constexpr int kTileBytes = (Cfg::NBUF * 64 * (2 * XS + BS) + 64 * CS) * (int)sizeof(T);
+  constexpr int kFixed = 64 * XS * (int)sizeof(T) + (3 * kTiles * 16 + 8 * kQ + Ex::kFloats + 4 * MP) * 4;
+  constexpr int NWB = kTileBytes + kFixed + 2 * WSZ * 4 <= 160 * 1024 - 512 ? 2 : 1;
+  constexpr int oW = oHG + 64 * XS * (int)sizeof(T);             // float weights, NWB chunks
+  constexpr int oSl = oW + NWB * WSZ * 4;                        // float slots R, C, F [10][16] each
   constexpr int oRd = oSl + 3 * kTiles * 16 * 4;                 // float [8][Q] per-wave token partials
   constexpr int oEx = oRd + 8 * kQ * 4;                          // float exchange
   constexpr int oSc = oEx + Ex::kFloats * 4;                     // float rates, log tau, scales
   __shared__ __align__(16) unsigned char sm[oSc + 4 * MP * 4];
   T* HGT = reinterpret_cast<T*>(sm + oHG);
-  float* W = reinterpret_cast<float*>(sm + oW);
-  float* P_A = W + NWA * MP * kQ;
+  float* const W0 = reinterpret_cast<float*>(sm + oW);
+  float* const W1 = W0 + (NWB - 1) * WSZ;
   float* slotR = reinterpret_cast<float*>(sm + oSl);
   float* slotC = slotR + kTiles * 16;
   float* slotF = slotC + kTiles * 16;
@@ -366,15 +371,6 @@ __global__ void __launch_bounds__(512) frac_bwd_state_kernel(ScanParams p, BwdWo
   float* s_lnt = s_rr + MP;
   float* s_E2 = s_lnt + MP;
   constexpr int SW = MP * kQ;  // stride of the weight arrays
-  const float* P_O = W;
-  const float* P_Vt = W + 1 * SW;
-  const float* P_rO = W + 2 * SW;
-  const float* P_Y = W + 3 * SW;
-  const float* P_wdc = W + 4 * SW;  // times r_m: the readout weight of e
-  const float* P_v = W + 5 * SW;
-  const float* P_c = W + 6 * SW;
-  const float* P_k = W + 7 * SW;
-  const float* P_wr = W + 8 * SW;
 
   if (tid < MP) {
     const float tau = (tid < M) ? p.tau[tid] : 1.0f;
@@ -458,14 +454,40 @@ __global__ void __launch_bounds__(512) frac_bwd_state_kernel(ScanParams p, BwdWo
   T* dCp = reinterpret_cast<T*>(wk.dCp);
   const int64_t bl_h = (int64_t)p.Bsz * L * H;
 
-  auto step = [&](int c, T* Xc, T* Yc, T* Bc, T* Xn, T* Yn, T* Bn) __attribute__((always_inline)) {
+  // Per-(token, mode) weights of chunk c into Wd, from the controls in dt_n, al_n,
+  // lam_n.  Chunk c + 1's weights are formed at the end of chunk c's step, so that
+  // their latency overlaps that step's state update.
+  float alast_c = 0.0f;  // chunk total of the effective steps
+  int unsafe_c = 0;      // modes past the factorisation bound
+  auto weights = [&](int c, float* Wd) __attribute__((always_inline)) {
+    const int t0 = c * kQ, nv = min(kQ, L - t0);
+    const ChunkCtl k = chunk_controls(dt_n, al_n, lam_n, lm_bh != nullptr, nv);
+    if (wave == 0) Wd[NWA * MP * kQ + lane] = k.A;
+    unsafe_c = pair_weights<MP, kState>(k, t0, nv, M, rl_bh, wl_bh, lg_st, s_rr, s_lnt, s_E2 + (c & 1) * MP,
+                                        s_E2 + ((c + 1) & 1) * MP, Wd);
+    alast_c = k.Alast;
+  };
+  barrier();  // rates and scales in LDS
+  if constexpr (NWB == 2) weights(0, W0);
+
+  auto step = [&](int c, T* Xc, T* Yc, T* Bc, T* Xn, T* Yn, T* Bn, float* W, float* Wn)
+                  __attribute__((always_inline)) {
     const int t0 = c * kQ, nv = min(kQ, L - t0);
     // lane-derived addresses recomputed per chunk rather than held across the loop
     const int tid = fresh_tid(), lane = tid & 63, li = lane & 15, lg = lane >> 4;
     const float* Ecur = s_E2 + (c & 1) * MP;
-    float* Enext = s_E2 + ((c + 1) & 1) * MP;
+    const float* P_O = W;
+    const float* P_Vt = W + 1 * SW;
+    const float* P_rO = W + 2 * SW;
+    const float* P_Y = W + 3 * SW;
+    const float* P_wdc = W + 4 * SW;  // times r_m: the readout weight of e
+    const float* P_v = W + 5 * SW;
+    const float* P_c = W + 6 * SW;
+    const float* P_k = W + 7 * SW;
+    const float* P_wr = W + 8 * SW;
+    const float* P_A = W + NWA * MP * kQ;
     wait_vmem();
-    barrier();  // this chunk's tiles have landed; the previous chunk is done
+    barrier();  // this chunk's tiles and weights have landed; the previous chunk is done
     if (Cfg::NBUF == 2) {
       if (c + 1 < nchunks) stage(c + 1, Xn, Yn, Bn);
     } else {
@@ -474,20 +496,18 @@ __global__ void __launch_bounds__(512) frac_bwd_state_kernel(ScanParams p, BwdWo
       wait_vmem();
       barrier();
     }
-    const float dtv = dt_n, al_l = al_n, lam_l = lam_n;
+    if constexpr (NWB == 1) weights(c, W);
     if (c + 1 < nchunks) load_controls(c + 1, dt_n, al_n, lam_n);
-    const ChunkCtl k = chunk_controls(dtv, al_l, lam_l, lm_bh != nullptr, nv);
-    if (wave == 0) P_A[lane] = k.A;
-    const int unsafe = pair_weights<MP, kState>(k, t0, nv, M, rl_bh, wl_bh, lg_st, s_rr, s_lnt, Ecur, Enext, W);
+    if constexpr (NWB == 1) barrier();  // weights in LDS
+    const int unsafe = unsafe_c;
     float renf[MPF];
     int renbits = 0;
 #pragma unroll
     for (int m = 0; m < MPF; ++m) {
-      const float Enew = uniform(Ecur[mo + m] * fexp(-s_rr[mo + m] * k.Alast));
+      const float Enew = uniform(Ecur[mo + m] * fexp(-s_rr[mo + m] * alast_c));
       renf[m] = Enew;
       if (__float_as_int(Enew) < __float_as_int(kRescaleFloor)) renbits |= 1 << m;
     }
-    barrier();  // weights in LDS
 
     __builtin_amdgcn_sched_barrier(0);
     // ---- intra-chunk tiles: HG = Gamma o D (LDS, transposed), row / column sums of
@@ -634,7 +654,7 @@ __global__ void __launch_bounds__(512) frac_bwd_state_kernel(ScanParams p, BwdWo
         for (int j = 0; j < 8; ++j) dd_acc += xv[j] * yv[j];
       }
     }
-    if (!active) return;
+    if (active) {  // waves holding state
 
     __builtin_amdgcn_sched_barrier(0);
     // ---- dC^T blocks this wave finishes: other parts + intra B^T (Gamma o dY X^T)^T, causal
@@ -690,13 +710,17 @@ __global__ void __launch_bounds__(512) frac_bwd_state_kernel(ScanParams p, BwdWo
         for (int pb = 0; pb < 4; ++pb) mma(S[m][pb], Xa[pb], Bv);
       }
     }
+    }  // active
+    if constexpr (NWB == 2) {
+      if (c + 1 < nchunks) weights(c + 1, Wn);
+    }
   };
 
   for (int c = 0; c < nchunks; c += 2) {
-    step(c, Xb0, Yb0, Bb0, Xb1, Yb1, Bb1);
+    step(c, Xb0, Yb0, Bb0, Xb1, Yb1, Bb1, W0, W1);
     if (c + 1 < nchunks) {
-      if (Cfg::NBUF == 2) step(c + 1, Xb1, Yb1, Bb1, Xb0, Yb0, Bb0);
-      else step(c + 1, Xb0, Yb0, Bb0, Xb0, Yb0, Bb0);
+      if (Cfg::NBUF == 2) step(c + 1, Xb1, Yb1, Bb1, Xb0, Yb0, Bb0, W1, W0);
+      else step(c + 1, Xb0, Yb0, Bb0, Xb0, Yb0, Bb0, W1, W0);
     }
   }
   wait_vmem();
