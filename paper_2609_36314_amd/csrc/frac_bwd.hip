@@ -59,23 +59,26 @@ __device__ __forceinline__ float uniform(float v) {
 }
 
 // Sum over the 16 lanes of a lane group of v[r] (r = 0..3); returned in every
-// lane whose index within the group has ((li >> 2) & 3) == r.
+// lane whose index within the group has ((li >> 2) & 3) == r.  Each step pairs a
+// lane with one whose index differs in the step's bit: the mirror lane in the
+// 16-lane row (li ^ 15), the mirror in the 8-lane half (li ^ 7), then li ^ 2 and
+// li ^ 1, all DPP row permutations; the pairs reached cover the 16 lanes.
 __device__ __forceinline__ float reduce16_4(float v[4], int li) {
 #pragma unroll
   for (int j = 0; j < 2; ++j) {
     const bool hi = li & 8;
     const float send = hi ? v[j] : v[j + 2];
     const float keep = hi ? v[j + 2] : v[j];
-    v[j] = keep + __shfl_xor(send, 8, 64);
+    v[j] = keep + dpp_move<0x140>(send);  // row_mirror
   }
   {
     const bool hi = li & 4;
     const float send = hi ? v[0] : v[1];
     const float keep = hi ? v[1] : v[0];
-    v[0] = keep + __shfl_xor(send, 4, 64);
+    v[0] = keep + dpp_move<0x141>(send);  // row_half_mirror
   }
-  v[0] += __shfl_xor(v[0], 2, 64);
-  v[0] += __shfl_xor(v[0], 1, 64);
+  v[0] += dpp_move<0x4E>(v[0]);  // quad_perm [2, 3, 0, 1]
+  v[0] += dpp_move<0xB1>(v[0]);  // quad_perm [1, 0, 3, 2]
   return v[0];
 }
 
@@ -112,7 +115,7 @@ __device__ __forceinline__ ChunkCtl chunk_controls(float dtv, float al, float la
   const float s_eff = has_lambda ? exp2f(log2f(lam) / al) : 1.0f;
   k.dtt = (lane < nv) ? dtv * s_eff : 0.0f;
   k.A = wave_inclusive_sum(k.dtt);
-  k.Alast = uniform(__shfl(k.A, 63, 64));
+  k.Alast = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(k.A), 63));
   k.al = al;
   return k;
 }
@@ -548,10 +551,8 @@ __global__ void __launch_bounds__(512) frac_bwd_state_kernel(ScanParams p, BwdWo
           }
           const float rs = reduce16_4(rv, li);
           if ((li & 3) == 0) slotR[tile * 16 + lg * 4 + ((li >> 2) & 3)] = rs;
-          ce += __shfl_xor(ce, 16, 64);
-          ce += __shfl_xor(ce, 32, 64);
-          cf += __shfl_xor(cf, 16, 64);
-          cf += __shfl_xor(cf, 32, 64);
+          ce = xor32_sum(xor16_sum(ce));
+          cf = xor32_sum(xor16_sum(cf));
           if (lg == 0) {
             slotC[tile * 16 + li] = ce;
             slotF[tile * 16 + li] = cf;
@@ -611,8 +612,7 @@ __global__ void __launch_bounds__(512) frac_bwd_state_kernel(ScanParams p, BwdWo
 #pragma unroll
       for (int tb = 0; tb < 4; ++tb) {
         float v = racc[tb];
-        v += __shfl_xor(v, 16, 64);
-        v += __shfl_xor(v, 32, 64);
+        v = xor32_sum(xor16_sum(v));
         if (lg == 0) redR[wave * kQ + tb * 16 + li] = v;
       }
     }
@@ -1295,10 +1295,8 @@ __global__ void __launch_bounds__(512) frac_bwd_rows_kernel(ScanParams p, BwdWor
 #pragma unroll
       for (int tb = 0; tb < 4; ++tb) {
         float e = ekf[tb], f = fkf[tb];
-        e += __shfl_xor(e, 16, 64);
-        e += __shfl_xor(e, 32, 64);
-        f += __shfl_xor(f, 16, 64);
-        f += __shfl_xor(f, 32, 64);
+        e = xor32_sum(xor16_sum(e));
+        f = xor32_sum(xor16_sum(f));
         if (lg == 0) {
           redE[wave * kQ + tb * 16 + li] = e;
           redF[wave * kQ + tb * 16 + li] = f;

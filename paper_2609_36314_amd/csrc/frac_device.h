@@ -149,13 +149,27 @@ __device__ __forceinline__ void zero8(T* dst) {
 
 // Inclusive prefix sum over the 64 lanes of a wave (Hillis-Steele, fixed order).
 __device__ __forceinline__ float wave_inclusive_sum(float v) {
-  const int lane = threadIdx.x & 63;
-#pragma unroll
-  for (int off = 1; off < 64; off <<= 1) {
-    const float o = __shfl_up(v, off, 64);
-    if (lane >= off) v += o;
-  }
+  // within each row of 16 lanes: add the lanes 1, 2, 4, 8 places lower (zero past
+  // the row start); then the last lane of row 0 (2) into row 1 (3), and lane 31
+  // into rows 2 and 3
+  v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x111, 0xF, 0xF, true));  // row_shr:1
+  v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x112, 0xF, 0xF, true));  // row_shr:2
+  v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x114, 0xF, 0xF, true));  // row_shr:4
+  v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x118, 0xF, 0xF, true));  // row_shr:8
+  v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x142, 0xA, 0xF, false)); // row_bcast:15
+  v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x143, 0xC, 0xF, false)); // row_bcast:31
   return v;
+}
+
+// v plus the value of lane ^ 16 (lane ^ 32): the two halves exchanged with one
+// cross-row swap, the sum formed in the same order in both lanes.
+__device__ __forceinline__ float xor16_sum(float v) {
+  const auto s = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return __uint_as_float(s[0]) + __uint_as_float(s[1]);
+}
+__device__ __forceinline__ float xor32_sum(float v) {
+  const auto s = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return __uint_as_float(s[0]) + __uint_as_float(s[1]);
 }
 
 // ------------------------------------------------------- per-token controls
@@ -229,15 +243,22 @@ __device__ __forceinline__ float dpp_move(float v) {
 // returned in every lane of the group, bit-identical across the group.  Groups
 // up to 16 lanes use DPP: swap neighbours, swap pairs (quad permutations), then
 // pair each lane with its mirror in the 8- and 16-lane rows, which at that point
-// belongs to the other half and already holds that half's result.
+// belongs to the other half and already holds that half's result; wider groups
+// swap rows.
 template <int G, typename Op>
 __device__ __forceinline__ float group_allreduce(float v, Op op) {
   if constexpr (G >= 2) v = op(v, dpp_move<0xB1>(v));   // quad_perm [1, 0, 3, 2]
   if constexpr (G >= 4) v = op(v, dpp_move<0x4E>(v));   // quad_perm [2, 3, 0, 1]
   if constexpr (G >= 8) v = op(v, dpp_move<0x141>(v));  // row_half_mirror
   if constexpr (G >= 16) v = op(v, dpp_move<0x140>(v)); // row_mirror
-  if constexpr (G >= 32) v = op(v, __shfl_xor(v, 16, 64));
-  if constexpr (G >= 64) v = op(v, __shfl_xor(v, 32, 64));
+  if constexpr (G >= 32) {  // the lane 16 places away, through a cross-row swap
+    const auto s = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    v = op(__uint_as_float(s[0]), __uint_as_float(s[1]));
+  }
+  if constexpr (G >= 64) {
+    const auto s = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    v = op(__uint_as_float(s[0]), __uint_as_float(s[1]));
+  }
   return v;
 }
 

@@ -321,7 +321,7 @@ __global__ void __launch_bounds__(512) frac_fwd_kernel(ScanParams p, const T* __
     const float s_eff_l = lm_bh ? exp2f(log2f(lam_l) / al_l) : 1.0f;
     const float dtt_l = (lane < nv) ? dtv * s_eff_l : 0.0f;
     const float A_l = wave_inclusive_sum(dtt_l);
-    const float Alast = uniform(__shfl(A_l, 63, 64));
+    const float Alast = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(A_l), 63));
     if (wave == 0) P_A[lane] = A_l;
 
     // ---- per (token, mode) controls and weights: thread pair = t MP + m
