@@ -4,9 +4,11 @@
 //
 // Per (batch, head) the step reads and rewrites the whole M x N x P float32 state
 // once; everything else is a few hundred bytes.  The kernel is therefore a
-// streaming kernel: one workgroup per (batch, head), the state walked as rows of P
-// floats with 16-byte loads and stores, the readout reduced over (m, n) in
-// registers and then across row groups through LDS in a fixed order.
+// streaming kernel: one workgroup of 1024 threads per (batch, head), the state
+// walked as rows of P floats with 16-byte loads and stores, the readout reduced
+// over (m, n) in registers and then across row groups through LDS in a fixed
+// order.  With 1024 threads a 4-mode state (128 KB) is read in one batch of
+// loads and then written back, which keeps the DRAM traffic in long runs.
 #include "frac_device.h"
 #include "frac_kernels.h"
 
@@ -14,7 +16,7 @@ namespace frac {
 
 namespace {
 
-constexpr int kDecodeThreads = 256;
+constexpr int kDecodeThreads = 1024;
 constexpr int kDecodeUnroll = 8;
 
 template <typename T, int MP>
