@@ -164,7 +164,8 @@ def bench_scan(torch, frac, w, steps, warmup):
     }
     if w.backward:
         res["bwd_ms"] = bms
-        res["bwd_roofline"] = roofline("mfma", th * bwd_flops_per_token_head(w), bms, peak, "TFLOP/s")
+        res["bwd_roofline"] = dict(roofline("mfma", th * bwd_flops_per_token_head(w), bms, peak, "TFLOP/s"),
+                                   traffic=measured_traffic("frac_scan_bwd", w.name))
         res["fwd_bwd_roofline"] = roofline(
             "mfma", th * (fwd_flops_per_token_head(w) + bwd_flops_per_token_head(w)), fms + bms, peak, "TFLOP/s")
     return res
@@ -197,7 +198,8 @@ def bench_decode(torch, frac, w, steps, warmup):
         "us_per_step": us_step,
         "wall_us_per_step": wall * 1e6 / (steps * S),
         "tokens_per_s": w.batch / (us_step * 1e-6),
-        "roofline": roofline("hbm", decode_bytes_per_step(w), us_step * 1e-3, PEAK_HBM_BYTES, "GB/s"),
+        "roofline": dict(roofline("hbm", decode_bytes_per_step(w), us_step * 1e-3, PEAK_HBM_BYTES, "GB/s"),
+                         traffic=measured_traffic("frac_decode_step", w.name)),
     }
 
 

@@ -40,7 +40,8 @@
  *    bfloat16 outputs are rounded to nearest even.
  *  - Supported sizes: headdim P and dstate N multiples of 8 with N <= 128;
  *    P <= 64 for the chunked scan (frac_scan_*), P <= 128 for frac_decode_step;
- *    1 <= nmodes <= 8; H % G == 0; chunk 0 (auto) or 64.  Anything else returns
+ *    1 <= nmodes <= 8 for the chunked scan, <= 32 for frac_decode_step;
+ *    H % G == 0; chunk 0 (auto) or 64.  Anything else returns
  *    FRAC_ERR_UNSUPPORTED (frac_scan_workspace_size returns 0).  batch or seqlen
  *    0 is a no-op.
  *  - The library keeps no state between calls; it is safe to call from several

@@ -49,7 +49,7 @@ frac_status fill_shape(const frac_shape* sh, frac::ScanParams& p) {
   if (sh->io_dtype != FRAC_F32 && sh->io_dtype != FRAC_BF16)
     return fail(FRAC_ERR_INVALID_ARG, "io_dtype %d is not a frac_dtype", (int)sh->io_dtype);
   if (sh->chunk != 0 && sh->chunk != 64) return fail(FRAC_ERR_UNSUPPORTED, "chunk %lld: only 64 (or 0 = auto) is built", (long long)sh->chunk);
-  if (sh->nmodes > 8) return fail(FRAC_ERR_UNSUPPORTED, "nmodes %lld > 8", (long long)sh->nmodes);
+  if (sh->nmodes > 32) return fail(FRAC_ERR_UNSUPPORTED, "nmodes %lld > 32", (long long)sh->nmodes);
   if (sh->dstate % 8 || sh->dstate > 128)
     return fail(FRAC_ERR_UNSUPPORTED, "dstate %lld: must be a multiple of 8 and <= 128", (long long)sh->dstate);
   if (sh->headdim % 8 || sh->headdim > 128)
@@ -70,11 +70,13 @@ frac_status fill_shape(const frac_shape* sh, frac::ScanParams& p) {
   return FRAC_OK;
 }
 
-// The chunked scan keeps one 64-column tile of x per chunk in LDS: headdim <= 64.
+// The chunked scan keeps one 64-column tile of x per chunk in LDS (headdim <= 64)
+// and its share of the state in registers (nmodes <= 8).
 // The tiles of 64 tokens are addressed with 32-bit byte offsets: 64 rows of x
 // (H P elements apart) and of B, C (G N elements apart) must span < 2 GiB.
 frac_status check_scan_shape(const frac::ScanParams& p, const char* what) {
   if (p.PP > 64) return fail(FRAC_ERR_UNSUPPORTED, "%s: headdim %d > 64 is not built", what, p.P);
+  if (p.M > 8) return fail(FRAC_ERR_UNSUPPORTED, "%s: nmodes %d > 8 is not built", what, p.M);
   const int64_t es = p.io_bf16 ? 2 : 4, lim = (int64_t)1 << 31;
   if (64 * (int64_t)p.H * p.P * es >= lim || 64 * (int64_t)p.G * p.N * es >= lim)
     return fail(FRAC_ERR_UNSUPPORTED, "%s: nheads * headdim or ngroups * dstate too large", what);

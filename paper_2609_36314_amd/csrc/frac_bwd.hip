@@ -1271,13 +1271,12 @@ __global__ void __launch_bounds__(512) frac_bwd_rows_kernel(ScanParams p, BwdWor
 #pragma unroll
               for (int kb = 0; kb < KBW; ++kb) mma(Z, Gf[kb], Ba[q][kb]);
               const int o = (mo + m) * kQ + tb * 16 + li;
-              const float wx = P_wdx[o], wf = P_wfk[o];
+              const float wx = P_wdx[o], wf = P_wfk[o], rwx = rm * wx;
 #pragma unroll
               for (int r = 0; r < 4; ++r) {
-                const float v = wx * Z[r];
-                dxa[tb][r] += v;
-                We[q][r] += rm * v;
-                Wf[q][r] += wf * Z[r];
+                dxa[tb][r] = __builtin_fmaf(wx, Z[r], dxa[tb][r]);
+                We[q][r] = __builtin_fmaf(rwx, Z[r], We[q][r]);
+                Wf[q][r] = __builtin_fmaf(wf, Z[r], Wf[q][r]);
               }
             }
           }

@@ -141,7 +141,9 @@ hipError_t launch_decode_mp(const ScanParams& p, float* state, hipStream_t strea
   if (p.M <= 1) return launch_decode_variant<T, 1>(p, state, stream);
   if (p.M <= 2) return launch_decode_variant<T, 2>(p, state, stream);
   if (p.M <= 4) return launch_decode_variant<T, 4>(p, state, stream);
-  return launch_decode_variant<T, 8>(p, state, stream);
+  if (p.M <= 8) return launch_decode_variant<T, 8>(p, state, stream);
+  if (p.M <= 16) return launch_decode_variant<T, 16>(p, state, stream);
+  return launch_decode_variant<T, 32>(p, state, stream);
 }
 
 }  // namespace

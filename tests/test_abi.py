@@ -62,6 +62,7 @@ def _shape(**kw):
     (dict(batch=-1), -1),
     (dict(io_dtype=7), -1),
     (dict(nmodes=9), -2),
+    (dict(nmodes=33), -2),
     (dict(dstate=12), -2),
     (dict(dstate=256), -2),
     (dict(headdim=20), -2),
@@ -113,3 +114,12 @@ def test_workspace_is_required_and_checked():
         setattr(a, f, ctypes.c_void_p(0x10000))
     assert lib.frac_scan_fwd(ctypes.byref(sh), ctypes.byref(a), None, 0, None) == -3
     assert lib.frac_scan_fwd(ctypes.byref(sh), ctypes.byref(a), ctypes.c_void_p(0x20000), need - 1, None) == -3
+
+
+@pytest.mark.parametrize("nmodes,status", [(33, -2), (0, -1)])
+def test_decode_mode_range_is_checked_on_the_host(nmodes, status):
+    """frac_decode_step takes up to 32 modes; the shape is checked before any argument."""
+    lib = _lib.load()
+    sh = _shape(seqlen=1, nmodes=nmodes)
+    a = FracStepArgs()
+    assert lib.frac_decode_step(ctypes.byref(sh), ctypes.byref(a), None) == status

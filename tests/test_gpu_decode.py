@@ -53,6 +53,11 @@ CASES = {
     "f32 extras groups": Workload("t", 2, 1, 4, 32, 64, 3, ngroups=2, io_dtype="f32", decode_steps=5,
                                   init_state=True, extras=True),
     "bf16 M8 P16": Workload("t", 2, 1, 2, 16, 32, 8, decode_steps=4, init_state=True),
+    # the paper's bank sizes beyond the scan's 8 modes
+    "bf16 M16 P128": Workload("t", 2, 1, 2, 128, 64, 16, decode_steps=3, init_state=True, extras=True),
+    "f32 M32 N16": Workload("t", 1, 1, 3, 32, 16, 32, io_dtype="f32", decode_steps=3, init_state=True,
+                            extras=True),
+    "bf16 M11": Workload("t", 2, 1, 2, 64, 32, 11, decode_steps=3, init_state=True, extras=True),
 }
 
 
