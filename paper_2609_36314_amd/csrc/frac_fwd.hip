@@ -153,7 +153,9 @@ struct FwdCfg {
   static constexpr int TBP = (kBf16 ? MPW * NBW < 16 : MPW * NBW < 8) ? 4 : (kBf16 || MPW * NBW < 16) ? 2 : 1;
 };
 
-template <typename T, int MP, int NB, int PS>
+// STATE_ONLY: only the state update over tokens [0, seg_len), ending in seg_state
+// (the first pass of a sequence-split forward).
+template <typename T, int MP, int NB, int PS, bool STATE_ONLY>
 __global__ void __launch_bounds__(512) frac_fwd_kernel(ScanParams p, const T* __restrict__ gtiles) {
   using Cfg = FwdCfg<T, MP, NB, PS>;
   constexpr int NP = Cfg::NP, XS = Cfg::XS, BS = Cfg::BS, CS = Cfg::CS, GS = Cfg::GS;
@@ -161,7 +163,13 @@ __global__ void __launch_bounds__(512) frac_fwd_kernel(ScanParams p, const T* __
   constexpr int NWT = 8;                  // waves in the workgroup
   const int tid = threadIdx.x;
   const int wave = tid >> 6, lane = tid & 63, li = lane & 15, lg = lane >> 4;
-  const int ps = blockIdx.x % Cfg::PS;                  // which columns of P
+  // Sequence segment: with p.seg_len > 0 the grid of the output pass holds the
+  // (batch, head) blocks twice, the second copy for tokens [seg_len, L) starting
+  // from the boundary state.
+  const int nbh_blocks = p.Bsz * p.H * Cfg::PS;
+  const int seg = (!STATE_ONLY && p.seg_len > 0 && (int)blockIdx.x >= nbh_blocks) ? 1 : 0;
+  const int bid = (int)blockIdx.x - seg * nbh_blocks;
+  const int ps = bid % Cfg::PS;                         // which columns of P
   const int pb = ps * Cfg::NPW + wave % Cfg::NPW, part = wave / Cfg::NPW;
   // waves past the P blocks (or the second part when there is one) only stage
   // tiles, compute controls and Gamma tiles
@@ -171,11 +179,16 @@ __global__ void __launch_bounds__(512) frac_fwd_kernel(ScanParams p, const T* __
   const int pc = pb * 16 + li;
   const int L = p.L, H = p.H, P = p.P, N = p.N, M = p.M, G = p.G;
   const int nchunks = (L + kQ - 1) / kQ;
+  const int T0 = seg ? p.seg_len : 0;                                       // first token
+  const int T1 = (STATE_ONLY || (p.seg_len > 0 && !seg)) ? p.seg_len : L;  // one past the last
+  const int c0 = T0 / kQ, c1 = (T1 + kQ - 1) / kQ;                          // chunks of the segment
+  const float* init_state = seg ? p.seg_state : p.init_state;
+  float* final_state = STATE_ONLY ? p.seg_state : (T1 == L ? p.final_state : nullptr);
 
   // Blocks are dealt round-robin to the 8 XCDs; give each XCD a contiguous run of
   // (batch, head) so that heads sharing B and C share one L2.
-  int j = blockIdx.x / Cfg::PS;
-  const int nblk = gridDim.x / Cfg::PS;
+  int j = bid / Cfg::PS;
+  const int nblk = nbh_blocks / Cfg::PS;
   if ((nblk & 7) == 0) j = (j & 7) * (nblk >> 3) + (j >> 3);
   const int b = j / H, h = j - b * H, g = h * G / H;
 
@@ -216,7 +229,7 @@ __global__ void __launch_bounds__(512) frac_fwd_kernel(ScanParams p, const T* __
     const float tau = (tid < M) ? p.tau[tid] : 1.0f;
     s_rr[tid] = (tid < M) ? 1.0f / tau : 0.0f;
     s_lnt[tid] = (tid < M) ? logf(tau) : 0.0f;
-    s_E2[tid] = 1.0f;
+    s_E2[tid] = s_E2[MP + tid] = 1.0f;
   }
   // tiles start zeroed: columns past P or N are never copied into
   for (int i = tid; i < 64 * GS; i += 512) GGT[i] = (T)0.0f;
@@ -240,8 +253,8 @@ __global__ void __launch_bounds__(512) frac_fwd_kernel(ScanParams p, const T* __
         for (int r = 0; r < 4; ++r) {
           const int n = (nbo + jb) * 16 + lg * 4 + r;
           float v = 0.0f;
-          if (p.init_state && active && mo + m < M && n < N && pc < P)
-            v = p.init_state[sbase + lo + ((int64_t)m * N + jb * 16 + r) * P];
+          if (init_state && active && mo + m < M && n < N && pc < P)
+            v = init_state[sbase + lo + ((int64_t)m * N + jb * 16 + r) * P];
           S[m][jb][r] = v;
         }
   }
@@ -259,7 +272,7 @@ __global__ void __launch_bounds__(512) frac_fwd_kernel(ScanParams p, const T* __
   const int64_t lg_st = (int64_t)H * M;
   auto load_controls = [&](int c, float& dtv, float& al, float& lam) {
     const int tg = c * kQ + lane;
-    const bool valid = tg < L;
+    const bool valid = tg < T1;
     dtv = valid ? dt_bh[(int64_t)tg * H] : 0.0f;
     al = valid ? al_bh[tg * al_st] : 1.0f;
     lam = (valid && lm_bh) ? lm_bh[tg * lm_st] : 1.0f;
@@ -271,15 +284,15 @@ __global__ void __launch_bounds__(512) frac_fwd_kernel(ScanParams p, const T* __
   planB.init(bstride, N);
   planC.init(bstride, N);
   auto stage = [&](int c, T* Xd, T* Bd, T* Cd) {
-    const int t0 = c * kQ, nv = min(kQ, L - t0);
+    const int t0 = c * kQ, nv = min(kQ, T1 - t0);
     planX.template issue<Cfg::NBUF == 1>(Xd, xg + (int64_t)t0 * xstride, xstride, nv);
     planB.template issue<Cfg::NBUF == 1>(Bd, Bgp + (int64_t)t0 * bstride, bstride, nv);
-    planC.template issue<Cfg::NBUF == 1>(Cd, Cgp + (int64_t)t0 * bstride, bstride, nv);
+    if constexpr (!STATE_ONLY) planC.template issue<Cfg::NBUF == 1>(Cd, Cgp + (int64_t)t0 * bstride, bstride, nv);
   };
   // output rows of chunk c (staged in Yb) -> global, 16 bytes per thread
   auto store_y = [&](int c) {
     constexpr int E8 = 16 / sizeof(T);
-    const int t0 = c * kQ, nv = min(kQ, L - t0);
+    const int t0 = c * kQ, nv = min(kQ, T1 - t0);
     constexpr int CY = 64 / E8;  // 16-byte chunks of a 64-column row
 #pragma unroll
     for (int i0 = 0; i0 < 64 * CY; i0 += 512) {
@@ -292,30 +305,31 @@ __global__ void __launch_bounds__(512) frac_fwd_kernel(ScanParams p, const T* __
   };
 
   float dt_n, al_n, lam_n;
-  load_controls(0, dt_n, al_n, lam_n);
+  load_controls(c0, dt_n, al_n, lam_n);
   TilePrefetch<T> gtile;  // C B^T tile values, loaded one chunk ahead
-  gtile.load(gtiles + ((int64_t)b * nchunks * G + g) * (kTiles * kTileElems), wave, lane);
-  if (Cfg::NBUF == 2) stage(0, Xb0, Bb0, Cb0);
+  if constexpr (!STATE_ONLY)
+    gtile.load(gtiles + (((int64_t)b * nchunks + c0) * G + g) * (kTiles * kTileElems), wave, lane);
+  if (Cfg::NBUF == 2) stage(c0, Xb0, Bb0, Cb0);
 
   // one chunk: Xc/Bc/Cc hold it (or receive it when single-buffered), Xn/Bn/Cn
   // receive the next one
   auto step = [&](int c, T* Xc, T* Bc, T* Cc, T* Xn, T* Bn, T* Cn) __attribute__((always_inline)) {
     const int t0 = c * kQ;
-    const int nv = min(kQ, L - t0);
+    const int nv = min(kQ, T1 - t0);
     const float* Ecur = s_E2 + (c & 1) * MP;
     float* Enext = s_E2 + ((c + 1) & 1) * MP;
     wait_vmem();
     barrier();  // this chunk's tiles have landed; every wave is done with the previous chunk
-    if (c > 0) store_y(c - 1);
+    if (!STATE_ONLY && c > c0) store_y(c - 1);
     if (Cfg::NBUF == 2) {
-      if (c + 1 < nchunks) stage(c + 1, Xn, Bn, Cn);
+      if (c + 1 < c1) stage(c + 1, Xn, Bn, Cn);
     } else {
       stage(c, Xc, Bc, Cc);
       wait_vmem();
       barrier();
     }
     const float dtv = dt_n, al_l = al_n, lam_l = lam_n;
-    if (c + 1 < nchunks) load_controls(c + 1, dt_n, al_n, lam_n);
+    if (c + 1 < c1) load_controls(c + 1, dt_n, al_n, lam_n);
 
     // ---- per-token step and its chunk-local cumulative sum (lane = token, every wave)
     const float s_eff_l = lm_bh ? exp2f(log2f(lam_l) / al_l) : 1.0f;
@@ -365,6 +379,7 @@ __global__ void __launch_bounds__(512) frac_fwd_kernel(ScanParams p, const T* __
       if (__float_as_int(Enew) < __float_as_int(kRescaleFloor)) renbits |= 1 << m;
     }
     barrier();  // controls in LDS
+    if constexpr (!STATE_ONLY) {
 
     __builtin_amdgcn_sched_barrier(0);
     // ---- ((C B^T) o Gamma)^T, lower-triangular 16x16 tiles split over the waves
@@ -408,7 +423,7 @@ __global__ void __launch_bounds__(512) frac_fwd_kernel(ScanParams p, const T* __
       }
     }
 
-    if (c + 1 < nchunks) gtile.load(gtiles + (((int64_t)b * nchunks + c + 1) * G + g) * (kTiles * kTileElems), wave, lane);
+    if (c + 1 < c1) gtile.load(gtiles + (((int64_t)b * nchunks + c + 1) * G + g) * (kTiles * kTileElems), wave, lane);
 
     __builtin_amdgcn_sched_barrier(0);
     // ---- readout of the state entering the chunk, this wave's modes
@@ -490,6 +505,8 @@ __global__ void __launch_bounds__(512) frac_fwd_kernel(ScanParams p, const T* __
 #pragma unroll
       for (int r = 0; r < 4; ++r) Yb[(tb * 16 + lg * 4 + r) * XS + pc] = (T)(Y[tb][r] + Dh * xv[r]);
     }
+    }  // !STATE_ONLY
+    if (!active) return;
 
     __builtin_amdgcn_sched_barrier(0);
     // ---- state update  S_m <- (rescale) + B^T (v_m o X), this wave's modes
@@ -529,19 +546,19 @@ __global__ void __launch_bounds__(512) frac_fwd_kernel(ScanParams p, const T* __
     }
   };
 
-  for (int c = 0; c < nchunks; c += 2) {
+  for (int c = c0; c < c1; c += 2) {
     step(c, Xb0, Bb0, Cb0, Xb1, Bb1, Cb1);
-    if (c + 1 < nchunks) {
+    if (c + 1 < c1) {
       if (Cfg::NBUF == 2) step(c + 1, Xb1, Bb1, Cb1, Xb0, Bb0, Cb0);
       else step(c + 1, Xb0, Bb0, Cb0, Xb0, Bb0, Cb0);
     }
   }
   wait_vmem();
   barrier();
-  store_y(nchunks - 1);
+  if constexpr (!STATE_ONLY) store_y(c1 - 1);
 
-  if (p.final_state && active) {
-    const float* Ef = s_E2 + (nchunks & 1) * MP;
+  if (final_state && active) {
+    const float* Ef = s_E2 + (c1 & 1) * MP;
     int lo = (mo * N + nbo * 16 + lg * 4) * P + pc;
     asm volatile("" : "+v"(lo));
 #pragma unroll
@@ -553,7 +570,7 @@ __global__ void __launch_bounds__(512) frac_fwd_kernel(ScanParams p, const T* __
         for (int r = 0; r < 4; ++r) {
           const int n = (nbo + jb) * 16 + lg * 4 + r;
           if (mo + m < M && n < N && pc < P)
-            p.final_state[sbase + lo + ((int64_t)m * N + jb * 16 + r) * P] = S[m][jb][r] * Em;
+            final_state[sbase + lo + ((int64_t)m * N + jb * 16 + r) * P] = S[m][jb][r] * Em;
         }
     }
   }
@@ -577,24 +594,51 @@ hipError_t launch_cb_variant(const ScanParams& p, T* gt, hipStream_t stream) {
   return hipGetLastError();
 }
 
-template <typename T, int MP, int NB>
-hipError_t launch_fwd_variant(const ScanParams& p, void* ws, hipStream_t stream) {
-  T* gt = reinterpret_cast<T*>(ws);
-  hipError_t e = launch_cb_variant<T, NB>(p, gt, stream);
-  if (e != hipSuccess) return e;
-  // Few (batch, head) pairs (long single-sequence prefill): split the columns of P
-  // over two workgroups per head so that more of the 256 compute units have work.
-  const bool split = MP >= 8 || (MP >= 4 && p.Bsz * p.H < 192);
-  if (split) {
-    constexpr int PS = MP >= 4 ? 2 : 1;
-    hipLaunchKernelGGL((frac_fwd_kernel<T, MP, NB, PS>), dim3(p.Bsz * p.H * PS), dim3(512), 0, stream, p,
-                       (const T*)gt);
-  } else {
-    constexpr int PS = MP >= 8 ? 2 : 1;
-    hipLaunchKernelGGL((frac_fwd_kernel<T, MP, NB, PS>), dim3(p.Bsz * p.H * PS), dim3(512), 0, stream, p,
-                       (const T*)gt);
-  }
+// Workgroups per (batch, head) along P: two with 8 modes (register budget), and
+// with 4 modes when few (batch, head) pairs would leave compute units idle.
+int fwd_p_split(const ScanParams& p) {
+  const int MP = p.M <= 1 ? 1 : p.M <= 2 ? 2 : p.M <= 4 ? 4 : 8;
+  return (MP >= 8 || (MP >= 4 && p.Bsz * p.H < 192)) ? 2 : 1;
+}
+
+// Sequence split: when the (batch, head) workgroups fill at most half of the 256
+// compute units and the sequence is long, the sequence is cut at a chunk boundary
+// near its middle.  A state-only pass scans the first part to the boundary state;
+// the output pass then runs both parts at once, the second from that state.
+int fwd_seg_len(const ScanParams& p) {
+  const int nchunks = (p.L + kQ - 1) / kQ;
+  if (2 * (int64_t)p.Bsz * p.H * fwd_p_split(p) > 256 || nchunks < 8) return 0;
+  return (nchunks / 2) * kQ;
+}
+
+size_t align256(size_t n) { return (n + 255) & ~(size_t)255; }
+
+template <typename T, int MP, int NB, int PS>
+hipError_t launch_fwd_ps(const ScanParams& p, const T* gt, hipStream_t stream) {
+  const unsigned blocks = (unsigned)(p.Bsz * p.H * PS);
+  if (p.seg_len > 0)
+    hipLaunchKernelGGL((frac_fwd_kernel<T, MP, NB, PS, true>), dim3(blocks), dim3(512), 0, stream, p, gt);
+  hipLaunchKernelGGL((frac_fwd_kernel<T, MP, NB, PS, false>), dim3(blocks * (p.seg_len > 0 ? 2 : 1)), dim3(512), 0,
+                     stream, p, gt);
   return hipGetLastError();
+}
+
+template <typename T, int MP, int NB>
+hipError_t launch_fwd_variant(const ScanParams& p0, void* ws, hipStream_t stream) {
+  T* gt = reinterpret_cast<T*>(ws);
+  hipError_t e = launch_cb_variant<T, NB>(p0, gt, stream);
+  if (e != hipSuccess) return e;
+  ScanParams p = p0;
+  p.seg_len = fwd_seg_len(p);
+  p.seg_state = p.seg_len > 0 ? reinterpret_cast<float*>(reinterpret_cast<char*>(ws) + align256(gtile_bytes<T>(p)))
+                              : nullptr;
+  if constexpr (MP >= 8) return launch_fwd_ps<T, MP, NB, 2>(p, gt, stream);
+  else if constexpr (MP >= 4) {
+    if (fwd_p_split(p) == 2) return launch_fwd_ps<T, MP, NB, 2>(p, gt, stream);
+    return launch_fwd_ps<T, MP, NB, 1>(p, gt, stream);
+  } else {
+    return launch_fwd_ps<T, MP, NB, 1>(p, gt, stream);
+  }
 }
 
 template <typename T, int MP>
@@ -647,7 +691,9 @@ hipError_t launch_cb_tiles(const ScanParams& p, void* tiles, hipStream_t stream)
 
 size_t scan_fwd_workspace(const ScanParams& p) {
   if (p.Bsz == 0 || p.L == 0) return 0;
-  return p.io_bf16 ? gtile_bytes<bf16>(p) : gtile_bytes<float>(p);
+  const size_t tiles = p.io_bf16 ? gtile_bytes<bf16>(p) : gtile_bytes<float>(p);
+  if (fwd_seg_len(p) == 0) return tiles;
+  return align256(tiles) + sizeof(float) * (size_t)p.Bsz * p.H * p.M * p.N * p.P;  // + the boundary state
 }
 
 hipError_t launch_scan_fwd(const ScanParams& p, void* ws, size_t, hipStream_t stream) {

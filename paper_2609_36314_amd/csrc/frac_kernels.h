@@ -29,6 +29,10 @@ struct ScanParams {
   const float* init_state;
   void* y;
   float* final_state;
+  // forward split into two sequence segments (0: one segment): tokens [0, seg_len)
+  // and [seg_len, L); seg_state holds the state at the boundary
+  int seg_len;
+  float* seg_state;
   // backward only
   const void* dy;
   const float* d_final_state;

@@ -85,6 +85,11 @@ SMALL = {
     # 8 modes split P over two workgroups: a partly filled second half, an empty one
     "bf16 M8 P48 groups": Workload("t", 2, 190, 4, 48, 64, 8, ngroups=2, final_state=True, init_state=True),
     "bf16 M6 P16 N32": Workload("t", 1, 129, 2, 16, 32, 6, final_state=True, extras=True),
+    # few heads and a long sequence: cut at a chunk boundary, a state-only pass to the
+    # boundary state, then both parts at once
+    "bf16 split M4 extras": Workload("t", 1, 700, 2, 64, 128, 4, extras=True, init_state=True, final_state=True),
+    "bf16 split M8": Workload("t", 1, 520, 2, 64, 64, 8, final_state=True),
+    "f32 split M2 ragged": Workload("t", 1, 777, 1, 32, 32, 2, io_dtype="f32", final_state=True, init_state=True),
 }
 
 
