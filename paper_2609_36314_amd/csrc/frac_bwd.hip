@@ -33,9 +33,12 @@
 //   rows   reverse, adjoint in row layout (lane = column p of P, rows n): dx and
 //          the adjoint parts of e and f;
 //   cols   reverse, adjoint transposed (lane = column n): dB (per head).
-// With many modes and a wide state the state and cols sweeps split N, and the
-// rows sweep splits P, over two workgroups per (batch, head), so that no
-// per-head output gets a second partial sum.  Tiles are copied straight into
+// The state sweep also writes each chunk's causal tiles (C B^T) o Gamma and
+// Gamma o (dY X^T) (bfloat16 for bfloat16 I/O, 10 tiles of 16x16 per chunk and
+// head), which the reverse sweeps read instead of forming Gamma again.  With many
+// modes and a wide state the state and cols sweeps split N, and the rows sweep
+// splits P, over two workgroups per (batch, head), so that no per-head output
+// gets a second partial sum.  Tiles are copied straight into
 // LDS (natural layout, padded rows) and read back as matrix-core fragments with
 // row reads or transposed 64-bit reads.  A finishing kernel forms ddt from the
 // suffix sums, and a reduction kernel sums dB and dC over the heads of each group
@@ -100,7 +103,7 @@ enum Role { kState = 0, kRows = 1, kCols = 2 };
 // Number of [MP][Q] weight arrays a role keeps in LDS (plus one [Q] array for A_t).
 template <int ROLE>
 constexpr int n_weight_arrays() {
-  return ROLE == kState ? 9 : ROLE == kRows ? 7 : 6;
+  return ROLE == kState ? 9 : ROLE == kRows ? 3 : 2;
 }
 
 // Per-wave chunk controls (lane = token): effective step, its chunk-local
@@ -125,10 +128,9 @@ __device__ __forceinline__ ChunkCtl chunk_controls(float dtv, float al, float la
 // decay exceeds the factorisation bound (bit m).
 //   state: 0 c e^{-rA}, 1 kappa e^{rA} (safe), 2 r c e^{-rA}, 3 r w rho e^{rA} (safe),
 //          4 c e^{-rA} E, 5 kappa e^{-r(A_Q-A)} upd, 6 c, 7 kappa, 8 r w rho
-//   rows:  0 c e^{-rA}, 1 kappa e^{rA} (safe), 2 c, 3 kappa, 4 kappa e^{-r(A_Q-A)} E,
-//          5 r w rho e^{-r(A_Q-A)} E, 6 c e^{-rA} upd
-//   cols:  0 c e^{-rA}, 1 kappa e^{rA} (safe), 2 c, 3 kappa, 4 kappa e^{-r(A_Q-A)} E,
-//          5 c e^{-rA} upd
+//   rows:  0 kappa e^{-r(A_Q-A)} E, 1 r w rho e^{-r(A_Q-A)} E, 2 c e^{-rA} upd
+//   cols:  0 kappa e^{-r(A_Q-A)} E, 1 c e^{-rA} upd
+// (the reverse sweeps read their Gamma tiles from the state sweep)
 // E is the scale of the state (or adjoint) before this chunk's update, upd the
 // factor on the update (1/E_new, or 1 when the accumulators are folded back).
 template <int MP, int ROLE>
@@ -157,7 +159,7 @@ __device__ __forceinline__ int pair_weights(const ChunkCtl& k, int t0, int nv, i
     const float beta = one_minus_exp_neg(dtt * r);
     const float kap = beta * ww;
     const float ea = fexp(-r * A);
-    const float ep = safe ? fexp(r * A) : 0.0f;
+    const float ep = (ROLE == kState && safe) ? fexp(r * A) : 0.0f;
     const float dec = fexp(-r * (k.Alast - A));
     float* o = w + m * kQ + t;
     constexpr int SW = MP * kQ;  // stride of the weight arrays
@@ -173,20 +175,12 @@ __device__ __forceinline__ int pair_weights(const ChunkCtl& k, int t0, int nv, i
       o[7 * SW] = kap;
       o[8 * SW] = rwr;
     } else if constexpr (ROLE == kRows) {
-      o[0 * SW] = cw * ea;
-      o[1 * SW] = kap * ep;
-      o[2 * SW] = cw;
-      o[3 * SW] = kap;
-      o[4 * SW] = kap * dec * E;
-      o[5 * SW] = r * ww * (1.0f - beta) * dec * E;
-      o[6 * SW] = cw * ea * upd;
+      o[0 * SW] = kap * dec * E;
+      o[1 * SW] = r * ww * (1.0f - beta) * dec * E;
+      o[2 * SW] = cw * ea * upd;
     } else {
-      o[0 * SW] = cw * ea;
-      o[1 * SW] = kap * ep;
-      o[2 * SW] = cw;
-      o[3 * SW] = kap;
-      o[4 * SW] = kap * dec * E;
-      o[5 * SW] = cw * ea * upd;
+      o[0 * SW] = kap * dec * E;
+      o[1 * SW] = cw * ea * upd;
     }
     if (pr < MP) Enext[m] = ren ? 1.0f : Enew;
   }
@@ -298,6 +292,8 @@ __device__ __forceinline__ void block_head(int PS, int H, int& b, int& h, int& p
 
 struct BwdWork {
   const void* tiles;  // C B^T tiles
+  void* gg;           // (C B^T) o Gamma per (batch, chunk, head), causal tiles in fragment order
+  void* hg;           // Gamma o (dY X^T), the same layout
   void* dBp;          // per-head dB, [B, L, H, N]
   void* dCp;          // per-head dC
   float* eA;          // [2][B H L] readout / intra part of e (per N half)
@@ -533,6 +529,20 @@ __global__ void __launch_bounds__(512) frac_bwd_state_kernel(ScanParams p, BwdWo
         T* dst = HGT + (kb * 16 + li) * XS + tb * 16 + lg * 4;
 #pragma unroll
         for (int r = 0; r < 4; ++r) dst[r] = (T)hv[r];
+        {  // the tiles of the reverse sweeps, once per head: (C B^T) o Gamma from the
+           // first workgroup of the head, Gamma o (dY X^T) from the last
+          const int64_t to = ((int64_t)(b * nchunks + c) * H + h) * (kTiles * kTileElems) + tile * kTileElems + lane * 4;
+          if (ps == 0) {
+            floatx4 gv;
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+              const int t = tb * 16 + lg * 4 + r, kk = kb * 16 + li;
+              gv[r] = (t >= kk) ? gtile.get(jt, r) * Gm[r] : 0.0f;
+            }
+            store4(reinterpret_cast<T*>(wk.gg) + to, gv);
+          }
+          if (ps == Cfg::PS - 1) store4(reinterpret_cast<T*>(wk.hg) + to, floatx4{hv[0], hv[1], hv[2], hv[3]});
+        }
         if (tile % Cfg::PS == ps) {  // the two halves of N share the tile sums
           floatx4 Ph = rank_m_tile<MP>(P_rO, P_Vt, tb * 16, kb * 16, tid);
           floatx4 Ps = rank_m_tile<MP>(P_O, P_Y, tb * 16, kb * 16, tid);
@@ -795,12 +805,8 @@ __global__ void __launch_bounds__(512) frac_bwd_cols_kernel(ScanParams p, BwdWor
   float* s_lnt = s_rr + MP;
   float* s_E2 = s_lnt + MP;
   constexpr int SW = MP * kQ;  // stride of the weight arrays
-  const float* P_O = W;
-  const float* P_Vt = W + 1 * SW;
-  const float* P_c = W + 2 * SW;
-  const float* P_k = W + 3 * SW;
-  const float* P_wdb = W + 4 * SW;
-  const float* P_om = W + 5 * SW;
+  const float* P_wdb = W;
+  const float* P_om = W + 1 * SW;
 
   if (tid < MP) {
     const float tau = (tid < M) ? p.tau[tid] : 1.0f;
@@ -856,17 +862,23 @@ __global__ void __launch_bounds__(512) frac_bwd_cols_kernel(ScanParams p, BwdWor
   DmaPlan<T, CS> planC;
   planX.init(xstride, P);
   planC.init(bstride, N);
+  // (LDS addresses passed opaquely: the compiler otherwise folds the address-space
+  // conversion of these tiles into an instruction it cannot encode)
   auto stage = [&](int c, T* Xd, T* Yd, T* Cd) {
     const int t0 = c * kQ, nv = min(kQ, L - t0);
-    planX.template issue<Cfg::NBUF == 1>(Xd, xg + (int64_t)t0 * xstride, xstride, nv);
-    planX.template issue<Cfg::NBUF == 1>(Yd, yg + (int64_t)t0 * xstride, xstride, nv);
-    planC.template issue<Cfg::NBUF == 1>(Cd, Cgp + (int64_t)t0 * bstride, bstride, nv);
+    planX.template issue<true>(Xd, xg + (int64_t)t0 * xstride, xstride, nv);
+    planX.template issue<true>(Yd, yg + (int64_t)t0 * xstride, xstride, nv);
+    planC.template issue<true>(Cd, Cgp + (int64_t)t0 * bstride, bstride, nv);
   };
 
   float dt_n, al_n, lam_n;
   load_controls(nchunks - 1, dt_n, al_n, lam_n);
   if (Cfg::NBUF == 2) stage(nchunks - 1, Xb0, Yb0, Cb0);
   T* dBp = reinterpret_cast<T*>(wk.dBp);
+  // Gamma o (dY X^T) tiles written by the state sweep, loaded one chunk ahead (in processing order)
+  const T* hgtiles = reinterpret_cast<const T*>(wk.hg);
+  TilePrefetch<T> hgt;
+  hgt.load(hgtiles + ((int64_t)(b * nchunks + nchunks - 1) * H + h) * (kTiles * kTileElems), wave, lane);
 
   // chunks in reverse order; i counts processed chunks (buffer parity)
   auto step = [&](int c, int i, T* Xc, T* Yc, T* Cc, T* Xn, T* Yn, T* Cn) __attribute__((always_inline)) {
@@ -899,17 +911,16 @@ __global__ void __launch_bounds__(512) frac_bwd_cols_kernel(ScanParams p, BwdWor
 
     __builtin_amdgcn_sched_barrier(0);
     // ---- HG = Gamma o dY X^T (natural [t][k], causal)
-    for (int tile = wave; tile < kTiles; tile += 8) {
-      const int tb = kTB[tile], kb = kKB[tile];
-      const floatx4 D = dyx_tile<T, XS>(Yc, Xc, tb, kb);
-      floatx4 Gm = rank_m_tile<MP>(P_O, P_Vt, tb * 16, kb * 16);
-      if (unsafe) unsafe_terms<MP>(Gm, unsafe, P_c, P_k, P_A, s_rr, tb, kb, false);
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int t = tb * 16 + lg * 4 + r, kk = kb * 16 + li;
-        HG[t * XS + kk] = (T)((t >= kk) ? Gm[r] * D[r] : 0.0f);
-      }
+    for (int jt = 0; jt < 2; ++jt) {
+      const int tile = wave + 8 * jt;
+      if (tile >= kTiles) break;
+      const int tb = kTB[tile], kb = kKB[tile];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) HG[(tb * 16 + lg * 4 + r) * XS + kb * 16 + li] = hgt.v[jt].e[r];
     }
+    (void)unsafe;
+    if (c > 0) hgt.load(hgtiles + ((int64_t)(b * nchunks + c - 1) * H + h) * (kTiles * kTileElems), wave, lane);
 
     __builtin_amdgcn_sched_barrier(0);
     // ---- V^T_m = G_m X^T (rows n of this wave's block, columns k) -> dB^T (inter)
@@ -1077,13 +1088,9 @@ __global__ void __launch_bounds__(512) frac_bwd_rows_kernel(ScanParams p, BwdWor
   float* s_lnt = s_rr + MP;
   float* s_E2 = s_lnt + MP;
   constexpr int SW = MP * kQ;  // stride of the weight arrays
-  const float* P_O = W;
-  const float* P_Vt = W + 1 * SW;
-  const float* P_c = W + 2 * SW;
-  const float* P_k = W + 3 * SW;
-  const float* P_wdx = W + 4 * SW;  // times r_m: the adjoint weight of e
-  const float* P_wfk = W + 5 * SW;
-  const float* P_om = W + 6 * SW;
+  const float* P_wdx = W;  // times r_m: the adjoint weight of e
+  const float* P_wfk = W + 1 * SW;
+  const float* P_om = W + 2 * SW;
 
   if (tid < MP) {
     const float tau = (tid < M) ? p.tau[tid] : 1.0f;
@@ -1176,10 +1183,11 @@ __global__ void __launch_bounds__(512) frac_bwd_rows_kernel(ScanParams p, BwdWor
     stage_late(nchunks - 1, Cb0, Yb0);
     stage_early(nchunks - 1);
   }
-  const T* gtiles = reinterpret_cast<const T*>(wk.tiles);
+  // (C B^T) o Gamma tiles written by the state sweep, loaded one chunk ahead (in processing order)
+  const T* ggtiles = reinterpret_cast<const T*>(wk.gg);
   const int64_t bl_h = (int64_t)p.Bsz * L * H;
-  TilePrefetch<T> gtile;  // C B^T tile values, loaded one chunk ahead (in processing order)
-  gtile.load(gtiles + (((int64_t)b * nchunks + nchunks - 1) * G + g) * (kTiles * kTileElems), wave, lane);
+  TilePrefetch<T> ggt;
+  ggt.load(ggtiles + ((int64_t)(b * nchunks + nchunks - 1) * H + h) * (kTiles * kTileElems), wave, lane);
 
   auto step = [&](int c, int i, T* Cc, T* Yc, T* Cn, T* Yn) __attribute__((always_inline)) {
     const int t0 = c * kQ, nv = min(kQ, L - t0);
@@ -1212,24 +1220,20 @@ __global__ void __launch_bounds__(512) frac_bwd_rows_kernel(ScanParams p, BwdWor
     barrier();  // weights in LDS
 
     __builtin_amdgcn_sched_barrier(0);
-    // ---- GG = (C B^T) o Gamma, natural [t'][k], causal
+    // ---- GG = (C B^T) o Gamma, natural [t'][k], causal (tiles from the state sweep)
     {
 #pragma unroll
       for (int jt = 0; jt < 2; ++jt) {
         const int tile = wave + 8 * jt;
         if (tile >= kTiles) break;
         const int tb = kTB[tile], kb = kKB[tile];
-        floatx4 Gm = rank_m_tile<MP>(P_O, P_Vt, tb * 16, kb * 16);
-        if (unsafe) unsafe_terms<MP>(Gm, unsafe, P_c, P_k, P_A, s_rr, tb, kb, false);
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int t = tb * 16 + lg * 4 + r, kk = kb * 16 + li;
-          GG[t * XS + kk] = (T)((t >= kk) ? gtile.get(jt, r) * Gm[r] : 0.0f);
-        }
+        for (int r = 0; r < 4; ++r) GG[(tb * 16 + lg * 4 + r) * XS + kb * 16 + li] = ggt.v[jt].e[r];
       }
     }
+    (void)unsafe;
 
-    if (c > 0) gtile.load(gtiles + (((int64_t)b * nchunks + c - 1) * G + g) * (kTiles * kTileElems), wave, lane);
+    if (c > 0) ggt.load(ggtiles + ((int64_t)(b * nchunks + c - 1) * H + h) * (kTiles * kTileElems), wave, lane);
 
     __builtin_amdgcn_sched_barrier(0);
     // ---- Z^T_m = G_m^T B^T (rows p of this wave's block, columns t) -> dx^T (inter)
@@ -1491,7 +1495,7 @@ __global__ void __launch_bounds__(256) frac_bwd_group_sum_kernel(ScanParams p, c
 }
 
 struct BwdLayout {
-  size_t tiles, dBp, dCp, scal, total;
+  size_t tiles, gg, hg, dBp, dCp, scal, total;
 };
 
 BwdLayout bwd_layout(const ScanParams& p) {
@@ -1500,7 +1504,10 @@ BwdLayout bwd_layout(const ScanParams& p) {
   const size_t bl = (size_t)p.Bsz * p.L;
   auto up = [](size_t v) { return (v + 255) / 256 * 256; };
   l.tiles = 0;
-  l.dBp = up(cb_tiles_bytes(p));
+  const size_t gtb = (size_t)p.Bsz * ((p.L + kQ - 1) / kQ) * p.H * kTiles * kTileElems * es;
+  l.gg = up(cb_tiles_bytes(p));
+  l.hg = l.gg + up(gtb);
+  l.dBp = l.hg + up(gtb);
   l.dCp = l.dBp + up(bl * p.H * p.N * es);
   l.scal = l.dCp + up(bl * p.H * p.N * es);
   // eA[2], fA[2], eB[2], fB[2] per token and head; F[2], dDp per head
@@ -1514,6 +1521,8 @@ hipError_t launch_bwd_variant(const ScanParams& p, void* ws, hipStream_t stream)
   unsigned char* base = reinterpret_cast<unsigned char*>(ws);
   BwdWork wk;
   wk.tiles = base + l.tiles;
+  wk.gg = base + l.gg;
+  wk.hg = base + l.hg;
   wk.dBp = base + l.dBp;
   wk.dCp = base + l.dCp;
   float* sc = reinterpret_cast<float*>(base + l.scal);
