@@ -302,6 +302,7 @@ struct BwdWork {
   float* fB;          // [2][B H L] adjoint part of f
   float* F;           // [2][B H] final-state term (per N half)
   float* dDp;         // [B H] sum(dy . x)
+  float* tsum;        // [B H][L / 64] totals of e over 64-token tiles
 };
 
 // ------------------------------------------------ state / cols sweep layout
@@ -1398,58 +1399,99 @@ __global__ void __launch_bounds__(512) frac_bwd_rows_kernel(ScanParams p, BwdWor
 
 // ---------------------------------------------------------- finishing kernels
 
-// ddt from the per-token terms: suffix sums over the sequence.  One block of 256
-// threads per (batch, head) walks the sequence backwards in tiles of 256 tokens
-// (coalesced reads of the [B, H, L] partials); fixed summation order.
-__global__ void __launch_bounds__(256) frac_bwd_ddt_kernel(ScanParams p, BwdWork wk, int nA, int nB) {
-  __shared__ float wsum[4];
-  const int bh = blockIdx.x, b = bh / p.H, h = bh - b * p.H;
+// ddt from the per-token terms: suffix sums over the sequence, in two steps with
+// a fixed summation order.  First the total of e over each 64-token tile of each
+// (batch, head); then one block of 16 waves per (batch, tile, 64 heads) forms, per head, the
+// sum over the later tiles, the suffix sums inside the tile (one wave per head,
+// lane = token), and writes ddt through LDS so that each token's heads are stored
+// contiguously.
+
+// e_t of one token: readout / intra parts minus adjoint parts (partials per half).
+__device__ __forceinline__ float ddt_e(const BwdWork& wk, int64_t blh, int64_t i, int nA, int nB) {
+  float e = 0.0f;
+  for (int q = 0; q < nA; ++q) e += wk.eA[q * blh + i];
+  for (int q = 0; q < nB; ++q) e -= wk.eB[q * blh + i];
+  return e;
+}
+
+__global__ void __launch_bounds__(256) frac_bwd_ddt_tiles_kernel(ScanParams p, BwdWork wk, float* tsum, int nA,
+                                                                 int nB) {
+  const int ntiles = (p.L + 63) / 64;
+  const int64_t wid = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);  // (b h) * ntiles + tile
+  const int lane = threadIdx.x & 63;
+  if (wid >= (int64_t)p.Bsz * p.H * ntiles) return;
+  const int64_t bh = wid / ntiles;
+  const int t = (int)(wid - bh * ntiles) * 64 + lane;
+  const int64_t blh = (int64_t)p.Bsz * p.L * p.H;
+  float e = t < p.L ? ddt_e(wk, blh, bh * p.L + t, nA, nB) : 0.0f;
+  e = group_allreduce<64>(e, [](float x, float y) { return x + y; });
+  if (lane == 0) tsum[wid] = e;
+}
+
+__global__ void __launch_bounds__(1024) frac_bwd_ddt_kernel(ScanParams p, BwdWork wk, const float* tsum, int nA,
+                                                           int nB) {
+  __shared__ float carry[64];
+  __shared__ float out[64][65];
+  const int L = p.L, H = p.H, ntiles = (L + 63) / 64;
+  const int b = blockIdx.x / ntiles, tile = blockIdx.x - b * ntiles, h0 = blockIdx.y * 64, t0 = tile * 64;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int L = p.L, H = p.H;
+  const int nh = min(64, H - h0);
   const int64_t blh = (int64_t)p.Bsz * L * H, bhn = (int64_t)p.Bsz * H;
-  const int64_t row = (int64_t)bh * L;  // this head's tokens in the partials
-  float Fv = 0.0f;
-  for (int q = 0; q < nA; ++q) Fv += wk.F[q * bhn + bh];
-  float carry = 0.0f;  // sum of e over the tokens after the current tile
-  for (int t0 = ((L - 1) / 256) * 256; t0 >= 0; t0 -= 256) {
-    const int t = t0 + tid;
-    const bool valid = t < L;
+  // per head: final-state term plus the totals of e over the later tiles (one wave
+  // per head, lane j adding tiles tile + 1 + j, tile + 65 + j, ...)
+  for (int hl = wave; hl < nh; hl += 16) {
+    const int64_t bh = (int64_t)b * H + h0 + hl;
+    float later = 0.0f;
+    for (int j = tile + 1 + lane; j < ntiles; j += 64) later += tsum[bh * ntiles + j];
+    later = group_allreduce<64>(later, [](float x, float y) { return x + y; });
+    if (lane == 0) {
+      float Fv = 0.0f;
+      for (int q = 0; q < nA; ++q) Fv += wk.F[q * bhn + bh];
+      carry[hl] = Fv + later;
+    }
+  }
+  __syncthreads();
+  const int t = t0 + lane;
+  for (int hl = wave; hl < nh; hl += 16) {
+    const int h = h0 + hl;
+    const int64_t i = ((int64_t)b * H + h) * L + t;  // [B, H, L]
     float e = 0.0f, f = 0.0f;
-    if (valid) {
-      for (int q = 0; q < nA; ++q) e += wk.eA[q * blh + row + t];
-      for (int q = 0; q < nB; ++q) {
-        e -= wk.eB[q * blh + row + t];
-        f += wk.fB[q * blh + row + t];
-      }
-      for (int q = 0; q < nA; ++q) f += wk.fA[q * blh + row + t];
+    if (t < L) {
+      e = ddt_e(wk, blh, i, nA, nB);
+      for (int q = 0; q < nA; ++q) f += wk.fA[q * blh + i];
+      for (int q = 0; q < nB; ++q) f += wk.fB[q * blh + i];
     }
-    // inclusive suffix sum within the wave (lane order reversed), then across the 4 waves
+    // inclusive suffix sum over the tile: within each 16-lane row (lanes above,
+    // zero past the row end), then the totals of the later rows
     float s = e;
-#pragma unroll
-    for (int off = 1; off < 64; off <<= 1) {
-      const float o = __shfl_down(s, off, 64);
-      if (lane + off < 64) s += o;
-    }
-    if (lane == 0) wsum[wave] = s;
-    __syncthreads();
-    float later = carry;  // waves after this one within the tile, in wave order
-    for (int w2 = 3; w2 > wave; --w2) later += wsum[w2];
-    float tile_total = 0.0f;
-    for (int w2 = 3; w2 >= 0; --w2) tile_total += wsum[w2];
-    __syncthreads();
-    if (valid) {
+    s += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(s), 0x101, 0xF, 0xF, true));  // row_shl:1
+    s += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(s), 0x102, 0xF, 0xF, true));  // row_shl:2
+    s += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(s), 0x104, 0xF, 0xF, true));  // row_shl:4
+    s += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(s), 0x108, 0xF, 0xF, true));  // row_shl:8
+    const float r1 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(s), 16));
+    const float r2 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(s), 32));
+    const float r3 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(s), 48));
+    const int row = lane >> 4;
+    const float rows_after = row == 0 ? (r3 + r2) + r1 : row == 1 ? r3 + r2 : row == 2 ? r3 : 0.0f;
+    s += rows_after;
+    float v = 0.0f;
+    if (t < L) {
       const float al = strided3(p.alpha, p.as0, p.as1, p.as2, b, t, h);
       const float lam = p.lambda ? strided3(p.lambda, p.ls0, p.ls1, p.ls2, b, t, h) : 1.0f;
       const float s_eff = p.lambda ? exp2f(log2f(lam) / al) : 1.0f;
-      const float ddtt = -Fv - (later + s) + f;
-      p.ddt[((int64_t)b * L + t) * H + h] = ddtt * s_eff;
+      v = (-carry[hl] - s + f) * s_eff;
     }
-    carry += tile_total;
+    out[lane][hl] = v;
   }
-  if (p.dD && b == 0 && tid == 0) {
+  __syncthreads();
+  for (int k = tid; k < 64 * 64; k += 1024) {
+    const int tt = k >> 6, hl = k & 63;
+    if (t0 + tt < L && hl < nh) p.ddt[((int64_t)b * L + t0 + tt) * H + h0 + hl] = out[tt][hl];
+  }
+  if (p.dD && b == 0 && tile == 0 && tid < nh) {
     float acc = 0.0f;
-    for (int bb = 0; bb < p.Bsz; ++bb) acc += wk.dDp[(int64_t)bb * H + h];
-    p.dD[h] = acc;
+    for (int bb = 0; bb < p.Bsz; ++bb) acc += wk.dDp[(int64_t)bb * H + h0 + tid];
+    p.dD[h0 + tid] = acc;
   }
 }
 
@@ -1510,8 +1552,9 @@ BwdLayout bwd_layout(const ScanParams& p) {
   l.dBp = l.hg + up(gtb);
   l.dCp = l.dBp + up(bl * p.H * p.N * es);
   l.scal = l.dCp + up(bl * p.H * p.N * es);
-  // eA[2], fA[2], eB[2], fB[2] per token and head; F[2], dDp per head
-  l.total = l.scal + up(sizeof(float) * (8 * bl * p.H + 3 * (size_t)p.Bsz * p.H));
+  // eA[2], fA[2], eB[2], fB[2] per token and head; F[2], dDp per head; tile totals
+  l.total = l.scal + up(sizeof(float) * (8 * bl * p.H + 3 * (size_t)p.Bsz * p.H +
+                                         (size_t)p.Bsz * p.H * ((p.L + 63) / 64)));
   return l;
 }
 
@@ -1533,6 +1576,7 @@ hipError_t launch_bwd_variant(const ScanParams& p, void* ws, hipStream_t stream)
   wk.fB = sc + 6 * blh;
   wk.F = sc + 8 * blh;
   wk.dDp = wk.F + 2 * (size_t)p.Bsz * p.H;
+  wk.tsum = wk.dDp + (size_t)p.Bsz * p.H;
 
   hipError_t e = launch_cb_tiles(p, base + l.tiles, stream);
   if (e != hipSuccess) return e;
@@ -1546,8 +1590,15 @@ hipError_t launch_bwd_variant(const ScanParams& p, void* ws, hipStream_t stream)
   hipLaunchKernelGGL((frac_bwd_cols_kernel<T, MP, NB>), dim3(bh * ColCfg<T, MP, NB>::PS), dim3(512), 0, stream, p,
                      wk);
   if ((e = hipGetLastError()) != hipSuccess) return e;
-  hipLaunchKernelGGL(frac_bwd_ddt_kernel, dim3(bh), dim3(256), 0, stream, p, wk, ColCfg<T, MP, NB>::PS,
-                     RowCfg<T, MP, NB>::PS);
+  {
+    const int ntiles = (p.L + 63) / 64;
+    const int64_t nt = (int64_t)bh * ntiles;
+    hipLaunchKernelGGL(frac_bwd_ddt_tiles_kernel, dim3((unsigned)((nt + 3) / 4)), dim3(256), 0, stream, p, wk, wk.tsum,
+                       ColCfg<T, MP, NB>::PS, RowCfg<T, MP, NB>::PS);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    hipLaunchKernelGGL(frac_bwd_ddt_kernel, dim3((unsigned)(ntiles * p.Bsz), (p.H + 63) / 64), dim3(1024), 0, stream, p, wk,
+                       (const float*)wk.tsum, ColCfg<T, MP, NB>::PS, RowCfg<T, MP, NB>::PS);
+  }
   if ((e = hipGetLastError()) != hipSuccess) return e;
   const int64_t nrows = (int64_t)p.Bsz * p.L;
   const int64_t nthr = nrows * p.G * (p.N / (16 / (int)sizeof(T)));
