@@ -126,7 +126,7 @@ __global__ void __launch_bounds__(256) frac_cb_kernel(ScanParams p, T* __restric
 // the LDS banks.  bfloat16 tiles are double-buffered: the next chunk is copied
 // in (direct global -> LDS) while the current one is computed.  The block is
 // always 8 waves: 4 blocks of 16 columns of P times 2 parts.
-template <typename T, int MP, int NB, int PS_ = (MP >= 8 ? 2 : 1)>
+template <typename T, int MP, int NB, int PS_ = (MP >= 8 ? 2 : 1), bool SO = false>
 struct FwdCfg {
   static constexpr int NP = NB * 16;
   static constexpr bool kBf16 = sizeof(T) == 2;
@@ -140,13 +140,18 @@ struct FwdCfg {
   // With 8 modes the columns of P are split over two workgroups (PS) so that
   // every wave holds at most 2 modes x all of N of state.  The 8 waves of a
   // workgroup are NPW blocks of 16 columns of P times NPART parts; the parts
-  // split the modes (2 or more modes) or N (one mode).
+  // split the modes (2 or more modes) or N (one mode).  The state-only pass (SO)
+  // has no outputs to exchange and splits the modes first, then N.
   static constexpr int PS = PS_;
   static constexpr int NPW = 4 / PS;
   static constexpr bool kModeSplit = MP >= 2;
-  static constexpr int NPART = kModeSplit ? 8 / NPW : (NB >= 2 ? 2 : 1);
-  static constexpr int MPW = kModeSplit ? MP / NPART : MP;           // modes per wave
-  static constexpr int NBW = (!kModeSplit && NB >= 2) ? NB / 2 : NB;  // 16-row blocks of N per wave
+  static constexpr int NPARTS = 8 / NPW;  // waves per 16-column block of P
+  static constexpr int NPM = SO ? (MP < NPARTS ? MP : NPARTS) : (kModeSplit ? NPARTS : 1);  // mode groups
+  static constexpr int NPN = SO ? (NPARTS / NPM < NB ? NPARTS / NPM : NB)
+                                : (kModeSplit ? 1 : (NB >= 2 ? 2 : 1));  // N groups
+  static constexpr int NPART = NPM * NPN;
+  static constexpr int MPW = MP / NPM;   // modes per wave
+  static constexpr int NBW = NB / NPN;   // 16-row blocks of N per wave
   static constexpr int KBW = (NBW + 1) / 2;                           // 32-deep K steps of the readout
   static constexpr int TBO = 4 / NPART;                               // row blocks of y finished per wave
   // row blocks of the readout whose C fragments are held at once (register budget)
@@ -157,7 +162,7 @@ struct FwdCfg {
 // (the first pass of a sequence-split forward).
 template <typename T, int MP, int NB, int PS, bool STATE_ONLY>
 __global__ void __launch_bounds__(512) frac_fwd_kernel(ScanParams p, const T* __restrict__ gtiles) {
-  using Cfg = FwdCfg<T, MP, NB, PS>;
+  using Cfg = FwdCfg<T, MP, NB, PS, STATE_ONLY>;
   constexpr int NP = Cfg::NP, XS = Cfg::XS, BS = Cfg::BS, CS = Cfg::CS, GS = Cfg::GS;
   constexpr int NPART = Cfg::NPART, MPW = Cfg::MPW, NBW = Cfg::NBW, KBW = Cfg::KBW, TBP = Cfg::TBP;
   constexpr int NWT = 8;                  // waves in the workgroup
@@ -174,8 +179,8 @@ __global__ void __launch_bounds__(512) frac_fwd_kernel(ScanParams p, const T* __
   // waves past the P blocks (or the second part when there is one) only stage
   // tiles, compute controls and Gamma tiles
   const bool active = pb * 16 < p.PP && part < NPART;
-  const int mo = Cfg::kModeSplit ? part * MPW : 0;                 // first mode of this wave
-  const int nbo = (!Cfg::kModeSplit && NPART == 2) ? part * NBW : 0;  // first N block of this wave
+  const int mo = (part % Cfg::NPM) * MPW;   // first mode of this wave
+  const int nbo = (part / Cfg::NPM) * NBW;  // first N block of this wave
   const int pc = pb * 16 + li;
   const int L = p.L, H = p.H, P = p.P, N = p.N, M = p.M, G = p.G;
   const int nchunks = (L + kQ - 1) / kQ;
@@ -616,8 +621,10 @@ size_t align256(size_t n) { return (n + 255) & ~(size_t)255; }
 template <typename T, int MP, int NB, int PS>
 hipError_t launch_fwd_ps(const ScanParams& p, const T* gt, hipStream_t stream) {
   const unsigned blocks = (unsigned)(p.Bsz * p.H * PS);
+  // the state-only pass: one workgroup per 16 columns of P
   if (p.seg_len > 0)
-    hipLaunchKernelGGL((frac_fwd_kernel<T, MP, NB, PS, true>), dim3(blocks), dim3(512), 0, stream, p, gt);
+    hipLaunchKernelGGL((frac_fwd_kernel<T, MP, NB, 4, true>), dim3((unsigned)(p.Bsz * p.H * 4)), dim3(512), 0, stream,
+                       p, gt);
   hipLaunchKernelGGL((frac_fwd_kernel<T, MP, NB, PS, false>), dim3(blocks * (p.seg_len > 0 ? 2 : 1)), dim3(512), 0,
                      stream, p, gt);
   return hipGetLastError();
