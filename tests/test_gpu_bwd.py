@@ -70,6 +70,14 @@ CASES = {
     "bf16 G=H M2 N32 P48": Workload("t", 1, 80, 2, 48, 32, 2, ngroups=2, backward=True),
     "bf16 M1 N16 P16": Workload("t", 2, 70, 3, 16, 16, 1, backward=True),
     "bf16 L1": Workload("t", 2, 1, 2, 64, 128, 4, backward=True, final_state=True, init_state=True),
+    # float32 with 8 modes and a full-width state (single-buffered tiles and weights)
+    "f32 M8 N128 extras dfinal": Workload("t", 1, 140, 2, 64, 128, 8, io_dtype="f32", extras=True, init_state=True,
+                                          backward=True, final_state=True),
+    # an odd mode count and state width, several chunks and a ragged tail
+    "bf16 M5 N96 P32 extras": Workload("t", 2, 333, 2, 32, 96, 5, extras=True, init_state=True, backward=True,
+                                       final_state=True),
+    # 8 modes with heads in two groups (per-head dB, dC partials summed per group)
+    "bf16 M8 groups P48": Workload("t", 1, 190, 4, 48, 64, 8, ngroups=2, backward=True),
 }
 
 
