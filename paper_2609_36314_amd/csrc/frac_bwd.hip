@@ -525,7 +525,7 @@ __global__ void __launch_bounds__(512) frac_bwd_state_kernel(ScanParams p, BwdWo
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int t = tb * 16 + lg * 4 + r, kk = kb * 16 + li;
-          hv[r] = (t >= kk) ? Gm[r] * D[r] : 0.0f;
+          hv[r] = keep_if_ge(Gm[r] * D[r], t, kk);
         }
         T* dst = HGT + (kb * 16 + li) * XS + tb * 16 + lg * 4;
 #pragma unroll
@@ -538,7 +538,7 @@ __global__ void __launch_bounds__(512) frac_bwd_state_kernel(ScanParams p, BwdWo
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
               const int t = tb * 16 + lg * 4 + r, kk = kb * 16 + li;
-              gv[r] = (t >= kk) ? gtile.get(jt, r) * Gm[r] : 0.0f;
+              gv[r] = keep_if_ge(gtile.get(jt, r) * Gm[r], t, kk);
             }
             store4(reinterpret_cast<T*>(wk.gg) + to, gv);
           }
@@ -555,7 +555,7 @@ __global__ void __launch_bounds__(512) frac_bwd_state_kernel(ScanParams p, BwdWo
 #pragma unroll
           for (int r = 0; r < 4; ++r) {
             const int t = tb * 16 + lg * 4 + r, kk = kb * 16 + li;
-            const float hm = (t >= kk) ? gtile.get(jt, r) * D[r] : 0.0f;
+            const float hm = keep_if_ge(gtile.get(jt, r) * D[r], t, kk);
             rv[r] = hm * Ph[r];
             ce += hm * Ph[r];
             cf += hm * Ps[r];

@@ -233,6 +233,12 @@ __device__ __forceinline__ void softmax_fast(float* z, int M) {
   for (int m = 0; m < MP; ++m) z[m] *= inv;
 }
 
+// x where row >= col, else +0: the mask is the sign of col - row - 1 spread over
+// all 32 bits, so no per-lane condition registers are formed (or kept live).
+__device__ __forceinline__ float keep_if_ge(float x, int row, int col) {
+  return __int_as_float(__float_as_int(x) & ((col - row - 1) >> 31));
+}
+
 // One DPP row permutation of a float (every lane of the wave active).
 template <int CTRL>
 __device__ __forceinline__ float dpp_move(float v) {

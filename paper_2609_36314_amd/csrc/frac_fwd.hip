@@ -420,7 +420,7 @@ __global__ void __launch_bounds__(512) frac_fwd_kernel(ScanParams p, const T* __
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int t = tb * 16 + lg * 4 + r, k = kb * 16 + li;
-          gv[r] = (t >= k) ? Gt[r] * Gm[r] : 0.0f;
+          gv[r] = keep_if_ge(Gt[r] * Gm[r], t, k);
         }
         T* dst = GGT + (kb * 16 + li) * GS + tb * 16 + lg * 4;
 #pragma unroll
