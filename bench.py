@@ -49,7 +49,7 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workloads", default="train-b4-l4096-m8,layer-fwd-b8-l2048,prefill-b1-l16384,"
+    ap.add_argument("--workloads", default="train-b4-l4096-m8,layer-fwd-b8-l2048,prefill-b1-l16384,paper-nfree-b8-l2048,"
                                            "decode-b256-128steps")
     ap.add_argument("--main", default="train-b4-l4096-m8")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -69,6 +69,12 @@ def fwd_flops_per_token_head(w):
 def bwd_flops_per_token_head(w):
     Q, P, N, M, G, H = w.chunk, w.headdim, w.dstate, w.nmodes, w.ngroups, w.nheads
     return 2 * (Q + 1) * P + 8 * M * N * P + 3 * (Q + 1) * N * G / H
+
+
+def nfree_fwd_bytes(w):
+    """Compulsory HBM bytes of the forward without B/C: x and y in the io dtype, dt."""
+    io = 2 if w.io_dtype == "bf16" else 4
+    return w.batch * w.seqlen * w.nheads * (2 * w.headdim * io + 4)
 
 
 def decode_bytes_per_step(w):
@@ -119,7 +125,7 @@ def bench_scan(torch, frac, w, steps, warmup):
     inp = device_inputs(torch, w)
     tau = frac.default_tau(w.nmodes, device="cuda")
     alpha = inp["alpha"]
-    x, dt, Bm, Cm = inp["x"], inp["dt"], inp["Bm"], inp["Cm"]
+    x, dt, Bm, Cm = inp["x"], inp["dt"], inp.get("Bm"), inp.get("Cm")
     y = torch.empty_like(x)
     fs = torch.empty((w.batch, w.nheads, w.nmodes, w.dstate, w.headdim), dtype=torch.float32,
                      device="cuda") if w.final_state else None
@@ -162,6 +168,8 @@ def bench_scan(torch, frac, w, steps, warmup):
         "fwd_ms": fms,
         "fwd_roofline": roofline("mfma", th * fwd_flops_per_token_head(w), fms, peak, "TFLOP/s"),
     }
+    if not w.bc:  # without B/C the forward moves more bytes than it does matrix-core work
+        res["fwd_roofline"] = roofline("hbm", nfree_fwd_bytes(w), fms, PEAK_HBM_BYTES, "GB/s")
     if w.backward:
         res["bwd_ms"] = bms
         res["bwd_roofline"] = dict(roofline("mfma", th * bwd_flops_per_token_head(w), bms, peak, "TFLOP/s"),

@@ -41,7 +41,12 @@
  *  - Supported sizes: headdim P and dstate N multiples of 8 with N <= 128;
  *    P <= 64 for the chunked scan (frac_scan_*), P <= 128 for frac_decode_step;
  *    1 <= nmodes <= 8 for the chunked scan, <= 32 for frac_decode_step;
- *    H % G == 0; chunk 0 (auto) or 64.  Anything else returns
+ *    H % G == 0; chunk 0 (auto) or 64.
+ *  - dstate 1 with Bm = Cm = NULL is the paper's own layer form without B/C
+ *    projections (B = C = 1; the recurrence of the Appendix-D algorithm, an
+ *    M x P state per head): frac_scan_fwd (P <= 256, nmodes <= 32, no workspace)
+ *    and frac_decode_step (P <= 256, nmodes <= 32); frac_scan_bwd returns
+ *    FRAC_ERR_UNSUPPORTED for it.  With dstate > 1, Bm and Cm are required.  Anything else returns
  *    FRAC_ERR_UNSUPPORTED (frac_scan_workspace_size returns 0).  batch or seqlen
  *    0 is a no-op.
  *  - The library keeps no state between calls; it is safe to call from several
@@ -78,6 +83,7 @@ typedef struct {
  *   x            [B,L,H,P] io_dtype        content input u_t (Algorithm input)
  *   dt           [B,L,H]   f32             step sizes Delta_t > 0, used verbatim (no clipping)
  *   Bm, Cm       [B,L,G,N] io_dtype        input / output projections of the widened state
+ *                (NULL with dstate 1: B = C = 1, the form without projections)
  *   alpha        f32, element (b,t,h) at alpha[b*s0 + t*s1 + h*s2] with s = alpha_stride;
  *                strides may be 0 to broadcast (a per-head alpha is strides {0,0,1}).
  *                Fractional order, 0 < alpha <= 1.  Required.

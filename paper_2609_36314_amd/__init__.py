@@ -78,13 +78,14 @@ def _stream():
 
 
 def _shape(x, Bm, nmodes, chunk, seqlen=None):
+    """Bm None: the form without B/C projections (dstate 1, B = C = 1)."""
     if x.dim() == 4:
         Bsz, L, H, P = x.shape
-        G, N = Bm.shape[2], Bm.shape[3]
+        G, N = (1, 1) if Bm is None else (Bm.shape[2], Bm.shape[3])
     else:
         Bsz, H, P = x.shape
         L = 1
-        G, N = Bm.shape[1], Bm.shape[2]
+        G, N = (1, 1) if Bm is None else (Bm.shape[1], Bm.shape[2])
     return FracShape(Bsz, L if seqlen is None else seqlen, H, P, N, G, nmodes, chunk, _io_dtype(x))
 
 
@@ -103,10 +104,12 @@ def default_tau(M: int, tau_min: float = TAU_MIN, tau_max: float = TAU_MAX, devi
 
 def _fwd_struct(x, dt, Bm, Cm, alpha, tau, lam, read_logit, write_logit, D, init_state, y, final_state):
     Bsz, L, H, P = x.shape
-    if Bm.dtype != x.dtype or Cm.dtype != x.dtype:
+    if (Bm is None) != (Cm is None):
+        raise TypeError("Bm and Cm are both given or both None (B = C = 1)")
+    if Bm is not None and (Bm.dtype != x.dtype or Cm.dtype != x.dtype):
         raise TypeError("x, Bm and Cm must share one dtype")
     for t, n in ((x, "x"), (Bm, "Bm"), (Cm, "Cm")):
-        if not t.is_contiguous():
+        if t is not None and not t.is_contiguous():
             raise ValueError("%s must be contiguous" % n)
     alpha_t, a_str = _strided(alpha, (Bsz, L, H), x.device, "alpha")
     lam_t, l_str = _strided(lam, (Bsz, L, H), x.device, "lambda")
@@ -126,14 +129,15 @@ def scan_fwd(x, dt, Bm, Cm, alpha, tau, *, lam=None, read_logit=None, write_logi
              init_state=None, return_final_state=False, chunk=0, y=None, final_state=None, workspace=None):
     """Chunked parallel scan, forward (frac_scan_fwd).
 
-    x [B,L,H,P], Bm/Cm [B,L,G,N] (float32 or bfloat16, one dtype); dt [B,L,H] f32;
+    x [B,L,H,P], Bm/Cm [B,L,G,N] (float32 or bfloat16, one dtype), or both None for the
+    form without B/C (B = C = 1, state [B,H,M,1,P], headdim <= 256, up to 32 modes); dt [B,L,H] f32;
     alpha, lam: float or f32 tensor broadcastable to [B,L,H]; read/write logits
     [B,L,H,M] f32; tau [M] f32; D [H] f32; init_state [B,H,M,N,P] f32.
     Returns y, or (y, final_state) when return_final_state."""
     M = int(tau.shape[0])
     shape = _shape(x, Bm, M, chunk)
     Bsz, L, H, P = x.shape
-    N = Bm.shape[3]
+    N = int(shape.dstate)
     if y is None:
         y = torch.empty_like(x)
     if return_final_state and final_state is None:
@@ -160,8 +164,8 @@ def scan_bwd(x, dt, Bm, Cm, alpha, tau, dy, *, lam=None, read_logit=None, write_
     if dy.dtype != x.dtype or not dy.is_contiguous():
         raise TypeError("dy must be contiguous with the dtype of x")
     fwd, keep = _fwd_struct(x, dt, Bm, Cm, alpha, tau, lam, read_logit, write_logit, D, init_state, None, None)
-    out = dict(dx=torch.empty_like(x), ddt=torch.empty_like(dt), dBm=torch.empty_like(Bm),
-               dCm=torch.empty_like(Cm), dD=None if D is None else torch.empty_like(D))
+    out = dict(dx=torch.empty_like(x), ddt=torch.empty_like(dt), dBm=None if Bm is None else torch.empty_like(Bm),
+               dCm=None if Cm is None else torch.empty_like(Cm), dD=None if D is None else torch.empty_like(D))
     a = FracBwdArgs()
     a.fwd = fwd
     a.dy, a.d_final_state = _ptr(dy), _ptr(_f32(d_final_state, "d_final_state"))
@@ -179,11 +183,13 @@ def scan_bwd(x, dt, Bm, Cm, alpha, tau, dy, *, lam=None, read_logit=None, write_
 def decode_step(state, x, dt, Bm, Cm, alpha, tau, *, lam=None, read_logit=None, write_logit=None, D=None,
                 y=None):
     """One decode token (frac_decode_step): updates `state` [B,H,M,N,P] f32 in place,
-    returns y [B,H,P].  x [B,H,P], dt [B,H], Bm/Cm [B,G,N]."""
+    returns y [B,H,P].  x [B,H,P], dt [B,H], Bm/Cm [B,G,N] (both None: B = C = 1, dstate 1)."""
     M = int(tau.shape[0])
     shape = _shape(x, Bm, M, 0, seqlen=1)
     Bsz, H, P = x.shape
-    if Bm.dtype != x.dtype or Cm.dtype != x.dtype:
+    if (Bm is None) != (Cm is None):
+        raise TypeError("Bm and Cm are both given or both None (B = C = 1)")
+    if Bm is not None and (Bm.dtype != x.dtype or Cm.dtype != x.dtype):
         raise TypeError("x, Bm and Cm must share one dtype")
     alpha_t, a_str = _strided(alpha, (Bsz, H), x.device, "alpha")
     lam_t, l_str = _strided(lam, (Bsz, H), x.device, "lambda")

@@ -50,10 +50,12 @@ frac_status fill_shape(const frac_shape* sh, frac::ScanParams& p) {
     return fail(FRAC_ERR_INVALID_ARG, "io_dtype %d is not a frac_dtype", (int)sh->io_dtype);
   if (sh->chunk != 0 && sh->chunk != 64) return fail(FRAC_ERR_UNSUPPORTED, "chunk %lld: only 64 (or 0 = auto) is built", (long long)sh->chunk);
   if (sh->nmodes > 32) return fail(FRAC_ERR_UNSUPPORTED, "nmodes %lld > 32", (long long)sh->nmodes);
-  if (sh->dstate % 8 || sh->dstate > 128)
-    return fail(FRAC_ERR_UNSUPPORTED, "dstate %lld: must be a multiple of 8 and <= 128", (long long)sh->dstate);
-  if (sh->headdim % 8 || sh->headdim > 128)
-    return fail(FRAC_ERR_UNSUPPORTED, "headdim %lld: must be a multiple of 8 and <= 128", (long long)sh->headdim);
+  if ((sh->dstate != 1 && sh->dstate % 8) || sh->dstate > 128)
+    return fail(FRAC_ERR_UNSUPPORTED, "dstate %lld: must be 1 or a multiple of 8 and <= 128", (long long)sh->dstate);
+  const int pmax = sh->dstate == 1 ? 256 : 128;  // the form without B/C takes wider heads
+  if (sh->headdim % 8 || sh->headdim > pmax)
+    return fail(FRAC_ERR_UNSUPPORTED, "headdim %lld: must be a multiple of 8 and <= %d", (long long)sh->headdim,
+                pmax);
   const int64_t lim = (int64_t)1 << 30;
   if (sh->batch > lim || sh->seqlen > lim || sh->nheads > lim || sh->batch * sh->nheads > lim)
     return fail(FRAC_ERR_UNSUPPORTED, "sizes beyond 2^30");
@@ -75,6 +77,13 @@ frac_status fill_shape(const frac_shape* sh, frac::ScanParams& p) {
 // The tiles of 64 tokens are addressed with 32-bit byte offsets: 64 rows of x
 // (H P elements apart) and of B, C (G N elements apart) must span < 2 GiB.
 frac_status check_scan_shape(const frac::ScanParams& p, const char* what) {
+  if (p.N == 1) {  // the form without B/C (B = C = 1): headdim <= 256, up to 32 modes
+    if (p.P > 256) return fail(FRAC_ERR_UNSUPPORTED, "%s: headdim %d > 256 is not built", what, p.P);
+    const int64_t es = p.io_bf16 ? 2 : 4;
+    if (64 * (int64_t)p.H * p.P * es >= ((int64_t)1 << 31))
+      return fail(FRAC_ERR_UNSUPPORTED, "%s: nheads * headdim too large", what);
+    return FRAC_OK;
+  }
   if (p.PP > 64) return fail(FRAC_ERR_UNSUPPORTED, "%s: headdim %d > 64 is not built", what, p.P);
   if (p.M > 8) return fail(FRAC_ERR_UNSUPPORTED, "%s: nmodes %d > 8 is not built", what, p.M);
   const int64_t es = p.io_bf16 ? 2 : 4, lim = (int64_t)1 << 31;
@@ -85,8 +94,10 @@ frac_status check_scan_shape(const frac::ScanParams& p, const char* what) {
 
 frac_status fill_fwd(const frac_fwd_args* a, frac::ScanParams& p, bool need_outputs) {
   if (!a) return fail(FRAC_ERR_INVALID_ARG, "args is NULL");
-  if (!a->x || !a->dt || !a->Bm || !a->Cm || !a->alpha || !a->tau)
-    return fail(FRAC_ERR_INVALID_ARG, "x, dt, Bm, Cm, alpha and tau are required");
+  if (!a->x || !a->dt || !a->alpha || !a->tau)
+    return fail(FRAC_ERR_INVALID_ARG, "x, dt, alpha and tau are required");
+  if (p.N == 1 ? (a->Bm || a->Cm) : (!a->Bm || !a->Cm))
+    return fail(FRAC_ERR_INVALID_ARG, "Bm and Cm are required for dstate > 1 and must be NULL for dstate 1");
   if (need_outputs && !a->y) return fail(FRAC_ERR_INVALID_ARG, "y is required");
   if (!aligned16(a->x) || !aligned16(a->Bm) || !aligned16(a->Cm) || !aligned16(a->init_state) ||
       (need_outputs && (!aligned16(a->y) || !aligned16(a->final_state))))
@@ -157,6 +168,7 @@ frac_status frac_default_tau(int M, double tau_min, double tau_max, float* out) 
 size_t frac_scan_workspace_size(const frac_shape* shape, int backward) {
   frac::ScanParams p{};
   if (fill_shape(shape, p) != FRAC_OK || check_scan_shape(p, "frac_scan_workspace_size") != FRAC_OK) return 0;
+  if (p.N == 1) return 0;  // the form without B/C needs no workspace (and has no backward)
   return backward ? frac::scan_bwd_workspace(p) : frac::scan_fwd_workspace(p);
 }
 
@@ -179,6 +191,7 @@ frac_status frac_scan_fwd(const frac_shape* shape, const frac_fwd_args* args, vo
   }
   s = fill_fwd(args, p, true);
   if (s != FRAC_OK) return s;
+  if (p.N == 1) return hip_status(frac::launch_nfree_fwd(p, st), "frac_scan_fwd launch");
   const size_t need = frac::scan_fwd_workspace(p);
   if (need && (!ws || ws_bytes < need))
     return fail(FRAC_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", need, ws ? ws_bytes : (size_t)0);
@@ -191,6 +204,7 @@ frac_status frac_scan_bwd(const frac_shape* shape, const frac_bwd_args* args, vo
   frac_status s = fill_shape(shape, p);
   if (s == FRAC_OK) s = check_scan_shape(p, "frac_scan_bwd");
   if (s != FRAC_OK) return s;
+  if (p.N == 1) return fail(FRAC_ERR_UNSUPPORTED, "frac_scan_bwd: the form without B/C (dstate 1) has no backward");
   if (p.Bsz == 0 || p.L == 0) {
     if (args && args->dD && p.Bsz >= 0) {
       hipLaunchKernelGGL(copy_or_zero_kernel, dim3(1), dim3(256), 0, reinterpret_cast<hipStream_t>(stream),
@@ -228,8 +242,10 @@ frac_status frac_decode_step(const frac_shape* shape, const frac_step_args* a, v
   if (shape->seqlen != 1) return fail(FRAC_ERR_INVALID_ARG, "frac_decode_step: shape.seqlen must be 1");
   if (p.Bsz == 0) return ok();
   if (!a) return fail(FRAC_ERR_INVALID_ARG, "args is NULL");
-  if (!a->x || !a->dt || !a->Bm || !a->Cm || !a->alpha || !a->tau || !a->state || !a->y)
-    return fail(FRAC_ERR_INVALID_ARG, "x, dt, Bm, Cm, alpha, tau, state and y are required");
+  if (!a->x || !a->dt || !a->alpha || !a->tau || !a->state || !a->y)
+    return fail(FRAC_ERR_INVALID_ARG, "x, dt, alpha, tau, state and y are required");
+  if (p.N == 1 ? (a->Bm || a->Cm) : (!a->Bm || !a->Cm))
+    return fail(FRAC_ERR_INVALID_ARG, "Bm and Cm are required for dstate > 1 and must be NULL for dstate 1");
   if (!aligned16(a->state)) return fail(FRAC_ERR_INVALID_ARG, "state must be 16-byte aligned");
   p.x = a->x;
   p.dt = a->dt;

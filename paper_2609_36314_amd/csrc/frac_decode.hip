@@ -26,7 +26,7 @@ __global__ void __launch_bounds__(kDecodeThreads) frac_decode_kernel(ScanParams 
   const int bh = blockIdx.x;
   const int b = bh / H, h = bh - b * H, g = h * p.G / H;
 
-  __shared__ float sB[128], sC[128], sx[128];
+  __shared__ float sB[128], sC[128], sx[256];
   __shared__ float s_rho[MP], s_kap[MP], s_c[MP];
   __shared__ float4 red[kDecodeThreads];
 
@@ -56,9 +56,9 @@ __global__ void __launch_bounds__(kDecodeThreads) frac_decode_kernel(ScanParams 
       s_c[m] = cw;
     }
   }
-  for (int i = tid; i < N; i += kDecodeThreads) {
-    sB[i] = to_f32(Bg[i]);
-    sC[i] = to_f32(Cg[i]);
+  for (int i = tid; i < N; i += kDecodeThreads) {  // without B/C (dstate 1) both are 1
+    sB[i] = p.Bm ? to_f32(Bg[i]) : 1.0f;
+    sC[i] = p.Cm ? to_f32(Cg[i]) : 1.0f;
   }
   for (int i = tid; i < P; i += kDecodeThreads) sx[i] = to_f32(x[i]);
   __syncthreads();

@@ -57,6 +57,9 @@ size_t scan_bwd_workspace(const ScanParams& p);
 
 hipError_t launch_decode_step(const ScanParams& p, float* state, hipStream_t stream);
 
+// The layer without B/C projections (dstate 1, B = C = 1): forward scan, no workspace.
+hipError_t launch_nfree_fwd(const ScanParams& p, hipStream_t stream);
+
 // True when a kernel variant exists for these sizes (M, N, P, dtype).
 bool scan_supported(const ScanParams& p, const char** why);
 

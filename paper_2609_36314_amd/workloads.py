@@ -9,9 +9,11 @@ state (decode), and for decode the per-step tokens step by step.
   alpha: a constant, or one value per head drawn from U[lo, hi]
   tau: the paper's geometric bank on [1, 2^17] (built by the library, not here)
   lambda, read/write logits and D are absent unless a test asks for them.
+  Without B/C projections (bc False, dstate 1): B = C = 1, nothing drawn for them.
 
 The named workloads are the five benchmark configurations of the Frac layer at
-the 1.3B-model layer shape (H = 64 heads, head dim 64, state 128, one B/C group).
+the 1.3B-model layer shape (H = 64 heads, head dim 64, state 128, one B/C group),
+and the paper's own layer form (no B/C, 16 heads of 256, 16 modes).
 """
 from __future__ import annotations
 
@@ -40,6 +42,7 @@ class Workload:
     decode_steps: int = 0              # > 0: decode workload (seqlen is 1 per step)
     init_state: bool = False
     extras: bool = False               # also draw lambda, logits and D (tests only)
+    bc: bool = True                    # False: the form without B/C (dstate 1, B = C = 1)
 
     def scaled(self, **kw) -> "Workload":
         return replace(self, **kw)
@@ -50,8 +53,10 @@ LAYER_FWD = Workload("layer-fwd-b8-l2048", 8, 2048, 64, 64, 128, 4)
 LONG_PREFILL = Workload("prefill-b1-l16384", 1, 16384, 64, 64, 128, 4, alpha_range=(0.3, 0.8), final_state=True)
 TRAIN = Workload("train-b4-l4096-m8", 4, 4096, 64, 64, 128, 8, backward=True)
 DECODE = Workload("decode-b256-128steps", 256, 1, 64, 64, 128, 4, decode_steps=128, init_state=True)
+# the paper's layer (state H x M x d_h, no B/C), forward at batch 8 x 2048 tokens
+PAPER_NFREE = Workload("paper-nfree-b8-l2048", 8, 2048, 16, 256, 1, 16, bc=False)
 
-WORKLOADS = {w.name: w for w in (TINY_F32, LAYER_FWD, LONG_PREFILL, TRAIN, DECODE)}
+WORKLOADS = {w.name: w for w in (TINY_F32, LAYER_FWD, LONG_PREFILL, TRAIN, DECODE, PAPER_NFREE)}
 
 
 def _softplus(v: np.ndarray) -> np.ndarray:
@@ -67,14 +72,16 @@ def generate(w: Workload, seed: int = 0) -> dict:
     if w.decode_steps:
         S = w.decode_steps
         out["x"] = rng.standard_normal((S, Bsz, H, P), dtype=f32)
-        out["Bm"] = (rng.standard_normal((S, Bsz, G, N), dtype=f32) / np.sqrt(N)).astype(f32)
-        out["Cm"] = (rng.standard_normal((S, Bsz, G, N), dtype=f32) / np.sqrt(N)).astype(f32)
+        if w.bc:
+            out["Bm"] = (rng.standard_normal((S, Bsz, G, N), dtype=f32) / np.sqrt(N)).astype(f32)
+            out["Cm"] = (rng.standard_normal((S, Bsz, G, N), dtype=f32) / np.sqrt(N)).astype(f32)
         out["dt"] = _softplus(rng.standard_normal((S, Bsz, H), dtype=f32) - 2.0)
     else:
         L = w.seqlen
         out["x"] = rng.standard_normal((Bsz, L, H, P), dtype=f32)
-        out["Bm"] = (rng.standard_normal((Bsz, L, G, N), dtype=f32) / np.sqrt(N)).astype(f32)
-        out["Cm"] = (rng.standard_normal((Bsz, L, G, N), dtype=f32) / np.sqrt(N)).astype(f32)
+        if w.bc:
+            out["Bm"] = (rng.standard_normal((Bsz, L, G, N), dtype=f32) / np.sqrt(N)).astype(f32)
+            out["Cm"] = (rng.standard_normal((Bsz, L, G, N), dtype=f32) / np.sqrt(N)).astype(f32)
         out["dt"] = _softplus(rng.standard_normal((Bsz, L, H), dtype=f32) - 2.0)
     if w.alpha_range is not None:
         out["alpha"] = rng.uniform(w.alpha_range[0], w.alpha_range[1], H).astype(f32)

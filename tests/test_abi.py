@@ -63,6 +63,7 @@ def _shape(**kw):
     (dict(io_dtype=7), -1),
     (dict(nmodes=9), -2),
     (dict(nmodes=33), -2),
+    (dict(dstate=1, headdim=264), -2),
     (dict(dstate=12), -2),
     (dict(dstate=256), -2),
     (dict(headdim=20), -2),
@@ -123,3 +124,18 @@ def test_decode_mode_range_is_checked_on_the_host(nmodes, status):
     sh = _shape(seqlen=1, nmodes=nmodes)
     a = FracStepArgs()
     assert lib.frac_decode_step(ctypes.byref(sh), ctypes.byref(a), None) == status
+
+
+def test_projection_free_form_checks_its_arguments_on_the_host():
+    """dstate 1 means B = C = 1: Bm and Cm must be NULL there (and are required
+    otherwise); its backward is reported unsupported; it needs no workspace."""
+    lib = _lib.load()
+    sh = _shape(dstate=1, headdim=256, nmodes=16)
+    assert lib.frac_scan_workspace_size(ctypes.byref(sh), 0) == 0
+    a = FracFwdArgs()
+    buf = (ctypes.c_float * 64)()
+    a.x = a.dt = a.alpha = a.tau = a.y = ctypes.cast(buf, ctypes.c_void_p)
+    a.Bm = ctypes.cast(buf, ctypes.c_void_p)  # given although dstate is 1
+    assert lib.frac_scan_fwd(ctypes.byref(sh), ctypes.byref(a), None, 0, None) == -1
+    b = FracBwdArgs()
+    assert lib.frac_scan_bwd(ctypes.byref(sh), ctypes.byref(b), None, 0, None) == -2

@@ -1,0 +1,131 @@
+"""GPU parity of the paper's own layer form -- no B/C projections (dstate 1,
+B = C = 1), an M x d_h state per head -- against the float64 oracle run with
+B = C = 1: the forward scan (frac_scan_fwd with Bm = Cm = NULL) and the decode
+step (frac_decode_step with Bm = Cm = NULL)."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2609_36314_amd as frac
+from paper_2609_36314_amd.workloads import PAPER_NFREE, Workload
+from harness import TOL, assert_close, device_inputs, f64
+
+pytestmark = pytest.mark.gpu
+
+
+def _tau(M):
+    t32 = oracle.default_tau(M).astype(np.float32)
+    return torch.from_numpy(t32).cuda(), t32.astype(np.float64)
+
+
+def _oracle_fwd(inp, tau64, sl=None):
+    x, dt = f64(inp["x"]), f64(inp["dt"])
+    g = lambda k: None if inp.get(k) is None else f64(inp[k])
+    kw = dict(lam=g("lam"), read_logit=g("read_logit"), write_logit=g("write_logit"), D=g("D"),
+              init_state=g("init_state"))
+    a = inp["alpha"]
+    alpha = np.broadcast_to(f64(a) if not isinstance(a, torch.Tensor) or a.dim() != 1 else f64(a)[None, None, :],
+                            dt.shape)
+    if sl is not None:
+        b, h = sl
+        x, dt, alpha = x[b:b + 1, :, h:h + 1], dt[b:b + 1, :, h:h + 1], alpha[b:b + 1, :, h:h + 1]
+        for k in ("lam", "read_logit", "write_logit"):
+            if kw[k] is not None:
+                kw[k] = kw[k][b:b + 1, :, h:h + 1]
+        if kw["D"] is not None:
+            kw["D"] = kw["D"][h:h + 1]
+        if kw["init_state"] is not None:
+            kw["init_state"] = kw["init_state"][b:b + 1, h:h + 1]
+    ones = np.ones(x.shape[:2] + (1, 1))
+    return oracle.forward(x, dt, ones, ones, alpha, tau64, **kw)
+
+
+def _run(inp, tau_d):
+    kw = {k: inp[k] for k in ("lam", "read_logit", "write_logit", "D", "init_state") if k in inp}
+    return frac.scan_fwd(inp["x"], inp["dt"], None, None, inp["alpha"], tau_d, return_final_state=True, **kw)
+
+
+SMALL = {
+    "bf16 paper shape M16 P256 extras": Workload("t", 2, 300, 3, 256, 1, 16, bc=False, extras=True, init_state=True,
+                                                 final_state=True),
+    "f32 M4 P64": Workload("t", 1, 200, 2, 64, 1, 4, bc=False, io_dtype="f32", final_state=True),
+    "bf16 M32 P128": Workload("t", 1, 130, 2, 128, 1, 32, bc=False, final_state=True, init_state=True),
+    "bf16 M8 P40 ragged": Workload("t", 2, 70, 2, 40, 1, 8, bc=False, final_state=True, extras=True),
+    "f32 M11 P96 extras": Workload("t", 1, 129, 2, 96, 1, 11, bc=False, io_dtype="f32", extras=True,
+                                   init_state=True, final_state=True),
+    "bf16 M16 L1": Workload("t", 2, 1, 2, 256, 1, 16, bc=False, final_state=True, init_state=True),
+}
+
+
+@pytest.mark.parametrize("name", list(SMALL))
+def test_nfree_fwd_parity(name):
+    w = SMALL[name]
+    inp = device_inputs(w, seed=11)
+    tau_d, tau64 = _tau(w.nmodes)
+    print("case", name, w, flush=True)
+    y, fs = _run(inp, tau_d)
+    torch.cuda.synchronize()
+    yr, fsr = _oracle_fwd(inp, tau64)
+    tol = TOL[w.io_dtype]
+    assert_close("y", f64(y), yr, tol)
+    for m in range(w.nmodes):
+        assert_close("final_state mode %d" % m, f64(fs)[:, :, m], fsr[:, :, m], tol)
+
+
+def test_nfree_large_steps_use_direct_decay():
+    """Steps large enough that the fast modes pass the factorisation bound."""
+    w = Workload("t", 1, 140, 2, 64, 1, 16, bc=False, final_state=True)
+    inp = device_inputs(w, seed=12)
+    inp["dt"] = (inp["dt"] * 8.0).contiguous()
+    tau_d, tau64 = _tau(16)
+    y, fs = _run(inp, tau_d)
+    torch.cuda.synchronize()
+    yr, fsr = _oracle_fwd(inp, tau64)
+    assert_close("y", f64(y), yr, TOL["bf16"])
+    for m in range(16):
+        assert_close("final_state mode %d" % m, f64(fs)[:, :, m], fsr[:, :, m], TOL["bf16"])
+
+
+def test_nfree_full_size_sampled():
+    """The paper-shape workload at full size; the oracle recomputes sampled (batch, head) slices."""
+    w = PAPER_NFREE
+    inp = device_inputs(w, seed=0)
+    tau_d, tau64 = _tau(w.nmodes)
+    print("full-size", w.name, flush=True)
+    y = frac.scan_fwd(inp["x"], inp["dt"], None, None, inp["alpha"], tau_d)
+    torch.cuda.synchronize()
+    assert torch.isfinite(y.float()).all()
+    for (b, h) in [(0, 0), (7, 15), (3, 9)]:
+        yr, _ = _oracle_fwd(inp, tau64, sl=(b, h))
+        assert_close("y[%d,:,%d]" % (b, h), f64(y[b:b + 1, :, h:h + 1]), yr, TOL["bf16"])
+
+
+def test_nfree_decode_matches_oracle_steps():
+    """Decode steps without B/C from a random state equal the oracle's recurrence."""
+    w = Workload("t", 2, 1, 3, 256, 1, 16, bc=False, decode_steps=4, init_state=True, extras=True)
+    a = device_inputs(w, seed=13)
+    tau_d, tau64 = _tau(16)
+    state = a["init_state"].clone()
+    ref = f64(state)
+    alpha = a["alpha"]  # [S, B, H] per step with extras
+    for s in range(w.decode_steps):
+        y = frac.decode_step(state, a["x"][s].contiguous(), a["dt"][s].contiguous(), None, None,
+                             alpha[s].contiguous(), tau_d, lam=a["lam"][s].contiguous(),
+                             read_logit=a["read_logit"][s].contiguous(), write_logit=a["write_logit"][s].contiguous(),
+                             D=a["D"])
+        torch.cuda.synchronize()
+        ones = np.ones((w.batch, 1, 1))
+        yr, ref = oracle.decode_step(ref, f64(a["x"][s]), f64(a["dt"][s]), ones, ones, f64(alpha[s]), tau64,
+                                     lam=f64(a["lam"][s]), read_logit=f64(a["read_logit"][s]),
+                                     write_logit=f64(a["write_logit"][s]), D=f64(a["D"]))
+        assert_close("decode y step %d" % s, f64(y), yr, TOL["bf16"])
+        assert_close("decode state step %d" % s, f64(state), ref, TOL["bf16"])
+
+
+def test_nfree_backward_is_reported_unsupported():
+    w = Workload("t", 1, 64, 2, 64, 1, 4, bc=False)
+    inp = device_inputs(w, seed=14)
+    tau_d, _ = _tau(4)
+    with pytest.raises(frac.FracError):
+        frac.scan_bwd(inp["x"], inp["dt"], None, None, inp["alpha"], tau_d, inp["x"])
