@@ -161,8 +161,8 @@ __device__ __forceinline__ int pair_weights(const ChunkCtl& k, int t0, int nv, i
     const float ea = fexp(-r * A);
     const float ep = (ROLE == kState && safe) ? fexp(r * A) : 0.0f;
     const float dec = fexp(-r * (k.Alast - A));
-    float* o = w + m * kQ + t;
-    constexpr int SW = MP * kQ;  // stride of the weight arrays
+    float* o = w + m * kWQ + t;
+    constexpr int SW = MP * kWQ;  // stride of the weight arrays
     if constexpr (ROLE == kState) {
       const float rwr = r * ww * (1.0f - beta);
       o[0 * SW] = cw * ea;
@@ -199,8 +199,8 @@ __device__ __forceinline__ floatx4 rank_m_tile(const float* a, const float* bm, 
 #pragma unroll
   for (int q = 0; q < (MP + 3) / 4; ++q) {
     const int m = q * 4 + lg;
-    const float av = (m < MP) ? a[m * kQ + row0 + li] : 0.0f;
-    const float bv = (m < MP) ? bm[m * kQ + col0 + li] : 0.0f;
+    const float av = (m < MP) ? a[m * kWQ + row0 + li] : 0.0f;
+    const float bv = (m < MP) ? bm[m * kWQ + col0 + li] : 0.0f;
     acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av, bv, acc, 0, 0, 0);
   }
   return acc;
@@ -218,7 +218,7 @@ __device__ __forceinline__ void unsafe_terms(floatx4& acc, int unsafe, const flo
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       const int t = tb * 16 + lg * 4 + r, k = kb * 16 + li;
-      if (t >= k) acc[r] += (scale_r ? rm : 1.0f) * a[m * kQ + t] * bm[m * kQ + k] * fexp(-rm * (A[t] - A[k]));
+      if (t >= k) acc[r] += (scale_r ? rm : 1.0f) * a[m * kWQ + t] * bm[m * kWQ + k] * fexp(-rm * (A[t] - A[k]));
     }
   }
 }
@@ -348,7 +348,7 @@ __global__ void __launch_bounds__(512) frac_bwd_state_kernel(ScanParams p, BwdWo
   __shared__ __align__(16) T Cb[64 * CS];
   constexpr int NWA = n_weight_arrays<kState>();
   constexpr int oHG = 0;                                         // T [k][t] (Gamma o dY X^T)^T, causal
-  constexpr int WSZ = NWA * MP * kQ + kQ;                        // one chunk's weights [NWA][MP][Q], A [Q]
+  constexpr int WSZ = NWA * MP * kWQ + kQ;                        // one chunk's weights [NWA][MP][Q], A [Q]
   // two chunks' weights (the next one formed during this one's update) when LDS allows
   constexpr int kTileBytes = (Cfg::NBUF * 64 * (2 * XS + BS) + 64 * CS) * (int)sizeof(T);
   constexpr int kFixed = 64 * XS * (int)sizeof(T) + (3 * kTiles * 16 + 8 * kQ + Ex::kFloats + 4 * MP) * 4;
@@ -370,7 +370,7 @@ __global__ void __launch_bounds__(512) frac_bwd_state_kernel(ScanParams p, BwdWo
   float* s_rr = reinterpret_cast<float*>(sm + oSc);
   float* s_lnt = s_rr + MP;
   float* s_E2 = s_lnt + MP;
-  constexpr int SW = MP * kQ;  // stride of the weight arrays
+  constexpr int SW = MP * kWQ;  // stride of the weight arrays
 
   if (tid < MP) {
     const float tau = (tid < M) ? p.tau[tid] : 1.0f;
@@ -462,7 +462,7 @@ __global__ void __launch_bounds__(512) frac_bwd_state_kernel(ScanParams p, BwdWo
   auto weights = [&](int c, float* Wd) __attribute__((always_inline)) {
     const int t0 = c * kQ, nv = min(kQ, L - t0);
     const ChunkCtl k = chunk_controls(dt_n, al_n, lam_n, lm_bh != nullptr, nv);
-    if (wave == 0) Wd[NWA * MP * kQ + lane] = k.A;
+    if (wave == 0) Wd[NWA * MP * kWQ + lane] = k.A;
     unsafe_c = pair_weights<MP, kState>(k, t0, nv, M, rl_bh, wl_bh, lg_st, s_rr, s_lnt, s_E2 + (c & 1) * MP,
                                         s_E2 + ((c + 1) & 1) * MP, Wd);
     alast_c = k.Alast;
@@ -485,7 +485,7 @@ __global__ void __launch_bounds__(512) frac_bwd_state_kernel(ScanParams p, BwdWo
     const float* P_c = W + 6 * SW;
     const float* P_k = W + 7 * SW;
     const float* P_wr = W + 8 * SW;
-    const float* P_A = W + NWA * MP * kQ;
+    const float* P_A = W + NWA * MP * kWQ;
     wait_vmem();
     barrier();  // this chunk's tiles and weights have landed; the previous chunk is done
     if (Cfg::NBUF == 2) {
@@ -603,7 +603,7 @@ __global__ void __launch_bounds__(512) frac_bwd_state_kernel(ScanParams p, BwdWo
             floatx4 U = {0.f, 0.f, 0.f, 0.f};
             mma(U, Sa[m][0], y0);
             mma(U, Sa[m][1], y1);
-            const float wd = P_wdc[(mo + m) * kQ + tb * 16 + li];
+            const float wd = P_wdc[(mo + m) * kWQ + tb * 16 + li];
             const float rm = s_rr[mo + m];
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
@@ -705,7 +705,7 @@ __global__ void __launch_bounds__(512) frac_bwd_state_kernel(ScanParams p, BwdWo
       for (int s = 0; s < 8; ++s) b8[s] = to_f32(bf.v[s]);
 #pragma unroll
       for (int m = 0; m < MPF; ++m) {
-        const float* pv = P_v + (mo + m) * kQ + kt * 32 + lg * 8;
+        const float* pv = P_v + (mo + m) * kWQ + kt * 32 + lg * 8;
         const float4 v0 = *reinterpret_cast<const float4*>(pv);
         const float4 v1 = *reinterpret_cast<const float4*>(pv + 4);
         Frag<T> Bv;
@@ -795,17 +795,17 @@ __global__ void __launch_bounds__(512) frac_bwd_cols_kernel(ScanParams p, BwdWor
   constexpr int NWA = n_weight_arrays<kCols>();
   constexpr int oHG = 0;                                         // T [t][k] Gamma o dY X^T, causal
   constexpr int oW = oHG + 64 * XS * (int)sizeof(T);
-  constexpr int oEx = oW + (NWA * MP * kQ + kQ) * 4;
+  constexpr int oEx = oW + (NWA * MP * kWQ + kQ) * 4;
   constexpr int oSc = oEx + Ex::kFloats * 4;
   __shared__ __align__(16) unsigned char sm[oSc + 4 * MP * 4];
   T* HG = reinterpret_cast<T*>(sm + oHG);
   float* W = reinterpret_cast<float*>(sm + oW);
-  float* P_A = W + NWA * MP * kQ;
+  float* P_A = W + NWA * MP * kWQ;
   float* XCH = reinterpret_cast<float*>(sm + oEx);
   float* s_rr = reinterpret_cast<float*>(sm + oSc);
   float* s_lnt = s_rr + MP;
   float* s_E2 = s_lnt + MP;
-  constexpr int SW = MP * kQ;  // stride of the weight arrays
+  constexpr int SW = MP * kWQ;  // stride of the weight arrays
   const float* P_wdb = W;
   const float* P_om = W + 1 * SW;
 
@@ -948,7 +948,7 @@ __global__ void __launch_bounds__(512) frac_bwd_cols_kernel(ScanParams p, BwdWor
           floatx4 V = {0.f, 0.f, 0.f, 0.f};
           mma(V, Ga[m][0], x0);
           mma(V, Ga[m][1], x1);
-          const float wb = P_wdb[(mo + m) * kQ + tb * 16 + li];
+          const float wb = P_wdb[(mo + m) * kWQ + tb * 16 + li];
 #pragma unroll
           for (int r = 0; r < 4; ++r) dBa[tb][r] += wb * V[r];
         }
@@ -995,7 +995,7 @@ __global__ void __launch_bounds__(512) frac_bwd_cols_kernel(ScanParams p, BwdWor
       for (int s = 0; s < 8; ++s) c8[s] = to_f32(cf.v[s]);
 #pragma unroll
       for (int m = 0; m < MPF; ++m) {
-        const float* pv = P_om + (mo + m) * kQ + kt * 32 + lg * 8;
+        const float* pv = P_om + (mo + m) * kWQ + kt * 32 + lg * 8;
         const float4 v0 = *reinterpret_cast<const float4*>(pv);
         const float4 v1 = *reinterpret_cast<const float4*>(pv + 4);
         Frag<T> Cv;
@@ -1074,21 +1074,21 @@ __global__ void __launch_bounds__(512) frac_bwd_rows_kernel(ScanParams p, BwdWor
   constexpr int oGG = 0;                                         // T [t'][k] (C B^T) o Gamma, causal
   constexpr int oDx = oGG + 64 * XS * (int)sizeof(T);            // T [t][p] dx rows of the previous chunk (bf16)
   constexpr int oW = oDx + (Cfg::kBf16 ? 64 * XS * (int)sizeof(T) : 0);
-  constexpr int oRd = oW + (NWA * MP * kQ + kQ) * 4;             // float [2][8][Q] token partials of e, f
+  constexpr int oRd = oW + (NWA * MP * kWQ + kQ) * 4;             // float [2][8][Q] token partials of e, f
   constexpr int oEx = oRd + 2 * 8 * kQ * 4;
   constexpr int oSc = oEx + Ex::kFloats * 4;
   __shared__ __align__(16) unsigned char sm[oSc + 4 * MP * 4];
   T* GG = reinterpret_cast<T*>(sm + oGG);
   T* Dxb = reinterpret_cast<T*>(sm + oDx);
   float* W = reinterpret_cast<float*>(sm + oW);
-  float* P_A = W + NWA * MP * kQ;
+  float* P_A = W + NWA * MP * kWQ;
   float* redE = reinterpret_cast<float*>(sm + oRd);
   float* redF = redE + 8 * kQ;
   float* XCH = reinterpret_cast<float*>(sm + oEx);
   float* s_rr = reinterpret_cast<float*>(sm + oSc);
   float* s_lnt = s_rr + MP;
   float* s_E2 = s_lnt + MP;
-  constexpr int SW = MP * kQ;  // stride of the weight arrays
+  constexpr int SW = MP * kWQ;  // stride of the weight arrays
   const float* P_wdx = W;  // times r_m: the adjoint weight of e
   const float* P_wfk = W + 1 * SW;
   const float* P_om = W + 2 * SW;
@@ -1275,7 +1275,7 @@ __global__ void __launch_bounds__(512) frac_bwd_rows_kernel(ScanParams p, BwdWor
               floatx4 Z = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
               for (int kb = 0; kb < KBW; ++kb) mma(Z, Gf[kb], Ba[q][kb]);
-              const int o = (mo + m) * kQ + tb * 16 + li;
+              const int o = (mo + m) * kWQ + tb * 16 + li;
               const float wx = P_wdx[o], wf = P_wfk[o], rwx = rm * wx;
 #pragma unroll
               for (int r = 0; r < 4; ++r) {
@@ -1363,7 +1363,7 @@ __global__ void __launch_bounds__(512) frac_bwd_rows_kernel(ScanParams p, BwdWor
       Frag<T> Yf[MPW];
 #pragma unroll
       for (int m = 0; m < MPW; ++m) {
-        const float* pv = P_om + (mo + m) * kQ + kt * 32 + lg * 8;
+        const float* pv = P_om + (mo + m) * kWQ + kt * 32 + lg * 8;
         const float4 v0 = *reinterpret_cast<const float4*>(pv);
         const float4 v1 = *reinterpret_cast<const float4*>(pv + 4);
         frag_set(Yf[m], 0, to_f32(yf.v[0]) * v0.x);

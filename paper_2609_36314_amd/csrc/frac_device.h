@@ -14,6 +14,10 @@ typedef float floatx4 __attribute__((ext_vector_type(4)));
 
 constexpr int kWave = 64;
 constexpr int kQ = 64;  // tokens per chunk
+// Row stride (floats) of the per-(token, mode) weight arrays [mode][token] in LDS:
+// 68 puts the stores of one wave (lanes = a few tokens x all modes) and the
+// 16-lane row reads of 4 modes into distinct banks; rows stay 16-byte aligned.
+constexpr int kWQ = kQ + 4;
 
 // ---------------------------------------------------------------- fragments
 //

@@ -205,7 +205,7 @@ __global__ void __launch_bounds__(512) frac_fwd_kernel(ScanParams p, const T* __
   constexpr int oYb = oGG + 64 * GS * (int)sizeof(T);           // T [64][XS] output rows of the previous chunk
   constexpr int oPrm = oYb + 64 * XS * (int)sizeof(T);          // float [6 MP + 1][Q] per-token weights
   constexpr int NSLOT = 4 - Cfg::TBO;                           // row blocks a wave hands over
-  constexpr int oYX = oPrm + (6 * MP * kQ + kQ) * 4;            // float [8 waves][NSLOT][4][64] readout exchange
+  constexpr int oYX = oPrm + (6 * MP * kWQ + kQ) * 4;            // float [8 waves][NSLOT][4][64] readout exchange
   constexpr int oSc = oYX + (NPART > 1 ? 8 * NSLOT * 256 : 4) * 4;  // float rates, log tau, scales
   __shared__ __align__(16) unsigned char sm[oSc + 4 * MP * 4];
   T* GGT = reinterpret_cast<T*>(sm + oGG);
@@ -216,12 +216,12 @@ __global__ void __launch_bounds__(512) frac_fwd_kernel(ScanParams p, const T* __
   float* s_lnt = s_rr + MP;
   float* s_E2 = s_lnt + MP;  // [2][MP] by chunk parity
   float* P_om = prm;              // [MP][Q] c e^{-rA_t} E_m        (readout)
-  float* P_v = P_om + MP * kQ;    // [MP][Q] kappa e^{-r(A_Q-A_t)} upd (update)
-  float* P_O = P_v + MP * kQ;     // [MP][Q] c e^{-r A_t}            (Gamma rows)
-  float* P_Vt = P_O + MP * kQ;    // [MP][Q] kappa e^{r A_t}, safe modes (Gamma columns)
-  float* P_c = P_Vt + MP * kQ;    // [MP][Q] c      (modes past the factorisation bound)
-  float* P_k = P_c + MP * kQ;     // [MP][Q] kappa
-  float* P_A = P_k + MP * kQ;     // [Q] A_t
+  float* P_v = P_om + MP * kWQ;    // [MP][Q] kappa e^{-r(A_Q-A_t)} upd (update)
+  float* P_O = P_v + MP * kWQ;     // [MP][Q] c e^{-r A_t}            (Gamma rows)
+  float* P_Vt = P_O + MP * kWQ;    // [MP][Q] kappa e^{r A_t}, safe modes (Gamma columns)
+  float* P_c = P_Vt + MP * kWQ;    // [MP][Q] c      (modes past the factorisation bound)
+  float* P_k = P_c + MP * kWQ;     // [MP][Q] kappa
+  float* P_A = P_k + MP * kWQ;     // [Q] A_t
 
   const T* xg = reinterpret_cast<const T*>(p.x) + (((int64_t)b * L) * H + h) * P;
   const T* Bgp = reinterpret_cast<const T*>(p.Bm) + (((int64_t)b * L) * G + g) * N;
@@ -366,12 +366,12 @@ __global__ void __launch_bounds__(512) frac_fwd_kernel(ScanParams p, const T* __
       const float upd = ren ? 1.0f : __frcp_rn(Enew);
       const float kap = one_minus_exp_neg(dtt * r) * ww;
       const float om = cw * fexp(-r * A);
-      P_O[m * kQ + t] = om;
-      P_om[m * kQ + t] = om * Ecur[m];
-      P_v[m * kQ + t] = kap * fexp(-r * (Alast - A)) * upd;
-      P_Vt[m * kQ + t] = safe ? kap * fexp(r * A) : 0.0f;
-      P_c[m * kQ + t] = cw;
-      P_k[m * kQ + t] = kap;
+      P_O[m * kWQ + t] = om;
+      P_om[m * kWQ + t] = om * Ecur[m];
+      P_v[m * kWQ + t] = kap * fexp(-r * (Alast - A)) * upd;
+      P_Vt[m * kWQ + t] = safe ? kap * fexp(r * A) : 0.0f;
+      P_c[m * kWQ + t] = cw;
+      P_k[m * kWQ + t] = kap;
       if (pr < MP) Enext[m] = ren ? 1.0f : Enew;
     }
     // this wave's modes: rescale flags and factors (wave-uniform)
@@ -401,8 +401,8 @@ __global__ void __launch_bounds__(512) frac_fwd_kernel(ScanParams p, const T* __
 #pragma unroll
         for (int q = 0; q < (MP + 3) / 4; ++q) {
           const int m = q * 4 + lg;
-          const float av = (m < MP) ? P_O[m * kQ + tb * 16 + li] : 0.0f;
-          const float bv = (m < MP) ? P_Vt[m * kQ + kb * 16 + li] : 0.0f;
+          const float av = (m < MP) ? P_O[m * kWQ + tb * 16 + li] : 0.0f;
+          const float bv = (m < MP) ? P_Vt[m * kWQ + kb * 16 + li] : 0.0f;
           Gm = __builtin_amdgcn_mfma_f32_16x16x4f32(av, bv, Gm, 0, 0, 0);
         }
         if (unsafe) {
@@ -412,7 +412,7 @@ __global__ void __launch_bounds__(512) frac_fwd_kernel(ScanParams p, const T* __
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
               const int t = tb * 16 + lg * 4 + r, k = kb * 16 + li;
-              if (t >= k) Gm[r] += P_c[m * kQ + t] * P_k[m * kQ + k] * fexp(-rm * (P_A[t] - P_A[k]));
+              if (t >= k) Gm[r] += P_c[m * kWQ + t] * P_k[m * kWQ + k] * fexp(-rm * (P_A[t] - P_A[k]));
             }
           }
         }
@@ -462,7 +462,7 @@ __global__ void __launch_bounds__(512) frac_fwd_kernel(ScanParams p, const T* __
           floatx4 Z = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
           for (int kb = 0; kb < KBW; ++kb) mma(Z, Ca[i][kb], Sf[kb]);
-          const float4 om = *reinterpret_cast<const float4*>(P_om + (mo + m) * kQ + tb * 16 + lg * 4);
+          const float4 om = *reinterpret_cast<const float4*>(P_om + (mo + m) * kWQ + tb * 16 + lg * 4);
           Y[tb][0] += om.x * Z[0];
           Y[tb][1] += om.y * Z[1];
           Y[tb][2] += om.z * Z[2];
@@ -529,7 +529,7 @@ __global__ void __launch_bounds__(512) frac_fwd_kernel(ScanParams p, const T* __
       Frag<T> Xf[MPW];
 #pragma unroll
       for (int m = 0; m < MPW; ++m) {
-        const float* pv = P_v + (mo + m) * kQ + kt * 32 + lg * 8;
+        const float* pv = P_v + (mo + m) * kWQ + kt * 32 + lg * 8;
         const float4 v0 = *reinterpret_cast<const float4*>(pv);
         const float4 v1 = *reinterpret_cast<const float4*>(pv + 4);
         frag_set(Xf[m], 0, to_f32(xf.v[0]) * v0.x);
