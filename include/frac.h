@@ -45,8 +45,9 @@
  *  - dstate 1 with Bm = Cm = NULL is the paper's own layer form without B/C
  *    projections (B = C = 1; the recurrence of the Appendix-D algorithm, an
  *    M x P state per head): frac_scan_fwd (P <= 256, nmodes <= 32, no workspace)
- *    and frac_decode_step (P <= 256, nmodes <= 32); frac_scan_bwd returns
- *    FRAC_ERR_UNSUPPORTED for it.  With dstate > 1, Bm and Cm are required.  Anything else returns
+ *    and frac_decode_step (P <= 256, nmodes <= 32), and frac_scan_bwd (dBm = dCm
+ *    = NULL; workspace from frac_scan_workspace_size).  With dstate > 1, Bm and
+ *    Cm (and dBm, dCm) are required.  Anything else returns
  *    FRAC_ERR_UNSUPPORTED (frac_scan_workspace_size returns 0).  batch or seqlen
  *    0 is a no-op.
  *  - The library keeps no state between calls; it is safe to call from several

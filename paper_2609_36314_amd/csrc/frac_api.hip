@@ -168,7 +168,7 @@ frac_status frac_default_tau(int M, double tau_min, double tau_max, float* out) 
 size_t frac_scan_workspace_size(const frac_shape* shape, int backward) {
   frac::ScanParams p{};
   if (fill_shape(shape, p) != FRAC_OK || check_scan_shape(p, "frac_scan_workspace_size") != FRAC_OK) return 0;
-  if (p.N == 1) return 0;  // the form without B/C needs no workspace (and has no backward)
+  if (p.N == 1) return backward ? frac::nfree_bwd_workspace(p) : 0;  // the form without B/C
   return backward ? frac::scan_bwd_workspace(p) : frac::scan_fwd_workspace(p);
 }
 
@@ -204,7 +204,6 @@ frac_status frac_scan_bwd(const frac_shape* shape, const frac_bwd_args* args, vo
   frac_status s = fill_shape(shape, p);
   if (s == FRAC_OK) s = check_scan_shape(p, "frac_scan_bwd");
   if (s != FRAC_OK) return s;
-  if (p.N == 1) return fail(FRAC_ERR_UNSUPPORTED, "frac_scan_bwd: the form without B/C (dstate 1) has no backward");
   if (p.Bsz == 0 || p.L == 0) {
     if (args && args->dD && p.Bsz >= 0) {
       hipLaunchKernelGGL(copy_or_zero_kernel, dim3(1), dim3(256), 0, reinterpret_cast<hipStream_t>(stream),
@@ -216,8 +215,10 @@ frac_status frac_scan_bwd(const frac_shape* shape, const frac_bwd_args* args, vo
   if (!args) return fail(FRAC_ERR_INVALID_ARG, "args is NULL");
   s = fill_fwd(&args->fwd, p, false);
   if (s != FRAC_OK) return s;
-  if (!args->dy || !args->dx || !args->ddt || !args->dBm || !args->dCm)
-    return fail(FRAC_ERR_INVALID_ARG, "dy, dx, ddt, dBm and dCm are required");
+  if (!args->dy || !args->dx || !args->ddt)
+    return fail(FRAC_ERR_INVALID_ARG, "dy, dx and ddt are required");
+  if (p.N == 1 ? (args->dBm || args->dCm) : (!args->dBm || !args->dCm))
+    return fail(FRAC_ERR_INVALID_ARG, "dBm and dCm are required for dstate > 1 and must be NULL for dstate 1");
   if (!aligned16(args->dy) || !aligned16(args->dx) || !aligned16(args->dBm) || !aligned16(args->dCm) ||
       !aligned16(args->d_final_state))
     return fail(FRAC_ERR_INVALID_ARG, "dy, dx, dBm, dCm and d_final_state must be 16-byte aligned");
@@ -228,9 +229,11 @@ frac_status frac_scan_bwd(const frac_shape* shape, const frac_bwd_args* args, vo
   p.dBm = args->dBm;
   p.dCm = args->dCm;
   p.dD = args->fwd.D ? args->dD : nullptr;
-  const size_t need = frac::scan_bwd_workspace(p);
+  const size_t need = p.N == 1 ? frac::nfree_bwd_workspace(p) : frac::scan_bwd_workspace(p);
   if (need && (!ws || ws_bytes < need))
     return fail(FRAC_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", need, ws ? ws_bytes : (size_t)0);
+  if (p.N == 1) return hip_status(frac::launch_nfree_bwd(p, ws, reinterpret_cast<hipStream_t>(stream)),
+                                  "frac_scan_bwd launch");
   return hip_status(frac::launch_scan_bwd(p, ws, ws_bytes, reinterpret_cast<hipStream_t>(stream)),
                     "frac_scan_bwd launch");
 }

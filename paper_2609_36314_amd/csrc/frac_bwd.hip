@@ -1429,7 +1429,7 @@ __global__ void __launch_bounds__(256) frac_bwd_ddt_tiles_kernel(ScanParams p, B
 }
 
 __global__ void __launch_bounds__(1024) frac_bwd_ddt_kernel(ScanParams p, BwdWork wk, const float* tsum, int nA,
-                                                           int nB) {
+                                                           int nB, int nD) {
   __shared__ float carry[64];
   __shared__ float out[64][65];
   const int L = p.L, H = p.H, ntiles = (L + 63) / 64;
@@ -1490,7 +1490,8 @@ __global__ void __launch_bounds__(1024) frac_bwd_ddt_kernel(ScanParams p, BwdWor
   }
   if (p.dD && b == 0 && tile == 0 && tid < nh) {
     float acc = 0.0f;
-    for (int bb = 0; bb < p.Bsz; ++bb) acc += wk.dDp[(int64_t)bb * H + h0 + tid];
+    for (int q = 0; q < nD; ++q)
+      for (int bb = 0; bb < p.Bsz; ++bb) acc += wk.dDp[((int64_t)q * p.Bsz + bb) * H + h0 + tid];
     p.dD[h0 + tid] = acc;
   }
 }
@@ -1597,7 +1598,7 @@ hipError_t launch_bwd_variant(const ScanParams& p, void* ws, hipStream_t stream)
                        ColCfg<T, MP, NB>::PS, RowCfg<T, MP, NB>::PS);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     hipLaunchKernelGGL(frac_bwd_ddt_kernel, dim3((unsigned)(ntiles * p.Bsz), (p.H + 63) / 64), dim3(1024), 0, stream, p, wk,
-                       (const float*)wk.tsum, ColCfg<T, MP, NB>::PS, RowCfg<T, MP, NB>::PS);
+                       (const float*)wk.tsum, ColCfg<T, MP, NB>::PS, RowCfg<T, MP, NB>::PS, 1);
   }
   if ((e = hipGetLastError()) != hipSuccess) return e;
   const int64_t nrows = (int64_t)p.Bsz * p.L;
@@ -1627,6 +1628,27 @@ hipError_t launch_bwd_mp(const ScanParams& p, void* ws, hipStream_t stream) {
 }
 
 }  // namespace
+
+hipError_t launch_ddt_finish(const ScanParams& p, float* eA, float* fA, float* eB, float* fB, float* F, float* dDp,
+                             float* tsum, int nA, int nB, int nD, hipStream_t stream) {
+  BwdWork wk{};
+  wk.eA = eA;
+  wk.fA = fA;
+  wk.eB = eB;
+  wk.fB = fB;
+  wk.F = F;
+  wk.dDp = dDp;
+  wk.tsum = tsum;
+  const int ntiles = (p.L + 63) / 64;
+  const int64_t nt = (int64_t)p.Bsz * p.H * ntiles;
+  hipLaunchKernelGGL(frac_bwd_ddt_tiles_kernel, dim3((unsigned)((nt + 3) / 4)), dim3(256), 0, stream, p, wk, tsum, nA,
+                     nB);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(frac_bwd_ddt_kernel, dim3((unsigned)(ntiles * p.Bsz), (p.H + 63) / 64), dim3(1024), 0, stream, p,
+                     wk, (const float*)tsum, nA, nB, nD);
+  return hipGetLastError();
+}
 
 size_t scan_bwd_workspace(const ScanParams& p) {
   if (p.Bsz == 0 || p.L == 0) return 0;

@@ -57,8 +57,17 @@ size_t scan_bwd_workspace(const ScanParams& p);
 
 hipError_t launch_decode_step(const ScanParams& p, float* state, hipStream_t stream);
 
-// The layer without B/C projections (dstate 1, B = C = 1): forward scan, no workspace.
+// The layer without B/C projections (dstate 1, B = C = 1): forward scan (no
+// workspace) and backward (workspace of nfree_bwd_workspace(p) bytes).
 hipError_t launch_nfree_fwd(const ScanParams& p, hipStream_t stream);
+size_t nfree_bwd_workspace(const ScanParams& p);
+hipError_t launch_nfree_bwd(const ScanParams& p, void* ws, hipStream_t stream);
+
+// ddt and dD from per-token partial terms: e = sum of nA eA arrays - sum of nB eB
+// arrays, f likewise added ([B H L] each), F [nA][B H], dDp [nD][B H]; tsum holds
+// B H ceil(L / 64) floats of scratch.
+hipError_t launch_ddt_finish(const ScanParams& p, float* eA, float* fA, float* eB, float* fB, float* F, float* dDp,
+                             float* tsum, int nA, int nB, int nD, hipStream_t stream);
 
 // True when a kernel variant exists for these sizes (M, N, P, dtype).
 bool scan_supported(const ScanParams& p, const char** why);

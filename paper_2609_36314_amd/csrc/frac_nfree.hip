@@ -30,8 +30,10 @@ constexpr float kNfSafe = 55.0f;
 constexpr float kNfFloor = 0x1p-60f;
 
 
-template <typename T, int MP>
-__global__ void __launch_bounds__(256) frac_nfree_fwd_kernel(ScanParams p) {
+// CKPT: no outputs; the state entering every chunk, and the final state, go to
+// ckpt [B H][nchunks + 1][M][P] (the first pass of the backward).
+template <typename T, int MP, bool CKPT>
+__global__ void __launch_bounds__(256) frac_nfree_fwd_kernel(ScanParams p, float* __restrict__ ckpt) {
   constexpr bool kBf16 = sizeof(T) == 2;
   constexpr int MB = (MP + 15) / 16;        // 16-row blocks of modes in the state
   constexpr int XS = kBf16 ? 64 + 8 : 64 + 4;  // [t][p] and [t][k] tile strides
@@ -125,6 +127,16 @@ __global__ void __launch_bounds__(256) frac_nfree_fwd_kernel(ScanParams p) {
     const bool tvalid = lane < nv;
     const float dtv = dt_n, al_l = al_n, lam = lam_n;
     if (c + 1 < nchunks) prefetch(c + 1);
+    if constexpr (CKPT) {  // the state entering this chunk
+      float* ck = ckpt + ((int64_t)bh * (nchunks + 1) + c) * M * P;
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int m = mb * 16 + lg * 4 + r;
+          if (active && m < M && pc < P) ck[(int64_t)m * P + pc] = S[mb][r] * Ecur[m];
+        }
+    }
     // ---- per-token controls (lane = token, every wave) and their chunk-local sum
     const float s_eff = lm_bh ? exp2f(log2f(lam) / al_l) : 1.0f;
     const float dtt_l = tvalid ? dtv * s_eff : 0.0f;
@@ -172,6 +184,7 @@ __global__ void __launch_bounds__(256) frac_nfree_fwd_kernel(ScanParams p) {
       }
     __syncthreads();  // x and the weights in LDS
 
+    if constexpr (!CKPT) {
     // ---- causal Gamma tiles [t][k] (float32 matrix cores, modes as K)
     for (int tile = wave; tile < 10; tile += 4) {
       const int tb = kNfTB[tile], kb = kNfKB[tile];
@@ -201,8 +214,10 @@ __global__ void __launch_bounds__(256) frac_nfree_fwd_kernel(ScanParams p) {
       }
     }
     __syncthreads();  // Gamma in LDS
+    }  // !CKPT
 
     if (active) {
+      if constexpr (!CKPT) {
       // ---- readout, intra-chunk product and skip term, 4 row blocks of 16 tokens
       Frag<T> Sf;  // the state as a B operand: slot s < 4 mode 4 lg + s, s >= 4 mode 16 + 4 lg + s - 4
 #pragma unroll
@@ -232,6 +247,7 @@ __global__ void __launch_bounds__(256) frac_nfree_fwd_kernel(ScanParams p) {
 #pragma unroll
         for (int r = 0; r < 4; ++r) Ys[(tb * 16 + lg * 4 + r) * XS + wave * 16 + li] = (T)(Y[r] + Dh * xv[r]);
       }
+      }  // !CKPT
 
       // ---- state update S_m <- (rescale) + V^T x, V = kappa e^{-r(A_Q - A_k)} upd
       if (ren_any) {
@@ -267,6 +283,7 @@ __global__ void __launch_bounds__(256) frac_nfree_fwd_kernel(ScanParams p) {
         }
       }
     }
+    if constexpr (CKPT) continue;
     __syncthreads();  // output rows in LDS
     // ---- output rows -> global, 16 bytes per thread
     for (int i = tid; i < 64 * CPR; i += 256) {
@@ -276,7 +293,9 @@ __global__ void __launch_bounds__(256) frac_nfree_fwd_kernel(ScanParams p) {
     }
   }
 
-  if (p.final_state && active) {
+  float* fin = CKPT ? ckpt + ((int64_t)bh * (nchunks + 1) + nchunks) * M * P
+                    : (p.final_state ? p.final_state + sbase : nullptr);
+  if (fin && active) {
     __syncthreads();
     const float* Ef = s_E2[nchunks & 1];
 #pragma unroll
@@ -284,22 +303,499 @@ __global__ void __launch_bounds__(256) frac_nfree_fwd_kernel(ScanParams p) {
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int m = mb * 16 + lg * 4 + r;
-        if (m < M && pc < P) p.final_state[sbase + (int64_t)m * P + pc] = S[mb][r] * Ef[m];
+        if (m < M && pc < P) fin[(int64_t)m * P + pc] = S[mb][r] * Ef[m];
       }
+  }
+}
+
+// ---------------------------------------------------------------- backward
+//
+// Reverse sweep over the chunks with the adjoint G_m (M x d_h per head, this
+// workgroup's 64 columns) in accumulator registers and each chunk's entering
+// state S0 read from the checkpoint pass.  Per chunk, with H = dY X^T over this
+// workgroup's columns (a partial sum over d_h) and Phi, Psi the rank-M tiles of
+// the B/C backward:
+//   dx_t = sum_m kappa_{t,m} e^{-r(A_Q-A_t)} G_m + sum_{t'>=t} Gamma_{t',t} dy_t' + D dy_t
+//   e_t  = sum_m r c_{t,m} e^{-rA_t} (S0_m . dy_t) + rowsum(H o Phi)_t - colsum(H o Phi)_t
+//          - sum_m r kappa_{t,m} e^{-r(A_Q-A_t)} (G_m . x_t)
+//   f_t  = colsum(H o Psi)_t + sum_m r w_{t,m} rho_{t,m} e^{-r(A_Q-A_t)} (G_m . x_t)
+//   G_m <- e^{-r_m A_Q} G_m + sum_t c_{t,m} e^{-r_m A_t} dy_t
+// e and f are summed over the workgroups of a head and turned into ddt (suffix
+// sums) by the finishing kernels of the B/C backward.
+
+struct NfWork {
+  const float* ckpt;  // [B H][nchunks + 1][M][P] states entering each chunk, then the final state
+  float* eA;          // [nps][B H L]
+  float* fA;          // [nps][B H L]
+  float* F;           // [nps][B H] sum_m r_m <dS_final, S_final> over this workgroup's columns
+  float* dDp;         // [nps][B H] sum dy . x over this workgroup's columns
+};
+
+template <typename T, int MP>
+__global__ void __launch_bounds__(256) frac_nfree_bwd_kernel(ScanParams p, NfWork wk) {
+  constexpr bool kBf16 = sizeof(T) == 2;
+  constexpr int MB = (MP + 15) / 16;
+  constexpr int XS = kBf16 ? 64 + 8 : 64 + 4;
+  constexpr int WQ = kWQ;
+  constexpr int NWA = 10;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, li = lane & 15, lg = lane >> 4;
+  const int L = p.L, H = p.H, P = p.P, M = p.M;
+  const int nps = (P + 63) / 64;
+  const int ps = blockIdx.x % nps, bh = blockIdx.x / nps, b = bh / H, h = bh - b * H;
+  const int p0 = ps * 64, pc = p0 + wave * 16 + li;
+  const bool active = p0 + wave * 16 < P;
+  const int nchunks = (L + kQ - 1) / kQ;
+  const int64_t blh = (int64_t)p.Bsz * L * H;
+
+  __shared__ __align__(16) T Xs[64 * XS];                      // x [t][p]
+  __shared__ __align__(16) T Ys[64 * XS];                      // dy [t][p]
+  __shared__ __align__(16) T GT[64 * XS];                      // Gamma^T [t][t'], t' >= t
+  __shared__ __align__(16) T DX[kBf16 ? 64 * XS : 8];          // dx rows [t][p] (bfloat16 staging)
+  __shared__ __align__(16) float Gt[MP * WQ];                  // the adjoint [m][p]
+  __shared__ __align__(16) float W[NWA * MP * WQ + kQ];
+  __shared__ float slot[3][10][16];  // row sums of H o Phi, column sums of H o Phi and of H o Psi
+  __shared__ float tokE[2][64], tokF[64];
+  __shared__ float s_rr[MP], s_lnt[MP];
+  __shared__ float red[256];
+  constexpr int SW = MP * WQ;
+  float* P_O = W;             // c e^{-rA}
+  float* P_Vt = W + 1 * SW;   // kappa e^{rA} (safe)
+  float* P_rO = W + 2 * SW;   // r c e^{-rA}
+  float* P_Yw = W + 3 * SW;   // r w rho e^{rA} (safe)
+  float* P_vq = W + 4 * SW;   // kappa e^{-r(A_Q-A)}
+  float* P_rv = W + 5 * SW;   // r kappa e^{-r(A_Q-A)}
+  float* P_fv = W + 6 * SW;   // r w rho e^{-r(A_Q-A)}
+  float* P_c = W + 7 * SW;    // c, kappa, r w rho (modes past the factorisation bound)
+  float* P_k = W + 8 * SW;
+  float* P_wr = W + 9 * SW;
+  float* P_A = W + NWA * SW;  // [Q] A_t
+
+  for (int i = tid; i < 64 * XS; i += 256) GT[i] = (T)0.0f;
+  if (tid < MP) {
+    const float tau = (tid < M) ? p.tau[tid] : 1.0f;
+    s_rr[tid] = (tid < M) ? 1.0f / tau : 0.0f;
+    s_lnt[tid] = (tid < M) ? logf(tau) : 0.0f;
+  }
+  __syncthreads();
+
+  // the adjoint of the final state and the final-state term of ddt
+  const int64_t sbase = (int64_t)bh * M * P;
+  const float* ck_bh = wk.ckpt + (int64_t)bh * (nchunks + 1) * M * P;
+  floatx4 G[MB];
+  float fpart = 0.0f;
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int m = mb * 16 + lg * 4 + r;
+      float g = 0.0f;
+      if (p.d_final_state && active && m < M && pc < P) {
+        g = p.d_final_state[sbase + (int64_t)m * P + pc];
+        fpart += s_rr[m] * g * ck_bh[(int64_t)nchunks * M * P + (int64_t)m * P + pc];
+      }
+      G[mb][r] = g;
+    }
+  const float Dh = p.D ? p.D[h] : 0.0f;
+  float dd_acc = 0.0f;
+
+  const T* xg = reinterpret_cast<const T*>(p.x) + (((int64_t)b * L) * H + h) * P + p0;
+  const T* yg = reinterpret_cast<const T*>(p.dy) + (((int64_t)b * L) * H + h) * P + p0;
+  T* dxg = reinterpret_cast<T*>(p.dx) + (((int64_t)b * L) * H + h) * P + p0;
+  const int64_t xstride = (int64_t)H * P;
+  const float* dt_bh = p.dt + (int64_t)b * L * H + h;
+  const float* al_bh = p.alpha + b * p.as0 + h * p.as2;
+  const float* lm_bh = p.lambda ? p.lambda + b * p.ls0 + h * p.ls2 : nullptr;
+  const float* rl_bh = p.read_logit ? p.read_logit + ((int64_t)b * L * H + h) * M : nullptr;
+  const float* wl_bh = p.write_logit ? p.write_logit + ((int64_t)b * L * H + h) * M : nullptr;
+  const int64_t lg_st = (int64_t)H * M;
+  constexpr int E16 = 16 / (int)sizeof(T);
+  constexpr int CPR = 64 / E16;
+  constexpr int XV = 64 * CPR / 256;
+
+  int4 xr[XV], yr[XV];
+  float dt_n, al_n, lam_n;
+  auto prefetch = [&](int c) {
+    const int t0 = c * kQ, nv = min(kQ, L - t0);
+#pragma unroll
+    for (int j = 0; j < XV; ++j) {
+      const int i = tid + 256 * j, t = i / CPR, col = (i - t * CPR) * E16;
+      xr[j] = yr[j] = make_int4(0, 0, 0, 0);
+      if (t < nv && p0 + col < P) {
+        xr[j] = *reinterpret_cast<const int4*>(xg + (int64_t)(t0 + t) * xstride + col);
+        yr[j] = *reinterpret_cast<const int4*>(yg + (int64_t)(t0 + t) * xstride + col);
+      }
+    }
+    const int tg = t0 + lane;
+    const bool tvalid = lane < nv;
+    dt_n = tvalid ? dt_bh[(int64_t)tg * H] : 0.0f;
+    al_n = tvalid ? al_bh[tg * p.as1] : 1.0f;
+    lam_n = (tvalid && lm_bh) ? lm_bh[tg * p.ls1] : 1.0f;
+  };
+  prefetch(nchunks - 1);
+
+  for (int c = nchunks - 1; c >= 0; --c) {
+    const int t0 = c * kQ, nv = min(kQ, L - t0);
+    __syncthreads();  // the previous chunk is done with every LDS array
+#pragma unroll
+    for (int j = 0; j < XV; ++j) {
+      const int i = tid + 256 * j, t = i / CPR, col = (i - t * CPR) * E16;
+      *reinterpret_cast<int4*>(Xs + t * XS + col) = xr[j];
+      *reinterpret_cast<int4*>(Ys + t * XS + col) = yr[j];
+    }
+    const bool tvalid = lane < nv;
+    const float dtv = dt_n, al_l = al_n, lam = lam_n;
+    if (c > 0) prefetch(c - 1);
+    const float s_eff = lm_bh ? exp2f(log2f(lam) / al_l) : 1.0f;
+    const float dtt_l = tvalid ? dtv * s_eff : 0.0f;
+    const float A_l = wave_inclusive_sum(dtt_l);
+    const float Alast = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(A_l), 63));
+    if (wave == 0) P_A[lane] = A_l;
+    const bool over = lane < MP && lane < M && !(s_rr[lane < MP ? lane : 0] * Alast <= kNfSafe);
+    const int unsafe = (int)(__ballot(over) & ((MP >= 32) ? 0xffffffffull : ((1ull << MP) - 1)));
+    // ---- per (token, mode) weights: pair = t MP + m
+    for (int pr = tid; pr < kQ * MP; pr += 256) {
+      const int t = pr / MP, m = pr - t * MP;
+      const float A = __shfl(A_l, t, 64), dtt = __shfl(dtt_l, t, 64), al = __shfl(al_l, t, 64);
+      const bool valid = t < nv;
+      const int64_t ith = (int64_t)(t0 + t) * lg_st + m;
+      const float r = s_rr[m], prior = -al * s_lnt[m];
+      const float zc = (m < M) ? prior + ((rl_bh && valid) ? rl_bh[ith] : 0.0f) : -INFINITY;
+      const float zw = (m < M) ? prior + ((wl_bh && valid) ? wl_bh[ith] : 0.0f) : -INFINITY;
+      const float cw = valid ? group_softmax<MP>(zc) : 0.0f;
+      const float ww = (rl_bh == wl_bh) ? cw : (valid ? group_softmax<MP>(zw) : 0.0f);
+      const bool safe = r * Alast <= kNfSafe;
+      const float beta = one_minus_exp_neg(dtt * r);
+      const float kap = beta * ww;
+      const float rwr = r * ww * (1.0f - beta);
+      const float ea = fexp(-r * A);
+      const float ep = safe ? fexp(r * A) : 0.0f;
+      const float dec = fexp(-r * (Alast - A));
+      float* o = W + m * WQ + t;
+      o[0 * SW] = cw * ea;
+      o[1 * SW] = kap * ep;
+      o[2 * SW] = r * cw * ea;
+      o[3 * SW] = rwr * ep;
+      o[4 * SW] = kap * dec;
+      o[5 * SW] = r * kap * dec;
+      o[6 * SW] = rwr * dec;
+      o[7 * SW] = cw;
+      o[8 * SW] = kap;
+      o[9 * SW] = rwr;
+    }
+    // the adjoint at the end of the chunk, [m][p], for its products with x
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int m = mb * 16 + lg * 4 + r;
+        if (m < MP) Gt[m * WQ + wave * 16 + li] = G[mb][r];
+      }
+    __syncthreads();  // x, dy, weights and the adjoint in LDS
+
+    // ---- causal tiles: Gamma^T into LDS; row / column sums of H o Phi, column sums of H o Psi
+    for (int tile = wave; tile < 10; tile += 4) {
+      const int tb = kNfTB[tile], kb = kNfKB[tile];
+      floatx4 D = {0.f, 0.f, 0.f, 0.f};  // H = dY X^T over this workgroup's columns
+#pragma unroll
+      for (int kp = 0; kp < 2; ++kp)
+        mma(D, frag_load8(Ys + (tb * 16 + li) * XS + kp * 32 + lg * 8), frag_load8(Xs + (kb * 16 + li) * XS + kp * 32 + lg * 8));
+      floatx4 Gm = {0.f, 0.f, 0.f, 0.f}, Ph = Gm, Ps = Gm;
+#pragma unroll
+      for (int q = 0; q < (MP + 3) / 4; ++q) {
+        const int m = q * 4 + lg;
+        const bool ok = m < MP;
+        const float aO = ok ? P_O[m * WQ + tb * 16 + li] : 0.0f;
+        const float arO = ok ? P_rO[m * WQ + tb * 16 + li] : 0.0f;
+        const float bVt = ok ? P_Vt[m * WQ + kb * 16 + li] : 0.0f;
+        const float bY = ok ? P_Yw[m * WQ + kb * 16 + li] : 0.0f;
+        Gm = __builtin_amdgcn_mfma_f32_16x16x4f32(aO, bVt, Gm, 0, 0, 0);
+        Ph = __builtin_amdgcn_mfma_f32_16x16x4f32(arO, bVt, Ph, 0, 0, 0);
+        Ps = __builtin_amdgcn_mfma_f32_16x16x4f32(aO, bY, Ps, 0, 0, 0);
+      }
+      if (unsafe) {
+        for (int m = 0; m < MP; ++m) {
+          if (!((unsafe >> m) & 1)) continue;
+          const float rm = s_rr[m];
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int t = tb * 16 + lg * 4 + r, k = kb * 16 + li;
+            if (t >= k) {
+              const float d = fexp(-rm * (P_A[t] - P_A[k]));
+              const float ck = P_c[m * WQ + t] * d;
+              Gm[r] += ck * P_k[m * WQ + k];
+              Ph[r] += rm * ck * P_k[m * WQ + k];
+              Ps[r] += ck * P_wr[m * WQ + k];
+            }
+          }
+        }
+      }
+      float rv[4], ce = 0.f, cf = 0.f;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int t = tb * 16 + lg * 4 + r, k = kb * 16 + li;
+        GT[k * XS + t] = (T)keep_if_ge(Gm[r], t, k);
+        const float hm = keep_if_ge(D[r], t, k);
+        rv[r] = hm * Ph[r];
+        ce += hm * Ph[r];
+        cf += hm * Ps[r];
+      }
+      // row sums: 16 lanes of a row group hold one row's 16 columns
+#pragma unroll
+      for (int r = 0; r < 4; ++r) rv[r] = group_allreduce<16>(rv[r], [](float x, float y) { return x + y; });
+      if (li == 0) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) slot[0][tile][lg * 4 + r] = rv[r];
+      }
+      ce = xor32_sum(xor16_sum(ce));
+      cf = xor32_sum(xor16_sum(cf));
+      if (lg == 0) {
+        slot[1][tile][li] = ce;
+        slot[2][tile][li] = cf;
+      }
+    }
+
+    // ---- per token (row block tb = wave): readout part of e from S0 . dy, adjoint
+    // parts of e and f from G . x (modes as output columns, reduced over 16 lanes)
+    {
+      const int tb = wave;
+      const float* ck = ck_bh + (int64_t)c * M * P;
+      float eR[4] = {0.f, 0.f, 0.f, 0.f}, eJ[4] = {0.f, 0.f, 0.f, 0.f}, fJ[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb) {
+        const int m = mb * 16 + li;  // output column of this lane
+        floatx4 U = {0.f, 0.f, 0.f, 0.f}, Z = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int kp = 0; kp < 2; ++kp) {
+          const int pk = p0 + kp * 32 + lg * 8;  // 8 columns of d_h
+          Frag<T> S0f, Gf;
+#pragma unroll
+          for (int s = 0; s < 8; ++s) {
+            const bool ok = m < M && pk + s < P;
+            frag_set(S0f, s, ok ? ck[(int64_t)m * P + pk + s] : 0.0f);
+            frag_set(Gf, s, (m < MP) ? Gt[m * WQ + kp * 32 + lg * 8 + s] : 0.0f);
+          }
+          mma(U, frag_load8(Ys + (tb * 16 + li) * XS + kp * 32 + lg * 8), S0f);
+          mma(Z, frag_load8(Xs + (tb * 16 + li) * XS + kp * 32 + lg * 8), Gf);
+        }
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int t = tb * 16 + lg * 4 + r;
+          const bool ok = m < MP;
+          eR[r] += (ok ? P_rO[m * WQ + t] : 0.0f) * U[r];
+          eJ[r] += (ok ? P_rv[m * WQ + t] : 0.0f) * Z[r];
+          fJ[r] += (ok ? P_fv[m * WQ + t] : 0.0f) * Z[r];
+        }
+      }
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        eR[r] = group_allreduce<16>(eR[r], [](float x, float y) { return x + y; });
+        eJ[r] = group_allreduce<16>(eJ[r], [](float x, float y) { return x + y; });
+        fJ[r] = group_allreduce<16>(fJ[r], [](float x, float y) { return x + y; });
+      }
+      if (li == 0) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          tokE[0][tb * 16 + lg * 4 + r] = eR[r];
+          tokE[1][tb * 16 + lg * 4 + r] = eJ[r];
+          tokF[tb * 16 + lg * 4 + r] = fJ[r];
+        }
+      }
+    }
+    // sum(dy . x) of the chunk for dD (columns past d_h and tokens past the sequence are zero)
+    if (p.dD) {
+      for (int i = tid; i < 64 * 64; i += 256) {
+        const int t = i >> 6, pcol = i & 63;
+        dd_acc += to_f32(Xs[t * XS + pcol]) * to_f32(Ys[t * XS + pcol]);
+      }
+    }
+    __syncthreads();  // Gamma^T, slots and token partials in LDS
+
+    if (active) {
+      // ---- dx: inter (weights x adjoint, K = modes), intra Gamma^T dY (K = t' >= t), skip term
+      Frag<T> Gf;  // the adjoint as a B operand: slot s < 4 mode 4 lg + s, s >= 4 mode 16 + 4 lg + s - 4
+#pragma unroll
+      for (int s = 0; s < 4; ++s) frag_set(Gf, s, G[0][s]);
+#pragma unroll
+      for (int s = 0; s < 4; ++s) frag_set(Gf, 4 + s, MB > 1 ? G[MB - 1][s] : 0.0f);
+#pragma unroll
+      for (int tb = 0; tb < 4; ++tb) {
+        const int t = tb * 16 + li;
+        floatx4 Y = {0.f, 0.f, 0.f, 0.f};
+        Frag<T> Vf;
+#pragma unroll
+        for (int s = 0; s < 4; ++s) {
+          const int m0 = lg * 4 + s, m1 = 16 + lg * 4 + s;
+          frag_set(Vf, s, (m0 < MP) ? P_vq[m0 * WQ + t] : 0.0f);
+          frag_set(Vf, 4 + s, (MB > 1 && m1 < MP) ? P_vq[m1 * WQ + t] : 0.0f);
+        }
+        mma(Y, Vf, Gf);
+#pragma unroll
+        for (int kk = tb / 2; kk < 2; ++kk)
+          mma(Y, frag_load8(GT + t * XS + kk * 32 + lg * 8), frag_load_rows(Ys, XS, kk * 32 + lg * 8, wave * 16));
+        float yv[4];
+        col4_rows(Ys, XS, tb * 16 + lg * 4, wave * 16, yv);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int tr = tb * 16 + lg * 4 + r;
+          const float v = Y[r] + Dh * yv[r];
+          if constexpr (kBf16) {
+            DX[tr * XS + wave * 16 + li] = (T)v;
+          } else {
+            if (tr < nv && pc < P) dxg[(int64_t)(t0 + tr) * xstride + wave * 16 + li] = (T)v;
+          }
+        }
+      }
+      // ---- adjoint update G <- e^{-r A_Q} G + (c e^{-rA})^T dY, rows m, column pc
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int m = mb * 16 + lg * 4 + r;
+          G[mb][r] *= (m < MP) ? fexp(-s_rr[m] * Alast) : 0.0f;
+        }
+#pragma unroll
+      for (int kt = 0; kt < 2; ++kt) {
+        const Frag<T> by = frag_load_rows(Ys, XS, kt * 32 + lg * 8, wave * 16);
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb) {
+          const int m = mb * 16 + li;
+          Frag<T> Of;
+          if (m < MP) {
+            const float* po = P_O + m * WQ + kt * 32 + lg * 8;
+            const float4 v0 = *reinterpret_cast<const float4*>(po);
+            const float4 v1 = *reinterpret_cast<const float4*>(po + 4);
+            frag_set(Of, 0, v0.x);
+            frag_set(Of, 1, v0.y);
+            frag_set(Of, 2, v0.z);
+            frag_set(Of, 3, v0.w);
+            frag_set(Of, 4, v1.x);
+            frag_set(Of, 5, v1.y);
+            frag_set(Of, 6, v1.z);
+            frag_set(Of, 7, v1.w);
+          } else {
+            Of = frag_zero<T>();
+          }
+          mma(G[mb], Of, by);
+        }
+      }
+    }
+    __syncthreads();  // dx rows in LDS
+
+    if (wave == 0) {
+      // token t: readout part + row sums of its row-block tiles - column sums of its
+      // column-block tiles - adjoint part; f: column sums + adjoint part (fixed order)
+      const int t = lane, tbt = t >> 4, tr = t & 15;
+      float e = tokE[0][t], f = 0.0f;
+      for (int kb2 = 0; kb2 <= tbt; ++kb2) e += slot[0][tbt * (tbt + 1) / 2 + kb2][tr];
+      for (int tb2 = tbt; tb2 < 4; ++tb2) {
+        const int tile = tb2 * (tb2 + 1) / 2 + tbt;
+        e -= slot[1][tile][tr];
+        f += slot[2][tile][tr];
+      }
+      e -= tokE[1][t];
+      f += tokF[t];
+      if (t < nv) {
+        const int64_t i = (int64_t)ps * blh + (int64_t)bh * L + t0 + t;  // [nps][B H L]
+        wk.eA[i] = e;
+        wk.fA[i] = f;
+      }
+    }
+    if constexpr (kBf16) {
+      for (int i = tid; i < 64 * CPR; i += 256) {
+        const int t = i / CPR, col = (i - t * CPR) * E16;
+        if (t < nv && p0 + col < P)
+          *reinterpret_cast<int4*>(dxg + (int64_t)(t0 + t) * xstride + col) = *reinterpret_cast<const int4*>(DX + t * XS + col);
+      }
+    }
+  }
+
+  // ---- per-workgroup totals: final-state term and sum(dy . x)
+  red[tid] = fpart;
+  __syncthreads();
+  if (tid == 0) {
+    float s = 0.f;
+    for (int i = 0; i < 256; ++i) s += red[i];
+    wk.F[(int64_t)ps * p.Bsz * H + bh] = s;
+  }
+  __syncthreads();
+  red[tid] = dd_acc;
+  __syncthreads();
+  if (tid == 0) {
+    float s = 0.f;
+    for (int i = 0; i < 256; ++i) s += red[i];
+    wk.dDp[(int64_t)ps * p.Bsz * H + bh] = s;
   }
 }
 
 template <typename T>
 hipError_t launch_nfree_t(const ScanParams& p, hipStream_t stream) {
   const unsigned blocks = (unsigned)((int64_t)p.Bsz * p.H * ((p.P + 63) / 64));
-  if (p.M <= 4) hipLaunchKernelGGL((frac_nfree_fwd_kernel<T, 4>), dim3(blocks), dim3(256), 0, stream, p);
-  else if (p.M <= 8) hipLaunchKernelGGL((frac_nfree_fwd_kernel<T, 8>), dim3(blocks), dim3(256), 0, stream, p);
-  else if (p.M <= 16) hipLaunchKernelGGL((frac_nfree_fwd_kernel<T, 16>), dim3(blocks), dim3(256), 0, stream, p);
-  else hipLaunchKernelGGL((frac_nfree_fwd_kernel<T, 32>), dim3(blocks), dim3(256), 0, stream, p);
+  if (p.M <= 4) hipLaunchKernelGGL((frac_nfree_fwd_kernel<T, 4, false>), dim3(blocks), dim3(256), 0, stream, p, nullptr);
+  else if (p.M <= 8) hipLaunchKernelGGL((frac_nfree_fwd_kernel<T, 8, false>), dim3(blocks), dim3(256), 0, stream, p, nullptr);
+  else if (p.M <= 16) hipLaunchKernelGGL((frac_nfree_fwd_kernel<T, 16, false>), dim3(blocks), dim3(256), 0, stream, p, nullptr);
+  else hipLaunchKernelGGL((frac_nfree_fwd_kernel<T, 32, false>), dim3(blocks), dim3(256), 0, stream, p, nullptr);
   return hipGetLastError();
 }
 
+struct NfLayout {
+  size_t ckpt, eA, fA, F, dDp, tsum, total;
+};
+
+NfLayout nfree_layout(const ScanParams& p) {
+  auto up = [](size_t v) { return (v + 255) / 256 * 256; };
+  const size_t bh = (size_t)p.Bsz * p.H, nps = (p.P + 63) / 64, nch = (p.L + kQ - 1) / kQ;
+  NfLayout l{};
+  l.ckpt = 0;
+  l.eA = up(sizeof(float) * bh * (nch + 1) * p.M * p.P);
+  l.fA = l.eA + up(sizeof(float) * nps * bh * p.L);
+  l.F = l.fA + up(sizeof(float) * nps * bh * p.L);
+  l.dDp = l.F + up(sizeof(float) * nps * bh);
+  l.tsum = l.dDp + up(sizeof(float) * nps * bh);
+  l.total = l.tsum + up(sizeof(float) * bh * ((p.L + 63) / 64));
+  return l;
+}
+
+template <typename T, int MP>
+hipError_t launch_nfree_bwd_mp(const ScanParams& p, void* ws, hipStream_t stream) {
+  const NfLayout l = nfree_layout(p);
+  unsigned char* base = reinterpret_cast<unsigned char*>(ws);
+  NfWork wk;
+  wk.ckpt = reinterpret_cast<float*>(base + l.ckpt);
+  wk.eA = reinterpret_cast<float*>(base + l.eA);
+  wk.fA = reinterpret_cast<float*>(base + l.fA);
+  wk.F = reinterpret_cast<float*>(base + l.F);
+  wk.dDp = reinterpret_cast<float*>(base + l.dDp);
+  const unsigned blocks = (unsigned)((int64_t)p.Bsz * p.H * ((p.P + 63) / 64));
+  hipLaunchKernelGGL((frac_nfree_fwd_kernel<T, MP, true>), dim3(blocks), dim3(256), 0, stream, p,
+                     reinterpret_cast<float*>(base + l.ckpt));
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL((frac_nfree_bwd_kernel<T, MP>), dim3(blocks), dim3(256), 0, stream, p, wk);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  const int nps = (p.P + 63) / 64;
+  return launch_ddt_finish(p, wk.eA, wk.fA, nullptr, nullptr, wk.F, wk.dDp, reinterpret_cast<float*>(base + l.tsum),
+                           nps, 0, nps, stream);
+}
+
+template <typename T>
+hipError_t launch_nfree_bwd_t(const ScanParams& p, void* ws, hipStream_t stream) {
+  if (p.M <= 4) return launch_nfree_bwd_mp<T, 4>(p, ws, stream);
+  if (p.M <= 8) return launch_nfree_bwd_mp<T, 8>(p, ws, stream);
+  if (p.M <= 16) return launch_nfree_bwd_mp<T, 16>(p, ws, stream);
+  return launch_nfree_bwd_mp<T, 32>(p, ws, stream);
+}
+
 }  // namespace
+
+size_t nfree_bwd_workspace(const ScanParams& p) {
+  if (p.Bsz == 0 || p.L == 0) return 0;
+  return nfree_layout(p).total;
+}
+
+hipError_t launch_nfree_bwd(const ScanParams& p, void* ws, hipStream_t stream) {
+  if (p.Bsz == 0 || p.L == 0) return hipSuccess;
+  return p.io_bf16 ? launch_nfree_bwd_t<bf16>(p, ws, stream) : launch_nfree_bwd_t<float>(p, ws, stream);
+}
 
 hipError_t launch_nfree_fwd(const ScanParams& p, hipStream_t stream) {
   if (p.Bsz == 0 || p.L == 0) return hipSuccess;

@@ -127,15 +127,24 @@ def test_decode_mode_range_is_checked_on_the_host(nmodes, status):
 
 
 def test_projection_free_form_checks_its_arguments_on_the_host():
-    """dstate 1 means B = C = 1: Bm and Cm must be NULL there (and are required
-    otherwise); its backward is reported unsupported; it needs no workspace."""
+    """dstate 1 means B = C = 1: Bm and Cm (dBm, dCm) must be NULL there (and are
+    required otherwise); its forward needs no workspace, its backward does."""
     lib = _lib.load()
     sh = _shape(dstate=1, headdim=256, nmodes=16)
     assert lib.frac_scan_workspace_size(ctypes.byref(sh), 0) == 0
+    assert lib.frac_scan_workspace_size(ctypes.byref(sh), 1) > 0
     a = FracFwdArgs()
     buf = (ctypes.c_float * 64)()
     a.x = a.dt = a.alpha = a.tau = a.y = ctypes.cast(buf, ctypes.c_void_p)
     a.Bm = ctypes.cast(buf, ctypes.c_void_p)  # given although dstate is 1
     assert lib.frac_scan_fwd(ctypes.byref(sh), ctypes.byref(a), None, 0, None) == -1
     b = FracBwdArgs()
-    assert lib.frac_scan_bwd(ctypes.byref(sh), ctypes.byref(b), None, 0, None) == -2
+    b.fwd = a
+    b.dy = b.dx = b.ddt = ctypes.cast(buf, ctypes.c_void_p)
+    assert lib.frac_scan_bwd(ctypes.byref(sh), ctypes.byref(b), None, 0, None) == -1
+    a.Bm = None
+    b.fwd = a
+    b.dBm = ctypes.cast(buf, ctypes.c_void_p)
+    assert lib.frac_scan_bwd(ctypes.byref(sh), ctypes.byref(b), None, 0, None) == -1
+    b.dBm = None
+    assert lib.frac_scan_bwd(ctypes.byref(sh), ctypes.byref(b), None, 0, None) == -3  # no workspace

@@ -1,7 +1,8 @@
 """GPU parity of the paper's own layer form -- no B/C projections (dstate 1,
 B = C = 1), an M x d_h state per head -- against the float64 oracle run with
-B = C = 1: the forward scan (frac_scan_fwd with Bm = Cm = NULL) and the decode
-step (frac_decode_step with Bm = Cm = NULL)."""
+B = C = 1: the forward scan (frac_scan_fwd with Bm = Cm = NULL), its backward
+(frac_scan_bwd with dBm = dCm = NULL) and the decode step (frac_decode_step
+with Bm = Cm = NULL)."""
 import numpy as np
 import pytest
 import torch
@@ -123,9 +124,64 @@ def test_nfree_decode_matches_oracle_steps():
         assert_close("decode state step %d" % s, f64(state), ref, TOL["bf16"])
 
 
-def test_nfree_backward_is_reported_unsupported():
-    w = Workload("t", 1, 64, 2, 64, 1, 4, bc=False)
-    inp = device_inputs(w, seed=14)
-    tau_d, _ = _tau(4)
-    with pytest.raises(frac.FracError):
-        frac.scan_bwd(inp["x"], inp["dt"], None, None, inp["alpha"], tau_d, inp["x"])
+def _oracle_bwd(inp, tau64, dfs=None):
+    x, dt, dy = f64(inp["x"]), f64(inp["dt"]), f64(inp["dy"])
+    a = inp["alpha"]
+    alpha = np.broadcast_to(f64(a) if not isinstance(a, torch.Tensor) or a.dim() != 1 else f64(a)[None, None, :],
+                            dt.shape)
+    kw = {k: f64(inp[k]) for k in ("lam", "read_logit", "write_logit", "D", "init_state") if k in inp}
+    ones = np.ones(x.shape[:2] + (1, 1))
+    return oracle.backward(x, dt, ones, ones, alpha, tau64, dy, d_final_state=None if dfs is None else f64(dfs), **kw)
+
+
+BWD = {
+    "bf16 paper shape M16 P256 extras dfinal": Workload("t", 2, 300, 2, 256, 1, 16, bc=False, extras=True,
+                                                        init_state=True, backward=True, final_state=True),
+    "f32 M4 P64": Workload("t", 1, 200, 2, 64, 1, 4, bc=False, io_dtype="f32", backward=True),
+    "bf16 M32 P128 init": Workload("t", 1, 130, 2, 128, 1, 32, bc=False, backward=True, init_state=True),
+    "bf16 M8 P40 ragged extras": Workload("t", 2, 70, 2, 40, 1, 8, bc=False, backward=True, extras=True),
+    "f32 M11 P96 extras dfinal": Workload("t", 1, 129, 2, 96, 1, 11, bc=False, io_dtype="f32", extras=True,
+                                          init_state=True, backward=True, final_state=True),
+    "bf16 M16 L1": Workload("t", 2, 1, 2, 256, 1, 16, bc=False, backward=True, init_state=True, final_state=True),
+}
+
+
+@pytest.mark.parametrize("name", list(BWD))
+def test_nfree_bwd_parity(name):
+    w = BWD[name]
+    inp = device_inputs(w, seed=15)
+    tau_d, tau64 = _tau(w.nmodes)
+    dfs = inp.get("d_final_state")
+    print("case", name, w, flush=True)
+    kw = {k: inp[k] for k in ("lam", "read_logit", "write_logit", "D", "init_state") if k in inp}
+    g = frac.scan_bwd(inp["x"], inp["dt"], None, None, inp["alpha"], tau_d, inp["dy"], d_final_state=dfs, **kw)
+    torch.cuda.synchronize()
+    ref = _oracle_bwd(inp, tau64, dfs)
+    tol = TOL[w.io_dtype]
+    assert g["dBm"] is None and g["dCm"] is None
+    assert_close("dx", f64(g["dx"]), ref["dx"], tol)
+    assert_close("ddt", f64(g["ddt"]), ref["ddt"], tol)
+    if "D" in inp:
+        assert_close("dD", f64(g["dD"]), ref["dD"], tol)
+
+
+def test_nfree_bwd_large_steps_use_direct_decay():
+    w = Workload("t", 1, 140, 2, 64, 1, 16, bc=False, backward=True)
+    inp = device_inputs(w, seed=16)
+    inp["dt"] = (inp["dt"] * 8.0).contiguous()
+    tau_d, tau64 = _tau(16)
+    g = frac.scan_bwd(inp["x"], inp["dt"], None, None, inp["alpha"], tau_d, inp["dy"])
+    torch.cuda.synchronize()
+    ref = _oracle_bwd(inp, tau64)
+    assert_close("dx", f64(g["dx"]), ref["dx"], TOL["bf16"])
+    assert_close("ddt", f64(g["ddt"]), ref["ddt"], TOL["bf16"])
+
+
+def test_nfree_bwd_deterministic():
+    w = Workload("t", 2, 192, 2, 256, 1, 16, bc=False, backward=True)
+    inp = device_inputs(w, seed=17)
+    tau_d, _ = _tau(16)
+    g1 = frac.scan_bwd(inp["x"], inp["dt"], None, None, inp["alpha"], tau_d, inp["dy"])
+    g2 = frac.scan_bwd(inp["x"], inp["dt"], None, None, inp["alpha"], tau_d, inp["dy"])
+    torch.cuda.synchronize()
+    assert torch.equal(g1["dx"], g2["dx"]) and torch.equal(g1["ddt"], g2["ddt"])
