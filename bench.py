@@ -50,7 +50,7 @@ def parse():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workloads", default="train-b4-l4096-m8,layer-fwd-b8-l2048,prefill-b1-l16384,paper-nfree-b8-l2048,"
-                                           "decode-b256-128steps")
+                                           "paper-nfree-train-b8-l2048,decode-b256-128steps")
     ap.add_argument("--main", default="train-b4-l4096-m8")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample-heads", type=int, default=64)
@@ -75,6 +75,12 @@ def nfree_fwd_bytes(w):
     """Compulsory HBM bytes of the forward without B/C: x and y in the io dtype, dt."""
     io = 2 if w.io_dtype == "bf16" else 4
     return w.batch * w.seqlen * w.nheads * (2 * w.headdim * io + 4)
+
+
+def nfree_bwd_bytes(w):
+    """Compulsory HBM bytes of the backward without B/C: x, dy, dx in the io dtype, dt, ddt."""
+    io = 2 if w.io_dtype == "bf16" else 4
+    return w.batch * w.seqlen * w.nheads * (3 * w.headdim * io + 8)
 
 
 def decode_bytes_per_step(w):
@@ -170,7 +176,13 @@ def bench_scan(torch, frac, w, steps, warmup):
     }
     if not w.bc:  # without B/C the forward moves more bytes than it does matrix-core work
         res["fwd_roofline"] = roofline("hbm", nfree_fwd_bytes(w), fms, PEAK_HBM_BYTES, "GB/s")
-    if w.backward:
+    if w.backward and not w.bc:
+        res["bwd_ms"] = bms
+        res["bwd_roofline"] = dict(roofline("hbm", nfree_bwd_bytes(w), bms, PEAK_HBM_BYTES, "GB/s"),
+                                   traffic=measured_traffic("frac_scan_bwd", w.name))
+        res["fwd_bwd_roofline"] = roofline("hbm", nfree_fwd_bytes(w) + nfree_bwd_bytes(w), fms + bms,
+                                           PEAK_HBM_BYTES, "GB/s")
+    elif w.backward:
         res["bwd_ms"] = bms
         res["bwd_roofline"] = dict(roofline("mfma", th * bwd_flops_per_token_head(w), bms, peak, "TFLOP/s"),
                                    traffic=measured_traffic("frac_scan_bwd", w.name))

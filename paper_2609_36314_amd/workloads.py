@@ -55,8 +55,9 @@ TRAIN = Workload("train-b4-l4096-m8", 4, 4096, 64, 64, 128, 8, backward=True)
 DECODE = Workload("decode-b256-128steps", 256, 1, 64, 64, 128, 4, decode_steps=128, init_state=True)
 # the paper's layer (state H x M x d_h, no B/C), forward at batch 8 x 2048 tokens
 PAPER_NFREE = Workload("paper-nfree-b8-l2048", 8, 2048, 16, 256, 1, 16, bc=False)
+PAPER_NFREE_TRAIN = Workload("paper-nfree-train-b8-l2048", 8, 2048, 16, 256, 1, 16, bc=False, backward=True)
 
-WORKLOADS = {w.name: w for w in (TINY_F32, LAYER_FWD, LONG_PREFILL, TRAIN, DECODE, PAPER_NFREE)}
+WORKLOADS = {w.name: w for w in (TINY_F32, LAYER_FWD, LONG_PREFILL, TRAIN, DECODE, PAPER_NFREE, PAPER_NFREE_TRAIN)}
 
 
 def _softplus(v: np.ndarray) -> np.ndarray:
