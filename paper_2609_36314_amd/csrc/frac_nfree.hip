@@ -51,7 +51,7 @@ __global__ void __launch_bounds__(256) frac_nfree_fwd_kernel(ScanParams p, float
   // per-token weight arrays [MP][WQ]: the row stride of 68 floats spreads the
   // stores of one wave (4 tokens x 16 modes, or 8 x 8) over distinct LDS banks
   constexpr int WQ = kQ + 4;
-  __shared__ __align__(16) float W[7 * MP * WQ + kQ];
+  __shared__ __align__(16) float W[6 * MP * WQ + kQ];
   __shared__ float s_rr[MP], s_lnt[MP], s_E2[2][MP];
   float* P_om = W;                 // [MP][Q] c e^{-rA_t} E_m   (readout)
   float* P_v = W + MP * WQ;        // [MP][Q] kappa e^{-r(A_Q-A_t)} upd (update)
@@ -59,7 +59,7 @@ __global__ void __launch_bounds__(256) frac_nfree_fwd_kernel(ScanParams p, float
   float* P_Vt = W + 3 * MP * WQ;   // [MP][Q] kappa e^{rA_t}, safe modes (Gamma columns)
   float* P_c = W + 4 * MP * WQ;    // [MP][Q] c, kappa (modes past the factorisation bound)
   float* P_k = W + 5 * MP * WQ;
-  float* P_A = W + 7 * MP * WQ;    // [Q] A_t
+  float* P_A = W + 6 * MP * WQ;    // [Q] A_t
 
   // Gamma tiles above the diagonal that the intra product reads are never written
   for (int i = tid; i < 64 * XS; i += 256) Gs[i] = (T)0.0f;
@@ -337,7 +337,7 @@ __global__ void __launch_bounds__(256) frac_nfree_bwd_kernel(ScanParams p, NfWor
   constexpr int MB = (MP + 15) / 16;
   constexpr int XS = kBf16 ? 64 + 8 : 64 + 4;
   constexpr int WQ = kWQ;
-  constexpr int NWA = 10;
+  constexpr int NWA = 8;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, li = lane & 15, lg = lane >> 4;
   const int L = p.L, H = p.H, P = p.P, M = p.M;
   const int nps = (P + 63) / 64;
@@ -350,7 +350,7 @@ __global__ void __launch_bounds__(256) frac_nfree_bwd_kernel(ScanParams p, NfWor
   __shared__ __align__(16) T Xs[64 * XS];                      // x [t][p]
   __shared__ __align__(16) T Ys[64 * XS];                      // dy [t][p]
   __shared__ __align__(16) T GT[64 * XS];                      // Gamma^T [t][t'], t' >= t
-  __shared__ __align__(16) T DX[kBf16 ? 64 * XS : 8];          // dx rows [t][p] (bfloat16 staging)
+  T* const DX = Xs;  // dx rows [t][p] (bfloat16 staging; x is no longer read by then)
   __shared__ __align__(16) float Gt[MP * WQ];                  // the adjoint [m][p]
   __shared__ __align__(16) float W[NWA * MP * WQ + kQ];
   __shared__ float slot[3][10][16];  // row sums of H o Phi, column sums of H o Phi and of H o Psi
@@ -359,15 +359,13 @@ __global__ void __launch_bounds__(256) frac_nfree_bwd_kernel(ScanParams p, NfWor
   __shared__ float red[256];
   constexpr int SW = MP * WQ;
   float* P_O = W;             // c e^{-rA}
-  float* P_Vt = W + 1 * SW;   // kappa e^{rA} (safe)
+  float* P_Vt = W + 1 * SW;   // kappa e^{rA} (safe modes), kappa (modes past the factorisation bound)
   float* P_rO = W + 2 * SW;   // r c e^{-rA}
-  float* P_Yw = W + 3 * SW;   // r w rho e^{rA} (safe)
+  float* P_Yw = W + 3 * SW;   // r w rho e^{rA} (safe modes), r w rho (the others)
   float* P_vq = W + 4 * SW;   // kappa e^{-r(A_Q-A)}
   float* P_rv = W + 5 * SW;   // r kappa e^{-r(A_Q-A)}
   float* P_fv = W + 6 * SW;   // r w rho e^{-r(A_Q-A)}
-  float* P_c = W + 7 * SW;    // c, kappa, r w rho (modes past the factorisation bound)
-  float* P_k = W + 8 * SW;
-  float* P_wr = W + 9 * SW;
+  float* P_c = W + 7 * SW;    // c (modes past the factorisation bound)
   float* P_A = W + NWA * SW;  // [Q] A_t
 
   for (int i = tid; i < 64 * XS; i += 256) GT[i] = (T)0.0f;
@@ -472,15 +470,13 @@ __global__ void __launch_bounds__(256) frac_nfree_bwd_kernel(ScanParams p, NfWor
       const float dec = fexp(-r * (Alast - A));
       float* o = W + m * WQ + t;
       o[0 * SW] = cw * ea;
-      o[1 * SW] = kap * ep;
+      o[1 * SW] = safe ? kap * ep : kap;
       o[2 * SW] = r * cw * ea;
-      o[3 * SW] = rwr * ep;
+      o[3 * SW] = safe ? rwr * ep : rwr;
       o[4 * SW] = kap * dec;
       o[5 * SW] = r * kap * dec;
       o[6 * SW] = rwr * dec;
       o[7 * SW] = cw;
-      o[8 * SW] = kap;
-      o[9 * SW] = rwr;
     }
     // the adjoint at the end of the chunk, [m][p], for its products with x
 #pragma unroll
@@ -503,7 +499,7 @@ __global__ void __launch_bounds__(256) frac_nfree_bwd_kernel(ScanParams p, NfWor
 #pragma unroll
       for (int q = 0; q < (MP + 3) / 4; ++q) {
         const int m = q * 4 + lg;
-        const bool ok = m < MP;
+        const bool ok = m < MP && !((unsafe >> m) & 1);
         const float aO = ok ? P_O[m * WQ + tb * 16 + li] : 0.0f;
         const float arO = ok ? P_rO[m * WQ + tb * 16 + li] : 0.0f;
         const float bVt = ok ? P_Vt[m * WQ + kb * 16 + li] : 0.0f;
@@ -522,9 +518,9 @@ __global__ void __launch_bounds__(256) frac_nfree_bwd_kernel(ScanParams p, NfWor
             if (t >= k) {
               const float d = fexp(-rm * (P_A[t] - P_A[k]));
               const float ck = P_c[m * WQ + t] * d;
-              Gm[r] += ck * P_k[m * WQ + k];
-              Ph[r] += rm * ck * P_k[m * WQ + k];
-              Ps[r] += ck * P_wr[m * WQ + k];
+              Gm[r] += ck * P_Vt[m * WQ + k];
+              Ph[r] += rm * ck * P_Vt[m * WQ + k];
+              Ps[r] += ck * P_Yw[m * WQ + k];
             }
           }
         }
