@@ -24,8 +24,9 @@ namespace frac {
 
 namespace {
 
-__constant__ int kNfTB[10] = {0, 1, 1, 2, 2, 2, 3, 3, 3, 3};
-__constant__ int kNfKB[10] = {0, 0, 1, 0, 1, 2, 0, 1, 2, 3};
+// The 10 causal 16x16 tiles of a 64-token chunk in row-major lower-triangular
+// order: tile -> (row block, column block), tile = tb (tb + 1) / 2 + kb.
+__device__ __forceinline__ int tile_row(int tile) { return (tile >= 1) + (tile >= 3) + (tile >= 6); }
 constexpr float kNfSafe = 55.0f;
 constexpr float kNfFloor = 0x1p-60f;
 
@@ -97,6 +98,8 @@ __global__ void __launch_bounds__(256) frac_nfree_fwd_kernel(ScanParams p, float
   // x and the per-token controls of a chunk, loaded one chunk ahead into registers
   int4 xr[XV];
   float dt_n, al_n, lam_n;
+  constexpr int NPR = kQ * MP / 256;  // (token, mode) pairs per thread: pair = t MP + m = tid + 256 j
+  float rlr[NPR], wlr[NPR];           // the read / write logits of this thread's pairs
   auto prefetch = [&](int c) {
     const int t0 = c * kQ, nv = min(kQ, L - t0);
 #pragma unroll
@@ -110,6 +113,14 @@ __global__ void __launch_bounds__(256) frac_nfree_fwd_kernel(ScanParams p, float
     dt_n = tvalid ? dt_bh[(int64_t)tg * H] : 0.0f;
     al_n = tvalid ? al_bh[tg * p.as1] : 1.0f;
     lam_n = (tvalid && lm_bh) ? lm_bh[tg * p.ls1] : 1.0f;
+#pragma unroll
+    for (int j = 0; j < NPR; ++j) {
+      const int pr = tid + 256 * j, t = pr / MP, m = pr - t * MP;
+      const bool ok = t < nv && m < M;
+      const int64_t ith = (int64_t)(t0 + t) * lg_st + m;
+      rlr[j] = (ok && rl_bh) ? rl_bh[ith] : 0.0f;
+      wlr[j] = (ok && wl_bh && wl_bh != rl_bh) ? wl_bh[ith] : 0.0f;  // unused when the two are one array
+    }
   };
   prefetch(0);
 
@@ -117,7 +128,7 @@ __global__ void __launch_bounds__(256) frac_nfree_fwd_kernel(ScanParams p, float
     const int t0 = c * kQ, nv = min(kQ, L - t0);
     const float* Ecur = s_E2[c & 1];
     float* Enext = s_E2[(c + 1) & 1];
-    __syncthreads();  // the previous chunk is done with every LDS array
+    barrier();  // the previous chunk is done with every LDS array
     // ---- x of the chunk into LDS (zeros past the sequence and past d_h)
 #pragma unroll
     for (int j = 0; j < XV; ++j) {
@@ -126,7 +137,6 @@ __global__ void __launch_bounds__(256) frac_nfree_fwd_kernel(ScanParams p, float
     }
     const bool tvalid = lane < nv;
     const float dtv = dt_n, al_l = al_n, lam = lam_n;
-    if (c + 1 < nchunks) prefetch(c + 1);
     if constexpr (CKPT) {  // the state entering this chunk
       float* ck = ckpt + ((int64_t)bh * (nchunks + 1) + c) * M * P;
 #pragma unroll
@@ -146,14 +156,14 @@ __global__ void __launch_bounds__(256) frac_nfree_fwd_kernel(ScanParams p, float
     const bool over = lane < MP && lane < M && !(s_rr[lane < MP ? lane : 0] * Alast <= kNfSafe);
     const int unsafe = (int)(__ballot(over) & ((MP >= 32) ? 0xffffffffull : ((1ull << MP) - 1)));
     // ---- per (token, mode) weights: pair = t MP + m
-    for (int pr = tid; pr < kQ * MP; pr += 256) {
-      const int t = pr / MP, m = pr - t * MP;
+#pragma unroll
+    for (int j = 0; j < NPR; ++j) {
+      const int pr = tid + 256 * j, t = pr / MP, m = pr - t * MP;
       const float A = __shfl(A_l, t, 64), dtt = __shfl(dtt_l, t, 64), al = __shfl(al_l, t, 64);
       const bool valid = t < nv;
-      const int64_t ith = (int64_t)(t0 + t) * lg_st + m;
       const float r = s_rr[m], prior = -al * s_lnt[m];
-      const float zc = (m < M) ? prior + ((rl_bh && valid) ? rl_bh[ith] : 0.0f) : -INFINITY;
-      const float zw = (m < M) ? prior + ((wl_bh && valid) ? wl_bh[ith] : 0.0f) : -INFINITY;
+      const float zc = (m < M) ? prior + rlr[j] : -INFINITY;
+      const float zw = (m < M) ? prior + wlr[j] : -INFINITY;
       const float cw = valid ? group_softmax<MP>(zc) : 0.0f;
       const float ww = (rl_bh == wl_bh) ? cw : (valid ? group_softmax<MP>(zw) : 0.0f);
       const float xr = r * Alast;
@@ -182,12 +192,13 @@ __global__ void __launch_bounds__(256) frac_nfree_fwd_kernel(ScanParams p, float
         renf[mb * 4 + r] = Enew;
         ren_any |= !(Enew >= kNfFloor);
       }
-    __syncthreads();  // x and the weights in LDS
+    barrier();  // x and the weights in LDS
+    if (c + 1 < nchunks) prefetch(c + 1);  // the registers of this chunk are consumed
 
     if constexpr (!CKPT) {
     // ---- causal Gamma tiles [t][k] (float32 matrix cores, modes as K)
     for (int tile = wave; tile < 10; tile += 4) {
-      const int tb = kNfTB[tile], kb = kNfKB[tile];
+      const int tb = tile_row(tile), kb = tile - tb * (tb + 1) / 2;
       floatx4 Gm = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int q = 0; q < (MP + 3) / 4; ++q) {
@@ -213,7 +224,7 @@ __global__ void __launch_bounds__(256) frac_nfree_fwd_kernel(ScanParams p, float
         Gs[t * XS + k] = (T)keep_if_ge(Gm[r], t, k);
       }
     }
-    __syncthreads();  // Gamma in LDS
+    barrier();  // Gamma in LDS
     }  // !CKPT
 
     if (active) {
@@ -284,7 +295,7 @@ __global__ void __launch_bounds__(256) frac_nfree_fwd_kernel(ScanParams p, float
       }
     }
     if constexpr (CKPT) continue;
-    __syncthreads();  // output rows in LDS
+    barrier();  // output rows in LDS
     // ---- output rows -> global, 16 bytes per thread
     for (int i = tid; i < 64 * CPR; i += 256) {
       const int t = i / CPR, ch = i - t * CPR, col = ch * E16;
@@ -412,6 +423,8 @@ __global__ void __launch_bounds__(256) frac_nfree_bwd_kernel(ScanParams p, NfWor
 
   int4 xr[XV], yr[XV];
   float dt_n, al_n, lam_n;
+  constexpr int NPR = kQ * MP / 256;  // (token, mode) pairs per thread: pair = t MP + m = tid + 256 j
+  float rlr[NPR], wlr[NPR];           // the read / write logits of this thread's pairs
   auto prefetch = [&](int c) {
     const int t0 = c * kQ, nv = min(kQ, L - t0);
 #pragma unroll
@@ -428,12 +441,39 @@ __global__ void __launch_bounds__(256) frac_nfree_bwd_kernel(ScanParams p, NfWor
     dt_n = tvalid ? dt_bh[(int64_t)tg * H] : 0.0f;
     al_n = tvalid ? al_bh[tg * p.as1] : 1.0f;
     lam_n = (tvalid && lm_bh) ? lm_bh[tg * p.ls1] : 1.0f;
+#pragma unroll
+    for (int j = 0; j < NPR; ++j) {
+      const int pr = tid + 256 * j, t = pr / MP, m = pr - t * MP;
+      const bool ok = t < nv && m < M;
+      const int64_t ith = (int64_t)(t0 + t) * lg_st + m;
+      rlr[j] = (ok && rl_bh) ? rl_bh[ith] : 0.0f;
+      wlr[j] = (ok && wl_bh && wl_bh != rl_bh) ? wl_bh[ith] : 0.0f;  // unused when the two are one array
+    }
+  };
+  // the state entering a chunk (from the checkpoint pass) as U-product operands:
+  // lane row m = 16 mb + lane % 16, 8 columns p0 + 32 kp + 8 (lane / 16) .. + 7
+  float4 s0r[MB][2][2];
+  auto prefetch_s0 = [&](int c) {
+    const float* ckc = ck_bh + (int64_t)c * M * P;
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+      for (int kp = 0; kp < 2; ++kp) {
+        const int m = mb * 16 + li, pk = p0 + kp * 32 + lg * 8;
+        s0r[mb][kp][0] = s0r[mb][kp][1] = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (m < M && pk < P) {  // P is a multiple of 8: all 8 columns or none
+          const float4* q = reinterpret_cast<const float4*>(ckc + (int64_t)m * P + pk);
+          s0r[mb][kp][0] = q[0];
+          s0r[mb][kp][1] = q[1];
+        }
+      }
   };
   prefetch(nchunks - 1);
+  prefetch_s0(nchunks - 1);
 
   for (int c = nchunks - 1; c >= 0; --c) {
     const int t0 = c * kQ, nv = min(kQ, L - t0);
-    __syncthreads();  // the previous chunk is done with every LDS array
+    barrier();  // the previous chunk is done with every LDS array
 #pragma unroll
     for (int j = 0; j < XV; ++j) {
       const int i = tid + 256 * j, t = i / CPR, col = (i - t * CPR) * E16;
@@ -442,7 +482,6 @@ __global__ void __launch_bounds__(256) frac_nfree_bwd_kernel(ScanParams p, NfWor
     }
     const bool tvalid = lane < nv;
     const float dtv = dt_n, al_l = al_n, lam = lam_n;
-    if (c > 0) prefetch(c - 1);
     const float s_eff = lm_bh ? exp2f(log2f(lam) / al_l) : 1.0f;
     const float dtt_l = tvalid ? dtv * s_eff : 0.0f;
     const float A_l = wave_inclusive_sum(dtt_l);
@@ -451,14 +490,14 @@ __global__ void __launch_bounds__(256) frac_nfree_bwd_kernel(ScanParams p, NfWor
     const bool over = lane < MP && lane < M && !(s_rr[lane < MP ? lane : 0] * Alast <= kNfSafe);
     const int unsafe = (int)(__ballot(over) & ((MP >= 32) ? 0xffffffffull : ((1ull << MP) - 1)));
     // ---- per (token, mode) weights: pair = t MP + m
-    for (int pr = tid; pr < kQ * MP; pr += 256) {
-      const int t = pr / MP, m = pr - t * MP;
+#pragma unroll
+    for (int j = 0; j < NPR; ++j) {
+      const int pr = tid + 256 * j, t = pr / MP, m = pr - t * MP;
       const float A = __shfl(A_l, t, 64), dtt = __shfl(dtt_l, t, 64), al = __shfl(al_l, t, 64);
       const bool valid = t < nv;
-      const int64_t ith = (int64_t)(t0 + t) * lg_st + m;
       const float r = s_rr[m], prior = -al * s_lnt[m];
-      const float zc = (m < M) ? prior + ((rl_bh && valid) ? rl_bh[ith] : 0.0f) : -INFINITY;
-      const float zw = (m < M) ? prior + ((wl_bh && valid) ? wl_bh[ith] : 0.0f) : -INFINITY;
+      const float zc = (m < M) ? prior + rlr[j] : -INFINITY;
+      const float zw = (m < M) ? prior + wlr[j] : -INFINITY;
       const float cw = valid ? group_softmax<MP>(zc) : 0.0f;
       const float ww = (rl_bh == wl_bh) ? cw : (valid ? group_softmax<MP>(zw) : 0.0f);
       const bool safe = r * Alast <= kNfSafe;
@@ -486,11 +525,11 @@ __global__ void __launch_bounds__(256) frac_nfree_bwd_kernel(ScanParams p, NfWor
         const int m = mb * 16 + lg * 4 + r;
         if (m < MP) Gt[m * WQ + wave * 16 + li] = G[mb][r];
       }
-    __syncthreads();  // x, dy, weights and the adjoint in LDS
+    barrier();  // x, dy, weights and the adjoint in LDS
 
     // ---- causal tiles: Gamma^T into LDS; row / column sums of H o Phi, column sums of H o Psi
     for (int tile = wave; tile < 10; tile += 4) {
-      const int tb = kNfTB[tile], kb = kNfKB[tile];
+      const int tb = tile_row(tile), kb = tile - tb * (tb + 1) / 2;
       floatx4 D = {0.f, 0.f, 0.f, 0.f};  // H = dY X^T over this workgroup's columns
 #pragma unroll
       for (int kp = 0; kp < 2; ++kp)
@@ -554,7 +593,6 @@ __global__ void __launch_bounds__(256) frac_nfree_bwd_kernel(ScanParams p, NfWor
     // parts of e and f from G . x (modes as output columns, reduced over 16 lanes)
     {
       const int tb = wave;
-      const float* ck = ck_bh + (int64_t)c * M * P;
       float eR[4] = {0.f, 0.f, 0.f, 0.f}, eJ[4] = {0.f, 0.f, 0.f, 0.f}, fJ[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int mb = 0; mb < MB; ++mb) {
@@ -562,14 +600,18 @@ __global__ void __launch_bounds__(256) frac_nfree_bwd_kernel(ScanParams p, NfWor
         floatx4 U = {0.f, 0.f, 0.f, 0.f}, Z = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int kp = 0; kp < 2; ++kp) {
-          const int pk = p0 + kp * 32 + lg * 8;  // 8 columns of d_h
           Frag<T> S0f, Gf;
+          const float4 a0 = s0r[mb][kp][0], a1 = s0r[mb][kp][1];
+          frag_set(S0f, 0, a0.x);
+          frag_set(S0f, 1, a0.y);
+          frag_set(S0f, 2, a0.z);
+          frag_set(S0f, 3, a0.w);
+          frag_set(S0f, 4, a1.x);
+          frag_set(S0f, 5, a1.y);
+          frag_set(S0f, 6, a1.z);
+          frag_set(S0f, 7, a1.w);
 #pragma unroll
-          for (int s = 0; s < 8; ++s) {
-            const bool ok = m < M && pk + s < P;
-            frag_set(S0f, s, ok ? ck[(int64_t)m * P + pk + s] : 0.0f);
-            frag_set(Gf, s, (m < MP) ? Gt[m * WQ + kp * 32 + lg * 8 + s] : 0.0f);
-          }
+          for (int s = 0; s < 8; ++s) frag_set(Gf, s, (m < MP) ? Gt[m * WQ + kp * 32 + lg * 8 + s] : 0.0f);
           mma(U, frag_load8(Ys + (tb * 16 + li) * XS + kp * 32 + lg * 8), S0f);
           mma(Z, frag_load8(Xs + (tb * 16 + li) * XS + kp * 32 + lg * 8), Gf);
         }
@@ -597,6 +639,11 @@ __global__ void __launch_bounds__(256) frac_nfree_bwd_kernel(ScanParams p, NfWor
         }
       }
     }
+    // the next chunk's inputs, issued once this chunk's copies have been consumed
+    if (c > 0) {
+      prefetch(c - 1);
+      prefetch_s0(c - 1);
+    }
     // sum(dy . x) of the chunk for dD (columns past d_h and tokens past the sequence are zero)
     if (p.dD) {
       for (int i = tid; i < 64 * 64; i += 256) {
@@ -604,7 +651,7 @@ __global__ void __launch_bounds__(256) frac_nfree_bwd_kernel(ScanParams p, NfWor
         dd_acc += to_f32(Xs[t * XS + pcol]) * to_f32(Ys[t * XS + pcol]);
       }
     }
-    __syncthreads();  // Gamma^T, slots and token partials in LDS
+    barrier();  // Gamma^T, slots and token partials in LDS
 
     if (active) {
       // ---- dx: inter (weights x adjoint, K = modes), intra Gamma^T dY (K = t' >= t), skip term
@@ -675,7 +722,7 @@ __global__ void __launch_bounds__(256) frac_nfree_bwd_kernel(ScanParams p, NfWor
         }
       }
     }
-    __syncthreads();  // dx rows in LDS
+    barrier();  // dx rows in LDS
 
     if (wave == 0) {
       // token t: readout part + row sums of its row-block tiles - column sums of its
