@@ -50,8 +50,6 @@ namespace frac {
 
 namespace {
 
-__constant__ int kTB[10] = {0, 1, 1, 2, 2, 2, 3, 3, 3, 3};
-__constant__ int kKB[10] = {0, 0, 1, 0, 1, 2, 0, 1, 2, 3};
 constexpr int kTiles = 10;
 constexpr int kTileElems = 256;
 constexpr float kSafeExponent = 55.0f;
@@ -134,19 +132,20 @@ __device__ __forceinline__ ChunkCtl chunk_controls(float dtv, float al, float la
 // E is the scale of the state (or adjoint) before this chunk's update, upd the
 // factor on the update (1/E_new, or 1 when the accumulators are folded back).
 template <int MP, int ROLE>
-__device__ __forceinline__ int pair_weights(const ChunkCtl& k, int t0, int nv, int M, const float* rl, const float* wl,
-                                            int64_t lg_st, const float* s_rr, const float* s_lnt, const float* Ecur,
+__device__ __forceinline__ int pair_weights(const ChunkCtl& k, int nv, int M, const PairLogits<MP, 512>& lgt,
+                                            bool w_is_c, const float* s_rr, const float* s_lnt, const float* Ecur,
                                             float* Enext, float* w) {
   const int tid = threadIdx.x;
-  const bool w_is_c = rl == wl;
-  for (int pr = tid; pr < kQ * MP; pr += 512) {
+#pragma unroll
+  for (int j = 0; j < lgt.NPR; ++j) {
+    const int pr = tid + 512 * j;
+    if (pr >= kQ * MP) break;  // wave-uniform
     const int t = pr / MP, m = pr - t * MP;
     const float A = __shfl(k.A, t, 64), dtt = __shfl(k.dtt, t, 64), al = __shfl(k.al, t, 64);
     const bool valid = t < nv;
-    const int64_t ith = (int64_t)(t0 + t) * lg_st + m;
     const float r = s_rr[m], prior = -al * s_lnt[m];
-    const float zc = (m < M) ? prior + ((rl && valid) ? rl[ith] : 0.0f) : -INFINITY;
-    const float zw = (m < M) ? prior + ((wl && valid) ? wl[ith] : 0.0f) : -INFINITY;
+    const float zc = (m < M) ? prior + lgt.rl[j] : -INFINITY;
+    const float zw = (m < M) ? prior + lgt.wl[j] : -INFINITY;
     // tokens past the sequence get zero weights (their tile rows may hold anything finite)
     const float cw = valid ? group_softmax<MP>(zc) : 0.0f;
     const float ww = w_is_c ? cw : (valid ? group_softmax<MP>(zw) : 0.0f);
@@ -417,12 +416,14 @@ __global__ void __launch_bounds__(512) frac_bwd_state_kernel(ScanParams p, BwdWo
   const float* rl_bh = p.read_logit ? p.read_logit + ((int64_t)b * L * H + h) * M : nullptr;
   const float* wl_bh = p.write_logit ? p.write_logit + ((int64_t)b * L * H + h) * M : nullptr;
   const int64_t lg_st = (int64_t)H * M;
+  PairLogits<MP, 512> lgt_n;  // the logits of the next chunk's weight pass
   auto load_controls = [&](int c, float& dtv, float& al, float& lam) {
     const int tg = c * kQ + lane;
     const bool valid = tg < L;
     dtv = valid ? dt_bh[(int64_t)tg * H] : 0.0f;
     al = valid ? al_bh[tg * p.as1] : 1.0f;
     lam = (valid && lm_bh) ? lm_bh[tg * p.ls1] : 1.0f;
+    lgt_n.load(rl_bh, wl_bh, c * kQ, min(kQ, L - c * kQ), M, lg_st, threadIdx.x);
   };
   DmaPlan<T, XS> planX;
   DmaPlan<T, BS> planB;
@@ -463,7 +464,7 @@ __global__ void __launch_bounds__(512) frac_bwd_state_kernel(ScanParams p, BwdWo
     const int t0 = c * kQ, nv = min(kQ, L - t0);
     const ChunkCtl k = chunk_controls(dt_n, al_n, lam_n, lm_bh != nullptr, nv);
     if (wave == 0) Wd[NWA * MP * kWQ + lane] = k.A;
-    unsafe_c = pair_weights<MP, kState>(k, t0, nv, M, rl_bh, wl_bh, lg_st, s_rr, s_lnt, s_E2 + (c & 1) * MP,
+    unsafe_c = pair_weights<MP, kState>(k, nv, M, lgt_n, rl_bh == wl_bh, s_rr, s_lnt, s_E2 + (c & 1) * MP,
                                         s_E2 + ((c + 1) & 1) * MP, Wd);
     alast_c = k.Alast;
   };
@@ -517,7 +518,7 @@ __global__ void __launch_bounds__(512) frac_bwd_state_kernel(ScanParams p, BwdWo
       for (int jt = 0; jt < 2; ++jt) {
         const int tile = wave + 8 * jt;
         if (tile >= kTiles) break;
-        const int tb = kTB[tile], kb = kKB[tile];
+        const int tb = tile_row(tile), kb = tile_col(tile);
         const floatx4 D = dyx_tile<T, XS>(Yc, Xc, tb, kb, tid);
         floatx4 Gm = rank_m_tile<MP>(P_O, P_Vt, tb * 16, kb * 16, tid);
         if (unsafe) unsafe_terms<MP>(Gm, unsafe, P_c, P_k, P_A, s_rr, tb, kb, false, tid);
@@ -852,12 +853,14 @@ __global__ void __launch_bounds__(512) frac_bwd_cols_kernel(ScanParams p, BwdWor
   const float* rl_bh = p.read_logit ? p.read_logit + ((int64_t)b * L * H + h) * M : nullptr;
   const float* wl_bh = p.write_logit ? p.write_logit + ((int64_t)b * L * H + h) * M : nullptr;
   const int64_t lg_st = (int64_t)H * M;
+  PairLogits<MP, 512> lgt_n;  // the logits of the next chunk's weight pass
   auto load_controls = [&](int c, float& dtv, float& al, float& lam) {
     const int tg = c * kQ + lane;
     const bool valid = tg < L;
     dtv = valid ? dt_bh[(int64_t)tg * H] : 0.0f;
     al = valid ? al_bh[tg * p.as1] : 1.0f;
     lam = (valid && lm_bh) ? lm_bh[tg * p.ls1] : 1.0f;
+    lgt_n.load(rl_bh, wl_bh, c * kQ, min(kQ, L - c * kQ), M, lg_st, threadIdx.x);
   };
   DmaPlan<T, XS> planX;
   DmaPlan<T, CS> planC;
@@ -896,10 +899,11 @@ __global__ void __launch_bounds__(512) frac_bwd_cols_kernel(ScanParams p, BwdWor
       barrier();
     }
     const float dtv = dt_n, al_l = al_n, lam_l = lam_n;
+    const PairLogits<MP, 512> lgt = lgt_n;
     if (c > 0) load_controls(c - 1, dt_n, al_n, lam_n);
     const ChunkCtl k = chunk_controls(dtv, al_l, lam_l, lm_bh != nullptr, nv);
     if (wave == 0) P_A[lane] = k.A;
-    const int unsafe = pair_weights<MP, kCols>(k, t0, nv, M, rl_bh, wl_bh, lg_st, s_rr, s_lnt, Ecur, Enext, W);
+    const int unsafe = pair_weights<MP, kCols>(k, nv, M, lgt, rl_bh == wl_bh, s_rr, s_lnt, Ecur, Enext, W);
     float renf[MPF];
     int renbits = 0;
 #pragma unroll
@@ -916,7 +920,7 @@ __global__ void __launch_bounds__(512) frac_bwd_cols_kernel(ScanParams p, BwdWor
     for (int jt = 0; jt < 2; ++jt) {
       const int tile = wave + 8 * jt;
       if (tile >= kTiles) break;
-      const int tb = kTB[tile], kb = kKB[tile];
+      const int tb = tile_row(tile), kb = tile_col(tile);
 #pragma unroll
       for (int r = 0; r < 4; ++r) HG[(tb * 16 + lg * 4 + r) * XS + kb * 16 + li] = hgt.v[jt].e[r];
     }
@@ -1140,12 +1144,14 @@ __global__ void __launch_bounds__(512) frac_bwd_rows_kernel(ScanParams p, BwdWor
   const float* rl_bh = p.read_logit ? p.read_logit + ((int64_t)b * L * H + h) * M : nullptr;
   const float* wl_bh = p.write_logit ? p.write_logit + ((int64_t)b * L * H + h) * M : nullptr;
   const int64_t lg_st = (int64_t)H * M;
+  PairLogits<MP, 512> lgt_n;  // the logits of the next chunk's weight pass
   auto load_controls = [&](int c, float& dtv, float& al, float& lam) {
     const int tg = c * kQ + lane;
     const bool valid = tg < L;
     dtv = valid ? dt_bh[(int64_t)tg * H] : 0.0f;
     al = valid ? al_bh[tg * p.as1] : 1.0f;
     lam = (valid && lm_bh) ? lm_bh[tg * p.ls1] : 1.0f;
+    lgt_n.load(rl_bh, wl_bh, c * kQ, min(kQ, L - c * kQ), M, lg_st, threadIdx.x);
   };
   DmaPlan<T, XS> planX;
   DmaPlan<T, BS> planB;
@@ -1206,10 +1212,11 @@ __global__ void __launch_bounds__(512) frac_bwd_rows_kernel(ScanParams p, BwdWor
       barrier();
     }
     const float dtv = dt_n, al_l = al_n, lam_l = lam_n;
+    const PairLogits<MP, 512> lgt = lgt_n;
     if (c > 0) load_controls(c - 1, dt_n, al_n, lam_n);
     const ChunkCtl k = chunk_controls(dtv, al_l, lam_l, lm_bh != nullptr, nv);
     if (wave == 0) P_A[lane] = k.A;
-    const int unsafe = pair_weights<MP, kRows>(k, t0, nv, M, rl_bh, wl_bh, lg_st, s_rr, s_lnt, Ecur, Enext, W);
+    const int unsafe = pair_weights<MP, kRows>(k, nv, M, lgt, rl_bh == wl_bh, s_rr, s_lnt, Ecur, Enext, W);
     float renf[MPW];
     int renbits = 0;
 #pragma unroll
@@ -1227,7 +1234,7 @@ __global__ void __launch_bounds__(512) frac_bwd_rows_kernel(ScanParams p, BwdWor
       for (int jt = 0; jt < 2; ++jt) {
         const int tile = wave + 8 * jt;
         if (tile >= kTiles) break;
-        const int tb = kTB[tile], kb = kKB[tile];
+        const int tb = tile_row(tile), kb = tile_col(tile);
 #pragma unroll
         for (int r = 0; r < 4; ++r) GG[(tb * 16 + lg * 4 + r) * XS + kb * 16 + li] = ggt.v[jt].e[r];
       }

@@ -19,6 +19,35 @@ constexpr int kQ = 64;  // tokens per chunk
 // 16-lane row reads of 4 modes into distinct banks; rows stay 16-byte aligned.
 constexpr int kWQ = kQ + 4;
 
+// The 10 causal 16x16 tiles of a 64-token chunk in row-major lower-triangular
+// order, tile = tb (tb + 1) / 2 + kb: the row block of a tile (plain arithmetic,
+// so no table load sits on the path of a tile loop).
+__device__ __forceinline__ int tile_row(int tile) { return (tile >= 1) + (tile >= 3) + (tile >= 6); }
+__device__ __forceinline__ int tile_col(int tile) { const int tb = tile_row(tile); return tile - tb * (tb + 1) / 2; }
+
+// The read / write logits of the (token, mode) pairs that a thread of an NT-thread
+// workgroup forms in a chunk's weight pass (pair = t MP + m = tid + NT j), loaded
+// one chunk ahead into registers: the weight pass then never waits on global
+// memory (a wait there would also drain the next chunk's tile copies).  Zero for
+// pairs past the chunk, absent logits, and wl when the write logits are the read
+// logits (the weight pass reuses the read weights then).
+template <int MP, int NT>
+struct PairLogits {
+  static constexpr int NPR = (kQ * MP + NT - 1) / NT;
+  float rl[NPR], wl[NPR];
+  __device__ __forceinline__ void load(const float* rlp, const float* wlp, int t0, int nv, int M, int64_t stride,
+                                       int tid) {
+#pragma unroll
+    for (int j = 0; j < NPR; ++j) {
+      const int pr = tid + NT * j, t = pr / MP, m = pr - t * MP;
+      const bool ok = pr < kQ * MP && t < nv && m < M;
+      const int64_t i = (int64_t)(t0 + t) * stride + m;
+      rl[j] = (ok && rlp) ? rlp[i] : 0.0f;
+      wl[j] = (ok && wlp && wlp != rlp) ? wlp[i] : 0.0f;
+    }
+  }
+};
+
 // ---------------------------------------------------------------- fragments
 //
 // A 16x16x32 matrix-core step consumes, per lane (i = lane % 16, g = lane / 16),

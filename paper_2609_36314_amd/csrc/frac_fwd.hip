@@ -55,8 +55,6 @@ namespace frac {
 namespace {
 
 // lower-triangular 16x16 tiles of the Q x Q matrix: (row block, column block)
-__constant__ int kTileTB[10] = {0, 1, 1, 2, 2, 2, 3, 3, 3, 3};
-__constant__ int kTileKB[10] = {0, 0, 1, 0, 1, 2, 0, 1, 2, 3};
 constexpr int kTiles = 10;
 constexpr int kTileElems = 256;  // one 16x16 tile: 64 lanes x 4 values
 
@@ -102,7 +100,7 @@ __global__ void __launch_bounds__(256) frac_cb_kernel(ScanParams p, T* __restric
   __syncthreads();
   T* out = gtiles + (((int64_t)b * nchunks + c) * G + g) * (kTiles * kTileElems);
   for (int tile = wave; tile < kTiles; tile += 4) {
-    const int tb = kTileTB[tile], kb = kTileKB[tile];
+    const int tb = tile_row(tile), kb = tile_col(tile);
     floatx4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int kk = 0; kk < KB; ++kk) {
@@ -275,12 +273,14 @@ __global__ void __launch_bounds__(512) frac_fwd_kernel(ScanParams p, const T* __
   const float* wl_bh = p.write_logit ? p.write_logit + ((int64_t)b * L * H + h) * M : nullptr;
   const bool w_is_c = wl_bh == rl_bh;  // then the write weights equal the read weights
   const int64_t lg_st = (int64_t)H * M;
+  PairLogits<MP, 512> lgt_n;  // the logits of the next chunk's weight pass
   auto load_controls = [&](int c, float& dtv, float& al, float& lam) {
     const int tg = c * kQ + lane;
     const bool valid = tg < T1;
     dtv = valid ? dt_bh[(int64_t)tg * H] : 0.0f;
     al = valid ? al_bh[tg * al_st] : 1.0f;
     lam = (valid && lm_bh) ? lm_bh[tg * lm_st] : 1.0f;
+    lgt_n.load(rl_bh, wl_bh, c * kQ, min(kQ, T1 - c * kQ), M, lg_st, tid);
   };
   DmaPlan<T, XS> planX;
   DmaPlan<T, BS> planB;
@@ -334,6 +334,7 @@ __global__ void __launch_bounds__(512) frac_fwd_kernel(ScanParams p, const T* __
       barrier();
     }
     const float dtv = dt_n, al_l = al_n, lam_l = lam_n;
+    const PairLogits<MP, 512> lgt = lgt_n;
     if (c + 1 < c1) load_controls(c + 1, dt_n, al_n, lam_n);
 
     // ---- per-token step and its chunk-local cumulative sum (lane = token, every wave)
@@ -348,14 +349,16 @@ __global__ void __launch_bounds__(512) frac_fwd_kernel(ScanParams p, const T* __
     // the same flags in every wave, lane m < MP testing mode m
     const bool over = lane < MP && lane < M && !(s_rr[lane < MP ? lane : 0] * Alast <= kSafeExponent);
     const int unsafe = (int)(__ballot(over) & ((1ull << MP) - 1));
-    for (int pr = tid; pr < kQ * MP; pr += 512) {
+#pragma unroll
+    for (int j = 0; j < lgt.NPR; ++j) {
+      const int pr = tid + 512 * j;
+      if (pr >= kQ * MP) break;  // wave-uniform
       const int t = pr / MP, m = pr - t * MP;
       const float A = __shfl(A_l, t, 64), dtt = __shfl(dtt_l, t, 64), al = __shfl(al_l, t, 64);
       const bool valid = t < nv;
-      const int64_t ith = (int64_t)(t0 + t) * lg_st + m;
       const float r = s_rr[m], prior = -al * s_lnt[m];
-      float zc = (m < M) ? prior + ((rl_bh && valid) ? rl_bh[ith] : 0.0f) : -INFINITY;
-      float zw = (m < M) ? prior + ((wl_bh && valid) ? wl_bh[ith] : 0.0f) : -INFINITY;
+      float zc = (m < M) ? prior + lgt.rl[j] : -INFINITY;
+      float zw = (m < M) ? prior + lgt.wl[j] : -INFINITY;
       // tokens past the sequence get zero weights (their tile rows may hold anything finite)
       const float cw = valid ? group_softmax<MP>(zc) : 0.0f;
       const float ww = w_is_c ? cw : (valid ? group_softmax<MP>(zw) : 0.0f);
@@ -393,7 +396,7 @@ __global__ void __launch_bounds__(512) frac_fwd_kernel(ScanParams p, const T* __
       for (int jt = 0; jt < 2; ++jt) {
         const int tile = wave + NWT * jt;
         if (tile >= kTiles) break;
-        const int tb = kTileTB[tile], kb = kTileKB[tile];
+        const int tb = tile_row(tile), kb = tile_col(tile);
         float Gt[4];
 #pragma unroll
         for (int r = 0; r < 4; ++r) Gt[r] = gtile.get(jt, r);

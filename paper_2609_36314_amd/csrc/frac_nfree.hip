@@ -24,9 +24,6 @@ namespace frac {
 
 namespace {
 
-// The 10 causal 16x16 tiles of a 64-token chunk in row-major lower-triangular
-// order: tile -> (row block, column block), tile = tb (tb + 1) / 2 + kb.
-__device__ __forceinline__ int tile_row(int tile) { return (tile >= 1) + (tile >= 3) + (tile >= 6); }
 constexpr float kNfSafe = 55.0f;
 constexpr float kNfFloor = 0x1p-60f;
 
@@ -198,7 +195,7 @@ __global__ void __launch_bounds__(256) frac_nfree_fwd_kernel(ScanParams p, float
     if constexpr (!CKPT) {
     // ---- causal Gamma tiles [t][k] (float32 matrix cores, modes as K)
     for (int tile = wave; tile < 10; tile += 4) {
-      const int tb = tile_row(tile), kb = tile - tb * (tb + 1) / 2;
+      const int tb = tile_row(tile), kb = tile_col(tile);
       floatx4 Gm = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int q = 0; q < (MP + 3) / 4; ++q) {
@@ -529,7 +526,7 @@ __global__ void __launch_bounds__(256) frac_nfree_bwd_kernel(ScanParams p, NfWor
 
     // ---- causal tiles: Gamma^T into LDS; row / column sums of H o Phi, column sums of H o Psi
     for (int tile = wave; tile < 10; tile += 4) {
-      const int tb = tile_row(tile), kb = tile - tb * (tb + 1) / 2;
+      const int tb = tile_row(tile), kb = tile_col(tile);
       floatx4 D = {0.f, 0.f, 0.f, 0.f};  // H = dY X^T over this workgroup's columns
 #pragma unroll
       for (int kp = 0; kp < 2; ++kp)
