@@ -121,8 +121,18 @@ typedef struct {
  *   ddt            [B,L,H] f32          written
  *   dBm, dCm       [B,L,G,N] io_dtype   written, summed over the heads of each group
  *   dD             [H] f32              written when fwd.D is non-NULL and dD is non-NULL
- * Gradients with respect to alpha, lambda, the logits, tau and init_state are not
- * produced. */
+ * The form without B/C (dstate 1) also produces, for each pointer that is
+ * non-NULL (all must be NULL with dstate > 1, else FRAC_ERR_UNSUPPORTED):
+ *   dalpha         [B,L,H] f32          gradient of alpha at every (b, t, h), through the
+ *                                       prior -alpha ln tau_m of both softmaxes (eq. read-softmax)
+ *                                       and the effective step Delta lambda^{1/alpha} (eq. tau-eff);
+ *                                       sum it over broadcast dimensions of alpha
+ *   dlambda        [B,L,H] f32          gradient of lambda (zeros when fwd.lambda is NULL)
+ *   dread_logit,
+ *   dwrite_logit   [B,L,H,M] f32        gradients of the logits (also when the logits are
+ *                                       NULL, i.e. at zero logits)
+ *   dinit_state    [B,H,M,1,P] f32      gradient of init_state (also when it is NULL)
+ * Gradients with respect to tau are not produced. */
 typedef struct {
   frac_fwd_args fwd;
   const void *dy;
@@ -131,6 +141,9 @@ typedef struct {
   float *ddt;
   void *dBm, *dCm;
   float *dD;
+  float *dalpha, *dlambda;
+  float *dread_logit, *dwrite_logit;
+  float *dinit_state;
 } frac_bwd_args;
 
 /* One decode token on a cached state (shape.seqlen must be 1).

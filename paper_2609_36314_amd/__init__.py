@@ -154,10 +154,12 @@ def scan_fwd(x, dt, Bm, Cm, alpha, tau, *, lam=None, read_logit=None, write_logi
 
 
 def scan_bwd(x, dt, Bm, Cm, alpha, tau, dy, *, lam=None, read_logit=None, write_logit=None, D=None,
-             init_state=None, d_final_state=None, chunk=0, workspace=None):
+             init_state=None, d_final_state=None, chunk=0, workspace=None, all_grads=False):
     """Chunked parallel scan, backward (frac_scan_bwd).
 
-    Returns dict(dx, ddt, dBm, dCm, dD) with dD None when D is None."""
+    Returns dict(dx, ddt, dBm, dCm, dD) with dD None when D is None.  With
+    all_grads (the form without B/C only) also dalpha [B,L,H], dlambda [B,L,H],
+    dread_logit, dwrite_logit [B,L,H,M] and dinit_state [B,H,M,1,P]."""
     M = int(tau.shape[0])
     shape = _shape(x, Bm, M, chunk)
     Bsz, L, H, P = x.shape
@@ -166,11 +168,20 @@ def scan_bwd(x, dt, Bm, Cm, alpha, tau, dy, *, lam=None, read_logit=None, write_
     fwd, keep = _fwd_struct(x, dt, Bm, Cm, alpha, tau, lam, read_logit, write_logit, D, init_state, None, None)
     out = dict(dx=torch.empty_like(x), ddt=torch.empty_like(dt), dBm=None if Bm is None else torch.empty_like(Bm),
                dCm=None if Cm is None else torch.empty_like(Cm), dD=None if D is None else torch.empty_like(D))
+    if all_grads:
+        f32 = dict(dtype=torch.float32, device=x.device)
+        out.update(dalpha=torch.empty((Bsz, L, H), **f32), dlambda=torch.empty((Bsz, L, H), **f32),
+                   dread_logit=torch.empty((Bsz, L, H, M), **f32), dwrite_logit=torch.empty((Bsz, L, H, M), **f32),
+                   dinit_state=torch.empty((Bsz, H, M, 1, P), **f32))
     a = FracBwdArgs()
     a.fwd = fwd
     a.dy, a.d_final_state = _ptr(dy), _ptr(_f32(d_final_state, "d_final_state"))
     a.dx, a.ddt, a.dBm, a.dCm, a.dD = (_ptr(out["dx"]), _ptr(out["ddt"]), _ptr(out["dBm"]), _ptr(out["dCm"]),
                                        _ptr(out["dD"]))
+    if all_grads:
+        a.dalpha, a.dlambda = _ptr(out["dalpha"]), _ptr(out["dlambda"])
+        a.dread_logit, a.dwrite_logit = _ptr(out["dread_logit"]), _ptr(out["dwrite_logit"])
+        a.dinit_state = _ptr(out["dinit_state"])
     ws_bytes = scan_workspace_size(shape, True)
     if workspace is None and ws_bytes:
         workspace = torch.empty(ws_bytes, dtype=torch.uint8, device=x.device)

@@ -40,7 +40,9 @@ class FracFwdArgs(ctypes.Structure):
 
 class FracBwdArgs(ctypes.Structure):
     _fields_ = [("fwd", FracFwdArgs), ("dy", c_void_p), ("d_final_state", c_void_p), ("dx", c_void_p),
-                ("ddt", c_void_p), ("dBm", c_void_p), ("dCm", c_void_p), ("dD", c_void_p)]
+                ("ddt", c_void_p), ("dBm", c_void_p), ("dCm", c_void_p), ("dD", c_void_p),
+                ("dalpha", c_void_p), ("dlambda", c_void_p), ("dread_logit", c_void_p),
+                ("dwrite_logit", c_void_p), ("dinit_state", c_void_p)]
 
 
 class FracStepArgs(ctypes.Structure):

@@ -204,7 +204,18 @@ frac_status frac_scan_bwd(const frac_shape* shape, const frac_bwd_args* args, vo
   frac_status s = fill_shape(shape, p);
   if (s == FRAC_OK) s = check_scan_shape(p, "frac_scan_bwd");
   if (s != FRAC_OK) return s;
+  if (args && p.N != 1 &&
+      (args->dalpha || args->dlambda || args->dread_logit || args->dwrite_logit || args->dinit_state))
+    return fail(FRAC_ERR_UNSUPPORTED,
+                "dalpha, dlambda, dread_logit, dwrite_logit and dinit_state are produced for dstate 1 only");
   if (p.Bsz == 0 || p.L == 0) {
+    if (args && args->dinit_state && p.Bsz > 0) {  // no tokens: the initial state is the final state
+      const int64_t n = (int64_t)p.Bsz * p.H * p.M * p.P;
+      hipLaunchKernelGGL(copy_or_zero_kernel, dim3(256), dim3(256), 0,
+                         reinterpret_cast<hipStream_t>(stream), args->dinit_state, args->d_final_state, n);
+      const frac_status e = hip_status(hipGetLastError(), "frac_scan_bwd (empty)");
+      if (e != FRAC_OK) return e;
+    }
     if (args && args->dD && p.Bsz >= 0) {
       hipLaunchKernelGGL(copy_or_zero_kernel, dim3(1), dim3(256), 0, reinterpret_cast<hipStream_t>(stream),
                          args->dD, (const float*)nullptr, (int64_t)p.H);
@@ -229,6 +240,11 @@ frac_status frac_scan_bwd(const frac_shape* shape, const frac_bwd_args* args, vo
   p.dBm = args->dBm;
   p.dCm = args->dCm;
   p.dD = args->fwd.D ? args->dD : nullptr;
+  p.dalpha = args->dalpha;
+  p.dlambda = args->dlambda;
+  p.dread_logit = args->dread_logit;
+  p.dwrite_logit = args->dwrite_logit;
+  p.dinit_state = args->dinit_state;
   const size_t need = p.N == 1 ? frac::nfree_bwd_workspace(p) : frac::scan_bwd_workspace(p);
   if (need && (!ws || ws_bytes < need))
     return fail(FRAC_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", need, ws ? ws_bytes : (size_t)0);

@@ -41,6 +41,12 @@ struct ScanParams {
   void* dBm;
   void* dCm;
   float* dD;
+  // further gradients (the form without B/C only; each NULL = not produced)
+  float* dalpha;
+  float* dlambda;
+  float* dread_logit;
+  float* dwrite_logit;
+  float* dinit_state;
 };
 
 // Each launcher returns hipSuccess or the launch error; `stream` may be null.

@@ -337,9 +337,13 @@ struct NfWork {
   float* fA;          // [nps][B H L]
   float* F;           // [nps][B H] sum_m r_m <dS_final, S_final> over this workgroup's columns
   float* dDp;         // [nps][B H] sum dy . x over this workgroup's columns
+  // per-(token, mode) partials over this workgroup's columns (NULL: not wanted)
+  float* dcp;         // [nps][B H L][M] <h_{t,m}, dy_t>: gradient of the read weight c_{t,m}
+  float* dkp;         // [nps][B H L][M] <G_{t,m}, x_t>: gradient of the injection kappa_{t,m}
 };
 
-template <typename T, int MP>
+// WGRAD: also the per-(token, mode) weight-gradient partials (wk.dcp, wk.dkp).
+template <typename T, int MP, bool WGRAD>
 __global__ void __launch_bounds__(256) frac_nfree_bwd_kernel(ScanParams p, NfWork wk) {
   constexpr bool kBf16 = sizeof(T) == 2;
   constexpr int MB = (MP + 15) / 16;
@@ -358,6 +362,7 @@ __global__ void __launch_bounds__(256) frac_nfree_bwd_kernel(ScanParams p, NfWor
   __shared__ __align__(16) T Xs[64 * XS];                      // x [t][p]
   __shared__ __align__(16) T Ys[64 * XS];                      // dy [t][p]
   __shared__ __align__(16) T GT[64 * XS];                      // Gamma^T [t][t'], t' >= t
+  __shared__ __align__(16) T HT[WGRAD ? 64 * XS : 8];         // dY X^T [t][k], k <= t (weight gradients)
   T* const DX = Xs;  // dx rows [t][p] (bfloat16 staging; x is no longer read by then)
   __shared__ __align__(16) float Gt[MP * WQ];                  // the adjoint [m][p]
   __shared__ __align__(16) float W[NWA * MP * WQ + kQ];
@@ -376,7 +381,10 @@ __global__ void __launch_bounds__(256) frac_nfree_bwd_kernel(ScanParams p, NfWor
   float* P_c = W + 7 * SW;    // c (modes past the factorisation bound)
   float* P_A = W + NWA * SW;  // [Q] A_t
 
-  for (int i = tid; i < 64 * XS; i += 256) GT[i] = (T)0.0f;
+  for (int i = tid; i < 64 * XS; i += 256) {
+    GT[i] = (T)0.0f;
+    if constexpr (WGRAD) HT[i] = (T)0.0f;
+  }
   if (tid < MP) {
     const float tau = (tid < M) ? p.tau[tid] : 1.0f;
     s_rr[tid] = (tid < M) ? 1.0f / tau : 0.0f;
@@ -567,6 +575,7 @@ __global__ void __launch_bounds__(256) frac_nfree_bwd_kernel(ScanParams p, NfWor
         const int t = tb * 16 + lg * 4 + r, k = kb * 16 + li;
         GT[k * XS + t] = (T)keep_if_ge(Gm[r], t, k);
         const float hm = keep_if_ge(D[r], t, k);
+        if constexpr (WGRAD) HT[t * XS + k] = (T)hm;
         rv[r] = hm * Ph[r];
         ce += hm * Ph[r];
         cf += hm * Ps[r];
@@ -588,13 +597,16 @@ __global__ void __launch_bounds__(256) frac_nfree_bwd_kernel(ScanParams p, NfWor
 
     // ---- per token (row block tb = wave): readout part of e from S0 . dy, adjoint
     // parts of e and f from G . x (modes as output columns, reduced over 16 lanes)
+    floatx4 Uk[MB], Zk[MB];  // S0 . dy and G . x of this wave's tokens, kept for the weight gradients
     {
       const int tb = wave;
       float eR[4] = {0.f, 0.f, 0.f, 0.f}, eJ[4] = {0.f, 0.f, 0.f, 0.f}, fJ[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int mb = 0; mb < MB; ++mb) {
         const int m = mb * 16 + li;  // output column of this lane
-        floatx4 U = {0.f, 0.f, 0.f, 0.f}, Z = {0.f, 0.f, 0.f, 0.f};
+        floatx4& U = Uk[mb];
+        floatx4& Z = Zk[mb];
+        U = Z = floatx4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int kp = 0; kp < 2; ++kp) {
           Frag<T> S0f, Gf;
@@ -649,6 +661,57 @@ __global__ void __launch_bounds__(256) frac_nfree_bwd_kernel(ScanParams p, NfWor
       }
     }
     barrier();  // Gamma^T, slots and token partials in LDS
+
+    if constexpr (WGRAD) {
+      // ---- per-(token, mode) partials, tokens of row block tb = wave, modes as columns:
+      //   dc_{t,m} = e^{-rA_t} (S0_m . dy_t) + sum_{k<=t} H_{t,k} kappa_{k,m} e^{-r(A_t-A_k)}
+      //   dk_{k,m} = e^{-r(A_Q-A_k)} (G_m . x_k) + sum_{t>=k} H_{t,k} c_{t,m} e^{-r(A_t-A_k)}
+      // with the sums as float32 matrix-core products (H kappa e^{rA}, H^T c e^{-rA}) for
+      // the factorised modes and one exp per pair for the others
+      const int tb = wave;
+      const float AQ = Alast;
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb) {
+        const int m = mb * 16 + li;
+        const bool fac = m < MP && !((unsafe >> m) & 1);
+        floatx4 cI = {0.f, 0.f, 0.f, 0.f}, kI = {0.f, 0.f, 0.f, 0.f};
+        for (int kq = 0; kq < (tb + 1) * 4; ++kq) {
+          const int k = kq * 4 + lg;
+          const float a = to_f32(HT[(tb * 16 + li) * XS + k]);
+          const float bb = fac ? P_Vt[m * WQ + k] : 0.0f;
+          cI = __builtin_amdgcn_mfma_f32_16x16x4f32(a, bb, cI, 0, 0, 0);
+        }
+        for (int tq = tb * 4; tq < 16; ++tq) {
+          const int t = tq * 4 + lg;
+          const float a = to_f32(HT[t * XS + tb * 16 + li]);
+          const float bb = fac ? P_O[m * WQ + t] : 0.0f;
+          kI = __builtin_amdgcn_mfma_f32_16x16x4f32(a, bb, kI, 0, 0, 0);
+        }
+        const bool direct = m < M && ((unsafe >> (m < MP ? m : 0)) & 1);
+        const float rm = (m < MP) ? s_rr[m] : 0.0f;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int t = tb * 16 + lg * 4 + r;
+          const float At = P_A[t];
+          float dc = fexp(-rm * At) * Uk[mb][r];
+          float dk = fexp(-rm * (AQ - At)) * Zk[mb][r];
+          if (!direct) {
+            dc += fexp(-rm * At) * cI[r];
+            dk += fexp(rm * At) * kI[r];
+          } else {
+            for (int k = 0; k <= t; ++k)
+              dc += to_f32(HT[t * XS + k]) * P_Vt[m * WQ + k] * fexp(-rm * (At - P_A[k]));
+            for (int t2 = t; t2 < 64; ++t2)
+              dk += to_f32(HT[t2 * XS + t]) * P_c[m * WQ + t2] * fexp(-rm * (P_A[t2] - At));
+          }
+          if (m < M && t < nv) {
+            const int64_t i = ((int64_t)ps * p.Bsz * H * L + (int64_t)bh * L + t0 + t) * M + m;  // [nps][B H L][M]
+            wk.dcp[i] = dc;
+            wk.dkp[i] = dk;
+          }
+        }
+      }
+    }
 
     if (active) {
       // ---- dx: inter (weights x adjoint, K = modes), intra Gamma^T dY (K = t' >= t), skip term
@@ -749,6 +812,17 @@ __global__ void __launch_bounds__(256) frac_nfree_bwd_kernel(ScanParams p, NfWor
     }
   }
 
+  // ---- the adjoint of the state before token 0
+  if (p.dinit_state && active) {
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int m = mb * 16 + lg * 4 + r;
+        if (m < M && pc < P) p.dinit_state[sbase + (int64_t)m * P + pc] = G[mb][r];
+      }
+  }
+
   // ---- per-workgroup totals: final-state term and sum(dy . x)
   red[tid] = fpart;
   __syncthreads();
@@ -767,6 +841,64 @@ __global__ void __launch_bounds__(256) frac_nfree_bwd_kernel(ScanParams p, NfWor
   }
 }
 
+// Gradients of the read / write logits, alpha and lambda from the per-(token, mode)
+// partials of the reverse sweep and the step-size gradient; MP lanes per (b, t, h):
+//   dz_c = c (dc - sum_m c dc),  dz_w = w (dw - sum_m w dw),  dw = beta dk
+// (softmax of eq. read-softmax, kappa = beta w), and with s = lambda^{1/alpha}
+// (eq. tau-eff) and the step-size gradient ddt = s dDelta~:
+//   dalpha  = -sum_m (dz_c + dz_w) ln tau_m - ddt Delta ln(lambda) / alpha^2
+//   dlambda = ddt Delta / (alpha lambda)
+template <int MP>
+__global__ void __launch_bounds__(256) frac_nfree_grads_kernel(ScanParams p, const float* __restrict__ dcp,
+                                                               const float* __restrict__ dkp, int nps) {
+  const int64_t pr = (int64_t)blockIdx.x * 256 + threadIdx.x;  // ((b L + t) H + h) MP + m
+  const int64_t ntok = (int64_t)p.Bsz * p.L * p.H;
+  const int64_t tok = pr / MP;
+  const int m = (int)(pr - tok * MP);
+  const bool tv = tok < ntok;  // whole groups of MP lanes past the end compute token 0 and store nothing
+  const int64_t tk = tv ? tok : 0;
+  const int M = p.M, L = p.L, H = p.H;
+  const int h = (int)(tk % H);
+  const int64_t bt = tk / H;
+  const int t = (int)(bt % L), b = (int)(bt / L);
+  const bool mv = m < M;
+  const float al = p.alpha[b * p.as0 + t * p.as1 + h * p.as2];
+  const float lam = p.lambda ? p.lambda[b * p.ls0 + t * p.ls1 + h * p.ls2] : 1.0f;
+  const float dtv = p.dt[tk];
+  const float s_eff = p.lambda ? exp2f(log2f(lam) / al) : 1.0f;
+  const float tau = mv ? p.tau[m] : 1.0f;
+  const float r = 1.0f / tau, lnt = logf(tau);
+  const float prior = -al * lnt;
+  const float zc = mv ? prior + (p.read_logit ? p.read_logit[tk * M + m] : 0.0f) : -INFINITY;
+  const float zw = mv ? prior + (p.write_logit ? p.write_logit[tk * M + m] : 0.0f) : -INFINITY;
+  const float c = group_softmax<MP>(zc);
+  const float w = (p.read_logit == p.write_logit) ? c : group_softmax<MP>(zw);
+  float dc = 0.0f, dk = 0.0f;
+  if (mv) {
+    const int64_t S = (int64_t)p.Bsz * H * L * M;
+    const int64_t i = (((int64_t)b * H + h) * L + t) * M + m;
+    for (int q = 0; q < nps; ++q) {
+      dc += dcp[q * S + i];
+      dk += dkp[q * S + i];
+    }
+  }
+  const float beta = one_minus_exp_neg(dtv * s_eff * r);
+  const float dw = beta * dk;
+  const float sc = group_allreduce<MP>(c * dc, [](float x, float y) { return x + y; });
+  const float sw = group_allreduce<MP>(w * dw, [](float x, float y) { return x + y; });
+  const float dzc = c * (dc - sc), dzw = w * (dw - sw);
+  if (tv && mv) {
+    if (p.dread_logit) p.dread_logit[tk * M + m] = dzc;
+    if (p.dwrite_logit) p.dwrite_logit[tk * M + m] = dzw;
+  }
+  const float dap = group_allreduce<MP>(mv ? -(dzc + dzw) * lnt : 0.0f, [](float x, float y) { return x + y; });
+  if (tv && m == 0) {
+    const float g = p.ddt[tk] * dtv;
+    if (p.dalpha) p.dalpha[tk] = dap + (p.lambda ? -g * logf(lam) / (al * al) : 0.0f);
+    if (p.dlambda) p.dlambda[tk] = p.lambda ? g / (al * lam) : 0.0f;
+  }
+}
+
 template <typename T>
 hipError_t launch_nfree_t(const ScanParams& p, hipStream_t stream) {
   const unsigned blocks = (unsigned)((int64_t)p.Bsz * p.H * ((p.P + 63) / 64));
@@ -778,7 +910,7 @@ hipError_t launch_nfree_t(const ScanParams& p, hipStream_t stream) {
 }
 
 struct NfLayout {
-  size_t ckpt, eA, fA, F, dDp, tsum, total;
+  size_t ckpt, eA, fA, F, dDp, tsum, dcp, dkp, total;
 };
 
 NfLayout nfree_layout(const ScanParams& p) {
@@ -791,7 +923,9 @@ NfLayout nfree_layout(const ScanParams& p) {
   l.F = l.fA + up(sizeof(float) * nps * bh * p.L);
   l.dDp = l.F + up(sizeof(float) * nps * bh);
   l.tsum = l.dDp + up(sizeof(float) * nps * bh);
-  l.total = l.tsum + up(sizeof(float) * bh * ((p.L + 63) / 64));
+  l.dcp = l.tsum + up(sizeof(float) * bh * ((p.L + 63) / 64));
+  l.dkp = l.dcp + up(sizeof(float) * nps * bh * p.L * p.M);
+  l.total = l.dkp + up(sizeof(float) * nps * bh * p.L * p.M);
   return l;
 }
 
@@ -805,16 +939,27 @@ hipError_t launch_nfree_bwd_mp(const ScanParams& p, void* ws, hipStream_t stream
   wk.fA = reinterpret_cast<float*>(base + l.fA);
   wk.F = reinterpret_cast<float*>(base + l.F);
   wk.dDp = reinterpret_cast<float*>(base + l.dDp);
+  const bool wgrad = p.dalpha || p.dlambda || p.dread_logit || p.dwrite_logit;
+  wk.dcp = wgrad ? reinterpret_cast<float*>(base + l.dcp) : nullptr;
+  wk.dkp = wgrad ? reinterpret_cast<float*>(base + l.dkp) : nullptr;
   const unsigned blocks = (unsigned)((int64_t)p.Bsz * p.H * ((p.P + 63) / 64));
   hipLaunchKernelGGL((frac_nfree_fwd_kernel<T, MP, true>), dim3(blocks), dim3(256), 0, stream, p,
                      reinterpret_cast<float*>(base + l.ckpt));
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((frac_nfree_bwd_kernel<T, MP>), dim3(blocks), dim3(256), 0, stream, p, wk);
+  if (wgrad)
+    hipLaunchKernelGGL((frac_nfree_bwd_kernel<T, MP, true>), dim3(blocks), dim3(256), 0, stream, p, wk);
+  else
+    hipLaunchKernelGGL((frac_nfree_bwd_kernel<T, MP, false>), dim3(blocks), dim3(256), 0, stream, p, wk);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   const int nps = (p.P + 63) / 64;
-  return launch_ddt_finish(p, wk.eA, wk.fA, nullptr, nullptr, wk.F, wk.dDp, reinterpret_cast<float*>(base + l.tsum),
-                           nps, 0, nps, stream);
+  e = launch_ddt_finish(p, wk.eA, wk.fA, nullptr, nullptr, wk.F, wk.dDp, reinterpret_cast<float*>(base + l.tsum), nps,
+                        0, nps, stream);
+  if (e != hipSuccess || !wgrad) return e;
+  const int64_t pairs = (int64_t)p.Bsz * p.L * p.H * MP;
+  hipLaunchKernelGGL((frac_nfree_grads_kernel<MP>), dim3((unsigned)((pairs + 255) / 256)), dim3(256), 0, stream, p,
+                     wk.dcp, wk.dkp, nps);
+  return hipGetLastError();
 }
 
 template <typename T>

@@ -148,3 +148,17 @@ def test_projection_free_form_checks_its_arguments_on_the_host():
     assert lib.frac_scan_bwd(ctypes.byref(sh), ctypes.byref(b), None, 0, None) == -1
     b.dBm = None
     assert lib.frac_scan_bwd(ctypes.byref(sh), ctypes.byref(b), None, 0, None) == -3  # no workspace
+
+
+@pytest.mark.parametrize("field", ["dalpha", "dlambda", "dread_logit", "dwrite_logit", "dinit_state"])
+def test_further_gradients_are_for_the_form_without_projections_only(field):
+    """dalpha, dlambda, the logit gradients and dinit_state exist for dstate 1 only;
+    asked for with B/C projections the call is refused on the host."""
+    lib = _lib.load()
+    sh = _shape()
+    assert sh.dstate > 1
+    buf = (ctypes.c_float * 64)()
+    b = FracBwdArgs()
+    setattr(b, field, ctypes.cast(buf, ctypes.c_void_p))
+    assert lib.frac_scan_bwd(ctypes.byref(sh), ctypes.byref(b), None, 0, None) == -2
+    assert field in lib.frac_last_error().decode()

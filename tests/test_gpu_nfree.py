@@ -154,7 +154,8 @@ def test_nfree_bwd_parity(name):
     dfs = inp.get("d_final_state")
     print("case", name, w, flush=True)
     kw = {k: inp[k] for k in ("lam", "read_logit", "write_logit", "D", "init_state") if k in inp}
-    g = frac.scan_bwd(inp["x"], inp["dt"], None, None, inp["alpha"], tau_d, inp["dy"], d_final_state=dfs, **kw)
+    g = frac.scan_bwd(inp["x"], inp["dt"], None, None, inp["alpha"], tau_d, inp["dy"], d_final_state=dfs,
+                      all_grads=True, **kw)
     torch.cuda.synchronize()
     ref = _oracle_bwd(inp, tau64, dfs)
     tol = TOL[w.io_dtype]
@@ -163,6 +164,21 @@ def test_nfree_bwd_parity(name):
     assert_close("ddt", f64(g["ddt"]), ref["ddt"], tol)
     if "D" in inp:
         assert_close("dD", f64(g["dD"]), ref["dD"], tol)
+    _check_further_grads(g, ref, tol, "lam" in inp)
+
+
+def _check_further_grads(g, ref, tol, has_lambda):
+    """Gradients of alpha, lambda, the logits (the oracle's, also at zero logits) and
+    the initial state."""
+    assert_close("dalpha", f64(g["dalpha"]), ref["dalpha"], tol)
+    if has_lambda:
+        assert_close("dlambda", f64(g["dlambda"]), ref["dlambda"], tol)
+    else:
+        assert not g["dlambda"].any()
+    assert_close("dread_logit", f64(g["dread_logit"]), ref["dread_logit"], tol)
+    assert_close("dwrite_logit", f64(g["dwrite_logit"]), ref["dwrite_logit"], tol)
+    for m in range(ref["dinit_state"].shape[2]):
+        assert_close("dinit_state mode %d" % m, f64(g["dinit_state"])[:, :, m], ref["dinit_state"][:, :, m], tol)
 
 
 def test_nfree_bwd_large_steps_use_direct_decay():
@@ -170,11 +186,26 @@ def test_nfree_bwd_large_steps_use_direct_decay():
     inp = device_inputs(w, seed=16)
     inp["dt"] = (inp["dt"] * 8.0).contiguous()
     tau_d, tau64 = _tau(16)
-    g = frac.scan_bwd(inp["x"], inp["dt"], None, None, inp["alpha"], tau_d, inp["dy"])
+    g = frac.scan_bwd(inp["x"], inp["dt"], None, None, inp["alpha"], tau_d, inp["dy"], all_grads=True)
     torch.cuda.synchronize()
     ref = _oracle_bwd(inp, tau64)
     assert_close("dx", f64(g["dx"]), ref["dx"], TOL["bf16"])
     assert_close("ddt", f64(g["ddt"]), ref["ddt"], TOL["bf16"])
+    _check_further_grads(g, ref, TOL["bf16"], False)
+
+
+def test_nfree_bwd_all_grads_leave_the_other_outputs_unchanged():
+    """Asking for the further gradients takes another kernel variant: dx, ddt and dD
+    must not change bit for bit."""
+    w = Workload("t", 1, 150, 2, 128, 1, 16, bc=False, backward=True, extras=True)
+    inp = device_inputs(w, seed=18)
+    tau_d, _ = _tau(16)
+    kw = {k: inp[k] for k in ("lam", "read_logit", "write_logit", "D") if k in inp}
+    g1 = frac.scan_bwd(inp["x"], inp["dt"], None, None, inp["alpha"], tau_d, inp["dy"], **kw)
+    g2 = frac.scan_bwd(inp["x"], inp["dt"], None, None, inp["alpha"], tau_d, inp["dy"], all_grads=True, **kw)
+    torch.cuda.synchronize()
+    for k in ("dx", "ddt", "dD"):
+        assert torch.equal(g1[k], g2[k]), k
 
 
 def test_nfree_bwd_deterministic():
