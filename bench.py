@@ -147,6 +147,9 @@ def bench_scan(torch, frac, w, steps, warmup):
     def bwd():
         frac.scan_bwd(x, dt, Bm, Cm, alpha, tau, dy, workspace=ws_b)
 
+    def bwd_all():  # the form without B/C: also the gradients of alpha, lambda, the logits, the initial state
+        frac.scan_bwd(x, dt, Bm, Cm, alpha, tau, dy, workspace=ws_b, all_grads=True)
+
     for _ in range(warmup):
         fwd()
         if w.backward:
@@ -177,6 +180,13 @@ def bench_scan(torch, frac, w, steps, warmup):
     if not w.bc:  # without B/C the forward moves more bytes than it does matrix-core work
         res["fwd_roofline"] = roofline("hbm", nfree_fwd_bytes(w), fms, PEAK_HBM_BYTES, "GB/s")
     if w.backward and not w.bc:
+        for _ in range(warmup):
+            bwd_all()
+        ta = Timer(torch)
+        for _ in range(steps):
+            with ta:
+                bwd_all()
+        res["bwd_all_grads_ms"] = float(np.mean(ta.ms()))
         res["bwd_ms"] = bms
         res["bwd_roofline"] = dict(roofline("hbm", nfree_bwd_bytes(w), bms, PEAK_HBM_BYTES, "GB/s"),
                                    traffic=measured_traffic("frac_scan_bwd", w.name))
