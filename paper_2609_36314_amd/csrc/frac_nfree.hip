@@ -344,7 +344,7 @@ struct NfWork {
 
 // WGRAD: also the per-(token, mode) weight-gradient partials (wk.dcp, wk.dkp).
 template <typename T, int MP, bool WGRAD>
-__global__ void __launch_bounds__(256) frac_nfree_bwd_kernel(ScanParams p, NfWork wk) {
+__global__ void __launch_bounds__(256, 2) frac_nfree_bwd_kernel(ScanParams p, NfWork wk) {
   constexpr bool kBf16 = sizeof(T) == 2;
   constexpr int MB = (MP + 15) / 16;
   constexpr int XS = kBf16 ? 64 + 8 : 64 + 4;
