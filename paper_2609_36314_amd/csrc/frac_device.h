@@ -31,6 +31,16 @@ __device__ __forceinline__ int tile_col(int tile) { const int tb = tile_row(tile
 // memory (a wait there would also drain the next chunk's tile copies).  Zero for
 // pairs past the chunk, absent logits, and wl when the write logits are the read
 // logits (the weight pass reuses the read weights then).
+// A value fixed in a register at this point.  A prefetched register read after
+// later memory operations have been issued makes the wave wait for those too (the
+// vector-memory counter drains in order, and direct-to-LDS copies are not tracked
+// by the compiler), so each chunk takes its prefetched values this way right after
+// its memory wait, before it issues the next chunk's copies and loads.
+__device__ __forceinline__ float pinned(float v) {
+  asm volatile("" : "+v"(v));
+  return v;
+}
+
 template <int MP, int NT>
 struct PairLogits {
   static constexpr int NPR = (kQ * MP + NT - 1) / NT;
@@ -45,6 +55,15 @@ struct PairLogits {
       rl[j] = (ok && rlp) ? rlp[i] : 0.0f;
       wl[j] = (ok && wlp && wlp != rlp) ? wlp[i] : 0.0f;
     }
+  }
+  __device__ __forceinline__ PairLogits pinned_copy() const {
+    PairLogits o;
+#pragma unroll
+    for (int j = 0; j < NPR; ++j) {
+      o.rl[j] = pinned(rl[j]);
+      o.wl[j] = pinned(wl[j]);
+    }
+    return o;
   }
 };
 
@@ -432,6 +451,19 @@ struct TilePrefetch {
     }
   }
   __device__ __forceinline__ float get(int j, int r) const { return to_f32(v[j].e[r]); }
+  __device__ __forceinline__ TilePrefetch pinned_copy() const {  // see pinned()
+    TilePrefetch o;
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      constexpr int W = sizeof(V) / 4;
+      uint32_t w[W];
+      __builtin_memcpy(w, &v[j], sizeof(V));
+#pragma unroll
+      for (int i = 0; i < W; ++i) asm volatile("" : "+v"(w[i]));
+      __builtin_memcpy(&o.v[j], w, sizeof(V));
+    }
+    return o;
+  }
 };
 
 // Wait for this wave's outstanding vector-memory operations (including the

@@ -325,6 +325,10 @@ __global__ void __launch_bounds__(512) frac_fwd_kernel(ScanParams p, const T* __
     float* Enext = s_E2 + ((c + 1) & 1) * MP;
     wait_vmem();
     barrier();  // this chunk's tiles have landed; every wave is done with the previous chunk
+    // this chunk's prefetched controls, logits and C B^T values, taken before any new memory operation
+    const float dtv = pinned(dt_n), al_l = pinned(al_n), lam_l = pinned(lam_n);
+    const PairLogits<MP, 512> lgt = lgt_n.pinned_copy();
+    const TilePrefetch<T> gcur = gtile.pinned_copy();
     if (!STATE_ONLY && c > c0) store_y(c - 1);
     if (Cfg::NBUF == 2) {
       if (c + 1 < c1) stage(c + 1, Xn, Bn, Cn);
@@ -333,8 +337,6 @@ __global__ void __launch_bounds__(512) frac_fwd_kernel(ScanParams p, const T* __
       wait_vmem();
       barrier();
     }
-    const float dtv = dt_n, al_l = al_n, lam_l = lam_n;
-    const PairLogits<MP, 512> lgt = lgt_n;
     if (c + 1 < c1) load_controls(c + 1, dt_n, al_n, lam_n);
 
     // ---- per-token step and its chunk-local cumulative sum (lane = token, every wave)
@@ -399,7 +401,7 @@ __global__ void __launch_bounds__(512) frac_fwd_kernel(ScanParams p, const T* __
         const int tb = tile_row(tile), kb = tile_col(tile);
         float Gt[4];
 #pragma unroll
-        for (int r = 0; r < 4; ++r) Gt[r] = gtile.get(jt, r);
+        for (int r = 0; r < 4; ++r) Gt[r] = gcur.get(jt, r);
         floatx4 Gm = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int q = 0; q < (MP + 3) / 4; ++q) {
