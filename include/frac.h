@@ -167,6 +167,49 @@ typedef struct {
   void *y;
 } frac_step_args;
 
+/* Parameter construction of the control branch (FracMixer, Sec. 3.3; clipping
+ * ranges of the experimental setup; gated read / write maps of the appendix on the
+ * state-transition algorithm), elementwise per (b, t, h) and (b, t, h, m):
+ *   dt          = clip(softplus(z_dt + dt_bias[h]), dt_min, dt_max)
+ *   alpha       = sigmoid(z_alpha)
+ *   lambda      = clip(softplus(z_lambda), lambda_min, lambda_max)
+ *   read_logit  = sigmoid(p_read)  * v_read      (v = W u, the caller's projection)
+ *   write_logit = sigmoid(p_write) * v_write
+ * The paper's ranges are dt in [1e-4, 1] and lambda in [0.25, 4]; the derivative
+ * of a clip is 1 on the closed range and 0 outside.  Uses shape.batch, seqlen,
+ * nheads, nmodes.  All pointers are device pointers to f32:
+ *   z_dt, z_alpha [B,L,H] and dt, alpha [B,L,H]: required
+ *   dt_bias [H]: NULL = 0
+ *   z_lambda [B,L,H] with lambda [B,L,H]: both or neither
+ *   v_read [B,L,H,M] with p_read (one scalar) and read_logit [B,L,H,M]: all or none;
+ *   likewise v_write, p_write, write_logit
+ *   dt_min <= dt_max, lambda_min <= lambda_max (else FRAC_ERR_INVALID_ARG). */
+typedef struct {
+  const float *z_dt, *dt_bias, *z_alpha, *z_lambda;
+  const float *v_read, *v_write;
+  const float *p_read, *p_write;
+  float dt_min, dt_max, lambda_min, lambda_max;
+  float *dt, *alpha, *lambda, *read_logit, *write_logit;
+} frac_params_args;
+
+/* Backward of frac_params_fwd.  fwd holds the forward's inputs (its outputs are
+ * ignored).  Gradients of the outputs (ddt, dalpha, dlambda [B,L,H], dread_logit,
+ * dwrite_logit [B,L,H,M]) may be NULL (zero).  Written when non-NULL: dz_dt,
+ * dz_alpha, dz_lambda [B,L,H], ddt_bias [H] (summed over b and t in a fixed order),
+ * dv_read, dv_write [B,L,H,M], dp_read, dp_write (one scalar each, fixed-order sums).
+ * ws: frac_params_workspace_size() bytes of device scratch. */
+typedef struct {
+  frac_params_args fwd;
+  const float *ddt, *dalpha, *dlambda, *dread_logit, *dwrite_logit;
+  float *dz_dt, *ddt_bias, *dz_alpha, *dz_lambda;
+  float *dv_read, *dv_write, *dp_read, *dp_write;
+} frac_params_bwd_args;
+
+frac_status frac_params_fwd(const frac_shape *shape, const frac_params_args *args, void *stream);
+size_t frac_params_workspace_size(const frac_shape *shape);
+frac_status frac_params_bwd(const frac_shape *shape, const frac_params_bwd_args *args, void *ws, size_t ws_bytes,
+                            void *stream);
+
 /* Bytes of device workspace frac_scan_fwd (backward = 0) or frac_scan_bwd
  * (backward = 1) needs for `shape`; 0 means none.  Returns 0 for an invalid shape
  * (the scan call then reports the error). */

@@ -216,3 +216,72 @@ def decode_step(state, x, dt, Bm, Cm, alpha, tau, *, lam=None, read_logit=None, 
     _lib.check(_lib.load().frac_decode_step(ctypes.byref(shape), ctypes.byref(a), _stream()))
     del alpha_t, lam_t
     return y
+
+
+DT_RANGE = (1e-4, 1.0)       # the paper's clipping of the step
+LAMBDA_RANGE = (0.25, 4.0)   # and of the fractional scale
+
+
+def _params_struct(z_dt, dt_bias, z_alpha, z_lambda, v_read, v_write, p_read, p_write, dt_range, lambda_range):
+    keep = [_f32(t, n) for t, n in ((z_dt, "z_dt"), (dt_bias, "dt_bias"), (z_alpha, "z_alpha"),
+                                    (z_lambda, "z_lambda"), (v_read, "v_read"), (v_write, "v_write"),
+                                    (p_read, "p_read"), (p_write, "p_write"))]
+    a = _lib.FracParamsArgs()
+    (a.z_dt, a.dt_bias, a.z_alpha, a.z_lambda, a.v_read, a.v_write, a.p_read, a.p_write) = (_ptr(t) for t in keep)
+    a.dt_min, a.dt_max = dt_range
+    a.lambda_min, a.lambda_max = lambda_range
+    return a, keep
+
+
+def _params_shape(z_dt, v):
+    B, L, H = z_dt.shape
+    return FracShape(B, L, H, 1, 1, 1, 1 if v is None else int(v.shape[-1]), 0, FRAC_F32)
+
+
+def params_fwd(z_dt, z_alpha, *, dt_bias=None, z_lambda=None, v_read=None, v_write=None, p_read=None, p_write=None,
+               dt_range=DT_RANGE, lambda_range=LAMBDA_RANGE):
+    """Control-branch parameter construction (frac_params_fwd): z_* [B,L,H], dt_bias [H],
+    v_* [B,L,H,M], p_* one-element tensors (all float32 on the device).  Returns
+    dict(dt, alpha, lam, read_logit, write_logit), None for what has no input."""
+    v = v_read if v_read is not None else v_write
+    shape = _params_shape(z_dt, v)
+    a, keep = _params_struct(z_dt, dt_bias, z_alpha, z_lambda, v_read, v_write, p_read, p_write, dt_range,
+                             lambda_range)
+    out = dict(dt=torch.empty_like(z_dt), alpha=torch.empty_like(z_dt),
+               lam=None if z_lambda is None else torch.empty_like(z_dt),
+               read_logit=None if v_read is None else torch.empty_like(v_read),
+               write_logit=None if v_write is None else torch.empty_like(v_write))
+    a.dt, a.alpha, a.lam = _ptr(out["dt"]), _ptr(out["alpha"]), _ptr(out["lam"])
+    a.read_logit, a.write_logit = _ptr(out["read_logit"]), _ptr(out["write_logit"])
+    _lib.check(_lib.load().frac_params_fwd(ctypes.byref(shape), ctypes.byref(a), _stream()))
+    del keep
+    return out
+
+
+def params_bwd(z_dt, z_alpha, *, dt_bias=None, z_lambda=None, v_read=None, v_write=None, p_read=None, p_write=None,
+               ddt=None, dalpha=None, dlambda=None, dread_logit=None, dwrite_logit=None, dt_range=DT_RANGE,
+               lambda_range=LAMBDA_RANGE):
+    """Backward of params_fwd (frac_params_bwd).  Returns dict(dz_dt, ddt_bias, dz_alpha,
+    dz_lambda, dv_read, dv_write, dp_read, dp_write), None for what has no input."""
+    v = v_read if v_read is not None else v_write
+    shape = _params_shape(z_dt, v)
+    f, keep = _params_struct(z_dt, dt_bias, z_alpha, z_lambda, v_read, v_write, p_read, p_write, dt_range,
+                             lambda_range)
+    grads = [_f32(t, n) for t, n in ((ddt, "ddt"), (dalpha, "dalpha"), (dlambda, "dlambda"),
+                                     (dread_logit, "dread_logit"), (dwrite_logit, "dwrite_logit"))]
+    H = z_dt.shape[-1]
+    e = lambda t: None if t is None else torch.empty_like(t)
+    out = dict(dz_dt=torch.empty_like(z_dt), ddt_bias=torch.empty(H, dtype=torch.float32, device=z_dt.device),
+               dz_alpha=torch.empty_like(z_dt), dz_lambda=e(z_lambda), dv_read=e(v_read), dv_write=e(v_write),
+               dp_read=None if v_read is None else torch.empty(1, dtype=torch.float32, device=z_dt.device),
+               dp_write=None if v_write is None else torch.empty(1, dtype=torch.float32, device=z_dt.device))
+    a = _lib.FracParamsBwdArgs()
+    a.fwd = f
+    a.ddt, a.dalpha, a.dlambda, a.dread_logit, a.dwrite_logit = (_ptr(t) for t in grads)
+    for k in out:
+        setattr(a, k, _ptr(out[k]))
+    ws = torch.empty(_lib.load().frac_params_workspace_size(ctypes.byref(shape)), dtype=torch.uint8,
+                     device=z_dt.device)
+    _lib.check(_lib.load().frac_params_bwd(ctypes.byref(shape), ctypes.byref(a), _ptr(ws), ws.numel(), _stream()))
+    del keep, grads
+    return out

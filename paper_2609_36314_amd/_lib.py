@@ -21,7 +21,8 @@ STATUS = {0: "FRAC_OK", -1: "FRAC_ERR_INVALID_ARG", -2: "FRAC_ERR_UNSUPPORTED", 
 
 # every symbol include/frac.h declares
 EXPORTS = ("frac_scan_workspace_size", "frac_scan_fwd", "frac_scan_bwd", "frac_decode_step", "frac_default_tau",
-           "frac_status_string", "frac_last_error")
+           "frac_status_string", "frac_last_error", "frac_params_fwd", "frac_params_workspace_size",
+           "frac_params_bwd")
 
 
 class FracShape(ctypes.Structure):
@@ -51,6 +52,21 @@ class FracStepArgs(ctypes.Structure):
                 ("lam", c_void_p), ("lambda_stride", c_int64 * 2),
                 ("read_logit", c_void_p), ("write_logit", c_void_p), ("tau", c_void_p), ("D", c_void_p),
                 ("state", c_void_p), ("y", c_void_p)]
+
+
+class FracParamsArgs(ctypes.Structure):
+    _fields_ = [("z_dt", c_void_p), ("dt_bias", c_void_p), ("z_alpha", c_void_p), ("z_lambda", c_void_p),
+                ("v_read", c_void_p), ("v_write", c_void_p), ("p_read", c_void_p), ("p_write", c_void_p),
+                ("dt_min", ctypes.c_float), ("dt_max", ctypes.c_float), ("lambda_min", ctypes.c_float),
+                ("lambda_max", ctypes.c_float), ("dt", c_void_p), ("alpha", c_void_p), ("lam", c_void_p),
+                ("read_logit", c_void_p), ("write_logit", c_void_p)]
+
+
+class FracParamsBwdArgs(ctypes.Structure):
+    _fields_ = [("fwd", FracParamsArgs), ("ddt", c_void_p), ("dalpha", c_void_p), ("dlambda", c_void_p),
+                ("dread_logit", c_void_p), ("dwrite_logit", c_void_p), ("dz_dt", c_void_p), ("ddt_bias", c_void_p),
+                ("dz_alpha", c_void_p), ("dz_lambda", c_void_p), ("dv_read", c_void_p), ("dv_write", c_void_p),
+                ("dp_read", c_void_p), ("dp_write", c_void_p)]
 
 
 class FracError(RuntimeError):
@@ -84,6 +100,12 @@ def load():
     lib.frac_status_string.restype = c_char_p
     lib.frac_last_error.argtypes = []
     lib.frac_last_error.restype = c_char_p
+    lib.frac_params_fwd.argtypes = [POINTER(FracShape), POINTER(FracParamsArgs), c_void_p]
+    lib.frac_params_fwd.restype = c_int
+    lib.frac_params_workspace_size.argtypes = [POINTER(FracShape)]
+    lib.frac_params_workspace_size.restype = c_size_t
+    lib.frac_params_bwd.argtypes = [POINTER(FracShape), POINTER(FracParamsBwdArgs), c_void_p, c_size_t, c_void_p]
+    lib.frac_params_bwd.restype = c_int
     _lib = lib
     return lib
 

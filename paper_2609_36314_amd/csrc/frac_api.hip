@@ -137,6 +137,41 @@ frac_status hip_status(hipError_t e, const char* what) {
 
 }  // namespace
 
+// ------------------------------------------------------- parameter construction
+
+namespace {
+
+frac_status params_dims(const frac_shape* sh, frac::ParamsDims& d) {
+  if (!sh) return fail(FRAC_ERR_INVALID_ARG, "shape is NULL");
+  if (sh->batch < 0 || sh->seqlen < 0) return fail(FRAC_ERR_INVALID_ARG, "batch and seqlen must be >= 0");
+  if (sh->nheads < 1 || sh->nmodes < 1) return fail(FRAC_ERR_INVALID_ARG, "nheads and nmodes must be >= 1");
+  if (sh->nheads > (1 << 24) || sh->nmodes > 4096)
+    return fail(FRAC_ERR_UNSUPPORTED, "nheads or nmodes too large for the parameter kernels");
+  d.rows = sh->batch * sh->seqlen;
+  d.H = (int)sh->nheads;
+  d.M = (int)sh->nmodes;
+  return ok();
+}
+
+frac_status params_inputs(const frac_params_args* a, bool need_outputs) {
+  if (!a) return fail(FRAC_ERR_INVALID_ARG, "args is NULL");
+  if (!a->z_dt || !a->z_alpha) return fail(FRAC_ERR_INVALID_ARG, "z_dt and z_alpha are required");
+  if (!(a->dt_min <= a->dt_max)) return fail(FRAC_ERR_INVALID_ARG, "dt_min must be <= dt_max");
+  if (a->z_lambda && !(a->lambda_min <= a->lambda_max))
+    return fail(FRAC_ERR_INVALID_ARG, "lambda_min must be <= lambda_max");
+  if ((a->v_read && !a->p_read) || (a->v_write && !a->p_write))
+    return fail(FRAC_ERR_INVALID_ARG, "v_read needs p_read and v_write needs p_write");
+  if (need_outputs) {
+    if (!a->dt || !a->alpha) return fail(FRAC_ERR_INVALID_ARG, "dt and alpha are required");
+    if (!a->z_lambda != !a->lambda) return fail(FRAC_ERR_INVALID_ARG, "z_lambda and lambda go together");
+    if (!a->v_read != !a->read_logit || !a->v_write != !a->write_logit)
+      return fail(FRAC_ERR_INVALID_ARG, "v_read / read_logit and v_write / write_logit go together");
+  }
+  return ok();
+}
+
+}  // namespace
+
 extern "C" {
 
 const char* frac_status_string(frac_status s) {
@@ -283,6 +318,42 @@ frac_status frac_decode_step(const frac_shape* shape, const frac_step_args* a, v
   p.y = a->y;
   return hip_status(frac::launch_decode_step(p, a->state, reinterpret_cast<hipStream_t>(stream)),
                     "frac_decode_step launch");
+}
+
+
+frac_status frac_params_fwd(const frac_shape* shape, const frac_params_args* a, void* stream) {
+  frac::ParamsDims d{};
+  frac_status s = params_dims(shape, d);
+  if (s != FRAC_OK) return s;
+  if (d.rows == 0) return ok();
+  if ((s = params_inputs(a, true)) != FRAC_OK) return s;
+  return hip_status(frac::launch_params_fwd(d, *a, reinterpret_cast<hipStream_t>(stream)), "frac_params_fwd launch");
+}
+
+size_t frac_params_workspace_size(const frac_shape* shape) {
+  (void)shape;
+  return sizeof(float) * 2 * frac::kParamsMaxBlocks;
+}
+
+frac_status frac_params_bwd(const frac_shape* shape, const frac_params_bwd_args* a, void* ws, size_t ws_bytes,
+                            void* stream) {
+  frac::ParamsDims d{};
+  frac_status s = params_dims(shape, d);
+  if (s != FRAC_OK) return s;
+  if (!a) return fail(FRAC_ERR_INVALID_ARG, "args is NULL");
+  if (d.rows == 0) {  // nothing to read: the sums are zero
+    const hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+    if (a->ddt_bias) hipLaunchKernelGGL(copy_or_zero_kernel, dim3(1), dim3(256), 0, st, a->ddt_bias, nullptr, (int64_t)d.H);
+    if (a->dp_read) hipLaunchKernelGGL(copy_or_zero_kernel, dim3(1), dim3(64), 0, st, a->dp_read, nullptr, (int64_t)1);
+    if (a->dp_write) hipLaunchKernelGGL(copy_or_zero_kernel, dim3(1), dim3(64), 0, st, a->dp_write, nullptr, (int64_t)1);
+    return hip_status(hipGetLastError(), "frac_params_bwd (empty)");
+  }
+  if ((s = params_inputs(&a->fwd, false)) != FRAC_OK) return s;
+  const size_t need = frac_params_workspace_size(shape);
+  if (!ws || ws_bytes < need)
+    return fail(FRAC_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", need, ws ? ws_bytes : (size_t)0);
+  return hip_status(frac::launch_params_bwd(d, *a, reinterpret_cast<float*>(ws), reinterpret_cast<hipStream_t>(stream)),
+                    "frac_params_bwd launch");
 }
 
 }  // extern "C"

@@ -6,6 +6,8 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include "frac.h"
+
 namespace frac {
 
 // Validated problem description handed to the kernel launchers.  Sizes are the
@@ -60,6 +62,15 @@ hipError_t launch_cb_tiles(const ScanParams& p, void* tiles, hipStream_t stream)
 
 hipError_t launch_scan_bwd(const ScanParams& p, void* ws, size_t ws_bytes, hipStream_t stream);
 size_t scan_bwd_workspace(const ScanParams& p);
+
+// Control-branch parameter construction (frac_params.hip).
+struct ParamsDims {
+  int64_t rows;  // B * L
+  int H, M;
+};
+hipError_t launch_params_fwd(const ParamsDims& d, const frac_params_args& a, hipStream_t stream);
+constexpr int kParamsMaxBlocks = 1024;  // partial sums of the backward: 2 floats per block
+hipError_t launch_params_bwd(const ParamsDims& d, const frac_params_bwd_args& a, float* part, hipStream_t stream);
 
 hipError_t launch_decode_step(const ScanParams& p, float* state, hipStream_t stream);
 

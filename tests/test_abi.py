@@ -162,3 +162,31 @@ def test_further_gradients_are_for_the_form_without_projections_only(field):
     setattr(b, field, ctypes.cast(buf, ctypes.c_void_p))
     assert lib.frac_scan_bwd(ctypes.byref(sh), ctypes.byref(b), None, 0, None) == -2
     assert field in lib.frac_last_error().decode()
+
+
+def test_parameter_construction_arguments_are_checked_on_the_host():
+    from paper_2609_36314_amd._lib import FracParamsArgs, FracParamsBwdArgs
+    lib = _lib.load()
+    sh = _shape()
+    buf = (ctypes.c_float * 64)()
+    p = ctypes.cast(buf, ctypes.c_void_p)
+    a = FracParamsArgs()
+    a.dt_min, a.dt_max, a.lambda_min, a.lambda_max = 1e-4, 1.0, 0.25, 4.0
+    assert lib.frac_params_fwd(ctypes.byref(sh), ctypes.byref(a), None) == -1  # no inputs
+    a.z_dt = a.z_alpha = p
+    assert lib.frac_params_fwd(ctypes.byref(sh), ctypes.byref(a), None) == -1  # no outputs
+    a.dt = a.alpha = p
+    a.v_read = p
+    assert lib.frac_params_fwd(ctypes.byref(sh), ctypes.byref(a), None) == -1  # v_read without p_read
+    assert "p_read" in lib.frac_last_error().decode()
+    a.v_read = None
+    a.z_lambda = p
+    assert lib.frac_params_fwd(ctypes.byref(sh), ctypes.byref(a), None) == -1  # z_lambda without lambda
+    a.z_lambda = None
+    a.dt_min, a.dt_max = 1.0, 1e-4
+    assert lib.frac_params_fwd(ctypes.byref(sh), ctypes.byref(a), None) == -1
+    a.dt_min, a.dt_max = 1e-4, 1.0
+    assert lib.frac_params_workspace_size(ctypes.byref(sh)) > 0
+    b = FracParamsBwdArgs()
+    b.fwd = a
+    assert lib.frac_params_bwd(ctypes.byref(sh), ctypes.byref(b), None, 0, None) == -3  # no workspace
