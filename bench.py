@@ -83,6 +83,38 @@ def nfree_bwd_bytes(w):
     return w.batch * w.seqlen * w.nheads * (3 * w.headdim * io + 8)
 
 
+def params_bytes(w):
+    """Compulsory HBM bytes of the parameter construction (f32): forward reads z_dt, z_alpha,
+    z_lambda, v_read, v_write and writes dt, alpha, lambda and the two logits; the backward
+    reads those inputs and the output gradients and writes the input gradients."""
+    n, M = w.batch * w.seqlen * w.nheads, w.nmodes
+    return n * (24 + 16 * M), n * (36 + 24 * M)
+
+
+def bench_params(torch, frac, w, steps, warmup):
+    """frac_params_fwd and frac_params_bwd at the workload's (B, L, H, M), with all inputs."""
+    g = torch.Generator().manual_seed(0)
+    B, L, H, M = w.batch, w.seqlen, w.nheads, w.nmodes
+    r = lambda *s: torch.randn(*s, generator=g).float().cuda()
+    inp = dict(z_dt=r(B, L, H), z_alpha=r(B, L, H), dt_bias=r(H), z_lambda=r(B, L, H), v_read=r(B, L, H, M),
+               v_write=r(B, L, H, M), p_read=r(1), p_write=r(1))
+    cot = dict(ddt=r(B, L, H), dalpha=r(B, L, H), dlambda=r(B, L, H), dread_logit=r(B, L, H, M),
+               dwrite_logit=r(B, L, H, M))
+    for _ in range(warmup):
+        frac.params_fwd(**inp)
+        frac.params_bwd(**inp, **cot)
+    tf, tb = Timer(torch), Timer(torch)
+    for _ in range(steps):
+        with tf:
+            frac.params_fwd(**inp)
+        with tb:
+            frac.params_bwd(**inp, **cot)
+    fms, bms = float(np.mean(tf.ms())), float(np.mean(tb.ms()))
+    fb, bb = params_bytes(w)
+    return {"params_fwd_ms": fms, "params_fwd_roofline": roofline("hbm", fb, fms, PEAK_HBM_BYTES, "GB/s"),
+            "params_bwd_ms": bms, "params_bwd_roofline": roofline("hbm", bb, bms, PEAK_HBM_BYTES, "GB/s")}
+
+
 def decode_bytes_per_step(w):
     B, H, P, N, M, G = w.batch, w.nheads, w.headdim, w.dstate, w.nmodes, w.ngroups
     io = 2 if w.io_dtype == "bf16" else 4
@@ -187,6 +219,7 @@ def bench_scan(torch, frac, w, steps, warmup):
             with ta:
                 bwd_all()
         res["bwd_all_grads_ms"] = float(np.mean(ta.ms()))
+        res.update(bench_params(torch, frac, w, steps, warmup))
         res["bwd_ms"] = bms
         res["bwd_roofline"] = dict(roofline("hbm", nfree_bwd_bytes(w), bms, PEAK_HBM_BYTES, "GB/s"),
                                    traffic=measured_traffic("frac_scan_bwd", w.name))

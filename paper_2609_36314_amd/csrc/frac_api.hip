@@ -331,8 +331,9 @@ frac_status frac_params_fwd(const frac_shape* shape, const frac_params_args* a, 
 }
 
 size_t frac_params_workspace_size(const frac_shape* shape) {
-  (void)shape;
-  return sizeof(float) * 2 * frac::kParamsMaxBlocks;
+  frac::ParamsDims d{};
+  if (params_dims(shape, d) != FRAC_OK) return 0;
+  return frac::params_workspace(d.H);
 }
 
 frac_status frac_params_bwd(const frac_shape* shape, const frac_params_bwd_args* a, void* ws, size_t ws_bytes,

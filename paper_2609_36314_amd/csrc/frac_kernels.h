@@ -69,7 +69,8 @@ struct ParamsDims {
   int H, M;
 };
 hipError_t launch_params_fwd(const ParamsDims& d, const frac_params_args& a, hipStream_t stream);
-constexpr int kParamsMaxBlocks = 1024;  // partial sums of the backward: 2 floats per block
+constexpr int kParamsMaxBlocks = 1024;  // partial sums of the backward: 2 floats per block, H per row block
+size_t params_workspace(int64_t H);
 hipError_t launch_params_bwd(const ParamsDims& d, const frac_params_bwd_args& a, float* part, hipStream_t stream);
 
 hipError_t launch_decode_step(const ScanParams& p, float* state, hipStream_t stream);

@@ -91,49 +91,56 @@ __global__ void __launch_bounds__(256) frac_params_bwd_kernel(ParamsDims d, frac
   }
 }
 
-// One workgroup: the bias gradient per head (16 row lanes x 64 heads, then the 16
-// lanes in order) and the two gate gradients from the per-block partials.
-__global__ void __launch_bounds__(1024) frac_params_reduce_kernel(ParamsDims d, frac_params_bwd_args a,
-                                                                  const float* part, int nblocks) {
+// Partial bias gradients: workgroup (x, y) sums rows x*4 + lane/64 + k*4*gridDim.x
+// of heads 64 y + lane%64 in order, then its 4 row lanes in order, into pb[x][h].
+__global__ void __launch_bounds__(256) frac_params_bias_kernel(ParamsDims d, frac_params_bwd_args a, float* pb) {
   const frac_params_args& f = a.fwd;
-  __shared__ float acc[16][65];
-  const int hh = threadIdx.x & 63, rl = threadIdx.x >> 6;
-  if (a.ddt_bias) {
-    for (int h0 = 0; h0 < d.H; h0 += 64) {
-      const int h = h0 + hh;
-      float s = 0.0f;
-      if (h < d.H && a.ddt) {
-        const float b = f.dt_bias ? f.dt_bias[h] : 0.0f;
-        for (int64_t r = rl; r < d.rows; r += 16) {
-          const int64_t i = r * d.H + h;
-          const float x = f.z_dt[i] + b;
-          float pass;
-          clip_f(softplus_f(x), f.dt_min, f.dt_max, &pass);
-          s += a.ddt[i] * pass * sigmoid_f(x);
-        }
-      }
-      acc[rl][hh] = s;
-      __syncthreads();
-      if (rl == 0 && h < d.H) {
-        float t = 0.0f;
-        for (int k = 0; k < 16; ++k) t += acc[k][hh];
-        a.ddt_bias[h] = t;
-      }
-      __syncthreads();
+  __shared__ float acc[4][64];
+  const int hh = threadIdx.x & 63, rl = threadIdx.x >> 6, h = blockIdx.y * 64 + hh;
+  float s = 0.0f;
+  if (h < d.H && a.ddt) {
+    const float b = f.dt_bias ? f.dt_bias[h] : 0.0f;
+    for (int64_t r = (int64_t)blockIdx.x * 4 + rl; r < d.rows; r += 4 * (int64_t)gridDim.x) {
+      const int64_t i = r * d.H + h;
+      const float x = f.z_dt[i] + b;
+      float pass;
+      clip_f(softplus_f(x), f.dt_min, f.dt_max, &pass);
+      s += a.ddt[i] * pass * sigmoid_f(x);
     }
   }
-  if (threadIdx.x < 2) {
-    const bool rd = threadIdx.x == 0;
+  acc[rl][hh] = s;
+  __syncthreads();
+  if (rl == 0 && h < d.H) pb[(int64_t)blockIdx.x * d.H + h] = (acc[0][hh] + acc[1][hh]) + (acc[2][hh] + acc[3][hh]);
+}
+
+// One wave per output: the bias gradient of each head (from the row-block partials)
+// and the two gate gradients (from the per-block partials).  Lane j adds partials
+// j, j + 64, ... in order, then the lanes are combined by a fixed butterfly.
+__global__ void __launch_bounds__(256) frac_params_reduce_kernel(ParamsDims d, frac_params_bwd_args a,
+                                                                 const float* part, int nblocks, const float* pb,
+                                                                 int nrb) {
+  const frac_params_args& f = a.fwd;
+  const int o = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;  // wave-uniform output
+  auto wave_sum = [&](const float* src, int n, int64_t stride) {
+    float t = 0.0f;
+    for (int q = lane; q < n; q += 64) t += src[(int64_t)q * stride];
+    return group_allreduce<64>(t, [](float x, float y) { return x + y; });
+  };
+  if (o < d.H) {
+    if (!a.ddt_bias) return;
+    const float t = wave_sum(pb + o, nrb, d.H);
+    if (lane == 0) a.ddt_bias[o] = t;
+  } else if (o < d.H + 2) {
+    const bool rd = o == d.H;
     float* out = rd ? a.dp_read : a.dp_write;
-    const float* p = rd ? f.p_read : f.p_write;
-    if (out && (rd ? f.v_read : f.v_write)) {
-      float s = 0.0f;
-      for (int q = 0; q < nblocks; ++q) s += part[2 * q + threadIdx.x];
-      const float g = sigmoid_f(*p);
-      *out = s * g * (1.0f - g);
-    } else if (out) {
-      *out = 0.0f;
+    if (!out) return;
+    if (!(rd ? f.v_read : f.v_write)) {
+      if (lane == 0) *out = 0.0f;
+      return;
     }
+    const float t = wave_sum(part + (rd ? 0 : 1), nblocks, 2);
+    const float g = sigmoid_f(*(rd ? f.p_read : f.p_write));
+    if (lane == 0) *out = t * g * (1.0f - g);
   }
 }
 
@@ -146,13 +153,22 @@ hipError_t launch_params_fwd(const ParamsDims& d, const frac_params_args& a, hip
   return hipGetLastError();
 }
 
+size_t params_workspace(int64_t H) { return sizeof(float) * (2 * kParamsMaxBlocks + (size_t)kParamsMaxBlocks * H); }
+
 hipError_t launch_params_bwd(const ParamsDims& d, const frac_params_bwd_args& a, float* part, hipStream_t stream) {
   const int64_t n = d.rows * d.H * d.M;
   const int blocks = (int)std::max<int64_t>(1, std::min<int64_t>((n + 255) / 256, kParamsMaxBlocks));
   hipLaunchKernelGGL(frac_params_bwd_kernel, dim3(blocks), dim3(256), 0, stream, d, a, part);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(frac_params_reduce_kernel, dim3(1), dim3(1024), 0, stream, d, a, (const float*)part, blocks);
+  float* pb = part + 2 * kParamsMaxBlocks;  // [nrb][H]
+  const int nrb = (int)std::max<int64_t>(1, std::min<int64_t>((d.rows + 3) / 4, kParamsMaxBlocks));
+  if (a.ddt_bias) {
+    hipLaunchKernelGGL(frac_params_bias_kernel, dim3(nrb, (d.H + 63) / 64), dim3(256), 0, stream, d, a, pb);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+  }
+  hipLaunchKernelGGL(frac_params_reduce_kernel, dim3((d.H + 2 + 3) / 4), dim3(256), 0, stream, d, a,
+                     (const float*)part, blocks, (const float*)pb, nrb);
   return hipGetLastError();
 }
 
