@@ -210,6 +210,38 @@ size_t frac_params_workspace_size(const frac_shape *shape);
 frac_status frac_params_bwd(const frac_shape *shape, const frac_params_bwd_args *args, void *ws, size_t ws_bytes,
                             void *stream);
 
+/* Causal depthwise 1-D convolution of the content branch (FracMixer, Sec. 3.3: a
+ * local depthwise causal convolution along the sequence; size 4 in the experiments),
+ * for every channel c of x [B,L,C] (shape.batch, shape.seqlen; io dtype shape.io_dtype):
+ *   pre[b,t,c] = bias[c] + sum_{j<K} w[c*K + j] * x[b, t-(K-1)+j, c]   (x = 0 before t = 0)
+ *   y = activation ? silu(pre) = pre * sigmoid(pre) : pre
+ *   x, y [B,L,C] io dtype (16-byte aligned); w [C,K] f32; bias [C] f32 or NULL.
+ *   channels C: a multiple of 8; width K: 1..4 (else FRAC_ERR_UNSUPPORTED). */
+typedef struct {
+  const void *x;
+  const float *w, *bias;
+  void *y;
+  int64_t channels;
+  int32_t width, activation;
+} frac_conv_args;
+
+/* Backward of frac_conv_fwd: fwd holds the forward's inputs (fwd.y ignored).
+ *   dy [B,L,C] io dtype; dx [B,L,C] io dtype, written;
+ *   dw [C,K] f32 and dbias [C] f32: written when non-NULL, summed over b and t in a
+ *   fixed order (identical bits on every call).
+ * ws: frac_conv_workspace_size() bytes of device scratch. */
+typedef struct {
+  frac_conv_args fwd;
+  const void *dy;
+  void *dx;
+  float *dw, *dbias;
+} frac_conv_bwd_args;
+
+frac_status frac_conv_fwd(const frac_shape *shape, const frac_conv_args *args, void *stream);
+size_t frac_conv_workspace_size(const frac_shape *shape, int64_t channels, int width);
+frac_status frac_conv_bwd(const frac_shape *shape, const frac_conv_bwd_args *args, void *ws, size_t ws_bytes,
+                          void *stream);
+
 /* Bytes of device workspace frac_scan_fwd (backward = 0) or frac_scan_bwd
  * (backward = 1) needs for `shape`; 0 means none.  Returns 0 for an invalid shape
  * (the scan call then reports the error). */

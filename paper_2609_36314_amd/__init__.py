@@ -285,3 +285,47 @@ def params_bwd(z_dt, z_alpha, *, dt_bias=None, z_lambda=None, v_read=None, v_wri
     _lib.check(_lib.load().frac_params_bwd(ctypes.byref(shape), ctypes.byref(a), _ptr(ws), ws.numel(), _stream()))
     del keep, grads
     return out
+
+
+def _conv_struct(x, w, bias, activation):
+    if x.dim() != 3 or not x.is_contiguous():
+        raise ValueError("x must be a contiguous [B, L, C] tensor")
+    C = x.shape[2]
+    if w.dim() != 2 or w.shape[0] != C:
+        raise ValueError("w must be [C, K]")
+    keep = [_f32(w, "w"), _f32(bias, "bias")]
+    a = _lib.FracConvArgs()
+    a.x, a.w, a.bias = _ptr(x), _ptr(keep[0]), _ptr(keep[1])
+    a.channels, a.width, a.activation = C, int(w.shape[1]), int(bool(activation))
+    B, L, _ = x.shape
+    shape = FracShape(B, L, 1, 1, 1, 1, 1, 0, _io_dtype(x))
+    return a, shape, keep
+
+
+def conv_fwd(x, w, *, bias=None, activation=True, y=None):
+    """Causal depthwise convolution of the content branch (frac_conv_fwd): x [B,L,C]
+    (bfloat16 or float32), w [C,K] and bias [C] float32; returns y like x."""
+    a, shape, keep = _conv_struct(x, w, bias, activation)
+    y = torch.empty_like(x) if y is None else y
+    a.y = _ptr(y)
+    _lib.check(_lib.load().frac_conv_fwd(ctypes.byref(shape), ctypes.byref(a), _stream()))
+    del keep
+    return y
+
+
+def conv_bwd(x, w, dy, *, bias=None, activation=True):
+    """Backward of conv_fwd (frac_conv_bwd): returns dict(dx, dw, dbias) (dbias None
+    without a bias)."""
+    a, shape, keep = _conv_struct(x, w, bias, activation)
+    if dy.shape != x.shape or dy.dtype != x.dtype or not dy.is_contiguous():
+        raise ValueError("dy must be contiguous, with the shape and dtype of x")
+    out = dict(dx=torch.empty_like(x), dw=torch.empty_like(w),
+               dbias=None if bias is None else torch.empty_like(bias))
+    b = _lib.FracConvBwdArgs()
+    b.fwd = a
+    b.dy, b.dx, b.dw, b.dbias = _ptr(dy), _ptr(out["dx"]), _ptr(out["dw"]), _ptr(out["dbias"])
+    nbytes = _lib.load().frac_conv_workspace_size(ctypes.byref(shape), a.channels, a.width)
+    ws = torch.empty(max(1, nbytes), dtype=torch.uint8, device=x.device)
+    _lib.check(_lib.load().frac_conv_bwd(ctypes.byref(shape), ctypes.byref(b), _ptr(ws), nbytes, _stream()))
+    del keep
+    return out

@@ -172,6 +172,29 @@ frac_status params_inputs(const frac_params_args* a, bool need_outputs) {
 
 }  // namespace
 
+// ------------------------------------------------------------- convolution
+
+namespace {
+
+frac_status conv_dims(const frac_shape* sh, int64_t channels, int width, frac::ConvDims& d) {
+  if (!sh) return fail(FRAC_ERR_INVALID_ARG, "shape is NULL");
+  if (sh->batch < 0 || sh->seqlen < 0) return fail(FRAC_ERR_INVALID_ARG, "batch and seqlen must be >= 0");
+  if (sh->seqlen > (1ll << 30)) return fail(FRAC_ERR_UNSUPPORTED, "seqlen too large");
+  if (sh->io_dtype != FRAC_F32 && sh->io_dtype != FRAC_BF16)
+    return fail(FRAC_ERR_INVALID_ARG, "io_dtype %d is not a frac_dtype", (int)sh->io_dtype);
+  if (channels < 8 || channels % 8 || channels > (1ll << 24))
+    return fail(FRAC_ERR_UNSUPPORTED, "channels %lld: must be a positive multiple of 8", (long long)channels);
+  if (width < 1 || width > 4) return fail(FRAC_ERR_UNSUPPORTED, "width %d: 1..4 is built", width);
+  d.rows = sh->batch * sh->seqlen;
+  d.L = (int)sh->seqlen;
+  d.C = (int)channels;
+  d.K = width;
+  d.bf16_io = sh->io_dtype == FRAC_BF16;
+  return ok();
+}
+
+}  // namespace
+
 extern "C" {
 
 const char* frac_status_string(frac_status s) {
@@ -355,6 +378,45 @@ frac_status frac_params_bwd(const frac_shape* shape, const frac_params_bwd_args*
     return fail(FRAC_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", need, ws ? ws_bytes : (size_t)0);
   return hip_status(frac::launch_params_bwd(d, *a, reinterpret_cast<float*>(ws), reinterpret_cast<hipStream_t>(stream)),
                     "frac_params_bwd launch");
+}
+
+frac_status frac_conv_fwd(const frac_shape* shape, const frac_conv_args* a, void* stream) {
+  if (!a) return fail(FRAC_ERR_INVALID_ARG, "args is NULL");
+  frac::ConvDims d{};
+  frac_status s = conv_dims(shape, a->channels, a->width, d);
+  if (s != FRAC_OK) return s;
+  if (d.rows == 0) return ok();
+  if (!a->x || !a->w || !a->y) return fail(FRAC_ERR_INVALID_ARG, "x, w and y are required");
+  if (!aligned16(a->x) || !aligned16(a->y)) return fail(FRAC_ERR_INVALID_ARG, "x and y must be 16-byte aligned");
+  return hip_status(frac::launch_conv_fwd(d, *a, reinterpret_cast<hipStream_t>(stream)), "frac_conv_fwd launch");
+}
+
+size_t frac_conv_workspace_size(const frac_shape* shape, int64_t channels, int width) {
+  frac::ConvDims d{};
+  if (conv_dims(shape, channels, width, d) != FRAC_OK) return 0;
+  return frac::conv_workspace(d.C, d.K);
+}
+
+frac_status frac_conv_bwd(const frac_shape* shape, const frac_conv_bwd_args* a, void* ws, size_t ws_bytes,
+                          void* stream) {
+  if (!a) return fail(FRAC_ERR_INVALID_ARG, "args is NULL");
+  frac::ConvDims d{};
+  frac_status s = conv_dims(shape, a->fwd.channels, a->fwd.width, d);
+  if (s != FRAC_OK) return s;
+  if (d.rows == 0) {  // no tokens: the sums are zero
+    const hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+    if (a->dw) hipLaunchKernelGGL(copy_or_zero_kernel, dim3(16), dim3(256), 0, st, a->dw, nullptr, (int64_t)d.C * d.K);
+    if (a->dbias) hipLaunchKernelGGL(copy_or_zero_kernel, dim3(16), dim3(256), 0, st, a->dbias, nullptr, (int64_t)d.C);
+    return hip_status(hipGetLastError(), "frac_conv_bwd (empty)");
+  }
+  if (!a->fwd.x || !a->fwd.w || !a->dy || !a->dx) return fail(FRAC_ERR_INVALID_ARG, "x, w, dy and dx are required");
+  if (!aligned16(a->fwd.x) || !aligned16(a->dy) || !aligned16(a->dx))
+    return fail(FRAC_ERR_INVALID_ARG, "x, dy and dx must be 16-byte aligned");
+  const size_t need = frac::conv_workspace(d.C, d.K);
+  if ((a->dw || a->dbias) && (!ws || ws_bytes < need))
+    return fail(FRAC_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", need, ws ? ws_bytes : (size_t)0);
+  return hip_status(frac::launch_conv_bwd(d, *a, reinterpret_cast<float*>(ws), reinterpret_cast<hipStream_t>(stream)),
+                    "frac_conv_bwd launch");
 }
 
 }  // extern "C"

@@ -73,6 +73,17 @@ constexpr int kParamsMaxBlocks = 1024;  // partial sums of the backward: 2 float
 size_t params_workspace(int64_t H);
 hipError_t launch_params_bwd(const ParamsDims& d, const frac_params_bwd_args& a, float* part, hipStream_t stream);
 
+// Causal depthwise convolution of the content branch (frac_conv.hip).
+struct ConvDims {
+  int64_t rows;  // B * L
+  int L, C, K;
+  bool bf16_io;
+};
+constexpr int kConvMaxRowBlocks = 256;
+size_t conv_workspace(int64_t C, int K);
+hipError_t launch_conv_fwd(const ConvDims& d, const frac_conv_args& a, hipStream_t stream);
+hipError_t launch_conv_bwd(const ConvDims& d, const frac_conv_bwd_args& a, float* ws, hipStream_t stream);
+
 hipError_t launch_decode_step(const ScanParams& p, float* state, hipStream_t stream);
 
 // The layer without B/C projections (dstate 1, B = C = 1): forward scan (no

@@ -190,3 +190,28 @@ def test_parameter_construction_arguments_are_checked_on_the_host():
     b = FracParamsBwdArgs()
     b.fwd = a
     assert lib.frac_params_bwd(ctypes.byref(sh), ctypes.byref(b), None, 0, None) == -3  # no workspace
+
+
+def test_convolution_arguments_are_checked_on_the_host():
+    from paper_2609_36314_amd._lib import FracConvArgs, FracConvBwdArgs
+    lib = _lib.load()
+    sh = _shape()
+    buf = (ctypes.c_float * 64)()
+    p = ctypes.cast(buf, ctypes.c_void_p)
+    a = FracConvArgs()
+    a.channels, a.width, a.activation = 64, 4, 1
+    assert lib.frac_conv_fwd(ctypes.byref(sh), ctypes.byref(a), None) == -1  # no pointers
+    a.x = a.w = a.y = p
+    for ch, wd, st in ((60, 4, -2), (64, 5, -2), (64, 0, -2), (0, 4, -2)):
+        a.channels, a.width = ch, wd
+        assert lib.frac_conv_fwd(ctypes.byref(sh), ctypes.byref(a), None) == st, (ch, wd)
+    a.channels, a.width = 64, 4
+    a.x = ctypes.c_void_p(ctypes.addressof(buf) + 4)
+    assert lib.frac_conv_fwd(ctypes.byref(sh), ctypes.byref(a), None) == -1  # misaligned
+    a.x = p
+    assert lib.frac_conv_workspace_size(ctypes.byref(sh), 64, 4) > 0
+    assert lib.frac_conv_workspace_size(ctypes.byref(sh), 64, 9) == 0
+    b = FracConvBwdArgs()
+    b.fwd = a
+    b.dy = b.dx = b.dw = p
+    assert lib.frac_conv_bwd(ctypes.byref(sh), ctypes.byref(b), None, 0, None) == -3  # no workspace
