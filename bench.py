@@ -115,6 +115,30 @@ def bench_params(torch, frac, w, steps, warmup):
             "params_bwd_ms": bms, "params_bwd_roofline": roofline("hbm", bb, bms, PEAK_HBM_BYTES, "GB/s")}
 
 
+def bench_conv(torch, frac, w, steps, warmup, K=4):
+    """frac_conv_fwd / frac_conv_bwd over the content branch of the workload (C = H P
+    channels, width 4, bias, SiLU) in the io dtype."""
+    g = torch.Generator().manual_seed(0)
+    B, L, C = w.batch, w.seqlen, w.nheads * w.headdim
+    io = torch.bfloat16 if w.io_dtype == "bf16" else torch.float32
+    x = torch.randn(B, L, C, generator=g).to(io).cuda()
+    dy = torch.randn(B, L, C, generator=g).to(io).cuda()
+    wt, b = (torch.randn(C, K, generator=g) / K).cuda(), torch.randn(C, generator=g).cuda()
+    for _ in range(warmup):
+        frac.conv_fwd(x, wt, bias=b)
+        frac.conv_bwd(x, wt, dy, bias=b)
+    tf, tb = Timer(torch), Timer(torch)
+    for _ in range(steps):
+        with tf:
+            frac.conv_fwd(x, wt, bias=b)
+        with tb:
+            frac.conv_bwd(x, wt, dy, bias=b)
+    fms, bms = float(np.mean(tf.ms())), float(np.mean(tb.ms()))
+    n = B * L * C * x.element_size()
+    return {"conv_fwd_ms": fms, "conv_fwd_roofline": roofline("hbm", 2 * n, fms, PEAK_HBM_BYTES, "GB/s"),
+            "conv_bwd_ms": bms, "conv_bwd_roofline": roofline("hbm", 3 * n, bms, PEAK_HBM_BYTES, "GB/s")}
+
+
 def decode_bytes_per_step(w):
     B, H, P, N, M, G = w.batch, w.nheads, w.headdim, w.dstate, w.nmodes, w.ngroups
     io = 2 if w.io_dtype == "bf16" else 4
@@ -220,6 +244,7 @@ def bench_scan(torch, frac, w, steps, warmup):
                 bwd_all()
         res["bwd_all_grads_ms"] = float(np.mean(ta.ms()))
         res.update(bench_params(torch, frac, w, steps, warmup))
+        res.update(bench_conv(torch, frac, w, steps, warmup))
         res["bwd_ms"] = bms
         res["bwd_roofline"] = dict(roofline("hbm", nfree_bwd_bytes(w), bms, PEAK_HBM_BYTES, "GB/s"),
                                    traffic=measured_traffic("frac_scan_bwd", w.name))

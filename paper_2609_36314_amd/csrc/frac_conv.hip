@@ -1,10 +1,10 @@
 // frac_conv.hip -- causal depthwise 1-D convolution of the content branch
 // (FracMixer, Sec. 3.3), forward and backward.  Bound by HBM: each thread owns 8
-// consecutive channels (one 16-byte bfloat16 vector) of one token and reads the
-// K - 1 earlier tokens of the same channels from cache.  The backward recomputes
-// the pre-activation in a (2K - 1)-token window, writes dx, and sums the weight and
-// bias gradients as fixed-order partials per row block, reduced by one wave per
-// output: repeated calls give identical bits.
+// consecutive channels (one 16-byte bfloat16 vector) of a run of 16 tokens, with its
+// weights in registers and the inputs in a sliding register window (one load per
+// token).  The backward recomputes the pre-activation in the window, writes dx, and
+// sums the weight and bias gradients as fixed-order partials per row block, reduced
+// by one wave per output: repeated calls give identical bits.
 #include <algorithm>
 
 #include "frac_device.h"
@@ -24,41 +24,69 @@ __device__ __forceinline__ void store8(float* p, const float* v) {
 }
 __device__ __forceinline__ float sigm(float x) { return 1.0f / (1.0f + __expf(-x)); }
 
+constexpr int kConvTR = 16;  // consecutive tokens per thread
+
+// Thread item = (b, segment of kConvTR tokens, 8-channel group), channel groups
+// fastest (coalesced); the weights are loaded once and x slides through a K-token
+// register window, one 16-byte load per token.
 template <typename T, int K>
 __global__ void __launch_bounds__(256) frac_conv_fwd_kernel(ConvDims d, frac_conv_args a) {
-  const int G = d.C / 8;
-  const int64_t n = d.rows * G;
-  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (int64_t)gridDim.x * 256) {
-    const int64_t row = i / G;
-    const int c0 = (int)(i - row * G) * 8, t = (int)(row % d.L);
-    const T* x = reinterpret_cast<const T*>(a.x) + row * d.C + c0;
-    float acc[8];
+  const int G = d.C / 8, nseg = (d.L + kConvTR - 1) / kConvTR;
+  const int64_t items = d.rows / d.L * nseg * G;
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < items; i += (int64_t)gridDim.x * 256) {
+    const int64_t bs = i / G;
+    const int c0 = (int)(i - bs * G) * 8, b = (int)(bs / nseg), t0 = (int)(bs % nseg) * kConvTR;
+    const int t1 = min(t0 + kConvTR, d.L);
+    float w[8][K], bias[8];
 #pragma unroll
-    for (int q = 0; q < 8; ++q) acc[q] = a.bias ? a.bias[c0 + q] : 0.0f;
+    for (int q = 0; q < 8; ++q) {
+      bias[q] = a.bias ? a.bias[c0 + q] : 0.0f;
 #pragma unroll
-    for (int j = 0; j < K; ++j) {
-      const int back = K - 1 - j;  // tap j reads the token `back` steps earlier
-      if (t < back) continue;
-      float v[8];
-      load8(x - (int64_t)back * d.C, v);
-#pragma unroll
-      for (int q = 0; q < 8; ++q) acc[q] += a.w[(c0 + q) * K + j] * v[q];
+      for (int j = 0; j < K; ++j) w[q][j] = a.w[(c0 + q) * K + j];
     }
-    if (a.activation) {
+    const int64_t base = (int64_t)b * d.L * d.C + c0;
+    const T* x = reinterpret_cast<const T*>(a.x) + base;
+    T* y = reinterpret_cast<T*>(a.y) + base;
+    float xv[K][8];  // x at tokens t - (K - 1) .. t
 #pragma unroll
-      for (int q = 0; q < 8; ++q) acc[q] *= sigm(acc[q]);
+    for (int u = 0; u < K - 1; ++u) {
+      const int tt = t0 - (K - 1) + u;
+      if (tt >= 0) {
+        load8(x + (int64_t)tt * d.C, xv[u]);
+      } else {
+#pragma unroll
+        for (int q = 0; q < 8; ++q) xv[u][q] = 0.0f;
+      }
     }
-    store8(reinterpret_cast<T*>(a.y) + row * d.C + c0, acc);
+    for (int t = t0; t < t1; ++t) {
+      load8(x + (int64_t)t * d.C, xv[K - 1]);
+      float acc[8];
+#pragma unroll
+      for (int q = 0; q < 8; ++q) {
+        float v = bias[q];
+#pragma unroll
+        for (int j = 0; j < K; ++j) v += w[q][j] * xv[j][q];
+        acc[q] = a.activation ? v * sigm(v) : v;
+      }
+      store8(y + (int64_t)t * d.C, acc);
+#pragma unroll
+      for (int u = 0; u < K - 1; ++u)
+#pragma unroll
+        for (int q = 0; q < 8; ++q) xv[u][q] = xv[u + 1][q];
+    }
   }
 }
 
 // Workgroup (x, y): channel groups 32 y .. 32 y + 31 (8 channels each) x 8 row lanes;
-// row lane rl takes rows 8 x + rl, then every 8 gridDim.x rows.  Writes dx, and the
-// workgroup's fixed-order sums of g x (weights) and g (bias) into pw [x][C][K], pb [x][C].
+// row lane rl takes token segments (b, kConvTR tokens) 8 x + rl, then every 8 gridDim.x
+// segments, each in token order with x (2K - 1 tokens) and g (K tokens) in sliding
+// register windows.  Writes dx, and the workgroup's fixed-order sums of g x (weights)
+// and g (bias) into pw [x][C][K], pb [x][C].
 template <typename T, int K>
 __global__ void __launch_bounds__(256) frac_conv_bwd_kernel(ConvDims d, frac_conv_bwd_args a, float* pw, float* pb) {
   const frac_conv_args& f = a.fwd;
-  const int G = d.C / 8;
+  const int G = d.C / 8, nseg = (d.L + kConvTR - 1) / kConvTR;
+  const int64_t segs = d.rows / d.L * nseg;
   const int cgl = threadIdx.x & 31, rl = threadIdx.x >> 5;
   const int cg = blockIdx.y * 32 + cgl, c0 = cg * 8;
   const bool active = cg < G;
@@ -74,62 +102,71 @@ __global__ void __launch_bounds__(256) frac_conv_bwd_kernel(ConvDims d, frac_con
 #pragma unroll
       for (int j = 0; j < K; ++j) w[q][j] = f.w[(c0 + q) * K + j];
     }
-    for (int64_t r = (int64_t)blockIdx.x * 8 + rl; r < d.rows; r += 8 * (int64_t)gridDim.x) {
-      const int t = (int)(r % d.L);
-      const T* x = reinterpret_cast<const T*>(f.x) + r * d.C + c0;
-      const T* dy = reinterpret_cast<const T*>(a.dy) + r * d.C + c0;
-      // x at tokens t - (K - 1) .. t + K - 1 of this sequence (zero outside it)
-      float xw[2 * K - 1][8];
+    // x at token p (zero outside the sequence); g = dL/dpre at token p (zero past the end)
+    auto ldx = [&](const T* x, int p, float* o) {
+      if (p >= 0 && p < d.L) {
+        load8(x + (int64_t)p * d.C, o);
+      } else {
 #pragma unroll
-      for (int u = 0; u < 2 * K - 1; ++u) {
-        const int off = u - (K - 1), tt = t + off;
-        if (tt >= 0 && tt < d.L) {
-          load8(x + (int64_t)off * d.C, xw[u]);
-        } else {
-#pragma unroll
-          for (int q = 0; q < 8; ++q) xw[u][q] = 0.0f;
-        }
+        for (int q = 0; q < 8; ++q) o[q] = 0.0f;
       }
-      // g = dL/dpre at tokens t .. t + K - 1
-      float g[K][8];
+    };
+    for (int64_t sg = (int64_t)blockIdx.x * 8 + rl; sg < segs; sg += 8 * (int64_t)gridDim.x) {
+      const int b = (int)(sg / nseg), t0 = (int)(sg % nseg) * kConvTR, t1 = min(t0 + kConvTR, d.L);
+      const int64_t base = (int64_t)b * d.L * d.C + c0;
+      const T* x = reinterpret_cast<const T*>(f.x) + base;
+      const T* dy = reinterpret_cast<const T*>(a.dy) + base;
+      T* dx = reinterpret_cast<T*>(a.dx) + base;
+      float xw[2 * K - 1][8];  // x at tokens t - (K - 1) .. t + K - 1
+      float g[K][8];           // g at tokens t .. t + K - 1
+      auto gat = [&](int p, const float (*xs)[8], float* o) {  // xs: x at p - (K - 1) .. p
+        if (p >= d.L) {
 #pragma unroll
-      for (int s = 0; s < K; ++s) {
-        if (t + s >= d.L) {
-#pragma unroll
-          for (int q = 0; q < 8; ++q) g[s][q] = 0.0f;
-          continue;
+          for (int q = 0; q < 8; ++q) o[q] = 0.0f;
+          return;
         }
         float gy[8];
-        load8(dy + (int64_t)s * d.C, gy);
+        load8(dy + (int64_t)p * d.C, gy);
 #pragma unroll
         for (int q = 0; q < 8; ++q) {
           if (f.activation) {
             float pre = bias[q];
 #pragma unroll
-            for (int j = 0; j < K; ++j) pre += w[q][j] * xw[s + j][q];
-            const float sg = sigm(pre);
-            g[s][q] = gy[q] * (sg + pre * sg * (1.0f - sg));
+            for (int j = 0; j < K; ++j) pre += w[q][j] * xs[j][q];
+            const float sgm = sigm(pre);
+            o[q] = gy[q] * (sgm + pre * sgm * (1.0f - sgm));
           } else {
-            g[s][q] = gy[q];
+            o[q] = gy[q];
           }
         }
-      }
-      // dx[t] = sum_j w_j g[t + K - 1 - j]
-      float dxv[8];
+      };
 #pragma unroll
-      for (int q = 0; q < 8; ++q) {
-        float v = 0.0f;
+      for (int u = 0; u < 2 * K - 2; ++u) ldx(x, t0 - (K - 1) + u, xw[u]);
 #pragma unroll
-        for (int j = 0; j < K; ++j) v += w[q][j] * g[K - 1 - j][q];
-        dxv[q] = v;
-      }
-      store8(reinterpret_cast<T*>(a.dx) + r * d.C + c0, dxv);
-      // dw[q][j] += g[t] x[t - (K - 1) + j], dbias[q] += g[t]
+      for (int s = 0; s < K - 1; ++s) gat(t0 + s, xw + s, g[s]);
+      for (int t = t0; t < t1; ++t) {
+        ldx(x, t + K - 1, xw[2 * K - 2]);
+        gat(t + K - 1, xw + (K - 1), g[K - 1]);
+        float dxv[8];
 #pragma unroll
-      for (int q = 0; q < 8; ++q) {
+        for (int q = 0; q < 8; ++q) {
+          float v = 0.0f;
 #pragma unroll
-        for (int j = 0; j < K; ++j) acc[q * K + j] += g[0][q] * xw[j][q];
-        acc[8 * K + q] += g[0][q];
+          for (int j = 0; j < K; ++j) v += w[q][j] * g[K - 1 - j][q];
+          dxv[q] = v;
+#pragma unroll
+          for (int j = 0; j < K; ++j) acc[q * K + j] += g[0][q] * xw[j][q];
+          acc[8 * K + q] += g[0][q];
+        }
+        store8(dx + (int64_t)t * d.C, dxv);
+#pragma unroll
+        for (int u = 0; u < 2 * K - 2; ++u)
+#pragma unroll
+          for (int q = 0; q < 8; ++q) xw[u][q] = xw[u + 1][q];
+#pragma unroll
+        for (int s = 0; s < K - 1; ++s)
+#pragma unroll
+          for (int q = 0; q < 8; ++q) g[s][q] = g[s + 1][q];
       }
     }
   }
@@ -141,15 +178,15 @@ __global__ void __launch_bounds__(256) frac_conv_bwd_kernel(ConvDims d, frac_con
   for (int i = threadIdx.x; i < 32 * NA; i += 256) {
     const int cl = i / NA, k = i - cl * NA, cgo = blockIdx.y * 32 + cl;
     if (cgo >= G) continue;
-    float s = 0.0f;
+    float sum = 0.0f;
 #pragma unroll
-    for (int l = 0; l < 8; ++l) s += red[l][cl][k];
+    for (int l = 0; l < 8; ++l) sum += red[l][cl][k];
     const int64_t base = (int64_t)blockIdx.x * d.C;
     if (k < 8 * K) {
       const int q = k / K, j = k - q * K;
-      pw[(base + cgo * 8 + q) * K + j] = s;
+      pw[(base + cgo * 8 + q) * K + j] = sum;
     } else {
-      pb[base + cgo * 8 + (k - 8 * K)] = s;
+      pb[base + cgo * 8 + (k - 8 * K)] = sum;
     }
   }
 }
@@ -177,7 +214,7 @@ __global__ void __launch_bounds__(256) frac_conv_reduce_kernel(ConvDims d, frac_
 
 template <typename T, int K>
 hipError_t conv_fwd_t(const ConvDims& d, const frac_conv_args& a, hipStream_t stream) {
-  const int64_t n = d.rows * (d.C / 8);
+  const int64_t n = d.rows / d.L * ((d.L + kConvTR - 1) / kConvTR) * (d.C / 8);
   const unsigned blocks = (unsigned)std::max<int64_t>(1, std::min<int64_t>((n + 255) / 256, 8192));
   hipLaunchKernelGGL((frac_conv_fwd_kernel<T, K>), dim3(blocks), dim3(256), 0, stream, d, a);
   return hipGetLastError();
@@ -185,7 +222,8 @@ hipError_t conv_fwd_t(const ConvDims& d, const frac_conv_args& a, hipStream_t st
 
 template <typename T, int K>
 hipError_t conv_bwd_t(const ConvDims& d, const frac_conv_bwd_args& a, float* ws, hipStream_t stream) {
-  const int nrb = (int)std::max<int64_t>(1, std::min<int64_t>((d.rows + 7) / 8, kConvMaxRowBlocks));
+  const int64_t segs = d.rows / d.L * ((d.L + kConvTR - 1) / kConvTR);
+  const int nrb = (int)std::max<int64_t>(1, std::min<int64_t>((segs + 7) / 8, kConvMaxRowBlocks));
   const bool sums = a.dw || a.dbias;
   float* pw = sums ? ws : nullptr;
   float* pb = sums ? ws + (size_t)kConvMaxRowBlocks * d.C * d.K : nullptr;
