@@ -242,6 +242,37 @@ size_t frac_conv_workspace_size(const frac_shape *shape, int64_t channels, int w
 frac_status frac_conv_bwd(const frac_shape *shape, const frac_conv_bwd_args *args, void *ws, size_t ws_bytes,
                           void *stream);
 
+/* Gated normalization of the layer output (Sec. 3.3 names it; the form is the gated
+ * RMS normalization of the Mamba-2 block, gate before the normalization), per token
+ * over groups of `group` consecutive channels of x, z [B,L,C] (io dtype shape.io_dtype):
+ *   u = x * silu(z),   y = u / sqrt(mean_group(u^2) + eps) * weight
+ *   weight [C] f32; y [B,L,C] io dtype.  x, z, y 16-byte aligned.
+ *   channels C: a multiple of 8, at most 4096; group: a multiple of 8 dividing C with
+ *   group / 8 a power of two (else FRAC_ERR_UNSUPPORTED). */
+typedef struct {
+  const void *x, *z;
+  const float *weight;
+  void *y;
+  int64_t channels, group;
+  float eps;
+} frac_gnorm_args;
+
+/* Backward of frac_gnorm_fwd: fwd holds the forward's inputs (fwd.y ignored).
+ *   dy [B,L,C] io dtype; dx, dz [B,L,C] io dtype, written;
+ *   dweight [C] f32, written when non-NULL (fixed-order sum over b and t).
+ * ws: frac_gnorm_workspace_size() bytes of device scratch. */
+typedef struct {
+  frac_gnorm_args fwd;
+  const void *dy;
+  void *dx, *dz;
+  float *dweight;
+} frac_gnorm_bwd_args;
+
+frac_status frac_gnorm_fwd(const frac_shape *shape, const frac_gnorm_args *args, void *stream);
+size_t frac_gnorm_workspace_size(const frac_shape *shape, int64_t channels);
+frac_status frac_gnorm_bwd(const frac_shape *shape, const frac_gnorm_bwd_args *args, void *ws, size_t ws_bytes,
+                           void *stream);
+
 /* Bytes of device workspace frac_scan_fwd (backward = 0) or frac_scan_bwd
  * (backward = 1) needs for `shape`; 0 means none.  Returns 0 for an invalid shape
  * (the scan call then reports the error). */

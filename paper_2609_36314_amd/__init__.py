@@ -329,3 +329,43 @@ def conv_bwd(x, w, dy, *, bias=None, activation=True):
     _lib.check(_lib.load().frac_conv_bwd(ctypes.byref(shape), ctypes.byref(b), _ptr(ws), nbytes, _stream()))
     del keep
     return out
+
+
+def _gnorm_struct(x, z, weight, group, eps):
+    if x.dim() != 3 or not x.is_contiguous() or z.shape != x.shape or z.dtype != x.dtype or not z.is_contiguous():
+        raise ValueError("x and z must be contiguous [B, L, C] tensors of one dtype")
+    C = x.shape[2]
+    keep = [_f32(weight, "weight")]
+    a = _lib.FracGnormArgs()
+    a.x, a.z, a.weight = _ptr(x), _ptr(z), _ptr(keep[0])
+    a.channels, a.group, a.eps = C, C if group is None else int(group), float(eps)
+    B, L, _ = x.shape
+    return a, FracShape(B, L, 1, 1, 1, 1, 1, 0, _io_dtype(x)), keep
+
+
+def gnorm_fwd(x, z, weight, *, group=None, eps=1e-5, y=None):
+    """Gated RMS normalization of the layer output (frac_gnorm_fwd): x, z [B,L,C]
+    (bfloat16 or float32), weight [C] float32, over groups of `group` channels (all C
+    by default).  Returns y like x."""
+    a, shape, keep = _gnorm_struct(x, z, weight, group, eps)
+    y = torch.empty_like(x) if y is None else y
+    a.y = _ptr(y)
+    _lib.check(_lib.load().frac_gnorm_fwd(ctypes.byref(shape), ctypes.byref(a), _stream()))
+    del keep
+    return y
+
+
+def gnorm_bwd(x, z, weight, dy, *, group=None, eps=1e-5):
+    """Backward of gnorm_fwd (frac_gnorm_bwd): returns dict(dx, dz, dweight)."""
+    a, shape, keep = _gnorm_struct(x, z, weight, group, eps)
+    if dy.shape != x.shape or dy.dtype != x.dtype or not dy.is_contiguous():
+        raise ValueError("dy must be contiguous, with the shape and dtype of x")
+    out = dict(dx=torch.empty_like(x), dz=torch.empty_like(x), dweight=torch.empty_like(weight))
+    b = _lib.FracGnormBwdArgs()
+    b.fwd = a
+    b.dy, b.dx, b.dz, b.dweight = _ptr(dy), _ptr(out["dx"]), _ptr(out["dz"]), _ptr(out["dweight"])
+    nbytes = _lib.load().frac_gnorm_workspace_size(ctypes.byref(shape), a.channels)
+    ws = torch.empty(max(1, nbytes), dtype=torch.uint8, device=x.device)
+    _lib.check(_lib.load().frac_gnorm_bwd(ctypes.byref(shape), ctypes.byref(b), _ptr(ws), nbytes, _stream()))
+    del keep
+    return out

@@ -22,7 +22,8 @@ STATUS = {0: "FRAC_OK", -1: "FRAC_ERR_INVALID_ARG", -2: "FRAC_ERR_UNSUPPORTED", 
 # every symbol include/frac.h declares
 EXPORTS = ("frac_scan_workspace_size", "frac_scan_fwd", "frac_scan_bwd", "frac_decode_step", "frac_default_tau",
            "frac_status_string", "frac_last_error", "frac_params_fwd", "frac_params_workspace_size",
-           "frac_params_bwd", "frac_conv_fwd", "frac_conv_workspace_size", "frac_conv_bwd")
+           "frac_params_bwd", "frac_conv_fwd", "frac_conv_workspace_size", "frac_conv_bwd",
+           "frac_gnorm_fwd", "frac_gnorm_workspace_size", "frac_gnorm_bwd")
 
 
 class FracShape(ctypes.Structure):
@@ -78,6 +79,16 @@ class FracConvBwdArgs(ctypes.Structure):
     _fields_ = [("fwd", FracConvArgs), ("dy", c_void_p), ("dx", c_void_p), ("dw", c_void_p), ("dbias", c_void_p)]
 
 
+class FracGnormArgs(ctypes.Structure):
+    _fields_ = [("x", c_void_p), ("z", c_void_p), ("weight", c_void_p), ("y", c_void_p), ("channels", c_int64),
+                ("group", c_int64), ("eps", ctypes.c_float)]
+
+
+class FracGnormBwdArgs(ctypes.Structure):
+    _fields_ = [("fwd", FracGnormArgs), ("dy", c_void_p), ("dx", c_void_p), ("dz", c_void_p),
+                ("dweight", c_void_p)]
+
+
 class FracError(RuntimeError):
     def __init__(self, status: int, message: str):
         super().__init__("%s: %s" % (STATUS.get(status, str(status)), message))
@@ -121,6 +132,12 @@ def load():
     lib.frac_conv_workspace_size.restype = c_size_t
     lib.frac_conv_bwd.argtypes = [POINTER(FracShape), POINTER(FracConvBwdArgs), c_void_p, c_size_t, c_void_p]
     lib.frac_conv_bwd.restype = c_int
+    lib.frac_gnorm_fwd.argtypes = [POINTER(FracShape), POINTER(FracGnormArgs), c_void_p]
+    lib.frac_gnorm_fwd.restype = c_int
+    lib.frac_gnorm_workspace_size.argtypes = [POINTER(FracShape), c_int64]
+    lib.frac_gnorm_workspace_size.restype = c_size_t
+    lib.frac_gnorm_bwd.argtypes = [POINTER(FracShape), POINTER(FracGnormBwdArgs), c_void_p, c_size_t, c_void_p]
+    lib.frac_gnorm_bwd.restype = c_int
     _lib = lib
     return lib
 

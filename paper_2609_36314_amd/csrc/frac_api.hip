@@ -193,6 +193,24 @@ frac_status conv_dims(const frac_shape* sh, int64_t channels, int width, frac::C
   return ok();
 }
 
+frac_status gnorm_dims(const frac_shape* sh, int64_t channels, int64_t group, frac::GnormDims& d) {
+  if (!sh) return fail(FRAC_ERR_INVALID_ARG, "shape is NULL");
+  if (sh->batch < 0 || sh->seqlen < 0) return fail(FRAC_ERR_INVALID_ARG, "batch and seqlen must be >= 0");
+  if (sh->io_dtype != FRAC_F32 && sh->io_dtype != FRAC_BF16)
+    return fail(FRAC_ERR_INVALID_ARG, "io_dtype %d is not a frac_dtype", (int)sh->io_dtype);
+  if (channels < 8 || channels % 8 || channels > 4096)
+    return fail(FRAC_ERR_UNSUPPORTED, "channels %lld: a multiple of 8 up to 4096 is built", (long long)channels);
+  const int64_t nvg = group / 8;
+  if (group < 8 || group % 8 || channels % group || (nvg & (nvg - 1)))
+    return fail(FRAC_ERR_UNSUPPORTED, "group %lld: a multiple of 8 dividing channels, group / 8 a power of two",
+                (long long)group);
+  d.rows = sh->batch * sh->seqlen;
+  d.C = (int)channels;
+  d.group = (int)group;
+  d.bf16_io = sh->io_dtype == FRAC_BF16;
+  return ok();
+}
+
 }  // namespace
 
 extern "C" {
@@ -417,6 +435,50 @@ frac_status frac_conv_bwd(const frac_shape* shape, const frac_conv_bwd_args* a, 
     return fail(FRAC_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", need, ws ? ws_bytes : (size_t)0);
   return hip_status(frac::launch_conv_bwd(d, *a, reinterpret_cast<float*>(ws), reinterpret_cast<hipStream_t>(stream)),
                     "frac_conv_bwd launch");
+}
+
+frac_status frac_gnorm_fwd(const frac_shape* shape, const frac_gnorm_args* a, void* stream) {
+  if (!a) return fail(FRAC_ERR_INVALID_ARG, "args is NULL");
+  frac::GnormDims d{};
+  frac_status s = gnorm_dims(shape, a->channels, a->group, d);
+  if (s != FRAC_OK) return s;
+  if (!(a->eps >= 0.0f)) return fail(FRAC_ERR_INVALID_ARG, "eps must be >= 0");
+  if (d.rows == 0) return ok();
+  if (!a->x || !a->z || !a->weight || !a->y) return fail(FRAC_ERR_INVALID_ARG, "x, z, weight and y are required");
+  if (!aligned16(a->x) || !aligned16(a->z) || !aligned16(a->y))
+    return fail(FRAC_ERR_INVALID_ARG, "x, z and y must be 16-byte aligned");
+  return hip_status(frac::launch_gnorm_fwd(d, *a, reinterpret_cast<hipStream_t>(stream)), "frac_gnorm_fwd launch");
+}
+
+size_t frac_gnorm_workspace_size(const frac_shape* shape, int64_t channels) {
+  if (!shape || channels < 8 || channels % 8 || channels > 4096) return 0;
+  return frac::gnorm_workspace(channels);
+}
+
+frac_status frac_gnorm_bwd(const frac_shape* shape, const frac_gnorm_bwd_args* a, void* ws, size_t ws_bytes,
+                           void* stream) {
+  if (!a) return fail(FRAC_ERR_INVALID_ARG, "args is NULL");
+  frac::GnormDims d{};
+  frac_status s = gnorm_dims(shape, a->fwd.channels, a->fwd.group, d);
+  if (s != FRAC_OK) return s;
+  if (!(a->fwd.eps >= 0.0f)) return fail(FRAC_ERR_INVALID_ARG, "eps must be >= 0");
+  if (d.rows == 0) {
+    if (a->dweight) {
+      hipLaunchKernelGGL(copy_or_zero_kernel, dim3(16), dim3(256), 0, reinterpret_cast<hipStream_t>(stream),
+                         a->dweight, nullptr, (int64_t)d.C);
+      return hip_status(hipGetLastError(), "frac_gnorm_bwd (empty)");
+    }
+    return ok();
+  }
+  if (!a->fwd.x || !a->fwd.z || !a->fwd.weight || !a->dy || !a->dx || !a->dz)
+    return fail(FRAC_ERR_INVALID_ARG, "x, z, weight, dy, dx and dz are required");
+  if (!aligned16(a->fwd.x) || !aligned16(a->fwd.z) || !aligned16(a->dy) || !aligned16(a->dx) || !aligned16(a->dz))
+    return fail(FRAC_ERR_INVALID_ARG, "x, z, dy, dx and dz must be 16-byte aligned");
+  const size_t need = frac::gnorm_workspace(d.C);
+  if (a->dweight && (!ws || ws_bytes < need))
+    return fail(FRAC_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", need, ws ? ws_bytes : (size_t)0);
+  return hip_status(frac::launch_gnorm_bwd(d, *a, reinterpret_cast<float*>(ws), reinterpret_cast<hipStream_t>(stream)),
+                    "frac_gnorm_bwd launch");
 }
 
 }  // extern "C"

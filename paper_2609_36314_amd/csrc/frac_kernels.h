@@ -84,6 +84,17 @@ size_t conv_workspace(int64_t C, int K);
 hipError_t launch_conv_fwd(const ConvDims& d, const frac_conv_args& a, hipStream_t stream);
 hipError_t launch_conv_bwd(const ConvDims& d, const frac_conv_bwd_args& a, float* ws, hipStream_t stream);
 
+// Gated normalization of the layer output (frac_gnorm.hip).
+struct GnormDims {
+  int64_t rows;  // B * L
+  int C, group;
+  bool bf16_io;
+};
+constexpr int kGnormMaxRowBlocks = 1024;
+size_t gnorm_workspace(int64_t C);
+hipError_t launch_gnorm_fwd(const GnormDims& d, const frac_gnorm_args& a, hipStream_t stream);
+hipError_t launch_gnorm_bwd(const GnormDims& d, const frac_gnorm_bwd_args& a, float* ws, hipStream_t stream);
+
 hipError_t launch_decode_step(const ScanParams& p, float* state, hipStream_t stream);
 
 // The layer without B/C projections (dstate 1, B = C = 1): forward scan (no

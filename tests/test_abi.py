@@ -215,3 +215,26 @@ def test_convolution_arguments_are_checked_on_the_host():
     b.fwd = a
     b.dy = b.dx = b.dw = p
     assert lib.frac_conv_bwd(ctypes.byref(sh), ctypes.byref(b), None, 0, None) == -3  # no workspace
+
+
+def test_gated_norm_arguments_are_checked_on_the_host():
+    from paper_2609_36314_amd._lib import FracGnormArgs, FracGnormBwdArgs
+    lib = _lib.load()
+    sh = _shape()
+    buf = (ctypes.c_float * 64)()
+    p = ctypes.cast(buf, ctypes.c_void_p)
+    a = FracGnormArgs()
+    a.channels, a.group, a.eps = 64, 64, 1e-5
+    assert lib.frac_gnorm_fwd(ctypes.byref(sh), ctypes.byref(a), None) == -1  # no pointers
+    a.x = a.z = a.weight = a.y = p
+    for ch, grp, st in ((64, 24, -2), (64, 48, -2), (60, 60, -2), (8192, 64, -2), (64, 128, -2)):
+        a.channels, a.group = ch, grp
+        assert lib.frac_gnorm_fwd(ctypes.byref(sh), ctypes.byref(a), None) == st, (ch, grp)
+    a.channels, a.group, a.eps = 64, 16, -1.0
+    assert lib.frac_gnorm_fwd(ctypes.byref(sh), ctypes.byref(a), None) == -1
+    a.eps = 1e-5
+    assert lib.frac_gnorm_workspace_size(ctypes.byref(sh), 64) > 0
+    b = FracGnormBwdArgs()
+    b.fwd = a
+    b.dy = b.dx = b.dz = b.dweight = p
+    assert lib.frac_gnorm_bwd(ctypes.byref(sh), ctypes.byref(b), None, 0, None) == -3  # no workspace
