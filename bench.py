@@ -139,6 +139,31 @@ def bench_conv(torch, frac, w, steps, warmup, K=4):
             "conv_bwd_ms": bms, "conv_bwd_roofline": roofline("hbm", 3 * n, bms, PEAK_HBM_BYTES, "GB/s")}
 
 
+def bench_layer(torch, frac, w, steps, warmup, d_model=2048):
+    """One Frac layer (paper_2609_36314_amd.layer.FracLayer, the 1.3B model's width
+    2048 and its H x d_h x M) forward + backward through autograd, in the io dtype."""
+    from paper_2609_36314_amd.layer import FracLayer
+    io = torch.bfloat16 if w.io_dtype == "bf16" else torch.float32
+    layer = FracLayer(d_model, w.nheads, w.headdim, w.nmodes, dtype=io)
+    g = torch.Generator().manual_seed(0)
+    h = torch.randn(w.batch, w.seqlen, d_model, generator=g).to(io).cuda().requires_grad_(True)
+    dout = torch.randn(w.batch, w.seqlen, d_model, generator=g).to(io).cuda()
+
+    def step():
+        layer.zero_grad(set_to_none=True)
+        h.grad = None
+        layer(h).backward(dout)
+
+    for _ in range(warmup):
+        step()
+    t = Timer(torch)
+    for _ in range(steps):
+        with t:
+            step()
+    ms = float(np.mean(t.ms()))
+    return {"layer_fwd_bwd_ms": ms, "layer_tokens_per_s": w.batch * w.seqlen / (ms * 1e-3), "layer_d_model": d_model}
+
+
 def decode_bytes_per_step(w):
     B, H, P, N, M, G = w.batch, w.nheads, w.headdim, w.dstate, w.nmodes, w.ngroups
     io = 2 if w.io_dtype == "bf16" else 4
@@ -245,6 +270,7 @@ def bench_scan(torch, frac, w, steps, warmup):
         res["bwd_all_grads_ms"] = float(np.mean(ta.ms()))
         res.update(bench_params(torch, frac, w, steps, warmup))
         res.update(bench_conv(torch, frac, w, steps, warmup))
+        res.update(bench_layer(torch, frac, w, steps, warmup))
         res["bwd_ms"] = bms
         res["bwd_roofline"] = dict(roofline("hbm", nfree_bwd_bytes(w), bms, PEAK_HBM_BYTES, "GB/s"),
                                    traffic=measured_traffic("frac_scan_bwd", w.name))
