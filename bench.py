@@ -53,6 +53,9 @@ def parse():
                                            "paper-nfree-train-b8-l2048,decode-b256-128steps")
     ap.add_argument("--main", default="train-b4-l4096-m8")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-extras", action="store_true",
+                    help="time only the scan entry points (no all-gradients backward, parameter construction, "
+                         "convolution or layer), e.g. for hardware-counter runs")
     ap.add_argument("--cpu-sample-heads", type=int, default=64)
     ap.add_argument("--cpu-sample-batch", type=int, default=4,
                     help="batch elements of the main workload the oracle runs (bounded CPU sample)")
@@ -208,7 +211,7 @@ def device_inputs(torch, w, seed=0):
     return out
 
 
-def bench_scan(torch, frac, w, steps, warmup):
+def bench_scan(torch, frac, w, steps, warmup, extras=True):
     inp = device_inputs(torch, w)
     tau = frac.default_tau(w.nmodes, device="cuda")
     alpha = inp["alpha"]
@@ -261,16 +264,17 @@ def bench_scan(torch, frac, w, steps, warmup):
     if not w.bc:  # without B/C the forward moves more bytes than it does matrix-core work
         res["fwd_roofline"] = roofline("hbm", nfree_fwd_bytes(w), fms, PEAK_HBM_BYTES, "GB/s")
     if w.backward and not w.bc:
-        for _ in range(warmup):
-            bwd_all()
-        ta = Timer(torch)
-        for _ in range(steps):
-            with ta:
+        if extras:
+            for _ in range(warmup):
                 bwd_all()
-        res["bwd_all_grads_ms"] = float(np.mean(ta.ms()))
-        res.update(bench_params(torch, frac, w, steps, warmup))
-        res.update(bench_conv(torch, frac, w, steps, warmup))
-        res.update(bench_layer(torch, frac, w, steps, warmup))
+            ta = Timer(torch)
+            for _ in range(steps):
+                with ta:
+                    bwd_all()
+            res["bwd_all_grads_ms"] = float(np.mean(ta.ms()))
+            res.update(bench_params(torch, frac, w, steps, warmup))
+            res.update(bench_conv(torch, frac, w, steps, warmup))
+            res.update(bench_layer(torch, frac, w, steps, warmup))
         res["bwd_ms"] = bms
         res["bwd_roofline"] = dict(roofline("hbm", nfree_bwd_bytes(w), bms, PEAK_HBM_BYTES, "GB/s"),
                                    traffic=measured_traffic("frac_scan_bwd", w.name))
@@ -403,7 +407,7 @@ def main():
         if w.decode_steps:
             results[n] = bench_decode(torch, frac, w, max(1, args.steps // 4), max(1, args.warmup // 2))
         else:
-            results[n] = bench_scan(torch, frac, w, args.steps, args.warmup)
+            results[n] = bench_scan(torch, frac, w, args.steps, args.warmup, extras=not args.no_extras)
         print("# %s: %s" % (n, json.dumps(results[n])), file=sys.stderr, flush=True)
         torch.cuda.empty_cache()
 
