@@ -489,6 +489,7 @@ __global__ void __launch_bounds__(512) frac_bwd_state_kernel(ScanParams p, BwdWo
     const float* P_A = W + NWA * MP * kWQ;
     wait_vmem();
     barrier();  // this chunk's tiles and weights have landed; the previous chunk is done
+    const TilePrefetch<T> gcur = gtile.pinned_copy();  // before any new memory operation
     if (Cfg::NBUF == 2) {
       if (c + 1 < nchunks) stage(c + 1, Xn, Yn, Bn);
     } else {
@@ -539,7 +540,7 @@ __global__ void __launch_bounds__(512) frac_bwd_state_kernel(ScanParams p, BwdWo
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
               const int t = tb * 16 + lg * 4 + r, kk = kb * 16 + li;
-              gv[r] = keep_if_ge(gtile.get(jt, r) * Gm[r], t, kk);
+              gv[r] = keep_if_ge(gcur.get(jt, r) * Gm[r], t, kk);
             }
             store4(reinterpret_cast<T*>(wk.gg) + to, gv);
           }
@@ -556,7 +557,7 @@ __global__ void __launch_bounds__(512) frac_bwd_state_kernel(ScanParams p, BwdWo
 #pragma unroll
           for (int r = 0; r < 4; ++r) {
             const int t = tb * 16 + lg * 4 + r, kk = kb * 16 + li;
-            const float hm = keep_if_ge(gtile.get(jt, r) * D[r], t, kk);
+            const float hm = keep_if_ge(gcur.get(jt, r) * D[r], t, kk);
             rv[r] = hm * Ph[r];
             ce += hm * Ph[r];
             cf += hm * Ps[r];
@@ -891,6 +892,10 @@ __global__ void __launch_bounds__(512) frac_bwd_cols_kernel(ScanParams p, BwdWor
     float* Enext = s_E2 + ((i + 1) & 1) * MP;
     wait_vmem();
     barrier();
+    // this chunk's prefetched controls, logits and tile values, taken before any new memory operation
+    const float dtv = pinned(dt_n), al_l = pinned(al_n), lam_l = pinned(lam_n);
+    const PairLogits<MP, 512> lgt = lgt_n.pinned_copy();
+    const TilePrefetch<T> hcur = hgt.pinned_copy();
     if (Cfg::NBUF == 2) {
       if (c > 0) stage(c - 1, Xn, Yn, Cn);
     } else {
@@ -898,8 +903,6 @@ __global__ void __launch_bounds__(512) frac_bwd_cols_kernel(ScanParams p, BwdWor
       wait_vmem();
       barrier();
     }
-    const float dtv = dt_n, al_l = al_n, lam_l = lam_n;
-    const PairLogits<MP, 512> lgt = lgt_n;
     if (c > 0) load_controls(c - 1, dt_n, al_n, lam_n);
     const ChunkCtl k = chunk_controls(dtv, al_l, lam_l, lm_bh != nullptr, nv);
     if (wave == 0) P_A[lane] = k.A;
@@ -922,7 +925,7 @@ __global__ void __launch_bounds__(512) frac_bwd_cols_kernel(ScanParams p, BwdWor
       if (tile >= kTiles) break;
       const int tb = tile_row(tile), kb = tile_col(tile);
 #pragma unroll
-      for (int r = 0; r < 4; ++r) HG[(tb * 16 + lg * 4 + r) * XS + kb * 16 + li] = hgt.v[jt].e[r];
+      for (int r = 0; r < 4; ++r) HG[(tb * 16 + lg * 4 + r) * XS + kb * 16 + li] = hcur.v[jt].e[r];
     }
     (void)unsafe;
     if (c > 0) hgt.load(hgtiles + ((int64_t)(b * nchunks + c - 1) * H + h) * (kTiles * kTileElems), wave, lane);
@@ -1202,6 +1205,10 @@ __global__ void __launch_bounds__(512) frac_bwd_rows_kernel(ScanParams p, BwdWor
     float* Enext = s_E2 + ((i + 1) & 1) * MP;
     wait_vmem();
     barrier();
+    // this chunk's prefetched controls, logits and tile values, taken before any new memory operation
+    const float dtv = pinned(dt_n), al_l = pinned(al_n), lam_l = pinned(lam_n);
+    const PairLogits<MP, 512> lgt = lgt_n.pinned_copy();
+    const TilePrefetch<T> gcur = ggt.pinned_copy();
     if (Cfg::kBf16 && i > 0) store_dx(c + 1);
     if (Cfg::NBUF == 2) {
       if (c > 0) stage_late(c - 1, Cn, Yn);
@@ -1211,8 +1218,6 @@ __global__ void __launch_bounds__(512) frac_bwd_rows_kernel(ScanParams p, BwdWor
       wait_vmem();
       barrier();
     }
-    const float dtv = dt_n, al_l = al_n, lam_l = lam_n;
-    const PairLogits<MP, 512> lgt = lgt_n;
     if (c > 0) load_controls(c - 1, dt_n, al_n, lam_n);
     const ChunkCtl k = chunk_controls(dtv, al_l, lam_l, lm_bh != nullptr, nv);
     if (wave == 0) P_A[lane] = k.A;
@@ -1236,7 +1241,7 @@ __global__ void __launch_bounds__(512) frac_bwd_rows_kernel(ScanParams p, BwdWor
         if (tile >= kTiles) break;
         const int tb = tile_row(tile), kb = tile_col(tile);
 #pragma unroll
-        for (int r = 0; r < 4; ++r) GG[(tb * 16 + lg * 4 + r) * XS + kb * 16 + li] = ggt.v[jt].e[r];
+        for (int r = 0; r < 4; ++r) GG[(tb * 16 + lg * 4 + r) * XS + kb * 16 + li] = gcur.v[jt].e[r];
       }
     }
     (void)unsafe;
