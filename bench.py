@@ -50,7 +50,7 @@ def parse():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workloads", default="train-b4-l4096-m8,layer-fwd-b8-l2048,prefill-b1-l16384,paper-nfree-b8-l2048,"
-                                           "paper-nfree-train-b8-l2048,decode-b256-128steps")
+                                           "paper-nfree-train-b8-l2048,decode-b256-128steps,paper-nfree-decode-b2048-128steps")
     ap.add_argument("--main", default="train-b4-l4096-m8")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-extras", action="store_true",
@@ -171,7 +171,7 @@ def decode_bytes_per_step(w):
     B, H, P, N, M, G = w.batch, w.nheads, w.headdim, w.dstate, w.nmodes, w.ngroups
     io = 2 if w.io_dtype == "bf16" else 4
     state = 2 * B * H * M * N * P * 4
-    tokens = B * H * P * io * 2 + 2 * B * G * N * io + B * H * 4
+    tokens = B * H * P * io * 2 + (2 * B * G * N * io if w.bc else 0) + B * H * 4
     return state + tokens
 
 
@@ -295,11 +295,12 @@ def bench_decode(torch, frac, w, steps, warmup):
     state = inp["init_state"]
     S = w.decode_steps
     ys = torch.empty((S, w.batch, w.nheads, w.headdim), dtype=inp["x"].dtype, device="cuda")
+    Bm, Cm = inp.get("Bm"), inp.get("Cm")  # absent in the form without B/C
 
     def one_pass():
         for s in range(S):
-            frac.decode_step(state, inp["x"][s], inp["dt"][s], inp["Bm"][s], inp["Cm"][s], inp["alpha"], tau,
-                             y=ys[s])
+            frac.decode_step(state, inp["x"][s], inp["dt"][s], Bm[s] if Bm is not None else None,
+                             Cm[s] if Cm is not None else None, inp["alpha"], tau, y=ys[s])
 
     for _ in range(warmup):
         one_pass()

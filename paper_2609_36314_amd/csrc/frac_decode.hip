@@ -19,8 +19,11 @@ namespace {
 constexpr int kDecodeThreads = 1024;
 constexpr int kDecodeUnroll = 8;
 
-template <typename T, int MP>
-__global__ void __launch_bounds__(kDecodeThreads) frac_decode_kernel(ScanParams p, float* __restrict__ state) {
+// NT threads per (b, h): 1024 for large states (one batch of loads, then the writes:
+// long DRAM runs), 256 when the state is at most 2048 float4 (the form without B/C),
+// where more resident workgroups hide the per-token coefficient latency.
+template <typename T, int MP, int NT>
+__global__ void __launch_bounds__(NT) frac_decode_kernel(ScanParams p, float* __restrict__ state) {
   const int tid = threadIdx.x;
   const int H = p.H, P = p.P, N = p.N, M = p.M;
   const int bh = blockIdx.x;
@@ -28,7 +31,7 @@ __global__ void __launch_bounds__(kDecodeThreads) frac_decode_kernel(ScanParams 
 
   __shared__ float sB[128], sC[128], sx[256];
   __shared__ float s_rho[MP], s_kap[MP], s_c[MP];
-  __shared__ float4 red[kDecodeThreads];
+  __shared__ float4 red[NT];
 
   const T* x = reinterpret_cast<const T*>(p.x) + ((int64_t)b * H + h) * P;
   const T* Bg = reinterpret_cast<const T*>(p.Bm) + ((int64_t)b * p.G + g) * N;
@@ -56,15 +59,15 @@ __global__ void __launch_bounds__(kDecodeThreads) frac_decode_kernel(ScanParams 
       s_c[m] = cw;
     }
   }
-  for (int i = tid; i < N; i += kDecodeThreads) {  // without B/C (dstate 1) both are 1
+  for (int i = tid; i < N; i += NT) {  // without B/C (dstate 1) both are 1
     sB[i] = p.Bm ? to_f32(Bg[i]) : 1.0f;
     sC[i] = p.Cm ? to_f32(Cg[i]) : 1.0f;
   }
-  for (int i = tid; i < P; i += kDecodeThreads) sx[i] = to_f32(x[i]);
+  for (int i = tid; i < P; i += NT) sx[i] = to_f32(x[i]);
   __syncthreads();
 
   const int P4 = P >> 2;             // float4 columns per state row
-  const int RG = kDecodeThreads / P4;  // row groups
+  const int RG = NT / P4;  // row groups
   const int col = tid % P4, rg = tid / P4;
   const float4 xv = make_float4(sx[4 * col], sx[4 * col + 1], sx[4 * col + 2], sx[4 * col + 3]);
   floatx4 acc = {0.f, 0.f, 0.f, 0.f};
@@ -132,7 +135,11 @@ __global__ void __launch_bounds__(kDecodeThreads) frac_decode_kernel(ScanParams 
 
 template <typename T, int MP>
 hipError_t launch_decode_variant(const ScanParams& p, float* state, hipStream_t stream) {
-  hipLaunchKernelGGL((frac_decode_kernel<T, MP>), dim3(p.Bsz * p.H), dim3(kDecodeThreads), 0, stream, p, state);
+  if ((int64_t)p.M * p.N * p.P / 4 <= 2048)
+    hipLaunchKernelGGL((frac_decode_kernel<T, MP, 256>), dim3(p.Bsz * p.H), dim3(256), 0, stream, p, state);
+  else
+    hipLaunchKernelGGL((frac_decode_kernel<T, MP, kDecodeThreads>), dim3(p.Bsz * p.H), dim3(kDecodeThreads), 0,
+                       stream, p, state);
   return hipGetLastError();
 }
 

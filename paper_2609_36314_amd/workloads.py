@@ -56,8 +56,12 @@ DECODE = Workload("decode-b256-128steps", 256, 1, 64, 64, 128, 4, decode_steps=1
 # the paper's layer (state H x M x d_h, no B/C), forward at batch 8 x 2048 tokens
 PAPER_NFREE = Workload("paper-nfree-b8-l2048", 8, 2048, 16, 256, 1, 16, bc=False)
 PAPER_NFREE_TRAIN = Workload("paper-nfree-train-b8-l2048", 8, 2048, 16, 256, 1, 16, bc=False, backward=True)
+# decode of the paper's form: 2048 sequences, a 537 MB float32 state (larger than the on-chip caches)
+PAPER_NFREE_DECODE = Workload("paper-nfree-decode-b2048-128steps", 2048, 1, 16, 256, 1, 16, bc=False,
+                              decode_steps=128, init_state=True)
 
-WORKLOADS = {w.name: w for w in (TINY_F32, LAYER_FWD, LONG_PREFILL, TRAIN, DECODE, PAPER_NFREE, PAPER_NFREE_TRAIN)}
+WORKLOADS = {w.name: w for w in (TINY_F32, LAYER_FWD, LONG_PREFILL, TRAIN, DECODE, PAPER_NFREE, PAPER_NFREE_TRAIN,
+                                  PAPER_NFREE_DECODE)}
 
 
 def _softplus(v: np.ndarray) -> np.ndarray:
