@@ -387,8 +387,8 @@ def cpu_baseline(w, heads, batch):
 def main():
     args = parse()
     if args.gpus != 1:
-        print("bench.py: this build runs on one GPU; --gpus %d is not supported (the scan shards by batch and "
-              "head without communication; see the design notes)" % args.gpus, file=sys.stderr)
+        print("bench.py: measures one GPU only; --gpus %d is not supported (the scan shards by batch and "
+              "head without communication, so N GPUs run N independent shares)" % args.gpus, file=sys.stderr)
         sys.exit(2)
     import torch
     import paper_2609_36314_amd as frac

@@ -15,7 +15,7 @@ def test_more_than_one_gpu_is_refused_with_a_message():
     r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"], capture_output=True, text=True,
                        timeout=120)
     assert r.returncode == 2
-    assert "one GPU" in r.stderr
+    assert "one GPU only" in r.stderr
 
 
 def test_roofline_arithmetic():
