@@ -50,3 +50,14 @@ def test_conv_forward_and_backward_match_oracle(name):
     for k in ("dx", "dw", "dbias"):
         if g[k] is not None:
             assert torch.equal(g[k], g2[k]), k  # fixed-order sums
+
+
+def test_conv_empty_sequence_gives_zero_sums():
+    x = torch.empty(2, 0, 16, dtype=torch.bfloat16, device="cuda")
+    w = torch.randn(16, 4).cuda()
+    b = torch.randn(16).cuda()
+    y = frac.conv_fwd(x, w, bias=b)
+    g = frac.conv_bwd(x, w, x.clone(), bias=b)
+    torch.cuda.synchronize()
+    assert y.shape == x.shape and g["dx"].shape == x.shape
+    assert not g["dw"].any() and not g["dbias"].any()

@@ -39,3 +39,12 @@ def test_gnorm_forward_and_backward_match_oracle(name):
     torch.cuda.synchronize()
     for k in gr:
         assert torch.equal(gr[k], gr2[k]), k
+
+
+def test_gnorm_empty_batch_gives_zero_weight_gradient():
+    x = torch.empty(0, 5, 64, dtype=torch.float32, device="cuda")
+    w = torch.randn(64).cuda()
+    y = frac.gnorm_fwd(x, x.clone(), w)
+    g = frac.gnorm_bwd(x, x.clone(), w, x.clone())
+    torch.cuda.synchronize()
+    assert y.shape == x.shape and not g["dweight"].any()

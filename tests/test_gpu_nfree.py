@@ -216,3 +216,19 @@ def test_nfree_bwd_deterministic():
     g2 = frac.scan_bwd(inp["x"], inp["dt"], None, None, inp["alpha"], tau_d, inp["dy"])
     torch.cuda.synchronize()
     assert torch.equal(g1["dx"], g2["dx"]) and torch.equal(g1["ddt"], g2["ddt"])
+
+
+def test_nfree_bwd_shared_logits_all_grads():
+    """One tensor passed as both read and write logits (the write weights then equal
+    the read weights); both logit gradients still match the oracle's."""
+    w = Workload("t", 1, 100, 2, 64, 1, 8, bc=False, backward=True, extras=True)
+    inp = device_inputs(w, seed=19)
+    inp["write_logit"] = inp["read_logit"]
+    tau_d, tau64 = _tau(8)
+    kw = {k: inp[k] for k in ("lam", "read_logit", "write_logit", "D") if k in inp}
+    g = frac.scan_bwd(inp["x"], inp["dt"], None, None, inp["alpha"], tau_d, inp["dy"], all_grads=True, **kw)
+    torch.cuda.synchronize()
+    ref = _oracle_bwd(inp, tau64)
+    tol = TOL["bf16"]
+    for k in ("dx", "ddt", "dalpha", "dlambda", "dread_logit", "dwrite_logit"):
+        assert_close(k, f64(g[k]), ref[k], tol)
