@@ -433,13 +433,13 @@ __global__ void __launch_bounds__(512) frac_bwd_state_kernel(ScanParams p, BwdWo
   planC.init(bstride, N);
   auto stage = [&](int c, T* Xd, T* Yd, T* Bd) {
     const int t0 = c * kQ, nv = min(kQ, L - t0);
-    planX.template issue<Cfg::NBUF == 1>(Xd, xg + (int64_t)t0 * xstride, xstride, nv);
-    planX.template issue<Cfg::NBUF == 1>(Yd, yg + (int64_t)t0 * xstride, xstride, nv);
-    planB.template issue<Cfg::NBUF == 1>(Bd, Bgp + (int64_t)t0 * bstride, bstride, nv);
+    planX.issue_async(Xd, xg + (int64_t)t0 * xstride, xstride, nv);
+    planX.issue_async(Yd, yg + (int64_t)t0 * xstride, xstride, nv);
+    planB.issue_async(Bd, Bgp + (int64_t)t0 * bstride, bstride, nv);
   };
   auto stageC = [&](int c) {
     const int t0 = c * kQ, nv = min(kQ, L - t0);
-    planC.template issue<Cfg::NBUF == 1>(Cb, Cgp + (int64_t)t0 * bstride, bstride, nv);
+    planC.issue_async(Cb, Cgp + (int64_t)t0 * bstride, bstride, nv);
   };
 
   float dt_n, al_n, lam_n;
@@ -871,9 +871,9 @@ __global__ void __launch_bounds__(512) frac_bwd_cols_kernel(ScanParams p, BwdWor
   // conversion of these tiles into an instruction it cannot encode)
   auto stage = [&](int c, T* Xd, T* Yd, T* Cd) {
     const int t0 = c * kQ, nv = min(kQ, L - t0);
-    planX.template issue<true>(Xd, xg + (int64_t)t0 * xstride, xstride, nv);
-    planX.template issue<true>(Yd, yg + (int64_t)t0 * xstride, xstride, nv);
-    planC.template issue<true>(Cd, Cgp + (int64_t)t0 * bstride, bstride, nv);
+    planX.issue_async(Xd, xg + (int64_t)t0 * xstride, xstride, nv);
+    planX.issue_async(Yd, yg + (int64_t)t0 * xstride, xstride, nv);
+    planC.issue_async(Cd, Cgp + (int64_t)t0 * bstride, bstride, nv);
   };
 
   float dt_n, al_n, lam_n;
@@ -1164,13 +1164,13 @@ __global__ void __launch_bounds__(512) frac_bwd_rows_kernel(ScanParams p, BwdWor
   planC.init(bstride, N);
   auto stage_late = [&](int c, T* Cd, T* Yd) {  // used through the whole chunk
     const int t0 = c * kQ, nv = min(kQ, L - t0);
-    planC.template issue<Cfg::NBUF == 1>(Cd, Cgp + (int64_t)t0 * bstride, bstride, nv);
-    planX.template issue<Cfg::NBUF == 1>(Yd, yg + (int64_t)t0 * xstride, xstride, nv);
+    planC.issue_async(Cd, Cgp + (int64_t)t0 * bstride, bstride, nv);
+    planX.issue_async(Yd, yg + (int64_t)t0 * xstride, xstride, nv);
   };
   auto stage_early = [&](int c) {  // read before the mid-chunk barrier only
     const int t0 = c * kQ, nv = min(kQ, L - t0);
-    planB.template issue<Cfg::NBUF == 1>(Bb, Bgp + (int64_t)t0 * bstride, bstride, nv);
-    planX.template issue<Cfg::NBUF == 1>(Xb, xg + (int64_t)t0 * xstride, xstride, nv);
+    planB.issue_async(Bb, Bgp + (int64_t)t0 * bstride, bstride, nv);
+    planX.issue_async(Xb, xg + (int64_t)t0 * xstride, xstride, nv);
   };
   // dx rows of chunk c (staged in Dxb) -> global, this workgroup's columns
   auto store_dx = [&](int c) {

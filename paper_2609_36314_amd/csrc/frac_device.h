@@ -432,6 +432,31 @@ struct DmaPlan {
       __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, l3, 16, (int)off[k], 0, 0, 0);
     }
   }
+  // The same copy issued as an instruction the compiler does not see as an LDS
+  // write: it then does not wait for the copy before every later LDS read (which it
+  // must assume may alias the copy's destination), so the next chunk's copy
+  // overlaps the current chunk's work.  The caller waits for it explicitly
+  // (wait_vmem) before the barrier that publishes the tile.
+  __device__ __forceinline__ void issue_async(T* lds, const T* src, int64_t gstride, int nv) const {
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const long long range = (long long)nv * gstride * (long long)sizeof(T);
+    const uint64_t a = (uint64_t)(uintptr_t)src;
+    typedef int i32x4 __attribute__((ext_vector_type(4)));
+    i32x4 rs;  // buffer resource: base, stride 0, byte range, raw-buffer flags
+    rs[0] = __builtin_amdgcn_readfirstlane((int)(uint32_t)a);
+    rs[1] = __builtin_amdgcn_readfirstlane((int)((uint32_t)(a >> 32) & 0xffffu));
+    rs[2] = __builtin_amdgcn_readfirstlane((int)(range < kOut ? range : kOut));
+    rs[3] = 0x00020000;
+#pragma unroll
+    for (int k = 0; k < KT; ++k) {
+      if (k * 8 + wave >= CPR) continue;  // past the tile (uniform)
+      const uint32_t m0 = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(lds + (k * 8 + wave) * 64 * E));
+      asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
+                   :
+                   : "s"(m0), "v"(off[k]), "s"(rs)
+                   : "memory", "m0");
+    }
+  }
 };
 
 // This lane's 4 io values of the C B^T tiles `wave` and `wave + 8` of one chunk

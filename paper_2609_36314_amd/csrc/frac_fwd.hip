@@ -290,9 +290,9 @@ __global__ void __launch_bounds__(512) frac_fwd_kernel(ScanParams p, const T* __
   planC.init(bstride, N);
   auto stage = [&](int c, T* Xd, T* Bd, T* Cd) {
     const int t0 = c * kQ, nv = min(kQ, T1 - t0);
-    planX.template issue<Cfg::NBUF == 1>(Xd, xg + (int64_t)t0 * xstride, xstride, nv);
-    planB.template issue<Cfg::NBUF == 1>(Bd, Bgp + (int64_t)t0 * bstride, bstride, nv);
-    if constexpr (!STATE_ONLY) planC.template issue<Cfg::NBUF == 1>(Cd, Cgp + (int64_t)t0 * bstride, bstride, nv);
+    planX.issue_async(Xd, xg + (int64_t)t0 * xstride, xstride, nv);
+    planB.issue_async(Bd, Bgp + (int64_t)t0 * bstride, bstride, nv);
+    if constexpr (!STATE_ONLY) planC.issue_async(Cd, Cgp + (int64_t)t0 * bstride, bstride, nv);
   };
   // output rows of chunk c (staged in Yb) -> global, 16 bytes per thread
   auto store_y = [&](int c) {
