@@ -542,12 +542,12 @@ __global__ void __launch_bounds__(256, 2) frac_nfree_bwd_kernel(ScanParams p, Nf
       floatx4 Gm = {0.f, 0.f, 0.f, 0.f}, Ph = Gm, Ps = Gm;
 #pragma unroll
       for (int q = 0; q < (MP + 3) / 4; ++q) {
-        const int m = q * 4 + lg;
-        const bool ok = m < MP && !((unsafe >> m) & 1);
-        const float aO = ok ? P_O[m * WQ + tb * 16 + li] : 0.0f;
-        const float arO = ok ? P_rO[m * WQ + tb * 16 + li] : 0.0f;
-        const float bVt = ok ? P_Vt[m * WQ + kb * 16 + li] : 0.0f;
-        const float bY = ok ? P_Yw[m * WQ + kb * 16 + li] : 0.0f;
+        const int m = q * 4 + lg;  // < MP (a multiple of 4): the loads need no guard
+        const bool ok = !((unsafe >> m) & 1);
+        const float vO = P_O[m * WQ + tb * 16 + li], vrO = P_rO[m * WQ + tb * 16 + li];
+        const float vVt = P_Vt[m * WQ + kb * 16 + li], vY = P_Yw[m * WQ + kb * 16 + li];
+        const float aO = ok ? vO : 0.0f, arO = ok ? vrO : 0.0f;  // selects, not branches
+        const float bVt = ok ? vVt : 0.0f, bY = ok ? vY : 0.0f;
         Gm = __builtin_amdgcn_mfma_f32_16x16x4f32(aO, bVt, Gm, 0, 0, 0);
         Ph = __builtin_amdgcn_mfma_f32_16x16x4f32(arO, bVt, Ph, 0, 0, 0);
         Ps = __builtin_amdgcn_mfma_f32_16x16x4f32(aO, bY, Ps, 0, 0, 0);
