@@ -542,7 +542,9 @@ __global__ void __launch_bounds__(256, 2) frac_nfree_bwd_kernel(ScanParams p, Nf
       floatx4 Gm = {0.f, 0.f, 0.f, 0.f}, Ph = Gm, Ps = Gm;
 #pragma unroll
       for (int q = 0; q < (MP + 3) / 4; ++q) {
-        const int m = q * 4 + lg;  // < MP (a multiple of 4): the loads need no guard
+        // mode of this lane's K slot: lg (MP / 4) + q puts the 64 lanes' [m][t] reads in distinct
+        // LDS banks for 16 modes (the K order of the sum is free); < MP, a multiple of 4
+        const int m = lg * (MP / 4) + q;
         const bool ok = !((unsafe >> m) & 1);
         const float vO = P_O[m * WQ + tb * 16 + li], vrO = P_rO[m * WQ + tb * 16 + li];
         const float vVt = P_Vt[m * WQ + kb * 16 + li], vY = P_Yw[m * WQ + kb * 16 + li];
