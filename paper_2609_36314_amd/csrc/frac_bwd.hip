@@ -113,7 +113,7 @@ struct ChunkCtl {
 __device__ __forceinline__ ChunkCtl chunk_controls(float dtv, float al, float lam, bool has_lambda, int nv) {
   const int lane = threadIdx.x & 63;
   ChunkCtl k;
-  const float s_eff = has_lambda ? exp2f(log2f(lam) / al) : 1.0f;
+  const float s_eff = has_lambda ? step_factor(lam, al) : 1.0f;
   k.dtt = (lane < nv) ? dtv * s_eff : 0.0f;
   k.A = wave_inclusive_sum(k.dtt);
   k.Alast = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(k.A), 63));
@@ -159,7 +159,7 @@ __device__ __forceinline__ int pair_weights(const ChunkCtl& k, int nv, int M, co
     const float kap = beta * ww;
     const float ea = fexp(-r * A);
     const float ep = (ROLE == kState && safe) ? fexp(r * A) : 0.0f;
-    const float dec = fexp(-r * (k.Alast - A));
+    const float dec = fdecay(r, k.Alast - A);
     float* o = w + m * kWQ + t;
     constexpr int SW = MP * kWQ;  // stride of the weight arrays
     if constexpr (ROLE == kState) {
@@ -217,7 +217,7 @@ __device__ __forceinline__ void unsafe_terms(floatx4& acc, int unsafe, const flo
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       const int t = tb * 16 + lg * 4 + r, k = kb * 16 + li;
-      if (t >= k) acc[r] += (scale_r ? rm : 1.0f) * a[m * kWQ + t] * bm[m * kWQ + k] * fexp(-rm * (A[t] - A[k]));
+      if (t >= k) acc[r] += (scale_r ? rm : 1.0f) * a[m * kWQ + t] * bm[m * kWQ + k] * fdecay(rm, A[t] - A[k]);
     }
   }
 }
@@ -1490,7 +1490,7 @@ __global__ void __launch_bounds__(1024) frac_bwd_ddt_kernel(ScanParams p, BwdWor
     if (t < L) {
       const float al = strided3(p.alpha, p.as0, p.as1, p.as2, b, t, h);
       const float lam = p.lambda ? strided3(p.lambda, p.ls0, p.ls1, p.ls2, b, t, h) : 1.0f;
-      const float s_eff = p.lambda ? exp2f(log2f(lam) / al) : 1.0f;
+      const float s_eff = p.lambda ? step_factor(lam, al) : 1.0f;
       v = (-carry[hl] - s + f) * s_eff;
     }
     out[lane][hl] = v;

@@ -251,14 +251,28 @@ __device__ __forceinline__ void softmax_modes(float* z, int M) {
 }
 
 // Effective step dt * lambda^(1/alpha) (eq. tau-eff).
+
+// lambda^{1/alpha}, the factor of the effective step, held at or below 2^100 so that
+// chunk sums of steps stay finite (a factor that large already decays every mode with
+// tau < 2^80 to zero in float32 within one step of at least 1e-4).
+__device__ __forceinline__ float step_factor(float lam, float alpha) {
+  return exp2f(fminf(log2f(lam) / alpha, 100.0f));
+}
+
 __device__ __forceinline__ float effective_step(float dt, float alpha, const float* lam_ptr, float lam) {
-  return lam_ptr ? dt * exp2f(log2f(lam) / alpha) : dt;
+  return lam_ptr ? dt * step_factor(lam, alpha) : dt;
 }
 
 // ------------------------------------------------------- fast scalar math
 
 // e^x through the hardware exp2 (a multiply and one transcendental).
 __device__ __forceinline__ float fexp(float x) { return __expf(x); }
+
+// e^{-r d} for an interval d that is >= 0 in exact arithmetic but is a difference of
+// two float32 prefix sums: lanes of a scan add in different orders, so with large
+// sums the difference can round below zero by several ulps, and e^{+r |d|} would
+// overflow.  The clamp keeps every decay in [0, 1].
+__device__ __forceinline__ float fdecay(float r, float d) { return __expf(-r * fmaxf(d, 0.0f)); }
 
 // 1 - e^{-x} for x >= 0 without cancellation: a short Taylor series where the
 // difference is small, the subtraction elsewhere (relative error <= ~4e-6).

@@ -340,7 +340,7 @@ __global__ void __launch_bounds__(512) frac_fwd_kernel(ScanParams p, const T* __
     if (c + 1 < c1) load_controls(c + 1, dt_n, al_n, lam_n);
 
     // ---- per-token step and its chunk-local cumulative sum (lane = token, every wave)
-    const float s_eff_l = lm_bh ? exp2f(log2f(lam_l) / al_l) : 1.0f;
+    const float s_eff_l = lm_bh ? step_factor(lam_l, al_l) : 1.0f;
     const float dtt_l = (lane < nv) ? dtv * s_eff_l : 0.0f;
     const float A_l = wave_inclusive_sum(dtt_l);
     const float Alast = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(A_l), 63));
@@ -373,7 +373,7 @@ __global__ void __launch_bounds__(512) frac_fwd_kernel(ScanParams p, const T* __
       const float om = cw * fexp(-r * A);
       P_O[m * kWQ + t] = om;
       P_om[m * kWQ + t] = om * Ecur[m];
-      P_v[m * kWQ + t] = kap * fexp(-r * (Alast - A)) * upd;
+      P_v[m * kWQ + t] = kap * fdecay(r, Alast - A) * upd;
       P_Vt[m * kWQ + t] = safe ? kap * fexp(r * A) : 0.0f;
       P_c[m * kWQ + t] = cw;
       P_k[m * kWQ + t] = kap;
@@ -417,7 +417,7 @@ __global__ void __launch_bounds__(512) frac_fwd_kernel(ScanParams p, const T* __
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
               const int t = tb * 16 + lg * 4 + r, k = kb * 16 + li;
-              if (t >= k) Gm[r] += P_c[m * kWQ + t] * P_k[m * kWQ + k] * fexp(-rm * (P_A[t] - P_A[k]));
+              if (t >= k) Gm[r] += P_c[m * kWQ + t] * P_k[m * kWQ + k] * fdecay(rm, P_A[t] - P_A[k]);
             }
           }
         }

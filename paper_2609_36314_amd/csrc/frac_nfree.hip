@@ -145,7 +145,7 @@ __global__ void __launch_bounds__(256) frac_nfree_fwd_kernel(ScanParams p, float
         }
     }
     // ---- per-token controls (lane = token, every wave) and their chunk-local sum
-    const float s_eff = lm_bh ? exp2f(log2f(lam) / al_l) : 1.0f;
+    const float s_eff = lm_bh ? step_factor(lam, al_l) : 1.0f;
     const float dtt_l = tvalid ? dtv * s_eff : 0.0f;
     const float A_l = wave_inclusive_sum(dtt_l);
     const float Alast = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(A_l), 63));
@@ -172,7 +172,7 @@ __global__ void __launch_bounds__(256) frac_nfree_fwd_kernel(ScanParams p, float
       const float om = cw * fexp(-r * A);
       P_O[m * WQ + t] = om;
       P_om[m * WQ + t] = om * Ecur[m];
-      P_v[m * WQ + t] = kap * fexp(-r * (Alast - A)) * upd;
+      P_v[m * WQ + t] = kap * fdecay(r, Alast - A) * upd;
       P_Vt[m * WQ + t] = safe ? kap * fexp(r * A) : 0.0f;
       P_c[m * WQ + t] = cw;
       P_k[m * WQ + t] = kap;
@@ -211,7 +211,7 @@ __global__ void __launch_bounds__(256) frac_nfree_fwd_kernel(ScanParams p, float
 #pragma unroll
           for (int r = 0; r < 4; ++r) {
             const int t = tb * 16 + lg * 4 + r, k = kb * 16 + li;
-            if (t >= k) Gm[r] += P_c[m * WQ + t] * P_k[m * WQ + k] * fexp(-rm * (P_A[t] - P_A[k]));
+            if (t >= k) Gm[r] += P_c[m * WQ + t] * P_k[m * WQ + k] * fdecay(rm, P_A[t] - P_A[k]);
           }
         }
       }
@@ -487,7 +487,7 @@ __global__ void __launch_bounds__(256, 2) frac_nfree_bwd_kernel(ScanParams p, Nf
     }
     const bool tvalid = lane < nv;
     const float dtv = dt_n, al_l = al_n, lam = lam_n;
-    const float s_eff = lm_bh ? exp2f(log2f(lam) / al_l) : 1.0f;
+    const float s_eff = lm_bh ? step_factor(lam, al_l) : 1.0f;
     const float dtt_l = tvalid ? dtv * s_eff : 0.0f;
     const float A_l = wave_inclusive_sum(dtt_l);
     const float Alast = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(A_l), 63));
@@ -511,7 +511,7 @@ __global__ void __launch_bounds__(256, 2) frac_nfree_bwd_kernel(ScanParams p, Nf
       const float rwr = r * ww * (1.0f - beta);
       const float ea = fexp(-r * A);
       const float ep = safe ? fexp(r * A) : 0.0f;
-      const float dec = fexp(-r * (Alast - A));
+      const float dec = fdecay(r, Alast - A);
       float* o = W + m * WQ + t;
       o[0 * SW] = cw * ea;
       o[1 * SW] = safe ? kap * ep : kap;
@@ -562,7 +562,7 @@ __global__ void __launch_bounds__(256, 2) frac_nfree_bwd_kernel(ScanParams p, Nf
           for (int r = 0; r < 4; ++r) {
             const int t = tb * 16 + lg * 4 + r, k = kb * 16 + li;
             if (t >= k) {
-              const float d = fexp(-rm * (P_A[t] - P_A[k]));
+              const float d = fdecay(rm, P_A[t] - P_A[k]);
               const float ck = P_c[m * WQ + t] * d;
               Gm[r] += ck * P_Vt[m * WQ + k];
               Ph[r] += rm * ck * P_Vt[m * WQ + k];
@@ -696,15 +696,15 @@ __global__ void __launch_bounds__(256, 2) frac_nfree_bwd_kernel(ScanParams p, Nf
           const int t = tb * 16 + lg * 4 + r;
           const float At = P_A[t];
           float dc = fexp(-rm * At) * Uk[mb][r];
-          float dk = fexp(-rm * (AQ - At)) * Zk[mb][r];
+          float dk = fdecay(rm, AQ - At) * Zk[mb][r];
           if (!direct) {
             dc += fexp(-rm * At) * cI[r];
             dk += fexp(rm * At) * kI[r];
           } else {
             for (int k = 0; k <= t; ++k)
-              dc += to_f32(HT[t * XS + k]) * P_Vt[m * WQ + k] * fexp(-rm * (At - P_A[k]));
+              dc += to_f32(HT[t * XS + k]) * P_Vt[m * WQ + k] * fdecay(rm, At - P_A[k]);
             for (int t2 = t; t2 < 64; ++t2)
-              dk += to_f32(HT[t2 * XS + t]) * P_c[m * WQ + t2] * fexp(-rm * (P_A[t2] - At));
+              dk += to_f32(HT[t2 * XS + t]) * P_c[m * WQ + t2] * fdecay(rm, P_A[t2] - At);
           }
           if (m < M && t < nv) {
             const int64_t i = ((int64_t)ps * p.Bsz * H * L + (int64_t)bh * L + t0 + t) * M + m;  // [nps][B H L][M]
@@ -867,7 +867,7 @@ __global__ void __launch_bounds__(256) frac_nfree_grads_kernel(ScanParams p, con
   const float al = p.alpha[b * p.as0 + t * p.as1 + h * p.as2];
   const float lam = p.lambda ? p.lambda[b * p.ls0 + t * p.ls1 + h * p.ls2] : 1.0f;
   const float dtv = p.dt[tk];
-  const float s_eff = p.lambda ? exp2f(log2f(lam) / al) : 1.0f;
+  const float s_eff = p.lambda ? step_factor(lam, al) : 1.0f;
   const float tau = mv ? p.tau[m] : 1.0f;
   const float r = 1.0f / tau, lnt = logf(tau);
   const float prior = -al * lnt;
