@@ -71,3 +71,35 @@ def test_bc_form_large_steps_stay_finite():
     torch.cuda.synchronize()
     for k in ("dx", "ddt", "dBm", "dCm"):
         _finite(k, gr[k])
+
+
+def test_paper_form_large_but_moderate_steps_match_the_oracle():
+    # alpha 0.25: factor 4^4 = 256 on half the tokens, 0.25^4 on the rest; chunk sums of
+    # the steps up to ~1.6e3, where float32 prefix sums still resolve the small steps.
+    from harness import TOL, assert_close, f64
+    B, L, H, P, M = 1, 200, 2, 32, 16
+    print("moderate large steps vs oracle", (B, L, H, P, M), flush=True)
+    g = torch.Generator().manual_seed(2)
+    dt = torch.rand(B, L, H, generator=g) * 0.09 + 0.01
+    alpha = torch.full((B, L, H), 0.25)
+    lam = torch.where(torch.rand(B, L, H, generator=g) < 0.5, 4.0, 0.25)
+    x = torch.randn(B, L, H, P, generator=g)
+    rl = torch.randn(B, L, H, M, generator=g)
+    wl = torch.randn(B, L, H, M, generator=g)
+    dy = torch.randn(B, L, H, P, generator=g)
+    t32 = oracle.default_tau(M).astype(np.float32)
+    tau = torch.from_numpy(t32).cuda()
+    c = lambda t: t.cuda()
+    kw = dict(lam=c(lam), read_logit=c(rl), write_logit=c(wl))
+    y, fin = frac.scan_fwd(c(x), c(dt), None, None, c(alpha), tau, return_final_state=True, **kw)
+    gr = frac.scan_bwd(c(x), c(dt), None, None, c(alpha), tau, c(dy), all_grads=True, **kw)
+    torch.cuda.synchronize()
+    ones = np.ones((B, L, 1, 1))
+    okw = dict(lam=f64(lam), read_logit=f64(rl), write_logit=f64(wl))
+    ry, rfin = oracle.forward(f64(x), f64(dt), ones, ones, f64(alpha), t32.astype(np.float64), **okw)
+    rg = oracle.backward(f64(x), f64(dt), ones, ones, f64(alpha), t32.astype(np.float64), f64(dy), **okw)
+    tol = TOL["f32"]
+    assert_close("y", f64(y), ry, tol)
+    assert_close("final_state", f64(fin), rfin, tol)
+    for k in ("dx", "ddt", "dalpha", "dlambda", "dread_logit", "dwrite_logit"):
+        assert_close(k, f64(gr[k]), rg[k], tol)
