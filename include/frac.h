@@ -121,8 +121,7 @@ typedef struct {
  *   ddt            [B,L,H] f32          written
  *   dBm, dCm       [B,L,G,N] io_dtype   written, summed over the heads of each group
  *   dD             [H] f32              written when fwd.D is non-NULL and dD is non-NULL
- * The form without B/C (dstate 1) also produces, for each pointer that is
- * non-NULL (all must be NULL with dstate > 1, else FRAC_ERR_UNSUPPORTED):
+ * Both forms also produce, for each of these pointers that is non-NULL:
  *   dalpha         [B,L,H] f32          gradient of alpha at every (b, t, h), through the
  *                                       prior -alpha ln tau_m of both softmaxes (eq. read-softmax)
  *                                       and the effective step Delta lambda^{1/alpha} (eq. tau-eff);
@@ -131,7 +130,11 @@ typedef struct {
  *   dread_logit,
  *   dwrite_logit   [B,L,H,M] f32        gradients of the logits (also when the logits are
  *                                       NULL, i.e. at zero logits)
- *   dinit_state    [B,H,M,1,P] f32      gradient of init_state (also when it is NULL)
+ *   dinit_state    [B,H,M,N,P] f32      gradient of init_state (also when it is NULL)
+ * Where the library holds lambda^{1/alpha} at 2^100 (log2(lambda) / alpha > 100) the
+ * held factor does not depend on alpha or lambda, and their gradients carry no step
+ * term there.  Every decay across a token whose exponent dtt / tau_m exceeds 110 is
+ * zero in float32; such a token's step gradient in mode m is taken as zero.
  * Gradients with respect to tau are not produced. */
 typedef struct {
   frac_fwd_args fwd;

@@ -158,8 +158,8 @@ def scan_bwd(x, dt, Bm, Cm, alpha, tau, dy, *, lam=None, read_logit=None, write_
     """Chunked parallel scan, backward (frac_scan_bwd).
 
     Returns dict(dx, ddt, dBm, dCm, dD) with dD None when D is None.  With
-    all_grads (the form without B/C only) also dalpha [B,L,H], dlambda [B,L,H],
-    dread_logit, dwrite_logit [B,L,H,M] and dinit_state [B,H,M,1,P]."""
+    all_grads also dalpha [B,L,H], dlambda [B,L,H], dread_logit, dwrite_logit
+    [B,L,H,M] and dinit_state [B,H,M,N,P] (N = 1 without B/C)."""
     M = int(tau.shape[0])
     shape = _shape(x, Bm, M, chunk)
     Bsz, L, H, P = x.shape
@@ -172,7 +172,7 @@ def scan_bwd(x, dt, Bm, Cm, alpha, tau, dy, *, lam=None, read_logit=None, write_
         f32 = dict(dtype=torch.float32, device=x.device)
         out.update(dalpha=torch.empty((Bsz, L, H), **f32), dlambda=torch.empty((Bsz, L, H), **f32),
                    dread_logit=torch.empty((Bsz, L, H, M), **f32), dwrite_logit=torch.empty((Bsz, L, H, M), **f32),
-                   dinit_state=torch.empty((Bsz, H, M, 1, P), **f32))
+                   dinit_state=torch.empty((Bsz, H, M, int(shape.dstate), P), **f32))
     a = FracBwdArgs()
     a.fwd = fwd
     a.dy, a.d_final_state = _ptr(dy), _ptr(_f32(d_final_state, "d_final_state"))

@@ -280,13 +280,9 @@ frac_status frac_scan_bwd(const frac_shape* shape, const frac_bwd_args* args, vo
   frac_status s = fill_shape(shape, p);
   if (s == FRAC_OK) s = check_scan_shape(p, "frac_scan_bwd");
   if (s != FRAC_OK) return s;
-  if (args && p.N != 1 &&
-      (args->dalpha || args->dlambda || args->dread_logit || args->dwrite_logit || args->dinit_state))
-    return fail(FRAC_ERR_UNSUPPORTED,
-                "dalpha, dlambda, dread_logit, dwrite_logit and dinit_state are produced for dstate 1 only");
   if (p.Bsz == 0 || p.L == 0) {
     if (args && args->dinit_state && p.Bsz > 0) {  // no tokens: the initial state is the final state
-      const int64_t n = (int64_t)p.Bsz * p.H * p.M * p.P;
+      const int64_t n = (int64_t)p.Bsz * p.H * p.M * p.N * p.P;
       hipLaunchKernelGGL(copy_or_zero_kernel, dim3(256), dim3(256), 0,
                          reinterpret_cast<hipStream_t>(stream), args->dinit_state, args->d_final_state, n);
       const frac_status e = hip_status(hipGetLastError(), "frac_scan_bwd (empty)");

@@ -2,36 +2,34 @@
 //
 // Reverse-mode derivative of the selective mode-bank recurrence of Sec. 3.2
 // (eq. frac-selective-update, eq. frac-readout, the Appendix-D algorithm), with
-// the B/C-widened state, evaluated chunk by chunk like the forward.  Per mode
-// (r = 1/tau_m), chunk-local inclusive cumulative step A_t, chunk total A_Q,
-// state entering the chunk S0 and adjoint of the chunk's last state G:
+// the B/C-widened state, evaluated chunk by chunk like the forward.  Per mode,
+// chunk log-decays l (the chunk-local sums of the capped exponents r_m dtt, in
+// float64), chunk total l_Q, state entering the chunk S0 and adjoint of the
+// chunk's last state G:
 //
-//   dC_t  = sum_m c_{t,m} e^{-r A_t} S0_m dy_t + sum_{k<=t} Gamma_{t,k} (dy_t . x_k) B_k
-//   dx_t  = sum_m kappa_{t,m} e^{-r(A_Q - A_t)} B_t G_m
+//   dC_t  = sum_m c_{t,m} e^{-l_t} S0_m dy_t + sum_{k<=t} Gamma_{t,k} (dy_t . x_k) B_k
+//   dx_t  = sum_m kappa_{t,m} e^{-(l_Q - l_t)} B_t G_m
 //           + sum_{t'>=t} Gamma_{t',t} (C_t' . B_t) dy_t' + D dy_t
-//   dB_t  = sum_m kappa_{t,m} e^{-r(A_Q - A_t)} G_m x_t
+//   dB_t  = sum_m kappa_{t,m} e^{-(l_Q - l_t)} G_m x_t
 //           + sum_{t'>=t} Gamma_{t',t} (dy_t' . x_t) C_t'
-//   G (entering the previous chunk) = e^{-r A_Q} G + sum_t c_{t,m} e^{-r A_t} C_t dy_t^T
+//   G (entering the previous chunk) = e^{-l_Q} G + sum_t c_{t,m} e^{-l_t} C_t dy_t^T
 //
-// and for the step sizes (dc = C^T S dy, dkappa = B^T G x per token and mode):
-//   ddtt_t = -sum_m r_m <dS_final, S_final>_m - sum_{t'>=t} e_t' + f_t
-//   e_t = sum_m r_m (c dc - kappa dkappa)_{t,m},  f_t = sum_m r_m w rho dkappa_{t,m}
-//   ddt_t = ddtt_t * lambda_t^(1/alpha_t)
-// (the gradient of the cumulative log-retention telescopes into the suffix sum of
-// e).  Inside a chunk the e/f terms reduce to row and column sums of
-//   H o Phi and H o Psi,  H = (C B^T) o (dY X^T),
-//   Phi_{t,k} = sum_m r_m c_{t,m} kappa_{k,m} e^{-r(A_t - A_k)},
-//   Psi_{t,k} = sum_m r_m c_{t,m} w_{k,m} rho_{k,m} e^{-r(A_t - A_k)},
-// rank-M products like Gamma.
+// and the gradients of the per-(token, mode) weights, from which the finishing
+// kernels (frac_grads.hip) form ddt, dalpha, dlambda and the logit gradients:
+//   dc_{t,m} = e^{-l_t} C_t . (S0_m dy_t) + sum_{k<=t} H_{t,k} kappa_{k,m} e^{-(l_t - l_k)}
+//   dk_{t,m} = e^{-(l_Q - l_t)} (B_t^T G_m) . x_t + sum_{t'>=t} H_{t',t} c_{t',m} e^{-(l_t' - l_t)}
+//   H = (C B^T) o (dY X^T)
 //
 // Three sweeps, each its own kernel; every wave keeps its share of a state or
 // adjoint (at most 2 x 4 16x16 float32 tiles per mode group) in matrix-core
 // accumulators for the whole sequence:
 //   state  forward in time, state transposed (lane = column n of N, rows p): dC
-//          (per head), the readout and intra-chunk parts of e and f, the
-//          final-state term and sum(dy . x) for dD;
-//   rows   reverse, adjoint in row layout (lane = column p of P, rows n): dx and
-//          the adjoint parts of e and f;
+//          (per head), the state part of dc (per mode, over the workgroup's rows
+//          of N), the final-state term <dS_final, S_final> per mode and sum(dy . x)
+//          for dD;
+//   rows   reverse, adjoint in row layout (lane = column p of P, rows n): dx, the
+//          adjoint part of dk (per mode, over the workgroup's columns of P) and the
+//          gradient of the initial state;
 //   cols   reverse, adjoint transposed (lane = column n): dB (per head).
 // The state sweep also writes each chunk's causal tiles (C B^T) o Gamma and
 // Gamma o (dY X^T) (bfloat16 for bfloat16 I/O, 10 tiles of 16x16 per chunk and
@@ -40,9 +38,9 @@
 // splits P, over two workgroups per (batch, head), so that no per-head output
 // gets a second partial sum.  Tiles are copied straight into
 // LDS (natural layout, padded rows) and read back as matrix-core fragments with
-// row reads or transposed 64-bit reads.  A finishing kernel forms ddt from the
-// suffix sums, and a reduction kernel sums dB and dC over the heads of each group
-// in a fixed order.
+// row reads or transposed 64-bit reads.  A chunk-parallel kernel forms the
+// intra-chunk parts of dc and dk, and a reduction kernel sums dB and dC over the
+// heads of each group in a fixed order.
 #include "frac_device.h"
 #include "frac_kernels.h"
 
@@ -59,30 +57,6 @@ __device__ __forceinline__ float uniform(float v) {
   return __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(v)));
 }
 
-// Sum over the 16 lanes of a lane group of v[r] (r = 0..3); returned in every
-// lane whose index within the group has ((li >> 2) & 3) == r.  Each step pairs a
-// lane with one whose index differs in the step's bit: the mirror lane in the
-// 16-lane row (li ^ 15), the mirror in the 8-lane half (li ^ 7), then li ^ 2 and
-// li ^ 1, all DPP row permutations; the pairs reached cover the 16 lanes.
-__device__ __forceinline__ float reduce16_4(float v[4], int li) {
-#pragma unroll
-  for (int j = 0; j < 2; ++j) {
-    const bool hi = li & 8;
-    const float send = hi ? v[j] : v[j + 2];
-    const float keep = hi ? v[j + 2] : v[j];
-    v[j] = keep + dpp_move<0x140>(send);  // row_mirror
-  }
-  {
-    const bool hi = li & 4;
-    const float send = hi ? v[0] : v[1];
-    const float keep = hi ? v[1] : v[0];
-    v[0] = keep + dpp_move<0x141>(send);  // row_half_mirror
-  }
-  v[0] += dpp_move<0x4E>(v[0]);  // quad_perm [2, 3, 0, 1]
-  v[0] += dpp_move<0xB1>(v[0]);  // quad_perm [1, 0, 3, 2]
-  return v[0];
-}
-
 // ------------------------------------------------------------ shared pieces
 
 template <typename T>
@@ -96,18 +70,18 @@ struct Pad {
 };
 
 // Which sweep computes a chunk's per-(token, mode) weights, and which of them.
-enum Role { kState = 0, kRows = 1, kCols = 2 };
+enum Role { kState = 0, kRows = 1, kCols = 2, kIntra = 3 };
 
-// Number of [MP][Q] weight arrays a role keeps in LDS (plus one [Q] array for A_t).
+// Number of [MP][Q] weight arrays a role keeps in LDS (plus two for the hi and lo
+// parts of the chunk log-decays).
 template <int ROLE>
 constexpr int n_weight_arrays() {
-  return ROLE == kState ? 9 : ROLE == kRows ? 3 : 2;
+  return ROLE == kState ? 4 : ROLE == kRows ? 3 : 2;
 }
 
-// Per-wave chunk controls (lane = token): effective step, its chunk-local
-// inclusive sum and the chunk total.
+// Per-wave chunk controls (lane = token): the effective step and the fractional order.
 struct ChunkCtl {
-  float dtt, A, al, Alast;
+  float dtt, al;
 };
 
 __device__ __forceinline__ ChunkCtl chunk_controls(float dtv, float al, float lam, bool has_lambda, int nv) {
@@ -115,33 +89,32 @@ __device__ __forceinline__ ChunkCtl chunk_controls(float dtv, float al, float la
   ChunkCtl k;
   const float s_eff = has_lambda ? step_factor(lam, al) : 1.0f;
   k.dtt = (lane < nv) ? dtv * s_eff : 0.0f;
-  k.A = wave_inclusive_sum(k.dtt);
-  k.Alast = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(k.A), 63));
   k.al = al;
   return k;
 }
 
 // Per-(token, mode) weights of one chunk, pair = t * MP + m, written to the
-// role's LDS arrays w[i * MP * Q + m * Q + t].  Returns the modes whose chunk
-// decay exceeds the factorisation bound (bit m).
-//   state: 0 c e^{-rA}, 1 kappa e^{rA} (safe), 2 r c e^{-rA}, 3 r w rho e^{rA} (safe),
-//          4 c e^{-rA} E, 5 kappa e^{-r(A_Q-A)} upd, 6 c, 7 kappa, 8 r w rho
-//   rows:  0 kappa e^{-r(A_Q-A)} E, 1 r w rho e^{-r(A_Q-A)} E, 2 c e^{-rA} upd
-//   cols:  0 kappa e^{-r(A_Q-A)} E, 1 c e^{-rA} upd
+// role's LDS arrays w[i * MP * Q + m * Q + t], from the chunk log-decays l (hi and
+// lo parts lh, ll).  Returns the modes whose chunk decay exceeds the factorisation
+// bound (bit m); for those the Gamma arrays hold c and kappa without the exponentials.
+//   state: 0 c e^{-l} (c), 1 kappa e^{l} (kappa), 2 c e^{-l} E, 3 kappa e^{-(l_Q-l)} upd
+//   rows:  0 kappa e^{-(l_Q-l)} E, 1 e^{-(l_Q-l)} E, 2 c e^{-l} upd
+//   cols:  0 kappa e^{-(l_Q-l)} E, 1 c e^{-l} upd
+//   intra: 0 c e^{-l} (c), 1 kappa e^{l} (kappa)
 // (the reverse sweeps read their Gamma tiles from the state sweep)
 // E is the scale of the state (or adjoint) before this chunk's update, upd the
 // factor on the update (1/E_new, or 1 when the accumulators are folded back).
-template <int MP, int ROLE>
-__device__ __forceinline__ int pair_weights(const ChunkCtl& k, int nv, int M, const PairLogits<MP, 512>& lgt,
-                                            bool w_is_c, const float* s_rr, const float* s_lnt, const float* Ecur,
-                                            float* Enext, float* w) {
+template <int MP, int ROLE, int NT = 512>
+__device__ __forceinline__ int pair_weights(const ChunkCtl& k, int nv, int M, const PairLogits<MP, NT>& lgt,
+                                            bool w_is_c, const float* s_rr, const float* s_lnt, const float* lh,
+                                            const float* ll, const float* Ecur, float* Enext, float* w) {
   const int tid = threadIdx.x;
 #pragma unroll
   for (int j = 0; j < lgt.NPR; ++j) {
-    const int pr = tid + 512 * j;
+    const int pr = tid + NT * j;
     if (pr >= kQ * MP) break;  // wave-uniform
     const int t = pr / MP, m = pr - t * MP;
-    const float A = __shfl(k.A, t, 64), dtt = __shfl(k.dtt, t, 64), al = __shfl(k.al, t, 64);
+    const float dtt = __shfl(k.dtt, t, 64), al = __shfl(k.al, t, 64);
     const bool valid = t < nv;
     const float r = s_rr[m], prior = -al * s_lnt[m];
     const float zc = (m < M) ? prior + lgt.rl[j] : -INFINITY;
@@ -149,75 +122,73 @@ __device__ __forceinline__ int pair_weights(const ChunkCtl& k, int nv, int M, co
     // tokens past the sequence get zero weights (their tile rows may hold anything finite)
     const float cw = valid ? group_softmax<MP>(zc) : 0.0f;
     const float ww = w_is_c ? cw : (valid ? group_softmax<MP>(zw) : 0.0f);
-    const float xr = r * k.Alast;
-    const bool safe = xr <= kSafeExponent;
-    const float E = Ecur[m];
-    const float Enew = E * fexp(-xr);
-    const bool ren = !(Enew >= kRescaleFloor);
-    const float upd = ren ? 1.0f : __frcp_rn(Enew);
-    const float beta = one_minus_exp_neg(dtt * r);
-    const float kap = beta * ww;
-    const float ea = fexp(-r * A);
-    const float ep = (ROLE == kState && safe) ? fexp(r * A) : 0.0f;
-    const float dec = fdecay(r, k.Alast - A);
+    const float lt = lh[m * kWQ + t], lQ = lh[m * kWQ + kQ - 1];
+    const bool safe = lQ <= kSafeExponent;
+    const float kap = one_minus_exp_neg(dtt * r) * ww;
+    const float ea = fexp(-lt);
     float* o = w + m * kWQ + t;
     constexpr int SW = MP * kWQ;  // stride of the weight arrays
-    if constexpr (ROLE == kState) {
-      const float rwr = r * ww * (1.0f - beta);
-      o[0 * SW] = cw * ea;
-      o[1 * SW] = kap * ep;
-      o[2 * SW] = r * cw * ea;
-      o[3 * SW] = rwr * ep;
-      o[4 * SW] = cw * ea * E;
-      o[5 * SW] = kap * dec * upd;
-      o[6 * SW] = cw;
-      o[7 * SW] = kap;
-      o[8 * SW] = rwr;
-    } else if constexpr (ROLE == kRows) {
-      o[0 * SW] = kap * dec * E;
-      o[1 * SW] = r * ww * (1.0f - beta) * dec * E;
-      o[2 * SW] = cw * ea * upd;
-    } else {
-      o[0 * SW] = kap * dec * E;
-      o[1 * SW] = cw * ea * upd;
+    if constexpr (ROLE == kState || ROLE == kIntra) {
+      o[0 * SW] = safe ? cw * ea : cw;
+      o[1 * SW] = safe ? kap * fexp(lt) : kap;
     }
-    if (pr < MP) Enext[m] = ren ? 1.0f : Enew;
+    if constexpr (ROLE != kIntra) {
+      const float E = Ecur[m];
+      const float Enew = E * fexp(-lQ);
+      const bool ren = !(Enew >= kRescaleFloor);
+      const float upd = ren ? 1.0f : __frcp_rn(Enew);
+      const float dec = ell_decay(lh + m * kWQ, ll + m * kWQ, kQ - 1, t);
+      if constexpr (ROLE == kState) {
+        o[2 * SW] = cw * ea * E;
+        o[3 * SW] = kap * dec * upd;
+      } else if constexpr (ROLE == kRows) {
+        o[0 * SW] = kap * dec * E;
+        o[1 * SW] = dec * E;
+        o[2 * SW] = cw * ea * upd;
+      } else {
+        o[0 * SW] = kap * dec * E;
+        o[1 * SW] = cw * ea * upd;
+      }
+      if (pr < MP) Enext[m] = ren ? 1.0f : Enew;
+    }
   }
   // the same flags in every wave: lane m < MP tests mode m
   const int lane = tid & 63;
-  const bool over = lane < MP && lane < M && !(s_rr[lane < MP ? lane : 0] * k.Alast <= kSafeExponent);
-  return (int)(__ballot(over) & ((1ull << MP) - 1));
+  const bool over = lane < MP && lane < M && !(lh[(lane < MP ? lane : 0) * kWQ + kQ - 1] <= kSafeExponent);
+  return (int)(__ballot(over) & ((MP >= 32) ? 0xffffffffull : ((1ull << MP) - 1)));
 }
 
 // Rank-M product sum_m a[m][row0 + i] b[m][col0 + j] over a 16x16 tile
-// (float32 matrix cores, modes as K), in the accumulator layout.
+// (float32 matrix cores, modes as K), in the accumulator layout, over the modes
+// whose bit in `unsafe` is clear.
 template <int MP>
-__device__ __forceinline__ floatx4 rank_m_tile(const float* a, const float* bm, int row0, int col0, int tid = threadIdx.x) {
+__device__ __forceinline__ floatx4 rank_m_tile(const float* a, const float* bm, int row0, int col0, int unsafe,
+                                               int tid = threadIdx.x) {
   const int li = tid & 15, lg = (tid >> 4) & 3;
   floatx4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
   for (int q = 0; q < (MP + 3) / 4; ++q) {
     const int m = q * 4 + lg;
-    const float av = (m < MP) ? a[m * kWQ + row0 + li] : 0.0f;
-    const float bv = (m < MP) ? bm[m * kWQ + col0 + li] : 0.0f;
-    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av, bv, acc, 0, 0, 0);
+    const bool ok = m < MP && !((unsafe >> (m < MP ? m : 0)) & 1);
+    const float av = (m < MP) ? a[(m < MP ? m : 0) * kWQ + row0 + li] : 0.0f;
+    const float bv = (m < MP) ? bm[(m < MP ? m : 0) * kWQ + col0 + li] : 0.0f;
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(ok ? av : 0.0f, ok ? bv : 0.0f, acc, 0, 0, 0);
   }
   return acc;
 }
 
 // Modes past the factorisation bound: add the pairwise-decay terms of
-// sum_m a_m[t] b_m[k] s_m e^{-r_m (A_t - A_k)} (t >= k) to a 16x16 tile.
+// sum_m a_m[t] b_m[k] e^{-(l_{t,m} - l_{k,m})} (t >= k) to a 16x16 tile.
 template <int MP>
-__device__ __forceinline__ void unsafe_terms(floatx4& acc, int unsafe, const float* a, const float* bm, const float* A,
-                                             const float* s_rr, int tb, int kb, bool scale_r, int tid = threadIdx.x) {
+__device__ __forceinline__ void unsafe_terms(floatx4& acc, int unsafe, const float* a, const float* bm,
+                                             const float* lh, const float* ll, int tb, int kb, int tid = threadIdx.x) {
   const int li = tid & 15, lg = (tid >> 4) & 3;
   for (int m = 0; m < MP; ++m) {
     if (!((unsafe >> m) & 1)) continue;
-    const float rm = s_rr[m];
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       const int t = tb * 16 + lg * 4 + r, k = kb * 16 + li;
-      if (t >= k) acc[r] += (scale_r ? rm : 1.0f) * a[m * kWQ + t] * bm[m * kWQ + k] * fdecay(rm, A[t] - A[k]);
+      if (t >= k) acc[r] += a[m * kWQ + t] * bm[m * kWQ + k] * ell_decay(lh + m * kWQ, ll + m * kWQ, t, k);
     }
   }
 }
@@ -295,13 +266,10 @@ struct BwdWork {
   void* hg;           // Gamma o (dY X^T), the same layout
   void* dBp;          // per-head dB, [B, L, H, N]
   void* dCp;          // per-head dC
-  float* eA;          // [2][B H L] readout / intra part of e (per N half)
-  float* fA;          // [2][B H L] intra part of f (per N half)
-  float* eB;          // [2][B H L] adjoint part of e (per P half)
-  float* fB;          // [2][B H L] adjoint part of f
-  float* F;           // [2][B H] final-state term (per N half)
+  float* dc;          // [slots][B H L][M] partials of dL/dc: state sweep (per N part), then the intra kernel
+  float* dk;          // [slots][B H L][M] partials of dL/dkappa: rows sweep (per P part), then the intra kernel
+  float* F;           // [PS][B H][M] <dS_final, S_final> per mode (per N part)
   float* dDp;         // [B H] sum(dy . x)
-  float* tsum;        // [B H][L / 64] totals of e over 64-token tiles
 };
 
 // ------------------------------------------------ state / cols sweep layout
@@ -347,24 +315,20 @@ __global__ void __launch_bounds__(512) frac_bwd_state_kernel(ScanParams p, BwdWo
   __shared__ __align__(16) T Cb[64 * CS];
   constexpr int NWA = n_weight_arrays<kState>();
   constexpr int oHG = 0;                                         // T [k][t] (Gamma o dY X^T)^T, causal
-  constexpr int WSZ = NWA * MP * kWQ + kQ;                        // one chunk's weights [NWA][MP][Q], A [Q]
+  constexpr int WSZ = (NWA + 2) * MP * kWQ;                      // one chunk's weights and log-decays
   // two chunks' weights (the next one formed during this one's update) when LDS allows
   constexpr int kTileBytes = (Cfg::NBUF * 64 * (2 * XS + BS) + 64 * CS) * (int)sizeof(T);
-  constexpr int kFixed = 64 * XS * (int)sizeof(T) + (3 * kTiles * 16 + 8 * kQ + Ex::kFloats + 4 * MP) * 4;
+  constexpr int kFixed = 64 * XS * (int)sizeof(T) + (8 * MPF * kQ + Ex::kFloats + 4 * MP) * 4;
   constexpr int NWB = kTileBytes + kFixed + 2 * WSZ * 4 <= 160 * 1024 - 512 ? 2 : 1;
   constexpr int oW = oHG + 64 * XS * (int)sizeof(T);             // float weights, NWB chunks
-  constexpr int oSl = oW + NWB * WSZ * 4;                        // float slots R, C, F [10][16] each
-  constexpr int oRd = oSl + 3 * kTiles * 16 * 4;                 // float [8][Q] per-wave token partials
-  constexpr int oEx = oRd + 8 * kQ * 4;                          // float exchange
+  constexpr int oRd = oW + NWB * WSZ * 4;                        // float [8 waves][MPF][Q] token partials
+  constexpr int oEx = oRd + 8 * MPF * kQ * 4;                    // float exchange
   constexpr int oSc = oEx + Ex::kFloats * 4;                     // float rates, log tau, scales
   __shared__ __align__(16) unsigned char sm[oSc + 4 * MP * 4];
   T* HGT = reinterpret_cast<T*>(sm + oHG);
   float* const W0 = reinterpret_cast<float*>(sm + oW);
   float* const W1 = W0 + (NWB - 1) * WSZ;
-  float* slotR = reinterpret_cast<float*>(sm + oSl);
-  float* slotC = slotR + kTiles * 16;
-  float* slotF = slotC + kTiles * 16;
-  float* redR = reinterpret_cast<float*>(sm + oRd);
+  float* redZ = reinterpret_cast<float*>(sm + oRd);
   float* XCH = reinterpret_cast<float*>(sm + oEx);
   float* s_rr = reinterpret_cast<float*>(sm + oSc);
   float* s_lnt = s_rr + MP;
@@ -453,20 +417,21 @@ __global__ void __launch_bounds__(512) frac_bwd_state_kernel(ScanParams p, BwdWo
   TilePrefetch<T> gtile;  // C B^T tile values, loaded one chunk ahead
   gtile.load(gtiles + ((int64_t)b * nchunks * G + g) * (kTiles * kTileElems), wave, lane);
   T* dCp = reinterpret_cast<T*>(wk.dCp);
-  const int64_t bl_h = (int64_t)p.Bsz * L * H;
+  const int64_t bh_i = (int64_t)b * H + h;
+  float* dcg = wk.dc + ((int64_t)ps * p.Bsz * H * L + bh_i * L) * M;  // this head's dc partial [L][M]
 
   // Per-(token, mode) weights of chunk c into Wd, from the controls in dt_n, al_n,
   // lam_n.  Chunk c + 1's weights are formed at the end of chunk c's step, so that
   // their latency overlaps that step's state update.
-  float alast_c = 0.0f;  // chunk total of the effective steps
-  int unsafe_c = 0;      // modes past the factorisation bound
+  int unsafe_c = 0;  // modes past the factorisation bound
   auto weights = [&](int c, float* Wd) __attribute__((always_inline)) {
     const int t0 = c * kQ, nv = min(kQ, L - t0);
     const ChunkCtl k = chunk_controls(dt_n, al_n, lam_n, lm_bh != nullptr, nv);
-    if (wave == 0) Wd[NWA * MP * kWQ + lane] = k.A;
-    unsafe_c = pair_weights<MP, kState>(k, nv, M, lgt_n, rl_bh == wl_bh, s_rr, s_lnt, s_E2 + (c & 1) * MP,
-                                        s_E2 + ((c + 1) & 1) * MP, Wd);
-    alast_c = k.Alast;
+    float* lh = Wd + NWA * SW;
+    chunk_log_decays<MP, 8>(k.dtt, s_rr, lh, lh + SW);
+    barrier();  // log-decays in LDS
+    unsafe_c = pair_weights<MP, kState>(k, nv, M, lgt_n, rl_bh == wl_bh, s_rr, s_lnt, lh, lh + SW,
+                                        s_E2 + (c & 1) * MP, s_E2 + ((c + 1) & 1) * MP, Wd);
   };
   barrier();  // rates and scales in LDS
   if constexpr (NWB == 2) weights(0, W0);
@@ -477,16 +442,12 @@ __global__ void __launch_bounds__(512) frac_bwd_state_kernel(ScanParams p, BwdWo
     // lane-derived addresses recomputed per chunk rather than held across the loop
     const int tid = fresh_tid(), lane = tid & 63, li = lane & 15, lg = lane >> 4;
     const float* Ecur = s_E2 + (c & 1) * MP;
-    const float* P_O = W;
-    const float* P_Vt = W + 1 * SW;
-    const float* P_rO = W + 2 * SW;
-    const float* P_Y = W + 3 * SW;
-    const float* P_wdc = W + 4 * SW;  // times r_m: the readout weight of e
-    const float* P_v = W + 5 * SW;
-    const float* P_c = W + 6 * SW;
-    const float* P_k = W + 7 * SW;
-    const float* P_wr = W + 8 * SW;
-    const float* P_A = W + NWA * MP * kWQ;
+    const float* P_O = W;             // c e^{-l} (c past the factorisation bound)
+    const float* P_Vt = W + 1 * SW;   // kappa e^{l} (kappa)
+    const float* P_wdc = W + 2 * SW;  // c e^{-l} E: the readout weight of dC
+    const float* P_v = W + 3 * SW;
+    const float* P_lh = W + NWA * SW;
+    const float* P_ll = P_lh + SW;
     wait_vmem();
     barrier();  // this chunk's tiles and weights have landed; the previous chunk is done
     const TilePrefetch<T> gcur = gtile.pinned_copy();  // before any new memory operation
@@ -506,14 +467,13 @@ __global__ void __launch_bounds__(512) frac_bwd_state_kernel(ScanParams p, BwdWo
     int renbits = 0;
 #pragma unroll
     for (int m = 0; m < MPF; ++m) {
-      const float Enew = uniform(Ecur[mo + m] * fexp(-s_rr[mo + m] * alast_c));
+      const float Enew = uniform(Ecur[mo + m] * fexp(-P_lh[(mo + m) * kWQ + kQ - 1]));
       renf[m] = Enew;
       if (__float_as_int(Enew) < __float_as_int(kRescaleFloor)) renbits |= 1 << m;
     }
 
     __builtin_amdgcn_sched_barrier(0);
-    // ---- intra-chunk tiles: HG = Gamma o D (LDS, transposed), row / column sums of
-    // H o Phi and column sums of H o Psi (first workgroup of the head only)
+    // ---- intra-chunk tiles: HG = Gamma o D (LDS, transposed); the tiles of the reverse sweeps
     {
 #pragma unroll
       for (int jt = 0; jt < 2; ++jt) {
@@ -521,8 +481,8 @@ __global__ void __launch_bounds__(512) frac_bwd_state_kernel(ScanParams p, BwdWo
         if (tile >= kTiles) break;
         const int tb = tile_row(tile), kb = tile_col(tile);
         const floatx4 D = dyx_tile<T, XS>(Yc, Xc, tb, kb, tid);
-        floatx4 Gm = rank_m_tile<MP>(P_O, P_Vt, tb * 16, kb * 16, tid);
-        if (unsafe) unsafe_terms<MP>(Gm, unsafe, P_c, P_k, P_A, s_rr, tb, kb, false, tid);
+        floatx4 Gm = rank_m_tile<MP>(P_O, P_Vt, tb * 16, kb * 16, unsafe, tid);
+        if (unsafe) unsafe_terms<MP>(Gm, unsafe, P_O, P_Vt, P_lh, P_ll, tb, kb, tid);
         float hv[4];
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
@@ -546,31 +506,6 @@ __global__ void __launch_bounds__(512) frac_bwd_state_kernel(ScanParams p, BwdWo
           }
           if (ps == Cfg::PS - 1) store4(reinterpret_cast<T*>(wk.hg) + to, floatx4{hv[0], hv[1], hv[2], hv[3]});
         }
-        if (tile % Cfg::PS == ps) {  // the two halves of N share the tile sums
-          floatx4 Ph = rank_m_tile<MP>(P_rO, P_Vt, tb * 16, kb * 16, tid);
-          floatx4 Ps = rank_m_tile<MP>(P_O, P_Y, tb * 16, kb * 16, tid);
-          if (unsafe) {
-            unsafe_terms<MP>(Ph, unsafe, P_c, P_k, P_A, s_rr, tb, kb, true, tid);
-            unsafe_terms<MP>(Ps, unsafe, P_c, P_wr, P_A, s_rr, tb, kb, false, tid);
-          }
-          float rv[4], ce = 0.f, cf = 0.f;
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const int t = tb * 16 + lg * 4 + r, kk = kb * 16 + li;
-            const float hm = keep_if_ge(gcur.get(jt, r) * D[r], t, kk);
-            rv[r] = hm * Ph[r];
-            ce += hm * Ph[r];
-            cf += hm * Ps[r];
-          }
-          const float rs = reduce16_4(rv, li);
-          if ((li & 3) == 0) slotR[tile * 16 + lg * 4 + ((li >> 2) & 3)] = rs;
-          ce = xor32_sum(xor16_sum(ce));
-          cf = xor32_sum(xor16_sum(cf));
-          if (lg == 0) {
-            slotC[tile * 16 + li] = ce;
-            slotF[tile * 16 + li] = cf;
-          }
-        }
       }
     }
 
@@ -578,13 +513,13 @@ __global__ void __launch_bounds__(512) frac_bwd_state_kernel(ScanParams p, BwdWo
 
     __builtin_amdgcn_sched_barrier(0);
     // ---- readout side of the state entering the chunk, transposed: U^T_m = S_m dY^T
-    // (rows n of this wave's block, columns t), dC^T (inter) and the readout part of e
+    // (rows n of this wave's block, columns t), dC^T (inter) and per mode
+    // z_{t,m} = C_t . (S_m dy_t) over this wave's rows of N
     floatx4 dCa[4];  // dC^T: rows n = 16 nb + 4 lg + r, column t = 16 tb + li
 #pragma unroll
     for (int tb = 0; tb < 4; ++tb) dCa[tb] = floatx4{0.f, 0.f, 0.f, 0.f};
-    {
-      float racc[4] = {0.f, 0.f, 0.f, 0.f};  // per row block: this lane's token
-      if (active) {
+    if (active) {
+      {
         Frag<T> Sa[MPF][2];
 #pragma unroll
         for (int m = 0; m < MPF; ++m)
@@ -599,60 +534,38 @@ __global__ void __launch_bounds__(512) frac_bwd_state_kernel(ScanParams p, BwdWo
         for (int tb = 0; tb < 4; ++tb) {
           const T* row = Yc + (tb * 16 + li) * XS + lg * 4;
           const Frag<T> y0 = frag_load4x2(row, row + 16), y1 = frag_load4x2(row + 32, row + 48);
-          floatx4 ws = {0.f, 0.f, 0.f, 0.f};
+          const T* crow = Cb + (tb * 16 + li) * CS + nb * 16 + lg * 4;
+          float cv[4];
+          load4(crow, cv);
 #pragma unroll
           for (int m = 0; m < MPF; ++m) {
             floatx4 U = {0.f, 0.f, 0.f, 0.f};
             mma(U, Sa[m][0], y0);
             mma(U, Sa[m][1], y1);
             const float wd = P_wdc[(mo + m) * kWQ + tb * 16 + li];
-            const float rm = s_rr[mo + m];
 #pragma unroll
-            for (int r = 0; r < 4; ++r) {
-              const float v = wd * U[r];
-              dCa[tb][r] += v;
-              ws[r] += rm * v;
-            }
+            for (int r = 0; r < 4; ++r) dCa[tb][r] += wd * U[r];
+            // z over this lane's 4 rows of N, then over the 4 lane groups (16 rows)
+            const float z = xor32_sum(xor16_sum(U[0] * cv[0] + U[1] * cv[1] + U[2] * cv[2] + U[3] * cv[3]));
+            if (lg == 0) redZ[(wave * MPF + m) * kQ + tb * 16 + li] = z;
           }
-          // sum over n of C_t[n] ws[n]: this lane's 4 values, then the 4 lane groups
-          const T* crow = Cb + (tb * 16 + li) * CS + nb * 16 + lg * 4;
-          float cv[4];
-          load4(crow, cv);
-          racc[tb] = ws[0] * cv[0] + ws[1] * cv[1] + ws[2] * cv[2] + ws[3] * cv[3];
         }
         if (Cfg::NACT > 1) Ex::put(XCH, wave, part, dCa);
       }
-#pragma unroll
-      for (int tb = 0; tb < 4; ++tb) {
-        float v = racc[tb];
-        v = xor32_sum(xor16_sum(v));
-        if (lg == 0) redR[wave * kQ + tb * 16 + li] = v;
-      }
     }
-    barrier();  // HG, slots, token partials and exchange complete; C is free
+    barrier();  // HG, token partials and exchange complete; C is free
     if (Cfg::NBUF == 2 && c + 1 < nchunks) stageC(c + 1);
 
-    if (wave == 0) {
-      // token t: readout part (all waves) [+ row sums of its row-block tiles - column
-      // sums of its column-block tiles], fixed order
-      const int t = lane, tbt = t >> 4, tr = t & 15;
-      float er = 0.f, ec = 0.f, ef = 0.f;
-      for (int w2 = 0; w2 < 8; ++w2) er += redR[w2 * kQ + t];
-      for (int kb2 = 0; kb2 <= tbt; ++kb2) {
-        const int tile = tbt * (tbt + 1) / 2 + kb2;
-        if (tile % Cfg::PS == ps) er += slotR[tile * 16 + tr];
-      }
-      for (int tb2 = tbt; tb2 < 4; ++tb2) {
-        const int tile = tb2 * (tb2 + 1) / 2 + tbt;
-        if (tile % Cfg::PS == ps) {
-          ec += slotC[tile * 16 + tr];
-          ef += slotF[tile * 16 + tr];
-        }
-      }
-      if (t < nv) {
-        const int64_t ith = ((int64_t)b * H + h) * L + t0 + t;  // [B, H, L]: one head's tokens contiguous
-        wk.eA[ps * bl_h + ith] = er - ec;
-        wk.fA[ps * bl_h + ith] = ef;
+    // ---- the state part of dL/dc over this workgroup's rows of N:
+    // e^{-l_t} E_m sum over the N blocks (in order) of z
+    for (int i = tid; i < kQ * MP; i += 512) {
+      const int t = i / MP, m = i - t * MP;
+      if (m < M && t < nv) {
+        const int pt = m / MPF, j = m - pt * MPF;
+        float z = 0.0f;
+#pragma unroll
+        for (int q = 0; q < NBF; ++q) z += redZ[((pt * NBF + q) * MPF + j) * kQ + t];
+        dcg[(int64_t)(t0 + t) * M + m] = fexp(-P_lh[m * kWQ + t]) * Ecur[m] * z;
       }
     }
     if (ps == 0 && p.dD) {
@@ -739,37 +652,49 @@ __global__ void __launch_bounds__(512) frac_bwd_state_kernel(ScanParams p, BwdWo
   wait_vmem();
   barrier();
 
-  // ---- final-state term sum_m r_m <dS_final_m, S_final_m> and sum(dy . x)
-  float fpart = 0.0f;
+  // ---- final-state term <dS_final_m, S_final_m> per mode over this workgroup's rows of N,
+  // and sum(dy . x); per wave over its lanes, then over the waves in order
+  float fpart[MPF];
+#pragma unroll
+  for (int m = 0; m < MPF; ++m) fpart[m] = 0.0f;
   if (p.d_final_state && active) {
     const float* Ef = s_E2 + (nchunks & 1) * MP;
     int lo = ncol * P + lg * 4;
     asm volatile("" : "+v"(lo));
 #pragma unroll
     for (int m = 0; m < MPF; ++m) {
-      const float scale = (mo + m < M) ? s_rr[mo + m] * Ef[mo + m] : 0.0f;
+      const float scale = (mo + m < M) ? Ef[mo + m] : 0.0f;
 #pragma unroll
       for (int pb = 0; pb < 4; ++pb)
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int pr = pb * 16 + lg * 4 + r;
           if (mo + m < M && ncol < N && pr < P)
-            fpart += scale * S[m][pb][r] * p.d_final_state[sbase + (int64_t)(mo + m) * N * P + lo + pb * 16 + r];
+            fpart[m] += scale * S[m][pb][r] * p.d_final_state[sbase + (int64_t)(mo + m) * N * P + lo + pb * 16 + r];
         }
     }
   }
-  float* red = reinterpret_cast<float*>(sm + oW);  // the weights are no longer needed
-  red[tid] = fpart;
-  red[512 + tid] = dd_acc;
+  float* red = redZ;  // the token partials are no longer needed
+#pragma unroll
+  for (int m = 0; m < MPF; ++m) {
+    const float v = group_allreduce<64>(fpart[m], [](float x, float y) { return x + y; });
+    if (lane == 0) red[wave * MPF + m] = v;
+  }
+  {
+    const float v = group_allreduce<64>(dd_acc, [](float x, float y) { return x + y; });
+    if (lane == 0) red[8 * MPF + wave] = v;
+  }
   barrier();
-  if (tid == 0) {
-    float fs = 0.f, ds = 0.f;
-    for (int i = 0; i < 512; ++i) {
-      fs += red[i];
-      ds += red[512 + i];
-    }
-    wk.F[(int64_t)ps * p.Bsz * H + (int64_t)b * H + h] = fs;
-    if (ps == 0) wk.dDp[(int64_t)b * H + h] = ds;
+  if (tid < M) {  // mode tid: the waves holding it, N blocks in order
+    const int pt = tid / MPF, j = tid - pt * MPF;
+    float fs = 0.f;
+    for (int q = 0; q < NBF; ++q) fs += red[(pt * NBF + q) * MPF + j];
+    wk.F[((int64_t)ps * p.Bsz * H + bh_i) * M + tid] = fs;
+  }
+  if (tid == 0 && ps == 0) {
+    float ds = 0.f;
+    for (int w2 = 0; w2 < 8; ++w2) ds += red[8 * MPF + w2];
+    wk.dDp[bh_i] = ds;
   }
 }
 
@@ -797,12 +722,13 @@ __global__ void __launch_bounds__(512) frac_bwd_cols_kernel(ScanParams p, BwdWor
   constexpr int NWA = n_weight_arrays<kCols>();
   constexpr int oHG = 0;                                         // T [t][k] Gamma o dY X^T, causal
   constexpr int oW = oHG + 64 * XS * (int)sizeof(T);
-  constexpr int oEx = oW + (NWA * MP * kWQ + kQ) * 4;
+  constexpr int oEx = oW + (NWA + 2) * MP * kWQ * 4;
   constexpr int oSc = oEx + Ex::kFloats * 4;
   __shared__ __align__(16) unsigned char sm[oSc + 4 * MP * 4];
   T* HG = reinterpret_cast<T*>(sm + oHG);
   float* W = reinterpret_cast<float*>(sm + oW);
-  float* P_A = W + NWA * MP * kWQ;
+  float* P_lh = W + NWA * MP * kWQ;  // chunk log-decays, hi and lo parts
+  float* P_ll = P_lh + MP * kWQ;
   float* XCH = reinterpret_cast<float*>(sm + oEx);
   float* s_rr = reinterpret_cast<float*>(sm + oSc);
   float* s_lnt = s_rr + MP;
@@ -905,13 +831,14 @@ __global__ void __launch_bounds__(512) frac_bwd_cols_kernel(ScanParams p, BwdWor
     }
     if (c > 0) load_controls(c - 1, dt_n, al_n, lam_n);
     const ChunkCtl k = chunk_controls(dtv, al_l, lam_l, lm_bh != nullptr, nv);
-    if (wave == 0) P_A[lane] = k.A;
-    const int unsafe = pair_weights<MP, kCols>(k, nv, M, lgt, rl_bh == wl_bh, s_rr, s_lnt, Ecur, Enext, W);
+    chunk_log_decays<MP, 8>(k.dtt, s_rr, P_lh, P_ll);
+    barrier();  // log-decays in LDS
+    const int unsafe = pair_weights<MP, kCols>(k, nv, M, lgt, rl_bh == wl_bh, s_rr, s_lnt, P_lh, P_ll, Ecur, Enext, W);
     float renf[MPF];
     int renbits = 0;
 #pragma unroll
     for (int m = 0; m < MPF; ++m) {
-      const float Enew = uniform(Ecur[mo + m] * fexp(-s_rr[mo + m] * k.Alast));
+      const float Enew = uniform(Ecur[mo + m] * fexp(-P_lh[(mo + m) * kWQ + kQ - 1]));
       renf[m] = Enew;
       if (__float_as_int(Enew) < __float_as_int(kRescaleFloor)) renbits |= 1 << m;
     }
@@ -1081,23 +1008,23 @@ __global__ void __launch_bounds__(512) frac_bwd_rows_kernel(ScanParams p, BwdWor
   constexpr int oGG = 0;                                         // T [t'][k] (C B^T) o Gamma, causal
   constexpr int oDx = oGG + 64 * XS * (int)sizeof(T);            // T [t][p] dx rows of the previous chunk (bf16)
   constexpr int oW = oDx + (Cfg::kBf16 ? 64 * XS * (int)sizeof(T) : 0);
-  constexpr int oRd = oW + (NWA * MP * kWQ + kQ) * 4;             // float [2][8][Q] token partials of e, f
-  constexpr int oEx = oRd + 2 * 8 * kQ * 4;
+  constexpr int oRd = oW + (NWA + 2) * MP * kWQ * 4;             // float [8 waves][MPW][Q] token partials
+  constexpr int oEx = oRd + 8 * MPW * kQ * 4;
   constexpr int oSc = oEx + Ex::kFloats * 4;
   __shared__ __align__(16) unsigned char sm[oSc + 4 * MP * 4];
   T* GG = reinterpret_cast<T*>(sm + oGG);
   T* Dxb = reinterpret_cast<T*>(sm + oDx);
   float* W = reinterpret_cast<float*>(sm + oW);
-  float* P_A = W + NWA * MP * kWQ;
-  float* redE = reinterpret_cast<float*>(sm + oRd);
-  float* redF = redE + 8 * kQ;
+  float* P_lh = W + NWA * MP * kWQ;  // chunk log-decays, hi and lo parts
+  float* P_ll = P_lh + MP * kWQ;
+  float* redW = reinterpret_cast<float*>(sm + oRd);
   float* XCH = reinterpret_cast<float*>(sm + oEx);
   float* s_rr = reinterpret_cast<float*>(sm + oSc);
   float* s_lnt = s_rr + MP;
   float* s_E2 = s_lnt + MP;
   constexpr int SW = MP * kWQ;  // stride of the weight arrays
-  const float* P_wdx = W;  // times r_m: the adjoint weight of e
-  const float* P_wfk = W + 1 * SW;
+  const float* P_wdx = W;          // kappa e^{-(l_Q-l)} E: the adjoint weight of dx
+  const float* P_dE = W + 1 * SW;   // e^{-(l_Q-l)} E: the adjoint weight of dL/dkappa
   const float* P_om = W + 2 * SW;
 
   if (tid < MP) {
@@ -1195,7 +1122,7 @@ __global__ void __launch_bounds__(512) frac_bwd_rows_kernel(ScanParams p, BwdWor
   }
   // (C B^T) o Gamma tiles written by the state sweep, loaded one chunk ahead (in processing order)
   const T* ggtiles = reinterpret_cast<const T*>(wk.gg);
-  const int64_t bl_h = (int64_t)p.Bsz * L * H;
+  float* dkg = wk.dk + ((int64_t)ps * p.Bsz * H * L + ((int64_t)b * H + h) * L) * M;  // this head's dk partial [L][M]
   TilePrefetch<T> ggt;
   ggt.load(ggtiles + ((int64_t)(b * nchunks + nchunks - 1) * H + h) * (kTiles * kTileElems), wave, lane);
 
@@ -1220,13 +1147,14 @@ __global__ void __launch_bounds__(512) frac_bwd_rows_kernel(ScanParams p, BwdWor
     }
     if (c > 0) load_controls(c - 1, dt_n, al_n, lam_n);
     const ChunkCtl k = chunk_controls(dtv, al_l, lam_l, lm_bh != nullptr, nv);
-    if (wave == 0) P_A[lane] = k.A;
-    const int unsafe = pair_weights<MP, kRows>(k, nv, M, lgt, rl_bh == wl_bh, s_rr, s_lnt, Ecur, Enext, W);
+    chunk_log_decays<MP, 8>(k.dtt, s_rr, P_lh, P_ll);
+    barrier();  // log-decays in LDS
+    const int unsafe = pair_weights<MP, kRows>(k, nv, M, lgt, rl_bh == wl_bh, s_rr, s_lnt, P_lh, P_ll, Ecur, Enext, W);
     float renf[MPW];
     int renbits = 0;
 #pragma unroll
     for (int m = 0; m < MPW; ++m) {
-      const float Enew = uniform(Ecur[mo + m] * fexp(-s_rr[mo + m] * k.Alast));
+      const float Enew = uniform(Ecur[mo + m] * fexp(-P_lh[(mo + m) * kWQ + kQ - 1]));
       renf[m] = Enew;
       if (__float_as_int(Enew) < __float_as_int(kRescaleFloor)) renbits |= 1 << m;
     }
@@ -1250,12 +1178,11 @@ __global__ void __launch_bounds__(512) frac_bwd_rows_kernel(ScanParams p, BwdWor
 
     __builtin_amdgcn_sched_barrier(0);
     // ---- Z^T_m = G_m^T B^T (rows p of this wave's block, columns t) -> dx^T (inter)
-    // and the adjoint parts of e, f
+    // and per mode w_{t,m} = (B_t^T G_m) . x_t over this wave's columns (and rows) of the adjoint
     floatx4 dxa[4];  // dx^T: rows p = 16 pb + 4 lg + r, column t = 16 tb + li
 #pragma unroll
     for (int tb = 0; tb < 4; ++tb) dxa[tb] = floatx4{0.f, 0.f, 0.f, 0.f};
     {
-      float ekf[4] = {0.f, 0.f, 0.f, 0.f}, fkf[4] = {0.f, 0.f, 0.f, 0.f};  // this lane's token, per row block
       if (active) {
 #pragma unroll
         for (int tp = 0; tp < 4 / TBP; ++tp) {
@@ -1267,9 +1194,6 @@ __global__ void __launch_bounds__(512) frac_bwd_rows_kernel(ScanParams p, BwdWor
               const T* row = Bb + ((tp * TBP + q) * 16 + li) * BS + nbo * 16 + kb * 32 + lg * 4;
               Ba[q][kb] = frag_load4x2(row, row + 16, 2 * kb + 1 < NBW);
             }
-          floatx4 We[TBP], Wf[TBP];
-#pragma unroll
-          for (int q = 0; q < TBP; ++q) We[q] = Wf[q] = floatx4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
           for (int m = 0; m < MPW; ++m) {
             Frag<T> Gf[KBW];
@@ -1280,59 +1204,44 @@ __global__ void __launch_bounds__(512) frac_bwd_rows_kernel(ScanParams p, BwdWor
 #pragma unroll
               for (int s = 0; s < 4; ++s) frag_set(Gf[kb], 4 + s, (2 * kb + 1 < NBW) ? Gs[m][2 * kb + 1][s] : 0.0f);
             }
-            const float rm = s_rr[mo + m];
 #pragma unroll
             for (int q = 0; q < TBP; ++q) {
               const int tb = tp * TBP + q;
               floatx4 Z = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
               for (int kb = 0; kb < KBW; ++kb) mma(Z, Gf[kb], Ba[q][kb]);
-              const int o = (mo + m) * kWQ + tb * 16 + li;
-              const float wx = P_wdx[o], wf = P_wfk[o], rwx = rm * wx;
+              const float wx = P_wdx[(mo + m) * kWQ + tb * 16 + li];
 #pragma unroll
-              for (int r = 0; r < 4; ++r) {
-                dxa[tb][r] = __builtin_fmaf(wx, Z[r], dxa[tb][r]);
-                We[q][r] = __builtin_fmaf(rwx, Z[r], We[q][r]);
-                Wf[q][r] = __builtin_fmaf(wf, Z[r], Wf[q][r]);
-              }
+              for (int r = 0; r < 4; ++r) dxa[tb][r] = __builtin_fmaf(wx, Z[r], dxa[tb][r]);
+              // w over this lane's 4 columns of P, then over the 4 lane groups (16 columns)
+              float xv[4];
+              load4(Xb + (tb * 16 + li) * XS + pb * 16 + lg * 4, xv);
+              const float wv = xor32_sum(xor16_sum(Z[0] * xv[0] + Z[1] * xv[1] + Z[2] * xv[2] + Z[3] * xv[3]));
+              if (lg == 0) redW[(wave * MPW + m) * kQ + tb * 16 + li] = wv;
             }
-          }
-#pragma unroll
-          for (int q = 0; q < TBP; ++q) {
-            const int tb = tp * TBP + q;
-            float xv[4];
-            load4(Xb + (tb * 16 + li) * XS + pb * 16 + lg * 4, xv);
-            ekf[tb] = We[q][0] * xv[0] + We[q][1] * xv[1] + We[q][2] * xv[2] + We[q][3] * xv[3];
-            fkf[tb] = Wf[q][0] * xv[0] + Wf[q][1] * xv[1] + Wf[q][2] * xv[2] + Wf[q][3] * xv[3];
           }
         }
         if (NPART > 1) Ex::put(XCH, wave, part, dxa);
-      }
-#pragma unroll
-      for (int tb = 0; tb < 4; ++tb) {
-        float e = ekf[tb], f = fkf[tb];
-        e = xor32_sum(xor16_sum(e));
-        f = xor32_sum(xor16_sum(f));
-        if (lg == 0) {
-          redE[wave * kQ + tb * 16 + li] = e;
-          redF[wave * kQ + tb * 16 + li] = f;
-        }
+      } else {
+        // waves without adjoint columns add nothing
+        for (int i2 = lane; i2 < MPW * kQ; i2 += 64) redW[wave * MPW * kQ + i2] = 0.0f;
       }
     }
     barrier();  // GG, exchange and token partials complete; B and x are free
     if (Cfg::NBUF == 2 && c > 0) stage_early(c - 1);
 
-    if (wave == 0) {
-      const int t = lane;
-      float e = 0.f, f = 0.f;
-      for (int w2 = 0; w2 < 8; ++w2) {
-        e += redE[w2 * kQ + t];
-        f += redF[w2 * kQ + t];
-      }
-      if (t < nv) {
-        const int64_t ith = ((int64_t)b * H + h) * L + t0 + t;  // [B, H, L]
-        wk.eB[ps * bl_h + ith] = e;
-        wk.fB[ps * bl_h + ith] = f;
+    // ---- the adjoint part of dL/dkappa over this workgroup's columns of P:
+    // e^{-(l_Q - l_t)} E_m times the sum over the waves holding mode m (in order) of w
+    for (int i2 = tid; i2 < kQ * MP; i2 += 512) {
+      const int t = i2 / MP, m = i2 - t * MP;
+      if (m < M && t < nv) {
+        float wsum = 0.0f;
+#pragma unroll
+        for (int w2 = 0; w2 < 8; ++w2) {
+          const int q = w2 / Cfg::NPW, mo2 = Cfg::kModeSplit ? q * MPW : 0;
+          if (q < NPART && m >= mo2 && m < mo2 + MPW) wsum += redW[(w2 * MPW + (m - mo2)) * kQ + t];
+        }
+        dkg[(int64_t)(t0 + t) * M + m] = P_dE[m * kWQ + t] * wsum;
       }
     }
     if (!active) return;
@@ -1407,104 +1316,154 @@ __global__ void __launch_bounds__(512) frac_bwd_rows_kernel(ScanParams p, BwdWor
   wait_vmem();
   barrier();
   if (Cfg::kBf16) store_dx(0);
+
+  // ---- the adjoint of the state before token 0 (this workgroup's columns of P)
+  if (p.dinit_state && active) {
+    const float* Ef = s_E2 + (nchunks & 1) * MP;
+    // lane offset kept opaque (as for the initial load) so that no per-element offset
+    // of this store is formed before, and held across, the sequence loop
+    int lo = (mo * N + nbo * 16 + lg * 4) * P + pc;
+    asm volatile("" : "+v"(lo));
+#pragma unroll
+    for (int m = 0; m < MPW; ++m)
+#pragma unroll
+      for (int jb = 0; jb < NBW; ++jb)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int n = (nbo + jb) * 16 + lg * 4 + r;
+          if (mo + m < M && n < N && pc < P)
+            p.dinit_state[sbase + lo + ((int64_t)m * N + jb * 16 + r) * P] = Gs[m][jb][r] * Ef[mo + m];
+        }
+  }
 }
 
-// ---------------------------------------------------------- finishing kernels
+// ------------------------------------------------------ intra-chunk parts
+//
+// The intra-chunk parts of dL/dc and dL/dkappa, one workgroup of four waves per
+// (batch, chunk, head), independent of every other chunk:
+//   dc_{t,m} += sum_{k<=t} H_{t,k} kappa_{k,m} e^{-(l_t - l_k)}
+//   dk_{k,m} += sum_{t>=k} H_{t,k} c_{t,m} e^{-(l_t - l_k)}
+//   H = (C B^T) o (dY X^T)   (causal)
+// as float32 matrix-core products e^{-l_t} (H kappa e^{l})_t and e^{l_k} (H^T c e^{-l})_k
+// for the modes whose chunk decay stays below the factorisation bound, one
+// exponential per pair for the others.
+template <typename T, int MP>
+__global__ void __launch_bounds__(256) frac_bwd_intra_kernel(ScanParams p, const T* __restrict__ gtiles,
+                                                             float* __restrict__ dc_out, float* __restrict__ dk_out) {
+  constexpr bool kBf16 = sizeof(T) == 2;
+  constexpr int XS = kBf16 ? 64 + 8 : 64 + 4;
+  constexpr int HS = kWQ;  // float H [t][k]
+  constexpr int MB = (MP + 15) / 16;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, li = lane & 15, lg = lane >> 4;
+  const int L = p.L, H = p.H, P = p.P, M = p.M, G = p.G;
+  const int nchunks = (L + kQ - 1) / kQ;
+  // block = (b, c, h), heads fastest: the heads of a group read the same C B^T tiles
+  const int h = (int)(blockIdx.x % H);
+  const int bc = (int)(blockIdx.x / H);
+  const int c = bc % nchunks, b = bc / nchunks;
+  const int g = h * G / H;
+  const int t0 = c * kQ, nv = min(kQ, L - t0);
 
-// ddt from the per-token terms: suffix sums over the sequence, in two steps with
-// a fixed summation order.  First the total of e over each 64-token tile of each
-// (batch, head); then one block of 16 waves per (batch, tile, 64 heads) forms, per head, the
-// sum over the later tiles, the suffix sums inside the tile (one wave per head,
-// lane = token), and writes ddt through LDS so that each token's heads are stored
-// contiguously.
+  __shared__ __align__(16) T Xs[64 * XS], Ys[64 * XS];
+  __shared__ __align__(16) float Hs[64 * HS];
+  __shared__ __align__(16) float W[4 * MP * kWQ];
+  __shared__ float s_rr[MP], s_lnt[MP];
+  float* P_O = W;                 // c e^{-l} (c past the factorisation bound)
+  float* P_Vt = W + MP * kWQ;     // kappa e^{l} (kappa)
+  float* P_lh = W + 2 * MP * kWQ; // chunk log-decays, hi and lo parts
+  float* P_ll = W + 3 * MP * kWQ;
 
-// e_t of one token: readout / intra parts minus adjoint parts (partials per half).
-__device__ __forceinline__ float ddt_e(const BwdWork& wk, int64_t blh, int64_t i, int nA, int nB) {
-  float e = 0.0f;
-  for (int q = 0; q < nA; ++q) e += wk.eA[q * blh + i];
-  for (int q = 0; q < nB; ++q) e -= wk.eB[q * blh + i];
-  return e;
-}
-
-__global__ void __launch_bounds__(256) frac_bwd_ddt_tiles_kernel(ScanParams p, BwdWork wk, float* tsum, int nA,
-                                                                 int nB) {
-  const int ntiles = (p.L + 63) / 64;
-  const int64_t wid = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);  // (b h) * ntiles + tile
-  const int lane = threadIdx.x & 63;
-  if (wid >= (int64_t)p.Bsz * p.H * ntiles) return;
-  const int64_t bh = wid / ntiles;
-  const int t = (int)(wid - bh * ntiles) * 64 + lane;
-  const int64_t blh = (int64_t)p.Bsz * p.L * p.H;
-  float e = t < p.L ? ddt_e(wk, blh, bh * p.L + t, nA, nB) : 0.0f;
-  e = group_allreduce<64>(e, [](float x, float y) { return x + y; });
-  if (lane == 0) tsum[wid] = e;
-}
-
-__global__ void __launch_bounds__(1024) frac_bwd_ddt_kernel(ScanParams p, BwdWork wk, const float* tsum, int nA,
-                                                           int nB, int nD) {
-  __shared__ float carry[64];
-  __shared__ float out[64][65];
-  const int L = p.L, H = p.H, ntiles = (L + 63) / 64;
-  const int b = blockIdx.x / ntiles, tile = blockIdx.x - b * ntiles, h0 = blockIdx.y * 64, t0 = tile * 64;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int nh = min(64, H - h0);
-  const int64_t blh = (int64_t)p.Bsz * L * H, bhn = (int64_t)p.Bsz * H;
-  // per head: final-state term plus the totals of e over the later tiles (one wave
-  // per head, lane j adding tiles tile + 1 + j, tile + 65 + j, ...)
-  for (int hl = wave; hl < nh; hl += 16) {
-    const int64_t bh = (int64_t)b * H + h0 + hl;
-    float later = 0.0f;
-    for (int j = tile + 1 + lane; j < ntiles; j += 64) later += tsum[bh * ntiles + j];
-    later = group_allreduce<64>(later, [](float x, float y) { return x + y; });
-    if (lane == 0) {
-      float Fv = 0.0f;
-      for (int q = 0; q < nA; ++q) Fv += wk.F[q * bhn + bh];
-      carry[hl] = Fv + later;
+  if (tid < MP) {
+    const float tau = (tid < M) ? p.tau[tid] : 1.0f;
+    s_rr[tid] = (tid < M) ? 1.0f / tau : 0.0f;
+    s_lnt[tid] = (tid < M) ? logf(tau) : 0.0f;
+  }
+  for (int i = tid; i < 64 * HS; i += 256) Hs[i] = 0.0f;
+  // x and dy of the chunk, 16 bytes per thread (columns past P, tokens past the sequence: zero)
+  {
+    constexpr int E16 = 16 / (int)sizeof(T), CPR = 64 / E16;
+    const int64_t xstride = (int64_t)H * P;
+    const T* xg = reinterpret_cast<const T*>(p.x) + (((int64_t)b * L + t0) * H + h) * P;
+    const T* yg = reinterpret_cast<const T*>(p.dy) + (((int64_t)b * L + t0) * H + h) * P;
+    for (int i = tid; i < 64 * CPR; i += 256) {
+      const int t = i / CPR, col = (i - t * CPR) * E16;
+      int4 vx = make_int4(0, 0, 0, 0), vy = vx;
+      if (t < nv && col < P) {
+        vx = *reinterpret_cast<const int4*>(xg + t * xstride + col);
+        vy = *reinterpret_cast<const int4*>(yg + t * xstride + col);
+      }
+      *reinterpret_cast<int4*>(Xs + t * XS + col) = vx;
+      *reinterpret_cast<int4*>(Ys + t * XS + col) = vy;
     }
   }
-  __syncthreads();
-  const int t = t0 + lane;
-  for (int hl = wave; hl < nh; hl += 16) {
-    const int h = h0 + hl;
-    const int64_t i = ((int64_t)b * H + h) * L + t;  // [B, H, L]
-    float e = 0.0f, f = 0.0f;
-    if (t < L) {
-      e = ddt_e(wk, blh, i, nA, nB);
-      for (int q = 0; q < nA; ++q) f += wk.fA[q * blh + i];
-      for (int q = 0; q < nB; ++q) f += wk.fB[q * blh + i];
+  // per-token controls (lane = token, every wave) and the (token, mode) logits
+  const bool tv = lane < nv;
+  const int64_t tok = ((int64_t)b * L + t0 + lane) * H + h;
+  const float dtv = tv ? p.dt[tok] : 0.0f;
+  const float al = tv ? strided3(p.alpha, p.as0, p.as1, p.as2, b, t0 + lane, h) : 1.0f;
+  const float lam = (tv && p.lambda) ? strided3(p.lambda, p.ls0, p.ls1, p.ls2, b, t0 + lane, h) : 1.0f;
+  const ChunkCtl k = chunk_controls(dtv, al, lam, p.lambda != nullptr, nv);
+  const float* rl_bh = p.read_logit ? p.read_logit + ((int64_t)b * L * H + h) * M : nullptr;
+  const float* wl_bh = p.write_logit ? p.write_logit + ((int64_t)b * L * H + h) * M : nullptr;
+  PairLogits<MP, 256> lgt;
+  lgt.load(rl_bh, wl_bh, t0, nv, M, (int64_t)H * M, tid);
+  __syncthreads();  // rates, zeroed H, x and dy in LDS
+  chunk_log_decays<MP, 4>(k.dtt, s_rr, P_lh, P_ll);
+  __syncthreads();  // log-decays in LDS
+  const int unsafe = pair_weights<MP, kIntra, 256>(k, nv, M, lgt, rl_bh == wl_bh, s_rr, s_lnt, P_lh, P_ll, nullptr,
+                                                   nullptr, W);
+  // ---- H = (C B^T) o (dY X^T), causal tiles [t][k]
+  const T* gt = gtiles + (((int64_t)b * nchunks + c) * G + g) * (kTiles * kTileElems);
+  for (int tile = wave; tile < kTiles; tile += 4) {
+    const int tb = tile_row(tile), kb = tile_col(tile);
+    const floatx4 D = dyx_tile<T, XS>(Ys, Xs, tb, kb, tid);
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int t = tb * 16 + lg * 4 + r, kk = kb * 16 + li;
+      Hs[t * HS + kk] = keep_if_ge(to_f32(gt[tile * kTileElems + lane * 4 + r]) * D[r], t, kk);
     }
-    // inclusive suffix sum over the tile: within each 16-lane row (lanes above,
-    // zero past the row end), then the totals of the later rows
-    float s = e;
-    s += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(s), 0x101, 0xF, 0xF, true));  // row_shl:1
-    s += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(s), 0x102, 0xF, 0xF, true));  // row_shl:2
-    s += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(s), 0x104, 0xF, 0xF, true));  // row_shl:4
-    s += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(s), 0x108, 0xF, 0xF, true));  // row_shl:8
-    const float r1 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(s), 16));
-    const float r2 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(s), 32));
-    const float r3 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(s), 48));
-    const int row = lane >> 4;
-    const float rows_after = row == 0 ? (r3 + r2) + r1 : row == 1 ? r3 + r2 : row == 2 ? r3 : 0.0f;
-    s += rows_after;
-    float v = 0.0f;
-    if (t < L) {
-      const float al = strided3(p.alpha, p.as0, p.as1, p.as2, b, t, h);
-      const float lam = p.lambda ? strided3(p.lambda, p.ls0, p.ls1, p.ls2, b, t, h) : 1.0f;
-      const float s_eff = p.lambda ? step_factor(lam, al) : 1.0f;
-      v = (-carry[hl] - s + f) * s_eff;
+  }
+  __syncthreads();  // H and the weights in LDS
+
+  // ---- tokens of row block tb = wave (dc) and column block tb (dk), modes as columns
+  const int tb = wave;
+  const int64_t obase = (((int64_t)b * H + h) * L + t0) * M;
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb) {
+    const int m = mb * 16 + li;
+    const int mm = m < MP ? m : 0;
+    const bool fac = m < MP && !((unsafe >> mm) & 1);
+    floatx4 cI = {0.f, 0.f, 0.f, 0.f}, kI = {0.f, 0.f, 0.f, 0.f};
+    for (int kq = 0; kq < (tb + 1) * 4; ++kq) {
+      const int kk = kq * 4 + lg;
+      cI = __builtin_amdgcn_mfma_f32_16x16x4f32(Hs[(tb * 16 + li) * HS + kk], fac ? P_Vt[mm * kWQ + kk] : 0.0f, cI,
+                                                0, 0, 0);
     }
-    out[lane][hl] = v;
-  }
-  __syncthreads();
-  for (int k = tid; k < 64 * 64; k += 1024) {
-    const int tt = k >> 6, hl = k & 63;
-    if (t0 + tt < L && hl < nh) p.ddt[((int64_t)b * L + t0 + tt) * H + h0 + hl] = out[tt][hl];
-  }
-  if (p.dD && b == 0 && tile == 0 && tid < nh) {
-    float acc = 0.0f;
-    for (int q = 0; q < nD; ++q)
-      for (int bb = 0; bb < p.Bsz; ++bb) acc += wk.dDp[((int64_t)q * p.Bsz + bb) * H + h0 + tid];
-    p.dD[h0 + tid] = acc;
+    for (int tq = tb * 4; tq < 16; ++tq) {
+      const int t = tq * 4 + lg;
+      kI = __builtin_amdgcn_mfma_f32_16x16x4f32(Hs[t * HS + tb * 16 + li], fac ? P_O[mm * kWQ + t] : 0.0f, kI, 0, 0,
+                                                0);
+    }
+    const bool direct = m < M && ((unsafe >> mm) & 1);
+    const float* lhm = P_lh + mm * kWQ;
+    const float* llm = P_ll + mm * kWQ;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int t = tb * 16 + lg * 4 + r;
+      float dc, dk;
+      if (!direct) {
+        dc = fexp(-lhm[t]) * cI[r];
+        dk = fexp(lhm[t]) * kI[r];
+      } else {
+        dc = dk = 0.0f;
+        for (int kk = 0; kk <= t; ++kk) dc += Hs[t * HS + kk] * P_Vt[mm * kWQ + kk] * ell_decay(lhm, llm, t, kk);
+        for (int t2 = t; t2 < 64; ++t2) dk += Hs[t2 * HS + t] * P_O[mm * kWQ + t2] * ell_decay(lhm, llm, t2, t);
+      }
+      if (m < M && t < nv) {
+        dc_out[obase + (int64_t)t * M + m] = dc;
+        dk_out[obase + (int64_t)t * M + m] = dk;
+      }
+    }
   }
 }
 
@@ -1549,14 +1508,20 @@ __global__ void __launch_bounds__(256) frac_bwd_group_sum_kernel(ScanParams p, c
   }
 }
 
+// Workgroups per head of the state sweep (along N) and of the rows sweep (along P),
+// as ColCfg and RowCfg choose them.
+int pad_modes(int M) { return M <= 1 ? 1 : M <= 2 ? 2 : M <= 4 ? 4 : 8; }
+int state_parts(const ScanParams& p) { return pad_modes(p.M) * (p.NP / 16) > 32 ? 2 : 1; }
+int rows_parts(const ScanParams& p) { return (pad_modes(p.M) >= 8 && p.io_bf16) ? 2 : 1; }
+
 struct BwdLayout {
-  size_t tiles, gg, hg, dBp, dCp, scal, total;
+  size_t tiles, gg, hg, dBp, dCp, dc, dk, F, dDp, gtl, total;
 };
 
 BwdLayout bwd_layout(const ScanParams& p) {
   BwdLayout l{};
   const size_t es = p.io_bf16 ? 2 : 4;
-  const size_t bl = (size_t)p.Bsz * p.L;
+  const size_t bl = (size_t)p.Bsz * p.L, blhm = bl * p.H * p.M, bh = (size_t)p.Bsz * p.H;
   auto up = [](size_t v) { return (v + 255) / 256 * 256; };
   l.tiles = 0;
   const size_t gtb = (size_t)p.Bsz * ((p.L + kQ - 1) / kQ) * p.H * kTiles * kTileElems * es;
@@ -1564,55 +1529,61 @@ BwdLayout bwd_layout(const ScanParams& p) {
   l.hg = l.gg + up(gtb);
   l.dBp = l.hg + up(gtb);
   l.dCp = l.dBp + up(bl * p.H * p.N * es);
-  l.scal = l.dCp + up(bl * p.H * p.N * es);
-  // eA[2], fA[2], eB[2], fB[2] per token and head; F[2], dDp per head; tile totals
-  l.total = l.scal + up(sizeof(float) * (8 * bl * p.H + 3 * (size_t)p.Bsz * p.H +
-                                         (size_t)p.Bsz * p.H * ((p.L + 63) / 64)));
+  l.dc = l.dCp + up(bl * p.H * p.N * es);
+  l.dk = l.dc + up(sizeof(float) * (state_parts(p) + 1) * blhm);
+  l.F = l.dk + up(sizeof(float) * (rows_parts(p) + 1) * blhm);
+  l.dDp = l.F + up(sizeof(float) * state_parts(p) * bh * p.M);
+  l.gtl = l.dDp + up(sizeof(float) * bh);
+  l.total = l.gtl + up(grad_tiles_bytes(p));
   return l;
 }
 
 template <typename T, int MP, int NB>
 hipError_t launch_bwd_variant(const ScanParams& p, void* ws, hipStream_t stream) {
+  using SC = ColCfg<T, MP, NB>;
+  using RC = RowCfg<T, MP, NB>;
+  if (SC::PS != state_parts(p) || RC::PS != rows_parts(p)) return hipErrorInvalidValue;
   const BwdLayout l = bwd_layout(p);
   unsigned char* base = reinterpret_cast<unsigned char*>(ws);
+  const size_t blhm = (size_t)p.Bsz * p.L * p.H * p.M;
   BwdWork wk;
   wk.tiles = base + l.tiles;
   wk.gg = base + l.gg;
   wk.hg = base + l.hg;
   wk.dBp = base + l.dBp;
   wk.dCp = base + l.dCp;
-  float* sc = reinterpret_cast<float*>(base + l.scal);
-  const size_t blh = (size_t)p.Bsz * p.L * p.H;
-  wk.eA = sc;
-  wk.fA = sc + 2 * blh;
-  wk.eB = sc + 4 * blh;
-  wk.fB = sc + 6 * blh;
-  wk.F = sc + 8 * blh;
-  wk.dDp = wk.F + 2 * (size_t)p.Bsz * p.H;
-  wk.tsum = wk.dDp + (size_t)p.Bsz * p.H;
+  wk.dc = reinterpret_cast<float*>(base + l.dc);
+  wk.dk = reinterpret_cast<float*>(base + l.dk);
+  wk.F = reinterpret_cast<float*>(base + l.F);
+  wk.dDp = reinterpret_cast<float*>(base + l.dDp);
 
   hipError_t e = launch_cb_tiles(p, base + l.tiles, stream);
   if (e != hipSuccess) return e;
   const int bh = p.Bsz * p.H;
-  hipLaunchKernelGGL((frac_bwd_state_kernel<T, MP, NB>), dim3(bh * ColCfg<T, MP, NB>::PS), dim3(512), 0, stream, p,
-                     wk);
+  hipLaunchKernelGGL((frac_bwd_state_kernel<T, MP, NB>), dim3(bh * SC::PS), dim3(512), 0, stream, p, wk);
   if ((e = hipGetLastError()) != hipSuccess) return e;
-  hipLaunchKernelGGL((frac_bwd_rows_kernel<T, MP, NB>), dim3(bh * RowCfg<T, MP, NB>::PS), dim3(512), 0, stream, p,
-                     wk);
+  hipLaunchKernelGGL((frac_bwd_rows_kernel<T, MP, NB>), dim3(bh * RC::PS), dim3(512), 0, stream, p, wk);
   if ((e = hipGetLastError()) != hipSuccess) return e;
-  hipLaunchKernelGGL((frac_bwd_cols_kernel<T, MP, NB>), dim3(bh * ColCfg<T, MP, NB>::PS), dim3(512), 0, stream, p,
-                     wk);
+  hipLaunchKernelGGL((frac_bwd_cols_kernel<T, MP, NB>), dim3(bh * SC::PS), dim3(512), 0, stream, p, wk);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   {
-    const int ntiles = (p.L + 63) / 64;
-    const int64_t nt = (int64_t)bh * ntiles;
-    hipLaunchKernelGGL(frac_bwd_ddt_tiles_kernel, dim3((unsigned)((nt + 3) / 4)), dim3(256), 0, stream, p, wk, wk.tsum,
-                       ColCfg<T, MP, NB>::PS, RowCfg<T, MP, NB>::PS);
+    const int64_t nblk = (int64_t)p.Bsz * ((p.L + kQ - 1) / kQ) * p.H;
+    hipLaunchKernelGGL((frac_bwd_intra_kernel<T, MP>), dim3((unsigned)nblk), dim3(256), 0, stream, p,
+                       reinterpret_cast<const T*>(base + l.tiles), wk.dc + SC::PS * blhm, wk.dk + RC::PS * blhm);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    hipLaunchKernelGGL(frac_bwd_ddt_kernel, dim3((unsigned)(ntiles * p.Bsz), (p.H + 63) / 64), dim3(1024), 0, stream, p, wk,
-                       (const float*)wk.tsum, ColCfg<T, MP, NB>::PS, RowCfg<T, MP, NB>::PS, 1);
   }
-  if ((e = hipGetLastError()) != hipSuccess) return e;
+  GradInputs gi;
+  gi.dc = wk.dc;
+  gi.dk = wk.dk;
+  gi.ndc = SC::PS + 1;
+  gi.ndk = RC::PS + 1;
+  gi.F = wk.F;
+  gi.nF = SC::PS;
+  gi.dDp = wk.dDp;
+  gi.nD = 1;
+  gi.tileV = reinterpret_cast<float*>(base + l.gtl);
+  gi.tileF = reinterpret_cast<int*>(base + l.gtl + sizeof(float) * (size_t)p.Bsz * p.H * ((p.L + 63) / 64) * p.M);
+  if ((e = launch_grad_finish(p, gi, stream)) != hipSuccess) return e;
   const int64_t nrows = (int64_t)p.Bsz * p.L;
   const int64_t nthr = nrows * p.G * (p.N / (16 / (int)sizeof(T)));
   hipLaunchKernelGGL((frac_bwd_group_sum_kernel<T>), dim3((unsigned)((nthr + 255) / 256)), dim3(256), 0, stream, p,
@@ -1640,27 +1611,6 @@ hipError_t launch_bwd_mp(const ScanParams& p, void* ws, hipStream_t stream) {
 }
 
 }  // namespace
-
-hipError_t launch_ddt_finish(const ScanParams& p, float* eA, float* fA, float* eB, float* fB, float* F, float* dDp,
-                             float* tsum, int nA, int nB, int nD, hipStream_t stream) {
-  BwdWork wk{};
-  wk.eA = eA;
-  wk.fA = fA;
-  wk.eB = eB;
-  wk.fB = fB;
-  wk.F = F;
-  wk.dDp = dDp;
-  wk.tsum = tsum;
-  const int ntiles = (p.L + 63) / 64;
-  const int64_t nt = (int64_t)p.Bsz * p.H * ntiles;
-  hipLaunchKernelGGL(frac_bwd_ddt_tiles_kernel, dim3((unsigned)((nt + 3) / 4)), dim3(256), 0, stream, p, wk, tsum, nA,
-                     nB);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(frac_bwd_ddt_kernel, dim3((unsigned)(ntiles * p.Bsz), (p.H + 63) / 64), dim3(1024), 0, stream, p,
-                     wk, (const float*)tsum, nA, nB, nD);
-  return hipGetLastError();
-}
 
 size_t scan_bwd_workspace(const ScanParams& p) {
   if (p.Bsz == 0 || p.L == 0) return 0;

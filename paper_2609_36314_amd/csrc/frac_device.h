@@ -213,6 +213,25 @@ __device__ __forceinline__ float wave_inclusive_sum(float v) {
   return v;
 }
 
+// The same inclusive prefix sum in float64 (each DPP move carries one half of the
+// value; lanes with no source read +0.0).
+template <int CTRL, int ROW_MASK, bool BOUND>
+__device__ __forceinline__ double dpp_move_f64(double v) {
+  const long long b = __double_as_longlong(v);
+  const int lo = __builtin_amdgcn_update_dpp(0, (int)(b & 0xffffffffll), CTRL, ROW_MASK, 0xF, BOUND);
+  const int hi = __builtin_amdgcn_update_dpp(0, (int)(b >> 32), CTRL, ROW_MASK, 0xF, BOUND);
+  return __longlong_as_double(((long long)hi << 32) | (long long)(unsigned)lo);
+}
+__device__ __forceinline__ double wave_inclusive_sum_f64(double v) {
+  v += dpp_move_f64<0x111, 0xF, true>(v);   // row_shr:1
+  v += dpp_move_f64<0x112, 0xF, true>(v);   // row_shr:2
+  v += dpp_move_f64<0x114, 0xF, true>(v);   // row_shr:4
+  v += dpp_move_f64<0x118, 0xF, true>(v);   // row_shr:8
+  v += dpp_move_f64<0x142, 0xA, false>(v);  // row_bcast:15
+  v += dpp_move_f64<0x143, 0xC, false>(v);  // row_bcast:31
+  return v;
+}
+
 // v plus the value of lane ^ 16 (lane ^ 32): the two halves exchanged with one
 // cross-row swap, the sum formed in the same order in both lanes.
 __device__ __forceinline__ float xor16_sum(float v) {
@@ -261,6 +280,52 @@ __device__ __forceinline__ float step_factor(float lam, float alpha) {
 
 __device__ __forceinline__ float effective_step(float dt, float alpha, const float* lam_ptr, float lam) {
   return lam_ptr ? dt * step_factor(lam, alpha) : dt;
+}
+
+// ------------------------------------------------- per-mode chunk log-decays
+//
+// The decay between tokens k <= t of one chunk in mode m is e^{-(l_{t,m} - l_{k,m})}
+// with l_{t,m} the chunk-local inclusive sum of r_m dtt_j (eq. rho-beta-def-frac:
+// the product of the retentions rho is the exponential of the summed exponents).
+// Each exponent is capped at kCapExp first: e^{-kCapExp} is zero in float32, so a
+// capped token still cuts every decay across it to exactly zero, while the sums
+// stay below 64 kCapExp.  The sums are formed per mode in float64 and kept as a
+// float pair (hi = float(l), lo = float(l - hi)): a difference of two such pairs
+// is exact to float32 rounding for any mix of effective steps in the chunk, where
+// one float32 prefix sum of dtt shared by all modes would lose the small steps
+// that follow a step near 1e13.
+constexpr float kCapExp = 110.0f;
+
+// r_m dtt capped; mask is 1 where the cap is not reached (the exponent then
+// depends on dtt with slope r_m, else not at all).
+__device__ __forceinline__ float capped_exponent(float r, float dtt) { return fminf(r * dtt, kCapExp); }
+
+// Wave w of an NW-wave workgroup, lane = token, forms modes w, w + NW, ... of the
+// chunk (dtt_l: this lane's effective step, 0 past the chunk's valid tokens;
+// s_rr: the rates, 0 for padding modes).  Writes hi / lo pairs [MP][kWQ].
+template <int MP, int NW>
+__device__ __forceinline__ void chunk_log_decays(float dtt_l, const float* s_rr, float* ell_hi, float* ell_lo) {
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+#pragma unroll
+  for (int m0 = 0; m0 < MP; m0 += NW) {
+    const int m = m0 + wave;
+    if (m0 + NW > MP && m >= MP) break;  // wave-uniform
+    const double v = wave_inclusive_sum_f64((double)capped_exponent(s_rr[m], dtt_l));
+    const float hi = (float)v;
+    ell_hi[m * kWQ + lane] = hi;
+    ell_lo[m * kWQ + lane] = (float)(v - (double)hi);
+  }
+}
+
+// l_a - l_b from two hi / lo pairs.
+__device__ __forceinline__ float ell_diff(float hia, float loa, float hib, float lob) {
+  return (hia - hib) + (loa - lob);
+}
+
+// e^{-(l_a - l_b)} for a >= b (entries a, b of one mode's row of the hi / lo arrays),
+// the interval clamped at zero so that rounding never lifts a decay above 1.
+__device__ __forceinline__ float ell_decay(const float* lh, const float* ll, int a, int b) {
+  return __expf(-fmaxf(ell_diff(lh[a], ll[a], lh[b], ll[b]), 0.0f));
 }
 
 // ------------------------------------------------------- fast scalar math

@@ -13,8 +13,9 @@
 //   S_m <- e^{-r_m A_Q} S_m + sum_k kappa_{k,m} e^{-r_m (A_Q - A_k)} B_k x_k^T
 //
 // The decay between two tokens is always formed from a difference of chunk-local
-// cumulative steps (the log-space form of the appendix), never from a ratio of
-// sequence-global products.
+// per-mode log-decays l_{t,m} (the log-space form of the appendix: chunk-local sums
+// of the capped exponents r_m dtt, in float64; frac_device.h), never from a ratio of
+// sequence-global products, so it is exact for any mix of effective steps.
 //
 // Kernels:
 //   frac_cb_kernel   G_chunk = C B^T (Q x Q, causal 16x16 tiles) once per
@@ -201,9 +202,9 @@ __global__ void __launch_bounds__(512) frac_fwd_kernel(ScanParams p, const T* __
   // everything else in one array, so that its addresses differ by constants
   constexpr int oGG = 0;                                        // T [64][GS] ((C B^T) o Gamma)^T, causal
   constexpr int oYb = oGG + 64 * GS * (int)sizeof(T);           // T [64][XS] output rows of the previous chunk
-  constexpr int oPrm = oYb + 64 * XS * (int)sizeof(T);          // float [6 MP + 1][Q] per-token weights
+  constexpr int oPrm = oYb + 64 * XS * (int)sizeof(T);          // float [8 MP][Q] per-token weights, log-decays
   constexpr int NSLOT = 4 - Cfg::TBO;                           // row blocks a wave hands over
-  constexpr int oYX = oPrm + (6 * MP * kWQ + kQ) * 4;            // float [8 waves][NSLOT][4][64] readout exchange
+  constexpr int oYX = oPrm + 8 * MP * kWQ * 4;                  // float [8 waves][NSLOT][4][64] readout exchange
   constexpr int oSc = oYX + (NPART > 1 ? 8 * NSLOT * 256 : 4) * 4;  // float rates, log tau, scales
   __shared__ __align__(16) unsigned char sm[oSc + 4 * MP * 4];
   T* GGT = reinterpret_cast<T*>(sm + oGG);
@@ -219,7 +220,8 @@ __global__ void __launch_bounds__(512) frac_fwd_kernel(ScanParams p, const T* __
   float* P_Vt = P_O + MP * kWQ;    // [MP][Q] kappa e^{r A_t}, safe modes (Gamma columns)
   float* P_c = P_Vt + MP * kWQ;    // [MP][Q] c      (modes past the factorisation bound)
   float* P_k = P_c + MP * kWQ;     // [MP][Q] kappa
-  float* P_A = P_k + MP * kWQ;     // [Q] A_t
+  float* P_lh = P_k + MP * kWQ;    // [MP][Q] chunk log-decays l_{t,m}, hi and lo parts
+  float* P_ll = P_lh + MP * kWQ;
 
   const T* xg = reinterpret_cast<const T*>(p.x) + (((int64_t)b * L) * H + h) * P;
   const T* Bgp = reinterpret_cast<const T*>(p.Bm) + (((int64_t)b * L) * G + g) * N;
@@ -339,24 +341,23 @@ __global__ void __launch_bounds__(512) frac_fwd_kernel(ScanParams p, const T* __
     }
     if (c + 1 < c1) load_controls(c + 1, dt_n, al_n, lam_n);
 
-    // ---- per-token step and its chunk-local cumulative sum (lane = token, every wave)
+    // ---- per-token step (lane = token, every wave) and the per-mode log-decays
     const float s_eff_l = lm_bh ? step_factor(lam_l, al_l) : 1.0f;
     const float dtt_l = (lane < nv) ? dtv * s_eff_l : 0.0f;
-    const float A_l = wave_inclusive_sum(dtt_l);
-    const float Alast = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(A_l), 63));
-    if (wave == 0) P_A[lane] = A_l;
+    chunk_log_decays<MP, NWT>(dtt_l, s_rr, P_lh, P_ll);
+    barrier();  // log-decays in LDS
 
     // ---- per (token, mode) controls and weights: thread pair = t MP + m
     // bit m of unsafe: the factorised Gamma would overflow for mode m (direct decay);
     // the same flags in every wave, lane m < MP testing mode m
-    const bool over = lane < MP && lane < M && !(s_rr[lane < MP ? lane : 0] * Alast <= kSafeExponent);
+    const bool over = lane < MP && lane < M && !(P_lh[(lane < MP ? lane : 0) * kWQ + kQ - 1] <= kSafeExponent);
     const int unsafe = (int)(__ballot(over) & ((1ull << MP) - 1));
 #pragma unroll
     for (int j = 0; j < lgt.NPR; ++j) {
       const int pr = tid + 512 * j;
       if (pr >= kQ * MP) break;  // wave-uniform
       const int t = pr / MP, m = pr - t * MP;
-      const float A = __shfl(A_l, t, 64), dtt = __shfl(dtt_l, t, 64), al = __shfl(al_l, t, 64);
+      const float dtt = __shfl(dtt_l, t, 64), al = __shfl(al_l, t, 64);
       const bool valid = t < nv;
       const float r = s_rr[m], prior = -al * s_lnt[m];
       float zc = (m < M) ? prior + lgt.rl[j] : -INFINITY;
@@ -364,17 +365,17 @@ __global__ void __launch_bounds__(512) frac_fwd_kernel(ScanParams p, const T* __
       // tokens past the sequence get zero weights (their tile rows may hold anything finite)
       const float cw = valid ? group_softmax<MP>(zc) : 0.0f;
       const float ww = w_is_c ? cw : (valid ? group_softmax<MP>(zw) : 0.0f);
-      const float xr = r * Alast;
-      const bool safe = xr <= kSafeExponent;
-      const float Enew = Ecur[m] * fexp(-xr);
+      const float lh = P_lh[m * kWQ + t], lhQ = P_lh[m * kWQ + kQ - 1];
+      const bool safe = lhQ <= kSafeExponent;
+      const float Enew = Ecur[m] * fexp(-lhQ);
       const bool ren = !(Enew >= kRescaleFloor);
       const float upd = ren ? 1.0f : __frcp_rn(Enew);
       const float kap = one_minus_exp_neg(dtt * r) * ww;
-      const float om = cw * fexp(-r * A);
+      const float om = cw * fexp(-lh);
       P_O[m * kWQ + t] = om;
       P_om[m * kWQ + t] = om * Ecur[m];
-      P_v[m * kWQ + t] = kap * fdecay(r, Alast - A) * upd;
-      P_Vt[m * kWQ + t] = safe ? kap * fexp(r * A) : 0.0f;
+      P_v[m * kWQ + t] = kap * ell_decay(P_lh + m * kWQ, P_ll + m * kWQ, kQ - 1, t) * upd;
+      P_Vt[m * kWQ + t] = safe ? kap * fexp(lh) : 0.0f;
       P_c[m * kWQ + t] = cw;
       P_k[m * kWQ + t] = kap;
       if (pr < MP) Enext[m] = ren ? 1.0f : Enew;
@@ -384,7 +385,7 @@ __global__ void __launch_bounds__(512) frac_fwd_kernel(ScanParams p, const T* __
     int renbits = 0;
 #pragma unroll
     for (int m = 0; m < MPW; ++m) {
-      const float Enew = uniform(Ecur[mo + m] * fexp(-s_rr[mo + m] * Alast));
+      const float Enew = uniform(Ecur[mo + m] * fexp(-P_lh[(mo + m) * kWQ + kQ - 1]));
       renf[m] = Enew;
       if (__float_as_int(Enew) < __float_as_int(kRescaleFloor)) renbits |= 1 << m;
     }
@@ -413,11 +414,10 @@ __global__ void __launch_bounds__(512) frac_fwd_kernel(ScanParams p, const T* __
         if (unsafe) {
           for (int m = 0; m < MP; ++m) {
             if (!((unsafe >> m) & 1)) continue;
-            const float rm = s_rr[m];
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
               const int t = tb * 16 + lg * 4 + r, k = kb * 16 + li;
-              if (t >= k) Gm[r] += P_c[m * kWQ + t] * P_k[m * kWQ + k] * fdecay(rm, P_A[t] - P_A[k]);
+              if (t >= k) Gm[r] += P_c[m * kWQ + t] * P_k[m * kWQ + k] * ell_decay(P_lh + m * kWQ, P_ll + m * kWQ, t, k);
             }
           }
         }

@@ -43,7 +43,7 @@ struct ScanParams {
   void* dBm;
   void* dCm;
   float* dD;
-  // further gradients (the form without B/C only; each NULL = not produced)
+  // further gradients (each NULL = not produced)
   float* dalpha;
   float* dlambda;
   float* dread_logit;
@@ -103,11 +103,28 @@ hipError_t launch_nfree_fwd(const ScanParams& p, hipStream_t stream);
 size_t nfree_bwd_workspace(const ScanParams& p);
 hipError_t launch_nfree_bwd(const ScanParams& p, void* ws, hipStream_t stream);
 
-// ddt and dD from per-token partial terms: e = sum of nA eA arrays - sum of nB eB
-// arrays, f likewise added ([B H L] each), F [nA][B H], dDp [nD][B H]; tsum holds
-// B H ceil(L / 64) floats of scratch.
-hipError_t launch_ddt_finish(const ScanParams& p, float* eA, float* fA, float* eB, float* fB, float* F, float* dDp,
-                             float* tsum, int nA, int nB, int nD, hipStream_t stream);
+// Gradients of dt, alpha, lambda, the read / write logits and D from the
+// per-(token, mode) partials of a reverse sweep (frac_grads.hip):
+//   dc [ndc][B H L][M]  partials of dL/dc_{t,m}      (slot 0 is overwritten with the sum)
+//   dk [ndk][B H L][M]  partials of dL/dkappa_{t,m}  (likewise)
+//   F  [nF][B H][M]     partials of <dS_final, S_final> per mode (the final-state term)
+//   dDp [nD][B H]       partials of sum(dy . x)
+//   tileV, tileF        scratch of grad_tiles_bytes(p) bytes (tileV first, then tileF)
+// Writes p.ddt and, where non-NULL, p.dalpha, p.dlambda, p.dread_logit,
+// p.dwrite_logit and p.dD.
+struct GradInputs {
+  float* dc;
+  float* dk;
+  int ndc, ndk;
+  const float* F;
+  int nF;
+  const float* dDp;
+  int nD;
+  float* tileV;
+  int* tileF;
+};
+size_t grad_tiles_bytes(const ScanParams& p);
+hipError_t launch_grad_finish(const ScanParams& p, const GradInputs& gi, hipStream_t stream);
 
 // True when a kernel variant exists for these sizes (M, N, P, dtype).
 bool scan_supported(const ScanParams& p, const char** why);

@@ -9,6 +9,10 @@
 //   Gamma_{t,k} = sum_m c_{t,m} kappa_{k,m} e^{-r_m (A_t - A_k)}
 //   S_m <- e^{-r_m A_Q} S_m + sum_k kappa_{k,m} e^{-r_m (A_Q - A_k)} x_k
 //
+// The decays are formed from per-mode chunk log-decays l_{t,m} (the chunk-local sums
+// of the capped exponents r_m dtt, in float64; frac_device.h), exact for any mix of
+// effective steps in a chunk.
+//
 // One workgroup of 4 waves per (batch, head, 64 columns of d_h); wave w owns
 // columns 16 w .. 16 w + 15 and the state of all modes for them (at most two
 // 16x16 float32 accumulator tiles, modes as rows).  Per chunk: x copied into LDS,
@@ -49,7 +53,7 @@ __global__ void __launch_bounds__(256) frac_nfree_fwd_kernel(ScanParams p, float
   // per-token weight arrays [MP][WQ]: the row stride of 68 floats spreads the
   // stores of one wave (4 tokens x 16 modes, or 8 x 8) over distinct LDS banks
   constexpr int WQ = kQ + 4;
-  __shared__ __align__(16) float W[6 * MP * WQ + kQ];
+  __shared__ __align__(16) float W[8 * MP * WQ];
   __shared__ float s_rr[MP], s_lnt[MP], s_E2[2][MP];
   float* P_om = W;                 // [MP][Q] c e^{-rA_t} E_m   (readout)
   float* P_v = W + MP * WQ;        // [MP][Q] kappa e^{-r(A_Q-A_t)} upd (update)
@@ -57,7 +61,8 @@ __global__ void __launch_bounds__(256) frac_nfree_fwd_kernel(ScanParams p, float
   float* P_Vt = W + 3 * MP * WQ;   // [MP][Q] kappa e^{rA_t}, safe modes (Gamma columns)
   float* P_c = W + 4 * MP * WQ;    // [MP][Q] c, kappa (modes past the factorisation bound)
   float* P_k = W + 5 * MP * WQ;
-  float* P_A = W + 6 * MP * WQ;    // [Q] A_t
+  float* P_lh = W + 6 * MP * WQ;   // [MP][Q] chunk log-decays l_{t,m}, hi and lo parts
+  float* P_ll = W + 7 * MP * WQ;
 
   // Gamma tiles above the diagonal that the intra product reads are never written
   for (int i = tid; i < 64 * XS; i += 256) Gs[i] = (T)0.0f;
@@ -144,36 +149,35 @@ __global__ void __launch_bounds__(256) frac_nfree_fwd_kernel(ScanParams p, float
           if (active && m < M && pc < P) ck[(int64_t)m * P + pc] = S[mb][r] * Ecur[m];
         }
     }
-    // ---- per-token controls (lane = token, every wave) and their chunk-local sum
+    // ---- per-token controls (lane = token, every wave) and the per-mode log-decays
     const float s_eff = lm_bh ? step_factor(lam, al_l) : 1.0f;
     const float dtt_l = tvalid ? dtv * s_eff : 0.0f;
-    const float A_l = wave_inclusive_sum(dtt_l);
-    const float Alast = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(A_l), 63));
-    if (wave == 0) P_A[lane] = A_l;
-    const bool over = lane < MP && lane < M && !(s_rr[lane < MP ? lane : 0] * Alast <= kNfSafe);
+    chunk_log_decays<MP, 4>(dtt_l, s_rr, P_lh, P_ll);
+    barrier();  // log-decays in LDS
+    const bool over = lane < MP && lane < M && !(P_lh[(lane < MP ? lane : 0) * WQ + kQ - 1] <= kNfSafe);
     const int unsafe = (int)(__ballot(over) & ((MP >= 32) ? 0xffffffffull : ((1ull << MP) - 1)));
     // ---- per (token, mode) weights: pair = t MP + m
 #pragma unroll
     for (int j = 0; j < NPR; ++j) {
       const int pr = tid + 256 * j, t = pr / MP, m = pr - t * MP;
-      const float A = __shfl(A_l, t, 64), dtt = __shfl(dtt_l, t, 64), al = __shfl(al_l, t, 64);
+      const float dtt = __shfl(dtt_l, t, 64), al = __shfl(al_l, t, 64);
       const bool valid = t < nv;
       const float r = s_rr[m], prior = -al * s_lnt[m];
       const float zc = (m < M) ? prior + rlr[j] : -INFINITY;
       const float zw = (m < M) ? prior + wlr[j] : -INFINITY;
       const float cw = valid ? group_softmax<MP>(zc) : 0.0f;
       const float ww = (rl_bh == wl_bh) ? cw : (valid ? group_softmax<MP>(zw) : 0.0f);
-      const float xr = r * Alast;
-      const bool safe = xr <= kNfSafe;
-      const float Enew = Ecur[m] * fexp(-xr);
+      const float lh = P_lh[m * WQ + t], lhQ = P_lh[m * WQ + kQ - 1];
+      const bool safe = lhQ <= kNfSafe;
+      const float Enew = Ecur[m] * fexp(-lhQ);
       const bool ren = !(Enew >= kNfFloor);
       const float upd = ren ? 1.0f : __frcp_rn(Enew);
       const float kap = one_minus_exp_neg(dtt * r) * ww;
-      const float om = cw * fexp(-r * A);
+      const float om = cw * fexp(-lh);
       P_O[m * WQ + t] = om;
       P_om[m * WQ + t] = om * Ecur[m];
-      P_v[m * WQ + t] = kap * fdecay(r, Alast - A) * upd;
-      P_Vt[m * WQ + t] = safe ? kap * fexp(r * A) : 0.0f;
+      P_v[m * WQ + t] = kap * ell_decay(P_lh + m * WQ, P_ll + m * WQ, kQ - 1, t) * upd;
+      P_Vt[m * WQ + t] = safe ? kap * fexp(lh) : 0.0f;
       P_c[m * WQ + t] = cw;
       P_k[m * WQ + t] = kap;
       if (pr < MP) Enext[m] = ren ? 1.0f : Enew;
@@ -185,7 +189,7 @@ __global__ void __launch_bounds__(256) frac_nfree_fwd_kernel(ScanParams p, float
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int m = mb * 16 + lg * 4 + r;
-        const float Enew = (m < MP) ? Ecur[m] * fexp(-s_rr[m] * Alast) : 1.0f;
+        const float Enew = (m < MP) ? Ecur[m] * fexp(-P_lh[(m < MP ? m : 0) * WQ + kQ - 1]) : 1.0f;
         renf[mb * 4 + r] = Enew;
         ren_any |= !(Enew >= kNfFloor);
       }
@@ -207,11 +211,10 @@ __global__ void __launch_bounds__(256) frac_nfree_fwd_kernel(ScanParams p, float
       if (unsafe) {
         for (int m = 0; m < MP; ++m) {
           if (!((unsafe >> m) & 1)) continue;
-          const float rm = s_rr[m];
 #pragma unroll
           for (int r = 0; r < 4; ++r) {
             const int t = tb * 16 + lg * 4 + r, k = kb * 16 + li;
-            if (t >= k) Gm[r] += P_c[m * WQ + t] * P_k[m * WQ + k] * fdecay(rm, P_A[t] - P_A[k]);
+            if (t >= k) Gm[r] += P_c[m * WQ + t] * P_k[m * WQ + k] * ell_decay(P_lh + m * WQ, P_ll + m * WQ, t, k);
           }
         }
       }
@@ -321,35 +324,30 @@ __global__ void __launch_bounds__(256) frac_nfree_fwd_kernel(ScanParams p, float
 // Reverse sweep over the chunks with the adjoint G_m (M x d_h per head, this
 // workgroup's 64 columns) in accumulator registers and each chunk's entering
 // state S0 read from the checkpoint pass.  Per chunk, with H = dY X^T over this
-// workgroup's columns (a partial sum over d_h) and Phi, Psi the rank-M tiles of
-// the B/C backward:
-//   dx_t = sum_m kappa_{t,m} e^{-r(A_Q-A_t)} G_m + sum_{t'>=t} Gamma_{t',t} dy_t' + D dy_t
-//   e_t  = sum_m r c_{t,m} e^{-rA_t} (S0_m . dy_t) + rowsum(H o Phi)_t - colsum(H o Phi)_t
-//          - sum_m r kappa_{t,m} e^{-r(A_Q-A_t)} (G_m . x_t)
-//   f_t  = colsum(H o Psi)_t + sum_m r w_{t,m} rho_{t,m} e^{-r(A_Q-A_t)} (G_m . x_t)
-//   G_m <- e^{-r_m A_Q} G_m + sum_t c_{t,m} e^{-r_m A_t} dy_t
-// e and f are summed over the workgroups of a head and turned into ddt (suffix
-// sums) by the finishing kernels of the B/C backward.
+// workgroup's columns (a partial sum over d_h) and l the chunk log-decays:
+//   dx_t = sum_m kappa_{t,m} e^{-(l_Q - l_t)} G_m + sum_{t'>=t} Gamma_{t',t} dy_t' + D dy_t
+//   dc_{t,m} = e^{-l_t} (S0_m . dy_t) + sum_{k<=t} H_{t,k} kappa_{k,m} e^{-(l_t - l_k)}
+//   dk_{k,m} = e^{-(l_Q - l_k)} (G_m . x_k) + sum_{t>=k} H_{t,k} c_{t,m} e^{-(l_t - l_k)}
+//   G_m <- e^{-l_Q} G_m + sum_t c_{t,m} e^{-l_t} dy_t
+// dc and dk (the gradients of the read weight and of the write gain, partial over
+// this workgroup's columns) go to the shared finishing kernels (frac_grads.hip),
+// which form ddt, dalpha, dlambda and the logit gradients.
 
 struct NfWork {
   const float* ckpt;  // [B H][nchunks + 1][M][P] states entering each chunk, then the final state
-  float* eA;          // [nps][B H L]
-  float* fA;          // [nps][B H L]
-  float* F;           // [nps][B H] sum_m r_m <dS_final, S_final> over this workgroup's columns
+  float* F;           // [nps][B H][M] <dS_final, S_final>_m over this workgroup's columns
   float* dDp;         // [nps][B H] sum dy . x over this workgroup's columns
-  // per-(token, mode) partials over this workgroup's columns (NULL: not wanted)
   float* dcp;         // [nps][B H L][M] <h_{t,m}, dy_t>: gradient of the read weight c_{t,m}
   float* dkp;         // [nps][B H L][M] <G_{t,m}, x_t>: gradient of the injection kappa_{t,m}
 };
 
-// WGRAD: also the per-(token, mode) weight-gradient partials (wk.dcp, wk.dkp).
-template <typename T, int MP, bool WGRAD>
+template <typename T, int MP>
 __global__ void __launch_bounds__(256, 2) frac_nfree_bwd_kernel(ScanParams p, NfWork wk) {
   constexpr bool kBf16 = sizeof(T) == 2;
   constexpr int MB = (MP + 15) / 16;
   constexpr int XS = kBf16 ? 64 + 8 : 64 + 4;
   constexpr int WQ = kWQ;
-  constexpr int NWA = 8;
+  constexpr int NWA = 6;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, li = lane & 15, lg = lane >> 4;
   const int L = p.L, H = p.H, P = p.P, M = p.M;
   const int nps = (P + 63) / 64;
@@ -357,34 +355,26 @@ __global__ void __launch_bounds__(256, 2) frac_nfree_bwd_kernel(ScanParams p, Nf
   const int p0 = ps * 64, pc = p0 + wave * 16 + li;
   const bool active = p0 + wave * 16 < P;
   const int nchunks = (L + kQ - 1) / kQ;
-  const int64_t blh = (int64_t)p.Bsz * L * H;
 
   __shared__ __align__(16) T Xs[64 * XS];                      // x [t][p]
   __shared__ __align__(16) T Ys[64 * XS];                      // dy [t][p]
   __shared__ __align__(16) T GT[64 * XS];                      // Gamma^T [t][t'], t' >= t
-  __shared__ __align__(16) T HT[WGRAD ? 64 * XS : 8];         // dY X^T [t][k], k <= t (weight gradients)
+  __shared__ __align__(16) T HT[64 * XS];                      // dY X^T [t][k], k <= t
   T* const DX = Xs;  // dx rows [t][p] (bfloat16 staging; x is no longer read by then)
   __shared__ __align__(16) float Gt[MP * WQ];                  // the adjoint [m][p]
-  __shared__ __align__(16) float W[NWA * MP * WQ + kQ];
-  __shared__ float slot[3][10][16];  // row sums of H o Phi, column sums of H o Phi and of H o Psi
-  __shared__ float tokE[2][64], tokF[64];
+  __shared__ __align__(16) float W[NWA * MP * WQ];
   __shared__ float s_rr[MP], s_lnt[MP];
-  __shared__ float red[256];
+  __shared__ float red[4][MP > 64 ? MP : 64];
+  __shared__ float redD[256];
   constexpr int SW = MP * WQ;
-  float* P_O = W;             // c e^{-rA}
-  float* P_Vt = W + 1 * SW;   // kappa e^{rA} (safe modes), kappa (modes past the factorisation bound)
-  float* P_rO = W + 2 * SW;   // r c e^{-rA}
-  float* P_Yw = W + 3 * SW;   // r w rho e^{rA} (safe modes), r w rho (the others)
-  float* P_vq = W + 4 * SW;   // kappa e^{-r(A_Q-A)}
-  float* P_rv = W + 5 * SW;   // r kappa e^{-r(A_Q-A)}
-  float* P_fv = W + 6 * SW;   // r w rho e^{-r(A_Q-A)}
-  float* P_c = W + 7 * SW;    // c (modes past the factorisation bound)
-  float* P_A = W + NWA * SW;  // [Q] A_t
+  float* P_O = W;             // c e^{-l}
+  float* P_Vt = W + 1 * SW;   // kappa e^{l} (safe modes), kappa (modes past the factorisation bound)
+  float* P_vq = W + 2 * SW;   // kappa e^{-(l_Q - l)}
+  float* P_c = W + 3 * SW;    // c (modes past the factorisation bound)
+  float* P_lh = W + 4 * SW;   // chunk log-decays, hi and lo parts
+  float* P_ll = W + 5 * SW;
 
-  for (int i = tid; i < 64 * XS; i += 256) {
-    GT[i] = (T)0.0f;
-    if constexpr (WGRAD) HT[i] = (T)0.0f;
-  }
+  for (int i = tid; i < 64 * XS; i += 256) GT[i] = HT[i] = (T)0.0f;
   if (tid < MP) {
     const float tau = (tid < M) ? p.tau[tid] : 1.0f;
     s_rr[tid] = (tid < M) ? 1.0f / tau : 0.0f;
@@ -392,23 +382,35 @@ __global__ void __launch_bounds__(256, 2) frac_nfree_bwd_kernel(ScanParams p, Nf
   }
   __syncthreads();
 
-  // the adjoint of the final state and the final-state term of ddt
+  // the adjoint of the final state and the final-state term <dS_final, S_final> per mode
   const int64_t sbase = (int64_t)bh * M * P;
   const float* ck_bh = wk.ckpt + (int64_t)bh * (nchunks + 1) * M * P;
   floatx4 G[MB];
-  float fpart = 0.0f;
+  float fpart[MB][4];
 #pragma unroll
   for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       const int m = mb * 16 + lg * 4 + r;
       float g = 0.0f;
+      fpart[mb][r] = 0.0f;
       if (p.d_final_state && active && m < M && pc < P) {
         g = p.d_final_state[sbase + (int64_t)m * P + pc];
-        fpart += s_rr[m] * g * ck_bh[(int64_t)nchunks * M * P + (int64_t)m * P + pc];
+        fpart[mb][r] = g * ck_bh[(int64_t)nchunks * M * P + (int64_t)m * P + pc];
       }
       G[mb][r] = g;
     }
+  // summed over the 16 columns of each lane group, then over the waves in order
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const float v = group_allreduce<16>(fpart[mb][r], [](float x, float y) { return x + y; });
+      const int m = mb * 16 + lg * 4 + r;
+      if (li == 0 && m < MP) red[wave][m] = v;
+    }
+  __syncthreads();
+  if (tid < MP && tid < M) wk.F[((int64_t)ps * p.Bsz * H + bh) * M + tid] = ((red[0][tid] + red[1][tid]) + red[2][tid]) + red[3][tid];
   const float Dh = p.D ? p.D[h] : 0.0f;
   float dd_acc = 0.0f;
 
@@ -489,38 +491,29 @@ __global__ void __launch_bounds__(256, 2) frac_nfree_bwd_kernel(ScanParams p, Nf
     const float dtv = dt_n, al_l = al_n, lam = lam_n;
     const float s_eff = lm_bh ? step_factor(lam, al_l) : 1.0f;
     const float dtt_l = tvalid ? dtv * s_eff : 0.0f;
-    const float A_l = wave_inclusive_sum(dtt_l);
-    const float Alast = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(A_l), 63));
-    if (wave == 0) P_A[lane] = A_l;
-    const bool over = lane < MP && lane < M && !(s_rr[lane < MP ? lane : 0] * Alast <= kNfSafe);
+    chunk_log_decays<MP, 4>(dtt_l, s_rr, P_lh, P_ll);
+    barrier();  // log-decays in LDS
+    const bool over = lane < MP && lane < M && !(P_lh[(lane < MP ? lane : 0) * WQ + kQ - 1] <= kNfSafe);
     const int unsafe = (int)(__ballot(over) & ((MP >= 32) ? 0xffffffffull : ((1ull << MP) - 1)));
     // ---- per (token, mode) weights: pair = t MP + m
 #pragma unroll
     for (int j = 0; j < NPR; ++j) {
       const int pr = tid + 256 * j, t = pr / MP, m = pr - t * MP;
-      const float A = __shfl(A_l, t, 64), dtt = __shfl(dtt_l, t, 64), al = __shfl(al_l, t, 64);
+      const float dtt = __shfl(dtt_l, t, 64), al = __shfl(al_l, t, 64);
       const bool valid = t < nv;
       const float r = s_rr[m], prior = -al * s_lnt[m];
       const float zc = (m < M) ? prior + rlr[j] : -INFINITY;
       const float zw = (m < M) ? prior + wlr[j] : -INFINITY;
       const float cw = valid ? group_softmax<MP>(zc) : 0.0f;
       const float ww = (rl_bh == wl_bh) ? cw : (valid ? group_softmax<MP>(zw) : 0.0f);
-      const bool safe = r * Alast <= kNfSafe;
-      const float beta = one_minus_exp_neg(dtt * r);
-      const float kap = beta * ww;
-      const float rwr = r * ww * (1.0f - beta);
-      const float ea = fexp(-r * A);
-      const float ep = safe ? fexp(r * A) : 0.0f;
-      const float dec = fdecay(r, Alast - A);
+      const float lh = P_lh[m * WQ + t];
+      const bool safe = P_lh[m * WQ + kQ - 1] <= kNfSafe;
+      const float kap = one_minus_exp_neg(dtt * r) * ww;
       float* o = W + m * WQ + t;
-      o[0 * SW] = cw * ea;
-      o[1 * SW] = safe ? kap * ep : kap;
-      o[2 * SW] = r * cw * ea;
-      o[3 * SW] = safe ? rwr * ep : rwr;
-      o[4 * SW] = kap * dec;
-      o[5 * SW] = r * kap * dec;
-      o[6 * SW] = rwr * dec;
-      o[7 * SW] = cw;
+      o[0 * SW] = cw * fexp(-lh);
+      o[1 * SW] = safe ? kap * fexp(lh) : kap;
+      o[2 * SW] = kap * ell_decay(P_lh + m * WQ, P_ll + m * WQ, kQ - 1, t);
+      o[3 * SW] = cw;
     }
     // the adjoint at the end of the chunk, [m][p], for its products with x
 #pragma unroll
@@ -532,77 +525,46 @@ __global__ void __launch_bounds__(256, 2) frac_nfree_bwd_kernel(ScanParams p, Nf
       }
     barrier();  // x, dy, weights and the adjoint in LDS
 
-    // ---- causal tiles: Gamma^T into LDS; row / column sums of H o Phi, column sums of H o Psi
+    // ---- causal tiles: Gamma^T and the masked H = dY X^T into LDS
     for (int tile = wave; tile < 10; tile += 4) {
       const int tb = tile_row(tile), kb = tile_col(tile);
-      floatx4 D = {0.f, 0.f, 0.f, 0.f};  // H = dY X^T over this workgroup's columns
+      floatx4 D = {0.f, 0.f, 0.f, 0.f};  // H over this workgroup's columns
 #pragma unroll
       for (int kp = 0; kp < 2; ++kp)
         mma(D, frag_load8(Ys + (tb * 16 + li) * XS + kp * 32 + lg * 8), frag_load8(Xs + (kb * 16 + li) * XS + kp * 32 + lg * 8));
-      floatx4 Gm = {0.f, 0.f, 0.f, 0.f}, Ph = Gm, Ps = Gm;
+      floatx4 Gm = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int q = 0; q < (MP + 3) / 4; ++q) {
         // mode of this lane's K slot: lg (MP / 4) + q puts the 64 lanes' [m][t] reads in distinct
         // LDS banks for 16 modes (the K order of the sum is free); < MP, a multiple of 4
         const int m = lg * (MP / 4) + q;
         const bool ok = !((unsafe >> m) & 1);
-        const float vO = P_O[m * WQ + tb * 16 + li], vrO = P_rO[m * WQ + tb * 16 + li];
-        const float vVt = P_Vt[m * WQ + kb * 16 + li], vY = P_Yw[m * WQ + kb * 16 + li];
-        const float aO = ok ? vO : 0.0f, arO = ok ? vrO : 0.0f;  // selects, not branches
-        const float bVt = ok ? vVt : 0.0f, bY = ok ? vY : 0.0f;
-        Gm = __builtin_amdgcn_mfma_f32_16x16x4f32(aO, bVt, Gm, 0, 0, 0);
-        Ph = __builtin_amdgcn_mfma_f32_16x16x4f32(arO, bVt, Ph, 0, 0, 0);
-        Ps = __builtin_amdgcn_mfma_f32_16x16x4f32(aO, bY, Ps, 0, 0, 0);
+        const float vO = P_O[m * WQ + tb * 16 + li];
+        const float vVt = P_Vt[m * WQ + kb * 16 + li];
+        Gm = __builtin_amdgcn_mfma_f32_16x16x4f32(ok ? vO : 0.0f, ok ? vVt : 0.0f, Gm, 0, 0, 0);
       }
       if (unsafe) {
         for (int m = 0; m < MP; ++m) {
           if (!((unsafe >> m) & 1)) continue;
-          const float rm = s_rr[m];
 #pragma unroll
           for (int r = 0; r < 4; ++r) {
             const int t = tb * 16 + lg * 4 + r, k = kb * 16 + li;
-            if (t >= k) {
-              const float d = fdecay(rm, P_A[t] - P_A[k]);
-              const float ck = P_c[m * WQ + t] * d;
-              Gm[r] += ck * P_Vt[m * WQ + k];
-              Ph[r] += rm * ck * P_Vt[m * WQ + k];
-              Ps[r] += ck * P_Yw[m * WQ + k];
-            }
+            if (t >= k) Gm[r] += P_c[m * WQ + t] * P_Vt[m * WQ + k] * ell_decay(P_lh + m * WQ, P_ll + m * WQ, t, k);
           }
         }
       }
-      float rv[4], ce = 0.f, cf = 0.f;
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int t = tb * 16 + lg * 4 + r, k = kb * 16 + li;
         GT[k * XS + t] = (T)keep_if_ge(Gm[r], t, k);
-        const float hm = keep_if_ge(D[r], t, k);
-        if constexpr (WGRAD) HT[t * XS + k] = (T)hm;
-        rv[r] = hm * Ph[r];
-        ce += hm * Ph[r];
-        cf += hm * Ps[r];
-      }
-      // row sums: 16 lanes of a row group hold one row's 16 columns
-#pragma unroll
-      for (int r = 0; r < 4; ++r) rv[r] = group_allreduce<16>(rv[r], [](float x, float y) { return x + y; });
-      if (li == 0) {
-#pragma unroll
-        for (int r = 0; r < 4; ++r) slot[0][tile][lg * 4 + r] = rv[r];
-      }
-      ce = xor32_sum(xor16_sum(ce));
-      cf = xor32_sum(xor16_sum(cf));
-      if (lg == 0) {
-        slot[1][tile][li] = ce;
-        slot[2][tile][li] = cf;
+        HT[t * XS + k] = (T)keep_if_ge(D[r], t, k);
       }
     }
 
-    // ---- per token (row block tb = wave): readout part of e from S0 . dy, adjoint
-    // parts of e and f from G . x (modes as output columns, reduced over 16 lanes)
-    floatx4 Uk[MB], Zk[MB];  // S0 . dy and G . x of this wave's tokens, kept for the weight gradients
+    // ---- per token (row block tb = wave): S0 . dy and G . x, modes as output columns
+    floatx4 Uk[MB], Zk[MB];
     {
       const int tb = wave;
-      float eR[4] = {0.f, 0.f, 0.f, 0.f}, eJ[4] = {0.f, 0.f, 0.f, 0.f}, fJ[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int mb = 0; mb < MB; ++mb) {
         const int m = mb * 16 + li;  // output column of this lane
@@ -626,28 +588,6 @@ __global__ void __launch_bounds__(256, 2) frac_nfree_bwd_kernel(ScanParams p, Nf
           mma(U, frag_load8(Ys + (tb * 16 + li) * XS + kp * 32 + lg * 8), S0f);
           mma(Z, frag_load8(Xs + (tb * 16 + li) * XS + kp * 32 + lg * 8), Gf);
         }
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int t = tb * 16 + lg * 4 + r;
-          const bool ok = m < MP;
-          eR[r] += (ok ? P_rO[m * WQ + t] : 0.0f) * U[r];
-          eJ[r] += (ok ? P_rv[m * WQ + t] : 0.0f) * Z[r];
-          fJ[r] += (ok ? P_fv[m * WQ + t] : 0.0f) * Z[r];
-        }
-      }
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        eR[r] = group_allreduce<16>(eR[r], [](float x, float y) { return x + y; });
-        eJ[r] = group_allreduce<16>(eJ[r], [](float x, float y) { return x + y; });
-        fJ[r] = group_allreduce<16>(fJ[r], [](float x, float y) { return x + y; });
-      }
-      if (li == 0) {
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          tokE[0][tb * 16 + lg * 4 + r] = eR[r];
-          tokE[1][tb * 16 + lg * 4 + r] = eJ[r];
-          tokF[tb * 16 + lg * 4 + r] = fJ[r];
-        }
       }
     }
     // the next chunk's inputs, issued once this chunk's copies have been consumed
@@ -662,49 +602,48 @@ __global__ void __launch_bounds__(256, 2) frac_nfree_bwd_kernel(ScanParams p, Nf
         dd_acc += to_f32(Xs[t * XS + pcol]) * to_f32(Ys[t * XS + pcol]);
       }
     }
-    barrier();  // Gamma^T, slots and token partials in LDS
+    barrier();  // Gamma^T and H in LDS
 
-    if constexpr (WGRAD) {
+    {
       // ---- per-(token, mode) partials, tokens of row block tb = wave, modes as columns:
-      //   dc_{t,m} = e^{-rA_t} (S0_m . dy_t) + sum_{k<=t} H_{t,k} kappa_{k,m} e^{-r(A_t-A_k)}
-      //   dk_{k,m} = e^{-r(A_Q-A_k)} (G_m . x_k) + sum_{t>=k} H_{t,k} c_{t,m} e^{-r(A_t-A_k)}
-      // with the sums as float32 matrix-core products (H kappa e^{rA}, H^T c e^{-rA}) for
+      //   dc_{t,m} = e^{-l_t} (S0_m . dy_t) + sum_{k<=t} H_{t,k} kappa_{k,m} e^{-(l_t - l_k)}
+      //   dk_{k,m} = e^{-(l_Q - l_k)} (G_m . x_k) + sum_{t>=k} H_{t,k} c_{t,m} e^{-(l_t - l_k)}
+      // with the sums as float32 matrix-core products (H kappa e^{l}, H^T c e^{-l}) for
       // the factorised modes and one exp per pair for the others
       const int tb = wave;
-      const float AQ = Alast;
 #pragma unroll
       for (int mb = 0; mb < MB; ++mb) {
         const int m = mb * 16 + li;
-        const bool fac = m < MP && !((unsafe >> m) & 1);
+        const int mm = m < MP ? m : 0;
+        const bool fac = m < MP && !((unsafe >> mm) & 1);
         floatx4 cI = {0.f, 0.f, 0.f, 0.f}, kI = {0.f, 0.f, 0.f, 0.f};
         for (int kq = 0; kq < (tb + 1) * 4; ++kq) {
           const int k = kq * 4 + lg;
           const float a = to_f32(HT[(tb * 16 + li) * XS + k]);
-          const float bb = fac ? P_Vt[m * WQ + k] : 0.0f;
+          const float bb = fac ? P_Vt[mm * WQ + k] : 0.0f;
           cI = __builtin_amdgcn_mfma_f32_16x16x4f32(a, bb, cI, 0, 0, 0);
         }
         for (int tq = tb * 4; tq < 16; ++tq) {
           const int t = tq * 4 + lg;
           const float a = to_f32(HT[t * XS + tb * 16 + li]);
-          const float bb = fac ? P_O[m * WQ + t] : 0.0f;
+          const float bb = fac ? P_O[mm * WQ + t] : 0.0f;
           kI = __builtin_amdgcn_mfma_f32_16x16x4f32(a, bb, kI, 0, 0, 0);
         }
-        const bool direct = m < M && ((unsafe >> (m < MP ? m : 0)) & 1);
-        const float rm = (m < MP) ? s_rr[m] : 0.0f;
+        const bool direct = m < M && ((unsafe >> mm) & 1);
+        const float* lhm = P_lh + mm * WQ;
+        const float* llm = P_ll + mm * WQ;
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int t = tb * 16 + lg * 4 + r;
-          const float At = P_A[t];
-          float dc = fexp(-rm * At) * Uk[mb][r];
-          float dk = fdecay(rm, AQ - At) * Zk[mb][r];
+          const float ea = fexp(-lhm[t]);
+          float dc = ea * Uk[mb][r];
+          float dk = ell_decay(lhm, llm, kQ - 1, t) * Zk[mb][r];
           if (!direct) {
-            dc += fexp(-rm * At) * cI[r];
-            dk += fexp(rm * At) * kI[r];
+            dc += ea * cI[r];
+            dk += fexp(lhm[t]) * kI[r];
           } else {
-            for (int k = 0; k <= t; ++k)
-              dc += to_f32(HT[t * XS + k]) * P_Vt[m * WQ + k] * fdecay(rm, At - P_A[k]);
-            for (int t2 = t; t2 < 64; ++t2)
-              dk += to_f32(HT[t2 * XS + t]) * P_c[m * WQ + t2] * fdecay(rm, P_A[t2] - At);
+            for (int k = 0; k <= t; ++k) dc += to_f32(HT[t * XS + k]) * P_Vt[mm * WQ + k] * ell_decay(lhm, llm, t, k);
+            for (int t2 = t; t2 < 64; ++t2) dk += to_f32(HT[t2 * XS + t]) * P_c[mm * WQ + t2] * ell_decay(lhm, llm, t2, t);
           }
           if (m < M && t < nv) {
             const int64_t i = ((int64_t)ps * p.Bsz * H * L + (int64_t)bh * L + t0 + t) * M + m;  // [nps][B H L][M]
@@ -750,13 +689,13 @@ __global__ void __launch_bounds__(256, 2) frac_nfree_bwd_kernel(ScanParams p, Nf
           }
         }
       }
-      // ---- adjoint update G <- e^{-r A_Q} G + (c e^{-rA})^T dY, rows m, column pc
+      // ---- adjoint update G <- e^{-l_Q} G + (c e^{-l})^T dY, rows m, column pc
 #pragma unroll
       for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int m = mb * 16 + lg * 4 + r;
-          G[mb][r] *= (m < MP) ? fexp(-s_rr[m] * Alast) : 0.0f;
+          G[mb][r] *= (m < MP) ? fexp(-P_lh[(m < MP ? m : 0) * WQ + kQ - 1]) : 0.0f;
         }
 #pragma unroll
       for (int kt = 0; kt < 2; ++kt) {
@@ -785,26 +724,6 @@ __global__ void __launch_bounds__(256, 2) frac_nfree_bwd_kernel(ScanParams p, Nf
       }
     }
     barrier();  // dx rows in LDS
-
-    if (wave == 0) {
-      // token t: readout part + row sums of its row-block tiles - column sums of its
-      // column-block tiles - adjoint part; f: column sums + adjoint part (fixed order)
-      const int t = lane, tbt = t >> 4, tr = t & 15;
-      float e = tokE[0][t], f = 0.0f;
-      for (int kb2 = 0; kb2 <= tbt; ++kb2) e += slot[0][tbt * (tbt + 1) / 2 + kb2][tr];
-      for (int tb2 = tbt; tb2 < 4; ++tb2) {
-        const int tile = tb2 * (tb2 + 1) / 2 + tbt;
-        e -= slot[1][tile][tr];
-        f += slot[2][tile][tr];
-      }
-      e -= tokE[1][t];
-      f += tokF[t];
-      if (t < nv) {
-        const int64_t i = (int64_t)ps * blh + (int64_t)bh * L + t0 + t;  // [nps][B H L]
-        wk.eA[i] = e;
-        wk.fA[i] = f;
-      }
-    }
     if constexpr (kBf16) {
       for (int i = tid; i < 64 * CPR; i += 256) {
         const int t = i / CPR, col = (i - t * CPR) * E16;
@@ -825,79 +744,13 @@ __global__ void __launch_bounds__(256, 2) frac_nfree_bwd_kernel(ScanParams p, Nf
       }
   }
 
-  // ---- per-workgroup totals: final-state term and sum(dy . x)
-  red[tid] = fpart;
+  // ---- per-workgroup total of sum(dy . x)
+  redD[tid] = dd_acc;
   __syncthreads();
   if (tid == 0) {
     float s = 0.f;
-    for (int i = 0; i < 256; ++i) s += red[i];
-    wk.F[(int64_t)ps * p.Bsz * H + bh] = s;
-  }
-  __syncthreads();
-  red[tid] = dd_acc;
-  __syncthreads();
-  if (tid == 0) {
-    float s = 0.f;
-    for (int i = 0; i < 256; ++i) s += red[i];
+    for (int i = 0; i < 256; ++i) s += redD[i];
     wk.dDp[(int64_t)ps * p.Bsz * H + bh] = s;
-  }
-}
-
-// Gradients of the read / write logits, alpha and lambda from the per-(token, mode)
-// partials of the reverse sweep and the step-size gradient; MP lanes per (b, t, h):
-//   dz_c = c (dc - sum_m c dc),  dz_w = w (dw - sum_m w dw),  dw = beta dk
-// (softmax of eq. read-softmax, kappa = beta w), and with s = lambda^{1/alpha}
-// (eq. tau-eff) and the step-size gradient ddt = s dDelta~:
-//   dalpha  = -sum_m (dz_c + dz_w) ln tau_m - ddt Delta ln(lambda) / alpha^2
-//   dlambda = ddt Delta / (alpha lambda)
-template <int MP>
-__global__ void __launch_bounds__(256) frac_nfree_grads_kernel(ScanParams p, const float* __restrict__ dcp,
-                                                               const float* __restrict__ dkp, int nps) {
-  const int64_t pr = (int64_t)blockIdx.x * 256 + threadIdx.x;  // ((b L + t) H + h) MP + m
-  const int64_t ntok = (int64_t)p.Bsz * p.L * p.H;
-  const int64_t tok = pr / MP;
-  const int m = (int)(pr - tok * MP);
-  const bool tv = tok < ntok;  // whole groups of MP lanes past the end compute token 0 and store nothing
-  const int64_t tk = tv ? tok : 0;
-  const int M = p.M, L = p.L, H = p.H;
-  const int h = (int)(tk % H);
-  const int64_t bt = tk / H;
-  const int t = (int)(bt % L), b = (int)(bt / L);
-  const bool mv = m < M;
-  const float al = p.alpha[b * p.as0 + t * p.as1 + h * p.as2];
-  const float lam = p.lambda ? p.lambda[b * p.ls0 + t * p.ls1 + h * p.ls2] : 1.0f;
-  const float dtv = p.dt[tk];
-  const float s_eff = p.lambda ? step_factor(lam, al) : 1.0f;
-  const float tau = mv ? p.tau[m] : 1.0f;
-  const float r = 1.0f / tau, lnt = logf(tau);
-  const float prior = -al * lnt;
-  const float zc = mv ? prior + (p.read_logit ? p.read_logit[tk * M + m] : 0.0f) : -INFINITY;
-  const float zw = mv ? prior + (p.write_logit ? p.write_logit[tk * M + m] : 0.0f) : -INFINITY;
-  const float c = group_softmax<MP>(zc);
-  const float w = (p.read_logit == p.write_logit) ? c : group_softmax<MP>(zw);
-  float dc = 0.0f, dk = 0.0f;
-  if (mv) {
-    const int64_t S = (int64_t)p.Bsz * H * L * M;
-    const int64_t i = (((int64_t)b * H + h) * L + t) * M + m;
-    for (int q = 0; q < nps; ++q) {
-      dc += dcp[q * S + i];
-      dk += dkp[q * S + i];
-    }
-  }
-  const float beta = one_minus_exp_neg(dtv * s_eff * r);
-  const float dw = beta * dk;
-  const float sc = group_allreduce<MP>(c * dc, [](float x, float y) { return x + y; });
-  const float sw = group_allreduce<MP>(w * dw, [](float x, float y) { return x + y; });
-  const float dzc = c * (dc - sc), dzw = w * (dw - sw);
-  if (tv && mv) {
-    if (p.dread_logit) p.dread_logit[tk * M + m] = dzc;
-    if (p.dwrite_logit) p.dwrite_logit[tk * M + m] = dzw;
-  }
-  const float dap = group_allreduce<MP>(mv ? -(dzc + dzw) * lnt : 0.0f, [](float x, float y) { return x + y; });
-  if (tv && m == 0) {
-    const float g = p.ddt[tk] * dtv;
-    if (p.dalpha) p.dalpha[tk] = dap + (p.lambda ? -g * logf(lam) / (al * al) : 0.0f);
-    if (p.dlambda) p.dlambda[tk] = p.lambda ? g / (al * lam) : 0.0f;
   }
 }
 
@@ -912,7 +765,7 @@ hipError_t launch_nfree_t(const ScanParams& p, hipStream_t stream) {
 }
 
 struct NfLayout {
-  size_t ckpt, eA, fA, F, dDp, tsum, dcp, dkp, total;
+  size_t ckpt, F, dDp, tiles, dcp, dkp, total;
 };
 
 NfLayout nfree_layout(const ScanParams& p) {
@@ -920,12 +773,10 @@ NfLayout nfree_layout(const ScanParams& p) {
   const size_t bh = (size_t)p.Bsz * p.H, nps = (p.P + 63) / 64, nch = (p.L + kQ - 1) / kQ;
   NfLayout l{};
   l.ckpt = 0;
-  l.eA = up(sizeof(float) * bh * (nch + 1) * p.M * p.P);
-  l.fA = l.eA + up(sizeof(float) * nps * bh * p.L);
-  l.F = l.fA + up(sizeof(float) * nps * bh * p.L);
-  l.dDp = l.F + up(sizeof(float) * nps * bh);
-  l.tsum = l.dDp + up(sizeof(float) * nps * bh);
-  l.dcp = l.tsum + up(sizeof(float) * bh * ((p.L + 63) / 64));
+  l.F = up(sizeof(float) * bh * (nch + 1) * p.M * p.P);
+  l.dDp = l.F + up(sizeof(float) * nps * bh * p.M);
+  l.tiles = l.dDp + up(sizeof(float) * nps * bh);
+  l.dcp = l.tiles + up(grad_tiles_bytes(p));
   l.dkp = l.dcp + up(sizeof(float) * nps * bh * p.L * p.M);
   l.total = l.dkp + up(sizeof(float) * nps * bh * p.L * p.M);
   return l;
@@ -937,31 +788,29 @@ hipError_t launch_nfree_bwd_mp(const ScanParams& p, void* ws, hipStream_t stream
   unsigned char* base = reinterpret_cast<unsigned char*>(ws);
   NfWork wk;
   wk.ckpt = reinterpret_cast<float*>(base + l.ckpt);
-  wk.eA = reinterpret_cast<float*>(base + l.eA);
-  wk.fA = reinterpret_cast<float*>(base + l.fA);
   wk.F = reinterpret_cast<float*>(base + l.F);
   wk.dDp = reinterpret_cast<float*>(base + l.dDp);
-  const bool wgrad = p.dalpha || p.dlambda || p.dread_logit || p.dwrite_logit;
-  wk.dcp = wgrad ? reinterpret_cast<float*>(base + l.dcp) : nullptr;
-  wk.dkp = wgrad ? reinterpret_cast<float*>(base + l.dkp) : nullptr;
+  wk.dcp = reinterpret_cast<float*>(base + l.dcp);
+  wk.dkp = reinterpret_cast<float*>(base + l.dkp);
   const unsigned blocks = (unsigned)((int64_t)p.Bsz * p.H * ((p.P + 63) / 64));
   hipLaunchKernelGGL((frac_nfree_fwd_kernel<T, MP, true>), dim3(blocks), dim3(256), 0, stream, p,
                      reinterpret_cast<float*>(base + l.ckpt));
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  if (wgrad)
-    hipLaunchKernelGGL((frac_nfree_bwd_kernel<T, MP, true>), dim3(blocks), dim3(256), 0, stream, p, wk);
-  else
-    hipLaunchKernelGGL((frac_nfree_bwd_kernel<T, MP, false>), dim3(blocks), dim3(256), 0, stream, p, wk);
+  hipLaunchKernelGGL((frac_nfree_bwd_kernel<T, MP>), dim3(blocks), dim3(256), 0, stream, p, wk);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   const int nps = (p.P + 63) / 64;
-  e = launch_ddt_finish(p, wk.eA, wk.fA, nullptr, nullptr, wk.F, wk.dDp, reinterpret_cast<float*>(base + l.tsum), nps,
-                        0, nps, stream);
-  if (e != hipSuccess || !wgrad) return e;
-  const int64_t pairs = (int64_t)p.Bsz * p.L * p.H * MP;
-  hipLaunchKernelGGL((frac_nfree_grads_kernel<MP>), dim3((unsigned)((pairs + 255) / 256)), dim3(256), 0, stream, p,
-                     wk.dcp, wk.dkp, nps);
-  return hipGetLastError();
+  GradInputs gi;
+  gi.dc = wk.dcp;
+  gi.dk = wk.dkp;
+  gi.ndc = gi.ndk = nps;
+  gi.F = wk.F;
+  gi.nF = nps;
+  gi.dDp = wk.dDp;
+  gi.nD = nps;
+  gi.tileV = reinterpret_cast<float*>(base + l.tiles);
+  gi.tileF = reinterpret_cast<int*>(base + l.tiles + sizeof(float) * (size_t)p.Bsz * p.H * ((p.L + 63) / 64) * p.M);
+  return launch_grad_finish(p, gi, stream);
 }
 
 template <typename T>

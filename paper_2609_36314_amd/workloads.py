@@ -8,7 +8,8 @@ state (decode), and for decode the per-step tokens step by step.
   x ~ N(0, 1);  B, C ~ N(0, 1/N);  dt = softplus(z - 2), z ~ N(0, 1) (not clipped)
   alpha: a constant, or one value per head drawn from U[lo, hi]
   tau: the paper's geometric bank on [1, 2^17] (built by the library, not here)
-  lambda, read/write logits and D are absent unless a test asks for them.
+  lambda, read/write logits and D are absent unless a test asks for them (then
+  lambda ~ U[0.25, 4], alpha ~ U[0.02, 1] per token, logits and D ~ N(0, 1)).
   Without B/C projections (bc False, dstate 1): B = C = 1, nothing drawn for them.
 
 The named workloads are the five benchmark configurations of the Frac layer at
@@ -100,9 +101,11 @@ def generate(w: Workload, seed: int = 0) -> dict:
         out["init_state"] = rng.standard_normal((Bsz, H, M, N, P), dtype=f32)
     if w.extras:
         lead = out["dt"].shape
-        out["lam"] = rng.uniform(0.5, 2.0, lead).astype(f32)
+        # the paper's ranges: lambda clipped to [0.25, 4], alpha = sigmoid(.) in (0, 1)
+        # (here down to 0.02, where lambda^{1/alpha} reaches 2^100)
+        out["lam"] = rng.uniform(0.25, 4.0, lead).astype(f32)
         out["read_logit"] = rng.standard_normal(lead + (M,), dtype=f32)
         out["write_logit"] = rng.standard_normal(lead + (M,), dtype=f32)
         out["D"] = rng.standard_normal(H, dtype=f32)
-        out["alpha"] = rng.uniform(0.3, 0.9, lead).astype(f32)
+        out["alpha"] = rng.uniform(0.02, 1.0, lead).astype(f32)
     return out

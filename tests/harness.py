@@ -51,7 +51,13 @@ def max_rel(got, ref) -> float:
 
 
 def assert_close(name, got, ref, tol):
+    """Relative L2 error within tol, and the largest element error relative to the
+    largest reference magnitude within 2 tol (an error confined to a few elements, one
+    head or one chunk fails the second)."""
     e = rel_l2(got, ref)
+    mr = max_rel(got, ref)
     assert np.all(np.isfinite(np.asarray(got, np.float64))), "%s: non-finite values" % name
-    assert e <= tol, "%s: relative L2 error %.3e > %.1e (max-rel %.3e)" % (name, e, tol, max_rel(got, ref))
+    assert e <= tol, "%s: relative L2 error %.3e > %.1e (max-rel %.3e)" % (name, e, tol, mr)
+    assert mr <= 2 * tol, "%s: max|err| / max|ref| = %.3e > %.1e (relative L2 %.3e)" % (name, mr, 2 * tol, e)
+    print("  %-24s rel-L2 %.2e  max-rel %.2e" % (name, e, mr), flush=True)
     return e

@@ -151,17 +151,27 @@ def test_projection_free_form_checks_its_arguments_on_the_host():
 
 
 @pytest.mark.parametrize("field", ["dalpha", "dlambda", "dread_logit", "dwrite_logit", "dinit_state"])
-def test_further_gradients_are_for_the_form_without_projections_only(field):
-    """dalpha, dlambda, the logit gradients and dinit_state exist for dstate 1 only;
-    asked for with B/C projections the call is refused on the host."""
+def test_further_gradients_are_accepted_for_both_forms(field):
+    """dalpha, dlambda, the logit gradients and dinit_state are produced with and without
+    B/C projections: with every required pointer given, the call passes validation and
+    stops only at the missing workspace (nothing is launched)."""
     lib = _lib.load()
-    sh = _shape()
-    assert sh.dstate > 1
     buf = (ctypes.c_float * 64)()
-    b = FracBwdArgs()
-    setattr(b, field, ctypes.cast(buf, ctypes.c_void_p))
-    assert lib.frac_scan_bwd(ctypes.byref(sh), ctypes.byref(b), None, 0, None) == -2
-    assert field in lib.frac_last_error().decode()
+    p = ctypes.cast(buf, ctypes.c_void_p)
+    for dstate in (16, 1):
+        sh = _shape()
+        sh.dstate = dstate
+        a = FracFwdArgs()
+        a.x = a.dt = a.alpha = a.tau = p
+        if dstate > 1:
+            a.Bm = a.Cm = p
+        b = FracBwdArgs()
+        b.fwd = a
+        b.dy = b.dx = b.ddt = p
+        if dstate > 1:
+            b.dBm = b.dCm = p
+        setattr(b, field, p)
+        assert lib.frac_scan_bwd(ctypes.byref(sh), ctypes.byref(b), None, 0, None) == -3, lib.frac_last_error()
 
 
 def test_parameter_construction_arguments_are_checked_on_the_host():

@@ -100,6 +100,50 @@ def test_bwd_parity_small(name):
         assert_close("dD", f64(g["dD"]), ref["dD"], tol)
 
 
+ALL_GRAD_CASES = ["f32 extras dfinal", "f32 M8 N128 extras dfinal", "bf16 M5 N96 P32 extras", "bf16 groups extras",
+                  "bf16 M8", "bf16 L1"]
+
+
+@pytest.mark.parametrize("moderate", [False, True])
+@pytest.mark.parametrize("name", ALL_GRAD_CASES)
+def test_bwd_all_gradients(name, moderate):
+    """With B/C projections: the gradients of alpha, lambda, both logits and the
+    initial state beside dx, ddt, dB, dC, dD.  The extras draw alpha and lambda over
+    the paper's ranges; `moderate` redraws them from alpha ~ U[0.3, 0.9], lambda ~
+    U[0.5, 2] (factors lambda^{1/alpha} up to 10).  In bfloat16 the gradient of the
+    final state is given with the moderate steps only (with large factors it limits
+    the step-size gradient to several percent: the final-state pairs enter its
+    telescoped sums through the bfloat16-rounded state and, separately, the rounded
+    adjoint)."""
+    w = CASES[name]
+    if moderate and not w.extras:
+        pytest.skip("no lambda or per-token alpha to redraw")
+    inp = device_inputs(w, seed=5)
+    if moderate:
+        g0 = torch.Generator().manual_seed(55)
+        shp = inp["dt"].shape
+        inp["alpha"] = (torch.rand(shp, generator=g0) * 0.6 + 0.3).cuda()
+        inp["lam"] = (torch.rand(shp, generator=g0) * 1.5 + 0.5).cuda()
+    tau_d, tau64 = _tau(w.nmodes)
+    dfs = inp.get("d_final_state")
+    if w.io_dtype == "bf16" and not moderate:
+        dfs = None
+    print("case", name, w, flush=True)
+    kw = {k: inp[k] for k in ("lam", "read_logit", "write_logit", "D", "init_state") if k in inp}
+    g = frac.scan_bwd(inp["x"], inp["dt"], inp["Bm"], inp["Cm"], inp["alpha"], tau_d, inp["dy"],
+                      d_final_state=dfs, all_grads=True, **kw)
+    torch.cuda.synchronize()
+    ref = _oracle_bwd(inp, tau64, dfs)
+    tol = TOL[w.io_dtype]
+    # (dalpha is per (b, t, h) on both sides, also where alpha is broadcast)
+    for k in ("dx", "ddt", "dBm", "dCm", "dinit_state", "dread_logit", "dwrite_logit", "dalpha"):
+        assert_close(k, f64(g[k]), ref[k], tol)
+    if "lam" in inp:
+        assert_close("dlambda", f64(g["dlambda"]), ref["dlambda"], tol)
+    if "D" in inp:
+        assert_close("dD", f64(g["dD"]), ref["dD"], tol)
+
+
 @pytest.mark.parametrize("io,M,N", [("f32", 4, 32), ("bf16", 4, 32), ("bf16", 8, 128)])
 def test_bwd_large_steps_use_direct_decay(io, M, N):
     """Steps large enough that r A_Q exceeds the factorisation bound for the fast
