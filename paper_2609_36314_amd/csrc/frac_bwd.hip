@@ -269,7 +269,9 @@ struct BwdWork {
   float* dc;          // [slots][B H L][M] partials of dL/dc: state sweep (per N part), then the intra kernel
   float* dk;          // [slots][B H L][M] partials of dL/dkappa: rows sweep (per P part), then the intra kernel
   float* F;           // [PS][B H][M] <dS_final, S_final> per mode (per N part)
+  float* I;           // [PS_rows][B H][M] <S_init, dS_init> per mode (per P part of the rows sweep)
   float* dDp;         // [B H] sum(dy . x)
+  float* dki;         // [B H L][M] the intra-chunk part of dL/dkappa (when the state sweep forms it)
 };
 
 // ------------------------------------------------ state / cols sweep layout
@@ -293,6 +295,22 @@ struct ColCfg {
 
 // ------------------------------------------------------------ state sweep
 
+// LDS of the state sweep (bytes): the staged tiles, the fixed arrays, one chunk's
+// weights; and whether the intra-chunk products of dc and dk (the masked H tile in
+// LDS) fit beside them (bfloat16 I/O).
+template <typename T, int MP, int NB>
+struct StateLds {
+  using Cfg = ColCfg<T, MP, NB>;
+  static constexpr int kTiles_ = (Cfg::NBUF * 64 * (2 * Cfg::XS + Cfg::BS) + 64 * Cfg::CS) * (int)sizeof(T);
+  static constexpr int kFixed = 64 * Cfg::XS * (int)sizeof(T) +
+                                (8 * Cfg::MPF * kQ + Exchange<Cfg::NACT>::kFloats + 4 * MP) * 4;
+  static constexpr int WSZ = (n_weight_arrays<kState>() + 2) * MP * kWQ;  // floats
+  static constexpr int kHH = 64 * Cfg::XS * (int)sizeof(T);
+  static constexpr int kLimit = 160 * 1024 - 512;
+  static constexpr bool kFold = sizeof(T) == 2 && kTiles_ + kFixed + kHH + WSZ * 4 <= kLimit;
+  static constexpr int NWB = kTiles_ + kFixed + (kFold ? kHH : 0) + 2 * WSZ * 4 <= kLimit ? 2 : 1;
+};
+
 template <typename T, int MP, int NB>
 __global__ void __launch_bounds__(512) frac_bwd_state_kernel(ScanParams p, BwdWork wk) {
   using Cfg = ColCfg<T, MP, NB>;
@@ -314,18 +332,20 @@ __global__ void __launch_bounds__(512) frac_bwd_state_kernel(ScanParams p, BwdWo
       Bb1[Cfg::NBUF == 2 ? 64 * BS : 8];
   __shared__ __align__(16) T Cb[64 * CS];
   constexpr int NWA = n_weight_arrays<kState>();
+  using Lds = StateLds<T, MP, NB>;
+  constexpr bool kFold = Lds::kFold;  // the intra-chunk parts of dc and dk formed here
   constexpr int oHG = 0;                                         // T [k][t] (Gamma o dY X^T)^T, causal
-  constexpr int WSZ = (NWA + 2) * MP * kWQ;                      // one chunk's weights and log-decays
+  constexpr int WSZ = Lds::WSZ;                                  // one chunk's weights and log-decays
   // two chunks' weights (the next one formed during this one's update) when LDS allows
-  constexpr int kTileBytes = (Cfg::NBUF * 64 * (2 * XS + BS) + 64 * CS) * (int)sizeof(T);
-  constexpr int kFixed = 64 * XS * (int)sizeof(T) + (8 * MPF * kQ + Ex::kFloats + 4 * MP) * 4;
-  constexpr int NWB = kTileBytes + kFixed + 2 * WSZ * 4 <= 160 * 1024 - 512 ? 2 : 1;
+  constexpr int NWB = Lds::NWB;
   constexpr int oW = oHG + 64 * XS * (int)sizeof(T);             // float weights, NWB chunks
   constexpr int oRd = oW + NWB * WSZ * 4;                        // float [8 waves][MPF][Q] token partials
   constexpr int oEx = oRd + 8 * MPF * kQ * 4;                    // float exchange
   constexpr int oSc = oEx + Ex::kFloats * 4;                     // float rates, log tau, scales
-  __shared__ __align__(16) unsigned char sm[oSc + 4 * MP * 4];
+  constexpr int oHH = (oSc + 4 * MP * 4 + 15) / 16 * 16;         // T [t][k] H = (C B^T) o (dY X^T), causal
+  __shared__ __align__(16) unsigned char sm[oHH + (kFold ? Lds::kHH : 16)];
   T* HGT = reinterpret_cast<T*>(sm + oHG);
+  T* HH = reinterpret_cast<T*>(sm + oHH);
   float* const W0 = reinterpret_cast<float*>(sm + oW);
   float* const W1 = W0 + (NWB - 1) * WSZ;
   float* redZ = reinterpret_cast<float*>(sm + oRd);
@@ -343,6 +363,7 @@ __global__ void __launch_bounds__(512) frac_bwd_state_kernel(ScanParams p, BwdWo
   }
   for (int i = tid; i < 64 * XS; i += 512) {
     HGT[i] = (T)0.0f;
+    if constexpr (kFold) HH[i] = (T)0.0f;
     Xb0[i] = Yb0[i] = (T)0.0f;
     Xb1[Cfg::NBUF == 2 ? i : 0] = Yb1[Cfg::NBUF == 2 ? i : 0] = (T)0.0f;
   }
@@ -492,6 +513,12 @@ __global__ void __launch_bounds__(512) frac_bwd_state_kernel(ScanParams p, BwdWo
         T* dst = HGT + (kb * 16 + li) * XS + tb * 16 + lg * 4;
 #pragma unroll
         for (int r = 0; r < 4; ++r) dst[r] = (T)hv[r];
+        if constexpr (kFold) {
+          T* hh = HH + (tb * 16 + lg * 4) * XS + kb * 16 + li;
+#pragma unroll
+          for (int r = 0; r < 4; ++r)
+            hh[r * XS] = (T)keep_if_ge(gcur.get(jt, r) * D[r], tb * 16 + lg * 4 + r, kb * 16 + li);
+        }
         {  // the tiles of the reverse sweeps, once per head: (C B^T) o Gamma from the
            // first workgroup of the head, Gamma o (dY X^T) from the last
           const int64_t to = ((int64_t)(b * nchunks + c) * H + h) * (kTiles * kTileElems) + tile * kTileElems + lane * 4;
@@ -556,18 +583,6 @@ __global__ void __launch_bounds__(512) frac_bwd_state_kernel(ScanParams p, BwdWo
     barrier();  // HG, token partials and exchange complete; C is free
     if (Cfg::NBUF == 2 && c + 1 < nchunks) stageC(c + 1);
 
-    // ---- the state part of dL/dc over this workgroup's rows of N:
-    // e^{-l_t} E_m sum over the N blocks (in order) of z
-    for (int i = tid; i < kQ * MP; i += 512) {
-      const int t = i / MP, m = i - t * MP;
-      if (m < M && t < nv) {
-        const int pt = m / MPF, j = m - pt * MPF;
-        float z = 0.0f;
-#pragma unroll
-        for (int q = 0; q < NBF; ++q) z += redZ[((pt * NBF + q) * MPF + j) * kQ + t];
-        dcg[(int64_t)(t0 + t) * M + m] = fexp(-P_lh[m * kWQ + t]) * Ecur[m] * z;
-      }
-    }
     if (ps == 0 && p.dD) {
       // sum(dy . x) of the chunk for dD: 8 consecutive columns of one token per
       // thread (columns past P hold zeros)
@@ -637,6 +652,95 @@ __global__ void __launch_bounds__(512) frac_bwd_state_kernel(ScanParams p, BwdWo
       }
     }
     }  // active
+
+    __builtin_amdgcn_sched_barrier(0);
+    // ---- the state part of dL/dc over this workgroup's rows of N: e^{-l_t} E_m times
+    // the sum over the N blocks (in order) of z; with the intra-chunk products here,
+    // the first workgroup of the head adds sum_{k<=t} H_{t,k} kappa_{k,m} e^{-(l_t - l_k)}
+    // (waves 0..3, row block = wave) and the last forms the intra-chunk part of dk,
+    // sum_{t'>=t} H_{t',t} c_{t',m} e^{-(l_t' - l_t)} (waves 4..7, column block = wave - 4)
+    if constexpr (!kFold) {
+      for (int i = tid; i < kQ * MP; i += 512) {
+        const int t = i / MP, m = i - t * MP;
+        if (m < M && t < nv) {
+          const int pt = m / MPF, j = m - pt * MPF;
+          float z = 0.0f;
+#pragma unroll
+          for (int q = 0; q < NBF; ++q) z += redZ[((pt * NBF + q) * MPF + j) * kQ + t];
+          dcg[(int64_t)(t0 + t) * M + m] = fexp(-P_lh[m * kWQ + t]) * Ecur[m] * z;
+        }
+      }
+    } else {
+      const int tb = wave & 3;
+      const bool cside = wave < 4;
+      const bool intra = cside ? ps == 0 : ps == Cfg::PS - 1;
+      constexpr int MB = (MP + 15) / 16;
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb) {
+        const int m = mb * 16 + li;
+        const int mm = m < MP ? m : 0;
+        const bool fac = m < MP && !((unsafe >> mm) & 1);
+        const bool direct = m < M && ((unsafe >> mm) & 1);
+        const float* lhm = P_lh + mm * kWQ;
+        const float* llm = P_ll + mm * kWQ;
+        floatx4 acc = {0.f, 0.f, 0.f, 0.f};
+        if (intra) {
+          if (cside) {
+            for (int kq = 0; kq < (tb + 1) * 4; ++kq) {
+              const int kk = kq * 4 + lg;
+              acc = __builtin_amdgcn_mfma_f32_16x16x4f32(to_f32(HH[(tb * 16 + li) * XS + kk]),
+                                                         fac ? P_Vt[mm * kWQ + kk] : 0.0f, acc, 0, 0, 0);
+            }
+          } else {
+            for (int tq = tb * 4; tq < 16; ++tq) {
+              const int t = tq * 4 + lg;
+              acc = __builtin_amdgcn_mfma_f32_16x16x4f32(to_f32(HH[t * XS + tb * 16 + li]),
+                                                         fac ? P_O[mm * kWQ + t] : 0.0f, acc, 0, 0, 0);
+            }
+          }
+        }
+        // modes past the factorisation bound: one exponential per pair, the lane's four
+        // rows in one loop
+        float dsum[4] = {0.f, 0.f, 0.f, 0.f};
+        if (intra && direct) {
+          const int tr0 = tb * 16 + lg * 4;
+          if (cside) {
+            for (int kk = 0; kk <= tr0 + 3; ++kk) {
+              const float v = P_Vt[mm * kWQ + kk];
+#pragma unroll
+              for (int r = 0; r < 4; ++r)
+                if (kk <= tr0 + r) dsum[r] += to_f32(HH[(tr0 + r) * XS + kk]) * v * ell_decay(lhm, llm, tr0 + r, kk);
+            }
+          } else {
+            for (int t2 = tr0; t2 < 64; ++t2) {
+              const float v = P_O[mm * kWQ + t2];
+#pragma unroll
+              for (int r = 0; r < 4; ++r)
+                if (t2 >= tr0 + r) dsum[r] += to_f32(HH[t2 * XS + tr0 + r]) * v * ell_decay(lhm, llm, t2, tr0 + r);
+            }
+          }
+        }
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int t = tb * 16 + lg * 4 + r;
+          if (cside) {
+            float z = 0.0f;
+            if (m < M) {
+              const int pt = m / MPF, j = m - pt * MPF;
+#pragma unroll
+              for (int q = 0; q < NBF; ++q) z += redZ[((pt * NBF + q) * MPF + j) * kQ + t];
+            }
+            float v = (m < M ? Ecur[mm] : 0.0f) * z;
+            if (intra && !direct) v += acc[r];
+            const float dc = fexp(-lhm[t]) * v + dsum[r];
+            if (m < M && t < nv) dcg[(int64_t)(t0 + t) * M + m] = dc;
+          } else if (intra) {
+            const float dk = direct ? dsum[r] : fexp(lhm[t]) * acc[r];
+            if (m < M && t < nv) wk.dki[(bh_i * L + t0 + t) * M + m] = dk;
+          }
+        }
+      }
+    }
     if constexpr (NWB == 2) {
       if (c + 1 < nchunks) weights(c + 1, Wn);
     }
@@ -1335,6 +1439,39 @@ __global__ void __launch_bounds__(512) frac_bwd_rows_kernel(ScanParams p, BwdWor
             p.dinit_state[sbase + lo + ((int64_t)m * N + jb * 16 + r) * P] = Gs[m][jb][r] * Ef[mo + m];
         }
   }
+
+  // ---- the initial-state term <S_init, dS_init> per mode over this workgroup's columns:
+  // per wave, then over the waves holding each mode in a fixed order
+  barrier();  // the token partials are no longer read
+  {
+    const float* Ef = s_E2 + (nchunks & 1) * MP;
+    int lo = (mo * N + nbo * 16 + lg * 4) * P + pc;
+    asm volatile("" : "+v"(lo));
+#pragma unroll
+    for (int m = 0; m < MPW; ++m) {
+      float ip = 0.0f;
+#pragma unroll
+      for (int jb = 0; jb < NBW; ++jb)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int n = (nbo + jb) * 16 + lg * 4 + r;
+          if (p.init_state && active && mo + m < M && n < N && pc < P)
+            ip += p.init_state[sbase + lo + ((int64_t)m * N + jb * 16 + r) * P] * Gs[m][jb][r];
+        }
+      ip = group_allreduce<64>(ip, [](float x, float y) { return x + y; });
+      if (lane == 0) redW[wave * MPW + m] = (active && mo + m < M) ? ip * Ef[mo + m] : 0.0f;
+    }
+  }
+  barrier();
+  if (tid < M) {
+    float s = 0.0f;
+    for (int w = 0; w < 8; ++w) {
+      const int pw = w / Cfg::NPW;
+      const int mow = Cfg::kModeSplit ? pw * MPW : 0;
+      if (pw < NPART && tid >= mow && tid < mow + MPW) s += redW[w * MPW + tid - mow];
+    }
+    wk.I[((int64_t)ps * p.Bsz * H + (int64_t)b * H + h) * M + tid] = s;
+  }
 }
 
 // ------------------------------------------------------ intra-chunk parts
@@ -1515,7 +1652,7 @@ int state_parts(const ScanParams& p) { return pad_modes(p.M) * (p.NP / 16) > 32 
 int rows_parts(const ScanParams& p) { return (pad_modes(p.M) >= 8 && p.io_bf16) ? 2 : 1; }
 
 struct BwdLayout {
-  size_t tiles, gg, hg, dBp, dCp, dc, dk, F, dDp, gtl, total;
+  size_t tiles, gg, hg, dBp, dCp, dc, dk, F, I, dDp, gtl, total;
 };
 
 BwdLayout bwd_layout(const ScanParams& p) {
@@ -1532,7 +1669,8 @@ BwdLayout bwd_layout(const ScanParams& p) {
   l.dc = l.dCp + up(bl * p.H * p.N * es);
   l.dk = l.dc + up(sizeof(float) * (state_parts(p) + 1) * blhm);
   l.F = l.dk + up(sizeof(float) * (rows_parts(p) + 1) * blhm);
-  l.dDp = l.F + up(sizeof(float) * state_parts(p) * bh * p.M);
+  l.I = l.F + up(sizeof(float) * state_parts(p) * bh * p.M);
+  l.dDp = l.I + up(sizeof(float) * rows_parts(p) * bh * p.M);
   l.gtl = l.dDp + up(sizeof(float) * bh);
   l.total = l.gtl + up(grad_tiles_bytes(p));
   return l;
@@ -1555,8 +1693,13 @@ hipError_t launch_bwd_variant(const ScanParams& p, void* ws, hipStream_t stream)
   wk.dc = reinterpret_cast<float*>(base + l.dc);
   wk.dk = reinterpret_cast<float*>(base + l.dk);
   wk.F = reinterpret_cast<float*>(base + l.F);
+  wk.I = reinterpret_cast<float*>(base + l.I);
   wk.dDp = reinterpret_cast<float*>(base + l.dDp);
 
+  constexpr bool kFold = StateLds<T, MP, NB>::kFold;
+  // dc: the state sweep's parts (the first with the intra-chunk part when folded), then
+  // the intra kernel's; dk: the rows sweep's parts, then the intra-chunk part
+  wk.dki = wk.dk + RC::PS * blhm;
   hipError_t e = launch_cb_tiles(p, base + l.tiles, stream);
   if (e != hipSuccess) return e;
   const int bh = p.Bsz * p.H;
@@ -1566,23 +1709,26 @@ hipError_t launch_bwd_variant(const ScanParams& p, void* ws, hipStream_t stream)
   if ((e = hipGetLastError()) != hipSuccess) return e;
   hipLaunchKernelGGL((frac_bwd_cols_kernel<T, MP, NB>), dim3(bh * SC::PS), dim3(512), 0, stream, p, wk);
   if ((e = hipGetLastError()) != hipSuccess) return e;
-  {
+  if constexpr (!kFold) {
     const int64_t nblk = (int64_t)p.Bsz * ((p.L + kQ - 1) / kQ) * p.H;
     hipLaunchKernelGGL((frac_bwd_intra_kernel<T, MP>), dim3((unsigned)nblk), dim3(256), 0, stream, p,
-                       reinterpret_cast<const T*>(base + l.tiles), wk.dc + SC::PS * blhm, wk.dk + RC::PS * blhm);
+                       reinterpret_cast<const T*>(base + l.tiles), wk.dc + SC::PS * blhm, wk.dki);
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
   GradInputs gi;
   gi.dc = wk.dc;
   gi.dk = wk.dk;
-  gi.ndc = SC::PS + 1;
-  gi.ndk = RC::PS + 1;
+  gi.dki = wk.dki;
+  gi.ndc = SC::PS + (kFold ? 0 : 1);
+  gi.ndk = RC::PS;
+  gi.ndki = 1;
   gi.F = wk.F;
   gi.nF = SC::PS;
+  gi.I = wk.I;
+  gi.nI = RC::PS;
   gi.dDp = wk.dDp;
   gi.nD = 1;
-  gi.tileV = reinterpret_cast<float*>(base + l.gtl);
-  gi.tileF = reinterpret_cast<int*>(base + l.gtl + sizeof(float) * (size_t)p.Bsz * p.H * ((p.L + 63) / 64) * p.M);
+  grad_tiles_at(p, base + l.gtl, gi);
   if ((e = launch_grad_finish(p, gi, stream)) != hipSuccess) return e;
   const int64_t nrows = (int64_t)p.Bsz * p.L;
   const int64_t nthr = nrows * p.G * (p.N / (16 / (int)sizeof(T)));

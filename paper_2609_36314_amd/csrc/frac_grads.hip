@@ -14,23 +14,44 @@
 //
 // The retention rho enters through the decays between tokens, exp(-sum of x over the
 // tokens between them).  Differentiating every decay that spans token j by x_j gives
-// the telescoped form (derived here; the paper does not state a backward pass):
+// (derived here; the paper does not state a backward pass)
 //
 //   d dtt_j = sum_m r_m mu_{j,m} X_m(j) + sum_m r_m rho_{j,m} w_{j,m} dk_{j,m}
-//   X_m(j)  = -(sum_{t' = j}^{j2 - 1} g_{t',m}  [+ <dS_final, S_final>_m if j2 = L])
-//   g_{t,m} = c_{t,m} dc_{t,m} - kappa_{t,m} dk_{t,m}
+//   X_m(j)  = -R_m(j),   R_m(j) = <rho_{j,m} dS_{j,m}, S_{j-1,m}>
 //
-// where j2 is the first token after j whose exponent x reaches the cut X_cut in mode m
-// (L if none) and mu_{j,m} is 1 when x_{j,m} is below it.  Every decay across such a
-// token is at most e^{-X_cut}, so what lies beyond it, and the token's own term
-// (proportional to that decay), is below the rounding of the path: the sum stops there
-// and the term is dropped.  X_cut is 16 for float32 I/O (e^{-16} ~ 1.1e-7) and 8 for
-// bfloat16 I/O (e^{-8} ~ 3.4e-4; the matrix-core operands of the state and adjoint
-// updates carry 2^-9 relative rounding).  Without the stop, the suffix sum across such
-// a token is a difference of terms whose exact value is near zero: each term is
-// formed once from the state side (dc) and once from the adjoint side (dk), each
-// rounded its own way, and that rounding, multiplied by r_m lambda^{1/alpha} (up to
-// 2^100), would swamp ddt.
+// R_m(j) pairs the adjoint carried back across token j with the state carried into
+// it.  It is never formed from the states (N x P per token and mode) but from the
+// per-(token, mode) partials, in one of three exact forms:
+//
+//   chunk-local, for j in a chunk C (the 64 tokens of one tile):
+//     R_m(j) = e^{-(l_end - l_start)} <G_C, S_C>_m + sum_{k in C, k < j} kappa_k dk^inter_k
+//              + sum_{t in C, t >= j} (c_t dc_t - kappa_t dk^intra_t)
+//     where dk = dk^inter + dk^intra splits the adjoint at the chunk's end (G_C, carried
+//     in from the later chunks) from the chunk's own readouts, S_C is the state before
+//     the chunk and l_end - l_start the chunk's total exponent;
+//   suffix:  R_m(j) = <dS_final, S_final>_m + sum_{t >= j} g_t
+//   prefix:  R_m(j) = <S_init, dS_init>_m - sum_{t < j} g_t,   g_t = c_t dc_t - kappa_t dk_t
+//
+// Every term of the chunk-local form carries the decay across token j, so the form
+// keeps the relative rounding of its terms, but its first term needs the state and
+// the adjoint at the chunk boundary together.  Where the chunk's total exponent
+// reaches X_cut that term is at most e^{-X_cut} of a pairing and is dropped: such a
+// "cut" chunk takes the chunk-local form without it.  The suffix and prefix forms
+// telescope: their terms largely cancel (what is written on one side of j and read on
+// the same side is not in R), each term is formed once from the state side (dc) and
+// once from the adjoint side (dk), each rounded its own way, and r_m lambda^{1/alpha}
+// (up to 2^100) multiplies what is left.  They serve the chunks that are not cut, and
+// every such sum stops at the nearest cut chunk, whose boundary values the chunk-local
+// form gives exactly: sum_{t in C} (c dc - kappa dk^intra) at the first token of a cut
+// chunk C, sum_{k in C} kappa dk^inter at the first token after it.  Each token of a
+// chunk that is not cut takes the form (suffix or prefix) whose range carries the
+// smaller sum of magnitudes |c dc| + |kappa dk|, the rounding of a sum growing with it.
+//
+// mu_{j,m} is 0 where x_{j,m} itself reaches X_cut: the term is then at most e^{-X_cut}
+// of the pairing it scales (and exactly 0 where the exponent is held at its cap).
+// X_cut is 16 for float32 I/O (e^{-16} ~ 1.1e-7) and 8 for bfloat16 I/O (e^{-8} ~
+// 3.4e-4; the matrix-core operands of the state and adjoint updates carry 2^-9
+// relative rounding).  A token at or past the cut lies in a cut chunk.
 //
 // Then ddt = s d dtt with s = lambda^{1/alpha}, and with ds = ddt dt:
 //   dalpha  = -sum_m (dz_c + dz_w)_m ln tau_m - ds ln(lambda) / alpha^2
@@ -40,10 +61,11 @@
 // 2^100: the held value does not depend on them).
 //
 // Two kernels, one workgroup of four waves (four heads, lane = token) per 64-token
-// tile: the first sums the partials and forms, per mode, the tile's head segment
-// (the sum of g from the tile's first token up to its first capped token); the
-// second forms the carry from the later tiles' segments, the segmented suffix sums
-// inside the tile, and every output.  All sums run in a fixed order.
+// tile: the first sums the partials and forms, per mode, whether the tile is cut and
+// its two segment values (the sums that the suffix and the prefix forms carry across
+// it, with the sums of magnitudes); the second forms the carries from the later and
+// the earlier tiles, the sums inside the tile, and every output.  All sums run in a
+// fixed order.
 #include "frac_device.h"
 #include "frac_kernels.h"
 
@@ -118,45 +140,117 @@ __device__ __forceinline__ void token_coef(const ScanParams& p, int b, int t, in
   softmax_fast<MP>(k.w, M);
 }
 
-// Composition of the maps z -> v_j + a_j z of lanes j .. 63 (a in {0, 1}), as (A, V).
-__device__ __forceinline__ void suffix_affine(float& A, float& V) {
+__device__ __forceinline__ float wave_sum(float v) {
+  return group_allreduce<64>(v, [](float x, float y) { return x + y; });
+}
+
+// Sum over lanes j .. 63 (inclusive suffix) and over lanes 0 .. j - 1 (exclusive prefix).
+__device__ __forceinline__ float suffix_sum(float v) {
   const int lane = threadIdx.x & 63;
 #pragma unroll
   for (int d = 1; d < 64; d <<= 1) {
-    const float Ad = __shfl_down(A, d, 64), Vd = __shfl_down(V, d, 64);
-    if (lane + d < 64) {
-      V = V + A * Vd;
-      A = A * Ad;
+    const float u = __shfl_down(v, d, 64);
+    if (lane + d < 64) v += u;
+  }
+  return v;
+}
+
+__device__ __forceinline__ float prefix_sum_excl(float v) {
+  const int lane = threadIdx.x & 63;
+  float s = v;
+#pragma unroll
+  for (int d = 1; d < 64; d <<= 1) {
+    const float u = __shfl_up(s, d, 64);
+    if (lane >= d) s += u;
+  }
+  const float e = __shfl_up(s, 1, 64);
+  return lane == 0 ? 0.0f : e;
+}
+
+// Per (tile, mode): the value the suffix form carries across the tile (vs) and the
+// prefix form (vp), with the sums of magnitudes (ns, np).  A cut tile stops both
+// carries and supplies the chunk-local boundary values.
+struct TileSeg {
+  float vs, ns, vp, np;
+};
+
+// Sum of the later tiles' suffix values, up to and including the first cut tile, else
+// up to the final-state term Fm (a virtual cut tile after the last).  Wave-uniform.
+__device__ __forceinline__ void suffix_carry(const TileSeg* seg, const int* tileF, int64_t row, int tile, int ntiles,
+                                             int M, int m, float Fm, float& cv, float& cn) {
+  const int lane = threadIdx.x & 63;
+  cv = cn = 0.0f;
+  for (int g0 = tile + 1; g0 <= ntiles; g0 += 64) {
+    const int tj = g0 + lane;
+    float v = 0.0f, n = 0.0f;
+    bool stop_here = false;
+    if (tj < ntiles) {
+      const TileSeg sg = seg[(row + tj) * M + m];
+      v = sg.vs;
+      n = sg.ns;
+      stop_here = tileF[(row + tj) * M + m] != 0;
+    } else if (tj == ntiles) {
+      v = Fm;
+      stop_here = true;
     }
+    const uint64_t sb = __ballot(stop_here);
+    const int stop = sb ? __builtin_ctzll(sb) : 64;  // the last lane taken
+    const bool take = lane <= stop && tj <= ntiles;
+    cv += wave_sum(take ? v : 0.0f);
+    cn += wave_sum(take ? n : 0.0f);
+    if (stop < 64) break;
   }
 }
 
-// The carry into `tile` from the later tiles of one (batch, head) and mode: the sum
-// of their head segments up to the first capped token, the final-state term Fm as
-// the segment of a virtual tile after the last.  Wave-uniform.
-__device__ __forceinline__ float tile_carry(const float* tileV, const int* tileF, int64_t row, int tile, int ntiles,
-                                            int M, int m, float Fm) {
+// The same for the prefix form: the earlier tiles, nearest first, up to and including
+// the first cut tile, else down to the initial-state term Im (a virtual cut tile
+// before the first).
+__device__ __forceinline__ void prefix_carry(const TileSeg* seg, const int* tileF, int64_t row, int tile, int M,
+                                             int m, float Im, float& cv, float& cn) {
   const int lane = threadIdx.x & 63;
-  float sum = 0.0f;
-  for (int g0 = tile + 1; g0 <= ntiles; g0 += 64) {
-    const int tj = g0 + lane;
-    float v = 0.0f;
-    int f = 3;  // bit 0: first token below the cap; bit 1: no capped token after it in the tile
-    if (tj < ntiles) {
-      v = tileV[(row + tj) * M + m];
-      f = tileF[(row + tj) * M + m];
-    } else if (tj == ntiles) {
-      v = Fm;
+  cv = cn = 0.0f;
+  for (int g0 = tile - 1; g0 >= -1; g0 -= 64) {
+    const int tj = g0 - lane;
+    float v = 0.0f, n = 0.0f;
+    bool stop_here = false;
+    if (tj >= 0) {
+      const TileSeg sg = seg[(row + tj) * M + m];
+      v = sg.vp;
+      n = sg.np;
+      stop_here = tileF[(row + tj) * M + m] != 0;
+    } else if (tj == -1) {
+      v = Im;
+      stop_here = true;
     }
-    // tile j is cut off by its own first token, or by a capped token inside tile j - 1
-    const uint64_t self = __ballot(!(f & 1));
-    const uint64_t after = __ballot(!(f & 2));
-    const uint64_t stop_mask = self | (after << 1);
-    const int stop = stop_mask ? __builtin_ctzll(stop_mask) : 64;
-    sum += group_allreduce<64>(lane < stop ? v : 0.0f, [](float x, float y) { return x + y; });
-    if (stop < 64 || ((after >> 63) & 1)) break;
+    const uint64_t sb = __ballot(stop_here);
+    const int stop = sb ? __builtin_ctzll(sb) : 64;
+    const bool take = lane <= stop && tj >= -1;
+    cv += wave_sum(take ? v : 0.0f);
+    cn += wave_sum(take ? n : 0.0f);
+    if (stop < 64) break;
   }
-  return sum;
+}
+
+// The two anchors of one (batch, head, mode): <dS_final, S_final> and <S_init, dS_init>.
+__device__ __forceinline__ void anchors(const GradInputs& gi, int64_t SF, int64_t i, float& Fm, float& Im) {
+  Fm = Im = 0.0f;
+  for (int q = 0; q < gi.nF; ++q) Fm += gi.F[q * SF + i];
+  for (int q = 0; q < gi.nI; ++q) Im += gi.I[q * SF + i];
+}
+
+// Sums the partial slots of one kind for this lane's token into v (zero past the sequence).
+template <int MP>
+__device__ __forceinline__ void sum_slots(const float* base, int n, int64_t S, int64_t i0, int M, bool valid,
+                                          float* v) {
+#pragma unroll
+  for (int m = 0; m < MP; ++m) v[m] = 0.0f;
+  if (!valid) return;
+  for (int q = 0; q < n; ++q) {
+    float u[MP];
+    load_modes<MP>(base + q * S + i0, M, u);
+#pragma unroll
+    for (int m = 0; m < MP; ++m) v[m] += u[m];
+  }
 }
 
 template <int MP>
@@ -182,40 +276,41 @@ __global__ void __launch_bounds__(256) frac_grad_tiles_kernel(ScanParams p, Grad
   const int64_t bh = (int64_t)b * p.H + h;
   const int64_t S = (int64_t)p.Bsz * p.H * L * M;
   const int64_t i0 = (bh * L + t) * M;
-  float dc[MP], dk[MP];
-#pragma unroll
-  for (int m = 0; m < MP; ++m) dc[m] = dk[m] = 0.0f;
-  if (valid) {
-    for (int q = 0; q < gi.ndc; ++q) {
-      float v[MP];
-      load_modes<MP>(gi.dc + q * S + i0, M, v);
-#pragma unroll
-      for (int m = 0; m < MP; ++m) dc[m] += v[m];
-    }
-    for (int q = 0; q < gi.ndk; ++q) {
-      float v[MP];
-      load_modes<MP>(gi.dk + q * S + i0, M, v);
-#pragma unroll
-      for (int m = 0; m < MP; ++m) dk[m] += v[m];
-    }
-    store_modes<MP>(gi.dc + i0, M, dc);  // the sums, for the second kernel
-    store_modes<MP>(gi.dk + i0, M, dk);
+  float dc[MP], dkx[MP], dki[MP];
+  sum_slots<MP>(gi.dc, gi.ndc, S, i0, M, valid, dc);
+  sum_slots<MP>(gi.dk, gi.ndk, S, i0, M, valid, dkx);
+  sum_slots<MP>(gi.dki, gi.ndki, S, i0, M, valid, dki);
+  if (valid) {  // the sums, for the second kernel
+    store_modes<MP>(gi.dc + i0, M, dc);
+    store_modes<MP>(gi.dk + i0, M, dkx);
+    store_modes<MP>(gi.dki + i0, M, dki);
   }
   const int64_t row = bh * ntiles;
+  const float xcut = cut_exponent(p);
+  TileSeg* seg = reinterpret_cast<TileSeg*>(gi.tileV);
 #pragma unroll
   for (int m = 0; m < MP; ++m) {
     if (m >= M) continue;  // wave-uniform
-    const float x = s_rr[m] * k.dtt;
-    const bool capped = valid && !(x < cut_exponent(p));
+    const float x = capped_exponent(s_rr[m], k.dtt);
+    const bool cut = !(wave_sum(valid ? x : 0.0f) < xcut);
     const float kap = one_minus_exp_neg(x) * k.w[m];
-    const float g = valid ? k.c[m] * dc[m] - kap * dk[m] : 0.0f;
-    const uint64_t cb = __ballot(capped);
-    const uint64_t after = cb & ~1ull;
-    const int fc = after ? __builtin_ctzll(after) : 64;
-    const float V = group_allreduce<64>(lane < fc ? g : 0.0f, [](float a, float c) { return a + c; });
+    const float rd = k.c[m] * dc[m], wx = kap * dkx[m], wi = kap * dki[m];
+    TileSeg sg;
+    if (cut) {
+      sg.vs = wave_sum(rd - wi);
+      sg.ns = wave_sum(fabsf(rd) + fabsf(wi));
+      sg.vp = wave_sum(wx);
+      sg.np = wave_sum(fabsf(wx));
+    } else {
+      const float g = rd - (wx + wi);
+      sg.vs = wave_sum(g);
+      sg.ns = wave_sum(fabsf(rd) + fabsf(wx + wi));
+      sg.vp = -sg.vs;
+      sg.np = sg.ns;
+    }
     if (lane == 0) {
-      gi.tileV[(row + tile) * M + m] = V;
-      gi.tileF[(row + tile) * M + m] = (capped ? 0 : 1) | (after ? 0 : 2);
+      seg[(row + tile) * M + m] = sg;
+      gi.tileF[(row + tile) * M + m] = cut ? 1 : 0;
     }
   }
 }
@@ -243,39 +338,51 @@ __global__ void __launch_bounds__(256) frac_grad_finish_kernel(ScanParams p, Gra
   const int64_t bh = (int64_t)b * H + h;
   const int64_t i0 = (bh * L + t) * M;
   float dc[MP], dk[MP];
-#pragma unroll
-  for (int m = 0; m < MP; ++m) dc[m] = dk[m] = 0.0f;
-  if (valid) {
-    load_modes<MP>(gi.dc + i0, M, dc);
-    load_modes<MP>(gi.dk + i0, M, dk);
-  }
   const int64_t row = bh * ntiles;
   const int64_t SF = (int64_t)p.Bsz * H * M;
+  const float xcut = cut_exponent(p);
+  const TileSeg* seg = reinterpret_cast<const TileSeg*>(gi.tileV);
   float ddtt = 0.0f, scd = 0.0f, swd = 0.0f;
   float beta[MP];
+  {
+    float dkx[MP], dki[MP];
 #pragma unroll
-  for (int m = 0; m < MP; ++m) {
-    beta[m] = 0.0f;
-    if (m >= M) continue;  // wave-uniform
-    const float r = s_rr[m];
-    const float x = r * k.dtt;
-    const bool mu = x < cut_exponent(p);
-    const float rho = __expf(-x);
-    beta[m] = one_minus_exp_neg(x);
-    const float kap = beta[m] * k.w[m];
-    const float g = valid ? k.c[m] * dc[m] - kap * dk[m] : 0.0f;
-    float Fm = 0.0f;
-    for (int q = 0; q < gi.nF; ++q) Fm += gi.F[q * SF + bh * M + m];
-    const float carry = tile_carry(gi.tileV, gi.tileF, row, tile, ntiles, M, m, Fm);
-    // acc_j = g_j + mu_{j+1} acc_{j+1} inside the tile, acc after the last lane = carry
-    const float mu_next = __shfl_down(mu ? 1.0f : 0.0f, 1, 64);
-    float A = (lane == 63) ? 1.0f : mu_next, V = g;  // tokens past the sequence: mask 1, g 0
-    suffix_affine(A, V);
-    const float acc = V + A * carry;
+    for (int m = 0; m < MP; ++m) dc[m] = dkx[m] = dki[m] = 0.0f;
     if (valid) {
-      ddtt += r * (mu ? -acc : 0.0f) + r * rho * k.w[m] * dk[m];
-      scd += k.c[m] * dc[m];
-      swd += k.w[m] * (beta[m] * dk[m]);
+      load_modes<MP>(gi.dc + i0, M, dc);
+      load_modes<MP>(gi.dk + i0, M, dkx);
+      load_modes<MP>(gi.dki + i0, M, dki);
+    }
+#pragma unroll
+    for (int m = 0; m < MP; ++m) {
+      dk[m] = dkx[m] + dki[m];
+      beta[m] = 0.0f;
+      if (m >= M) continue;  // wave-uniform
+      const float r = s_rr[m];
+      const float x = capped_exponent(r, k.dtt);
+      const bool mu = x < xcut;
+      const float rho = __expf(-x);
+      beta[m] = one_minus_exp_neg(x);
+      const float kap = beta[m] * k.w[m];
+      const float rd = k.c[m] * dc[m], wx = kap * dkx[m], wi = kap * dki[m];
+      float R;
+      if (gi.tileF[(row + tile) * M + m]) {  // cut tile: the chunk-local form
+        R = prefix_sum_excl(wx) + suffix_sum(rd - wi);
+      } else {
+        float Fm, Im, cv, cn;
+        anchors(gi, SF, bh * M + m, Fm, Im);
+        const float g = rd - (wx + wi), a = fabsf(rd) + fabsf(wx + wi);
+        suffix_carry(seg, gi.tileF, row, tile, ntiles, M, m, Fm, cv, cn);
+        const float rs = cv + suffix_sum(g), ns = cn + suffix_sum(a);
+        prefix_carry(seg, gi.tileF, row, tile, M, m, Im, cv, cn);
+        const float rp = cv - prefix_sum_excl(g), np = cn + prefix_sum_excl(a);
+        R = (np < ns) ? rp : rs;
+      }
+      if (valid) {
+        ddtt += r * (mu ? -R : 0.0f) + r * rho * k.w[m] * dk[m];
+        scd += k.c[m] * dc[m];
+        swd += k.w[m] * (beta[m] * dk[m]);
+      }
     }
   }
   const int64_t tok = ((int64_t)b * L + t) * H + h;
@@ -326,7 +433,13 @@ hipError_t launch_grads_mp(const ScanParams& p, const GradInputs& gi, hipStream_
 
 size_t grad_tiles_bytes(const ScanParams& p) {
   const size_t n = (size_t)p.Bsz * p.H * ((p.L + 63) / 64) * p.M;
-  return n * (sizeof(float) + sizeof(int));
+  return n * (sizeof(TileSeg) + sizeof(int));
+}
+
+void grad_tiles_at(const ScanParams& p, void* base, GradInputs& gi) {
+  const size_t n = (size_t)p.Bsz * p.H * ((p.L + 63) / 64) * p.M;
+  gi.tileV = reinterpret_cast<float*>(base);
+  gi.tileF = reinterpret_cast<int*>(reinterpret_cast<unsigned char*>(base) + n * sizeof(TileSeg));
 }
 
 hipError_t launch_grad_finish(const ScanParams& p, const GradInputs& gi, hipStream_t stream) {

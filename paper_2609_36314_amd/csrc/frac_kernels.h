@@ -105,25 +105,32 @@ hipError_t launch_nfree_bwd(const ScanParams& p, void* ws, hipStream_t stream);
 
 // Gradients of dt, alpha, lambda, the read / write logits and D from the
 // per-(token, mode) partials of a reverse sweep (frac_grads.hip):
-//   dc [ndc][B H L][M]  partials of dL/dc_{t,m}      (slot 0 is overwritten with the sum)
-//   dk [ndk][B H L][M]  partials of dL/dkappa_{t,m}  (likewise)
+//   dc [ndc][B H L][M]    partials of dL/dc_{t,m}  (slot 0 is overwritten with the sum)
+//   dk [ndk][B H L][M]    partials of the inter-chunk part of dL/dkappa_{t,m} (through
+//                         the adjoint carried in from the later chunks; likewise)
+//   dki [ndki][B H L][M]  partials of its intra-chunk part (likewise)
 //   F  [nF][B H][M]     partials of <dS_final, S_final> per mode (the final-state term)
+//   I  [nI][B H][M]     partials of <S_init, dS_init> per mode (the initial-state term)
 //   dDp [nD][B H]       partials of sum(dy . x)
-//   tileV, tileF        scratch of grad_tiles_bytes(p) bytes (tileV first, then tileF)
+//   tileV, tileF        scratch of grad_tiles_bytes(p) bytes, placed by grad_tiles_at
 // Writes p.ddt and, where non-NULL, p.dalpha, p.dlambda, p.dread_logit,
 // p.dwrite_logit and p.dD.
 struct GradInputs {
   float* dc;
   float* dk;
-  int ndc, ndk;
+  float* dki;
+  int ndc, ndk, ndki;
   const float* F;
   int nF;
+  const float* I;
+  int nI;
   const float* dDp;
   int nD;
   float* tileV;
   int* tileF;
 };
 size_t grad_tiles_bytes(const ScanParams& p);
+void grad_tiles_at(const ScanParams& p, void* base, GradInputs& gi);
 hipError_t launch_grad_finish(const ScanParams& p, const GradInputs& gi, hipStream_t stream);
 
 // True when a kernel variant exists for these sizes (M, N, P, dtype).

@@ -336,9 +336,12 @@ __global__ void __launch_bounds__(256) frac_nfree_fwd_kernel(ScanParams p, float
 struct NfWork {
   const float* ckpt;  // [B H][nchunks + 1][M][P] states entering each chunk, then the final state
   float* F;           // [nps][B H][M] <dS_final, S_final>_m over this workgroup's columns
+  float* I;           // [nps][B H][M] <S_init, dS_init>_m over this workgroup's columns
   float* dDp;         // [nps][B H] sum dy . x over this workgroup's columns
   float* dcp;         // [nps][B H L][M] <h_{t,m}, dy_t>: gradient of the read weight c_{t,m}
-  float* dkp;         // [nps][B H L][M] <G_{t,m}, x_t>: gradient of the injection kappa_{t,m}
+  float* dkp;         // [nps][B H L][M] <G_{t,m}, x_t>: gradient of the injection kappa_{t,m},
+                      // the part through the adjoint carried in from the later chunks
+  float* dkip;        // [nps][B H L][M] its part through the chunk's own readouts
 };
 
 template <typename T, int MP>
@@ -637,18 +640,20 @@ __global__ void __launch_bounds__(256, 2) frac_nfree_bwd_kernel(ScanParams p, Nf
           const int t = tb * 16 + lg * 4 + r;
           const float ea = fexp(-lhm[t]);
           float dc = ea * Uk[mb][r];
-          float dk = ell_decay(lhm, llm, kQ - 1, t) * Zk[mb][r];
+          const float dk = ell_decay(lhm, llm, kQ - 1, t) * Zk[mb][r];
+          float dki = 0.0f;
           if (!direct) {
             dc += ea * cI[r];
-            dk += fexp(lhm[t]) * kI[r];
+            dki = fexp(lhm[t]) * kI[r];
           } else {
             for (int k = 0; k <= t; ++k) dc += to_f32(HT[t * XS + k]) * P_Vt[mm * WQ + k] * ell_decay(lhm, llm, t, k);
-            for (int t2 = t; t2 < 64; ++t2) dk += to_f32(HT[t2 * XS + t]) * P_c[mm * WQ + t2] * ell_decay(lhm, llm, t2, t);
+            for (int t2 = t; t2 < 64; ++t2) dki += to_f32(HT[t2 * XS + t]) * P_c[mm * WQ + t2] * ell_decay(lhm, llm, t2, t);
           }
           if (m < M && t < nv) {
             const int64_t i = ((int64_t)ps * p.Bsz * H * L + (int64_t)bh * L + t0 + t) * M + m;  // [nps][B H L][M]
             wk.dcp[i] = dc;
             wk.dkp[i] = dk;
+            wk.dkip[i] = dki;
           }
         }
       }
@@ -733,7 +738,8 @@ __global__ void __launch_bounds__(256, 2) frac_nfree_bwd_kernel(ScanParams p, Nf
     }
   }
 
-  // ---- the adjoint of the state before token 0
+  // ---- the adjoint of the state before token 0, and the initial-state term
+  // <S_init, dS_init> per mode over this workgroup's columns
   if (p.dinit_state && active) {
 #pragma unroll
     for (int mb = 0; mb < MB; ++mb)
@@ -743,10 +749,22 @@ __global__ void __launch_bounds__(256, 2) frac_nfree_bwd_kernel(ScanParams p, Nf
         if (m < M && pc < P) p.dinit_state[sbase + (int64_t)m * P + pc] = G[mb][r];
       }
   }
+  __syncthreads();  // red is free again
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int m = mb * 16 + lg * 4 + r;
+      const float ip = (p.init_state && active && m < M && pc < P) ? p.init_state[sbase + (int64_t)m * P + pc] * G[mb][r]
+                                                                    : 0.0f;
+      const float v = group_allreduce<16>(ip, [](float x, float y) { return x + y; });
+      if (li == 0 && m < MP) red[wave][m] = v;
+    }
 
   // ---- per-workgroup total of sum(dy . x)
   redD[tid] = dd_acc;
   __syncthreads();
+  if (tid < MP && tid < M) wk.I[((int64_t)ps * p.Bsz * H + bh) * M + tid] = ((red[0][tid] + red[1][tid]) + red[2][tid]) + red[3][tid];
   if (tid == 0) {
     float s = 0.f;
     for (int i = 0; i < 256; ++i) s += redD[i];
@@ -765,7 +783,7 @@ hipError_t launch_nfree_t(const ScanParams& p, hipStream_t stream) {
 }
 
 struct NfLayout {
-  size_t ckpt, F, dDp, tiles, dcp, dkp, total;
+  size_t ckpt, F, I, dDp, tiles, dcp, dkp, dkip, total;
 };
 
 NfLayout nfree_layout(const ScanParams& p) {
@@ -774,11 +792,13 @@ NfLayout nfree_layout(const ScanParams& p) {
   NfLayout l{};
   l.ckpt = 0;
   l.F = up(sizeof(float) * bh * (nch + 1) * p.M * p.P);
-  l.dDp = l.F + up(sizeof(float) * nps * bh * p.M);
+  l.I = l.F + up(sizeof(float) * nps * bh * p.M);
+  l.dDp = l.I + up(sizeof(float) * nps * bh * p.M);
   l.tiles = l.dDp + up(sizeof(float) * nps * bh);
   l.dcp = l.tiles + up(grad_tiles_bytes(p));
   l.dkp = l.dcp + up(sizeof(float) * nps * bh * p.L * p.M);
-  l.total = l.dkp + up(sizeof(float) * nps * bh * p.L * p.M);
+  l.dkip = l.dkp + up(sizeof(float) * nps * bh * p.L * p.M);
+  l.total = l.dkip + up(sizeof(float) * nps * bh * p.L * p.M);
   return l;
 }
 
@@ -789,9 +809,11 @@ hipError_t launch_nfree_bwd_mp(const ScanParams& p, void* ws, hipStream_t stream
   NfWork wk;
   wk.ckpt = reinterpret_cast<float*>(base + l.ckpt);
   wk.F = reinterpret_cast<float*>(base + l.F);
+  wk.I = reinterpret_cast<float*>(base + l.I);
   wk.dDp = reinterpret_cast<float*>(base + l.dDp);
   wk.dcp = reinterpret_cast<float*>(base + l.dcp);
   wk.dkp = reinterpret_cast<float*>(base + l.dkp);
+  wk.dkip = reinterpret_cast<float*>(base + l.dkip);
   const unsigned blocks = (unsigned)((int64_t)p.Bsz * p.H * ((p.P + 63) / 64));
   hipLaunchKernelGGL((frac_nfree_fwd_kernel<T, MP, true>), dim3(blocks), dim3(256), 0, stream, p,
                      reinterpret_cast<float*>(base + l.ckpt));
@@ -803,13 +825,15 @@ hipError_t launch_nfree_bwd_mp(const ScanParams& p, void* ws, hipStream_t stream
   GradInputs gi;
   gi.dc = wk.dcp;
   gi.dk = wk.dkp;
-  gi.ndc = gi.ndk = nps;
+  gi.dki = wk.dkip;
+  gi.ndc = gi.ndk = gi.ndki = nps;
   gi.F = wk.F;
   gi.nF = nps;
+  gi.I = wk.I;
+  gi.nI = nps;
   gi.dDp = wk.dDp;
   gi.nD = nps;
-  gi.tileV = reinterpret_cast<float*>(base + l.tiles);
-  gi.tileF = reinterpret_cast<int*>(base + l.tiles + sizeof(float) * (size_t)p.Bsz * p.H * ((p.L + 63) / 64) * p.M);
+  grad_tiles_at(p, base + l.tiles, gi);
   return launch_grad_finish(p, gi, stream);
 }
 
