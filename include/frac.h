@@ -287,6 +287,23 @@ size_t frac_scan_workspace_size(const frac_shape *shape, int backward);
 frac_status frac_scan_fwd(const frac_shape *shape, const frac_fwd_args *args, void *ws, size_t ws_bytes,
                           void *stream);
 
+/* frac_scan_fwd for callers that cannot allocate device memory (code under HIP
+ * graph capture, serving loops that forbid hipMalloc): the same kernels, with a
+ * static scratch array of the library, of frac_scan_fwd_noalloc_limit() bytes
+ * (64 MiB), in place of the workspace.  Each GPU the library runs on holds its
+ * own copy of that array from the first use until the process ends.  The caller
+ * still passes every input and output.  The call allocates nothing (no hipMalloc,
+ * hipFree or allocating library routine) and runs on the current device; `stream`
+ * must belong to it.  Shapes whose workspace (frac_scan_workspace_size(shape, 0))
+ * exceeds the limit return FRAC_ERR_WORKSPACE.  Every call on one GPU shares its
+ * array and leaves it holding scratch (nothing in it must start at zero): calls
+ * that overlap in time on one GPU, on different streams or host threads, race and
+ * give undefined results. */
+frac_status frac_scan_fwd_noalloc(const frac_shape *shape, const frac_fwd_args *args, void *stream);
+
+/* Bytes of the static scratch frac_scan_fwd_noalloc uses. */
+size_t frac_scan_fwd_noalloc_limit(void);
+
 /* Chunked parallel scan, backward (see frac_bwd_args). */
 frac_status frac_scan_bwd(const frac_shape *shape, const frac_bwd_args *args, void *ws, size_t ws_bytes,
                           void *stream);

@@ -153,6 +153,24 @@ def scan_fwd(x, dt, Bm, Cm, alpha, tau, *, lam=None, read_logit=None, write_logi
     return (y, final_state) if return_final_state else y
 
 
+def scan_fwd_noalloc(x, dt, Bm, Cm, alpha, tau, *, y, lam=None, read_logit=None, write_logit=None, D=None,
+                     init_state=None, final_state=None, chunk=0):
+    """frac_scan_fwd_noalloc: the forward with the library's static scratch in place of a
+    workspace.  The outputs y (and final_state, when wanted) are the caller's; the call
+    allocates no device memory."""
+    M = int(tau.shape[0])
+    shape = _shape(x, Bm, M, chunk)
+    args, keep = _fwd_struct(x, dt, Bm, Cm, alpha, tau, lam, read_logit, write_logit, D, init_state, y, final_state)
+    _lib.check(_lib.load().frac_scan_fwd_noalloc(ctypes.byref(shape), ctypes.byref(args), _stream()))
+    del keep
+    return y
+
+
+def scan_fwd_noalloc_limit():
+    """Bytes of the static scratch of scan_fwd_noalloc."""
+    return int(_lib.load().frac_scan_fwd_noalloc_limit())
+
+
 def scan_bwd(x, dt, Bm, Cm, alpha, tau, dy, *, lam=None, read_logit=None, write_logit=None, D=None,
              init_state=None, d_final_state=None, chunk=0, workspace=None, all_grads=False):
     """Chunked parallel scan, backward (frac_scan_bwd).

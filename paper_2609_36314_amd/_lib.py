@@ -23,7 +23,8 @@ STATUS = {0: "FRAC_OK", -1: "FRAC_ERR_INVALID_ARG", -2: "FRAC_ERR_UNSUPPORTED", 
 EXPORTS = ("frac_scan_workspace_size", "frac_scan_fwd", "frac_scan_bwd", "frac_decode_step", "frac_default_tau",
            "frac_status_string", "frac_last_error", "frac_params_fwd", "frac_params_workspace_size",
            "frac_params_bwd", "frac_conv_fwd", "frac_conv_workspace_size", "frac_conv_bwd",
-           "frac_gnorm_fwd", "frac_gnorm_workspace_size", "frac_gnorm_bwd")
+           "frac_gnorm_fwd", "frac_gnorm_workspace_size", "frac_gnorm_bwd", "frac_scan_fwd_noalloc",
+           "frac_scan_fwd_noalloc_limit")
 
 
 class FracShape(ctypes.Structure):
@@ -110,6 +111,10 @@ def load():
     lib.frac_scan_workspace_size.restype = c_size_t
     lib.frac_scan_fwd.argtypes = [POINTER(FracShape), POINTER(FracFwdArgs), c_void_p, c_size_t, c_void_p]
     lib.frac_scan_fwd.restype = c_int
+    lib.frac_scan_fwd_noalloc.argtypes = [POINTER(FracShape), POINTER(FracFwdArgs), c_void_p]
+    lib.frac_scan_fwd_noalloc.restype = c_int
+    lib.frac_scan_fwd_noalloc_limit.argtypes = []
+    lib.frac_scan_fwd_noalloc_limit.restype = c_size_t
     lib.frac_scan_bwd.argtypes = [POINTER(FracShape), POINTER(FracBwdArgs), c_void_p, c_size_t, c_void_p]
     lib.frac_scan_bwd.restype = c_int
     lib.frac_decode_step.argtypes = [POINTER(FracShape), POINTER(FracStepArgs), c_void_p]

@@ -5,10 +5,17 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <mutex>
 #include <string>
 
 #include "frac.h"
 #include "frac_kernels.h"
+
+// Device scratch of frac_scan_fwd_noalloc: one copy per GPU, held from the library's
+// first use on that GPU until the process ends.  In host code `scratch` names a
+// host-side stand-in; the device address comes from hipGetSymbolAddress.
+constexpr size_t kStaticScratchBytes = (size_t)64 << 20;
+static __device__ __align__(256) unsigned char scratch[kStaticScratchBytes];
 
 namespace {
 
@@ -248,11 +255,37 @@ size_t frac_scan_workspace_size(const frac_shape* shape, int backward) {
   return backward ? frac::scan_bwd_workspace(p) : frac::scan_fwd_workspace(p);
 }
 
-frac_status frac_scan_fwd(const frac_shape* shape, const frac_fwd_args* args, void* ws, size_t ws_bytes,
-                          void* stream) {
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices];  // device address of `scratch`, per device
+
+// The current device's copy of the static scratch, looked up once per device.
+frac_status static_scratch(void** out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_status(e, "frac_scan_fwd_noalloc: hipGetDevice");
+  if (dev < 0 || dev >= kMaxDevices) return fail(FRAC_ERR_UNSUPPORTED, "frac_scan_fwd_noalloc: device %d", dev);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* ptr = nullptr;
+    e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !ptr) return hip_status(e != hipSuccess ? e : hipErrorInvalidSymbol,
+                                                   "frac_scan_fwd_noalloc: hipGetSymbolAddress(scratch)");
+    g_scratch_ptr[dev] = ptr;
+  }
+  *out = g_scratch_ptr[dev];
+  return FRAC_OK;
+}
+
+// frac_scan_fwd with either the caller's workspace or (use_static) the static scratch.
+frac_status scan_fwd_impl(const frac_shape* shape, const frac_fwd_args* args, void* ws, size_t ws_bytes,
+                          void* stream, bool use_static) {
+  const char* name = use_static ? "frac_scan_fwd_noalloc" : "frac_scan_fwd";
   frac::ScanParams p{};
   frac_status s = fill_shape(shape, p);
-  if (s == FRAC_OK) s = check_scan_shape(p, "frac_scan_fwd");
+  if (s == FRAC_OK) s = check_scan_shape(p, name);
   if (s != FRAC_OK) return s;
   if (p.Bsz == 0) return ok();
   if (!args) return fail(FRAC_ERR_INVALID_ARG, "args is NULL");
@@ -269,10 +302,32 @@ frac_status frac_scan_fwd(const frac_shape* shape, const frac_fwd_args* args, vo
   if (s != FRAC_OK) return s;
   if (p.N == 1) return hip_status(frac::launch_nfree_fwd(p, st), "frac_scan_fwd launch");
   const size_t need = frac::scan_fwd_workspace(p);
-  if (need && (!ws || ws_bytes < need))
+  if (use_static) {
+    if (need > kStaticScratchBytes)
+      return fail(FRAC_ERR_WORKSPACE, "frac_scan_fwd_noalloc: this shape needs %zu bytes of scratch, the static "
+                  "scratch holds %zu (use frac_scan_fwd with a workspace)", need, kStaticScratchBytes);
+    ws = nullptr;
+    ws_bytes = need;
+    if (need && (s = static_scratch(&ws)) != FRAC_OK) return s;
+  } else if (need && (!ws || ws_bytes < need)) {
     return fail(FRAC_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", need, ws ? ws_bytes : (size_t)0);
-  return hip_status(frac::launch_scan_fwd(p, ws, ws_bytes, st), "frac_scan_fwd launch");
+  }
+  return hip_status(frac::launch_scan_fwd(p, ws, ws_bytes, st), use_static ? "frac_scan_fwd_noalloc launch"
+                                                                           : "frac_scan_fwd launch");
 }
+
+}  // namespace
+
+frac_status frac_scan_fwd(const frac_shape* shape, const frac_fwd_args* args, void* ws, size_t ws_bytes,
+                          void* stream) {
+  return scan_fwd_impl(shape, args, ws, ws_bytes, stream, false);
+}
+
+frac_status frac_scan_fwd_noalloc(const frac_shape* shape, const frac_fwd_args* args, void* stream) {
+  return scan_fwd_impl(shape, args, nullptr, 0, stream, true);
+}
+
+size_t frac_scan_fwd_noalloc_limit(void) { return kStaticScratchBytes; }
 
 frac_status frac_scan_bwd(const frac_shape* shape, const frac_bwd_args* args, void* ws, size_t ws_bytes,
                           void* stream) {

@@ -117,6 +117,22 @@ def test_workspace_is_required_and_checked():
     assert lib.frac_scan_fwd(ctypes.byref(sh), ctypes.byref(a), ctypes.c_void_p(0x20000), need - 1, None) == -3
 
 
+def test_noalloc_forward_rejects_shapes_beyond_its_scratch():
+    """frac_scan_fwd_noalloc checks the shape's workspace against its static scratch on
+    the host, before any device call."""
+    lib = _lib.load()
+    limit = lib.frac_scan_fwd_noalloc_limit()
+    assert limit == 64 << 20
+    sh = _shape(batch=16, seqlen=65536)
+    assert lib.frac_scan_workspace_size(ctypes.byref(sh), 0) > limit
+    a = FracFwdArgs()
+    for f in ("x", "dt", "Bm", "Cm", "alpha", "tau", "y"):
+        setattr(a, f, ctypes.c_void_p(0x10000))
+    assert lib.frac_scan_fwd_noalloc(ctypes.byref(sh), ctypes.byref(a), None) == -3
+    assert "static scratch" in lib.frac_last_error().decode()
+    assert lib.frac_scan_fwd_noalloc(None, ctypes.byref(a), None) == -1
+
+
 @pytest.mark.parametrize("nmodes,status", [(33, -2), (0, -1)])
 def test_decode_mode_range_is_checked_on_the_host(nmodes, status):
     """frac_decode_step takes up to 32 modes; the shape is checked before any argument."""
