@@ -73,6 +73,7 @@ frac_status fill_shape(const frac_shape* sh, frac::ScanParams& p) {
   p.N = (int)sh->dstate;
   p.G = (int)sh->ngroups;
   p.M = (int)sh->nmodes;
+  p.Mall = p.M;
   p.PP = (p.P + 15) / 16 * 16;
   p.NP = next_tile_n(p.N);
   p.io_bf16 = sh->io_dtype == FRAC_BF16;
@@ -83,7 +84,7 @@ frac_status fill_shape(const frac_shape* sh, frac::ScanParams& p) {
 // and its share of the state in registers (nmodes <= 8).
 // The tiles of 64 tokens are addressed with 32-bit byte offsets: 64 rows of x
 // (H P elements apart) and of B, C (G N elements apart) must span < 2 GiB.
-frac_status check_scan_shape(const frac::ScanParams& p, const char* what) {
+frac_status check_scan_shape(const frac::ScanParams& p, const char* what, bool backward) {
   if (p.N == 1) {  // the form without B/C (B = C = 1): headdim <= 256, up to 32 modes
     if (p.P > 256) return fail(FRAC_ERR_UNSUPPORTED, "%s: headdim %d > 256 is not built", what, p.P);
     const int64_t es = p.io_bf16 ? 2 : 4;
@@ -92,7 +93,8 @@ frac_status check_scan_shape(const frac::ScanParams& p, const char* what) {
     return FRAC_OK;
   }
   if (p.PP > 64) return fail(FRAC_ERR_UNSUPPORTED, "%s: headdim %d > 64 is not built", what, p.P);
-  if (p.M > 8) return fail(FRAC_ERR_UNSUPPORTED, "%s: nmodes %d > 8 is not built", what, p.M);
+  if (p.M > 8 && backward)
+    return fail(FRAC_ERR_UNSUPPORTED, "%s: nmodes %d > 8 is built for the forward only", what, p.M);
   const int64_t es = p.io_bf16 ? 2 : 4, lim = (int64_t)1 << 31;
   if (64 * (int64_t)p.H * p.P * es >= lim || 64 * (int64_t)p.G * p.N * es >= lim)
     return fail(FRAC_ERR_UNSUPPORTED, "%s: nheads * headdim or ngroups * dstate too large", what);
@@ -250,7 +252,7 @@ frac_status frac_default_tau(int M, double tau_min, double tau_max, float* out) 
 
 size_t frac_scan_workspace_size(const frac_shape* shape, int backward) {
   frac::ScanParams p{};
-  if (fill_shape(shape, p) != FRAC_OK || check_scan_shape(p, "frac_scan_workspace_size") != FRAC_OK) return 0;
+  if (fill_shape(shape, p) != FRAC_OK || check_scan_shape(p, "frac_scan_workspace_size", backward) != FRAC_OK) return 0;
   if (p.N == 1) return backward ? frac::nfree_bwd_workspace(p) : 0;  // the form without B/C
   return backward ? frac::scan_bwd_workspace(p) : frac::scan_fwd_workspace(p);
 }
@@ -285,7 +287,7 @@ frac_status scan_fwd_impl(const frac_shape* shape, const frac_fwd_args* args, vo
   const char* name = use_static ? "frac_scan_fwd_noalloc" : "frac_scan_fwd";
   frac::ScanParams p{};
   frac_status s = fill_shape(shape, p);
-  if (s == FRAC_OK) s = check_scan_shape(p, name);
+  if (s == FRAC_OK) s = check_scan_shape(p, name, false);
   if (s != FRAC_OK) return s;
   if (p.Bsz == 0) return ok();
   if (!args) return fail(FRAC_ERR_INVALID_ARG, "args is NULL");
@@ -333,7 +335,7 @@ frac_status frac_scan_bwd(const frac_shape* shape, const frac_bwd_args* args, vo
                           void* stream) {
   frac::ScanParams p{};
   frac_status s = fill_shape(shape, p);
-  if (s == FRAC_OK) s = check_scan_shape(p, "frac_scan_bwd");
+  if (s == FRAC_OK) s = check_scan_shape(p, "frac_scan_bwd", true);
   if (s != FRAC_OK) return s;
   if (p.Bsz == 0 || p.L == 0) {
     if (args && args->dinit_state && p.Bsz > 0) {  // no tokens: the initial state is the final state

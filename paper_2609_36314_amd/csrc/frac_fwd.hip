@@ -159,7 +159,9 @@ struct FwdCfg {
 
 // STATE_ONLY: only the state update over tokens [0, seg_len), ending in seg_state
 // (the first pass of a sequence-split forward).
-template <typename T, int MP, int NB, int PS, bool STATE_ONLY>
+// BLK: one block of a mode-block launch sequence (weights normalised with p.lse,
+// outputs accumulated through p.y_in / p.y_part).
+template <typename T, int MP, int NB, int PS, bool STATE_ONLY, bool BLK = false>
 __global__ void __launch_bounds__(512) frac_fwd_kernel(ScanParams p, const T* __restrict__ gtiles) {
   using Cfg = FwdCfg<T, MP, NB, PS, STATE_ONLY>;
   constexpr int NP = Cfg::NP, XS = Cfg::XS, BS = Cfg::BS, CS = Cfg::CS, GS = Cfg::GS;
@@ -243,7 +245,7 @@ __global__ void __launch_bounds__(512) frac_fwd_kernel(ScanParams p, const T* __
   for (int i = tid; i < 64 * CS; i += 512) Cb0[i] = Cb1[Cfg::NBUF == 2 ? i : 0] = (T)0.0f;
 
   // ---- state: S[m][jb] holds mode mo + m, rows n = 16 (nbo + jb) + 4 lg + r, column pc
-  const int64_t sbase = ((int64_t)b * H + h) * (int64_t)M * N * P;
+  const int64_t sbase = ((int64_t)b * H + h) * (int64_t)p.Mall * N * P;
   floatx4 S[MPW][NBW];
   {
     // lane offset kept opaque so that the final store cannot share (and keep alive
@@ -271,10 +273,11 @@ __global__ void __launch_bounds__(512) frac_fwd_kernel(ScanParams p, const T* __
   const int64_t al_st = p.as1;
   const float* lm_bh = p.lambda ? p.lambda + b * p.ls0 + h * p.ls2 : nullptr;
   const int64_t lm_st = p.ls1;
-  const float* rl_bh = p.read_logit ? p.read_logit + ((int64_t)b * L * H + h) * M : nullptr;
-  const float* wl_bh = p.write_logit ? p.write_logit + ((int64_t)b * L * H + h) * M : nullptr;
+  const float* rl_bh = p.read_logit ? p.read_logit + ((int64_t)b * L * H + h) * p.Mall : nullptr;
+  const float* wl_bh = p.write_logit ? p.write_logit + ((int64_t)b * L * H + h) * p.Mall : nullptr;
   const bool w_is_c = wl_bh == rl_bh;  // then the write weights equal the read weights
-  const int64_t lg_st = (int64_t)H * M;
+  const int64_t lg_st = (int64_t)H * p.Mall;
+  const float* lse_bh = BLK ? p.lse + ((int64_t)b * L * H + h) * 2 : nullptr;  // [t][H][2]
   PairLogits<MP, 512> lgt_n;  // the logits of the next chunk's weight pass
   auto load_controls = [&](int c, float& dtv, float& al, float& lam) {
     const int tg = c * kQ + lane;
@@ -331,7 +334,7 @@ __global__ void __launch_bounds__(512) frac_fwd_kernel(ScanParams p, const T* __
     const float dtv = pinned(dt_n), al_l = pinned(al_n), lam_l = pinned(lam_n);
     const PairLogits<MP, 512> lgt = lgt_n.pinned_copy();
     const TilePrefetch<T> gcur = gtile.pinned_copy();
-    if (!STATE_ONLY && c > c0) store_y(c - 1);
+    if (!STATE_ONLY && c > c0 && !(BLK && p.y_part)) store_y(c - 1);
     if (Cfg::NBUF == 2) {
       if (c + 1 < c1) stage(c + 1, Xn, Bn, Cn);
     } else {
@@ -362,9 +365,18 @@ __global__ void __launch_bounds__(512) frac_fwd_kernel(ScanParams p, const T* __
       const float r = s_rr[m], prior = -al * s_lnt[m];
       float zc = (m < M) ? prior + lgt.rl[j] : -INFINITY;
       float zw = (m < M) ? prior + lgt.wl[j] : -INFINITY;
-      // tokens past the sequence get zero weights (their tile rows may hold anything finite)
-      const float cw = valid ? group_softmax<MP>(zc) : 0.0f;
-      const float ww = w_is_c ? cw : (valid ? group_softmax<MP>(zw) : 0.0f);
+      // tokens past the sequence get zero weights (their tile rows may hold anything finite);
+      // a mode block normalises over all modes with the precomputed log-normalizers
+      float cw, ww;
+      if constexpr (BLK) {
+        const float2 ln = valid ? *reinterpret_cast<const float2*>(lse_bh + (int64_t)(t0 + t) * H * 2)
+                                : float2{0.0f, 0.0f};
+        cw = valid ? __expf(zc - ln.x) : 0.0f;
+        ww = w_is_c ? cw : (valid ? __expf(zw - ln.y) : 0.0f);
+      } else {
+        cw = valid ? group_softmax<MP>(zc) : 0.0f;
+        ww = w_is_c ? cw : (valid ? group_softmax<MP>(zw) : 0.0f);
+      }
       const float lh = P_lh[m * kWQ + t], lhQ = P_lh[m * kWQ + kQ - 1];
       const bool safe = lhQ <= kSafeExponent;
       const float Enew = Ecur[m] * fexp(-lhQ);
@@ -512,8 +524,21 @@ __global__ void __launch_bounds__(512) frac_fwd_kernel(ScanParams p, const T* __
       }
       float xv[4];
       col4_rows(Xc, XS, tb * 16 + lg * 4, pb * 16, xv);
+      if constexpr (BLK) {  // a mode block: float32 partial sums across the blocks
 #pragma unroll
-      for (int r = 0; r < 4; ++r) Yb[(tb * 16 + lg * 4 + r) * XS + pc] = (T)(Y[tb][r] + Dh * xv[r]);
+        for (int r = 0; r < 4; ++r) {
+          const int tr = tb * 16 + lg * 4 + r;
+          const int64_t yi = (((int64_t)b * L + t0 + tr) * H + h) * P + pc;
+          if (tr < nv && pc < P) {
+            if (p.y_in) Y[tb][r] += p.y_in[yi];
+            if (p.y_part) p.y_part[yi] = Y[tb][r];
+          }
+        }
+      }
+      if (!(BLK && p.y_part)) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) Yb[(tb * 16 + lg * 4 + r) * XS + pc] = (T)(Y[tb][r] + Dh * xv[r]);
+      }
     }
     }  // !STATE_ONLY
     if (!active) return;
@@ -565,7 +590,7 @@ __global__ void __launch_bounds__(512) frac_fwd_kernel(ScanParams p, const T* __
   }
   wait_vmem();
   barrier();
-  if constexpr (!STATE_ONLY) store_y(c1 - 1);
+  if (!STATE_ONLY && !(BLK && p.y_part)) store_y(c1 - 1);
 
   if (final_state && active) {
     const float* Ef = s_E2 + (c1 & 1) * MP;
@@ -623,15 +648,15 @@ int fwd_seg_len(const ScanParams& p) {
 
 size_t align256(size_t n) { return (n + 255) & ~(size_t)255; }
 
-template <typename T, int MP, int NB, int PS>
+template <typename T, int MP, int NB, int PS, bool BLK = false>
 hipError_t launch_fwd_ps(const ScanParams& p, const T* gt, hipStream_t stream) {
   const unsigned blocks = (unsigned)(p.Bsz * p.H * PS);
   // the state-only pass: one workgroup per 16 columns of P
   if (p.seg_len > 0)
-    hipLaunchKernelGGL((frac_fwd_kernel<T, MP, NB, 4, true>), dim3((unsigned)(p.Bsz * p.H * 4)), dim3(512), 0, stream,
-                       p, gt);
-  hipLaunchKernelGGL((frac_fwd_kernel<T, MP, NB, PS, false>), dim3(blocks * (p.seg_len > 0 ? 2 : 1)), dim3(512), 0,
-                     stream, p, gt);
+    hipLaunchKernelGGL((frac_fwd_kernel<T, MP, NB, 4, true, BLK>), dim3((unsigned)(p.Bsz * p.H * 4)), dim3(512), 0,
+                       stream, p, gt);
+  hipLaunchKernelGGL((frac_fwd_kernel<T, MP, NB, PS, false, BLK>), dim3(blocks * (p.seg_len > 0 ? 2 : 1)), dim3(512),
+                     0, stream, p, gt);
   return hipGetLastError();
 }
 
@@ -653,14 +678,108 @@ hipError_t launch_fwd_variant(const ScanParams& p0, void* ws, hipStream_t stream
   }
 }
 
+// Per token (b, t, h): the log-normalizers of the read and write softmax over all
+// Mall modes, z_m = -alpha ln tau_m + logit_m (eq. read-softmax), as max + log sum exp.
+__global__ void __launch_bounds__(256) frac_mode_lse_kernel(ScanParams p, float* __restrict__ lse) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= (int64_t)p.Bsz * p.L * p.H) return;
+  const int h = (int)(i % p.H);
+  const int64_t bt = i / p.H;
+  const int t = (int)(bt % p.L), b = (int)(bt / p.L);
+  const int Ma = p.Mall;
+  const float al = strided3(p.alpha, p.as0, p.as1, p.as2, b, t, h);
+  const float* rl = p.read_logit ? p.read_logit + i * Ma : nullptr;
+  const float* wl = (p.write_logit && p.write_logit != p.read_logit) ? p.write_logit + i * Ma : nullptr;
+  const bool w_is_c = p.write_logit == p.read_logit;
+  float mc = -INFINITY, mw = -INFINITY;
+  for (int m = 0; m < Ma; ++m) {
+    const float prior = -al * logf(p.tau[m]);
+    mc = fmaxf(mc, prior + (rl ? rl[m] : 0.0f));
+    mw = fmaxf(mw, prior + (wl ? wl[m] : 0.0f));
+  }
+  float sc = 0.0f, sw = 0.0f;
+  for (int m = 0; m < Ma; ++m) {
+    const float prior = -al * logf(p.tau[m]);
+    sc += __expf(prior + (rl ? rl[m] : 0.0f) - mc);
+    sw += __expf(prior + (wl ? wl[m] : 0.0f) - mw);
+  }
+  const float lc = mc + logf(sc);
+  reinterpret_cast<float2*>(lse)[i] = float2{lc, w_is_c ? lc : mw + logf(sw)};
+}
+
+constexpr int kModeBlock = 8;  // modes per launch of the mode-block forward
+
+// Workspace of the mode-block forward: [C B^T tiles][boundary state, all modes]
+// [log-normalizers][float32 partial output].
+struct FwdBlockLayout {
+  size_t seg, lse, ypart, total;
+  int seg_len;
+};
+
+template <typename T>
+FwdBlockLayout fwd_block_layout(const ScanParams& p) {
+  ScanParams pb = p;
+  pb.M = kModeBlock;
+  FwdBlockLayout l{};
+  l.seg_len = fwd_seg_len(pb);
+  l.seg = align256(gtile_bytes<T>(p));
+  l.lse = l.seg + (l.seg_len ? align256(sizeof(float) * (size_t)p.Bsz * p.H * p.Mall * p.N * p.P) : 0);
+  l.ypart = l.lse + align256(sizeof(float) * 2 * (size_t)p.Bsz * p.L * p.H);
+  l.total = l.ypart + sizeof(float) * (size_t)p.Bsz * p.L * p.H * p.P;
+  return l;
+}
+
+// More modes than one workgroup's registers hold: the modes in blocks of eight, one
+// forward launch per block (the recurrence is linear in the modes once the weights
+// are fixed), the weights normalised over all modes, the outputs summed in float32
+// in block order; the last block adds the skip term and writes y.
+template <typename T, int NB>
+hipError_t launch_fwd_blocks(const ScanParams& p0, void* ws, hipStream_t stream) {
+  const FwdBlockLayout l = fwd_block_layout<T>(p0);
+  unsigned char* base = reinterpret_cast<unsigned char*>(ws);
+  T* gt = reinterpret_cast<T*>(ws);
+  hipError_t e = launch_cb_variant<T, NB>(p0, gt, stream);
+  if (e != hipSuccess) return e;
+  float* lse = reinterpret_cast<float*>(base + l.lse);
+  float* ypart = reinterpret_cast<float*>(base + l.ypart);
+  if ((e = launch_mode_lse(p0, lse, stream)) != hipSuccess) return e;
+  const int64_t NP = (int64_t)p0.N * p0.P;
+  for (int mo = 0; mo < p0.Mall; mo += kModeBlock) {
+    ScanParams p = p0;
+    p.M = min(kModeBlock, p0.Mall - mo);
+    p.tau = p0.tau + mo;
+    if (p0.read_logit) p.read_logit = p0.read_logit + mo;
+    if (p0.write_logit) p.write_logit = p0.write_logit + mo;
+    if (p0.init_state) p.init_state = p0.init_state + mo * NP;
+    if (p0.final_state) p.final_state = p0.final_state + mo * NP;
+    p.lse = lse;
+    p.y_in = mo > 0 ? ypart : nullptr;
+    p.y_part = mo + kModeBlock < p0.Mall ? ypart : nullptr;
+    p.seg_len = l.seg_len;
+    p.seg_state = l.seg_len ? reinterpret_cast<float*>(base + l.seg) + mo * NP : nullptr;
+    if ((e = launch_fwd_ps<T, kModeBlock, NB, 2, true>(p, gt, stream)) != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
+
 template <typename T, int MP>
 hipError_t launch_fwd_nb(const ScanParams& p, void* ws, hipStream_t stream) {
-  switch (p.NP / 16) {
-    case 1: return launch_fwd_variant<T, MP, 1>(p, ws, stream);
-    case 2: return launch_fwd_variant<T, MP, 2>(p, ws, stream);
-    case 4: return launch_fwd_variant<T, MP, 4>(p, ws, stream);
-    case 8: return launch_fwd_variant<T, MP, 8>(p, ws, stream);
-    default: return hipErrorInvalidValue;
+  if constexpr (MP > kModeBlock) {
+    switch (p.NP / 16) {
+      case 1: return launch_fwd_blocks<T, 1>(p, ws, stream);
+      case 2: return launch_fwd_blocks<T, 2>(p, ws, stream);
+      case 4: return launch_fwd_blocks<T, 4>(p, ws, stream);
+      case 8: return launch_fwd_blocks<T, 8>(p, ws, stream);
+      default: return hipErrorInvalidValue;
+    }
+  } else {
+    switch (p.NP / 16) {
+      case 1: return launch_fwd_variant<T, MP, 1>(p, ws, stream);
+      case 2: return launch_fwd_variant<T, MP, 2>(p, ws, stream);
+      case 4: return launch_fwd_variant<T, MP, 4>(p, ws, stream);
+      case 8: return launch_fwd_variant<T, MP, 8>(p, ws, stream);
+      default: return hipErrorInvalidValue;
+    }
   }
 }
 
@@ -669,7 +788,8 @@ hipError_t launch_fwd_mp(const ScanParams& p, void* ws, hipStream_t stream) {
   if (p.M <= 1) return launch_fwd_nb<T, 1>(p, ws, stream);
   if (p.M <= 2) return launch_fwd_nb<T, 2>(p, ws, stream);
   if (p.M <= 4) return launch_fwd_nb<T, 4>(p, ws, stream);
-  return launch_fwd_nb<T, 8>(p, ws, stream);
+  if (p.M <= 8) return launch_fwd_nb<T, 8>(p, ws, stream);
+  return launch_fwd_nb<T, 32>(p, ws, stream);
 }
 
 }  // namespace
@@ -701,8 +821,16 @@ hipError_t launch_cb_tiles(const ScanParams& p, void* tiles, hipStream_t stream)
   return hipErrorInvalidValue;
 }
 
+hipError_t launch_mode_lse(const ScanParams& p, float* lse, hipStream_t stream) {
+  const int64_t n = (int64_t)p.Bsz * p.L * p.H;
+  if (n == 0) return hipSuccess;
+  hipLaunchKernelGGL(frac_mode_lse_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, stream, p, lse);
+  return hipGetLastError();
+}
+
 size_t scan_fwd_workspace(const ScanParams& p) {
   if (p.Bsz == 0 || p.L == 0) return 0;
+  if (p.Mall > kModeBlock) return p.io_bf16 ? fwd_block_layout<bf16>(p).total : fwd_block_layout<float>(p).total;
   const size_t tiles = p.io_bf16 ? gtile_bytes<bf16>(p) : gtile_bytes<float>(p);
   if (fwd_seg_len(p) == 0) return tiles;
   return align256(tiles) + sizeof(float) * (size_t)p.Bsz * p.H * p.M * p.N * p.P;  // + the boundary state

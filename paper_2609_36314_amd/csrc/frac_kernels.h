@@ -35,6 +35,17 @@ struct ScanParams {
   // and [seg_len, L); seg_state holds the state at the boundary
   int seg_len;
   float* seg_state;
+  // Mode blocks (more modes than one launch holds): a launch covers M modes of Mall
+  // (the per-mode pointers tau, logits and states already offset to its first mode;
+  // logits and states keep the strides of Mall).  lse: per token the log-normalizers
+  // of the read and write softmax over all Mall modes ([B L H][2]; NULL: over the
+  // launch's own modes).  y_in: float32 sum of the earlier blocks' outputs (NULL for
+  // the first); y_part: float32 output of a block that is not the last (NULL: write
+  // y, with the skip term).
+  int Mall;
+  const float* lse;
+  const float* y_in;
+  float* y_part;
   // backward only
   const void* dy;
   const float* d_final_state;
@@ -54,6 +65,10 @@ struct ScanParams {
 // Each launcher returns hipSuccess or the launch error; `stream` may be null.
 hipError_t launch_scan_fwd(const ScanParams& p, void* ws, size_t ws_bytes, hipStream_t stream);
 size_t scan_fwd_workspace(const ScanParams& p);
+
+// The per-token log-normalizers of the read and write softmax over all p.Mall modes
+// (the mode blocks' weights), [B L H][2].
+hipError_t launch_mode_lse(const ScanParams& p, float* lse, hipStream_t stream);
 
 // C B^T of every chunk (causal 16x16 tiles, per-lane fragment order), shared by
 // the heads of a group; `tiles` holds cb_tiles_bytes(p) bytes.

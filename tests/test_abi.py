@@ -61,7 +61,6 @@ def _shape(**kw):
     (dict(nmodes=0), -1),
     (dict(batch=-1), -1),
     (dict(io_dtype=7), -1),
-    (dict(nmodes=9), -2),
     (dict(nmodes=33), -2),
     (dict(dstate=1, headdim=264), -2),
     (dict(dstate=12), -2),
@@ -80,6 +79,18 @@ def test_invalid_shapes_are_rejected_on_the_host(kw, status):
     b = FracBwdArgs()
     assert lib.frac_scan_bwd(ctypes.byref(sh), ctypes.byref(b), None, 0, None) == status
     assert lib.frac_scan_workspace_size(ctypes.byref(sh), 0) == 0
+
+
+def test_mode_blocks_are_sized_on_the_host():
+    """More than 8 modes (up to 32) run the forward in blocks of eight: the shape is
+    accepted and the workspace holds the float32 partial output."""
+    lib = _lib.load()
+    for M in (9, 16, 32):
+        sh = _shape(nmodes=M)
+        need = lib.frac_scan_workspace_size(ctypes.byref(sh), 0)
+        assert need >= sh.batch * sh.seqlen * sh.nheads * sh.headdim * 4, M
+        a = FracFwdArgs()
+        assert lib.frac_scan_fwd(ctypes.byref(sh), ctypes.byref(a), None, 0, None) == -1  # pointers missing
 
 
 def test_missing_pointers_are_rejected():

@@ -90,6 +90,13 @@ SMALL = {
     "bf16 split M4 extras": Workload("t", 1, 700, 2, 64, 128, 4, extras=True, init_state=True, final_state=True),
     "bf16 split M8": Workload("t", 1, 520, 2, 64, 64, 8, final_state=True),
     "f32 split M2 ragged": Workload("t", 1, 777, 1, 32, 32, 2, io_dtype="f32", final_state=True, init_state=True),
+    # more modes than one launch holds: blocks of eight, weights normalised over all
+    # modes, outputs summed across the blocks (the paper's bank of 16, its ablation's 32)
+    "bf16 M16 extras": Workload("t", 2, 200, 2, 64, 128, 16, extras=True, init_state=True, final_state=True),
+    "f32 M12 N64 extras": Workload("t", 1, 150, 2, 32, 64, 12, io_dtype="f32", extras=True, init_state=True,
+                                   final_state=True),
+    "bf16 M32": Workload("t", 1, 130, 2, 64, 128, 32, final_state=True),
+    "bf16 split M16": Workload("t", 1, 600, 2, 64, 128, 16, init_state=True, final_state=True),
 }
 
 
@@ -107,17 +114,18 @@ def test_fwd_parity_small(name):
     _check_state(f64(fs), fsr, tol, w.nmodes)
 
 
-@pytest.mark.parametrize("mode", [0, 1, 2, 3])
-def test_fwd_mode_isolation(mode):
+@pytest.mark.parametrize("M,mode", [(4, 0), (4, 1), (4, 2), (4, 3), (16, 0), (16, 7), (16, 8), (16, 15)])
+def test_fwd_mode_isolation(M, mode):
     """One-hot read/write logits (+-30) route everything through one mode, so the
-    slow modes, invisible under the prior weights, are checked in y as well."""
-    w = Workload("t", 1, 200, 2, 64, 128, 4, final_state=True)
+    slow modes, invisible under the prior weights, are checked in y as well; with 16
+    modes, the first and last mode of each block of eight."""
+    w = Workload("t", 1, 200, 2, 64, 128, M, final_state=True)
     inp = device_inputs(w, seed=2)
-    lg = torch.full((1, 200, 2, 4), -30.0, device="cuda")
+    lg = torch.full((1, 200, 2, M), -30.0, device="cuda")
     lg[..., mode] = 30.0
     inp["read_logit"] = lg.contiguous()
     inp["write_logit"] = lg.clone()
-    tau_d, tau64 = _tau(4)
+    tau_d, tau64 = _tau(M)
     y, fs = _run(w, inp, tau_d)
     torch.cuda.synchronize()
     yr, fsr = _oracle(inp, tau64)
@@ -182,7 +190,8 @@ def test_fwd_empty_sequence_returns_init_state():
 
 @pytest.mark.parametrize("w,slices", [
     (LAYER_FWD, [(0, 0), (3, 17), (7, 63)]),
-    (LONG_PREFILL, [(0, 0), (0, 41)]),
+    (LONG_PREFILL, [(0, 0), (0, 41), (0, 63)]),
+    (LAYER_FWD.scaled(nmodes=16), [(0, 0), (7, 63)]),
 ])
 def test_fwd_full_size_sampled(w, slices):
     """Benchmark workloads at full size, launched as the benchmark launches them;
