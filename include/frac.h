@@ -40,9 +40,9 @@
  *    bfloat16 outputs are rounded to nearest even.
  *  - Supported sizes: headdim P and dstate N multiples of 8 with N <= 128;
  *    P <= 64 for the chunked scan (frac_scan_*), P <= 128 for frac_decode_step;
- *    1 <= nmodes <= 32 for frac_scan_fwd and frac_decode_step, <= 8 for
- *    frac_scan_bwd (more than 8 modes run the forward in blocks of eight, the
- *    weights normalised over all modes and the blocks' outputs summed in float32);
+ *    1 <= nmodes <= 32 (with B/C, more than 8 modes run the chunked scan in
+ *    blocks of eight modes: the weights normalised over the whole bank, the
+ *    blocks' y, dx, dB and dC summed in float32 in block order);
  *    H % G == 0; chunk 0 (auto) or 64.
  *  - dstate 1 with Bm = Cm = NULL is the paper's own layer form without B/C
  *    projections (B = C = 1; the recurrence of the Appendix-D algorithm, an

@@ -84,7 +84,7 @@ frac_status fill_shape(const frac_shape* sh, frac::ScanParams& p) {
 // and its share of the state in registers (nmodes <= 8).
 // The tiles of 64 tokens are addressed with 32-bit byte offsets: 64 rows of x
 // (H P elements apart) and of B, C (G N elements apart) must span < 2 GiB.
-frac_status check_scan_shape(const frac::ScanParams& p, const char* what, bool backward) {
+frac_status check_scan_shape(const frac::ScanParams& p, const char* what, bool) {
   if (p.N == 1) {  // the form without B/C (B = C = 1): headdim <= 256, up to 32 modes
     if (p.P > 256) return fail(FRAC_ERR_UNSUPPORTED, "%s: headdim %d > 256 is not built", what, p.P);
     const int64_t es = p.io_bf16 ? 2 : 4;
@@ -93,8 +93,6 @@ frac_status check_scan_shape(const frac::ScanParams& p, const char* what, bool b
     return FRAC_OK;
   }
   if (p.PP > 64) return fail(FRAC_ERR_UNSUPPORTED, "%s: headdim %d > 64 is not built", what, p.P);
-  if (p.M > 8 && backward)
-    return fail(FRAC_ERR_UNSUPPORTED, "%s: nmodes %d > 8 is built for the forward only", what, p.M);
   const int64_t es = p.io_bf16 ? 2 : 4, lim = (int64_t)1 << 31;
   if (64 * (int64_t)p.H * p.P * es >= lim || 64 * (int64_t)p.G * p.N * es >= lim)
     return fail(FRAC_ERR_UNSUPPORTED, "%s: nheads * headdim or ngroups * dstate too large", what);

@@ -104,10 +104,13 @@ __device__ __forceinline__ ChunkCtl chunk_controls(float dtv, float al, float la
 // (the reverse sweeps read their Gamma tiles from the state sweep)
 // E is the scale of the state (or adjoint) before this chunk's update, upd the
 // factor on the update (1/E_new, or 1 when the accumulators are folded back).
-template <int MP, int ROLE, int NT = 512>
+// BLK (one block of a mode-block launch sequence): the weights are normalised over
+// the whole bank with the per-token log-normalizers lse_t[t * lse_st + {0, 1}].
+template <int MP, int ROLE, int NT = 512, bool BLK = false>
 __device__ __forceinline__ int pair_weights(const ChunkCtl& k, int nv, int M, const PairLogits<MP, NT>& lgt,
                                             bool w_is_c, const float* s_rr, const float* s_lnt, const float* lh,
-                                            const float* ll, const float* Ecur, float* Enext, float* w) {
+                                            const float* ll, const float* Ecur, float* Enext, float* w,
+                                            const float* lse_t = nullptr, int64_t lse_st = 0) {
   const int tid = threadIdx.x;
 #pragma unroll
   for (int j = 0; j < lgt.NPR; ++j) {
@@ -120,8 +123,15 @@ __device__ __forceinline__ int pair_weights(const ChunkCtl& k, int nv, int M, co
     const float zc = (m < M) ? prior + lgt.rl[j] : -INFINITY;
     const float zw = (m < M) ? prior + lgt.wl[j] : -INFINITY;
     // tokens past the sequence get zero weights (their tile rows may hold anything finite)
-    const float cw = valid ? group_softmax<MP>(zc) : 0.0f;
-    const float ww = w_is_c ? cw : (valid ? group_softmax<MP>(zw) : 0.0f);
+    float cw, ww;
+    if constexpr (BLK) {
+      const float2 ln = valid ? *reinterpret_cast<const float2*>(lse_t + (int64_t)t * lse_st) : float2{0.0f, 0.0f};
+      cw = valid ? __expf(zc - ln.x) : 0.0f;
+      ww = w_is_c ? cw : (valid ? __expf(zw - ln.y) : 0.0f);
+    } else {
+      cw = valid ? group_softmax<MP>(zc) : 0.0f;
+      ww = w_is_c ? cw : (valid ? group_softmax<MP>(zw) : 0.0f);
+    }
     const float lt = lh[m * kWQ + t], lQ = lh[m * kWQ + kQ - 1];
     const bool safe = lQ <= kSafeExponent;
     const float kap = one_minus_exp_neg(dtt * r) * ww;
@@ -311,7 +321,7 @@ struct StateLds {
   static constexpr int NWB = kTiles_ + kFixed + (kFold ? kHH : 0) + 2 * WSZ * 4 <= kLimit ? 2 : 1;
 };
 
-template <typename T, int MP, int NB>
+template <typename T, int MP, int NB, bool BLK = false>
 __global__ void __launch_bounds__(512) frac_bwd_state_kernel(ScanParams p, BwdWork wk) {
   using Cfg = ColCfg<T, MP, NB>;
   constexpr int NP = Cfg::NP, XS = Cfg::XS, BS = Cfg::BS, CS = Cfg::CS;
@@ -371,7 +381,7 @@ __global__ void __launch_bounds__(512) frac_bwd_state_kernel(ScanParams p, BwdWo
   for (int i = tid; i < 64 * CS; i += 512) Cb[i] = (T)0.0f;
 
   // ---- state S^T: S[m][pb] holds mode mo + m, rows p = 16 pb + 4 lg + r, column ncol
-  const int64_t sbase = ((int64_t)b * H + h) * (int64_t)M * N * P;
+  const int64_t sbase = ((int64_t)b * H + h) * (int64_t)p.Mall * N * P;
   floatx4 S[MPF][4];
   {
     int lo = ncol * P + lg * 4;
@@ -398,9 +408,10 @@ __global__ void __launch_bounds__(512) frac_bwd_state_kernel(ScanParams p, BwdWo
   const float* dt_bh = p.dt + (int64_t)b * L * H + h;
   const float* al_bh = p.alpha + b * p.as0 + h * p.as2;
   const float* lm_bh = p.lambda ? p.lambda + b * p.ls0 + h * p.ls2 : nullptr;
-  const float* rl_bh = p.read_logit ? p.read_logit + ((int64_t)b * L * H + h) * M : nullptr;
-  const float* wl_bh = p.write_logit ? p.write_logit + ((int64_t)b * L * H + h) * M : nullptr;
-  const int64_t lg_st = (int64_t)H * M;
+  const float* rl_bh = p.read_logit ? p.read_logit + ((int64_t)b * L * H + h) * p.Mall : nullptr;
+  const float* wl_bh = p.write_logit ? p.write_logit + ((int64_t)b * L * H + h) * p.Mall : nullptr;
+  const int64_t lg_st = (int64_t)H * p.Mall;
+  const float* lse_bh = BLK ? p.lse + ((int64_t)b * L * H + h) * 2 : nullptr;  // [t][H][2]
   PairLogits<MP, 512> lgt_n;  // the logits of the next chunk's weight pass
   auto load_controls = [&](int c, float& dtv, float& al, float& lam) {
     const int tg = c * kQ + lane;
@@ -439,7 +450,7 @@ __global__ void __launch_bounds__(512) frac_bwd_state_kernel(ScanParams p, BwdWo
   gtile.load(gtiles + ((int64_t)b * nchunks * G + g) * (kTiles * kTileElems), wave, lane);
   T* dCp = reinterpret_cast<T*>(wk.dCp);
   const int64_t bh_i = (int64_t)b * H + h;
-  float* dcg = wk.dc + ((int64_t)ps * p.Bsz * H * L + bh_i * L) * M;  // this head's dc partial [L][M]
+  float* dcg = wk.dc + ((int64_t)ps * p.Bsz * H * L + bh_i * L) * p.Mall;  // this head's dc partial [L][Mall]
 
   // Per-(token, mode) weights of chunk c into Wd, from the controls in dt_n, al_n,
   // lam_n.  Chunk c + 1's weights are formed at the end of chunk c's step, so that
@@ -451,8 +462,9 @@ __global__ void __launch_bounds__(512) frac_bwd_state_kernel(ScanParams p, BwdWo
     float* lh = Wd + NWA * SW;
     chunk_log_decays<MP, 8>(k.dtt, s_rr, lh, lh + SW);
     barrier();  // log-decays in LDS
-    unsafe_c = pair_weights<MP, kState>(k, nv, M, lgt_n, rl_bh == wl_bh, s_rr, s_lnt, lh, lh + SW,
-                                        s_E2 + (c & 1) * MP, s_E2 + ((c + 1) & 1) * MP, Wd);
+    unsafe_c = pair_weights<MP, kState, 512, BLK>(k, nv, M, lgt_n, rl_bh == wl_bh, s_rr, s_lnt, lh, lh + SW,
+                                                  s_E2 + (c & 1) * MP, s_E2 + ((c + 1) & 1) * MP, Wd,
+                                                  BLK ? lse_bh + (int64_t)t0 * H * 2 : nullptr, (int64_t)H * 2);
   };
   barrier();  // rates and scales in LDS
   if constexpr (NWB == 2) weights(0, W0);
@@ -667,7 +679,7 @@ __global__ void __launch_bounds__(512) frac_bwd_state_kernel(ScanParams p, BwdWo
           float z = 0.0f;
 #pragma unroll
           for (int q = 0; q < NBF; ++q) z += redZ[((pt * NBF + q) * MPF + j) * kQ + t];
-          dcg[(int64_t)(t0 + t) * M + m] = fexp(-P_lh[m * kWQ + t]) * Ecur[m] * z;
+          dcg[(int64_t)(t0 + t) * p.Mall + m] = fexp(-P_lh[m * kWQ + t]) * Ecur[m] * z;
         }
       }
     } else {
@@ -733,10 +745,10 @@ __global__ void __launch_bounds__(512) frac_bwd_state_kernel(ScanParams p, BwdWo
             float v = (m < M ? Ecur[mm] : 0.0f) * z;
             if (intra && !direct) v += acc[r];
             const float dc = fexp(-lhm[t]) * v + dsum[r];
-            if (m < M && t < nv) dcg[(int64_t)(t0 + t) * M + m] = dc;
+            if (m < M && t < nv) dcg[(int64_t)(t0 + t) * p.Mall + m] = dc;
           } else if (intra) {
             const float dk = direct ? dsum[r] : fexp(lhm[t]) * acc[r];
-            if (m < M && t < nv) wk.dki[(bh_i * L + t0 + t) * M + m] = dk;
+            if (m < M && t < nv) wk.dki[(bh_i * L + t0 + t) * p.Mall + m] = dk;
           }
         }
       }
@@ -793,7 +805,7 @@ __global__ void __launch_bounds__(512) frac_bwd_state_kernel(ScanParams p, BwdWo
     const int pt = tid / MPF, j = tid - pt * MPF;
     float fs = 0.f;
     for (int q = 0; q < NBF; ++q) fs += red[(pt * NBF + q) * MPF + j];
-    wk.F[((int64_t)ps * p.Bsz * H + bh_i) * M + tid] = fs;
+    wk.F[((int64_t)ps * p.Bsz * H + bh_i) * p.Mall + tid] = fs;
   }
   if (tid == 0 && ps == 0) {
     float ds = 0.f;
@@ -804,7 +816,7 @@ __global__ void __launch_bounds__(512) frac_bwd_state_kernel(ScanParams p, BwdWo
 
 // ------------------------------------------------------------- cols sweep
 
-template <typename T, int MP, int NB>
+template <typename T, int MP, int NB, bool BLK = false>
 __global__ void __launch_bounds__(512) frac_bwd_cols_kernel(ScanParams p, BwdWork wk) {
   using Cfg = ColCfg<T, MP, NB>;
   constexpr int NP = Cfg::NP, XS = Cfg::XS, CS = Cfg::BS;  // C is read transposed here
@@ -855,7 +867,7 @@ __global__ void __launch_bounds__(512) frac_bwd_cols_kernel(ScanParams p, BwdWor
   for (int i = tid; i < 64 * CS; i += 512) Cb0[i] = Cb1[Cfg::NBUF == 2 ? i : 0] = (T)0.0f;
 
   // ---- adjoint G^T: Gs[m][pb] holds mode mo + m, rows p = 16 pb + 4 lg + r, column ncol
-  const int64_t sbase = ((int64_t)b * H + h) * (int64_t)M * N * P;
+  const int64_t sbase = ((int64_t)b * H + h) * (int64_t)p.Mall * N * P;
   floatx4 Gs[MPF][4];
   {
     int lo = ncol * P + lg * 4;
@@ -881,9 +893,10 @@ __global__ void __launch_bounds__(512) frac_bwd_cols_kernel(ScanParams p, BwdWor
   const float* dt_bh = p.dt + (int64_t)b * L * H + h;
   const float* al_bh = p.alpha + b * p.as0 + h * p.as2;
   const float* lm_bh = p.lambda ? p.lambda + b * p.ls0 + h * p.ls2 : nullptr;
-  const float* rl_bh = p.read_logit ? p.read_logit + ((int64_t)b * L * H + h) * M : nullptr;
-  const float* wl_bh = p.write_logit ? p.write_logit + ((int64_t)b * L * H + h) * M : nullptr;
-  const int64_t lg_st = (int64_t)H * M;
+  const float* rl_bh = p.read_logit ? p.read_logit + ((int64_t)b * L * H + h) * p.Mall : nullptr;
+  const float* wl_bh = p.write_logit ? p.write_logit + ((int64_t)b * L * H + h) * p.Mall : nullptr;
+  const int64_t lg_st = (int64_t)H * p.Mall;
+  const float* lse_bh = BLK ? p.lse + ((int64_t)b * L * H + h) * 2 : nullptr;  // [t][H][2]
   PairLogits<MP, 512> lgt_n;  // the logits of the next chunk's weight pass
   auto load_controls = [&](int c, float& dtv, float& al, float& lam) {
     const int tg = c * kQ + lane;
@@ -937,7 +950,9 @@ __global__ void __launch_bounds__(512) frac_bwd_cols_kernel(ScanParams p, BwdWor
     const ChunkCtl k = chunk_controls(dtv, al_l, lam_l, lm_bh != nullptr, nv);
     chunk_log_decays<MP, 8>(k.dtt, s_rr, P_lh, P_ll);
     barrier();  // log-decays in LDS
-    const int unsafe = pair_weights<MP, kCols>(k, nv, M, lgt, rl_bh == wl_bh, s_rr, s_lnt, P_lh, P_ll, Ecur, Enext, W);
+    const int unsafe = pair_weights<MP, kCols, 512, BLK>(k, nv, M, lgt, rl_bh == wl_bh, s_rr, s_lnt, P_lh, P_ll, Ecur,
+                                                         Enext, W, BLK ? lse_bh + (int64_t)t0 * H * 2 : nullptr,
+                                                         (int64_t)H * 2);
     float renf[MPF];
     int renbits = 0;
 #pragma unroll
@@ -1085,7 +1100,7 @@ struct RowCfg {
   static constexpr int TBP = (kBf16 ? MPW * NBW < 16 : MPW * NBW < 8) ? 4 : (kBf16 || MPW * NBW < 16) ? 2 : 1;
 };
 
-template <typename T, int MP, int NB>
+template <typename T, int MP, int NB, bool BLK = false>
 __global__ void __launch_bounds__(512) frac_bwd_rows_kernel(ScanParams p, BwdWork wk) {
   using Cfg = RowCfg<T, MP, NB>;
   constexpr int NP = Cfg::NP, XS = Cfg::XS, BS = Cfg::BS, CS = Cfg::CS;
@@ -1146,7 +1161,7 @@ __global__ void __launch_bounds__(512) frac_bwd_rows_kernel(ScanParams p, BwdWor
   for (int i = tid; i < 64 * CS; i += 512) Cb0[i] = Cb1[Cfg::NBUF == 2 ? i : 0] = (T)0.0f;
 
   // ---- adjoint G: Gs[m][jb] holds mode mo + m, rows n = 16 (nbo + jb) + 4 lg + r, column pc
-  const int64_t sbase = ((int64_t)b * H + h) * (int64_t)M * N * P;
+  const int64_t sbase = ((int64_t)b * H + h) * (int64_t)p.Mall * N * P;
   floatx4 Gs[MPW][NBW];
   {
     int lo = (mo * N + nbo * 16 + lg * 4) * P + pc;
@@ -1175,9 +1190,10 @@ __global__ void __launch_bounds__(512) frac_bwd_rows_kernel(ScanParams p, BwdWor
   const float* dt_bh = p.dt + (int64_t)b * L * H + h;
   const float* al_bh = p.alpha + b * p.as0 + h * p.as2;
   const float* lm_bh = p.lambda ? p.lambda + b * p.ls0 + h * p.ls2 : nullptr;
-  const float* rl_bh = p.read_logit ? p.read_logit + ((int64_t)b * L * H + h) * M : nullptr;
-  const float* wl_bh = p.write_logit ? p.write_logit + ((int64_t)b * L * H + h) * M : nullptr;
-  const int64_t lg_st = (int64_t)H * M;
+  const float* rl_bh = p.read_logit ? p.read_logit + ((int64_t)b * L * H + h) * p.Mall : nullptr;
+  const float* wl_bh = p.write_logit ? p.write_logit + ((int64_t)b * L * H + h) * p.Mall : nullptr;
+  const int64_t lg_st = (int64_t)H * p.Mall;
+  const float* lse_bh = BLK ? p.lse + ((int64_t)b * L * H + h) * 2 : nullptr;  // [t][H][2]
   PairLogits<MP, 512> lgt_n;  // the logits of the next chunk's weight pass
   auto load_controls = [&](int c, float& dtv, float& al, float& lam) {
     const int tg = c * kQ + lane;
@@ -1226,7 +1242,7 @@ __global__ void __launch_bounds__(512) frac_bwd_rows_kernel(ScanParams p, BwdWor
   }
   // (C B^T) o Gamma tiles written by the state sweep, loaded one chunk ahead (in processing order)
   const T* ggtiles = reinterpret_cast<const T*>(wk.gg);
-  float* dkg = wk.dk + ((int64_t)ps * p.Bsz * H * L + ((int64_t)b * H + h) * L) * M;  // this head's dk partial [L][M]
+  float* dkg = wk.dk + ((int64_t)ps * p.Bsz * H * L + ((int64_t)b * H + h) * L) * p.Mall;  // [L][Mall]
   TilePrefetch<T> ggt;
   ggt.load(ggtiles + ((int64_t)(b * nchunks + nchunks - 1) * H + h) * (kTiles * kTileElems), wave, lane);
 
@@ -1240,7 +1256,7 @@ __global__ void __launch_bounds__(512) frac_bwd_rows_kernel(ScanParams p, BwdWor
     const float dtv = pinned(dt_n), al_l = pinned(al_n), lam_l = pinned(lam_n);
     const PairLogits<MP, 512> lgt = lgt_n.pinned_copy();
     const TilePrefetch<T> gcur = ggt.pinned_copy();
-    if (Cfg::kBf16 && i > 0) store_dx(c + 1);
+    if (Cfg::kBf16 && i > 0 && !(BLK && p.y_part)) store_dx(c + 1);
     if (Cfg::NBUF == 2) {
       if (c > 0) stage_late(c - 1, Cn, Yn);
     } else {
@@ -1253,7 +1269,9 @@ __global__ void __launch_bounds__(512) frac_bwd_rows_kernel(ScanParams p, BwdWor
     const ChunkCtl k = chunk_controls(dtv, al_l, lam_l, lm_bh != nullptr, nv);
     chunk_log_decays<MP, 8>(k.dtt, s_rr, P_lh, P_ll);
     barrier();  // log-decays in LDS
-    const int unsafe = pair_weights<MP, kRows>(k, nv, M, lgt, rl_bh == wl_bh, s_rr, s_lnt, P_lh, P_ll, Ecur, Enext, W);
+    const int unsafe = pair_weights<MP, kRows, 512, BLK>(k, nv, M, lgt, rl_bh == wl_bh, s_rr, s_lnt, P_lh, P_ll, Ecur,
+                                                         Enext, W, BLK ? lse_bh + (int64_t)t0 * H * 2 : nullptr,
+                                                         (int64_t)H * 2);
     float renf[MPW];
     int renbits = 0;
 #pragma unroll
@@ -1345,7 +1363,7 @@ __global__ void __launch_bounds__(512) frac_bwd_rows_kernel(ScanParams p, BwdWor
           const int q = w2 / Cfg::NPW, mo2 = Cfg::kModeSplit ? q * MPW : 0;
           if (q < NPART && m >= mo2 && m < mo2 + MPW) wsum += redW[(w2 * MPW + (m - mo2)) * kQ + t];
         }
-        dkg[(int64_t)(t0 + t) * M + m] = P_dE[m * kWQ + t] * wsum;
+        dkg[(int64_t)(t0 + t) * p.Mall + m] = P_dE[m * kWQ + t] * wsum;
       }
     }
     if (!active) return;
@@ -1365,11 +1383,26 @@ __global__ void __launch_bounds__(512) frac_bwd_rows_kernel(ScanParams p, BwdWor
       const int t = tb * 16 + li, pr = pb * 16 + lg * 4;
       float yv[4];
       load4(Yc + t * XS + pr, yv);
-      floatx4 v;
+      floatx4 v = dxa[tb];
+      if constexpr (BLK) {  // a mode block: float32 partial sums across the blocks
+        const int64_t xi = (((int64_t)b * L + t0 + t) * H + h) * P + pr;
+        if (t < nv && pr < P) {
+          if (p.y_in) {
+            const float4 u = *reinterpret_cast<const float4*>(p.y_in + xi);
+            v[0] += u.x;
+            v[1] += u.y;
+            v[2] += u.z;
+            v[3] += u.w;
+          }
+          if (p.y_part) *reinterpret_cast<float4*>(p.y_part + xi) = make_float4(v[0], v[1], v[2], v[3]);
+        }
+      }
 #pragma unroll
-      for (int r = 0; r < 4; ++r) v[r] = dxa[tb][r] + Dh * yv[r];
-      if (Cfg::kBf16) store4(Dxb + t * XS + pr, v);  // staged, stored 16 bytes at a time
-      else if (t < nv && pr < P) store4(dxg + (int64_t)t0 * xstride + t * (H * P) + pr, v);
+      for (int r = 0; r < 4; ++r) v[r] += Dh * yv[r];
+      if (!(BLK && p.y_part)) {
+        if (Cfg::kBf16) store4(Dxb + t * XS + pr, v);  // staged, stored 16 bytes at a time
+        else if (t < nv && pr < P) store4(dxg + (int64_t)t0 * xstride + t * (H * P) + pr, v);
+      }
     }
 
     __builtin_amdgcn_sched_barrier(0);
@@ -1419,7 +1452,7 @@ __global__ void __launch_bounds__(512) frac_bwd_rows_kernel(ScanParams p, BwdWor
   }
   wait_vmem();
   barrier();
-  if (Cfg::kBf16) store_dx(0);
+  if (Cfg::kBf16 && !(BLK && p.y_part)) store_dx(0);
 
   // ---- the adjoint of the state before token 0 (this workgroup's columns of P)
   if (p.dinit_state && active) {
@@ -1470,7 +1503,7 @@ __global__ void __launch_bounds__(512) frac_bwd_rows_kernel(ScanParams p, BwdWor
       const int mow = Cfg::kModeSplit ? pw * MPW : 0;
       if (pw < NPART && tid >= mow && tid < mow + MPW) s += redW[w * MPW + tid - mow];
     }
-    wk.I[((int64_t)ps * p.Bsz * H + (int64_t)b * H + h) * M + tid] = s;
+    wk.I[((int64_t)ps * p.Bsz * H + (int64_t)b * H + h) * p.Mall + tid] = s;
   }
 }
 
@@ -1484,7 +1517,7 @@ __global__ void __launch_bounds__(512) frac_bwd_rows_kernel(ScanParams p, BwdWor
 // as float32 matrix-core products e^{-l_t} (H kappa e^{l})_t and e^{l_k} (H^T c e^{-l})_k
 // for the modes whose chunk decay stays below the factorisation bound, one
 // exponential per pair for the others.
-template <typename T, int MP>
+template <typename T, int MP, bool BLK = false>
 __global__ void __launch_bounds__(256) frac_bwd_intra_kernel(ScanParams p, const T* __restrict__ gtiles,
                                                              float* __restrict__ dc_out, float* __restrict__ dk_out) {
   constexpr bool kBf16 = sizeof(T) == 2;
@@ -1540,15 +1573,16 @@ __global__ void __launch_bounds__(256) frac_bwd_intra_kernel(ScanParams p, const
   const float al = tv ? strided3(p.alpha, p.as0, p.as1, p.as2, b, t0 + lane, h) : 1.0f;
   const float lam = (tv && p.lambda) ? strided3(p.lambda, p.ls0, p.ls1, p.ls2, b, t0 + lane, h) : 1.0f;
   const ChunkCtl k = chunk_controls(dtv, al, lam, p.lambda != nullptr, nv);
-  const float* rl_bh = p.read_logit ? p.read_logit + ((int64_t)b * L * H + h) * M : nullptr;
-  const float* wl_bh = p.write_logit ? p.write_logit + ((int64_t)b * L * H + h) * M : nullptr;
+  const float* rl_bh = p.read_logit ? p.read_logit + ((int64_t)b * L * H + h) * p.Mall : nullptr;
+  const float* wl_bh = p.write_logit ? p.write_logit + ((int64_t)b * L * H + h) * p.Mall : nullptr;
   PairLogits<MP, 256> lgt;
-  lgt.load(rl_bh, wl_bh, t0, nv, M, (int64_t)H * M, tid);
+  lgt.load(rl_bh, wl_bh, t0, nv, M, (int64_t)H * p.Mall, tid);
+  const float* lse_c = BLK ? p.lse + (((int64_t)b * L + t0) * H + h) * 2 : nullptr;
   __syncthreads();  // rates, zeroed H, x and dy in LDS
   chunk_log_decays<MP, 4>(k.dtt, s_rr, P_lh, P_ll);
   __syncthreads();  // log-decays in LDS
-  const int unsafe = pair_weights<MP, kIntra, 256>(k, nv, M, lgt, rl_bh == wl_bh, s_rr, s_lnt, P_lh, P_ll, nullptr,
-                                                   nullptr, W);
+  const int unsafe = pair_weights<MP, kIntra, 256, BLK>(k, nv, M, lgt, rl_bh == wl_bh, s_rr, s_lnt, P_lh, P_ll,
+                                                        nullptr, nullptr, W, lse_c, (int64_t)H * 2);
   // ---- H = (C B^T) o (dY X^T), causal tiles [t][k]
   const T* gt = gtiles + (((int64_t)b * nchunks + c) * G + g) * (kTiles * kTileElems);
   for (int tile = wave; tile < kTiles; tile += 4) {
@@ -1564,7 +1598,7 @@ __global__ void __launch_bounds__(256) frac_bwd_intra_kernel(ScanParams p, const
 
   // ---- tokens of row block tb = wave (dc) and column block tb (dk), modes as columns
   const int tb = wave;
-  const int64_t obase = (((int64_t)b * H + h) * L + t0) * M;
+  const int64_t obase = (((int64_t)b * H + h) * L + t0) * p.Mall;
 #pragma unroll
   for (int mb = 0; mb < MB; ++mb) {
     const int m = mb * 16 + li;
@@ -1597,18 +1631,19 @@ __global__ void __launch_bounds__(256) frac_bwd_intra_kernel(ScanParams p, const
         for (int t2 = t; t2 < 64; ++t2) dk += Hs[t2 * HS + t] * P_O[mm * kWQ + t2] * ell_decay(lhm, llm, t2, t);
       }
       if (m < M && t < nv) {
-        dc_out[obase + (int64_t)t * M + m] = dc;
-        dk_out[obase + (int64_t)t * M + m] = dk;
+        dc_out[obase + (int64_t)t * p.Mall + m] = dc;
+        dk_out[obase + (int64_t)t * p.Mall + m] = dk;
       }
     }
   }
 }
 
-// dB, dC of each group: fixed-order sum of the per-head partials; each thread
-// sums 16 bytes of a (token, group) row over the group's heads.
+// dB, dC of each group: fixed-order sum of the per-head partials (over the mode
+// blocks, then the group's heads); each thread sums 16 bytes of a (token, group) row.
 template <typename T>
 __global__ void __launch_bounds__(256) frac_bwd_group_sum_kernel(ScanParams p, const T* __restrict__ dBp,
-                                                                 const T* __restrict__ dCp, int64_t nrows) {
+                                                                 const T* __restrict__ dCp, int64_t nrows, int nslot,
+                                                                 int64_t slot_stride) {
   constexpr int E = 16 / sizeof(T);
   const int H = p.H, N = p.N, G = p.G, hpg = H / G, cpr = N / E;  // 16-byte chunks per row
   const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
@@ -1620,22 +1655,23 @@ __global__ void __launch_bounds__(256) frac_bwd_group_sum_kernel(ScanParams p, c
   float sb[E], sc[E];
 #pragma unroll
   for (int k = 0; k < E; ++k) sb[k] = sc[k] = 0.0f;
-  for (int j = 0; j < hpg; ++j) {
-    const int64_t off = (bt * H + g * hpg + j) * N + ch * E;
-    float vb[E], vc[E];
-    if constexpr (E == 8) {
-      load8(dBp + off, vb);
-      load8(dCp + off, vc);
-    } else {
-      load4(dBp + off, vb);
-      load4(dCp + off, vc);
-    }
+  for (int q = 0; q < nslot; ++q)
+    for (int j = 0; j < hpg; ++j) {
+      const int64_t off = q * slot_stride + (bt * H + g * hpg + j) * N + ch * E;
+      float vb[E], vc[E];
+      if constexpr (E == 8) {
+        load8(dBp + off, vb);
+        load8(dCp + off, vc);
+      } else {
+        load4(dBp + off, vb);
+        load4(dCp + off, vc);
+      }
 #pragma unroll
-    for (int k = 0; k < E; ++k) {
-      sb[k] += vb[k];
-      sc[k] += vc[k];
+      for (int k = 0; k < E; ++k) {
+        sb[k] += vb[k];
+        sc[k] += vc[k];
+      }
     }
-  }
   T* dB = reinterpret_cast<T*>(p.dBm) + rg * N + ch * E;
   T* dC = reinterpret_cast<T*>(p.dCm) + rg * N + ch * E;
 #pragma unroll
@@ -1645,35 +1681,69 @@ __global__ void __launch_bounds__(256) frac_bwd_group_sum_kernel(ScanParams p, c
   }
 }
 
+constexpr int kModeBlock = 8;  // modes per launch of the mode-block backward
+
 // Workgroups per head of the state sweep (along N) and of the rows sweep (along P),
 // as ColCfg and RowCfg choose them.
 int pad_modes(int M) { return M <= 1 ? 1 : M <= 2 ? 2 : M <= 4 ? 4 : 8; }
 int state_parts(const ScanParams& p) { return pad_modes(p.M) * (p.NP / 16) > 32 ? 2 : 1; }
 int rows_parts(const ScanParams& p) { return (pad_modes(p.M) >= 8 && p.io_bf16) ? 2 : 1; }
+int mode_blocks(const ScanParams& p) { return p.Mall > kModeBlock ? (p.Mall + kModeBlock - 1) / kModeBlock : 1; }
 
+// Workspace: C B^T tiles, the state sweep's Gamma tiles, per-head dB / dC partials
+// (per mode block), the (token, mode) partials, per-mode terms, dD partials, the
+// finisher's tile sums; with mode blocks also the log-normalizers and the float32
+// partial dx.
 struct BwdLayout {
-  size_t tiles, gg, hg, dBp, dCp, dc, dk, F, I, dDp, gtl, total;
+  size_t tiles, gg, hg, dBp, dCp, dc, dk, F, I, dDp, gtl, lse, dxp, total;
 };
 
 BwdLayout bwd_layout(const ScanParams& p) {
   BwdLayout l{};
   const size_t es = p.io_bf16 ? 2 : 4;
-  const size_t bl = (size_t)p.Bsz * p.L, blhm = bl * p.H * p.M, bh = (size_t)p.Bsz * p.H;
+  const size_t bl = (size_t)p.Bsz * p.L, blhm = bl * p.H * p.Mall, bh = (size_t)p.Bsz * p.H;
+  const size_t nmb = (size_t)mode_blocks(p);
   auto up = [](size_t v) { return (v + 255) / 256 * 256; };
   l.tiles = 0;
   const size_t gtb = (size_t)p.Bsz * ((p.L + kQ - 1) / kQ) * p.H * kTiles * kTileElems * es;
   l.gg = up(cb_tiles_bytes(p));
   l.hg = l.gg + up(gtb);
   l.dBp = l.hg + up(gtb);
-  l.dCp = l.dBp + up(bl * p.H * p.N * es);
-  l.dc = l.dCp + up(bl * p.H * p.N * es);
+  l.dCp = l.dBp + up(nmb * bl * p.H * p.N * es);
+  l.dc = l.dCp + up(nmb * bl * p.H * p.N * es);
   l.dk = l.dc + up(sizeof(float) * (state_parts(p) + 1) * blhm);
   l.F = l.dk + up(sizeof(float) * (rows_parts(p) + 1) * blhm);
-  l.I = l.F + up(sizeof(float) * state_parts(p) * bh * p.M);
-  l.dDp = l.I + up(sizeof(float) * rows_parts(p) * bh * p.M);
+  l.I = l.F + up(sizeof(float) * state_parts(p) * bh * p.Mall);
+  l.dDp = l.I + up(sizeof(float) * rows_parts(p) * bh * p.Mall);
   l.gtl = l.dDp + up(sizeof(float) * bh);
-  l.total = l.gtl + up(grad_tiles_bytes(p));
+  l.lse = l.gtl + up(grad_tiles_bytes(p));
+  l.dxp = l.lse + (nmb > 1 ? up(sizeof(float) * 2 * bl * p.H) : 0);
+  l.total = l.dxp + (nmb > 1 ? up(sizeof(float) * bl * p.H * p.P) : 0);
   return l;
+}
+
+// The three sweeps (and the intra-chunk kernel when the state sweep does not fold
+// it in) for the modes p covers.
+template <typename T, int MP, int NB, bool BLK>
+hipError_t launch_bwd_sweeps(const ScanParams& p, const BwdWork& wk, const T* tiles, size_t blhm, hipStream_t stream) {
+  using SC = ColCfg<T, MP, NB>;
+  using RC = RowCfg<T, MP, NB>;
+  constexpr bool kFold = StateLds<T, MP, NB>::kFold;
+  const int bh = p.Bsz * p.H;
+  hipLaunchKernelGGL((frac_bwd_state_kernel<T, MP, NB, BLK>), dim3(bh * SC::PS), dim3(512), 0, stream, p, wk);
+  hipError_t e;
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  hipLaunchKernelGGL((frac_bwd_rows_kernel<T, MP, NB, BLK>), dim3(bh * RC::PS), dim3(512), 0, stream, p, wk);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  hipLaunchKernelGGL((frac_bwd_cols_kernel<T, MP, NB, BLK>), dim3(bh * SC::PS), dim3(512), 0, stream, p, wk);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  if constexpr (!kFold) {
+    const int64_t nblk = (int64_t)p.Bsz * ((p.L + kQ - 1) / kQ) * p.H;
+    hipLaunchKernelGGL((frac_bwd_intra_kernel<T, MP, BLK>), dim3((unsigned)nblk), dim3(256), 0, stream, p, tiles,
+                       wk.dc + SC::PS * blhm, wk.dki);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+  }
+  return hipSuccess;
 }
 
 template <typename T, int MP, int NB>
@@ -1683,7 +1753,7 @@ hipError_t launch_bwd_variant(const ScanParams& p, void* ws, hipStream_t stream)
   if (SC::PS != state_parts(p) || RC::PS != rows_parts(p)) return hipErrorInvalidValue;
   const BwdLayout l = bwd_layout(p);
   unsigned char* base = reinterpret_cast<unsigned char*>(ws);
-  const size_t blhm = (size_t)p.Bsz * p.L * p.H * p.M;
+  const size_t blhm = (size_t)p.Bsz * p.L * p.H * p.Mall;
   BwdWork wk;
   wk.tiles = base + l.tiles;
   wk.gg = base + l.gg;
@@ -1702,18 +1772,44 @@ hipError_t launch_bwd_variant(const ScanParams& p, void* ws, hipStream_t stream)
   wk.dki = wk.dk + RC::PS * blhm;
   hipError_t e = launch_cb_tiles(p, base + l.tiles, stream);
   if (e != hipSuccess) return e;
-  const int bh = p.Bsz * p.H;
-  hipLaunchKernelGGL((frac_bwd_state_kernel<T, MP, NB>), dim3(bh * SC::PS), dim3(512), 0, stream, p, wk);
-  if ((e = hipGetLastError()) != hipSuccess) return e;
-  hipLaunchKernelGGL((frac_bwd_rows_kernel<T, MP, NB>), dim3(bh * RC::PS), dim3(512), 0, stream, p, wk);
-  if ((e = hipGetLastError()) != hipSuccess) return e;
-  hipLaunchKernelGGL((frac_bwd_cols_kernel<T, MP, NB>), dim3(bh * SC::PS), dim3(512), 0, stream, p, wk);
-  if ((e = hipGetLastError()) != hipSuccess) return e;
-  if constexpr (!kFold) {
-    const int64_t nblk = (int64_t)p.Bsz * ((p.L + kQ - 1) / kQ) * p.H;
-    hipLaunchKernelGGL((frac_bwd_intra_kernel<T, MP>), dim3((unsigned)nblk), dim3(256), 0, stream, p,
-                       reinterpret_cast<const T*>(base + l.tiles), wk.dc + SC::PS * blhm, wk.dki);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
+  const T* tiles = reinterpret_cast<const T*>(base + l.tiles);
+  const int nmb = mode_blocks(p);
+  if (nmb == 1) {
+    if ((e = launch_bwd_sweeps<T, MP, NB, false>(p, wk, tiles, blhm, stream)) != hipSuccess) return e;
+  } else if constexpr (MP == kModeBlock) {
+    // More modes than one workgroup's registers hold: the sweeps once per block of
+    // eight modes, the weights normalised over the bank, dx summed in float32 in
+    // block order (the last block adds the skip term), dB and dC per block.
+    float* lse = reinterpret_cast<float*>(base + l.lse);
+    float* dxp = reinterpret_cast<float*>(base + l.dxp);
+    if ((e = launch_mode_lse(p, lse, stream)) != hipSuccess) return e;
+    const int64_t NPs = (int64_t)p.N * p.P;
+    const size_t slot = (size_t)p.Bsz * p.L * p.H * p.N * sizeof(T);
+    for (int q = 0; q < nmb; ++q) {
+      const int mo = q * kModeBlock;
+      ScanParams pb = p;
+      pb.M = min(kModeBlock, p.Mall - mo);
+      pb.tau = p.tau + mo;
+      if (p.read_logit) pb.read_logit = p.read_logit + mo;
+      if (p.write_logit) pb.write_logit = p.write_logit + mo;
+      if (p.init_state) pb.init_state = p.init_state + mo * NPs;
+      if (p.d_final_state) pb.d_final_state = p.d_final_state + mo * NPs;
+      if (p.dinit_state) pb.dinit_state = p.dinit_state + mo * NPs;
+      pb.lse = lse;
+      pb.y_in = q > 0 ? dxp : nullptr;
+      pb.y_part = q + 1 < nmb ? dxp : nullptr;
+      BwdWork wb = wk;
+      wb.dBp = reinterpret_cast<unsigned char*>(wk.dBp) + q * slot;
+      wb.dCp = reinterpret_cast<unsigned char*>(wk.dCp) + q * slot;
+      wb.dc = wk.dc + mo;
+      wb.dk = wk.dk + mo;
+      wb.dki = wk.dki + mo;
+      wb.F = wk.F + mo;
+      wb.I = wk.I + mo;
+      if ((e = launch_bwd_sweeps<T, MP, NB, true>(pb, wb, tiles, blhm, stream)) != hipSuccess) return e;
+    }
+  } else {
+    return hipErrorInvalidValue;
   }
   GradInputs gi;
   gi.dc = wk.dc;
@@ -1733,7 +1829,8 @@ hipError_t launch_bwd_variant(const ScanParams& p, void* ws, hipStream_t stream)
   const int64_t nrows = (int64_t)p.Bsz * p.L;
   const int64_t nthr = nrows * p.G * (p.N / (16 / (int)sizeof(T)));
   hipLaunchKernelGGL((frac_bwd_group_sum_kernel<T>), dim3((unsigned)((nthr + 255) / 256)), dim3(256), 0, stream, p,
-                     reinterpret_cast<const T*>(wk.dBp), reinterpret_cast<const T*>(wk.dCp), nrows);
+                     reinterpret_cast<const T*>(wk.dBp), reinterpret_cast<const T*>(wk.dCp), nrows, nmb,
+                     (int64_t)p.Bsz * p.L * p.H * p.N);
   return hipGetLastError();
 }
 

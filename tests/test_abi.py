@@ -82,15 +82,18 @@ def test_invalid_shapes_are_rejected_on_the_host(kw, status):
 
 
 def test_mode_blocks_are_sized_on_the_host():
-    """More than 8 modes (up to 32) run the forward in blocks of eight: the shape is
-    accepted and the workspace holds the float32 partial output."""
+    """More than 8 modes (up to 32) run the scan in blocks of eight: the shape is
+    accepted and both workspaces hold the float32 partial output."""
     lib = _lib.load()
     for M in (9, 16, 32):
         sh = _shape(nmodes=M)
-        need = lib.frac_scan_workspace_size(ctypes.byref(sh), 0)
-        assert need >= sh.batch * sh.seqlen * sh.nheads * sh.headdim * 4, M
+        for bwd in (0, 1):
+            need = lib.frac_scan_workspace_size(ctypes.byref(sh), bwd)
+            assert need >= sh.batch * sh.seqlen * sh.nheads * sh.headdim * 4, (M, bwd)
         a = FracFwdArgs()
         assert lib.frac_scan_fwd(ctypes.byref(sh), ctypes.byref(a), None, 0, None) == -1  # pointers missing
+        b = FracBwdArgs()
+        assert lib.frac_scan_bwd(ctypes.byref(sh), ctypes.byref(b), None, 0, None) == -1
 
 
 def test_missing_pointers_are_rejected():

@@ -78,6 +78,12 @@ CASES = {
                                        final_state=True),
     # 8 modes with heads in two groups (per-head dB, dC partials summed per group)
     "bf16 M8 groups P48": Workload("t", 1, 190, 4, 48, 64, 8, ngroups=2, backward=True),
+    # banks of more than 8 modes: the sweeps once per block of eight modes
+    "bf16 M16 extras dfinal": Workload("t", 1, 200, 2, 64, 128, 16, extras=True, init_state=True, backward=True,
+                                       final_state=True),
+    "f32 M12 N64 extras dfinal": Workload("t", 1, 150, 2, 32, 64, 12, io_dtype="f32", extras=True, init_state=True,
+                                          backward=True, final_state=True),
+    "bf16 M32 groups": Workload("t", 1, 140, 4, 64, 64, 32, ngroups=2, backward=True, final_state=True),
 }
 
 
@@ -101,7 +107,7 @@ def test_bwd_parity_small(name):
 
 
 ALL_GRAD_CASES = ["f32 extras dfinal", "f32 M8 N128 extras dfinal", "bf16 M5 N96 P32 extras", "bf16 groups extras",
-                  "bf16 M8", "bf16 L1"]
+                  "bf16 M8", "bf16 L1", "bf16 M16 extras dfinal", "f32 M12 N64 extras dfinal", "bf16 M32 groups"]
 
 
 @pytest.mark.parametrize("moderate", [False, True])
@@ -163,6 +169,24 @@ def test_bwd_deterministic():
     torch.cuda.synchronize()
     for k in ("dx", "ddt", "dBm", "dCm"):
         assert torch.equal(g1[k], g2[k]), k
+
+
+def test_bwd_full_size_sampled_bank_of_16():
+    """The training workload with the paper's bank of 16 modes (two blocks of eight),
+    at full size: dx and ddt on sampled heads, the last batch element and last head
+    among them."""
+    w = TRAIN.scaled(nmodes=16)
+    inp = device_inputs(w, seed=6)
+    tau_d, tau64 = _tau(w.nmodes)
+    print("full-size", w.name, "M16", flush=True)
+    g = _run_bwd(inp, tau_d)
+    torch.cuda.synchronize()
+    for k in ("dx", "ddt", "dBm", "dCm"):
+        assert torch.isfinite(g[k].float()).all(), k
+    for (b, h) in [(0, 0), (3, 63)]:
+        ref = _oracle_bwd(inp, tau64, b=b, h=h)
+        assert_close("dx[%d,:,%d]" % (b, h), f64(g["dx"][b:b + 1, :, h:h + 1]), ref["dx"], TOL["bf16"])
+        assert_close("ddt[%d,:,%d]" % (b, h), f64(g["ddt"][b:b + 1, :, h:h + 1]), ref["ddt"], TOL["bf16"])
 
 
 def test_bwd_full_size_sampled():
