@@ -48,6 +48,8 @@
 // accumulators every chunk: the state is held as E_m * S^_m with a float scale E_m
 // that absorbs the chunk decays, and the accumulators are rescaled only when E_m
 // would fall below 2^-60.
+#include <algorithm>
+
 #include "frac_device.h"
 #include "frac_kernels.h"
 
@@ -157,8 +159,10 @@ struct FwdCfg {
   static constexpr int TBP = (kBf16 ? MPW * NBW < 16 : MPW * NBW < 8) ? 4 : (kBf16 || MPW * NBW < 16) ? 2 : 1;
 };
 
-// STATE_ONLY: only the state update over tokens [0, seg_len), ending in seg_state
-// (the first pass of a sequence-split forward).
+// STATE_ONLY: only the state update over one sequence segment (all but the last),
+// from a zero state (the first segment: the initial state), ending in that
+// segment's slot of seg_state, with the segment's per-mode decay (the first pass
+// of a sequence-split forward).
 // BLK: one block of a mode-block launch sequence (weights normalised with p.lse,
 // outputs accumulated through p.y_in / p.y_part).
 template <typename T, int MP, int NB, int PS, bool STATE_ONLY, bool BLK = false>
@@ -169,11 +173,11 @@ __global__ void __launch_bounds__(512) frac_fwd_kernel(ScanParams p, const T* __
   constexpr int NWT = 8;                  // waves in the workgroup
   const int tid = threadIdx.x;
   const int wave = tid >> 6, lane = tid & 63, li = lane & 15, lg = lane >> 4;
-  // Sequence segment: with p.seg_len > 0 the grid of the output pass holds the
-  // (batch, head) blocks twice, the second copy for tokens [seg_len, L) starting
-  // from the boundary state.
+  // Sequence segment: with p.nseg > 1 the grid holds the (batch, head) blocks once
+  // per segment (the state-only pass: per segment but the last), segment k covering
+  // tokens [k seg_len, (k + 1) seg_len).
   const int nbh_blocks = p.Bsz * p.H * Cfg::PS;
-  const int seg = (!STATE_ONLY && p.seg_len > 0 && (int)blockIdx.x >= nbh_blocks) ? 1 : 0;
+  const int seg = p.nseg > 1 ? (int)blockIdx.x / nbh_blocks : 0;
   const int bid = (int)blockIdx.x - seg * nbh_blocks;
   const int ps = bid % Cfg::PS;                         // which columns of P
   const int pb = ps * Cfg::NPW + wave % Cfg::NPW, part = wave / Cfg::NPW;
@@ -185,11 +189,13 @@ __global__ void __launch_bounds__(512) frac_fwd_kernel(ScanParams p, const T* __
   const int pc = pb * 16 + li;
   const int L = p.L, H = p.H, P = p.P, N = p.N, M = p.M, G = p.G;
   const int nchunks = (L + kQ - 1) / kQ;
-  const int T0 = seg ? p.seg_len : 0;                                       // first token
-  const int T1 = (STATE_ONLY || (p.seg_len > 0 && !seg)) ? p.seg_len : L;  // one past the last
-  const int c0 = T0 / kQ, c1 = (T1 + kQ - 1) / kQ;                          // chunks of the segment
-  const float* init_state = seg ? p.seg_state : p.init_state;
-  float* final_state = STATE_ONLY ? p.seg_state : (T1 == L ? p.final_state : nullptr);
+  const int T0 = seg * p.seg_len;                                                // first token
+  const int T1 = p.nseg > 1 ? min(L, (seg + 1) * p.seg_len) : L;                // one past the last
+  const int c0 = T0 / kQ, c1 = (T1 + kQ - 1) / kQ;                              // chunks of the segment
+  const int64_t seg_ss = (int64_t)p.Bsz * p.H * p.Mall * p.N * p.P;             // one boundary state
+  const float* init_state = seg == 0 ? p.init_state : (STATE_ONLY ? nullptr : p.seg_state + (seg - 1) * seg_ss);
+  float* final_state = STATE_ONLY ? p.seg_state + seg * seg_ss : (T1 == L ? p.final_state : nullptr);
+  double seg_ell = 0.0;  // state-only pass, thread m < M: the segment's summed log-decay of mode m
 
   // Blocks are dealt round-robin to the 8 XCDs; give each XCD a contiguous run of
   // (batch, head) so that heads sharing B and C share one L2.
@@ -349,6 +355,7 @@ __global__ void __launch_bounds__(512) frac_fwd_kernel(ScanParams p, const T* __
     const float dtt_l = (lane < nv) ? dtv * s_eff_l : 0.0f;
     chunk_log_decays<MP, NWT>(dtt_l, s_rr, P_lh, P_ll);
     barrier();  // log-decays in LDS
+    if (STATE_ONLY && tid < MP) seg_ell += (double)P_lh[tid * kWQ + kQ - 1] + (double)P_ll[tid * kWQ + kQ - 1];
 
     // ---- per (token, mode) controls and weights: thread pair = t MP + m
     // bit m of unsafe: the factorised Gamma would overflow for mode m (direct decay);
@@ -591,6 +598,8 @@ __global__ void __launch_bounds__(512) frac_fwd_kernel(ScanParams p, const T* __
   wait_vmem();
   barrier();
   if (!STATE_ONLY && !(BLK && p.y_part)) store_y(c1 - 1);
+  if (STATE_ONLY && ps == 0 && tid < M)
+    p.seg_decay[((int64_t)seg * p.Bsz * H + (int64_t)b * H + h) * p.Mall + tid] = (float)exp(-seg_ell);
 
   if (final_state && active) {
     const float* Ef = s_E2 + (c1 & 1) * MP;
@@ -629,35 +638,100 @@ hipError_t launch_cb_variant(const ScanParams& p, T* gt, hipStream_t stream) {
   return hipGetLastError();
 }
 
-// Workgroups per (batch, head) along P: two with 8 modes (register budget), and
-// with 4 modes when few (batch, head) pairs would leave compute units idle.
+// Workgroups per (batch, head) along P: two with 8 modes (register budget); with 4
+// modes two when few (batch, head) pairs would leave compute units idle and the
+// sequence is too short to split.
 int fwd_p_split(const ScanParams& p) {
   const int MP = p.M <= 1 ? 1 : p.M <= 2 ? 2 : p.M <= 4 ? 4 : 8;
-  return (MP >= 8 || (MP >= 4 && p.Bsz * p.H < 192)) ? 2 : 1;
+  const int nchunks = (p.L + kQ - 1) / kQ;
+  return (MP >= 8 || (MP >= 4 && p.Bsz * p.H < 192 && nchunks < 16)) ? 2 : 1;
 }
 
-// Sequence split: when the (batch, head) workgroups fill at most half of the 256
-// compute units and the sequence is long, the sequence is cut at a chunk boundary
-// near its middle.  A state-only pass scans the first part to the boundary state;
-// the output pass then runs both parts at once, the second from that state.
-int fwd_seg_len(const ScanParams& p) {
+// Sequence split: when the (batch, head) workgroups fill fewer than two per compute
+// unit (512) and the sequence is long, it is cut into up to 16 segments of whole
+// chunks (at least 4 each).  A state-only pass scans every segment but the last
+// from a zero state, a combine pass chains their end states into the boundary
+// states, and the output pass runs all segments at once.
+struct FwdSplit {
+  int nseg, seg_len;
+};
+
+FwdSplit fwd_split(const ScanParams& p) {
   const int nchunks = (p.L + kQ - 1) / kQ;
-  if (2 * (int64_t)p.Bsz * p.H * fwd_p_split(p) > 256 || nchunks < 8) return 0;
-  return (nchunks / 2) * kQ;
+  const int64_t wg = (int64_t)p.Bsz * p.H * fwd_p_split(p);
+  if (wg >= 512 || nchunks < 8) return {1, p.L};
+  int k = (int)std::min<int64_t>({(int64_t)16, (512 + wg - 1) / wg, (int64_t)(nchunks / 4)});
+  if (k < 2) return {1, p.L};
+  const int per = (nchunks + k - 1) / k;
+  return {(nchunks + per - 1) / per, per * kQ};
 }
 
 size_t align256(size_t n) { return (n + 255) & ~(size_t)255; }
 
-template <typename T, int MP, int NB, int PS, bool BLK = false>
-hipError_t launch_fwd_ps(const ScanParams& p, const T* gt, hipStream_t stream) {
-  const unsigned blocks = (unsigned)(p.Bsz * p.H * PS);
-  // the state-only pass: one workgroup per 16 columns of P
-  if (p.seg_len > 0)
-    hipLaunchKernelGGL((frac_fwd_kernel<T, MP, NB, 4, true, BLK>), dim3((unsigned)(p.Bsz * p.H * 4)), dim3(512), 0,
-                       stream, p, gt);
-  hipLaunchKernelGGL((frac_fwd_kernel<T, MP, NB, PS, false, BLK>), dim3(blocks * (p.seg_len > 0 ? 2 : 1)), dim3(512),
-                     0, stream, p, gt);
+// Boundary states and decays of a split forward, after the C B^T tiles.
+size_t split_bytes(const ScanParams& p, const FwdSplit& sp) {
+  if (sp.nseg <= 1) return 0;
+  const size_t ns = (size_t)sp.nseg - 1, bhm = (size_t)p.Bsz * p.H * p.Mall;
+  return align256(sizeof(float) * ns * bhm * p.N * p.P) + align256(sizeof(float) * ns * bhm);
+}
+
+void place_split(ScanParams& p, const FwdSplit& sp, unsigned char* at) {
+  p.nseg = sp.nseg;
+  p.seg_len = sp.seg_len;
+  if (sp.nseg <= 1) {
+    p.seg_state = nullptr;
+    p.seg_decay = nullptr;
+    return;
+  }
+  const size_t ns = (size_t)sp.nseg - 1, bhm = (size_t)p.Bsz * p.H * p.Mall;
+  p.seg_state = reinterpret_cast<float*>(at);
+  p.seg_decay = reinterpret_cast<float*>(at + align256(sizeof(float) * ns * bhm * p.N * p.P));
+}
+
+// The boundary states: S_k = decay_k S_{k-1} + (segment k's own end state), in
+// segment order, per state element (all modes of the bank).
+__global__ void __launch_bounds__(256) frac_seg_combine_kernel(ScanParams p) {
+  const int64_t ss = (int64_t)p.Bsz * p.H * p.Mall * p.N * p.P;
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= ss) return;
+  const int64_t bhm = i / ((int64_t)p.N * p.P), nbhm = (int64_t)p.Bsz * p.H * p.Mall;
+  float s = p.seg_state[i];
+  for (int k = 1; k + 1 < p.nseg; ++k) {
+    s = p.seg_decay[k * nbhm + bhm] * s + p.seg_state[k * ss + i];
+    p.seg_state[k * ss + i] = s;
+  }
+}
+
+hipError_t launch_seg_combine(const ScanParams& p, hipStream_t stream) {
+  if (p.nseg <= 2) return hipSuccess;  // one boundary: the first segment's end state
+  const int64_t ss = (int64_t)p.Bsz * p.H * p.Mall * p.N * p.P;
+  hipLaunchKernelGGL(frac_seg_combine_kernel, dim3((unsigned)((ss + 255) / 256)), dim3(256), 0, stream, p);
   return hipGetLastError();
+}
+
+// The state-only pass over every segment but the last (one workgroup per (batch,
+// head) and PS column blocks, as the output pass).
+template <typename T, int MP, int NB, int PS, bool BLK = false>
+hipError_t launch_fwd_state_pass(const ScanParams& p, const T* gt, hipStream_t stream) {
+  if (p.nseg <= 1) return hipSuccess;
+  const unsigned blocks = (unsigned)(p.Bsz * p.H * PS * (p.nseg - 1));
+  hipLaunchKernelGGL((frac_fwd_kernel<T, MP, NB, PS, true, BLK>), dim3(blocks), dim3(512), 0, stream, p, gt);
+  return hipGetLastError();
+}
+
+template <typename T, int MP, int NB, int PS, bool BLK = false>
+hipError_t launch_fwd_out_pass(const ScanParams& p, const T* gt, hipStream_t stream) {
+  const unsigned blocks = (unsigned)(p.Bsz * p.H * PS * p.nseg);
+  hipLaunchKernelGGL((frac_fwd_kernel<T, MP, NB, PS, false, BLK>), dim3(blocks), dim3(512), 0, stream, p, gt);
+  return hipGetLastError();
+}
+
+template <typename T, int MP, int NB, int PS>
+hipError_t launch_fwd_ps(const ScanParams& p, const T* gt, hipStream_t stream) {
+  hipError_t e = launch_fwd_state_pass<T, MP, NB, PS>(p, gt, stream);
+  if (e == hipSuccess) e = launch_seg_combine(p, stream);
+  if (e == hipSuccess) e = launch_fwd_out_pass<T, MP, NB, PS>(p, gt, stream);
+  return e;
 }
 
 template <typename T, int MP, int NB>
@@ -666,9 +740,7 @@ hipError_t launch_fwd_variant(const ScanParams& p0, void* ws, hipStream_t stream
   hipError_t e = launch_cb_variant<T, NB>(p0, gt, stream);
   if (e != hipSuccess) return e;
   ScanParams p = p0;
-  p.seg_len = fwd_seg_len(p);
-  p.seg_state = p.seg_len > 0 ? reinterpret_cast<float*>(reinterpret_cast<char*>(ws) + align256(gtile_bytes<T>(p)))
-                              : nullptr;
+  place_split(p, fwd_split(p), reinterpret_cast<unsigned char*>(ws) + align256(gtile_bytes<T>(p)));
   if constexpr (MP >= 8) return launch_fwd_ps<T, MP, NB, 2>(p, gt, stream);
   else if constexpr (MP >= 4) {
     if (fwd_p_split(p) == 2) return launch_fwd_ps<T, MP, NB, 2>(p, gt, stream);
@@ -713,7 +785,7 @@ constexpr int kModeBlock = 8;  // modes per launch of the mode-block forward
 // [log-normalizers][float32 partial output].
 struct FwdBlockLayout {
   size_t seg, lse, ypart, total;
-  int seg_len;
+  FwdSplit split;
 };
 
 template <typename T>
@@ -721,9 +793,9 @@ FwdBlockLayout fwd_block_layout(const ScanParams& p) {
   ScanParams pb = p;
   pb.M = kModeBlock;
   FwdBlockLayout l{};
-  l.seg_len = fwd_seg_len(pb);
+  l.split = fwd_split(pb);
   l.seg = align256(gtile_bytes<T>(p));
-  l.lse = l.seg + (l.seg_len ? align256(sizeof(float) * (size_t)p.Bsz * p.H * p.Mall * p.N * p.P) : 0);
+  l.lse = l.seg + split_bytes(p, l.split);
   l.ypart = l.lse + align256(sizeof(float) * 2 * (size_t)p.Bsz * p.L * p.H);
   l.total = l.ypart + sizeof(float) * (size_t)p.Bsz * p.L * p.H * p.P;
   return l;
@@ -744,8 +816,11 @@ hipError_t launch_fwd_blocks(const ScanParams& p0, void* ws, hipStream_t stream)
   float* ypart = reinterpret_cast<float*>(base + l.ypart);
   if ((e = launch_mode_lse(p0, lse, stream)) != hipSuccess) return e;
   const int64_t NP = (int64_t)p0.N * p0.P;
-  for (int mo = 0; mo < p0.Mall; mo += kModeBlock) {
-    ScanParams p = p0;
+  ScanParams ps0 = p0;
+  place_split(ps0, l.split, base + l.seg);
+  // the state-only passes of every block, the boundary states, then the output passes
+  auto block = [&](int mo) {
+    ScanParams p = ps0;
     p.M = min(kModeBlock, p0.Mall - mo);
     p.tau = p0.tau + mo;
     if (p0.read_logit) p.read_logit = p0.read_logit + mo;
@@ -755,10 +830,17 @@ hipError_t launch_fwd_blocks(const ScanParams& p0, void* ws, hipStream_t stream)
     p.lse = lse;
     p.y_in = mo > 0 ? ypart : nullptr;
     p.y_part = mo + kModeBlock < p0.Mall ? ypart : nullptr;
-    p.seg_len = l.seg_len;
-    p.seg_state = l.seg_len ? reinterpret_cast<float*>(base + l.seg) + mo * NP : nullptr;
-    if ((e = launch_fwd_ps<T, kModeBlock, NB, 2, true>(p, gt, stream)) != hipSuccess) return e;
-  }
+    if (p.nseg > 1) {
+      p.seg_state = ps0.seg_state + mo * NP;
+      p.seg_decay = ps0.seg_decay + mo;
+    }
+    return p;
+  };
+  for (int mo = 0; mo < p0.Mall; mo += kModeBlock)
+    if ((e = launch_fwd_state_pass<T, kModeBlock, NB, 2, true>(block(mo), gt, stream)) != hipSuccess) return e;
+  if ((e = launch_seg_combine(ps0, stream)) != hipSuccess) return e;
+  for (int mo = 0; mo < p0.Mall; mo += kModeBlock)
+    if ((e = launch_fwd_out_pass<T, kModeBlock, NB, 2, true>(block(mo), gt, stream)) != hipSuccess) return e;
   return hipSuccess;
 }
 
@@ -832,8 +914,7 @@ size_t scan_fwd_workspace(const ScanParams& p) {
   if (p.Bsz == 0 || p.L == 0) return 0;
   if (p.Mall > kModeBlock) return p.io_bf16 ? fwd_block_layout<bf16>(p).total : fwd_block_layout<float>(p).total;
   const size_t tiles = p.io_bf16 ? gtile_bytes<bf16>(p) : gtile_bytes<float>(p);
-  if (fwd_seg_len(p) == 0) return tiles;
-  return align256(tiles) + sizeof(float) * (size_t)p.Bsz * p.H * p.M * p.N * p.P;  // + the boundary state
+  return align256(tiles) + split_bytes(p, fwd_split(p));  // + the boundary states and decays
 }
 
 hipError_t launch_scan_fwd(const ScanParams& p, void* ws, size_t, hipStream_t stream) {

@@ -31,10 +31,14 @@ struct ScanParams {
   const float* init_state;
   void* y;
   float* final_state;
-  // forward split into two sequence segments (0: one segment): tokens [0, seg_len)
-  // and [seg_len, L); seg_state holds the state at the boundary
-  int seg_len;
+  // forward split into nseg sequence segments of seg_len tokens (the last shorter;
+  // nseg 1: no split).  seg_state [nseg-1][B H Mall N P]: the state after each
+  // segment but the last (first each segment's own end state from a zero start,
+  // then the true boundary state); seg_decay [nseg-1][B H Mall]: each segment's
+  // total per-mode decay e^{-sum of the capped exponents}.
+  int seg_len, nseg;
   float* seg_state;
+  float* seg_decay;
   // Mode blocks (more modes than one launch holds): a launch covers M modes of Mall
   // (the per-mode pointers tau, logits and states already offset to its first mode;
   // logits and states keep the strides of Mall).  lse: per token the log-normalizers

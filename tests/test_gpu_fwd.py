@@ -97,6 +97,11 @@ SMALL = {
                                    final_state=True),
     "bf16 M32": Workload("t", 1, 130, 2, 64, 128, 32, final_state=True),
     "bf16 split M16": Workload("t", 1, 600, 2, 64, 128, 16, init_state=True, final_state=True),
+    # longer sequences: up to 16 segments, a state-only pass per segment, the boundary
+    # states chained, then every segment at once
+    "bf16 split8 M4 extras": Workload("t", 1, 2000, 2, 64, 128, 4, extras=True, init_state=True, final_state=True),
+    "f32 split6 M3 ragged": Workload("t", 1, 1500, 1, 32, 32, 3, io_dtype="f32", init_state=True, final_state=True),
+    "bf16 split4 M16": Workload("t", 1, 1100, 2, 64, 128, 16, extras=True, init_state=True, final_state=True),
 }
 
 
