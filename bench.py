@@ -49,8 +49,9 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workloads", default="train-b4-l4096-m8,layer-fwd-b8-l2048,prefill-b1-l16384,paper-nfree-b8-l2048,"
-                                           "paper-nfree-train-b8-l2048,decode-b256-128steps,paper-nfree-decode-b2048-128steps")
+    ap.add_argument("--workloads", default="train-b4-l4096-m8,layer-fwd-b8-l2048,prefill-b1-l16384,train-b4-l4096-m16,"
+                                           "paper-nfree-b8-l2048,paper-nfree-train-b8-l2048,decode-b256-128steps,"
+                                           "paper-nfree-decode-b2048-128steps")
     ap.add_argument("--main", default="train-b4-l4096-m8")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-extras", action="store_true",
@@ -61,6 +62,8 @@ def parse():
                     help="batch elements of the main workload the oracle runs (bounded CPU sample)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run one plain 1 GiB device copy (reference for the HBM byte counters)")
+    ap.add_argument("--no-measured-peaks", action="store_true",
+                    help="skip the device copy and bf16 GEMM that measure attainable bandwidth and matrix-core rate")
     return ap.parse_args()
 
 
@@ -231,7 +234,7 @@ def bench_scan(torch, frac, w, steps, warmup, extras=True):
     def bwd():
         frac.scan_bwd(x, dt, Bm, Cm, alpha, tau, dy, workspace=ws_b)
 
-    def bwd_all():  # the form without B/C: also the gradients of alpha, lambda, the logits, the initial state
+    def bwd_all():  # also the gradients of alpha, lambda, the logits and the initial state
         frac.scan_bwd(x, dt, Bm, Cm, alpha, tau, dy, workspace=ws_b, all_grads=True)
 
     for _ in range(warmup):
@@ -281,6 +284,14 @@ def bench_scan(torch, frac, w, steps, warmup, extras=True):
         res["fwd_bwd_roofline"] = roofline("hbm", nfree_fwd_bytes(w) + nfree_bwd_bytes(w), fms + bms,
                                            PEAK_HBM_BYTES, "GB/s")
     elif w.backward:
+        if extras:
+            for _ in range(warmup):
+                bwd_all()
+            ta = Timer(torch)
+            for _ in range(steps):
+                with ta:
+                    bwd_all()
+            res["bwd_all_grads_ms"] = float(np.mean(ta.ms()))
         res["bwd_ms"] = bms
         res["bwd_roofline"] = dict(roofline("mfma", th * bwd_flops_per_token_head(w), bms, peak, "TFLOP/s"),
                                    traffic=measured_traffic("frac_scan_bwd", w.name))
@@ -360,6 +371,19 @@ def roofline(bound, work, ms, peak, unit):
             "work_per_launch": work, "ms_per_launch": ms, "traffic": None}
 
 
+def _oracle_slice(a, w, nb, H):
+    """The first nb batch elements and H heads of generated inputs, float64 (alpha broadcast)."""
+    sl = lambda k: np.asarray(a[k])[0:nb].astype(np.float64)
+    x, dt = sl("x")[:, :, :H], sl("dt")[:, :, :H]
+    if "Bm" in a:
+        Bm, Cm = sl("Bm"), sl("Cm")
+    else:  # the form without B/C: B = C = 1
+        Bm = Cm = np.ones((nb, w.seqlen, 1, 1))
+    al = np.asarray(a["alpha"], np.float64)
+    alpha = np.broadcast_to(al[:H] if al.ndim == 1 else al, dt.shape)
+    return x, dt, Bm, Cm, alpha
+
+
 def cpu_baseline(w, heads, batch):
     """The float64 oracle on a bounded slice: the first `batch` batch elements, `heads` heads, full length."""
     import oracle
@@ -368,20 +392,90 @@ def cpu_baseline(w, heads, batch):
     H = min(heads, w.nheads)
     nb = max(1, min(batch, w.batch))
     tau = oracle.default_tau(w.nmodes)
-    sl = lambda k: np.asarray(a[k])[0:nb].astype(np.float64)
-    x, dt = sl("x")[:, :, :H], sl("dt")[:, :, :H]
-    Bm, Cm = sl("Bm"), sl("Cm")
-    alpha = np.broadcast_to(np.asarray(a["alpha"], np.float64), dt.shape)
+    x, dt, Bm, Cm, alpha = _oracle_slice(a, w, nb, H)
     t0 = time.perf_counter()
     oracle.forward(x, dt, Bm, Cm, alpha, tau)
     if w.backward:
-        oracle.backward(x, dt, Bm, Cm, alpha, tau, sl("dy")[:, :, :H])
+        oracle.backward(x, dt, Bm, Cm, alpha, tau, np.asarray(a["dy"])[0:nb, :, :H].astype(np.float64))
     sec = time.perf_counter() - t0
     tokens = nb * w.seqlen * H / w.nheads  # token-equivalents of the full head count
     return {"value": tokens / sec, "unit": "tokens/s", "cores": oracle.num_threads(), "kind": "oracle",
             "sample": "%d of %d batch elements, %d of %d heads, %d tokens, %s" % (
                 nb, w.batch, H, w.nheads, w.seqlen, "forward + backward" if w.backward else "forward"),
             "seconds": sec}
+
+
+def cpu_baseline_decode(w, batch, steps):
+    """The float64 oracle's decode step on the first `batch` sequences (all heads) for `steps` steps."""
+    import oracle
+    from paper_2609_36314_amd.workloads import generate
+    a = generate(w, 0)
+    nb = max(1, min(batch, w.batch))
+    tau = oracle.default_tau(w.nmodes)
+    state = np.asarray(a["init_state"])[0:nb].astype(np.float64)
+    al = np.asarray(a["alpha"], np.float64)
+    t0 = time.perf_counter()
+    for s in range(steps):
+        g = lambda k: np.asarray(a[k])[s, 0:nb].astype(np.float64) if k in a else None
+        x, dt = g("x"), g("dt")
+        alpha = np.broadcast_to(al if al.ndim == 0 else al[None, :], dt.shape)
+        Bm = g("Bm") if w.bc else np.ones((nb, 1, 1))
+        Cm = g("Cm") if w.bc else np.ones((nb, 1, 1))
+        _, state = oracle.decode_step(state, x, dt, Bm, Cm, alpha, tau)
+    sec = time.perf_counter() - t0
+    return {"value": nb * steps / sec, "unit": "tokens/s", "cores": oracle.num_threads(), "kind": "oracle",
+            "sample": "%d of %d sequences, all %d heads, %d steps" % (nb, w.batch, w.nheads, steps),
+            "seconds": sec}
+
+
+# bounded oracle samples beside each workload (batch elements, heads) or (sequences, steps)
+CPU_SAMPLES = {
+    "layer-fwd-b8-l2048": (1, 64),
+    "prefill-b1-l16384": (1, 16),
+    "train-b4-l4096-m16": (1, 4),
+    "paper-nfree-b8-l2048": (8, 16),
+    "paper-nfree-train-b8-l2048": (2, 16),
+    "decode-b256-128steps": (8, 128),
+    "paper-nfree-decode-b2048-128steps": (256, 128),
+}
+
+
+def measured_peaks(torch):
+    """Attainable rates on this GPU: a 1 GiB device-to-device copy (bytes read + written per
+    second) and a 8192^3 bfloat16 GEMM on the platform BLAS (flops per second)."""
+    src = torch.empty(1 << 29, dtype=torch.bfloat16, device="cuda").fill_(1.0)
+    dst = torch.empty_like(src)
+    a = torch.randn(8192, 8192, device="cuda").to(torch.bfloat16)
+    b = torch.randn(8192, 8192, device="cuda").to(torch.bfloat16)
+    c = torch.empty(8192, 8192, dtype=torch.bfloat16, device="cuda")
+    for _ in range(3):
+        dst.copy_(src)
+        torch.matmul(a, b, out=c)
+    torch.cuda.synchronize()
+    tc, tg = Timer(torch), Timer(torch)
+    for _ in range(10):
+        with tc:
+            dst.copy_(src)
+    for _ in range(10):
+        with tg:
+            torch.matmul(a, b, out=c)
+    torch.cuda.synchronize()
+    copy = 2.0 * src.numel() * 2 / (float(np.median(tc.ms())) * 1e-3)
+    gemm = 2.0 * 8192 ** 3 / (float(np.median(tg.ms())) * 1e-3)
+    del src, dst, a, b, c
+    torch.cuda.empty_cache()
+    return {"copy_GBps": copy / 1e9, "gemm_bf16_TFLOPs": gemm / 1e12}
+
+
+def with_measured(rf, mp):
+    """A roofline dict with its fraction of the measured attainable rate beside the published one."""
+    if not rf or not mp:
+        return rf
+    ref = mp["copy_GBps"] if rf.get("bound") == "hbm" else (mp["gemm_bf16_TFLOPs"] if rf.get("peak") == 2500.0
+                                                             else None)
+    if ref:
+        rf = dict(rf, measured_peak=ref, frac_of_measured=rf["achieved"] / ref)
+    return rf
 
 
 def main():
@@ -401,6 +495,7 @@ def main():
         dst.copy_(src)
         torch.cuda.synchronize()
         del src, dst
+    mp = None if args.no_measured_peaks else measured_peaks(torch)
     names = [n for n in args.workloads.split(",") if n]
     results = {}
     for n in names:
@@ -409,6 +504,9 @@ def main():
             results[n] = bench_decode(torch, frac, w, max(1, args.steps // 4), max(1, args.warmup // 2))
         else:
             results[n] = bench_scan(torch, frac, w, args.steps, args.warmup, extras=not args.no_extras)
+        for k in list(results[n]):
+            if k.endswith("roofline"):
+                results[n][k] = with_measured(results[n][k], mp)
         print("# %s: %s" % (n, json.dumps(results[n])), file=sys.stderr, flush=True)
         torch.cuda.empty_cache()
 
@@ -445,9 +543,21 @@ def main():
         else:
             line["roofline"] = dict(mres["fwd_roofline"], kernel="frac_scan_fwd",
                                     traffic=measured_traffic("frac_scan_fwd", main_w.name))
+    if "roofline" in line:
+        line["roofline"] = with_measured(line["roofline"], mp)
+    if mp:
+        line["measured_peaks"] = mp
     line["workloads"] = results
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(main_w, args.cpu_sample_heads, args.cpu_sample_batch)
+        for n in names:
+            if n == args.main or n not in CPU_SAMPLES:
+                continue
+            w = WORKLOADS[n]
+            a, b = CPU_SAMPLES[n]
+            results[n]["cpu_baseline"] = (cpu_baseline_decode(w, a, min(b, w.decode_steps)) if w.decode_steps
+                                          else cpu_baseline(w, b, a))
+            print("# cpu %s: %s" % (n, json.dumps(results[n]["cpu_baseline"])), file=sys.stderr, flush=True)
     print(json.dumps(line))
 
 

@@ -362,7 +362,8 @@ __global__ void __launch_bounds__(256, 2) frac_nfree_bwd_kernel(ScanParams p, Nf
   __shared__ __align__(16) T Xs[64 * XS];                      // x [t][p]
   __shared__ __align__(16) T Ys[64 * XS];                      // dy [t][p]
   __shared__ __align__(16) T GT[64 * XS];                      // Gamma^T [t][t'], t' >= t
-  __shared__ __align__(16) T HT[64 * XS];                      // dY X^T [t][k], k <= t
+  constexpr int HS = 64 + 4;
+  __shared__ __align__(16) float HT[64 * HS];                  // dY X^T [t][k], k <= t (float32)
   T* const DX = Xs;  // dx rows [t][p] (bfloat16 staging; x is no longer read by then)
   __shared__ __align__(16) float Gt[MP * WQ];                  // the adjoint [m][p]
   __shared__ __align__(16) float W[NWA * MP * WQ];
@@ -377,7 +378,8 @@ __global__ void __launch_bounds__(256, 2) frac_nfree_bwd_kernel(ScanParams p, Nf
   float* P_lh = W + 4 * SW;   // chunk log-decays, hi and lo parts
   float* P_ll = W + 5 * SW;
 
-  for (int i = tid; i < 64 * XS; i += 256) GT[i] = HT[i] = (T)0.0f;
+  for (int i = tid; i < 64 * XS; i += 256) GT[i] = (T)0.0f;
+  for (int i = tid; i < 64 * HS; i += 256) HT[i] = 0.0f;
   if (tid < MP) {
     const float tau = (tid < M) ? p.tau[tid] : 1.0f;
     s_rr[tid] = (tid < M) ? 1.0f / tau : 0.0f;
@@ -560,11 +562,14 @@ __global__ void __launch_bounds__(256, 2) frac_nfree_bwd_kernel(ScanParams p, Nf
       for (int r = 0; r < 4; ++r) {
         const int t = tb * 16 + lg * 4 + r, k = kb * 16 + li;
         GT[k * XS + t] = (T)keep_if_ge(Gm[r], t, k);
-        HT[t * XS + k] = (T)keep_if_ge(D[r], t, k);
+        HT[t * HS + k] = keep_if_ge(D[r], t, k);
       }
     }
 
-    // ---- per token (row block tb = wave): S0 . dy and G . x, modes as output columns
+    // ---- per token (row block tb = wave): S0 . dy and G . x, modes as output columns; with
+    // bfloat16 operands the float32 state and adjoint enter as a rounded value plus its
+    // rounded remainder (two products), so that these weight gradients keep float32
+    // accuracy: the step-size and order gradients are differences of their sums
     floatx4 Uk[MB], Zk[MB];
     {
       const int tb = wave;
@@ -576,20 +581,30 @@ __global__ void __launch_bounds__(256, 2) frac_nfree_bwd_kernel(ScanParams p, Nf
         U = Z = floatx4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int kp = 0; kp < 2; ++kp) {
-          Frag<T> S0f, Gf;
           const float4 a0 = s0r[mb][kp][0], a1 = s0r[mb][kp][1];
-          frag_set(S0f, 0, a0.x);
-          frag_set(S0f, 1, a0.y);
-          frag_set(S0f, 2, a0.z);
-          frag_set(S0f, 3, a0.w);
-          frag_set(S0f, 4, a1.x);
-          frag_set(S0f, 5, a1.y);
-          frag_set(S0f, 6, a1.z);
-          frag_set(S0f, 7, a1.w);
+          const float sv[8] = {a0.x, a0.y, a0.z, a0.w, a1.x, a1.y, a1.z, a1.w};
+          float gv[8];
 #pragma unroll
-          for (int s = 0; s < 8; ++s) frag_set(Gf, s, (m < MP) ? Gt[m * WQ + kp * 32 + lg * 8 + s] : 0.0f);
-          mma(U, frag_load8(Ys + (tb * 16 + li) * XS + kp * 32 + lg * 8), S0f);
-          mma(Z, frag_load8(Xs + (tb * 16 + li) * XS + kp * 32 + lg * 8), Gf);
+          for (int s = 0; s < 8; ++s) gv[s] = (m < MP) ? Gt[m * WQ + kp * 32 + lg * 8 + s] : 0.0f;
+          Frag<T> S0f, Gf;
+#pragma unroll
+          for (int s = 0; s < 8; ++s) {
+            frag_set(S0f, s, sv[s]);
+            frag_set(Gf, s, gv[s]);
+          }
+          const Frag<T> yf = frag_load8(Ys + (tb * 16 + li) * XS + kp * 32 + lg * 8);
+          const Frag<T> xf = frag_load8(Xs + (tb * 16 + li) * XS + kp * 32 + lg * 8);
+          mma(U, yf, S0f);
+          mma(Z, xf, Gf);
+          if constexpr (kBf16) {  // the remainders
+#pragma unroll
+            for (int s = 0; s < 8; ++s) {
+              frag_set(S0f, s, sv[s] - to_f32((T)sv[s]));
+              frag_set(Gf, s, gv[s] - to_f32((T)gv[s]));
+            }
+            mma(U, yf, S0f);
+            mma(Z, xf, Gf);
+          }
         }
       }
     }
@@ -622,13 +637,13 @@ __global__ void __launch_bounds__(256, 2) frac_nfree_bwd_kernel(ScanParams p, Nf
         floatx4 cI = {0.f, 0.f, 0.f, 0.f}, kI = {0.f, 0.f, 0.f, 0.f};
         for (int kq = 0; kq < (tb + 1) * 4; ++kq) {
           const int k = kq * 4 + lg;
-          const float a = to_f32(HT[(tb * 16 + li) * XS + k]);
+          const float a = HT[(tb * 16 + li) * HS + k];
           const float bb = fac ? P_Vt[mm * WQ + k] : 0.0f;
           cI = __builtin_amdgcn_mfma_f32_16x16x4f32(a, bb, cI, 0, 0, 0);
         }
         for (int tq = tb * 4; tq < 16; ++tq) {
           const int t = tq * 4 + lg;
-          const float a = to_f32(HT[t * XS + tb * 16 + li]);
+          const float a = HT[t * HS + tb * 16 + li];
           const float bb = fac ? P_O[mm * WQ + t] : 0.0f;
           kI = __builtin_amdgcn_mfma_f32_16x16x4f32(a, bb, kI, 0, 0, 0);
         }
@@ -646,8 +661,8 @@ __global__ void __launch_bounds__(256, 2) frac_nfree_bwd_kernel(ScanParams p, Nf
             dc += ea * cI[r];
             dki = fexp(lhm[t]) * kI[r];
           } else {
-            for (int k = 0; k <= t; ++k) dc += to_f32(HT[t * XS + k]) * P_Vt[mm * WQ + k] * ell_decay(lhm, llm, t, k);
-            for (int t2 = t; t2 < 64; ++t2) dki += to_f32(HT[t2 * XS + t]) * P_c[mm * WQ + t2] * ell_decay(lhm, llm, t2, t);
+            for (int k = 0; k <= t; ++k) dc += HT[t * HS + k] * P_Vt[mm * WQ + k] * ell_decay(lhm, llm, t, k);
+            for (int t2 = t; t2 < 64; ++t2) dki += HT[t2 * HS + t] * P_c[mm * WQ + t2] * ell_decay(lhm, llm, t2, t);
           }
           if (m < M && t < nv) {
             const int64_t i = ((int64_t)ps * p.Bsz * H * L + (int64_t)bh * L + t0 + t) * M + m;  // [nps][B H L][M]

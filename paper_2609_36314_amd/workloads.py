@@ -53,6 +53,8 @@ TINY_F32 = Workload("tiny-f32", 1, 256, 2, 16, 16, 4, io_dtype="f32")
 LAYER_FWD = Workload("layer-fwd-b8-l2048", 8, 2048, 64, 64, 128, 4)
 LONG_PREFILL = Workload("prefill-b1-l16384", 1, 16384, 64, 64, 128, 4, alpha_range=(0.3, 0.8), final_state=True)
 TRAIN = Workload("train-b4-l4096-m8", 4, 4096, 64, 64, 128, 8, backward=True)
+# the same step with the paper's bank of 16 modes (two blocks of eight)
+TRAIN_M16 = Workload("train-b4-l4096-m16", 4, 4096, 64, 64, 128, 16, backward=True)
 DECODE = Workload("decode-b256-128steps", 256, 1, 64, 64, 128, 4, decode_steps=128, init_state=True)
 # the paper's layer (state H x M x d_h, no B/C), forward at batch 8 x 2048 tokens
 PAPER_NFREE = Workload("paper-nfree-b8-l2048", 8, 2048, 16, 256, 1, 16, bc=False)
@@ -61,8 +63,8 @@ PAPER_NFREE_TRAIN = Workload("paper-nfree-train-b8-l2048", 8, 2048, 16, 256, 1, 
 PAPER_NFREE_DECODE = Workload("paper-nfree-decode-b2048-128steps", 2048, 1, 16, 256, 1, 16, bc=False,
                               decode_steps=128, init_state=True)
 
-WORKLOADS = {w.name: w for w in (TINY_F32, LAYER_FWD, LONG_PREFILL, TRAIN, DECODE, PAPER_NFREE, PAPER_NFREE_TRAIN,
-                                  PAPER_NFREE_DECODE)}
+WORKLOADS = {w.name: w for w in (TINY_F32, LAYER_FWD, LONG_PREFILL, TRAIN, TRAIN_M16, DECODE, PAPER_NFREE,
+                                  PAPER_NFREE_TRAIN, PAPER_NFREE_DECODE)}
 
 
 def _softplus(v: np.ndarray) -> np.ndarray:

@@ -189,6 +189,29 @@ def test_bwd_full_size_sampled_bank_of_16():
         assert_close("ddt[%d,:,%d]" % (b, h), f64(g["ddt"][b:b + 1, :, h:h + 1]), ref["ddt"], TOL["bf16"])
 
 
+def test_bwd_full_size_all_grads_sampled():
+    """The training workload at full size with lambda, both logits, D, an initial
+    state and a final-state gradient drawn over the paper's ranges, all gradients
+    (the all-gradients launch the benchmark times): every per-head gradient of the
+    first and the last (batch, head) recomputed by the oracle."""
+    w = TRAIN.scaled(extras=True, init_state=True, final_state=True)
+    inp = device_inputs(w, seed=7)
+    tau_d, tau64 = _tau(w.nmodes)
+    dfs = inp["d_final_state"]
+    print("full-size", w.name, "all gradients", flush=True)
+    kw = {k: inp[k] for k in ("lam", "read_logit", "write_logit", "D", "init_state")}
+    g = frac.scan_bwd(inp["x"], inp["dt"], inp["Bm"], inp["Cm"], inp["alpha"], tau_d, inp["dy"], d_final_state=dfs,
+                      all_grads=True, **kw)
+    torch.cuda.synchronize()
+    tol = TOL["bf16"]
+    for (b, h) in [(0, 0), (3, 63)]:
+        ref = _oracle_bwd(inp, tau64, dfs, b=b, h=h)
+        print("slice", b, h, flush=True)
+        for k in ("dx", "ddt", "dalpha", "dlambda", "dread_logit", "dwrite_logit"):
+            assert_close("%s[%d,:,%d]" % (k, b, h), f64(g[k][b:b + 1, :, h:h + 1]), ref[k], tol)
+        assert_close("dinit_state[%d,%d]" % (b, h), f64(g["dinit_state"][b:b + 1, h:h + 1]), ref["dinit_state"], tol)
+
+
 def test_bwd_full_size_sampled():
     """The training workload at full size (batch 4, L 4096, 64 heads, M 8), as the
     benchmark launches it.  dx and ddt are checked on sampled heads (they depend

@@ -79,3 +79,92 @@ def test_layer_forward_and_backward_match_the_oracle_chain(shape):
     assert_close("dh", f64(h.grad), ref_dh, tol)
     for name, prm in layer.named_parameters():
         assert_close("d" + name, f64(prm.grad), ref_g[name], tol)
+
+
+def test_bf16_layer_stages_match_the_oracles_on_their_own_inputs():
+    """The bfloat16 layer (the paper's shape scaled down: 2 heads of 64, 16 modes),
+    forward and backward through autograd, with every call into the library
+    recorded: each stage -- convolution, parameter construction, scan, gated
+    normalization, forward and backward -- is recomputed by its float64 oracle from
+    the inputs the GPU stage actually received (the bfloat16-rounded activations of
+    the stages before it), so that each kernel's own error is measured apart from
+    the rounding that the chain compounds.  The end-to-end errors against the
+    float64 chain are printed beside them."""
+    import paper_2609_36314_amd.layer as lay
+    calls = {}
+
+    def rec(name, fn):
+        def wrapped(*a, **kw):
+            out = fn(*a, **kw)
+            calls[name] = (a, kw, out)
+            return out
+        return wrapped
+
+    saved = {n: getattr(lay, n) for n in ("conv_fwd", "conv_bwd", "params_fwd", "params_bwd", "scan_fwd", "scan_bwd",
+                                          "gnorm_fwd", "gnorm_bwd")}
+    B, L, d_model, H, P, M = 2, 150, 64, 2, 64, 16
+    layer = FracLayer(d_model, H, P, M, dtype=torch.bfloat16, seed=7)
+    with torch.no_grad():
+        layer.p_read.fill_(0.4)
+        layer.p_write.fill_(-0.3)
+        layer.conv_b.normal_(0, 0.1)
+        layer.D.normal_(1.0, 0.3)
+    gen = torch.Generator().manual_seed(8)
+    h = torch.randn(B, L, d_model, generator=gen).to(torch.bfloat16).cuda().requires_grad_(True)
+    dout = torch.randn(B, L, d_model, generator=gen).to(torch.bfloat16).cuda()
+    try:
+        for n, fn in saved.items():
+            setattr(lay, n, rec(n, fn))
+        out = layer(h)
+        out.backward(dout)
+        torch.cuda.synchronize()
+    finally:
+        for n, fn in saved.items():
+            setattr(lay, n, fn)
+    tol = 2e-2
+    g = lambda t: None if t is None else f64(t)
+    # convolution
+    (x, w), kw, u = calls["conv_fwd"][0], calls["conv_fwd"][1], calls["conv_fwd"][2]
+    assert_close("conv y", f64(u), oc.conv_forward(g(x), g(w), g(kw["bias"])), tol)
+    (x, w, dy), kw, cb = calls["conv_bwd"]
+    ref = oc.conv_backward(g(x), g(w), g(dy), g(kw["bias"]))
+    for k in ("dx", "dw", "dbias"):
+        assert_close("conv " + k, f64(cb[k]), ref[k], tol)
+    # parameter construction (float32 in and out)
+    (z_dt, z_a), kw, po = calls["params_fwd"]
+    args = (g(z_dt), g(kw["dt_bias"]), g(z_a), g(kw["z_lambda"]), g(kw["v_read"]), g(kw["v_write"]),
+            float(kw["p_read"][0]), float(kw["p_write"][0]))
+    ref = op.params_forward(*args)
+    for k, rk in (("dt", "dt"), ("alpha", "alpha"), ("lam", "lambda"), ("read_logit", "read_logit"),
+                  ("write_logit", "write_logit")):
+        assert_close("params " + k, f64(po[k]), ref[rk], 1e-4)
+    _, kw, pg = calls["params_bwd"]
+    ref = op.params_backward(*args, ddt=g(kw["ddt"]), dalpha=g(kw["dalpha"]), dlambda=g(kw["dlambda"]),
+                             dread_logit=g(kw["dread_logit"]), dwrite_logit=g(kw["dwrite_logit"]))
+    for k, rk in (("dz_dt", "dz_dt"), ("dz_alpha", "dz_alpha"), ("dz_lambda", "dz_lambda"), ("dv_read", "dv_read"),
+                  ("dv_write", "dv_write"), ("ddt_bias", "ddt_bias")):
+        assert_close("params " + k, f64(pg[k]), ref[rk], 1e-4)
+    # scan without B/C, all gradients
+    (x, dt, _, _, alpha, tau), kw, y = calls["scan_fwd"]
+    ones = np.ones((B, L, 1, 1))
+    okw = dict(lam=g(kw["lam"]), read_logit=g(kw["read_logit"]), write_logit=g(kw["write_logit"]), D=g(kw["D"]))
+    ry, _ = oracle.forward(g(x), g(dt), ones, ones, g(alpha), g(tau), **okw)
+    assert_close("scan y", f64(y), ry, tol)
+    (x, dt, _, _, alpha, tau, dy), kw, sg = calls["scan_bwd"]
+    ref = oracle.backward(g(x), g(dt), ones, ones, g(alpha), g(tau), g(dy), **okw)
+    for k in ("dx", "ddt", "dalpha", "dlambda", "dread_logit", "dwrite_logit", "dD"):
+        assert_close("scan " + k, f64(sg[k]), ref[k], tol)
+    # gated normalization
+    (x, z, w), kw, o = calls["gnorm_fwd"]
+    assert_close("gnorm y", f64(o), og.gnorm_forward(g(x), g(z), g(w), kw["group"]), tol)
+    (x, z, w, dy), kw, gg = calls["gnorm_bwd"]
+    ref = og.gnorm_backward(g(x), g(z), g(w), g(dy), kw["group"])
+    for k, rk in (("dx", "dx"), ("dz", "dz"), ("dweight", "dweight")):
+        assert_close("gnorm " + k, f64(gg[k]), ref[rk], tol)
+    # the compounded error of the whole bfloat16 chain, for the record
+    from harness import rel_l2
+    ref_out, ref_dh, ref_g = _reference(layer, h.detach(), dout)
+    print("end-to-end bf16 vs float64 chain: out %.2e, dh %.2e" % (rel_l2(f64(out.detach()), ref_out),
+                                                                   rel_l2(f64(h.grad), ref_dh)), flush=True)
+    for name, prm in layer.named_parameters():
+        print("  d%-10s rel-L2 %.2e" % (name, rel_l2(f64(prm.grad), ref_g[name])), flush=True)

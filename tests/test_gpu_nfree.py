@@ -9,7 +9,7 @@ import torch
 
 import oracle
 import paper_2609_36314_amd as frac
-from paper_2609_36314_amd.workloads import PAPER_NFREE, Workload
+from paper_2609_36314_amd.workloads import PAPER_NFREE, PAPER_NFREE_TRAIN, Workload
 from harness import TOL, assert_close, device_inputs, f64
 
 pytestmark = pytest.mark.gpu
@@ -232,3 +232,38 @@ def test_nfree_bwd_shared_logits_all_grads():
     tol = TOL["bf16"]
     for k in ("dx", "ddt", "dalpha", "dlambda", "dread_logit", "dwrite_logit"):
         assert_close(k, f64(g[k]), ref[k], tol)
+
+
+def test_nfree_bwd_full_size_all_grads_sampled():
+    """The paper-shape training workload at full size (batch 8, L 2048, 16 heads of
+    256, 16 modes), with lambda, both logits, D, an initial state and a final-state
+    gradient drawn over the paper's ranges, all gradients: every gradient of sampled
+    (batch, head) slices, the first and the last, recomputed by the oracle; dD of the
+    sampled heads over all batch elements."""
+    w = PAPER_NFREE_TRAIN.scaled(extras=True, init_state=True, final_state=True)
+    inp = device_inputs(w, seed=20)
+    tau_d, tau64 = _tau(w.nmodes)
+    dfs = inp["d_final_state"]
+    print("full-size", w.name, "all gradients", flush=True)
+    kw = {k: inp[k] for k in ("lam", "read_logit", "write_logit", "D", "init_state")}
+    g = frac.scan_bwd(inp["x"], inp["dt"], None, None, inp["alpha"], tau_d, inp["dy"], d_final_state=dfs,
+                      all_grads=True, **kw)
+    torch.cuda.synchronize()
+    tol = TOL["bf16"]
+    for (b, h) in [(0, 0), (3, 9), (7, 15)]:
+        sl = {k: inp[k][b:b + 1, :, h:h + 1] for k in ("x", "dt", "dy", "alpha", "lam", "read_logit", "write_logit")}
+        sl["D"] = inp["D"][h:h + 1]
+        sl["init_state"] = inp["init_state"][b:b + 1, h:h + 1]
+        ref = _oracle_bwd(sl, tau64, dfs[b:b + 1, h:h + 1])
+        sg = {k: g[k][b:b + 1, :, h:h + 1] for k in ("dx", "ddt", "dalpha", "dlambda", "dread_logit", "dwrite_logit")}
+        sg["dinit_state"] = g["dinit_state"][b:b + 1, h:h + 1]
+        print("slice", b, h, flush=True)
+        assert_close("dx", f64(sg["dx"]), ref["dx"], tol)
+        assert_close("ddt", f64(sg["ddt"]), ref["ddt"], tol)
+        _check_further_grads(sg, ref, tol, True)
+    for h in (0, 15):
+        sl = {k: inp[k][:, :, h:h + 1] for k in ("x", "dt", "dy", "alpha", "lam", "read_logit", "write_logit")}
+        sl["D"] = inp["D"][h:h + 1]
+        sl["init_state"] = inp["init_state"][:, h:h + 1]
+        ref = _oracle_bwd(sl, tau64, dfs[:, h:h + 1])
+        assert_close("dD[%d]" % h, f64(g["dD"][h:h + 1]), ref["dD"], tol)
