@@ -144,27 +144,56 @@ __device__ __forceinline__ float wave_sum(float v) {
   return group_allreduce<64>(v, [](float x, float y) { return x + y; });
 }
 
-// Sum over lanes j .. 63 (inclusive suffix) and over lanes 0 .. j - 1 (exclusive prefix).
-__device__ __forceinline__ float suffix_sum(float v) {
-  const int lane = threadIdx.x & 63;
-#pragma unroll
-  for (int d = 1; d < 64; d <<= 1) {
-    const float u = __shfl_down(v, d, 64);
-    if (lane + d < 64) v += u;
-  }
+template <int CTRL, int ROW_MASK, bool BOUND>
+__device__ __forceinline__ float dpp_rows(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, ROW_MASK, 0xF, BOUND));
+}
+
+// Inclusive sum over lanes 0 .. j (row shifts, then the row broadcasts).
+__device__ __forceinline__ float wave_prefix_sum(float v) {
+  v += dpp_rows<0x111, 0xF, true>(v);   // row_shr:1
+  v += dpp_rows<0x112, 0xF, true>(v);   // row_shr:2
+  v += dpp_rows<0x114, 0xF, true>(v);   // row_shr:4
+  v += dpp_rows<0x118, 0xF, true>(v);   // row_shr:8
+  v += dpp_rows<0x142, 0xA, false>(v);  // row_bcast:15
+  v += dpp_rows<0x143, 0xC, false>(v);  // row_bcast:31
   return v;
 }
 
-__device__ __forceinline__ float prefix_sum_excl(float v) {
+// The sums over lanes 0 .. j - 1 (excl) and j .. 63 (suffix) of v.
+__device__ __forceinline__ void excl_and_suffix(float v, float& excl, float& suffix) {
+  const float inc = wave_prefix_sum(v);
+  excl = inc - v;
+  suffix = __shfl(inc, 63, 64) - excl;
+}
+
+// Composition of the maps z -> v_j + a_j z of lanes j .. 63 (a in {0, 1}), as (A, V, W)
+// for two value streams V, W under the same masks.
+__device__ __forceinline__ void suffix_affine(float& A, float& V, float& W) {
   const int lane = threadIdx.x & 63;
-  float s = v;
 #pragma unroll
   for (int d = 1; d < 64; d <<= 1) {
-    const float u = __shfl_up(s, d, 64);
-    if (lane >= d) s += u;
+    const float Ad = __shfl_down(A, d, 64), Vd = __shfl_down(V, d, 64), Wd = __shfl_down(W, d, 64);
+    if (lane + d < 64) {
+      V = V + A * Vd;
+      W = W + A * Wd;
+      A = A * Ad;
+    }
   }
-  const float e = __shfl_up(s, 1, 64);
-  return lane == 0 ? 0.0f : e;
+}
+
+// Composition of the maps z -> v_j + a_j z of lanes 0 .. j applied in lane order.
+__device__ __forceinline__ void prefix_affine(float& A, float& V, float& W) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int d = 1; d < 64; d <<= 1) {
+    const float Ad = __shfl_up(A, d, 64), Vd = __shfl_up(V, d, 64), Wd = __shfl_up(W, d, 64);
+    if (lane >= d) {
+      V = A * Vd + V;
+      W = A * Wd + W;
+      A = A * Ad;
+    }
+  }
 }
 
 // Per (tile, mode): the value the suffix form carries across the tile (vs) and the
@@ -174,68 +203,72 @@ struct TileSeg {
   float vs, ns, vp, np;
 };
 
-// Sum of the later tiles' suffix values, up to and including the first cut tile, else
-// up to the final-state term Fm (a virtual cut tile after the last).  Wave-uniform.
-__device__ __forceinline__ void suffix_carry(const TileSeg* seg, const int* tileF, int64_t row, int tile, int ntiles,
-                                             int M, int m, float Fm, float& cv, float& cn) {
-  const int lane = threadIdx.x & 63;
-  cv = cn = 0.0f;
-  for (int g0 = tile + 1; g0 <= ntiles; g0 += 64) {
-    const int tj = g0 + lane;
-    float v = 0.0f, n = 0.0f;
-    bool stop_here = false;
-    if (tj < ntiles) {
-      const TileSeg sg = seg[(row + tj) * M + m];
-      v = sg.vs;
-      n = sg.ns;
-      stop_here = tileF[(row + tj) * M + m] != 0;
-    } else if (tj == ntiles) {
-      v = Fm;
-      stop_here = true;
+// The carries into every tile of one (batch, head, mode) row, one wave per row:
+//   suffix  C_s(j) = vs_{j+1} + (tile j+1 cut ? 0 : C_s(j+1)),  C_s(last) = <dS_final, S_final>
+//   prefix  C_p(j) = vp_{j-1} + (tile j-1 cut ? 0 : C_p(j-1)),  C_p(0) = <S_init, dS_init>
+// with the magnitude sums alongside (the anchors count 0), in blocks of 64 tiles.
+__global__ void __launch_bounds__(256) frac_grad_carry_kernel(ScanParams p, GradInputs gi) {
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int64_t rowid = (int64_t)blockIdx.x * 4 + wave;  // (b H + h) M + m
+  const int M = p.M, ntiles = (p.L + 63) / 64;
+  if (rowid >= (int64_t)p.Bsz * p.H * M) return;
+  const int m = (int)(rowid % M);
+  const int64_t bh = rowid / M, row = bh * ntiles;
+  const int64_t SF = (int64_t)p.Bsz * p.H * M;
+  float Fm = 0.0f, Im = 0.0f;
+  for (int q = 0; q < gi.nF; ++q) Fm += gi.F[q * SF + rowid];
+  for (int q = 0; q < gi.nI; ++q) Im += gi.I[q * SF + rowid];
+  const TileSeg* seg = reinterpret_cast<const TileSeg*>(gi.tileV);
+  float4* carry = reinterpret_cast<float4*>(gi.carry);
+  const int nblk = (ntiles + 63) / 64;
+  // suffix, from the last block
+  float zv = 0.0f, zn = 0.0f;  // C_s, N_s of the first tile after the block
+  for (int kb = nblk - 1; kb >= 0; --kb) {
+    const int j = kb * 64 + lane;
+    float A = 1.0f, V = 0.0f, W = 0.0f;
+    if (j == ntiles - 1) {
+      A = 0.0f;
+      V = Fm;
+    } else if (j < ntiles - 1) {
+      const TileSeg sg = seg[(row + j + 1) * M + m];
+      A = gi.tileF[(row + j + 1) * M + m] ? 0.0f : 1.0f;
+      V = sg.vs;
+      W = sg.ns;
     }
-    const uint64_t sb = __ballot(stop_here);
-    const int stop = sb ? __builtin_ctzll(sb) : 64;  // the last lane taken
-    const bool take = lane <= stop && tj <= ntiles;
-    cv += wave_sum(take ? v : 0.0f);
-    cn += wave_sum(take ? n : 0.0f);
-    if (stop < 64) break;
-  }
-}
-
-// The same for the prefix form: the earlier tiles, nearest first, up to and including
-// the first cut tile, else down to the initial-state term Im (a virtual cut tile
-// before the first).
-__device__ __forceinline__ void prefix_carry(const TileSeg* seg, const int* tileF, int64_t row, int tile, int M,
-                                             int m, float Im, float& cv, float& cn) {
-  const int lane = threadIdx.x & 63;
-  cv = cn = 0.0f;
-  for (int g0 = tile - 1; g0 >= -1; g0 -= 64) {
-    const int tj = g0 - lane;
-    float v = 0.0f, n = 0.0f;
-    bool stop_here = false;
-    if (tj >= 0) {
-      const TileSeg sg = seg[(row + tj) * M + m];
-      v = sg.vp;
-      n = sg.np;
-      stop_here = tileF[(row + tj) * M + m] != 0;
-    } else if (tj == -1) {
-      v = Im;
-      stop_here = true;
+    suffix_affine(A, V, W);
+    const float cv = V + A * zv, cn = W + A * zn;
+    if (j < ntiles) {
+      float4& c = carry[(row + j) * M + m];
+      c.x = cv;
+      c.y = cn;
     }
-    const uint64_t sb = __ballot(stop_here);
-    const int stop = sb ? __builtin_ctzll(sb) : 64;
-    const bool take = lane <= stop && tj >= -1;
-    cv += wave_sum(take ? v : 0.0f);
-    cn += wave_sum(take ? n : 0.0f);
-    if (stop < 64) break;
+    zv = __shfl(cv, 0, 64);
+    zn = __shfl(cn, 0, 64);
   }
-}
-
-// The two anchors of one (batch, head, mode): <dS_final, S_final> and <S_init, dS_init>.
-__device__ __forceinline__ void anchors(const GradInputs& gi, int64_t SF, int64_t i, float& Fm, float& Im) {
-  Fm = Im = 0.0f;
-  for (int q = 0; q < gi.nF; ++q) Fm += gi.F[q * SF + i];
-  for (int q = 0; q < gi.nI; ++q) Im += gi.I[q * SF + i];
+  // prefix, from the first block
+  zv = zn = 0.0f;
+  for (int kb = 0; kb < nblk; ++kb) {
+    const int j = kb * 64 + lane;
+    float A = 1.0f, V = 0.0f, W = 0.0f;
+    if (j == 0) {
+      A = 0.0f;
+      V = Im;
+    } else if (j < ntiles) {
+      const TileSeg sg = seg[(row + j - 1) * M + m];
+      A = gi.tileF[(row + j - 1) * M + m] ? 0.0f : 1.0f;
+      V = sg.vp;
+      W = sg.np;
+    }
+    prefix_affine(A, V, W);
+    const float cv = V + A * zv, cn = W + A * zn;
+    if (j < ntiles) {
+      float4& c = carry[(row + j) * M + m];
+      c.z = cv;
+      c.w = cn;
+    }
+    zv = __shfl(cv, 63, 64);
+    zn = __shfl(cn, 63, 64);
+  }
 }
 
 // Sums the partial slots of one kind for this lane's token into v (zero past the sequence).
@@ -280,11 +313,6 @@ __global__ void __launch_bounds__(256) frac_grad_tiles_kernel(ScanParams p, Grad
   sum_slots<MP>(gi.dc, gi.ndc, S, i0, M, valid, dc);
   sum_slots<MP>(gi.dk, gi.ndk, S, i0, M, valid, dkx);
   sum_slots<MP>(gi.dki, gi.ndki, S, i0, M, valid, dki);
-  if (valid) {  // the sums, for the second kernel
-    store_modes<MP>(gi.dc + i0, M, dc);
-    store_modes<MP>(gi.dk + i0, M, dkx);
-    store_modes<MP>(gi.dki + i0, M, dki);
-  }
   const int64_t row = bh * ntiles;
   const float xcut = cut_exponent(p);
   TileSeg* seg = reinterpret_cast<TileSeg*>(gi.tileV);
@@ -339,20 +367,17 @@ __global__ void __launch_bounds__(256) frac_grad_finish_kernel(ScanParams p, Gra
   const int64_t i0 = (bh * L + t) * M;
   float dc[MP], dk[MP];
   const int64_t row = bh * ntiles;
-  const int64_t SF = (int64_t)p.Bsz * H * M;
   const float xcut = cut_exponent(p);
-  const TileSeg* seg = reinterpret_cast<const TileSeg*>(gi.tileV);
+  const float4* carry = reinterpret_cast<const float4*>(gi.carry);
   float ddtt = 0.0f, scd = 0.0f, swd = 0.0f;
   float beta[MP];
   {
+    // the partial slots summed again, in the first kernel's order
+    const int64_t S = (int64_t)p.Bsz * H * L * M;
     float dkx[MP], dki[MP];
-#pragma unroll
-    for (int m = 0; m < MP; ++m) dc[m] = dkx[m] = dki[m] = 0.0f;
-    if (valid) {
-      load_modes<MP>(gi.dc + i0, M, dc);
-      load_modes<MP>(gi.dk + i0, M, dkx);
-      load_modes<MP>(gi.dki + i0, M, dki);
-    }
+    sum_slots<MP>(gi.dc, gi.ndc, S, i0, M, valid, dc);
+    sum_slots<MP>(gi.dk, gi.ndk, S, i0, M, valid, dkx);
+    sum_slots<MP>(gi.dki, gi.ndki, S, i0, M, valid, dki);
 #pragma unroll
     for (int m = 0; m < MP; ++m) {
       dk[m] = dkx[m] + dki[m];
@@ -365,17 +390,20 @@ __global__ void __launch_bounds__(256) frac_grad_finish_kernel(ScanParams p, Gra
       beta[m] = one_minus_exp_neg(x);
       const float kap = beta[m] * k.w[m];
       const float rd = k.c[m] * dc[m], wx = kap * dkx[m], wi = kap * dki[m];
-      float R;
+      float R, e0, s0;
       if (gi.tileF[(row + tile) * M + m]) {  // cut tile: the chunk-local form
-        R = prefix_sum_excl(wx) + suffix_sum(rd - wi);
-      } else {
-        float Fm, Im, cv, cn;
-        anchors(gi, SF, bh * M + m, Fm, Im);
+        float e1, s1;
+        excl_and_suffix(wx, e0, s0);
+        excl_and_suffix(rd - wi, e1, s1);
+        R = e0 + s1;
+      } else {  // the suffix or the prefix form, whichever range carries less magnitude
+        const float4 cr = carry[(row + tile) * M + m];
         const float g = rd - (wx + wi), a = fabsf(rd) + fabsf(wx + wi);
-        suffix_carry(seg, gi.tileF, row, tile, ntiles, M, m, Fm, cv, cn);
-        const float rs = cv + suffix_sum(g), ns = cn + suffix_sum(a);
-        prefix_carry(seg, gi.tileF, row, tile, M, m, Im, cv, cn);
-        const float rp = cv - prefix_sum_excl(g), np = cn + prefix_sum_excl(a);
+        float e1, s1;
+        excl_and_suffix(g, e0, s0);
+        excl_and_suffix(a, e1, s1);
+        const float rs = cr.x + s0, ns = cr.y + s1;
+        const float rp = cr.z - e0, np = cr.w + e1;
         R = (np < ns) ? rp : rs;
       }
       if (valid) {
@@ -425,6 +453,9 @@ hipError_t launch_grads_mp(const ScanParams& p, const GradInputs& gi, hipStream_
   hipLaunchKernelGGL((frac_grad_tiles_kernel<MP>), grid, dim3(256), 0, stream, p, gi);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
+  const int64_t rows = (int64_t)p.Bsz * p.H * p.M;
+  hipLaunchKernelGGL(frac_grad_carry_kernel, dim3((unsigned)((rows + 3) / 4)), dim3(256), 0, stream, p, gi);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
   hipLaunchKernelGGL((frac_grad_finish_kernel<MP>), grid, dim3(256), 0, stream, p, gi);
   return hipGetLastError();
 }
@@ -433,13 +464,15 @@ hipError_t launch_grads_mp(const ScanParams& p, const GradInputs& gi, hipStream_
 
 size_t grad_tiles_bytes(const ScanParams& p) {
   const size_t n = (size_t)p.Bsz * p.H * ((p.L + 63) / 64) * p.M;
-  return n * (sizeof(TileSeg) + sizeof(int));
+  return n * (sizeof(TileSeg) + sizeof(float4) + sizeof(int));
 }
 
 void grad_tiles_at(const ScanParams& p, void* base, GradInputs& gi) {
   const size_t n = (size_t)p.Bsz * p.H * ((p.L + 63) / 64) * p.M;
-  gi.tileV = reinterpret_cast<float*>(base);
-  gi.tileF = reinterpret_cast<int*>(reinterpret_cast<unsigned char*>(base) + n * sizeof(TileSeg));
+  unsigned char* at = reinterpret_cast<unsigned char*>(base);
+  gi.tileV = reinterpret_cast<float*>(at);
+  gi.carry = reinterpret_cast<float*>(at + n * sizeof(TileSeg));
+  gi.tileF = reinterpret_cast<int*>(at + n * (sizeof(TileSeg) + sizeof(float4)));
 }
 
 hipError_t launch_grad_finish(const ScanParams& p, const GradInputs& gi, hipStream_t stream) {

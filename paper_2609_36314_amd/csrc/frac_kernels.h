@@ -124,10 +124,10 @@ hipError_t launch_nfree_bwd(const ScanParams& p, void* ws, hipStream_t stream);
 
 // Gradients of dt, alpha, lambda, the read / write logits and D from the
 // per-(token, mode) partials of a reverse sweep (frac_grads.hip):
-//   dc [ndc][B H L][M]    partials of dL/dc_{t,m}  (slot 0 is overwritten with the sum)
+//   dc [ndc][B H L][M]    partials of dL/dc_{t,m}
 //   dk [ndk][B H L][M]    partials of the inter-chunk part of dL/dkappa_{t,m} (through
-//                         the adjoint carried in from the later chunks; likewise)
-//   dki [ndki][B H L][M]  partials of its intra-chunk part (likewise)
+//                         the adjoint carried in from the later chunks)
+//   dki [ndki][B H L][M]  partials of its intra-chunk part
 //   F  [nF][B H][M]     partials of <dS_final, S_final> per mode (the final-state term)
 //   I  [nI][B H][M]     partials of <S_init, dS_init> per mode (the initial-state term)
 //   dDp [nD][B H]       partials of sum(dy . x)
@@ -146,6 +146,7 @@ struct GradInputs {
   const float* dDp;
   int nD;
   float* tileV;
+  float* carry;
   int* tileF;
 };
 size_t grad_tiles_bytes(const ScanParams& p);
