@@ -313,6 +313,11 @@ __global__ void __launch_bounds__(256) frac_grad_tiles_kernel(ScanParams p, Grad
   sum_slots<MP>(gi.dc, gi.ndc, S, i0, M, valid, dc);
   sum_slots<MP>(gi.dk, gi.ndk, S, i0, M, valid, dkx);
   sum_slots<MP>(gi.dki, gi.ndki, S, i0, M, valid, dki);
+  if (gi.store_sums && valid) {  // many slots: the sums, for the second kernel
+    store_modes<MP>(gi.dc + i0, M, dc);
+    store_modes<MP>(gi.dk + i0, M, dkx);
+    store_modes<MP>(gi.dki + i0, M, dki);
+  }
   const int64_t row = bh * ntiles;
   const float xcut = cut_exponent(p);
   TileSeg* seg = reinterpret_cast<TileSeg*>(gi.tileV);
@@ -372,12 +377,13 @@ __global__ void __launch_bounds__(256) frac_grad_finish_kernel(ScanParams p, Gra
   float ddtt = 0.0f, scd = 0.0f, swd = 0.0f;
   float beta[MP];
   {
-    // the partial slots summed again, in the first kernel's order
+    // the partial slots summed again in the first kernel's order, or the sums it stored
     const int64_t S = (int64_t)p.Bsz * H * L * M;
+    const bool one = gi.store_sums != 0;
     float dkx[MP], dki[MP];
-    sum_slots<MP>(gi.dc, gi.ndc, S, i0, M, valid, dc);
-    sum_slots<MP>(gi.dk, gi.ndk, S, i0, M, valid, dkx);
-    sum_slots<MP>(gi.dki, gi.ndki, S, i0, M, valid, dki);
+    sum_slots<MP>(gi.dc, one ? 1 : gi.ndc, S, i0, M, valid, dc);
+    sum_slots<MP>(gi.dk, one ? 1 : gi.ndk, S, i0, M, valid, dkx);
+    sum_slots<MP>(gi.dki, one ? 1 : gi.ndki, S, i0, M, valid, dki);
 #pragma unroll
     for (int m = 0; m < MP; ++m) {
       dk[m] = dkx[m] + dki[m];
@@ -447,7 +453,10 @@ __global__ void __launch_bounds__(256) frac_grad_finish_kernel(ScanParams p, Gra
 }
 
 template <int MP>
-hipError_t launch_grads_mp(const ScanParams& p, const GradInputs& gi, hipStream_t stream) {
+hipError_t launch_grads_mp(const ScanParams& p, const GradInputs& gi0, hipStream_t stream) {
+  GradInputs gi = gi0;
+  // with many partial slots, writing their sums once costs less than reading them twice
+  gi.store_sums = gi.ndc + gi.ndk + gi.ndki > 6;
   const int64_t nblk = (int64_t)p.Bsz * ((p.L + 63) / 64) * ((p.H + 3) / 4);
   const dim3 grid((unsigned)nblk);
   hipLaunchKernelGGL((frac_grad_tiles_kernel<MP>), grid, dim3(256), 0, stream, p, gi);

@@ -124,7 +124,7 @@ hipError_t launch_nfree_bwd(const ScanParams& p, void* ws, hipStream_t stream);
 
 // Gradients of dt, alpha, lambda, the read / write logits and D from the
 // per-(token, mode) partials of a reverse sweep (frac_grads.hip):
-//   dc [ndc][B H L][M]    partials of dL/dc_{t,m}
+//   dc [ndc][B H L][M]    partials of dL/dc_{t,m}  (slot 0 may be overwritten with the sum)
 //   dk [ndk][B H L][M]    partials of the inter-chunk part of dL/dkappa_{t,m} (through
 //                         the adjoint carried in from the later chunks)
 //   dki [ndki][B H L][M]  partials of its intra-chunk part
@@ -139,6 +139,7 @@ struct GradInputs {
   float* dk;
   float* dki;
   int ndc, ndk, ndki;
+  int store_sums;  // set by the launcher: the first kernel writes the sums into slot 0
   const float* F;
   int nF;
   const float* I;
