@@ -96,6 +96,37 @@ def test_decode_matches_prefill():
     assert_close("state", f64(state), f64(fs), 1e-3)
 
 
+@pytest.mark.parametrize("M", [16, 32])
+def test_prefill_then_decode_with_the_paper_bank(M):
+    """The hand-off at the paper's bank sizes with B/C: a chunked forward over a prompt
+    (modes in blocks of eight) returns the final state, decode steps continue from it,
+    and the tokens decoded match the chunked forward over prompt and continuation."""
+    w = Workload("t", 2, 1, 2, 64, 128, M, decode_steps=150, init_state=True, extras=True)
+    inp = device_inputs(w, seed=3)
+    tau_d, _ = _tau(M)
+    seq = lambda k: inp[k].transpose(0, 1).contiguous()
+    x, dt, Bm, Cm, lam, rl, wl = (seq(k) for k in ("x", "dt", "Bm", "Cm", "lam", "read_logit", "write_logit"))
+    alpha = seq("alpha")
+    kw = lambda sl: dict(lam=lam[:, sl].contiguous(), read_logit=rl[:, sl].contiguous(),
+                         write_logit=wl[:, sl].contiguous(), D=inp["D"])
+    P0 = 130  # prompt: two chunks and a ragged third
+    _, st = frac.scan_fwd(x[:, :P0].contiguous(), dt[:, :P0].contiguous(), Bm[:, :P0].contiguous(),
+                          Cm[:, :P0].contiguous(), alpha[:, :P0].contiguous(), tau_d, init_state=inp["init_state"],
+                          return_final_state=True, **kw(slice(0, P0)))
+    ys = []
+    for s in range(P0, w.decode_steps):
+        c = lambda t: t[:, s].contiguous()
+        ys.append(frac.decode_step(st, c(x), c(dt), c(Bm), c(Cm), c(alpha), tau_d,
+                                   lam=c(lam), read_logit=c(rl), write_logit=c(wl), D=inp["D"]))
+    y_f, fs = frac.scan_fwd(x, dt, Bm, Cm, alpha, tau_d, init_state=inp["init_state"], return_final_state=True,
+                            **kw(slice(None)))
+    torch.cuda.synchronize()
+    print("prefill then decode, M", M, flush=True)
+    assert_close("decoded y", f64(torch.stack(ys, 1)), f64(y_f[:, P0:]), TOL["bf16"])
+    for m in range(M):  # (the chunked update rounds its matrix-core operands to bfloat16, decode does not)
+        assert_close("state mode %d" % m, f64(st)[:, :, m], f64(fs)[:, :, m], TOL["bf16"])
+
+
 def test_decode_full_size_sampled():
     """The decode workload at full size (2 GiB float32 state), three steps as the
     benchmark runs them, checked on sampled (batch, head) slices."""
