@@ -39,7 +39,8 @@
  *    is float32 (bfloat16 operands of the matrix cores, float32 accumulation);
  *    bfloat16 outputs are rounded to nearest even.
  *  - Supported sizes: headdim P and dstate N multiples of 8 with N <= 128;
- *    P <= 64 for the chunked scan (frac_scan_*), P <= 128 for frac_decode_step;
+ *    P <= 128 (with B/C, headdim above 64 runs in independent groups of 64
+ *    columns, their sums over P added in a fixed order);
  *    1 <= nmodes <= 32 (with B/C, more than 8 modes run the chunked scan in
  *    blocks of eight modes: the weights normalised over the whole bank, the
  *    blocks' y, dx, dB and dC summed in float32 in block order);

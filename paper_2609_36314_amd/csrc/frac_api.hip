@@ -75,6 +75,7 @@ frac_status fill_shape(const frac_shape* sh, frac::ScanParams& p) {
   p.M = (int)sh->nmodes;
   p.Mall = p.M;
   p.PP = (p.P + 15) / 16 * 16;
+  p.Pst = p.P;
   p.NP = next_tile_n(p.N);
   p.io_bf16 = sh->io_dtype == FRAC_BF16;
   return FRAC_OK;
@@ -92,7 +93,7 @@ frac_status check_scan_shape(const frac::ScanParams& p, const char* what, bool) 
       return fail(FRAC_ERR_UNSUPPORTED, "%s: nheads * headdim too large", what);
     return FRAC_OK;
   }
-  if (p.PP > 64) return fail(FRAC_ERR_UNSUPPORTED, "%s: headdim %d > 64 is not built", what, p.P);
+  if (p.P > 128) return fail(FRAC_ERR_UNSUPPORTED, "%s: headdim %d > 128 is not built", what, p.P);
   const int64_t es = p.io_bf16 ? 2 : 4, lim = (int64_t)1 << 31;
   if (64 * (int64_t)p.H * p.P * es >= lim || 64 * (int64_t)p.G * p.N * es >= lim)
     return fail(FRAC_ERR_UNSUPPORTED, "%s: nheads * headdim or ngroups * dstate too large", what);

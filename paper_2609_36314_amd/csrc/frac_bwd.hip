@@ -329,6 +329,7 @@ __global__ void __launch_bounds__(512) frac_bwd_state_kernel(ScanParams p, BwdWo
   using Ex = Exchange<Cfg::NACT>;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, li = lane & 15, lg = lane >> 4;
   const int L = p.L, H = p.H, P = p.P, N = p.N, M = p.M, G = p.G;
+  const int Ps = p.Pst;  // row stride of x, dy, dx and the P extent of the states
   const int nchunks = (L + kQ - 1) / kQ;
   int b, h, ps;
   block_head(Cfg::PS, H, b, h, ps);
@@ -381,10 +382,10 @@ __global__ void __launch_bounds__(512) frac_bwd_state_kernel(ScanParams p, BwdWo
   for (int i = tid; i < 64 * CS; i += 512) Cb[i] = (T)0.0f;
 
   // ---- state S^T: S[m][pb] holds mode mo + m, rows p = 16 pb + 4 lg + r, column ncol
-  const int64_t sbase = ((int64_t)b * H + h) * (int64_t)p.Mall * N * P;
+  const int64_t sbase = ((int64_t)b * H + h) * (int64_t)p.Mall * N * Ps;
   floatx4 S[MPF][4];
   {
-    int lo = ncol * P + lg * 4;
+    int lo = ncol * Ps + lg * 4;
     asm volatile("" : "+v"(lo));
 #pragma unroll
     for (int m = 0; m < MPF; ++m)
@@ -395,16 +396,16 @@ __global__ void __launch_bounds__(512) frac_bwd_state_kernel(ScanParams p, BwdWo
           const int pr = pb * 16 + lg * 4 + r;
           float v = 0.0f;
           if (p.init_state && active && mo + m < M && ncol < N && pr < P)
-            v = p.init_state[sbase + (int64_t)(mo + m) * N * P + lo + pb * 16 + r];
+            v = p.init_state[sbase + (int64_t)(mo + m) * N * Ps + lo + pb * 16 + r];
           S[m][pb][r] = v;
         }
   }
 
-  const T* xg = reinterpret_cast<const T*>(p.x) + (((int64_t)b * L) * H + h) * P;
-  const T* yg = reinterpret_cast<const T*>(p.dy) + (((int64_t)b * L) * H + h) * P;
+  const T* xg = reinterpret_cast<const T*>(p.x) + (((int64_t)b * L) * H + h) * Ps;
+  const T* yg = reinterpret_cast<const T*>(p.dy) + (((int64_t)b * L) * H + h) * Ps;
   const T* Bgp = reinterpret_cast<const T*>(p.Bm) + (((int64_t)b * L) * G + g) * N;
   const T* Cgp = reinterpret_cast<const T*>(p.Cm) + (((int64_t)b * L) * G + g) * N;
-  const int64_t xstride = (int64_t)H * P, bstride = (int64_t)G * N;
+  const int64_t xstride = (int64_t)H * Ps, bstride = (int64_t)G * N;
   const float* dt_bh = p.dt + (int64_t)b * L * H + h;
   const float* al_bh = p.alpha + b * p.as0 + h * p.as2;
   const float* lm_bh = p.lambda ? p.lambda + b * p.ls0 + h * p.ls2 : nullptr;
@@ -775,7 +776,7 @@ __global__ void __launch_bounds__(512) frac_bwd_state_kernel(ScanParams p, BwdWo
   for (int m = 0; m < MPF; ++m) fpart[m] = 0.0f;
   if (p.d_final_state && active) {
     const float* Ef = s_E2 + (nchunks & 1) * MP;
-    int lo = ncol * P + lg * 4;
+    int lo = ncol * Ps + lg * 4;
     asm volatile("" : "+v"(lo));
 #pragma unroll
     for (int m = 0; m < MPF; ++m) {
@@ -786,7 +787,7 @@ __global__ void __launch_bounds__(512) frac_bwd_state_kernel(ScanParams p, BwdWo
         for (int r = 0; r < 4; ++r) {
           const int pr = pb * 16 + lg * 4 + r;
           if (mo + m < M && ncol < N && pr < P)
-            fpart[m] += scale * S[m][pb][r] * p.d_final_state[sbase + (int64_t)(mo + m) * N * P + lo + pb * 16 + r];
+            fpart[m] += scale * S[m][pb][r] * p.d_final_state[sbase + (int64_t)(mo + m) * N * Ps + lo + pb * 16 + r];
         }
     }
   }
@@ -824,6 +825,7 @@ __global__ void __launch_bounds__(512) frac_bwd_cols_kernel(ScanParams p, BwdWor
   using Ex = Exchange<Cfg::NACT>;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, li = lane & 15, lg = lane >> 4;
   const int L = p.L, H = p.H, P = p.P, N = p.N, M = p.M, G = p.G;
+  const int Ps = p.Pst;  // row stride of x, dy, dx and the P extent of the states
   const int nchunks = (L + kQ - 1) / kQ;
   int b, h, ps;
   block_head(Cfg::PS, H, b, h, ps);
@@ -867,10 +869,10 @@ __global__ void __launch_bounds__(512) frac_bwd_cols_kernel(ScanParams p, BwdWor
   for (int i = tid; i < 64 * CS; i += 512) Cb0[i] = Cb1[Cfg::NBUF == 2 ? i : 0] = (T)0.0f;
 
   // ---- adjoint G^T: Gs[m][pb] holds mode mo + m, rows p = 16 pb + 4 lg + r, column ncol
-  const int64_t sbase = ((int64_t)b * H + h) * (int64_t)p.Mall * N * P;
+  const int64_t sbase = ((int64_t)b * H + h) * (int64_t)p.Mall * N * Ps;
   floatx4 Gs[MPF][4];
   {
-    int lo = ncol * P + lg * 4;
+    int lo = ncol * Ps + lg * 4;
     asm volatile("" : "+v"(lo));
 #pragma unroll
     for (int m = 0; m < MPF; ++m)
@@ -881,15 +883,15 @@ __global__ void __launch_bounds__(512) frac_bwd_cols_kernel(ScanParams p, BwdWor
           const int pr = pb * 16 + lg * 4 + r;
           float v = 0.0f;
           if (p.d_final_state && active && mo + m < M && ncol < N && pr < P)
-            v = p.d_final_state[sbase + (int64_t)(mo + m) * N * P + lo + pb * 16 + r];
+            v = p.d_final_state[sbase + (int64_t)(mo + m) * N * Ps + lo + pb * 16 + r];
           Gs[m][pb][r] = v;
         }
   }
 
-  const T* xg = reinterpret_cast<const T*>(p.x) + (((int64_t)b * L) * H + h) * P;
-  const T* yg = reinterpret_cast<const T*>(p.dy) + (((int64_t)b * L) * H + h) * P;
+  const T* xg = reinterpret_cast<const T*>(p.x) + (((int64_t)b * L) * H + h) * Ps;
+  const T* yg = reinterpret_cast<const T*>(p.dy) + (((int64_t)b * L) * H + h) * Ps;
   const T* Cgp = reinterpret_cast<const T*>(p.Cm) + (((int64_t)b * L) * G + g) * N;
-  const int64_t xstride = (int64_t)H * P, bstride = (int64_t)G * N;
+  const int64_t xstride = (int64_t)H * Ps, bstride = (int64_t)G * N;
   const float* dt_bh = p.dt + (int64_t)b * L * H + h;
   const float* al_bh = p.alpha + b * p.as0 + h * p.as2;
   const float* lm_bh = p.lambda ? p.lambda + b * p.ls0 + h * p.ls2 : nullptr;
@@ -1108,6 +1110,7 @@ __global__ void __launch_bounds__(512) frac_bwd_rows_kernel(ScanParams p, BwdWor
   using Ex = Exchange<NPART>;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, li = lane & 15, lg = lane >> 4;
   const int L = p.L, H = p.H, P = p.P, N = p.N, M = p.M, G = p.G;
+  const int Ps = p.Pst;  // row stride of x, dy, dx and the P extent of the states
   const int nchunks = (L + kQ - 1) / kQ;
   int b, h, ps;
   block_head(Cfg::PS, H, b, h, ps);
@@ -1161,10 +1164,10 @@ __global__ void __launch_bounds__(512) frac_bwd_rows_kernel(ScanParams p, BwdWor
   for (int i = tid; i < 64 * CS; i += 512) Cb0[i] = Cb1[Cfg::NBUF == 2 ? i : 0] = (T)0.0f;
 
   // ---- adjoint G: Gs[m][jb] holds mode mo + m, rows n = 16 (nbo + jb) + 4 lg + r, column pc
-  const int64_t sbase = ((int64_t)b * H + h) * (int64_t)p.Mall * N * P;
+  const int64_t sbase = ((int64_t)b * H + h) * (int64_t)p.Mall * N * Ps;
   floatx4 Gs[MPW][NBW];
   {
-    int lo = (mo * N + nbo * 16 + lg * 4) * P + pc;
+    int lo = (mo * N + nbo * 16 + lg * 4) * Ps + pc;
     asm volatile("" : "+v"(lo));
 #pragma unroll
     for (int m = 0; m < MPW; ++m)
@@ -1175,18 +1178,18 @@ __global__ void __launch_bounds__(512) frac_bwd_rows_kernel(ScanParams p, BwdWor
           const int n = (nbo + jb) * 16 + lg * 4 + r;
           float v = 0.0f;
           if (p.d_final_state && active && mo + m < M && n < N && pc < P)
-            v = p.d_final_state[sbase + lo + ((int64_t)m * N + jb * 16 + r) * P];
+            v = p.d_final_state[sbase + lo + ((int64_t)m * N + jb * 16 + r) * Ps];
           Gs[m][jb][r] = v;
         }
   }
   const float Dh = p.D ? p.D[h] : 0.0f;
 
-  const T* xg = reinterpret_cast<const T*>(p.x) + (((int64_t)b * L) * H + h) * P;
-  const T* yg = reinterpret_cast<const T*>(p.dy) + (((int64_t)b * L) * H + h) * P;
-  T* dxg = reinterpret_cast<T*>(p.dx) + (((int64_t)b * L) * H + h) * P;
+  const T* xg = reinterpret_cast<const T*>(p.x) + (((int64_t)b * L) * H + h) * Ps;
+  const T* yg = reinterpret_cast<const T*>(p.dy) + (((int64_t)b * L) * H + h) * Ps;
+  T* dxg = reinterpret_cast<T*>(p.dx) + (((int64_t)b * L) * H + h) * Ps;
   const T* Bgp = reinterpret_cast<const T*>(p.Bm) + (((int64_t)b * L) * G + g) * N;
   const T* Cgp = reinterpret_cast<const T*>(p.Cm) + (((int64_t)b * L) * G + g) * N;
-  const int64_t xstride = (int64_t)H * P, bstride = (int64_t)G * N;
+  const int64_t xstride = (int64_t)H * Ps, bstride = (int64_t)G * N;
   const float* dt_bh = p.dt + (int64_t)b * L * H + h;
   const float* al_bh = p.alpha + b * p.as0 + h * p.as2;
   const float* lm_bh = p.lambda ? p.lambda + b * p.ls0 + h * p.ls2 : nullptr;
@@ -1385,7 +1388,7 @@ __global__ void __launch_bounds__(512) frac_bwd_rows_kernel(ScanParams p, BwdWor
       load4(Yc + t * XS + pr, yv);
       floatx4 v = dxa[tb];
       if constexpr (BLK) {  // a mode block: float32 partial sums across the blocks
-        const int64_t xi = (((int64_t)b * L + t0 + t) * H + h) * P + pr;
+        const int64_t xi = (((int64_t)b * L + t0 + t) * H + h) * Ps + pr;
         if (t < nv && pr < P) {
           if (p.y_in) {
             const float4 u = *reinterpret_cast<const float4*>(p.y_in + xi);
@@ -1401,7 +1404,7 @@ __global__ void __launch_bounds__(512) frac_bwd_rows_kernel(ScanParams p, BwdWor
       for (int r = 0; r < 4; ++r) v[r] += Dh * yv[r];
       if (!(BLK && p.y_part)) {
         if (Cfg::kBf16) store4(Dxb + t * XS + pr, v);  // staged, stored 16 bytes at a time
-        else if (t < nv && pr < P) store4(dxg + (int64_t)t0 * xstride + t * (H * P) + pr, v);
+        else if (t < nv && pr < P) store4(dxg + (int64_t)t0 * xstride + t * xstride + pr, v);
       }
     }
 
@@ -1459,7 +1462,7 @@ __global__ void __launch_bounds__(512) frac_bwd_rows_kernel(ScanParams p, BwdWor
     const float* Ef = s_E2 + (nchunks & 1) * MP;
     // lane offset kept opaque (as for the initial load) so that no per-element offset
     // of this store is formed before, and held across, the sequence loop
-    int lo = (mo * N + nbo * 16 + lg * 4) * P + pc;
+    int lo = (mo * N + nbo * 16 + lg * 4) * Ps + pc;
     asm volatile("" : "+v"(lo));
 #pragma unroll
     for (int m = 0; m < MPW; ++m)
@@ -1469,7 +1472,7 @@ __global__ void __launch_bounds__(512) frac_bwd_rows_kernel(ScanParams p, BwdWor
         for (int r = 0; r < 4; ++r) {
           const int n = (nbo + jb) * 16 + lg * 4 + r;
           if (mo + m < M && n < N && pc < P)
-            p.dinit_state[sbase + lo + ((int64_t)m * N + jb * 16 + r) * P] = Gs[m][jb][r] * Ef[mo + m];
+            p.dinit_state[sbase + lo + ((int64_t)m * N + jb * 16 + r) * Ps] = Gs[m][jb][r] * Ef[mo + m];
         }
   }
 
@@ -1478,7 +1481,7 @@ __global__ void __launch_bounds__(512) frac_bwd_rows_kernel(ScanParams p, BwdWor
   barrier();  // the token partials are no longer read
   {
     const float* Ef = s_E2 + (nchunks & 1) * MP;
-    int lo = (mo * N + nbo * 16 + lg * 4) * P + pc;
+    int lo = (mo * N + nbo * 16 + lg * 4) * Ps + pc;
     asm volatile("" : "+v"(lo));
 #pragma unroll
     for (int m = 0; m < MPW; ++m) {
@@ -1489,7 +1492,7 @@ __global__ void __launch_bounds__(512) frac_bwd_rows_kernel(ScanParams p, BwdWor
         for (int r = 0; r < 4; ++r) {
           const int n = (nbo + jb) * 16 + lg * 4 + r;
           if (p.init_state && active && mo + m < M && n < N && pc < P)
-            ip += p.init_state[sbase + lo + ((int64_t)m * N + jb * 16 + r) * P] * Gs[m][jb][r];
+            ip += p.init_state[sbase + lo + ((int64_t)m * N + jb * 16 + r) * Ps] * Gs[m][jb][r];
         }
       ip = group_allreduce<64>(ip, [](float x, float y) { return x + y; });
       if (lane == 0) redW[wave * MPW + m] = (active && mo + m < M) ? ip * Ef[mo + m] : 0.0f;
@@ -1526,6 +1529,7 @@ __global__ void __launch_bounds__(256) frac_bwd_intra_kernel(ScanParams p, const
   constexpr int MB = (MP + 15) / 16;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, li = lane & 15, lg = lane >> 4;
   const int L = p.L, H = p.H, P = p.P, M = p.M, G = p.G;
+  const int Ps = p.Pst;
   const int nchunks = (L + kQ - 1) / kQ;
   // block = (b, c, h), heads fastest: the heads of a group read the same C B^T tiles
   const int h = (int)(blockIdx.x % H);
@@ -1552,9 +1556,9 @@ __global__ void __launch_bounds__(256) frac_bwd_intra_kernel(ScanParams p, const
   // x and dy of the chunk, 16 bytes per thread (columns past P, tokens past the sequence: zero)
   {
     constexpr int E16 = 16 / (int)sizeof(T), CPR = 64 / E16;
-    const int64_t xstride = (int64_t)H * P;
-    const T* xg = reinterpret_cast<const T*>(p.x) + (((int64_t)b * L + t0) * H + h) * P;
-    const T* yg = reinterpret_cast<const T*>(p.dy) + (((int64_t)b * L + t0) * H + h) * P;
+    const int64_t xstride = (int64_t)H * Ps;
+    const T* xg = reinterpret_cast<const T*>(p.x) + (((int64_t)b * L + t0) * H + h) * Ps;
+    const T* yg = reinterpret_cast<const T*>(p.dy) + (((int64_t)b * L + t0) * H + h) * Ps;
     for (int i = tid; i < 64 * CPR; i += 256) {
       const int t = i / CPR, col = (i - t * CPR) * E16;
       int4 vx = make_int4(0, 0, 0, 0), vy = vx;
@@ -1689,41 +1693,43 @@ int pad_modes(int M) { return M <= 1 ? 1 : M <= 2 ? 2 : M <= 4 ? 4 : 8; }
 int state_parts(const ScanParams& p) { return pad_modes(p.M) * (p.NP / 16) > 32 ? 2 : 1; }
 int rows_parts(const ScanParams& p) { return (pad_modes(p.M) >= 8 && p.io_bf16) ? 2 : 1; }
 int mode_blocks(const ScanParams& p) { return p.Mall > kModeBlock ? (p.Mall + kModeBlock - 1) / kModeBlock : 1; }
+int column_groups(const ScanParams& p) { return (p.Pst + 63) / 64; }
 
 // Workspace: C B^T tiles, the state sweep's Gamma tiles, per-head dB / dC partials
-// (per mode block), the (token, mode) partials, per-mode terms, dD partials, the
-// finisher's tile sums; with mode blocks also the log-normalizers and the float32
-// partial dx.
+// (per mode block and column group), the (token, mode) partials (per sweep part and
+// column group), per-mode terms, dD partials, the finisher's tile sums; with mode
+// blocks also the log-normalizers and the float32 partial dx.
 struct BwdLayout {
-  size_t tiles, gg, hg, dBp, dCp, dc, dk, F, I, dDp, gtl, lse, dxp, total;
+  size_t tiles, gg, hg, dBp, dCp, dc, dk, dki, F, I, dDp, gtl, lse, dxp, total;
 };
 
 BwdLayout bwd_layout(const ScanParams& p) {
   BwdLayout l{};
   const size_t es = p.io_bf16 ? 2 : 4;
   const size_t bl = (size_t)p.Bsz * p.L, blhm = bl * p.H * p.Mall, bh = (size_t)p.Bsz * p.H;
-  const size_t nmb = (size_t)mode_blocks(p);
+  const size_t nmb = (size_t)mode_blocks(p), R = (size_t)column_groups(p);
   auto up = [](size_t v) { return (v + 255) / 256 * 256; };
   l.tiles = 0;
   const size_t gtb = (size_t)p.Bsz * ((p.L + kQ - 1) / kQ) * p.H * kTiles * kTileElems * es;
   l.gg = up(cb_tiles_bytes(p));
   l.hg = l.gg + up(gtb);
   l.dBp = l.hg + up(gtb);
-  l.dCp = l.dBp + up(nmb * bl * p.H * p.N * es);
-  l.dc = l.dCp + up(nmb * bl * p.H * p.N * es);
-  l.dk = l.dc + up(sizeof(float) * (state_parts(p) + 1) * blhm);
-  l.F = l.dk + up(sizeof(float) * (rows_parts(p) + 1) * blhm);
-  l.I = l.F + up(sizeof(float) * state_parts(p) * bh * p.Mall);
-  l.dDp = l.I + up(sizeof(float) * rows_parts(p) * bh * p.Mall);
-  l.gtl = l.dDp + up(sizeof(float) * bh);
+  l.dCp = l.dBp + up(R * nmb * bl * p.H * p.N * es);
+  l.dc = l.dCp + up(R * nmb * bl * p.H * p.N * es);
+  l.dk = l.dc + up(sizeof(float) * R * (state_parts(p) + 1) * blhm);
+  l.dki = l.dk + up(sizeof(float) * R * rows_parts(p) * blhm);
+  l.F = l.dki + up(sizeof(float) * R * blhm);
+  l.I = l.F + up(sizeof(float) * R * state_parts(p) * bh * p.Mall);
+  l.dDp = l.I + up(sizeof(float) * R * rows_parts(p) * bh * p.Mall);
+  l.gtl = l.dDp + up(sizeof(float) * R * bh);
   l.lse = l.gtl + up(grad_tiles_bytes(p));
   l.dxp = l.lse + (nmb > 1 ? up(sizeof(float) * 2 * bl * p.H) : 0);
-  l.total = l.dxp + (nmb > 1 ? up(sizeof(float) * bl * p.H * p.P) : 0);
+  l.total = l.dxp + (nmb > 1 ? up(sizeof(float) * bl * p.H * p.Pst) : 0);
   return l;
 }
 
 // The three sweeps (and the intra-chunk kernel when the state sweep does not fold
-// it in) for the modes p covers.
+// it in) for the modes and columns p covers.
 template <typename T, int MP, int NB, bool BLK>
 hipError_t launch_bwd_sweeps(const ScanParams& p, const BwdWork& wk, const T* tiles, size_t blhm, hipStream_t stream) {
   using SC = ColCfg<T, MP, NB>;
@@ -1753,7 +1759,9 @@ hipError_t launch_bwd_variant(const ScanParams& p, void* ws, hipStream_t stream)
   if (SC::PS != state_parts(p) || RC::PS != rows_parts(p)) return hipErrorInvalidValue;
   const BwdLayout l = bwd_layout(p);
   unsigned char* base = reinterpret_cast<unsigned char*>(ws);
-  const size_t blhm = (size_t)p.Bsz * p.L * p.H * p.Mall;
+  const size_t blhm = (size_t)p.Bsz * p.L * p.H * p.Mall, bhm = (size_t)p.Bsz * p.H * p.Mall;
+  constexpr bool kFold = StateLds<T, MP, NB>::kFold;
+  constexpr int NDC = SC::PS + (kFold ? 0 : 1);  // dc slots per column group
   BwdWork wk;
   wk.tiles = base + l.tiles;
   wk.gg = base + l.gg;
@@ -1762,74 +1770,76 @@ hipError_t launch_bwd_variant(const ScanParams& p, void* ws, hipStream_t stream)
   wk.dCp = base + l.dCp;
   wk.dc = reinterpret_cast<float*>(base + l.dc);
   wk.dk = reinterpret_cast<float*>(base + l.dk);
+  wk.dki = reinterpret_cast<float*>(base + l.dki);
   wk.F = reinterpret_cast<float*>(base + l.F);
   wk.I = reinterpret_cast<float*>(base + l.I);
   wk.dDp = reinterpret_cast<float*>(base + l.dDp);
-
-  constexpr bool kFold = StateLds<T, MP, NB>::kFold;
-  // dc: the state sweep's parts (the first with the intra-chunk part when folded), then
-  // the intra kernel's; dk: the rows sweep's parts, then the intra-chunk part
-  wk.dki = wk.dk + RC::PS * blhm;
   hipError_t e = launch_cb_tiles(p, base + l.tiles, stream);
   if (e != hipSuccess) return e;
   const T* tiles = reinterpret_cast<const T*>(base + l.tiles);
-  const int nmb = mode_blocks(p);
-  if (nmb == 1) {
-    if ((e = launch_bwd_sweeps<T, MP, NB, false>(p, wk, tiles, blhm, stream)) != hipSuccess) return e;
-  } else if constexpr (MP == kModeBlock) {
-    // More modes than one workgroup's registers hold: the sweeps once per block of
-    // eight modes, the weights normalised over the bank, dx summed in float32 in
-    // block order (the last block adds the skip term), dB and dC per block.
-    float* lse = reinterpret_cast<float*>(base + l.lse);
-    float* dxp = reinterpret_cast<float*>(base + l.dxp);
-    if ((e = launch_mode_lse(p, lse, stream)) != hipSuccess) return e;
-    const int64_t NPs = (int64_t)p.N * p.P;
-    const size_t slot = (size_t)p.Bsz * p.L * p.H * p.N * sizeof(T);
+  const int nmb = mode_blocks(p), R = column_groups(p);
+  float* lse = reinterpret_cast<float*>(base + l.lse);
+  if (nmb > 1 && (e = launch_mode_lse(p, lse, stream)) != hipSuccess) return e;
+  const size_t slot = (size_t)p.Bsz * p.L * p.H * p.N * sizeof(T);  // one dB / dC partial
+  // Per column group of 64 columns of P (independent but for their sums over P, which
+  // get their own slots), per block of eight modes: the weights normalised over the
+  // bank, dx summed in float32 in block order (the last block adds the skip term).
+  for (int r = 0; r < R; ++r) {
+    const ScanParams pc = column_group(p, r * 64);
     for (int q = 0; q < nmb; ++q) {
       const int mo = q * kModeBlock;
-      ScanParams pb = p;
-      pb.M = min(kModeBlock, p.Mall - mo);
-      pb.tau = p.tau + mo;
-      if (p.read_logit) pb.read_logit = p.read_logit + mo;
-      if (p.write_logit) pb.write_logit = p.write_logit + mo;
-      if (p.init_state) pb.init_state = p.init_state + mo * NPs;
-      if (p.d_final_state) pb.d_final_state = p.d_final_state + mo * NPs;
-      if (p.dinit_state) pb.dinit_state = p.dinit_state + mo * NPs;
-      pb.lse = lse;
-      pb.y_in = q > 0 ? dxp : nullptr;
-      pb.y_part = q + 1 < nmb ? dxp : nullptr;
+      ScanParams pb = pc;
       BwdWork wb = wk;
-      wb.dBp = reinterpret_cast<unsigned char*>(wk.dBp) + q * slot;
-      wb.dCp = reinterpret_cast<unsigned char*>(wk.dCp) + q * slot;
-      wb.dc = wk.dc + mo;
-      wb.dk = wk.dk + mo;
-      wb.dki = wk.dki + mo;
-      wb.F = wk.F + mo;
-      wb.I = wk.I + mo;
-      if ((e = launch_bwd_sweeps<T, MP, NB, true>(pb, wb, tiles, blhm, stream)) != hipSuccess) return e;
+      wb.dBp = reinterpret_cast<unsigned char*>(wk.dBp) + (size_t)(r * nmb + q) * slot;
+      wb.dCp = reinterpret_cast<unsigned char*>(wk.dCp) + (size_t)(r * nmb + q) * slot;
+      wb.dc = wk.dc + (size_t)r * NDC * blhm + mo;
+      wb.dk = wk.dk + (size_t)r * RC::PS * blhm + mo;
+      wb.dki = wk.dki + (size_t)r * blhm + mo;
+      wb.F = wk.F + (size_t)r * SC::PS * bhm + mo;
+      wb.I = wk.I + (size_t)r * RC::PS * bhm + mo;
+      wb.dDp = wk.dDp + (size_t)r * p.Bsz * p.H;
+      if (nmb == 1) {
+        if ((e = launch_bwd_sweeps<T, MP, NB, false>(pb, wb, tiles, blhm, stream)) != hipSuccess) return e;
+        continue;
+      }
+      if constexpr (MP == kModeBlock) {
+        const int64_t NPs = (int64_t)p.N * p.Pst;
+        float* dxp = reinterpret_cast<float*>(base + l.dxp) + r * 64;
+        pb.M = min(kModeBlock, p.Mall - mo);
+        pb.tau = p.tau + mo;
+        if (p.read_logit) pb.read_logit = p.read_logit + mo;
+        if (p.write_logit) pb.write_logit = p.write_logit + mo;
+        if (pc.init_state) pb.init_state = pc.init_state + mo * NPs;
+        if (pc.d_final_state) pb.d_final_state = pc.d_final_state + mo * NPs;
+        if (pc.dinit_state) pb.dinit_state = pc.dinit_state + mo * NPs;
+        pb.lse = lse;
+        pb.y_in = q > 0 ? dxp : nullptr;
+        pb.y_part = q + 1 < nmb ? dxp : nullptr;
+        if ((e = launch_bwd_sweeps<T, MP, NB, true>(pb, wb, tiles, blhm, stream)) != hipSuccess) return e;
+      } else {
+        return hipErrorInvalidValue;
+      }
     }
-  } else {
-    return hipErrorInvalidValue;
   }
   GradInputs gi;
   gi.dc = wk.dc;
   gi.dk = wk.dk;
   gi.dki = wk.dki;
-  gi.ndc = SC::PS + (kFold ? 0 : 1);
-  gi.ndk = RC::PS;
-  gi.ndki = 1;
+  gi.ndc = R * NDC;
+  gi.ndk = R * RC::PS;
+  gi.ndki = R;
   gi.F = wk.F;
-  gi.nF = SC::PS;
+  gi.nF = R * SC::PS;
   gi.I = wk.I;
-  gi.nI = RC::PS;
+  gi.nI = R * RC::PS;
   gi.dDp = wk.dDp;
-  gi.nD = 1;
+  gi.nD = R;
   grad_tiles_at(p, base + l.gtl, gi);
   if ((e = launch_grad_finish(p, gi, stream)) != hipSuccess) return e;
   const int64_t nrows = (int64_t)p.Bsz * p.L;
   const int64_t nthr = nrows * p.G * (p.N / (16 / (int)sizeof(T)));
   hipLaunchKernelGGL((frac_bwd_group_sum_kernel<T>), dim3((unsigned)((nthr + 255) / 256)), dim3(256), 0, stream, p,
-                     reinterpret_cast<const T*>(wk.dBp), reinterpret_cast<const T*>(wk.dCp), nrows, nmb,
+                     reinterpret_cast<const T*>(wk.dBp), reinterpret_cast<const T*>(wk.dCp), nrows, R * nmb,
                      (int64_t)p.Bsz * p.L * p.H * p.N);
   return hipGetLastError();
 }

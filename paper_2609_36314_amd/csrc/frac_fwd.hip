@@ -188,11 +188,12 @@ __global__ void __launch_bounds__(512) frac_fwd_kernel(ScanParams p, const T* __
   const int nbo = (part / Cfg::NPM) * NBW;  // first N block of this wave
   const int pc = pb * 16 + li;
   const int L = p.L, H = p.H, P = p.P, N = p.N, M = p.M, G = p.G;
+  const int Ps = p.Pst;  // row stride of x, y and the P extent of the states
   const int nchunks = (L + kQ - 1) / kQ;
   const int T0 = seg * p.seg_len;                                                // first token
   const int T1 = p.nseg > 1 ? min(L, (seg + 1) * p.seg_len) : L;                // one past the last
   const int c0 = T0 / kQ, c1 = (T1 + kQ - 1) / kQ;                              // chunks of the segment
-  const int64_t seg_ss = (int64_t)p.Bsz * p.H * p.Mall * p.N * p.P;             // one boundary state
+  const int64_t seg_ss = (int64_t)p.Bsz * p.H * p.Mall * p.N * Ps;              // one boundary state
   const float* init_state = seg == 0 ? p.init_state : (STATE_ONLY ? nullptr : p.seg_state + (seg - 1) * seg_ss);
   float* final_state = STATE_ONLY ? p.seg_state + seg * seg_ss : (T1 == L ? p.final_state : nullptr);
   double seg_ell = 0.0;  // state-only pass, thread m < M: the segment's summed log-decay of mode m
@@ -231,11 +232,11 @@ __global__ void __launch_bounds__(512) frac_fwd_kernel(ScanParams p, const T* __
   float* P_lh = P_k + MP * kWQ;    // [MP][Q] chunk log-decays l_{t,m}, hi and lo parts
   float* P_ll = P_lh + MP * kWQ;
 
-  const T* xg = reinterpret_cast<const T*>(p.x) + (((int64_t)b * L) * H + h) * P;
+  const T* xg = reinterpret_cast<const T*>(p.x) + (((int64_t)b * L) * H + h) * Ps;
   const T* Bgp = reinterpret_cast<const T*>(p.Bm) + (((int64_t)b * L) * G + g) * N;
   const T* Cgp = reinterpret_cast<const T*>(p.Cm) + (((int64_t)b * L) * G + g) * N;
-  T* yg = reinterpret_cast<T*>(p.y) + (((int64_t)b * L) * H + h) * P;
-  const int64_t xstride = (int64_t)H * P, bstride = (int64_t)G * N;
+  T* yg = reinterpret_cast<T*>(p.y) + (((int64_t)b * L) * H + h) * Ps;
+  const int64_t xstride = (int64_t)H * Ps, bstride = (int64_t)G * N;
 
   // per-mode rates 1/tau_m, log tau_m and state scales E_m (by chunk parity) in LDS
   if (tid < MP) {
@@ -251,12 +252,12 @@ __global__ void __launch_bounds__(512) frac_fwd_kernel(ScanParams p, const T* __
   for (int i = tid; i < 64 * CS; i += 512) Cb0[i] = Cb1[Cfg::NBUF == 2 ? i : 0] = (T)0.0f;
 
   // ---- state: S[m][jb] holds mode mo + m, rows n = 16 (nbo + jb) + 4 lg + r, column pc
-  const int64_t sbase = ((int64_t)b * H + h) * (int64_t)p.Mall * N * P;
+  const int64_t sbase = ((int64_t)b * H + h) * (int64_t)p.Mall * N * Ps;
   floatx4 S[MPW][NBW];
   {
     // lane offset kept opaque so that the final store cannot share (and keep alive
     // across the sequence loop) the per-element offsets of this load
-    int lo = (mo * N + nbo * 16 + lg * 4) * P + pc;
+    int lo = (mo * N + nbo * 16 + lg * 4) * Ps + pc;
     asm volatile("" : "+v"(lo));
 #pragma unroll
     for (int m = 0; m < MPW; ++m)
@@ -267,7 +268,7 @@ __global__ void __launch_bounds__(512) frac_fwd_kernel(ScanParams p, const T* __
           const int n = (nbo + jb) * 16 + lg * 4 + r;
           float v = 0.0f;
           if (init_state && active && mo + m < M && n < N && pc < P)
-            v = init_state[sbase + lo + ((int64_t)m * N + jb * 16 + r) * P];
+            v = init_state[sbase + lo + ((int64_t)m * N + jb * 16 + r) * Ps];
           S[m][jb][r] = v;
         }
   }
@@ -535,7 +536,7 @@ __global__ void __launch_bounds__(512) frac_fwd_kernel(ScanParams p, const T* __
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int tr = tb * 16 + lg * 4 + r;
-          const int64_t yi = (((int64_t)b * L + t0 + tr) * H + h) * P + pc;
+          const int64_t yi = (((int64_t)b * L + t0 + tr) * H + h) * Ps + pc;
           if (tr < nv && pc < P) {
             if (p.y_in) Y[tb][r] += p.y_in[yi];
             if (p.y_part) p.y_part[yi] = Y[tb][r];
@@ -603,7 +604,7 @@ __global__ void __launch_bounds__(512) frac_fwd_kernel(ScanParams p, const T* __
 
   if (final_state && active) {
     const float* Ef = s_E2 + (c1 & 1) * MP;
-    int lo = (mo * N + nbo * 16 + lg * 4) * P + pc;
+    int lo = (mo * N + nbo * 16 + lg * 4) * Ps + pc;
     asm volatile("" : "+v"(lo));
 #pragma unroll
     for (int m = 0; m < MPW; ++m) {
@@ -614,7 +615,7 @@ __global__ void __launch_bounds__(512) frac_fwd_kernel(ScanParams p, const T* __
         for (int r = 0; r < 4; ++r) {
           const int n = (nbo + jb) * 16 + lg * 4 + r;
           if (mo + m < M && n < N && pc < P)
-            final_state[sbase + lo + ((int64_t)m * N + jb * 16 + r) * P] = S[m][jb][r] * Em;
+            final_state[sbase + lo + ((int64_t)m * N + jb * 16 + r) * Ps] = S[m][jb][r] * Em;
         }
     }
   }
@@ -672,7 +673,7 @@ size_t align256(size_t n) { return (n + 255) & ~(size_t)255; }
 size_t split_bytes(const ScanParams& p, const FwdSplit& sp) {
   if (sp.nseg <= 1) return 0;
   const size_t ns = (size_t)sp.nseg - 1, bhm = (size_t)p.Bsz * p.H * p.Mall;
-  return align256(sizeof(float) * ns * bhm * p.N * p.P) + align256(sizeof(float) * ns * bhm);
+  return align256(sizeof(float) * ns * bhm * p.N * p.Pst) + align256(sizeof(float) * ns * bhm);
 }
 
 void place_split(ScanParams& p, const FwdSplit& sp, unsigned char* at) {
@@ -684,28 +685,29 @@ void place_split(ScanParams& p, const FwdSplit& sp, unsigned char* at) {
     return;
   }
   const size_t ns = (size_t)sp.nseg - 1, bhm = (size_t)p.Bsz * p.H * p.Mall;
-  p.seg_state = reinterpret_cast<float*>(at);
-  p.seg_decay = reinterpret_cast<float*>(at + align256(sizeof(float) * ns * bhm * p.N * p.P));
+  p.seg_state = reinterpret_cast<float*>(at) + p.col0;  // this column group's columns
+  p.seg_decay = reinterpret_cast<float*>(at + align256(sizeof(float) * ns * bhm * p.N * p.Pst));
 }
 
 // The boundary states: S_k = decay_k S_{k-1} + (segment k's own end state), in
-// segment order, per state element (all modes of the bank).
+// segment order, per state element (all modes of the bank, this column group's P).
 __global__ void __launch_bounds__(256) frac_seg_combine_kernel(ScanParams p) {
-  const int64_t ss = (int64_t)p.Bsz * p.H * p.Mall * p.N * p.P;
+  const int64_t ss = (int64_t)p.Bsz * p.H * p.Mall * p.N * p.Pst;  // one boundary state
   const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (i >= ss) return;
-  const int64_t bhm = i / ((int64_t)p.N * p.P), nbhm = (int64_t)p.Bsz * p.H * p.Mall;
-  float s = p.seg_state[i];
+  if (i >= (int64_t)p.Bsz * p.H * p.Mall * p.N * p.P) return;
+  const int64_t row = i / p.P, e = row * p.Pst + (i - row * p.P);  // (b, h, m, n) row, column
+  const int64_t bhm = row / p.N, nbhm = (int64_t)p.Bsz * p.H * p.Mall;
+  float s = p.seg_state[e];
   for (int k = 1; k + 1 < p.nseg; ++k) {
-    s = p.seg_decay[k * nbhm + bhm] * s + p.seg_state[k * ss + i];
-    p.seg_state[k * ss + i] = s;
+    s = p.seg_decay[k * nbhm + bhm] * s + p.seg_state[k * ss + e];
+    p.seg_state[k * ss + e] = s;
   }
 }
 
 hipError_t launch_seg_combine(const ScanParams& p, hipStream_t stream) {
   if (p.nseg <= 2) return hipSuccess;  // one boundary: the first segment's end state
-  const int64_t ss = (int64_t)p.Bsz * p.H * p.Mall * p.N * p.P;
-  hipLaunchKernelGGL(frac_seg_combine_kernel, dim3((unsigned)((ss + 255) / 256)), dim3(256), 0, stream, p);
+  const int64_t n = (int64_t)p.Bsz * p.H * p.Mall * p.N * p.P;
+  hipLaunchKernelGGL(frac_seg_combine_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, stream, p);
   return hipGetLastError();
 }
 
@@ -797,7 +799,7 @@ FwdBlockLayout fwd_block_layout(const ScanParams& p) {
   l.seg = align256(gtile_bytes<T>(p));
   l.lse = l.seg + split_bytes(p, l.split);
   l.ypart = l.lse + align256(sizeof(float) * 2 * (size_t)p.Bsz * p.L * p.H);
-  l.total = l.ypart + sizeof(float) * (size_t)p.Bsz * p.L * p.H * p.P;
+  l.total = l.ypart + sizeof(float) * (size_t)p.Bsz * p.L * p.H * p.Pst;
   return l;
 }
 
@@ -813,9 +815,9 @@ hipError_t launch_fwd_blocks(const ScanParams& p0, void* ws, hipStream_t stream)
   hipError_t e = launch_cb_variant<T, NB>(p0, gt, stream);
   if (e != hipSuccess) return e;
   float* lse = reinterpret_cast<float*>(base + l.lse);
-  float* ypart = reinterpret_cast<float*>(base + l.ypart);
+  float* ypart = reinterpret_cast<float*>(base + l.ypart) + p0.col0;  // this column group's columns
   if ((e = launch_mode_lse(p0, lse, stream)) != hipSuccess) return e;
-  const int64_t NP = (int64_t)p0.N * p0.P;
+  const int64_t NP = (int64_t)p0.N * p0.Pst;
   ScanParams ps0 = p0;
   place_split(ps0, l.split, base + l.seg);
   // the state-only passes of every block, the boundary states, then the output passes
@@ -919,7 +921,13 @@ size_t scan_fwd_workspace(const ScanParams& p) {
 
 hipError_t launch_scan_fwd(const ScanParams& p, void* ws, size_t, hipStream_t stream) {
   if (p.Bsz == 0 || p.L == 0) return hipSuccess;
-  return p.io_bf16 ? launch_fwd_mp<bf16>(p, ws, stream) : launch_fwd_mp<float>(p, ws, stream);
+  // headdim above 64: independent groups of 64 columns (the recurrence is per column of P)
+  for (int c0 = 0; c0 < p.Pst; c0 += 64) {
+    const ScanParams q = column_group(p, c0);
+    const hipError_t e = p.io_bf16 ? launch_fwd_mp<bf16>(q, ws, stream) : launch_fwd_mp<float>(q, ws, stream);
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
 }
 
 }  // namespace frac

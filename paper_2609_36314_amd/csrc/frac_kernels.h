@@ -15,6 +15,10 @@ namespace frac {
 struct ScanParams {
   int Bsz, L, H, P, N, G, M;
   int PP, NP;
+  // Row stride of x, y, dx, dy and the P extent of the states (the caller's headdim).
+  // A launch may cover P <= Pst columns of it (a column group, its pointers offset).
+  int Pst;
+  int col0;  // the first column of this launch's group (offsets the workspace's P-wide arrays)
   int io_bf16;
   const void* x;
   const float* dt;
@@ -65,6 +69,26 @@ struct ScanParams {
   float* dwrite_logit;
   float* dinit_state;
 };
+
+// The launch parameters of the columns [c0, c0 + 64) of P (at most 64): the column
+// count, and every pointer whose last dimension is P offset to the first column.
+inline ScanParams column_group(const ScanParams& p, int c0) {
+  ScanParams q = p;
+  q.col0 = c0;
+  q.P = p.Pst - c0 < 64 ? p.Pst - c0 : 64;
+  q.PP = (q.P + 15) / 16 * 16;
+  const size_t es = p.io_bf16 ? 2 : 4;
+  auto off = [&](const void* v) { return v ? static_cast<const void*>(static_cast<const char*>(v) + es * c0) : v; };
+  q.x = off(p.x);
+  q.y = p.y ? static_cast<char*>(p.y) + es * c0 : nullptr;
+  q.dy = off(p.dy);
+  q.dx = p.dx ? static_cast<char*>(p.dx) + es * c0 : nullptr;
+  q.init_state = p.init_state ? p.init_state + c0 : nullptr;
+  q.final_state = p.final_state ? p.final_state + c0 : nullptr;
+  q.d_final_state = p.d_final_state ? p.d_final_state + c0 : nullptr;
+  q.dinit_state = p.dinit_state ? p.dinit_state + c0 : nullptr;
+  return q;
+}
 
 // Each launcher returns hipSuccess or the launch error; `stream` may be null.
 hipError_t launch_scan_fwd(const ScanParams& p, void* ws, size_t ws_bytes, hipStream_t stream);

@@ -66,8 +66,8 @@ def _shape(**kw):
     (dict(dstate=12), -2),
     (dict(dstate=256), -2),
     (dict(headdim=20), -2),
-    (dict(headdim=128, dstate=128), -2),
-    (dict(headdim=128, dstate=16), -2),
+    (dict(headdim=136, dstate=128), -2),
+    (dict(headdim=136, dstate=16), -2),
     (dict(chunk=128), -2),
 ])
 def test_invalid_shapes_are_rejected_on_the_host(kw, status):

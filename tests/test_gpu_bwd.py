@@ -84,6 +84,11 @@ CASES = {
     "f32 M12 N64 extras dfinal": Workload("t", 1, 150, 2, 32, 64, 12, io_dtype="f32", extras=True, init_state=True,
                                           backward=True, final_state=True),
     "bf16 M32 groups": Workload("t", 1, 140, 4, 64, 64, 32, ngroups=2, backward=True, final_state=True),
+    # headdim above 64: groups of 64 columns, their sums over P in slots of their own
+    "bf16 P128 extras dfinal": Workload("t", 1, 150, 2, 128, 128, 8, extras=True, init_state=True, backward=True,
+                                        final_state=True),
+    "f32 P96 M16 extras": Workload("t", 1, 130, 2, 96, 64, 16, io_dtype="f32", extras=True, init_state=True,
+                                   backward=True, final_state=True),
 }
 
 
@@ -107,7 +112,8 @@ def test_bwd_parity_small(name):
 
 
 ALL_GRAD_CASES = ["f32 extras dfinal", "f32 M8 N128 extras dfinal", "bf16 M5 N96 P32 extras", "bf16 groups extras",
-                  "bf16 M8", "bf16 L1", "bf16 M16 extras dfinal", "f32 M12 N64 extras dfinal", "bf16 M32 groups"]
+                  "bf16 M8", "bf16 L1", "bf16 M16 extras dfinal", "f32 M12 N64 extras dfinal", "bf16 M32 groups",
+                  "bf16 P128 extras dfinal", "f32 P96 M16 extras"]
 
 
 @pytest.mark.parametrize("moderate", [False, True])

@@ -102,6 +102,10 @@ SMALL = {
     "bf16 split8 M4 extras": Workload("t", 1, 2000, 2, 64, 128, 4, extras=True, init_state=True, final_state=True),
     "f32 split6 M3 ragged": Workload("t", 1, 1500, 1, 32, 32, 3, io_dtype="f32", init_state=True, final_state=True),
     "bf16 split4 M16": Workload("t", 1, 1100, 2, 64, 128, 16, extras=True, init_state=True, final_state=True),
+    # headdim above 64: groups of 64 columns (the last one partial)
+    "bf16 P128 extras": Workload("t", 2, 150, 2, 128, 128, 4, extras=True, init_state=True, final_state=True),
+    "f32 P96 M8": Workload("t", 1, 130, 2, 96, 64, 8, io_dtype="f32", init_state=True, final_state=True),
+    "bf16 P128 M16 split": Workload("t", 1, 1300, 2, 128, 128, 16, init_state=True, final_state=True),
 }
 
 
