@@ -165,21 +165,28 @@ __global__ void __launch_bounds__(256) frac_nfree_fwd_kernel(ScanParams p, float
       const float r = s_rr[m], prior = -al * s_lnt[m];
       const float zc = (m < M) ? prior + rlr[j] : -INFINITY;
       const float zw = (m < M) ? prior + wlr[j] : -INFINITY;
-      const float cw = valid ? group_softmax<MP>(zc) : 0.0f;
-      const float ww = (rl_bh == wl_bh) ? cw : (valid ? group_softmax<MP>(zw) : 0.0f);
-      const float lh = P_lh[m * WQ + t], lhQ = P_lh[m * WQ + kQ - 1];
-      const bool safe = lhQ <= kNfSafe;
+      const float lhQ = P_lh[m * WQ + kQ - 1];
       const float Enew = Ecur[m] * fexp(-lhQ);
       const bool ren = !(Enew >= kNfFloor);
       const float upd = ren ? 1.0f : __frcp_rn(Enew);
-      const float kap = one_minus_exp_neg(dtt * r) * ww;
-      const float om = cw * fexp(-lh);
-      P_O[m * WQ + t] = om;
-      P_om[m * WQ + t] = om * Ecur[m];
-      P_v[m * WQ + t] = kap * ell_decay(P_lh + m * WQ, P_ll + m * WQ, kQ - 1, t) * upd;
-      P_Vt[m * WQ + t] = safe ? kap * fexp(lh) : 0.0f;
-      P_c[m * WQ + t] = cw;
-      P_k[m * WQ + t] = kap;
+      if constexpr (CKPT) {  // the state update only: the write weights
+        const float ww = valid ? group_softmax<MP>((rl_bh == wl_bh) ? zc : zw) : 0.0f;
+        const float kap = one_minus_exp_neg(dtt * r) * ww;
+        P_v[m * WQ + t] = kap * ell_decay(P_lh + m * WQ, P_ll + m * WQ, kQ - 1, t) * upd;
+      } else {
+        const float cw = valid ? group_softmax<MP>(zc) : 0.0f;
+        const float ww = (rl_bh == wl_bh) ? cw : (valid ? group_softmax<MP>(zw) : 0.0f);
+        const float lh = P_lh[m * WQ + t];
+        const bool safe = lhQ <= kNfSafe;
+        const float kap = one_minus_exp_neg(dtt * r) * ww;
+        const float om = cw * fexp(-lh);
+        P_O[m * WQ + t] = om;
+        P_om[m * WQ + t] = om * Ecur[m];
+        P_v[m * WQ + t] = kap * ell_decay(P_lh + m * WQ, P_ll + m * WQ, kQ - 1, t) * upd;
+        P_Vt[m * WQ + t] = safe ? kap * fexp(lh) : 0.0f;
+        P_c[m * WQ + t] = cw;
+        P_k[m * WQ + t] = kap;
+      }
       if (pr < MP) Enext[m] = ren ? 1.0f : Enew;
     }
     float renf[MB * 4];
