@@ -375,29 +375,43 @@ __global__ void __launch_bounds__(512) frac_fwd_kernel(ScanParams p, const T* __
       float zw = (m < M) ? prior + lgt.wl[j] : -INFINITY;
       // tokens past the sequence get zero weights (their tile rows may hold anything finite);
       // a mode block normalises over all modes with the precomputed log-normalizers
-      float cw, ww;
-      if constexpr (BLK) {
-        const float2 ln = valid ? *reinterpret_cast<const float2*>(lse_bh + (int64_t)(t0 + t) * H * 2)
-                                : float2{0.0f, 0.0f};
-        cw = valid ? __expf(zc - ln.x) : 0.0f;
-        ww = w_is_c ? cw : (valid ? __expf(zw - ln.y) : 0.0f);
-      } else {
-        cw = valid ? group_softmax<MP>(zc) : 0.0f;
-        ww = w_is_c ? cw : (valid ? group_softmax<MP>(zw) : 0.0f);
-      }
-      const float lh = P_lh[m * kWQ + t], lhQ = P_lh[m * kWQ + kQ - 1];
-      const bool safe = lhQ <= kSafeExponent;
+      const float lhQ = P_lh[m * kWQ + kQ - 1];
       const float Enew = Ecur[m] * fexp(-lhQ);
       const bool ren = !(Enew >= kRescaleFloor);
       const float upd = ren ? 1.0f : __frcp_rn(Enew);
-      const float kap = one_minus_exp_neg(dtt * r) * ww;
-      const float om = cw * fexp(-lh);
-      P_O[m * kWQ + t] = om;
-      P_om[m * kWQ + t] = om * Ecur[m];
-      P_v[m * kWQ + t] = kap * ell_decay(P_lh + m * kWQ, P_ll + m * kWQ, kQ - 1, t) * upd;
-      P_Vt[m * kWQ + t] = safe ? kap * fexp(lh) : 0.0f;
-      P_c[m * kWQ + t] = cw;
-      P_k[m * kWQ + t] = kap;
+      if constexpr (STATE_ONLY) {  // the state update only: the write weights
+        float ww;
+        if constexpr (BLK) {
+          const float2 ln = valid ? *reinterpret_cast<const float2*>(lse_bh + (int64_t)(t0 + t) * H * 2)
+                                  : float2{0.0f, 0.0f};
+          ww = valid ? __expf((w_is_c ? zc : zw) - (w_is_c ? ln.x : ln.y)) : 0.0f;
+        } else {
+          ww = valid ? group_softmax<MP>(w_is_c ? zc : zw) : 0.0f;
+        }
+        const float kap = one_minus_exp_neg(dtt * r) * ww;
+        P_v[m * kWQ + t] = kap * ell_decay(P_lh + m * kWQ, P_ll + m * kWQ, kQ - 1, t) * upd;
+      } else {
+        float cw, ww;
+        if constexpr (BLK) {
+          const float2 ln = valid ? *reinterpret_cast<const float2*>(lse_bh + (int64_t)(t0 + t) * H * 2)
+                                  : float2{0.0f, 0.0f};
+          cw = valid ? __expf(zc - ln.x) : 0.0f;
+          ww = w_is_c ? cw : (valid ? __expf(zw - ln.y) : 0.0f);
+        } else {
+          cw = valid ? group_softmax<MP>(zc) : 0.0f;
+          ww = w_is_c ? cw : (valid ? group_softmax<MP>(zw) : 0.0f);
+        }
+        const float lh = P_lh[m * kWQ + t];
+        const bool safe = lhQ <= kSafeExponent;
+        const float kap = one_minus_exp_neg(dtt * r) * ww;
+        const float om = cw * fexp(-lh);
+        P_O[m * kWQ + t] = om;
+        P_om[m * kWQ + t] = om * Ecur[m];
+        P_v[m * kWQ + t] = kap * ell_decay(P_lh + m * kWQ, P_ll + m * kWQ, kQ - 1, t) * upd;
+        P_Vt[m * kWQ + t] = safe ? kap * fexp(lh) : 0.0f;
+        P_c[m * kWQ + t] = cw;
+        P_k[m * kWQ + t] = kap;
+      }
       if (pr < MP) Enext[m] = ren ? 1.0f : Enew;
     }
     // this wave's modes: rescale flags and factors (wave-uniform)
