@@ -24,12 +24,13 @@
 // adjoint (at most 2 x 4 16x16 float32 tiles per mode group) in matrix-core
 // accumulators for the whole sequence:
 //   state  forward in time, state transposed (lane = column n of N, rows p): dC
-//          (per head), the state part of dc (per mode, over the workgroup's rows
-//          of N), the final-state term <dS_final, S_final> per mode and sum(dy . x)
-//          for dD;
+//          (per head), dc (per mode, over the workgroup's rows of N; with the
+//          intra-chunk parts of dc and dk when they fit in LDS), the final-state
+//          term <dS_final, S_final> per mode and sum(dy . x) for dD;
 //   rows   reverse, adjoint in row layout (lane = column p of P, rows n): dx, the
-//          adjoint part of dk (per mode, over the workgroup's columns of P) and the
-//          gradient of the initial state;
+//          inter-chunk part of dk (through the adjoint carried in from the later
+//          chunks, per mode, over the workgroup's columns of P), the gradient of
+//          the initial state and the term <S_init, dS_init> per mode;
 //   cols   reverse, adjoint transposed (lane = column n): dB (per head).
 // The state sweep also writes each chunk's causal tiles (C B^T) o Gamma and
 // Gamma o (dY X^T) (bfloat16 for bfloat16 I/O, 10 tiles of 16x16 per chunk and
@@ -39,8 +40,12 @@
 // gets a second partial sum.  Tiles are copied straight into
 // LDS (natural layout, padded rows) and read back as matrix-core fragments with
 // row reads or transposed 64-bit reads.  A chunk-parallel kernel forms the
-// intra-chunk parts of dc and dk, and a reduction kernel sums dB and dC over the
-// heads of each group in a fixed order.
+// intra-chunk parts of dc and dk where the state sweep cannot, the finisher of
+// frac_grads.hip turns the per-(token, mode) partials into the step-size, order
+// and logit gradients, and a reduction kernel sums dB and dC over the heads of
+// each group in a fixed order.  Banks of more than eight modes run the sweeps once
+// per block of eight modes, and heads wider than 64 columns once per group of 64
+// columns, each with slots of its own for the sums that span them.
 #include "frac_device.h"
 #include "frac_kernels.h"
 

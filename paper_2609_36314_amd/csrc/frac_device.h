@@ -333,12 +333,6 @@ __device__ __forceinline__ float ell_decay(const float* lh, const float* ll, int
 // e^x through the hardware exp2 (a multiply and one transcendental).
 __device__ __forceinline__ float fexp(float x) { return __expf(x); }
 
-// e^{-r d} for an interval d that is >= 0 in exact arithmetic but is a difference of
-// two float32 prefix sums: lanes of a scan add in different orders, so with large
-// sums the difference can round below zero by several ulps, and e^{+r |d|} would
-// overflow.  The clamp keeps every decay in [0, 1].
-__device__ __forceinline__ float fdecay(float r, float d) { return __expf(-r * fmaxf(d, 0.0f)); }
-
 // 1 - e^{-x} for x >= 0 without cancellation: a short Taylor series where the
 // difference is small, the subtraction elsewhere (relative error <= ~4e-6).
 __device__ __forceinline__ float one_minus_exp_neg(float x) {

@@ -40,6 +40,11 @@
 //                    becomes the K-slot order, matched by the order in which C is
 //                    read from LDS.  Waves that split the modes add their partial
 //                    outputs through LDS exchange slots before y is stored.
+//                    A state-only instance scans the segments of a split sequence
+//                    to their end states (frac_seg_combine_kernel chains them into
+//                    boundary states); a mode-block instance covers eight modes of
+//                    a larger bank, its weights normalised over the whole bank
+//                    (frac_mode_lse_kernel), its outputs summed in float32.
 //
 // Gamma uses the factorised form (c e^{-r A_t}) (kappa e^{r A_k}) through a float32
 // 16x16x4 product with the modes as K, for every mode whose chunk decay r_m A_Q
