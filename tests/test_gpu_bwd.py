@@ -89,6 +89,9 @@ CASES = {
                                         final_state=True),
     "f32 P96 M16 extras": Workload("t", 1, 130, 2, 96, 64, 16, io_dtype="f32", extras=True, init_state=True,
                                    backward=True, final_state=True),
+    # the largest sizes built: four mode blocks x two column groups
+    "bf16 max M32 N128 P128": Workload("t", 1, 100, 2, 128, 128, 32, extras=True, init_state=True, backward=True,
+                                       final_state=True),
 }
 
 
@@ -113,7 +116,7 @@ def test_bwd_parity_small(name):
 
 ALL_GRAD_CASES = ["f32 extras dfinal", "f32 M8 N128 extras dfinal", "bf16 M5 N96 P32 extras", "bf16 groups extras",
                   "bf16 M8", "bf16 L1", "bf16 M16 extras dfinal", "f32 M12 N64 extras dfinal", "bf16 M32 groups",
-                  "bf16 P128 extras dfinal", "f32 P96 M16 extras"]
+                  "bf16 P128 extras dfinal", "f32 P96 M16 extras", "bf16 max M32 N128 P128"]
 
 
 @pytest.mark.parametrize("moderate", [False, True])

@@ -106,6 +106,9 @@ SMALL = {
     "bf16 P128 extras": Workload("t", 2, 150, 2, 128, 128, 4, extras=True, init_state=True, final_state=True),
     "f32 P96 M8": Workload("t", 1, 130, 2, 96, 64, 8, io_dtype="f32", init_state=True, final_state=True),
     "bf16 P128 M16 split": Workload("t", 1, 1300, 2, 128, 128, 16, init_state=True, final_state=True),
+    # the largest sizes built: 32 modes, state 128, headdim 128 (four mode blocks x two column groups)
+    "bf16 max M32 N128 P128": Workload("t", 1, 100, 2, 128, 128, 32, extras=True, init_state=True,
+                                       final_state=True),
 }
 
 
