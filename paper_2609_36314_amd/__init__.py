@@ -156,8 +156,10 @@ def scan_fwd(x, dt, Bm, Cm, alpha, tau, *, lam=None, read_logit=None, write_logi
 def scan_fwd_noalloc(x, dt, Bm, Cm, alpha, tau, *, y, lam=None, read_logit=None, write_logit=None, D=None,
                      init_state=None, final_state=None, chunk=0):
     """frac_scan_fwd_noalloc: the forward with the library's static scratch in place of a
-    workspace.  The outputs y (and final_state, when wanted) are the caller's; the call
-    allocates no device memory."""
+    workspace.  The outputs y (and final_state, when wanted) are the caller's; the library
+    call allocates no device memory.  (A Python float for alpha or lam is turned into a
+    cached one-element device tensor the first time it is seen: pass tensors where no
+    allocation at all may happen.)"""
     M = int(tau.shape[0])
     shape = _shape(x, Bm, M, chunk)
     args, keep = _fwd_struct(x, dt, Bm, Cm, alpha, tau, lam, read_logit, write_logit, D, init_state, y, final_state)
