@@ -242,3 +242,34 @@ def test_bwd_full_size_sampled():
     assert_close("dB[0]", f64(g["dBm"][0:1]), ref["dBm"], TOL["bf16"])
     assert_close("dC[0]", f64(g["dCm"][0:1]), ref["dCm"], TOL["bf16"])
     assert_close("dx[0]", f64(g["dx"][0:1]), ref["dx"], TOL["bf16"])
+
+
+@pytest.mark.parametrize("io", ["f32", "bf16"])
+def test_custom_tau_bank(io):
+    """A caller's own timescale bank instead of the geometric default: unsorted, with
+    modes faster than one step (tau < 1, rates above 1) beside very slow ones; the
+    forward and every gradient against the oracle on the same bank."""
+    M = 6
+    w = Workload("t", 1, 170, 2, 64, 64, M, io_dtype=io, extras=True, init_state=True, backward=True,
+                 final_state=True)
+    inp = device_inputs(w, seed=21)
+    t32 = np.array([30.0, 0.25, 4000.0, 1.0, 0.6, 150000.0], dtype=np.float32)
+    tau_d, tau64 = torch.from_numpy(t32).cuda(), t32.astype(np.float64)
+    dfs = inp["d_final_state"]
+    kw = {k: inp[k] for k in ("lam", "read_logit", "write_logit", "D", "init_state")}
+    print("custom tau", io, flush=True)
+    y, fin = frac.scan_fwd(inp["x"], inp["dt"], inp["Bm"], inp["Cm"], inp["alpha"], tau_d, return_final_state=True,
+                           **kw)
+    g = frac.scan_bwd(inp["x"], inp["dt"], inp["Bm"], inp["Cm"], inp["alpha"], tau_d, inp["dy"], d_final_state=dfs,
+                      all_grads=True, **kw)
+    torch.cuda.synchronize()
+    okw = {k: f64(inp[k]) for k in ("lam", "read_logit", "write_logit", "D", "init_state")}
+    args = (f64(inp["x"]), f64(inp["dt"]), f64(inp["Bm"]), f64(inp["Cm"]), f64(inp["alpha"]), tau64)
+    ry, rfin = oracle.forward(*args, **okw)
+    ref = oracle.backward(*args, f64(inp["dy"]), d_final_state=f64(dfs), **okw)
+    tol = TOL[io]
+    assert_close("y", f64(y), ry, tol)
+    for m in range(M):
+        assert_close("final_state mode %d" % m, f64(fin)[:, :, m], rfin[:, :, m], tol)
+    for k in ("dx", "ddt", "dBm", "dCm", "dinit_state", "dread_logit", "dwrite_logit", "dalpha", "dlambda", "dD"):
+        assert_close(k, f64(g[k]), ref[k], tol)

@@ -267,3 +267,28 @@ def test_nfree_bwd_full_size_all_grads_sampled():
         sl["init_state"] = inp["init_state"][:, h:h + 1]
         ref = _oracle_bwd(sl, tau64, dfs[:, h:h + 1])
         assert_close("dD[%d]" % h, f64(g["dD"][h:h + 1]), ref["dD"], tol)
+
+
+def test_nfree_custom_tau_bank():
+    """The paper's form with an unsorted bank of the caller's own timescales, modes faster
+    than one step among them: forward, final state and every gradient."""
+    M = 8
+    w = Workload("t", 1, 150, 2, 128, 1, M, bc=False, extras=True, init_state=True, backward=True, final_state=True)
+    inp = device_inputs(w, seed=22)
+    t32 = np.array([2.0, 0.3, 9000.0, 50.0, 0.8, 131072.0, 7.0, 1.0], dtype=np.float32)
+    tau_d, tau64 = torch.from_numpy(t32).cuda(), t32.astype(np.float64)
+    dfs = inp["d_final_state"]
+    kw = {k: inp[k] for k in ("lam", "read_logit", "write_logit", "D", "init_state")}
+    y, fin = frac.scan_fwd(inp["x"], inp["dt"], None, None, inp["alpha"], tau_d, return_final_state=True, **kw)
+    g = frac.scan_bwd(inp["x"], inp["dt"], None, None, inp["alpha"], tau_d, inp["dy"], d_final_state=dfs,
+                      all_grads=True, **kw)
+    torch.cuda.synchronize()
+    yr, fr = _oracle_fwd(inp, tau64)
+    ref = _oracle_bwd(inp, tau64, dfs)
+    tol = TOL["bf16"]
+    assert_close("y", f64(y), yr, tol)
+    assert_close("final_state", f64(fin), fr, tol)
+    assert_close("dx", f64(g["dx"]), ref["dx"], tol)
+    assert_close("ddt", f64(g["ddt"]), ref["ddt"], tol)
+    assert_close("dD", f64(g["dD"]), ref["dD"], tol)
+    _check_further_grads(g, ref, tol, True)
