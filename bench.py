@@ -364,6 +364,31 @@ def measured_traffic(entry, workload):
     return float(rec["bytes_per_launch"])
 
 
+# kernels whose counters belong to each entry point's launch
+_ENTRY_KERNELS = {"frac_scan_bwd": ("frac_cb_kernel", "frac_bwd_", "frac_grad_", "frac_nfree_fwd_kernel<bf16,16,1>",
+                                    "frac_nfree_bwd_"),
+                  "frac_scan_fwd": ("frac_cb_kernel", "frac_fwd_", "frac_seg_combine", "frac_mode_lse",
+                                    "frac_nfree_fwd_kernel<bf16,16,0>")}
+
+
+def measured_mfma_busy(entry, workload):
+    """Matrix-core busy share per kernel of `entry` on `workload` from the committed counter
+    summary (SQ_VALU_MFMA_BUSY_CYCLES over the SIMD cycles of the launch), or None when the
+    kernels have changed since the counters were taken or the workload was not profiled."""
+    path = os.path.join(ROOT, "profiles", "pmc_scan_kernels.md")
+    if not os.path.exists(path) or entry not in _ENTRY_KERNELS:
+        return None
+    for m in re.finditer(r"^counters: (\{.*\})\s*$", open(path).read(), re.M):
+        rec = json.loads(m.group(1))
+        if rec.get("workload") != workload:
+            continue
+        if rec.get("source_sha256") != kernel_source_digest():
+            return None
+        busy = {k: v for k, v in rec["mfma_busy"].items() if k.startswith(_ENTRY_KERNELS[entry])}
+        return busy or None
+    return None
+
+
 def roofline(bound, work, ms, peak, unit):
     rate = work / (ms * 1e-3)
     scale = 1e12 if unit == "TFLOP/s" else 1e9
@@ -535,14 +560,16 @@ def main():
             # the dominant entry point of the step: frac_scan_bwd (C B^T tiles, state / row / column
             # sweeps, ddt suffix sums, group sum of dB and dC), one launch per step
             line["roofline"] = dict(mres["bwd_roofline"], kernel="frac_scan_bwd",
-                                    traffic=measured_traffic("frac_scan_bwd", main_w.name))
+                                    traffic=measured_traffic("frac_scan_bwd", main_w.name),
+                                    mfma_busy=measured_mfma_busy("frac_scan_bwd", main_w.name))
             line["step_roofline"] = dict(mres["fwd_bwd_roofline"], kernel="frac_scan_fwd + frac_scan_bwd")
         elif "roofline" in mres:
             line["roofline"] = dict(mres["roofline"], kernel="frac_decode_step",
                                     traffic=measured_traffic("frac_decode_step", main_w.name))
         else:
             line["roofline"] = dict(mres["fwd_roofline"], kernel="frac_scan_fwd",
-                                    traffic=measured_traffic("frac_scan_fwd", main_w.name))
+                                    traffic=measured_traffic("frac_scan_fwd", main_w.name),
+                                    mfma_busy=measured_mfma_busy("frac_scan_fwd", main_w.name))
     if "roofline" in line:
         line["roofline"] = with_measured(line["roofline"], mp)
     if mp:

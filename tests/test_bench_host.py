@@ -39,3 +39,15 @@ def test_traffic_is_reported_only_for_the_sources_it_was_measured_on(monkeypatch
     monkeypatch.setattr(bench, "kernel_source_digest", lambda: "0" * 64)
     assert bench.measured_traffic("frac_scan_bwd", "train-b4-l4096-m8") is None
     assert bench.measured_traffic("frac_scan_bwd", "no-such-workload") is None
+
+
+def test_mfma_busy_is_reported_only_for_the_sources_it_was_measured_on(monkeypatch):
+    got = bench.measured_mfma_busy("frac_scan_bwd", "train-b4-l4096-m8")
+    if got is not None:  # the backward's sweeps, each a share of the SIMD cycles
+        assert any(k.startswith("frac_bwd_state_kernel") for k in got)
+        assert all(0.0 <= v <= 1.0 for v in got.values())
+        assert not any(k.startswith("frac_fwd_kernel") for k in got)
+    assert bench.measured_mfma_busy("frac_decode_step", "decode-b256-128steps") is None
+    assert bench.measured_mfma_busy("frac_scan_bwd", "no-such-workload") is None
+    monkeypatch.setattr(bench, "kernel_source_digest", lambda: "0" * 64)
+    assert bench.measured_mfma_busy("frac_scan_bwd", "train-b4-l4096-m8") is None
