@@ -170,8 +170,10 @@ struct FwdCfg {
 // of a sequence-split forward).
 // BLK: one block of a mode-block launch sequence (weights normalised with p.lse,
 // outputs accumulated through p.y_in / p.y_part).
+// The state-only pass allocates no C, output or Gamma tiles and is held to 128
+// registers, so that two of its workgroups share a CU.
 template <typename T, int MP, int NB, int PS, bool STATE_ONLY, bool BLK = false>
-__global__ void __launch_bounds__(512) frac_fwd_kernel(ScanParams p, const T* __restrict__ gtiles) {
+__global__ void __launch_bounds__(512, STATE_ONLY ? 4 : 1) frac_fwd_kernel(ScanParams p, const T* __restrict__ gtiles) {
   using Cfg = FwdCfg<T, MP, NB, PS, STATE_ONLY>;
   constexpr int NP = Cfg::NP, XS = Cfg::XS, BS = Cfg::BS, CS = Cfg::CS, GS = Cfg::GS;
   constexpr int NPART = Cfg::NPART, MPW = Cfg::MPW, NBW = Cfg::NBW, KBW = Cfg::KBW, TBP = Cfg::TBP;
@@ -210,16 +212,16 @@ __global__ void __launch_bounds__(512) frac_fwd_kernel(ScanParams p, const T* __
   if ((nblk & 7) == 0) j = (j & 7) * (nblk >> 3) + (j >> 3);
   const int b = j / H, h = j - b * H, g = h * G / H;
 
-  __shared__ __align__(16) T Xb0[64 * XS], Bb0[64 * BS], Cb0[64 * CS];
+  __shared__ __align__(16) T Xb0[64 * XS], Bb0[64 * BS], Cb0[STATE_ONLY ? 8 : 64 * CS];
   __shared__ __align__(16) T Xb1[Cfg::NBUF == 2 ? 64 * XS : 8], Bb1[Cfg::NBUF == 2 ? 64 * BS : 8],
-      Cb1[Cfg::NBUF == 2 ? 64 * CS : 8];
+      Cb1[Cfg::NBUF == 2 && !STATE_ONLY ? 64 * CS : 8];
   // everything else in one array, so that its addresses differ by constants
   constexpr int oGG = 0;                                        // T [64][GS] ((C B^T) o Gamma)^T, causal
-  constexpr int oYb = oGG + 64 * GS * (int)sizeof(T);           // T [64][XS] output rows of the previous chunk
-  constexpr int oPrm = oYb + 64 * XS * (int)sizeof(T);          // float [8 MP][Q] per-token weights, log-decays
+  constexpr int oYb = oGG + (STATE_ONLY ? 0 : 64 * GS * (int)sizeof(T));           // T [64][XS] output rows of the previous chunk
+  constexpr int oPrm = oYb + (STATE_ONLY ? 0 : 64 * XS * (int)sizeof(T));          // float [8 MP][Q] per-token weights, log-decays
   constexpr int NSLOT = 4 - Cfg::TBO;                           // row blocks a wave hands over
   constexpr int oYX = oPrm + 8 * MP * kWQ * 4;                  // float [8 waves][NSLOT][4][64] readout exchange
-  constexpr int oSc = oYX + (NPART > 1 ? 8 * NSLOT * 256 : 4) * 4;  // float rates, log tau, scales
+  constexpr int oSc = oYX + (NPART > 1 && !STATE_ONLY ? 8 * NSLOT * 256 : 4) * 4;  // float rates, log tau, scales
   __shared__ __align__(16) unsigned char sm[oSc + 4 * MP * 4];
   T* GGT = reinterpret_cast<T*>(sm + oGG);
   T* Yb = reinterpret_cast<T*>(sm + oYb);
@@ -251,10 +253,12 @@ __global__ void __launch_bounds__(512) frac_fwd_kernel(ScanParams p, const T* __
     s_E2[tid] = s_E2[MP + tid] = 1.0f;
   }
   // tiles start zeroed: columns past P or N are never copied into
-  for (int i = tid; i < 64 * GS; i += 512) GGT[i] = (T)0.0f;
+  if constexpr (!STATE_ONLY)
+    for (int i = tid; i < 64 * GS; i += 512) GGT[i] = (T)0.0f;
   for (int i = tid; i < 64 * XS; i += 512) Xb0[i] = Xb1[Cfg::NBUF == 2 ? i : 0] = (T)0.0f;
   for (int i = tid; i < 64 * BS; i += 512) Bb0[i] = Bb1[Cfg::NBUF == 2 ? i : 0] = (T)0.0f;
-  for (int i = tid; i < 64 * CS; i += 512) Cb0[i] = Cb1[Cfg::NBUF == 2 ? i : 0] = (T)0.0f;
+  if constexpr (!STATE_ONLY)
+    for (int i = tid; i < 64 * CS; i += 512) Cb0[i] = Cb1[Cfg::NBUF == 2 ? i : 0] = (T)0.0f;
 
   // ---- state: S[m][jb] holds mode mo + m, rows n = 16 (nbo + jb) + 4 lg + r, column pc
   const int64_t sbase = ((int64_t)b * H + h) * (int64_t)p.Mall * N * Ps;
