@@ -110,12 +110,11 @@ __device__ __forceinline__ ChunkCtl chunk_controls(float dtv, float al, float la
 // E is the scale of the state (or adjoint) before this chunk's update, upd the
 // factor on the update (1/E_new, or 1 when the accumulators are folded back).
 // BLK (one block of a mode-block launch sequence): the weights are normalised over
-// the whole bank with the per-token log-normalizers lse_t[t * lse_st + {0, 1}].
+// the whole bank with the per-token log-normalizers that lgt carries (lane = token).
 template <int MP, int ROLE, int NT = 512, bool BLK = false>
-__device__ __forceinline__ int pair_weights(const ChunkCtl& k, int nv, int M, const PairLogits<MP, NT>& lgt,
+__device__ __forceinline__ int pair_weights(const ChunkCtl& k, int nv, int M, const PairLogits<MP, NT, BLK>& lgt,
                                             bool w_is_c, const float* s_rr, const float* s_lnt, const float* lh,
-                                            const float* ll, const float* Ecur, float* Enext, float* w,
-                                            const float* lse_t = nullptr, int64_t lse_st = 0) {
+                                            const float* ll, const float* Ecur, float* Enext, float* w) {
   const int tid = threadIdx.x;
 #pragma unroll
   for (int j = 0; j < lgt.NPR; ++j) {
@@ -130,9 +129,9 @@ __device__ __forceinline__ int pair_weights(const ChunkCtl& k, int nv, int M, co
     // tokens past the sequence get zero weights (their tile rows may hold anything finite)
     float cw, ww;
     if constexpr (BLK) {
-      const float2 ln = valid ? *reinterpret_cast<const float2*>(lse_t + (int64_t)t * lse_st) : float2{0.0f, 0.0f};
-      cw = valid ? __expf(zc - ln.x) : 0.0f;
-      ww = w_is_c ? cw : (valid ? __expf(zw - ln.y) : 0.0f);
+      const float lnc = __shfl(lgt.ln_c, t, 64), lnw = __shfl(lgt.ln_w, t, 64);
+      cw = valid ? __expf(zc - lnc) : 0.0f;
+      ww = w_is_c ? cw : (valid ? __expf(zw - lnw) : 0.0f);
     } else {
       cw = valid ? group_softmax<MP>(zc) : 0.0f;
       ww = w_is_c ? cw : (valid ? group_softmax<MP>(zw) : 0.0f);
@@ -418,14 +417,14 @@ __global__ void __launch_bounds__(512) frac_bwd_state_kernel(ScanParams p, BwdWo
   const float* wl_bh = p.write_logit ? p.write_logit + ((int64_t)b * L * H + h) * p.Mall : nullptr;
   const int64_t lg_st = (int64_t)H * p.Mall;
   const float* lse_bh = BLK ? p.lse + ((int64_t)b * L * H + h) * 2 : nullptr;  // [t][H][2]
-  PairLogits<MP, 512> lgt_n;  // the logits of the next chunk's weight pass
+  PairLogits<MP, 512, BLK> lgt_n;  // the logits (and normalizers) of the next chunk's weight pass
   auto load_controls = [&](int c, float& dtv, float& al, float& lam) {
     const int tg = c * kQ + lane;
     const bool valid = tg < L;
     dtv = valid ? dt_bh[(int64_t)tg * H] : 0.0f;
     al = valid ? al_bh[tg * p.as1] : 1.0f;
     lam = (valid && lm_bh) ? lm_bh[tg * p.ls1] : 1.0f;
-    lgt_n.load(rl_bh, wl_bh, c * kQ, min(kQ, L - c * kQ), M, lg_st, threadIdx.x);
+    lgt_n.load(rl_bh, wl_bh, c * kQ, min(kQ, L - c * kQ), M, lg_st, threadIdx.x, lse_bh, (int64_t)H * 2);
   };
   DmaPlan<T, XS> planX;
   DmaPlan<T, BS> planB;
@@ -469,8 +468,7 @@ __global__ void __launch_bounds__(512) frac_bwd_state_kernel(ScanParams p, BwdWo
     chunk_log_decays<MP, 8>(k.dtt, s_rr, lh, lh + SW);
     barrier();  // log-decays in LDS
     unsafe_c = pair_weights<MP, kState, 512, BLK>(k, nv, M, lgt_n, rl_bh == wl_bh, s_rr, s_lnt, lh, lh + SW,
-                                                  s_E2 + (c & 1) * MP, s_E2 + ((c + 1) & 1) * MP, Wd,
-                                                  BLK ? lse_bh + (int64_t)t0 * H * 2 : nullptr, (int64_t)H * 2);
+                                                  s_E2 + (c & 1) * MP, s_E2 + ((c + 1) & 1) * MP, Wd);
   };
   barrier();  // rates and scales in LDS
   if constexpr (NWB == 2) weights(0, W0);
@@ -904,14 +902,14 @@ __global__ void __launch_bounds__(512) frac_bwd_cols_kernel(ScanParams p, BwdWor
   const float* wl_bh = p.write_logit ? p.write_logit + ((int64_t)b * L * H + h) * p.Mall : nullptr;
   const int64_t lg_st = (int64_t)H * p.Mall;
   const float* lse_bh = BLK ? p.lse + ((int64_t)b * L * H + h) * 2 : nullptr;  // [t][H][2]
-  PairLogits<MP, 512> lgt_n;  // the logits of the next chunk's weight pass
+  PairLogits<MP, 512, BLK> lgt_n;  // the logits (and normalizers) of the next chunk's weight pass
   auto load_controls = [&](int c, float& dtv, float& al, float& lam) {
     const int tg = c * kQ + lane;
     const bool valid = tg < L;
     dtv = valid ? dt_bh[(int64_t)tg * H] : 0.0f;
     al = valid ? al_bh[tg * p.as1] : 1.0f;
     lam = (valid && lm_bh) ? lm_bh[tg * p.ls1] : 1.0f;
-    lgt_n.load(rl_bh, wl_bh, c * kQ, min(kQ, L - c * kQ), M, lg_st, threadIdx.x);
+    lgt_n.load(rl_bh, wl_bh, c * kQ, min(kQ, L - c * kQ), M, lg_st, threadIdx.x, lse_bh, (int64_t)H * 2);
   };
   DmaPlan<T, XS> planX;
   DmaPlan<T, CS> planC;
@@ -944,7 +942,7 @@ __global__ void __launch_bounds__(512) frac_bwd_cols_kernel(ScanParams p, BwdWor
     barrier();
     // this chunk's prefetched controls, logits and tile values, taken before any new memory operation
     const float dtv = pinned(dt_n), al_l = pinned(al_n), lam_l = pinned(lam_n);
-    const PairLogits<MP, 512> lgt = lgt_n.pinned_copy();
+    const PairLogits<MP, 512, BLK> lgt = lgt_n.pinned_copy();
     const TilePrefetch<T> hcur = hgt.pinned_copy();
     if (Cfg::NBUF == 2) {
       if (c > 0) stage(c - 1, Xn, Yn, Cn);
@@ -958,8 +956,7 @@ __global__ void __launch_bounds__(512) frac_bwd_cols_kernel(ScanParams p, BwdWor
     chunk_log_decays<MP, 8>(k.dtt, s_rr, P_lh, P_ll);
     barrier();  // log-decays in LDS
     const int unsafe = pair_weights<MP, kCols, 512, BLK>(k, nv, M, lgt, rl_bh == wl_bh, s_rr, s_lnt, P_lh, P_ll, Ecur,
-                                                         Enext, W, BLK ? lse_bh + (int64_t)t0 * H * 2 : nullptr,
-                                                         (int64_t)H * 2);
+                                                         Enext, W);
     float renf[MPF];
     int renbits = 0;
 #pragma unroll
@@ -1202,14 +1199,14 @@ __global__ void __launch_bounds__(512) frac_bwd_rows_kernel(ScanParams p, BwdWor
   const float* wl_bh = p.write_logit ? p.write_logit + ((int64_t)b * L * H + h) * p.Mall : nullptr;
   const int64_t lg_st = (int64_t)H * p.Mall;
   const float* lse_bh = BLK ? p.lse + ((int64_t)b * L * H + h) * 2 : nullptr;  // [t][H][2]
-  PairLogits<MP, 512> lgt_n;  // the logits of the next chunk's weight pass
+  PairLogits<MP, 512, BLK> lgt_n;  // the logits (and normalizers) of the next chunk's weight pass
   auto load_controls = [&](int c, float& dtv, float& al, float& lam) {
     const int tg = c * kQ + lane;
     const bool valid = tg < L;
     dtv = valid ? dt_bh[(int64_t)tg * H] : 0.0f;
     al = valid ? al_bh[tg * p.as1] : 1.0f;
     lam = (valid && lm_bh) ? lm_bh[tg * p.ls1] : 1.0f;
-    lgt_n.load(rl_bh, wl_bh, c * kQ, min(kQ, L - c * kQ), M, lg_st, threadIdx.x);
+    lgt_n.load(rl_bh, wl_bh, c * kQ, min(kQ, L - c * kQ), M, lg_st, threadIdx.x, lse_bh, (int64_t)H * 2);
   };
   DmaPlan<T, XS> planX;
   DmaPlan<T, BS> planB;
@@ -1262,7 +1259,7 @@ __global__ void __launch_bounds__(512) frac_bwd_rows_kernel(ScanParams p, BwdWor
     barrier();
     // this chunk's prefetched controls, logits and tile values, taken before any new memory operation
     const float dtv = pinned(dt_n), al_l = pinned(al_n), lam_l = pinned(lam_n);
-    const PairLogits<MP, 512> lgt = lgt_n.pinned_copy();
+    const PairLogits<MP, 512, BLK> lgt = lgt_n.pinned_copy();
     const TilePrefetch<T> gcur = ggt.pinned_copy();
     if (Cfg::kBf16 && i > 0 && !(BLK && p.y_part)) store_dx(c + 1);
     if (Cfg::NBUF == 2) {
@@ -1278,8 +1275,7 @@ __global__ void __launch_bounds__(512) frac_bwd_rows_kernel(ScanParams p, BwdWor
     chunk_log_decays<MP, 8>(k.dtt, s_rr, P_lh, P_ll);
     barrier();  // log-decays in LDS
     const int unsafe = pair_weights<MP, kRows, 512, BLK>(k, nv, M, lgt, rl_bh == wl_bh, s_rr, s_lnt, P_lh, P_ll, Ecur,
-                                                         Enext, W, BLK ? lse_bh + (int64_t)t0 * H * 2 : nullptr,
-                                                         (int64_t)H * 2);
+                                                         Enext, W);
     float renf[MPW];
     int renbits = 0;
 #pragma unroll
@@ -1584,14 +1580,14 @@ __global__ void __launch_bounds__(256) frac_bwd_intra_kernel(ScanParams p, const
   const ChunkCtl k = chunk_controls(dtv, al, lam, p.lambda != nullptr, nv);
   const float* rl_bh = p.read_logit ? p.read_logit + ((int64_t)b * L * H + h) * p.Mall : nullptr;
   const float* wl_bh = p.write_logit ? p.write_logit + ((int64_t)b * L * H + h) * p.Mall : nullptr;
-  PairLogits<MP, 256> lgt;
-  lgt.load(rl_bh, wl_bh, t0, nv, M, (int64_t)H * p.Mall, tid);
-  const float* lse_c = BLK ? p.lse + (((int64_t)b * L + t0) * H + h) * 2 : nullptr;
+  PairLogits<MP, 256, BLK> lgt;
+  lgt.load(rl_bh, wl_bh, t0, nv, M, (int64_t)H * p.Mall, tid, BLK ? p.lse + ((int64_t)b * L * H + h) * 2 : nullptr,
+           (int64_t)H * 2);
   __syncthreads();  // rates, zeroed H, x and dy in LDS
   chunk_log_decays<MP, 4>(k.dtt, s_rr, P_lh, P_ll);
   __syncthreads();  // log-decays in LDS
   const int unsafe = pair_weights<MP, kIntra, 256, BLK>(k, nv, M, lgt, rl_bh == wl_bh, s_rr, s_lnt, P_lh, P_ll,
-                                                        nullptr, nullptr, W, lse_c, (int64_t)H * 2);
+                                                        nullptr, nullptr, W);
   // ---- H = (C B^T) o (dY X^T), causal tiles [t][k]
   const T* gt = gtiles + (((int64_t)b * nchunks + c) * G + g) * (kTiles * kTileElems);
   for (int tile = wave; tile < kTiles; tile += 4) {

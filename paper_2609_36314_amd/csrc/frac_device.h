@@ -25,12 +25,6 @@ constexpr int kWQ = kQ + 4;
 __device__ __forceinline__ int tile_row(int tile) { return (tile >= 1) + (tile >= 3) + (tile >= 6); }
 __device__ __forceinline__ int tile_col(int tile) { const int tb = tile_row(tile); return tile - tb * (tb + 1) / 2; }
 
-// The read / write logits of the (token, mode) pairs that a thread of an NT-thread
-// workgroup forms in a chunk's weight pass (pair = t MP + m = tid + NT j), loaded
-// one chunk ahead into registers: the weight pass then never waits on global
-// memory (a wait there would also drain the next chunk's tile copies).  Zero for
-// pairs past the chunk, absent logits, and wl when the write logits are the read
-// logits (the weight pass reuses the read weights then).
 // A value fixed in a register at this point.  A prefetched register read after
 // later memory operations have been issued makes the wave wait for those too (the
 // vector-memory counter drains in order, and direct-to-LDS copies are not tracked
@@ -41,12 +35,21 @@ __device__ __forceinline__ float pinned(float v) {
   return v;
 }
 
-template <int MP, int NT>
+// The read / write logits of the (token, mode) pairs that a thread of an NT-thread
+// workgroup forms in a chunk's weight pass (pair = t MP + m = tid + NT j), loaded
+// one chunk ahead into registers: the weight pass then never waits on global
+// memory (a wait there would also drain the next chunk's tile copies).  Zero for
+// pairs past the chunk, absent logits, and wl when the write logits are the read
+// logits (the weight pass reuses the read weights then).
+// LSE (a mode block): also the two per-token log-normalizers lse[t * lse_st + {0, 1}],
+// lane = token, which the weight pass takes with a lane shuffle.
+template <int MP, int NT, bool LSE = false>
 struct PairLogits {
   static constexpr int NPR = (kQ * MP + NT - 1) / NT;
   float rl[NPR], wl[NPR];
+  float ln_c = 0.0f, ln_w = 0.0f;
   __device__ __forceinline__ void load(const float* rlp, const float* wlp, int t0, int nv, int M, int64_t stride,
-                                       int tid) {
+                                       int tid, const float* lse = nullptr, int64_t lse_st = 0) {
 #pragma unroll
     for (int j = 0; j < NPR; ++j) {
       const int pr = tid + NT * j, t = pr / MP, m = pr - t * MP;
@@ -55,6 +58,12 @@ struct PairLogits {
       rl[j] = (ok && rlp) ? rlp[i] : 0.0f;
       wl[j] = (ok && wlp && wlp != rlp) ? wlp[i] : 0.0f;
     }
+    if constexpr (LSE) {
+      const int tl = tid & 63;
+      const float2 v = tl < nv ? *reinterpret_cast<const float2*>(lse + (int64_t)(t0 + tl) * lse_st) : float2{0.0f, 0.0f};
+      ln_c = v.x;
+      ln_w = v.y;
+    }
   }
   __device__ __forceinline__ PairLogits pinned_copy() const {
     PairLogits o;
@@ -62,6 +71,10 @@ struct PairLogits {
     for (int j = 0; j < NPR; ++j) {
       o.rl[j] = pinned(rl[j]);
       o.wl[j] = pinned(wl[j]);
+    }
+    if constexpr (LSE) {
+      o.ln_c = pinned(ln_c);
+      o.ln_w = pinned(ln_w);
     }
     return o;
   }

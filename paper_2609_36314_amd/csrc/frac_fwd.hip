@@ -294,14 +294,14 @@ __global__ void __launch_bounds__(512, STATE_ONLY ? 4 : 1) frac_fwd_kernel(ScanP
   const bool w_is_c = wl_bh == rl_bh;  // then the write weights equal the read weights
   const int64_t lg_st = (int64_t)H * p.Mall;
   const float* lse_bh = BLK ? p.lse + ((int64_t)b * L * H + h) * 2 : nullptr;  // [t][H][2]
-  PairLogits<MP, 512> lgt_n;  // the logits of the next chunk's weight pass
+  PairLogits<MP, 512, BLK> lgt_n;  // the logits (and normalizers) of the next chunk's weight pass
   auto load_controls = [&](int c, float& dtv, float& al, float& lam) {
     const int tg = c * kQ + lane;
     const bool valid = tg < T1;
     dtv = valid ? dt_bh[(int64_t)tg * H] : 0.0f;
     al = valid ? al_bh[tg * al_st] : 1.0f;
     lam = (valid && lm_bh) ? lm_bh[tg * lm_st] : 1.0f;
-    lgt_n.load(rl_bh, wl_bh, c * kQ, min(kQ, T1 - c * kQ), M, lg_st, tid);
+    lgt_n.load(rl_bh, wl_bh, c * kQ, min(kQ, T1 - c * kQ), M, lg_st, tid, lse_bh, (int64_t)H * 2);
   };
   DmaPlan<T, XS> planX;
   DmaPlan<T, BS> planB;
@@ -348,7 +348,7 @@ __global__ void __launch_bounds__(512, STATE_ONLY ? 4 : 1) frac_fwd_kernel(ScanP
     barrier();  // this chunk's tiles have landed; every wave is done with the previous chunk
     // this chunk's prefetched controls, logits and C B^T values, taken before any new memory operation
     const float dtv = pinned(dt_n), al_l = pinned(al_n), lam_l = pinned(lam_n);
-    const PairLogits<MP, 512> lgt = lgt_n.pinned_copy();
+    const PairLogits<MP, 512, BLK> lgt = lgt_n.pinned_copy();
     const TilePrefetch<T> gcur = gtile.pinned_copy();
     if (!STATE_ONLY && c > c0 && !(BLK && p.y_part)) store_y(c - 1);
     if (Cfg::NBUF == 2) {
@@ -391,9 +391,8 @@ __global__ void __launch_bounds__(512, STATE_ONLY ? 4 : 1) frac_fwd_kernel(ScanP
       if constexpr (STATE_ONLY) {  // the state update only: the write weights
         float ww;
         if constexpr (BLK) {
-          const float2 ln = valid ? *reinterpret_cast<const float2*>(lse_bh + (int64_t)(t0 + t) * H * 2)
-                                  : float2{0.0f, 0.0f};
-          ww = valid ? __expf((w_is_c ? zc : zw) - (w_is_c ? ln.x : ln.y)) : 0.0f;
+          const float ln = w_is_c ? __shfl(lgt.ln_c, t, 64) : __shfl(lgt.ln_w, t, 64);
+          ww = valid ? __expf((w_is_c ? zc : zw) - ln) : 0.0f;
         } else {
           ww = valid ? group_softmax<MP>(w_is_c ? zc : zw) : 0.0f;
         }
@@ -402,10 +401,9 @@ __global__ void __launch_bounds__(512, STATE_ONLY ? 4 : 1) frac_fwd_kernel(ScanP
       } else {
         float cw, ww;
         if constexpr (BLK) {
-          const float2 ln = valid ? *reinterpret_cast<const float2*>(lse_bh + (int64_t)(t0 + t) * H * 2)
-                                  : float2{0.0f, 0.0f};
-          cw = valid ? __expf(zc - ln.x) : 0.0f;
-          ww = w_is_c ? cw : (valid ? __expf(zw - ln.y) : 0.0f);
+          const float lnc = __shfl(lgt.ln_c, t, 64), lnw = __shfl(lgt.ln_w, t, 64);
+          cw = valid ? __expf(zc - lnc) : 0.0f;
+          ww = w_is_c ? cw : (valid ? __expf(zw - lnw) : 0.0f);
         } else {
           cw = valid ? group_softmax<MP>(zc) : 0.0f;
           ww = w_is_c ? cw : (valid ? group_softmax<MP>(zw) : 0.0f);
