@@ -47,8 +47,8 @@ PEAK_HBM_BYTES = 8.0e12      # MI355X HBM3E
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workloads", default="train-b4-l4096-m8,layer-fwd-b8-l2048,prefill-b1-l16384,train-b4-l4096-m16,"
                                            "paper-nfree-b8-l2048,paper-nfree-train-b8-l2048,decode-b256-128steps,"
                                            "paper-nfree-decode-b2048-128steps")
