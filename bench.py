@@ -254,6 +254,7 @@ def bench_scan(torch, frac, w, steps, warmup, extras=True):
     wall = time.perf_counter() - t0
     fms = float(np.mean(tf.ms()))
     bms = float(np.mean(tb.ms())) if w.backward else 0.0
+    spread = lambda v: {"min": float(np.min(v)), "median": float(np.median(v)), "max": float(np.max(v))}
     tokens = w.batch * w.seqlen
     step_ms = wall * 1e3 / steps
     th = tokens * w.nheads
@@ -262,8 +263,11 @@ def bench_scan(torch, frac, w, steps, warmup, extras=True):
         "tokens_per_s": tokens / (step_ms * 1e-3),
         "ms_per_step": step_ms,
         "fwd_ms": fms,
+        "fwd_ms_spread": spread(tf.ms()),
         "fwd_roofline": roofline("mfma", th * fwd_flops_per_token_head(w), fms, peak, "TFLOP/s"),
     }
+    if w.backward:  # per-step spread of the timed launches: a one-off stall shows as max >> median
+        res["bwd_ms_spread"] = spread(tb.ms())
     if not w.bc:  # without B/C the forward moves more bytes than it does matrix-core work
         res["fwd_roofline"] = roofline("hbm", nfree_fwd_bytes(w), fms, PEAK_HBM_BYTES, "GB/s")
     if w.backward and not w.bc:
