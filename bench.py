@@ -25,6 +25,7 @@ slice of the same workload on the host cores.
 from __future__ import annotations
 
 import argparse
+import gc
 import glob
 import hashlib
 import json
@@ -524,6 +525,11 @@ def main():
         dst.copy_(src)
         torch.cuda.synchronize()
         del src, dst
+    # Python's cyclic garbage collector stays off while the GPU is timed: a full collection
+    # (tens of ms with torch loaded) inside a timed launch group leaves the GPU idle and is
+    # counted as GPU time.  Objects made per step are freed by reference counting.
+    gc.collect()
+    gc.disable()
     mp = None if args.no_measured_peaks else measured_peaks(torch)
     names = [n for n in args.workloads.split(",") if n]
     results = {}
@@ -539,6 +545,7 @@ def main():
         print("# %s: %s" % (n, json.dumps(results[n])), file=sys.stderr, flush=True)
         torch.cuda.empty_cache()
 
+    gc.enable()
     main_w = WORKLOADS[args.main]
     mres = results.get(args.main)
     line = {
