@@ -554,14 +554,23 @@ __global__ void __launch_bounds__(512, STATE_ONLY ? 4 : 1) frac_fwd_kernel(ScanP
       float xv[4];
       col4_rows(Xc, XS, tb * 16 + lg * 4, pb * 16, xv);
       if constexpr (BLK) {  // a mode block: float32 partial sums across the blocks
+        // one 64-bit base per row block and 32-bit row offsets (per-element 64-bit
+        // indices spilled 32 registers here); the four loads issue before any is used
+        const int64_t y0 = (((int64_t)b * L + t0 + tb * 16 + lg * 4) * H + h) * Ps + pc;
+        const int rs = H * Ps;
+        const float* yq = p.y_in;
+        float* yp = p.y_part;
+        float yv[4];
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int tr = tb * 16 + lg * 4 + r;
-          const int64_t yi = (((int64_t)b * L + t0 + tr) * H + h) * Ps + pc;
-          if (tr < nv && pc < P) {
-            if (p.y_in) Y[tb][r] += p.y_in[yi];
-            if (p.y_part) p.y_part[yi] = Y[tb][r];
-          }
+          yv[r] = (yq && tr < nv && pc < P) ? yq[y0 + r * rs] : 0.0f;
+        }
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int tr = tb * 16 + lg * 4 + r;
+          Y[tb][r] += yv[r];
+          if (yp && tr < nv && pc < P) yp[y0 + r * rs] = Y[tb][r];
         }
       }
       if (!(BLK && p.y_part)) {
