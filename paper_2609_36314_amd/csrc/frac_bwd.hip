@@ -1389,7 +1389,9 @@ __global__ void __launch_bounds__(512) frac_bwd_rows_kernel(ScanParams p, BwdWor
       load4(Yc + t * XS + pr, yv);
       floatx4 v = dxa[tb];
       if constexpr (BLK) {  // a mode block: float32 partial sums across the blocks
-        const int64_t xi = (((int64_t)b * L + t0 + t) * H + h) * Ps + pr;
+        // a wave-uniform 64-bit base and a 32-bit lane offset: a per-lane 64-bit index
+        // spilled here and its reload waited on every outstanding copy
+        const int64_t xi = (((int64_t)b * L + t0) * H + h) * Ps + (int64_t)(t * H * Ps + pr);
         if (t < nv && pr < P) {
           if (p.y_in) {
             const float4 u = *reinterpret_cast<const float4*>(p.y_in + xi);
