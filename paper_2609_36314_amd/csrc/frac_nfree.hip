@@ -13,9 +13,10 @@
 // of the capped exponents r_m dtt, in float64; frac_device.h), exact for any mix of
 // effective steps in a chunk.
 //
-// One workgroup of 4 waves per (batch, head, 64 columns of d_h); wave w owns
-// columns 16 w .. 16 w + 15 and the state of all modes for them (at most two
-// 16x16 float32 accumulator tiles, modes as rows).  Per chunk: x copied into LDS,
+// One workgroup of NW waves per (batch, head, 16 NW columns of d_h): 8 waves and
+// 128 columns for head dims above 128, else 4 and 64; wave w owns columns
+// 16 w .. 16 w + 15 and the state of all modes for them (at most two 16x16
+// float32 accumulator tiles, modes as rows).  Per chunk: x copied into LDS,
 // per-(token, mode) weights, Gamma in causal 16x16 tiles (float32 matrix cores,
 // modes as K; one exponential per pair for modes whose chunk decay passes the
 // factorisation bound), then the readout (weights x state, K = modes), the
@@ -34,21 +35,26 @@ constexpr float kNfFloor = 0x1p-60f;
 
 // CKPT: no outputs; the state entering every chunk, and the final state, go to
 // ckpt [B H][nchunks + 1][M][P] (the first pass of the backward).
-template <typename T, int MP, bool CKPT>
-__global__ void __launch_bounds__(256) frac_nfree_fwd_kernel(ScanParams p, float* __restrict__ ckpt) {
+// NW waves per workgroup, 16 NW columns of d_h: with more waves per workgroup the
+// per-chunk work that does not depend on the columns (the log-decays, the weights,
+// the Gamma tiles) is done once for more columns and split over more waves.
+template <typename T, int MP, bool CKPT, int NW = 4>
+__global__ void __launch_bounds__(64 * NW) frac_nfree_fwd_kernel(ScanParams p, float* __restrict__ ckpt) {
   constexpr bool kBf16 = sizeof(T) == 2;
   constexpr int MB = (MP + 15) / 16;        // 16-row blocks of modes in the state
-  constexpr int XS = kBf16 ? 64 + 8 : 64 + 4;  // [t][p] and [t][k] tile strides
+  constexpr int NT = 64 * NW, CW = 16 * NW;  // threads, columns of d_h per workgroup
+  constexpr int XS = kBf16 ? CW + 8 : CW + 4;  // [t][p] tile stride
+  constexpr int GS = kBf16 ? 64 + 8 : 64 + 4;  // [t][k] tile stride
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, li = lane & 15, lg = lane >> 4;
   const int L = p.L, H = p.H, P = p.P, M = p.M;
-  const int nps = (P + 63) / 64;
+  const int nps = (P + CW - 1) / CW;
   const int ps = blockIdx.x % nps, bh = blockIdx.x / nps, b = bh / H, h = bh - b * H;
-  const int p0 = ps * 64, pc = p0 + wave * 16 + li;  // this lane's column of d_h
+  const int p0 = ps * CW, pc = p0 + wave * 16 + li;  // this lane's column of d_h
   const bool active = p0 + wave * 16 < P;
   const int nchunks = (L + kQ - 1) / kQ;
 
   __shared__ __align__(16) T Xs[64 * XS];  // x of the chunk [t][p]
-  __shared__ __align__(16) T Gs[64 * XS];  // causal Gamma [t][k]
+  __shared__ __align__(16) T Gs[64 * GS];  // causal Gamma [t][k]
   __shared__ __align__(16) T Ys[64 * XS];  // output rows [t][p]
   // per-token weight arrays [MP][WQ]: the row stride of 68 floats spreads the
   // stores of one wave (4 tokens x 16 modes, or 8 x 8) over distinct LDS banks
@@ -65,7 +71,7 @@ __global__ void __launch_bounds__(256) frac_nfree_fwd_kernel(ScanParams p, float
   float* P_ll = W + 7 * MP * WQ;
 
   // Gamma tiles above the diagonal that the intra product reads are never written
-  for (int i = tid; i < 64 * XS; i += 256) Gs[i] = (T)0.0f;
+  for (int i = tid; i < 64 * GS; i += NT) Gs[i] = (T)0.0f;
   if (tid < MP) {
     const float tau = (tid < M) ? p.tau[tid] : 1.0f;
     s_rr[tid] = (tid < M) ? 1.0f / tau : 0.0f;
@@ -94,19 +100,19 @@ __global__ void __launch_bounds__(256) frac_nfree_fwd_kernel(ScanParams p, float
   const float* wl_bh = p.write_logit ? p.write_logit + ((int64_t)b * L * H + h) * M : nullptr;
   const int64_t lg_st = (int64_t)H * M;
   constexpr int E16 = 16 / (int)sizeof(T);  // elements per 16-byte vector
-  constexpr int CPR = 64 / E16;             // 16-byte vectors per 64-column row
-  constexpr int XV = 64 * CPR / 256;        // 16-byte vectors of x per thread and chunk
+  constexpr int CPR = CW / E16;             // 16-byte vectors per row of this workgroup's columns
+  constexpr int XV = 64 * CPR / NT;         // 16-byte vectors of x per thread and chunk
 
   // x and the per-token controls of a chunk, loaded one chunk ahead into registers
   int4 xr[XV];
   float dt_n, al_n, lam_n;
-  constexpr int NPR = kQ * MP / 256;  // (token, mode) pairs per thread: pair = t MP + m = tid + 256 j
+  constexpr int NPR = (kQ * MP + NT - 1) / NT;  // (token, mode) pairs per thread: pair = t MP + m = tid + NT j
   float rlr[NPR], wlr[NPR];           // the read / write logits of this thread's pairs
   auto prefetch = [&](int c) {
     const int t0 = c * kQ, nv = min(kQ, L - t0);
 #pragma unroll
     for (int j = 0; j < XV; ++j) {
-      const int i = tid + 256 * j, t = i / CPR, col = (i - t * CPR) * E16;
+      const int i = tid + NT * j, t = i / CPR, col = (i - t * CPR) * E16;
       xr[j] = make_int4(0, 0, 0, 0);
       if (t < nv && p0 + col < P) xr[j] = *reinterpret_cast<const int4*>(xg + (int64_t)(t0 + t) * xstride + col);
     }
@@ -117,8 +123,8 @@ __global__ void __launch_bounds__(256) frac_nfree_fwd_kernel(ScanParams p, float
     lam_n = (tvalid && lm_bh) ? lm_bh[tg * p.ls1] : 1.0f;
 #pragma unroll
     for (int j = 0; j < NPR; ++j) {
-      const int pr = tid + 256 * j, t = pr / MP, m = pr - t * MP;
-      const bool ok = t < nv && m < M;
+      const int pr = tid + NT * j, t = pr / MP, m = pr - t * MP;
+      const bool ok = pr < kQ * MP && t < nv && m < M;
       const int64_t ith = (int64_t)(t0 + t) * lg_st + m;
       rlr[j] = (ok && rl_bh) ? rl_bh[ith] : 0.0f;
       wlr[j] = (ok && wl_bh && wl_bh != rl_bh) ? wl_bh[ith] : 0.0f;  // unused when the two are one array
@@ -134,7 +140,7 @@ __global__ void __launch_bounds__(256) frac_nfree_fwd_kernel(ScanParams p, float
     // ---- x of the chunk into LDS (zeros past the sequence and past d_h)
 #pragma unroll
     for (int j = 0; j < XV; ++j) {
-      const int i = tid + 256 * j, t = i / CPR, col = (i - t * CPR) * E16;
+      const int i = tid + NT * j, t = i / CPR, col = (i - t * CPR) * E16;
       *reinterpret_cast<int4*>(Xs + t * XS + col) = xr[j];
     }
     const bool tvalid = lane < nv;
@@ -152,14 +158,15 @@ __global__ void __launch_bounds__(256) frac_nfree_fwd_kernel(ScanParams p, float
     // ---- per-token controls (lane = token, every wave) and the per-mode log-decays
     const float s_eff = lm_bh ? step_factor(lam, al_l) : 1.0f;
     const float dtt_l = tvalid ? dtv * s_eff : 0.0f;
-    chunk_log_decays<MP, 4>(dtt_l, s_rr, P_lh, P_ll);
+    chunk_log_decays<MP, NW>(dtt_l, s_rr, P_lh, P_ll);
     barrier();  // log-decays in LDS
     const bool over = lane < MP && lane < M && !(P_lh[(lane < MP ? lane : 0) * WQ + kQ - 1] <= kNfSafe);
     const int unsafe = (int)(__ballot(over) & ((MP >= 32) ? 0xffffffffull : ((1ull << MP) - 1)));
     // ---- per (token, mode) weights: pair = t MP + m
 #pragma unroll
     for (int j = 0; j < NPR; ++j) {
-      const int pr = tid + 256 * j, t = pr / MP, m = pr - t * MP;
+      const int pr = tid + NT * j, t = pr / MP, m = pr - t * MP;
+      if (pr >= kQ * MP) break;  // wave-uniform
       const float dtt = __shfl(dtt_l, t, 64), al = __shfl(al_l, t, 64);
       const bool valid = t < nv;
       const float r = s_rr[m], prior = -al * s_lnt[m];
@@ -205,7 +212,7 @@ __global__ void __launch_bounds__(256) frac_nfree_fwd_kernel(ScanParams p, float
 
     if constexpr (!CKPT) {
     // ---- causal Gamma tiles [t][k] (float32 matrix cores, modes as K)
-    for (int tile = wave; tile < 10; tile += 4) {
+    for (int tile = wave; tile < 10; tile += NW) {
       const int tb = tile_row(tile), kb = tile_col(tile);
       floatx4 Gm = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
@@ -228,7 +235,7 @@ __global__ void __launch_bounds__(256) frac_nfree_fwd_kernel(ScanParams p, float
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int t = tb * 16 + lg * 4 + r, k = kb * 16 + li;
-        Gs[t * XS + k] = (T)keep_if_ge(Gm[r], t, k);
+        Gs[t * GS + k] = (T)keep_if_ge(Gm[r], t, k);
       }
     }
     barrier();  // Gamma in LDS
@@ -256,7 +263,7 @@ __global__ void __launch_bounds__(256) frac_nfree_fwd_kernel(ScanParams p, float
         mma(Y, Of, Sf);
 #pragma unroll
         for (int kk = 0; kk <= tb / 2; ++kk) {
-          const Frag<T> a = frag_load8(Gs + t * XS + kk * 32 + lg * 8);
+          const Frag<T> a = frag_load8(Gs + t * GS + kk * 32 + lg * 8);
           const Frag<T> bx = frag_load_rows(Xs, XS, kk * 32 + lg * 8, wave * 16);
           mma(Y, a, bx);
         }
@@ -304,7 +311,7 @@ __global__ void __launch_bounds__(256) frac_nfree_fwd_kernel(ScanParams p, float
     if constexpr (CKPT) continue;
     barrier();  // output rows in LDS
     // ---- output rows -> global, 16 bytes per thread
-    for (int i = tid; i < 64 * CPR; i += 256) {
+    for (int i = tid; i < 64 * CPR; i += NT) {
       const int t = i / CPR, ch = i - t * CPR, col = ch * E16;
       if (t < nv && p0 + col < P)
         *reinterpret_cast<int4*>(yg + (int64_t)(t0 + t) * xstride + col) = *reinterpret_cast<const int4*>(Ys + t * XS + col);
@@ -794,14 +801,27 @@ __global__ void __launch_bounds__(256, 2) frac_nfree_bwd_kernel(ScanParams p, Nf
   }
 }
 
+// The forward pass (CKPT: the checkpoint pass of the backward) in workgroups of NW
+// waves: 8 (128 columns) for head dims above 128, else 4 (64 columns).
+template <typename T, int MP, bool CKPT, int NW>
+hipError_t launch_nfree_fwd_nw(const ScanParams& p, float* ckpt, hipStream_t stream) {
+  const unsigned blocks = (unsigned)((int64_t)p.Bsz * p.H * ((p.P + 16 * NW - 1) / (16 * NW)));
+  hipLaunchKernelGGL((frac_nfree_fwd_kernel<T, MP, CKPT, NW>), dim3(blocks), dim3(64 * NW), 0, stream, p, ckpt);
+  return hipGetLastError();
+}
+
+template <typename T, int MP, bool CKPT>
+hipError_t launch_nfree_fwd(const ScanParams& p, float* ckpt, hipStream_t stream) {
+  return p.P > 128 ? launch_nfree_fwd_nw<T, MP, CKPT, 8>(p, ckpt, stream)
+                   : launch_nfree_fwd_nw<T, MP, CKPT, 4>(p, ckpt, stream);
+}
+
 template <typename T>
 hipError_t launch_nfree_t(const ScanParams& p, hipStream_t stream) {
-  const unsigned blocks = (unsigned)((int64_t)p.Bsz * p.H * ((p.P + 63) / 64));
-  if (p.M <= 4) hipLaunchKernelGGL((frac_nfree_fwd_kernel<T, 4, false>), dim3(blocks), dim3(256), 0, stream, p, nullptr);
-  else if (p.M <= 8) hipLaunchKernelGGL((frac_nfree_fwd_kernel<T, 8, false>), dim3(blocks), dim3(256), 0, stream, p, nullptr);
-  else if (p.M <= 16) hipLaunchKernelGGL((frac_nfree_fwd_kernel<T, 16, false>), dim3(blocks), dim3(256), 0, stream, p, nullptr);
-  else hipLaunchKernelGGL((frac_nfree_fwd_kernel<T, 32, false>), dim3(blocks), dim3(256), 0, stream, p, nullptr);
-  return hipGetLastError();
+  if (p.M <= 4) return launch_nfree_fwd<T, 4, false>(p, nullptr, stream);
+  if (p.M <= 8) return launch_nfree_fwd<T, 8, false>(p, nullptr, stream);
+  if (p.M <= 16) return launch_nfree_fwd<T, 16, false>(p, nullptr, stream);
+  return launch_nfree_fwd<T, 32, false>(p, nullptr, stream);
 }
 
 struct NfLayout {
@@ -837,9 +857,7 @@ hipError_t launch_nfree_bwd_mp(const ScanParams& p, void* ws, hipStream_t stream
   wk.dkp = reinterpret_cast<float*>(base + l.dkp);
   wk.dkip = reinterpret_cast<float*>(base + l.dkip);
   const unsigned blocks = (unsigned)((int64_t)p.Bsz * p.H * ((p.P + 63) / 64));
-  hipLaunchKernelGGL((frac_nfree_fwd_kernel<T, MP, true>), dim3(blocks), dim3(256), 0, stream, p,
-                     reinterpret_cast<float*>(base + l.ckpt));
-  hipError_t e = hipGetLastError();
+  hipError_t e = launch_nfree_fwd<T, MP, true>(p, reinterpret_cast<float*>(base + l.ckpt), stream);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL((frac_nfree_bwd_kernel<T, MP>), dim3(blocks), dim3(256), 0, stream, p, wk);
   if ((e = hipGetLastError()) != hipSuccess) return e;
