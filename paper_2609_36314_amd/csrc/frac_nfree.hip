@@ -358,32 +358,48 @@ struct NfWork {
   float* dkip;        // [nps][B H L][M] its part through the chunk's own readouts
 };
 
-template <typename T, int MP>
-__global__ void __launch_bounds__(256, 2) frac_nfree_bwd_kernel(ScanParams p, NfWork wk) {
+// NW waves per workgroup over 16 NW columns of d_h, as the forward.  With 8 waves
+// the per-token products and partials of row block tb are split: waves tb form
+// S0 . dy and dc, waves 4 + tb form G . x, dk and the intra dk.
+template <typename T, int MP, int NW = 4>
+__global__ void __launch_bounds__(64 * NW, NW == 4 ? 2 : 1) frac_nfree_bwd_kernel(ScanParams p, NfWork wk) {
   constexpr bool kBf16 = sizeof(T) == 2;
   constexpr int MB = (MP + 15) / 16;
-  constexpr int XS = kBf16 ? 64 + 8 : 64 + 4;
+  constexpr int NT = 64 * NW, CW = 16 * NW;    // threads, columns of d_h per workgroup
+  constexpr int XS = kBf16 ? CW + 8 : CW + 4;  // [t][p] tile stride
+  constexpr int GS = kBf16 ? 64 + 8 : 64 + 4;  // [t][t'] tile stride
+  constexpr int GQ = CW + 4;                   // row stride of the adjoint [m][p]
+  constexpr int KP = CW / 32;                  // 32-column K steps over this workgroup's columns
+  constexpr bool kSplit = NW == 8;
   constexpr int WQ = kWQ;
   constexpr int NWA = 6;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, li = lane & 15, lg = lane >> 4;
   const int L = p.L, H = p.H, P = p.P, M = p.M;
-  const int nps = (P + 63) / 64;
+  const int nps = (P + CW - 1) / CW;
   const int ps = blockIdx.x % nps, bh = blockIdx.x / nps, b = bh / H, h = bh - b * H;
-  const int p0 = ps * 64, pc = p0 + wave * 16 + li;
+  const int p0 = ps * CW, pc = p0 + wave * 16 + li;
   const bool active = p0 + wave * 16 < P;
   const int nchunks = (L + kQ - 1) / kQ;
+  const bool doU = !kSplit || wave < 4, doZ = !kSplit || wave >= 4;  // this wave's per-token products
 
   __shared__ __align__(16) T Xs[64 * XS];                      // x [t][p]
   __shared__ __align__(16) T Ys[64 * XS];                      // dy [t][p]
-  __shared__ __align__(16) T GT[64 * XS];                      // Gamma^T [t][t'], t' >= t
+  __shared__ __align__(16) T GT[64 * GS];                      // Gamma^T [t][t'], t' >= t
   constexpr int HS = 64 + 4;
   __shared__ __align__(16) float HT[64 * HS];                  // dY X^T [t][k], k <= t (float32)
   T* const DX = Xs;  // dx rows [t][p] (bfloat16 staging; x is no longer read by then)
-  __shared__ __align__(16) float Gt[MP * WQ];                  // the adjoint [m][p]
+  __shared__ __align__(16) float Gt[MP * GQ];                  // the adjoint [m][p]
   __shared__ __align__(16) float W[NWA * MP * WQ];
   __shared__ float s_rr[MP], s_lnt[MP];
-  __shared__ float red[4][MP > 64 ? MP : 64];
-  __shared__ float redD[256];
+  __shared__ float red[NW][MP > 64 ? MP : 64];
+  __shared__ float redD[NT];
+  // a sum of the waves' partials, in wave order
+  auto red_sum = [&](int m) {
+    float v = red[0][m];
+#pragma unroll
+    for (int w = 1; w < NW; ++w) v += red[w][m];
+    return v;
+  };
   constexpr int SW = MP * WQ;
   float* P_O = W;             // c e^{-l}
   float* P_Vt = W + 1 * SW;   // kappa e^{l} (safe modes), kappa (modes past the factorisation bound)
@@ -392,8 +408,8 @@ __global__ void __launch_bounds__(256, 2) frac_nfree_bwd_kernel(ScanParams p, Nf
   float* P_lh = W + 4 * SW;   // chunk log-decays, hi and lo parts
   float* P_ll = W + 5 * SW;
 
-  for (int i = tid; i < 64 * XS; i += 256) GT[i] = (T)0.0f;
-  for (int i = tid; i < 64 * HS; i += 256) HT[i] = 0.0f;
+  for (int i = tid; i < 64 * GS; i += NT) GT[i] = (T)0.0f;
+  for (int i = tid; i < 64 * HS; i += NT) HT[i] = 0.0f;
   if (tid < MP) {
     const float tau = (tid < M) ? p.tau[tid] : 1.0f;
     s_rr[tid] = (tid < M) ? 1.0f / tau : 0.0f;
@@ -429,7 +445,7 @@ __global__ void __launch_bounds__(256, 2) frac_nfree_bwd_kernel(ScanParams p, Nf
       if (li == 0 && m < MP) red[wave][m] = v;
     }
   __syncthreads();
-  if (tid < MP && tid < M) wk.F[((int64_t)ps * p.Bsz * H + bh) * M + tid] = ((red[0][tid] + red[1][tid]) + red[2][tid]) + red[3][tid];
+  if (tid < MP && tid < M) wk.F[((int64_t)ps * p.Bsz * H + bh) * M + tid] = red_sum(tid);
   const float Dh = p.D ? p.D[h] : 0.0f;
   float dd_acc = 0.0f;
 
@@ -444,18 +460,18 @@ __global__ void __launch_bounds__(256, 2) frac_nfree_bwd_kernel(ScanParams p, Nf
   const float* wl_bh = p.write_logit ? p.write_logit + ((int64_t)b * L * H + h) * M : nullptr;
   const int64_t lg_st = (int64_t)H * M;
   constexpr int E16 = 16 / (int)sizeof(T);
-  constexpr int CPR = 64 / E16;
-  constexpr int XV = 64 * CPR / 256;
+  constexpr int CPR = CW / E16;
+  constexpr int XV = 64 * CPR / NT;
 
   int4 xr[XV], yr[XV];
   float dt_n, al_n, lam_n;
-  constexpr int NPR = kQ * MP / 256;  // (token, mode) pairs per thread: pair = t MP + m = tid + 256 j
+  constexpr int NPR = (kQ * MP + NT - 1) / NT;  // (token, mode) pairs per thread: pair = t MP + m = tid + NT j
   float rlr[NPR], wlr[NPR];           // the read / write logits of this thread's pairs
   auto prefetch = [&](int c) {
     const int t0 = c * kQ, nv = min(kQ, L - t0);
 #pragma unroll
     for (int j = 0; j < XV; ++j) {
-      const int i = tid + 256 * j, t = i / CPR, col = (i - t * CPR) * E16;
+      const int i = tid + NT * j, t = i / CPR, col = (i - t * CPR) * E16;
       xr[j] = yr[j] = make_int4(0, 0, 0, 0);
       if (t < nv && p0 + col < P) {
         xr[j] = *reinterpret_cast<const int4*>(xg + (int64_t)(t0 + t) * xstride + col);
@@ -469,8 +485,8 @@ __global__ void __launch_bounds__(256, 2) frac_nfree_bwd_kernel(ScanParams p, Nf
     lam_n = (tvalid && lm_bh) ? lm_bh[tg * p.ls1] : 1.0f;
 #pragma unroll
     for (int j = 0; j < NPR; ++j) {
-      const int pr = tid + 256 * j, t = pr / MP, m = pr - t * MP;
-      const bool ok = t < nv && m < M;
+      const int pr = tid + NT * j, t = pr / MP, m = pr - t * MP;
+      const bool ok = pr < kQ * MP && t < nv && m < M;
       const int64_t ith = (int64_t)(t0 + t) * lg_st + m;
       rlr[j] = (ok && rl_bh) ? rl_bh[ith] : 0.0f;
       wlr[j] = (ok && wl_bh && wl_bh != rl_bh) ? wl_bh[ith] : 0.0f;  // unused when the two are one array
@@ -478,16 +494,16 @@ __global__ void __launch_bounds__(256, 2) frac_nfree_bwd_kernel(ScanParams p, Nf
   };
   // the state entering a chunk (from the checkpoint pass) as U-product operands:
   // lane row m = 16 mb + lane % 16, 8 columns p0 + 32 kp + 8 (lane / 16) .. + 7
-  float4 s0r[MB][2][2];
+  float4 s0r[MB][KP][2];
   auto prefetch_s0 = [&](int c) {
     const float* ckc = ck_bh + (int64_t)c * M * P;
 #pragma unroll
     for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
-      for (int kp = 0; kp < 2; ++kp) {
+      for (int kp = 0; kp < KP; ++kp) {
         const int m = mb * 16 + li, pk = p0 + kp * 32 + lg * 8;
         s0r[mb][kp][0] = s0r[mb][kp][1] = make_float4(0.f, 0.f, 0.f, 0.f);
-        if (m < M && pk < P) {  // P is a multiple of 8: all 8 columns or none
+        if (doU && m < M && pk < P) {  // P is a multiple of 8: all 8 columns or none
           const float4* q = reinterpret_cast<const float4*>(ckc + (int64_t)m * P + pk);
           s0r[mb][kp][0] = q[0];
           s0r[mb][kp][1] = q[1];
@@ -502,7 +518,7 @@ __global__ void __launch_bounds__(256, 2) frac_nfree_bwd_kernel(ScanParams p, Nf
     barrier();  // the previous chunk is done with every LDS array
 #pragma unroll
     for (int j = 0; j < XV; ++j) {
-      const int i = tid + 256 * j, t = i / CPR, col = (i - t * CPR) * E16;
+      const int i = tid + NT * j, t = i / CPR, col = (i - t * CPR) * E16;
       *reinterpret_cast<int4*>(Xs + t * XS + col) = xr[j];
       *reinterpret_cast<int4*>(Ys + t * XS + col) = yr[j];
     }
@@ -510,14 +526,15 @@ __global__ void __launch_bounds__(256, 2) frac_nfree_bwd_kernel(ScanParams p, Nf
     const float dtv = dt_n, al_l = al_n, lam = lam_n;
     const float s_eff = lm_bh ? step_factor(lam, al_l) : 1.0f;
     const float dtt_l = tvalid ? dtv * s_eff : 0.0f;
-    chunk_log_decays<MP, 4>(dtt_l, s_rr, P_lh, P_ll);
+    chunk_log_decays<MP, NW>(dtt_l, s_rr, P_lh, P_ll);
     barrier();  // log-decays in LDS
     const bool over = lane < MP && lane < M && !(P_lh[(lane < MP ? lane : 0) * WQ + kQ - 1] <= kNfSafe);
     const int unsafe = (int)(__ballot(over) & ((MP >= 32) ? 0xffffffffull : ((1ull << MP) - 1)));
     // ---- per (token, mode) weights: pair = t MP + m
 #pragma unroll
     for (int j = 0; j < NPR; ++j) {
-      const int pr = tid + 256 * j, t = pr / MP, m = pr - t * MP;
+      const int pr = tid + NT * j, t = pr / MP, m = pr - t * MP;
+      if (pr >= kQ * MP) break;  // wave-uniform
       const float dtt = __shfl(dtt_l, t, 64), al = __shfl(al_l, t, 64);
       const bool valid = t < nv;
       const float r = s_rr[m], prior = -al * s_lnt[m];
@@ -540,16 +557,16 @@ __global__ void __launch_bounds__(256, 2) frac_nfree_bwd_kernel(ScanParams p, Nf
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int m = mb * 16 + lg * 4 + r;
-        if (m < MP) Gt[m * WQ + wave * 16 + li] = G[mb][r];
+        if (m < MP) Gt[m * GQ + wave * 16 + li] = G[mb][r];
       }
     barrier();  // x, dy, weights and the adjoint in LDS
 
     // ---- causal tiles: Gamma^T and the masked H = dY X^T into LDS
-    for (int tile = wave; tile < 10; tile += 4) {
+    for (int tile = wave; tile < 10; tile += NW) {
       const int tb = tile_row(tile), kb = tile_col(tile);
       floatx4 D = {0.f, 0.f, 0.f, 0.f};  // H over this workgroup's columns
 #pragma unroll
-      for (int kp = 0; kp < 2; ++kp)
+      for (int kp = 0; kp < KP; ++kp)
         mma(D, frag_load8(Ys + (tb * 16 + li) * XS + kp * 32 + lg * 8), frag_load8(Xs + (kb * 16 + li) * XS + kp * 32 + lg * 8));
       floatx4 Gm = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
@@ -575,7 +592,7 @@ __global__ void __launch_bounds__(256, 2) frac_nfree_bwd_kernel(ScanParams p, Nf
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int t = tb * 16 + lg * 4 + r, k = kb * 16 + li;
-        GT[k * XS + t] = (T)keep_if_ge(Gm[r], t, k);
+        GT[k * GS + t] = (T)keep_if_ge(Gm[r], t, k);
         HT[t * HS + k] = keep_if_ge(D[r], t, k);
       }
     }
@@ -586,7 +603,7 @@ __global__ void __launch_bounds__(256, 2) frac_nfree_bwd_kernel(ScanParams p, Nf
     // accuracy: the step-size and order gradients are differences of their sums
     floatx4 Uk[MB], Zk[MB];
     {
-      const int tb = wave;
+      const int tb = wave & 3;
 #pragma unroll
       for (int mb = 0; mb < MB; ++mb) {
         const int m = mb * 16 + li;  // output column of this lane
@@ -594,30 +611,35 @@ __global__ void __launch_bounds__(256, 2) frac_nfree_bwd_kernel(ScanParams p, Nf
         floatx4& Z = Zk[mb];
         U = Z = floatx4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int kp = 0; kp < 2; ++kp) {
-          const float4 a0 = s0r[mb][kp][0], a1 = s0r[mb][kp][1];
-          const float sv[8] = {a0.x, a0.y, a0.z, a0.w, a1.x, a1.y, a1.z, a1.w};
-          float gv[8];
+        for (int kp = 0; kp < KP; ++kp) {
+          if (doU) {
+            const float4 a0 = s0r[mb][kp][0], a1 = s0r[mb][kp][1];
+            const float sv[8] = {a0.x, a0.y, a0.z, a0.w, a1.x, a1.y, a1.z, a1.w};
+            Frag<T> S0f;
 #pragma unroll
-          for (int s = 0; s < 8; ++s) gv[s] = (m < MP) ? Gt[m * WQ + kp * 32 + lg * 8 + s] : 0.0f;
-          Frag<T> S0f, Gf;
-#pragma unroll
-          for (int s = 0; s < 8; ++s) {
-            frag_set(S0f, s, sv[s]);
-            frag_set(Gf, s, gv[s]);
-          }
-          const Frag<T> yf = frag_load8(Ys + (tb * 16 + li) * XS + kp * 32 + lg * 8);
-          const Frag<T> xf = frag_load8(Xs + (tb * 16 + li) * XS + kp * 32 + lg * 8);
-          mma(U, yf, S0f);
-          mma(Z, xf, Gf);
-          if constexpr (kBf16) {  // the remainders
-#pragma unroll
-            for (int s = 0; s < 8; ++s) {
-              frag_set(S0f, s, sv[s] - to_f32((T)sv[s]));
-              frag_set(Gf, s, gv[s] - to_f32((T)gv[s]));
-            }
+            for (int s = 0; s < 8; ++s) frag_set(S0f, s, sv[s]);
+            const Frag<T> yf = frag_load8(Ys + (tb * 16 + li) * XS + kp * 32 + lg * 8);
             mma(U, yf, S0f);
+            if constexpr (kBf16) {  // the remainder
+#pragma unroll
+              for (int s = 0; s < 8; ++s) frag_set(S0f, s, sv[s] - to_f32((T)sv[s]));
+              mma(U, yf, S0f);
+            }
+          }
+          if (doZ) {
+            float gv[8];
+#pragma unroll
+            for (int s = 0; s < 8; ++s) gv[s] = (m < MP) ? Gt[m * GQ + kp * 32 + lg * 8 + s] : 0.0f;
+            Frag<T> Gf;
+#pragma unroll
+            for (int s = 0; s < 8; ++s) frag_set(Gf, s, gv[s]);
+            const Frag<T> xf = frag_load8(Xs + (tb * 16 + li) * XS + kp * 32 + lg * 8);
             mma(Z, xf, Gf);
+            if constexpr (kBf16) {  // the remainder
+#pragma unroll
+              for (int s = 0; s < 8; ++s) frag_set(Gf, s, gv[s] - to_f32((T)gv[s]));
+              mma(Z, xf, Gf);
+            }
           }
         }
       }
@@ -629,8 +651,8 @@ __global__ void __launch_bounds__(256, 2) frac_nfree_bwd_kernel(ScanParams p, Nf
     }
     // sum(dy . x) of the chunk for dD (columns past d_h and tokens past the sequence are zero)
     if (p.dD) {
-      for (int i = tid; i < 64 * 64; i += 256) {
-        const int t = i >> 6, pcol = i & 63;
+      for (int i = tid; i < 64 * CW; i += NT) {
+        const int t = i / CW, pcol = i - t * CW;
         dd_acc += to_f32(Xs[t * XS + pcol]) * to_f32(Ys[t * XS + pcol]);
       }
     }
@@ -642,24 +664,28 @@ __global__ void __launch_bounds__(256, 2) frac_nfree_bwd_kernel(ScanParams p, Nf
       //   dk_{k,m} = e^{-(l_Q - l_k)} (G_m . x_k) + sum_{t>=k} H_{t,k} c_{t,m} e^{-(l_t - l_k)}
       // with the sums as float32 matrix-core products (H kappa e^{l}, H^T c e^{-l}) for
       // the factorised modes and one exp per pair for the others
-      const int tb = wave;
+      const int tb = wave & 3;
 #pragma unroll
       for (int mb = 0; mb < MB; ++mb) {
         const int m = mb * 16 + li;
         const int mm = m < MP ? m : 0;
         const bool fac = m < MP && !((unsafe >> mm) & 1);
         floatx4 cI = {0.f, 0.f, 0.f, 0.f}, kI = {0.f, 0.f, 0.f, 0.f};
-        for (int kq = 0; kq < (tb + 1) * 4; ++kq) {
-          const int k = kq * 4 + lg;
-          const float a = HT[(tb * 16 + li) * HS + k];
-          const float bb = fac ? P_Vt[mm * WQ + k] : 0.0f;
-          cI = __builtin_amdgcn_mfma_f32_16x16x4f32(a, bb, cI, 0, 0, 0);
+        if (doU) {
+          for (int kq = 0; kq < (tb + 1) * 4; ++kq) {
+            const int k = kq * 4 + lg;
+            const float a = HT[(tb * 16 + li) * HS + k];
+            const float bb = fac ? P_Vt[mm * WQ + k] : 0.0f;
+            cI = __builtin_amdgcn_mfma_f32_16x16x4f32(a, bb, cI, 0, 0, 0);
+          }
         }
-        for (int tq = tb * 4; tq < 16; ++tq) {
-          const int t = tq * 4 + lg;
-          const float a = HT[t * HS + tb * 16 + li];
-          const float bb = fac ? P_O[mm * WQ + t] : 0.0f;
-          kI = __builtin_amdgcn_mfma_f32_16x16x4f32(a, bb, kI, 0, 0, 0);
+        if (doZ) {
+          for (int tq = tb * 4; tq < 16; ++tq) {
+            const int t = tq * 4 + lg;
+            const float a = HT[t * HS + tb * 16 + li];
+            const float bb = fac ? P_O[mm * WQ + t] : 0.0f;
+            kI = __builtin_amdgcn_mfma_f32_16x16x4f32(a, bb, kI, 0, 0, 0);
+          }
         }
         const bool direct = m < M && ((unsafe >> mm) & 1);
         const float* lhm = P_lh + mm * WQ;
@@ -667,22 +693,25 @@ __global__ void __launch_bounds__(256, 2) frac_nfree_bwd_kernel(ScanParams p, Nf
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int t = tb * 16 + lg * 4 + r;
-          const float ea = fexp(-lhm[t]);
-          float dc = ea * Uk[mb][r];
-          const float dk = ell_decay(lhm, llm, kQ - 1, t) * Zk[mb][r];
-          float dki = 0.0f;
-          if (!direct) {
-            dc += ea * cI[r];
-            dki = fexp(lhm[t]) * kI[r];
-          } else {
-            for (int k = 0; k <= t; ++k) dc += HT[t * HS + k] * P_Vt[mm * WQ + k] * ell_decay(lhm, llm, t, k);
-            for (int t2 = t; t2 < 64; ++t2) dki += HT[t2 * HS + t] * P_c[mm * WQ + t2] * ell_decay(lhm, llm, t2, t);
+          const int64_t i = ((int64_t)ps * p.Bsz * H * L + (int64_t)bh * L + t0 + t) * M + m;  // [nps][B H L][M]
+          if (doU) {
+            const float ea = fexp(-lhm[t]);
+            float dc = ea * Uk[mb][r];
+            if (!direct) dc += ea * cI[r];
+            else
+              for (int k = 0; k <= t; ++k) dc += HT[t * HS + k] * P_Vt[mm * WQ + k] * ell_decay(lhm, llm, t, k);
+            if (m < M && t < nv) wk.dcp[i] = dc;
           }
-          if (m < M && t < nv) {
-            const int64_t i = ((int64_t)ps * p.Bsz * H * L + (int64_t)bh * L + t0 + t) * M + m;  // [nps][B H L][M]
-            wk.dcp[i] = dc;
-            wk.dkp[i] = dk;
-            wk.dkip[i] = dki;
+          if (doZ) {
+            const float dk = ell_decay(lhm, llm, kQ - 1, t) * Zk[mb][r];
+            float dki = 0.0f;
+            if (!direct) dki = fexp(lhm[t]) * kI[r];
+            else
+              for (int t2 = t; t2 < 64; ++t2) dki += HT[t2 * HS + t] * P_c[mm * WQ + t2] * ell_decay(lhm, llm, t2, t);
+            if (m < M && t < nv) {
+              wk.dkp[i] = dk;
+              wk.dkip[i] = dki;
+            }
           }
         }
       }
@@ -709,7 +738,7 @@ __global__ void __launch_bounds__(256, 2) frac_nfree_bwd_kernel(ScanParams p, Nf
         mma(Y, Vf, Gf);
 #pragma unroll
         for (int kk = tb / 2; kk < 2; ++kk)
-          mma(Y, frag_load8(GT + t * XS + kk * 32 + lg * 8), frag_load_rows(Ys, XS, kk * 32 + lg * 8, wave * 16));
+          mma(Y, frag_load8(GT + t * GS + kk * 32 + lg * 8), frag_load_rows(Ys, XS, kk * 32 + lg * 8, wave * 16));
         float yv[4];
         col4_rows(Ys, XS, tb * 16 + lg * 4, wave * 16, yv);
 #pragma unroll
@@ -759,7 +788,7 @@ __global__ void __launch_bounds__(256, 2) frac_nfree_bwd_kernel(ScanParams p, Nf
     }
     barrier();  // dx rows in LDS
     if constexpr (kBf16) {
-      for (int i = tid; i < 64 * CPR; i += 256) {
+      for (int i = tid; i < 64 * CPR; i += NT) {
         const int t = i / CPR, col = (i - t * CPR) * E16;
         if (t < nv && p0 + col < P)
           *reinterpret_cast<int4*>(dxg + (int64_t)(t0 + t) * xstride + col) = *reinterpret_cast<const int4*>(DX + t * XS + col);
@@ -793,16 +822,21 @@ __global__ void __launch_bounds__(256, 2) frac_nfree_bwd_kernel(ScanParams p, Nf
   // ---- per-workgroup total of sum(dy . x)
   redD[tid] = dd_acc;
   __syncthreads();
-  if (tid < MP && tid < M) wk.I[((int64_t)ps * p.Bsz * H + bh) * M + tid] = ((red[0][tid] + red[1][tid]) + red[2][tid]) + red[3][tid];
+  if (tid < MP && tid < M) wk.I[((int64_t)ps * p.Bsz * H + bh) * M + tid] = red_sum(tid);
   if (tid == 0) {
     float s = 0.f;
-    for (int i = 0; i < 256; ++i) s += redD[i];
+    for (int i = 0; i < NT; ++i) s += redD[i];
     wk.dDp[(int64_t)ps * p.Bsz * H + bh] = s;
   }
 }
 
+// Columns of d_h per workgroup: 128 (8 waves) for head dims above 128, else 64 (4
+// waves); the backward of float32 inputs with 32 modes keeps 64 (LDS).
+int nfree_cols(const ScanParams& p) { return p.P > 128 ? 128 : 64; }
+int nfree_bwd_cols(const ScanParams& p) { return (p.P > 128 && (p.io_bf16 || p.M <= 16)) ? 128 : 64; }
+
 // The forward pass (CKPT: the checkpoint pass of the backward) in workgroups of NW
-// waves: 8 (128 columns) for head dims above 128, else 4 (64 columns).
+// waves, 16 NW columns each.
 template <typename T, int MP, bool CKPT, int NW>
 hipError_t launch_nfree_fwd_nw(const ScanParams& p, float* ckpt, hipStream_t stream) {
   const unsigned blocks = (unsigned)((int64_t)p.Bsz * p.H * ((p.P + 16 * NW - 1) / (16 * NW)));
@@ -812,8 +846,8 @@ hipError_t launch_nfree_fwd_nw(const ScanParams& p, float* ckpt, hipStream_t str
 
 template <typename T, int MP, bool CKPT>
 hipError_t launch_nfree_fwd(const ScanParams& p, float* ckpt, hipStream_t stream) {
-  return p.P > 128 ? launch_nfree_fwd_nw<T, MP, CKPT, 8>(p, ckpt, stream)
-                   : launch_nfree_fwd_nw<T, MP, CKPT, 4>(p, ckpt, stream);
+  return nfree_cols(p) == 128 ? launch_nfree_fwd_nw<T, MP, CKPT, 8>(p, ckpt, stream)
+                              : launch_nfree_fwd_nw<T, MP, CKPT, 4>(p, ckpt, stream);
 }
 
 template <typename T>
@@ -830,7 +864,8 @@ struct NfLayout {
 
 NfLayout nfree_layout(const ScanParams& p) {
   auto up = [](size_t v) { return (v + 255) / 256 * 256; };
-  const size_t bh = (size_t)p.Bsz * p.H, nps = (p.P + 63) / 64, nch = (p.L + kQ - 1) / kQ;
+  const int cw = nfree_bwd_cols(p);
+  const size_t bh = (size_t)p.Bsz * p.H, nps = (p.P + cw - 1) / cw, nch = (p.L + kQ - 1) / kQ;
   NfLayout l{};
   l.ckpt = 0;
   l.F = up(sizeof(float) * bh * (nch + 1) * p.M * p.P);
@@ -856,12 +891,18 @@ hipError_t launch_nfree_bwd_mp(const ScanParams& p, void* ws, hipStream_t stream
   wk.dcp = reinterpret_cast<float*>(base + l.dcp);
   wk.dkp = reinterpret_cast<float*>(base + l.dkp);
   wk.dkip = reinterpret_cast<float*>(base + l.dkip);
-  const unsigned blocks = (unsigned)((int64_t)p.Bsz * p.H * ((p.P + 63) / 64));
   hipError_t e = launch_nfree_fwd<T, MP, true>(p, reinterpret_cast<float*>(base + l.ckpt), stream);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((frac_nfree_bwd_kernel<T, MP>), dim3(blocks), dim3(256), 0, stream, p, wk);
+  const int cw = nfree_bwd_cols(p), nps = (p.P + cw - 1) / cw;
+  const unsigned blocks = (unsigned)((int64_t)p.Bsz * p.H * nps);
+  constexpr bool kWide = sizeof(T) == 2 || MP <= 16;  // an 8-wave instance fits the LDS
+  if constexpr (kWide) {
+    if (cw == 128) hipLaunchKernelGGL((frac_nfree_bwd_kernel<T, MP, 8>), dim3(blocks), dim3(512), 0, stream, p, wk);
+    else hipLaunchKernelGGL((frac_nfree_bwd_kernel<T, MP, 4>), dim3(blocks), dim3(256), 0, stream, p, wk);
+  } else {
+    hipLaunchKernelGGL((frac_nfree_bwd_kernel<T, MP, 4>), dim3(blocks), dim3(256), 0, stream, p, wk);
+  }
   if ((e = hipGetLastError()) != hipSuccess) return e;
-  const int nps = (p.P + 63) / 64;
   GradInputs gi;
   gi.dc = wk.dcp;
   gi.dk = wk.dkp;

@@ -56,6 +56,12 @@ SMALL = {
     "f32 M11 P96 extras": Workload("t", 1, 129, 2, 96, 1, 11, bc=False, io_dtype="f32", extras=True,
                                    init_state=True, final_state=True),
     "bf16 M16 L1": Workload("t", 2, 1, 2, 256, 1, 16, bc=False, final_state=True, init_state=True),
+    # 128-column workgroups (head dims above 128): a half-filled second group, 4 and 32 modes, float32
+    "bf16 M4 P192 ragged extras": Workload("t", 1, 201, 2, 192, 1, 4, bc=False, extras=True, init_state=True,
+                                           final_state=True),
+    "bf16 M32 P256": Workload("t", 1, 150, 2, 256, 1, 32, bc=False, final_state=True, init_state=True),
+    "f32 M16 P256 extras": Workload("t", 1, 130, 2, 256, 1, 16, bc=False, io_dtype="f32", extras=True,
+                                    final_state=True),
 }
 
 
@@ -143,6 +149,15 @@ BWD = {
     "f32 M11 P96 extras dfinal": Workload("t", 1, 129, 2, 96, 1, 11, bc=False, io_dtype="f32", extras=True,
                                           init_state=True, backward=True, final_state=True),
     "bf16 M16 L1": Workload("t", 2, 1, 2, 256, 1, 16, bc=False, backward=True, init_state=True, final_state=True),
+    # 128-column workgroups (head dims above 128): a half-filled second group, 4 and 32 modes, float32
+    # (with 32 modes the float32 backward keeps 64-column workgroups)
+    "bf16 M4 P192 ragged extras dfinal": Workload("t", 1, 201, 2, 192, 1, 4, bc=False, extras=True,
+                                                  init_state=True, backward=True, final_state=True),
+    "bf16 M32 P256 init": Workload("t", 1, 150, 2, 256, 1, 32, bc=False, backward=True, init_state=True),
+    "f32 M16 P256 extras": Workload("t", 1, 130, 2, 256, 1, 16, bc=False, io_dtype="f32", extras=True,
+                                    backward=True),
+    "f32 M32 P256 extras": Workload("t", 1, 90, 2, 256, 1, 32, bc=False, io_dtype="f32", extras=True,
+                                    backward=True),
 }
 
 
