@@ -227,16 +227,18 @@ def bench_scan(torch, frac, w, steps, warmup, extras=True):
     ws_f = torch.empty(max(1, frac.scan_workspace_size(shape, False)), dtype=torch.uint8, device="cuda")
     ws_b = torch.empty(max(1, frac.scan_workspace_size(shape, True)), dtype=torch.uint8, device="cuda")
     dy = inp.get("dy")
+    # the form without B/C keeps the forward's chunk states for the backward of a training step
+    cs = frac.chunk_states_like(x, w.nmodes) if (w.backward and not w.bc) else None
 
     def fwd():
         frac.scan_fwd(x, dt, Bm, Cm, alpha, tau, y=y, final_state=fs, return_final_state=fs is not None,
-                      workspace=ws_f)
+                      workspace=ws_f, chunk_states=cs)
 
     def bwd():
-        frac.scan_bwd(x, dt, Bm, Cm, alpha, tau, dy, workspace=ws_b)
+        frac.scan_bwd(x, dt, Bm, Cm, alpha, tau, dy, workspace=ws_b, chunk_states=cs)
 
     def bwd_all():  # also the gradients of alpha, lambda, the logits and the initial state
-        frac.scan_bwd(x, dt, Bm, Cm, alpha, tau, dy, workspace=ws_b, all_grads=True)
+        frac.scan_bwd(x, dt, Bm, Cm, alpha, tau, dy, workspace=ws_b, all_grads=True, chunk_states=cs)
 
     for _ in range(warmup):
         fwd()
@@ -370,10 +372,10 @@ def measured_traffic(entry, workload):
 
 
 # kernels whose counters belong to each entry point's launch
-_ENTRY_KERNELS = {"frac_scan_bwd": ("frac_cb_kernel", "frac_bwd_", "frac_grad_", "frac_nfree_fwd_kernel<bf16,16,1>",
+_ENTRY_KERNELS = {"frac_scan_bwd": ("frac_cb_kernel", "frac_bwd_", "frac_grad_", "frac_nfree_fwd_kernel<bf16,16,1",
                                     "frac_nfree_bwd_"),
                   "frac_scan_fwd": ("frac_cb_kernel", "frac_fwd_", "frac_seg_combine", "frac_mode_lse",
-                                    "frac_nfree_fwd_kernel<bf16,16,0>")}
+                                    "frac_nfree_fwd_kernel<bf16,16,0")}
 
 
 def measured_mfma_busy(entry, workload):

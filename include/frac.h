@@ -98,7 +98,14 @@ typedef struct {
  *   D            [H] f32 feedthrough; NULL = no skip term.
  *   init_state   [B,H,M,N,P] f32 state before token 0; NULL = zeros.
  *   y            [B,L,H,P] io_dtype, written.
- *   final_state  [B,H,M,N,P] f32 state after the last token, written; NULL = not produced. */
+ *   final_state  [B,H,M,N,P] f32 state after the last token, written; NULL = not produced.
+ *   chunk_states [B,H,C+1,M,P] f32 with C = ceil(seqlen / 64), the form without B/C only
+ *                (dstate 1; must be NULL otherwise): the state entering each 64-token
+ *                chunk and, in slot C, the state after the last token; frac_scan_fwd
+ *                writes it when non-NULL (frac_chunk_states_size gives its bytes).  In
+ *                frac_bwd_args.fwd, when non-NULL, it is read as frac_scan_fwd wrote it
+ *                for the same inputs, in place of the backward's own pass that recomputes
+ *                these states (the chunked scan's stored chunk states, Sec. 3.2). */
 typedef struct {
   const void *x;
   const float *dt;
@@ -113,11 +120,13 @@ typedef struct {
   const float *init_state;
   void *y;
   float *final_state;
+  float *chunk_states;
 } frac_fwd_args;
 
 /* Backward of frac_scan_fwd.  `fwd` holds the same inputs as the forward call
  * (fwd.y and fwd.final_state are ignored); the backward recomputes everything it
- * needs from them, nothing is carried between calls.
+ * needs from them, except the chunk states when fwd.chunk_states carries them from
+ * the forward (the form without B/C).
  *   dy             [B,L,H,P] io_dtype   gradient of y
  *   d_final_state  [B,H,M,N,P] f32      gradient of final_state; NULL = zero
  *   dx             [B,L,H,P] io_dtype   written
@@ -283,6 +292,12 @@ frac_status frac_gnorm_bwd(const frac_shape *shape, const frac_gnorm_bwd_args *a
  * (backward = 1) needs for `shape`; 0 means none.  Returns 0 for an invalid shape
  * (the scan call then reports the error). */
 size_t frac_scan_workspace_size(const frac_shape *shape, int backward);
+
+/* Bytes of frac_fwd_args.chunk_states for `shape` (the form without B/C:
+ * batch * nheads * (ceil(seqlen / 64) + 1) * nmodes * headdim * 4) in *bytes.
+ * FRAC_ERR_UNSUPPORTED for dstate > 1, FRAC_ERR_INVALID_ARG for a NULL pointer or an
+ * invalid shape. */
+frac_status frac_chunk_states_size(const frac_shape *shape, size_t *bytes);
 
 /* Chunked parallel scan, forward.  ws/ws_bytes: caller-owned device workspace of
  * at least frac_scan_workspace_size(shape, 0) bytes (may be NULL when that is 0);

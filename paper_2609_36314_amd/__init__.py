@@ -102,7 +102,8 @@ def default_tau(M: int, tau_min: float = TAU_MIN, tau_max: float = TAU_MAX, devi
     return t if device is None else t.to(device)
 
 
-def _fwd_struct(x, dt, Bm, Cm, alpha, tau, lam, read_logit, write_logit, D, init_state, y, final_state):
+def _fwd_struct(x, dt, Bm, Cm, alpha, tau, lam, read_logit, write_logit, D, init_state, y, final_state,
+                chunk_states=None):
     Bsz, L, H, P = x.shape
     if (Bm is None) != (Cm is None):
         raise TypeError("Bm and Cm are both given or both None (B = C = 1)")
@@ -121,18 +122,22 @@ def _fwd_struct(x, dt, Bm, Cm, alpha, tau, lam, read_logit, write_logit, D, init
     a.tau, a.D = _ptr(_f32(tau, "tau")), _ptr(_f32(D, "D"))
     a.init_state = _ptr(_f32(init_state, "init_state"))
     a.y, a.final_state = _ptr(y), _ptr(final_state)
+    a.chunk_states = _ptr(_f32(chunk_states, "chunk_states"))
     keep = (alpha_t, lam_t)
     return a, keep
 
 
 def scan_fwd(x, dt, Bm, Cm, alpha, tau, *, lam=None, read_logit=None, write_logit=None, D=None,
-             init_state=None, return_final_state=False, chunk=0, y=None, final_state=None, workspace=None):
+             init_state=None, return_final_state=False, chunk=0, y=None, final_state=None, workspace=None,
+             chunk_states=None):
     """Chunked parallel scan, forward (frac_scan_fwd).
 
     x [B,L,H,P], Bm/Cm [B,L,G,N] (float32 or bfloat16, one dtype), or both None for the
     form without B/C (B = C = 1, state [B,H,M,1,P], headdim <= 256, up to 32 modes); dt [B,L,H] f32;
     alpha, lam: float or f32 tensor broadcastable to [B,L,H]; read/write logits
     [B,L,H,M] f32; tau [M] f32; D [H] f32; init_state [B,H,M,N,P] f32.
+    chunk_states (the form without B/C): an f32 tensor of chunk_states_size bytes the
+    forward fills with the state entering each 64-token chunk, for scan_bwd.
     Returns y, or (y, final_state) when return_final_state."""
     M = int(tau.shape[0])
     shape = _shape(x, Bm, M, chunk)
@@ -143,7 +148,7 @@ def scan_fwd(x, dt, Bm, Cm, alpha, tau, *, lam=None, read_logit=None, write_logi
     if return_final_state and final_state is None:
         final_state = torch.empty((Bsz, H, M, N, P), dtype=torch.float32, device=x.device)
     args, keep = _fwd_struct(x, dt, Bm, Cm, alpha, tau, lam, read_logit, write_logit, D, init_state, y,
-                             final_state if return_final_state else None)
+                             final_state if return_final_state else None, chunk_states)
     ws_bytes = scan_workspace_size(shape, False)
     if workspace is None and ws_bytes:
         workspace = torch.empty(ws_bytes, dtype=torch.uint8, device=x.device)
@@ -151,6 +156,19 @@ def scan_fwd(x, dt, Bm, Cm, alpha, tau, *, lam=None, read_logit=None, write_logi
                                          ws_bytes if workspace is not None else 0, _stream()))
     del keep
     return (y, final_state) if return_final_state else y
+
+
+def chunk_states_size(shape):
+    """Bytes of the chunk states scan_fwd keeps for scan_bwd (frac_chunk_states_size; the
+    form without B/C only)."""
+    n = ctypes.c_size_t(0)
+    _lib.check(_lib.load().frac_chunk_states_size(ctypes.byref(shape), ctypes.byref(n)))
+    return int(n.value)
+
+
+def chunk_states_like(x, nmodes):
+    """An f32 tensor for the chunk states of x [B,L,H,P] with nmodes modes (no B/C)."""
+    return torch.empty(chunk_states_size(_shape(x, None, nmodes, 0)) // 4, dtype=torch.float32, device=x.device)
 
 
 def scan_fwd_noalloc(x, dt, Bm, Cm, alpha, tau, *, y, lam=None, read_logit=None, write_logit=None, D=None,
@@ -174,18 +192,20 @@ def scan_fwd_noalloc_limit():
 
 
 def scan_bwd(x, dt, Bm, Cm, alpha, tau, dy, *, lam=None, read_logit=None, write_logit=None, D=None,
-             init_state=None, d_final_state=None, chunk=0, workspace=None, all_grads=False):
+             init_state=None, d_final_state=None, chunk=0, workspace=None, all_grads=False, chunk_states=None):
     """Chunked parallel scan, backward (frac_scan_bwd).
 
     Returns dict(dx, ddt, dBm, dCm, dD) with dD None when D is None.  With
     all_grads also dalpha [B,L,H], dlambda [B,L,H], dread_logit, dwrite_logit
-    [B,L,H,M] and dinit_state [B,H,M,N,P] (N = 1 without B/C)."""
+    [B,L,H,M] and dinit_state [B,H,M,N,P] (N = 1 without B/C).  chunk_states: the tensor
+    scan_fwd filled for these inputs (the form without B/C), read instead of recomputed."""
     M = int(tau.shape[0])
     shape = _shape(x, Bm, M, chunk)
     Bsz, L, H, P = x.shape
     if dy.dtype != x.dtype or not dy.is_contiguous():
         raise TypeError("dy must be contiguous with the dtype of x")
-    fwd, keep = _fwd_struct(x, dt, Bm, Cm, alpha, tau, lam, read_logit, write_logit, D, init_state, None, None)
+    fwd, keep = _fwd_struct(x, dt, Bm, Cm, alpha, tau, lam, read_logit, write_logit, D, init_state, None, None,
+                            chunk_states)
     out = dict(dx=torch.empty_like(x), ddt=torch.empty_like(dt), dBm=None if Bm is None else torch.empty_like(Bm),
                dCm=None if Cm is None else torch.empty_like(Cm), dD=None if D is None else torch.empty_like(D))
     if all_grads:

@@ -20,8 +20,8 @@ STATUS = {0: "FRAC_OK", -1: "FRAC_ERR_INVALID_ARG", -2: "FRAC_ERR_UNSUPPORTED", 
           -4: "FRAC_ERR_HIP"}
 
 # every symbol include/frac.h declares
-EXPORTS = ("frac_scan_workspace_size", "frac_scan_fwd", "frac_scan_bwd", "frac_decode_step", "frac_default_tau",
-           "frac_status_string", "frac_last_error", "frac_params_fwd", "frac_params_workspace_size",
+EXPORTS = ("frac_scan_workspace_size", "frac_chunk_states_size", "frac_scan_fwd", "frac_scan_bwd", "frac_decode_step",
+           "frac_default_tau", "frac_status_string", "frac_last_error", "frac_params_fwd", "frac_params_workspace_size",
            "frac_params_bwd", "frac_conv_fwd", "frac_conv_workspace_size", "frac_conv_bwd",
            "frac_gnorm_fwd", "frac_gnorm_workspace_size", "frac_gnorm_bwd", "frac_scan_fwd_noalloc",
            "frac_scan_fwd_noalloc_limit")
@@ -38,7 +38,8 @@ class FracFwdArgs(ctypes.Structure):
                 ("alpha", c_void_p), ("alpha_stride", c_int64 * 3),
                 ("lam", c_void_p), ("lambda_stride", c_int64 * 3),
                 ("read_logit", c_void_p), ("write_logit", c_void_p), ("tau", c_void_p), ("D", c_void_p),
-                ("init_state", c_void_p), ("y", c_void_p), ("final_state", c_void_p)]
+                ("init_state", c_void_p), ("y", c_void_p), ("final_state", c_void_p),
+                ("chunk_states", c_void_p)]
 
 
 class FracBwdArgs(ctypes.Structure):
@@ -109,6 +110,8 @@ def load():
     lib = ctypes.CDLL(LIB_PATH)
     lib.frac_scan_workspace_size.argtypes = [POINTER(FracShape), c_int]
     lib.frac_scan_workspace_size.restype = c_size_t
+    lib.frac_chunk_states_size.argtypes = [POINTER(FracShape), POINTER(c_size_t)]
+    lib.frac_chunk_states_size.restype = c_int
     lib.frac_scan_fwd.argtypes = [POINTER(FracShape), POINTER(FracFwdArgs), c_void_p, c_size_t, c_void_p]
     lib.frac_scan_fwd.restype = c_int
     lib.frac_scan_fwd_noalloc.argtypes = [POINTER(FracShape), POINTER(FracFwdArgs), c_void_p]

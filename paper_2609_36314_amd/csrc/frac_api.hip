@@ -107,8 +107,10 @@ frac_status fill_fwd(const frac_fwd_args* a, frac::ScanParams& p, bool need_outp
   if (p.N == 1 ? (a->Bm || a->Cm) : (!a->Bm || !a->Cm))
     return fail(FRAC_ERR_INVALID_ARG, "Bm and Cm are required for dstate > 1 and must be NULL for dstate 1");
   if (need_outputs && !a->y) return fail(FRAC_ERR_INVALID_ARG, "y is required");
+  if (a->chunk_states && p.N != 1)
+    return fail(FRAC_ERR_UNSUPPORTED, "chunk_states are kept for the form without B/C (dstate 1) only");
   if (!aligned16(a->x) || !aligned16(a->Bm) || !aligned16(a->Cm) || !aligned16(a->init_state) ||
-      (need_outputs && (!aligned16(a->y) || !aligned16(a->final_state))))
+      !aligned16(a->chunk_states) || (need_outputs && (!aligned16(a->y) || !aligned16(a->final_state))))
     return fail(FRAC_ERR_INVALID_ARG, "x, Bm, Cm, y and the state arrays must be 16-byte aligned");
   p.x = a->x;
   p.dt = a->dt;
@@ -129,6 +131,7 @@ frac_status fill_fwd(const frac_fwd_args* a, frac::ScanParams& p, bool need_outp
   p.init_state = a->init_state;
   p.y = need_outputs ? a->y : nullptr;
   p.final_state = need_outputs ? a->final_state : nullptr;
+  p.chunk_states = a->chunk_states;
   return FRAC_OK;
 }
 
@@ -249,6 +252,19 @@ frac_status frac_default_tau(int M, double tau_min, double tau_max, float* out) 
   return ok();
 }
 
+frac_status frac_chunk_states_size(const frac_shape* shape, size_t* bytes) {
+  if (!bytes) return fail(FRAC_ERR_INVALID_ARG, "bytes is NULL");
+  *bytes = 0;
+  frac::ScanParams p{};
+  frac_status s = fill_shape(shape, p);
+  if (s == FRAC_OK) s = check_scan_shape(p, "frac_chunk_states_size", false);
+  if (s != FRAC_OK) return s;
+  if (p.N != 1) return fail(FRAC_ERR_UNSUPPORTED, "chunk_states are kept for the form without B/C (dstate 1) only");
+  const int64_t nchunks = ((int64_t)p.L + 63) / 64;
+  *bytes = sizeof(float) * (size_t)p.Bsz * p.H * (size_t)(nchunks + 1) * p.M * p.P;
+  return ok();
+}
+
 size_t frac_scan_workspace_size(const frac_shape* shape, int backward) {
   frac::ScanParams p{};
   if (fill_shape(shape, p) != FRAC_OK || check_scan_shape(p, "frac_scan_workspace_size", backward) != FRAC_OK) return 0;
@@ -292,10 +308,15 @@ frac_status scan_fwd_impl(const frac_shape* shape, const frac_fwd_args* args, vo
   if (!args) return fail(FRAC_ERR_INVALID_ARG, "args is NULL");
   hipStream_t st = reinterpret_cast<hipStream_t>(stream);
   if (p.L == 0) {
-    if (args->final_state) {
-      const int64_t n = (int64_t)p.Bsz * p.H * p.M * p.N * p.P;
-      hipLaunchKernelGGL(copy_or_zero_kernel, dim3(256), dim3(256), 0, st, args->final_state, args->init_state, n);
-      return hip_status(hipGetLastError(), "frac_scan_fwd (empty sequence)");
+    if (args->chunk_states && p.N != 1)
+      return fail(FRAC_ERR_UNSUPPORTED, "chunk_states are kept for the form without B/C (dstate 1) only");
+    const int64_t n = (int64_t)p.Bsz * p.H * p.M * p.N * p.P;
+    // [B H][1][M][P]: the single slot of an empty sequence is its final state
+    for (float* dst : {args->final_state, args->chunk_states}) {
+      if (!dst) continue;
+      hipLaunchKernelGGL(copy_or_zero_kernel, dim3(256), dim3(256), 0, st, dst, args->init_state, n);
+      const hipError_t e = hipGetLastError();
+      if (e != hipSuccess) return hip_status(e, "frac_scan_fwd (empty sequence)");
     }
     return ok();
   }

@@ -35,6 +35,10 @@ struct ScanParams {
   const float* init_state;
   void* y;
   float* final_state;
+  // the form without B/C: [B H][nchunks + 1][M][P] the state entering each chunk, then
+  // the final state; written by the forward, read by the backward in place of its own
+  // checkpoint pass (NULL: not kept)
+  float* chunk_states;
   // forward split into nseg sequence segments of seg_len tokens (the last shorter;
   // nseg 1: no split).  seg_state [nseg-1][B H Mall N P]: the state after each
   // segment but the last (first each segment's own end state from a zero start,

@@ -34,7 +34,9 @@ constexpr float kNfFloor = 0x1p-60f;
 
 
 // CKPT: no outputs; the state entering every chunk, and the final state, go to
-// ckpt [B H][nchunks + 1][M][P] (the first pass of the backward).
+// ckpt [B H][nchunks + 1][M][P] (the first pass of the backward).  Without CKPT a
+// non-NULL ckpt receives the same states beside the outputs (the caller's chunk
+// states, which its backward then reads instead of running that pass).
 // NW waves per workgroup, 16 NW columns of d_h: with more waves per workgroup the
 // per-chunk work that does not depend on the columns (the log-decays, the weights,
 // the Gamma tiles) is done once for more columns and split over more waves.
@@ -145,7 +147,7 @@ __global__ void __launch_bounds__(64 * NW) frac_nfree_fwd_kernel(ScanParams p, f
     }
     const bool tvalid = lane < nv;
     const float dtv = dt_n, al_l = al_n, lam = lam_n;
-    if constexpr (CKPT) {  // the state entering this chunk
+    if (CKPT || ckpt) {  // the state entering this chunk
       float* ck = ckpt + ((int64_t)bh * (nchunks + 1) + c) * M * P;
 #pragma unroll
       for (int mb = 0; mb < MB; ++mb)
@@ -318,9 +320,9 @@ __global__ void __launch_bounds__(64 * NW) frac_nfree_fwd_kernel(ScanParams p, f
     }
   }
 
-  float* fin = CKPT ? ckpt + ((int64_t)bh * (nchunks + 1) + nchunks) * M * P
-                    : (p.final_state ? p.final_state + sbase : nullptr);
-  if (fin && active) {
+  float* fin_ck = ckpt ? ckpt + ((int64_t)bh * (nchunks + 1) + nchunks) * M * P : nullptr;
+  float* fin = (!CKPT && p.final_state) ? p.final_state + sbase : nullptr;
+  if ((fin || fin_ck) && active) {
     __syncthreads();
     const float* Ef = s_E2[nchunks & 1];
 #pragma unroll
@@ -328,7 +330,11 @@ __global__ void __launch_bounds__(64 * NW) frac_nfree_fwd_kernel(ScanParams p, f
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int m = mb * 16 + lg * 4 + r;
-        if (m < M && pc < P) fin[(int64_t)m * P + pc] = S[mb][r] * Ef[m];
+        if (m < M && pc < P) {
+          const float v = S[mb][r] * Ef[m];
+          if (fin) fin[(int64_t)m * P + pc] = v;
+          if (fin_ck) fin_ck[(int64_t)m * P + pc] = v;
+        }
       }
   }
 }
@@ -852,10 +858,10 @@ hipError_t launch_nfree_fwd(const ScanParams& p, float* ckpt, hipStream_t stream
 
 template <typename T>
 hipError_t launch_nfree_t(const ScanParams& p, hipStream_t stream) {
-  if (p.M <= 4) return launch_nfree_fwd<T, 4, false>(p, nullptr, stream);
-  if (p.M <= 8) return launch_nfree_fwd<T, 8, false>(p, nullptr, stream);
-  if (p.M <= 16) return launch_nfree_fwd<T, 16, false>(p, nullptr, stream);
-  return launch_nfree_fwd<T, 32, false>(p, nullptr, stream);
+  if (p.M <= 4) return launch_nfree_fwd<T, 4, false>(p, p.chunk_states, stream);
+  if (p.M <= 8) return launch_nfree_fwd<T, 8, false>(p, p.chunk_states, stream);
+  if (p.M <= 16) return launch_nfree_fwd<T, 16, false>(p, p.chunk_states, stream);
+  return launch_nfree_fwd<T, 32, false>(p, p.chunk_states, stream);
 }
 
 struct NfLayout {
@@ -884,15 +890,17 @@ hipError_t launch_nfree_bwd_mp(const ScanParams& p, void* ws, hipStream_t stream
   const NfLayout l = nfree_layout(p);
   unsigned char* base = reinterpret_cast<unsigned char*>(ws);
   NfWork wk;
-  wk.ckpt = reinterpret_cast<float*>(base + l.ckpt);
+  // the chunk states: the caller's, from its forward, or this backward's own first pass
+  float* ck = p.chunk_states ? p.chunk_states : reinterpret_cast<float*>(base + l.ckpt);
+  wk.ckpt = ck;
   wk.F = reinterpret_cast<float*>(base + l.F);
   wk.I = reinterpret_cast<float*>(base + l.I);
   wk.dDp = reinterpret_cast<float*>(base + l.dDp);
   wk.dcp = reinterpret_cast<float*>(base + l.dcp);
   wk.dkp = reinterpret_cast<float*>(base + l.dkp);
   wk.dkip = reinterpret_cast<float*>(base + l.dkip);
-  hipError_t e = launch_nfree_fwd<T, MP, true>(p, reinterpret_cast<float*>(base + l.ckpt), stream);
-  if (e != hipSuccess) return e;
+  hipError_t e = hipSuccess;
+  if (!p.chunk_states && (e = launch_nfree_fwd<T, MP, true>(p, ck, stream)) != hipSuccess) return e;
   const int cw = nfree_bwd_cols(p), nps = (p.P + cw - 1) / cw;
   const unsigned blocks = (unsigned)((int64_t)p.Bsz * p.H * nps);
   constexpr bool kWide = sizeof(T) == 2 || MP <= 16;  // an 8-wave instance fits the LDS

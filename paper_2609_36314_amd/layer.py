@@ -22,7 +22,8 @@ import math
 import torch
 import torch.nn.functional as F
 
-from . import conv_bwd, conv_fwd, default_tau, gnorm_bwd, gnorm_fwd, params_bwd, params_fwd, scan_bwd, scan_fwd
+from . import (chunk_states_like, conv_bwd, conv_fwd, default_tau, gnorm_bwd, gnorm_fwd, params_bwd, params_fwd,
+               scan_bwd, scan_fwd)
 
 
 class _Conv(torch.autograd.Function):
@@ -58,16 +59,20 @@ class _Params(torch.autograd.Function):
 
 
 class _Scan(torch.autograd.Function):
+    """The scan keeps the state entering each chunk from its forward (B H M P floats per
+    64 tokens) for its backward, which then skips recomputing them."""
+
     @staticmethod
     def forward(ctx, x, dt, alpha, lam, rl, wl, D, tau):
-        ctx.save_for_backward(x, dt, alpha, lam, rl, wl, D, tau)
-        return scan_fwd(x, dt, None, None, alpha, tau, lam=lam, read_logit=rl, write_logit=wl, D=D)
+        cs = chunk_states_like(x, int(tau.shape[0]))
+        ctx.save_for_backward(x, dt, alpha, lam, rl, wl, D, tau, cs)
+        return scan_fwd(x, dt, None, None, alpha, tau, lam=lam, read_logit=rl, write_logit=wl, D=D, chunk_states=cs)
 
     @staticmethod
     def backward(ctx, dy):
-        x, dt, alpha, lam, rl, wl, D, tau = ctx.saved_tensors
+        x, dt, alpha, lam, rl, wl, D, tau, cs = ctx.saved_tensors
         g = scan_bwd(x, dt, None, None, alpha, tau, dy.contiguous(), lam=lam, read_logit=rl, write_logit=wl, D=D,
-                     all_grads=True)
+                     all_grads=True, chunk_states=cs)
         return g["dx"], g["ddt"], g["dalpha"], g["dlambda"], g["dread_logit"], g["dwrite_logit"], g["dD"], None
 
 

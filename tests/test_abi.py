@@ -278,3 +278,32 @@ def test_gated_norm_arguments_are_checked_on_the_host():
     b.fwd = a
     b.dy = b.dx = b.dz = b.dweight = p
     assert lib.frac_gnorm_bwd(ctypes.byref(sh), ctypes.byref(b), None, 0, None) == -3  # no workspace
+
+
+def test_chunk_states_are_sized_and_checked_on_the_host():
+    """The forward keeps the per-chunk states for the backward only without B/C: there
+    they are B H (ceil(L / 64) + 1) M P floats; with B/C the size query and a forward or
+    backward given chunk_states are refused before anything is launched."""
+    lib = _lib.load()
+    n = ctypes.c_size_t(7)
+    sh1 = _shape(dstate=1, headdim=256, nmodes=16, batch=2, seqlen=200)
+    assert lib.frac_chunk_states_size(ctypes.byref(sh1), ctypes.byref(n)) == 0
+    assert n.value == 2 * sh1.nheads * (4 + 1) * 16 * 256 * 4
+    assert lib.frac_chunk_states_size(ctypes.byref(sh1), None) == -1
+    sh = _shape()  # with B/C
+    assert lib.frac_chunk_states_size(ctypes.byref(sh), ctypes.byref(n)) == -2 and n.value == 0
+    buf = (ctypes.c_float * 64)()
+    p = ctypes.cast(buf, ctypes.c_void_p)
+    a = FracFwdArgs()
+    a.x = a.dt = a.alpha = a.tau = a.y = a.Bm = a.Cm = p
+    a.chunk_states = p
+    assert lib.frac_scan_fwd(ctypes.byref(sh), ctypes.byref(a), None, 0, None) == -2
+    assert "dstate 1" in lib.frac_last_error().decode()
+    b = FracBwdArgs()
+    b.fwd = a
+    b.dy = b.dx = b.ddt = b.dBm = b.dCm = p
+    assert lib.frac_scan_bwd(ctypes.byref(sh), ctypes.byref(b), None, 0, None) == -2
+    a.chunk_states = ctypes.c_void_p(0x10004)  # misaligned, without B/C
+    a.Bm = a.Cm = None
+    assert lib.frac_scan_fwd(ctypes.byref(sh1), ctypes.byref(a), None, 0, None) == -1
+    assert "aligned" in lib.frac_last_error().decode()

@@ -307,3 +307,41 @@ def test_nfree_custom_tau_bank():
     assert_close("ddt", f64(g["ddt"]), ref["ddt"], tol)
     assert_close("dD", f64(g["dD"]), ref["dD"], tol)
     _check_further_grads(g, ref, tol, True)
+
+
+@pytest.mark.parametrize("P,M,io", [(256, 16, "bf16"), (192, 8, "bf16"), (64, 4, "f32")])
+def test_chunk_states_from_the_forward_feed_the_backward(P, M, io):
+    """The chunk states the forward keeps: slot 0 is the initial state, slot k the state
+    after the first 64 k tokens (against the oracle's final state on that prefix), the last
+    slot the final state; y and final_state are those of a forward that keeps none, and the
+    backward that reads them returns the gradients of the one that recomputes them."""
+    L = 200
+    w = Workload("t", 2, L, 2, P, 1, M, bc=False, io_dtype=io, extras=True, init_state=True, backward=True,
+                 final_state=True)
+    inp = device_inputs(w, seed=23)
+    tau_d, tau64 = _tau(M)
+    kw = {k: inp[k] for k in ("lam", "read_logit", "write_logit", "D", "init_state")}
+    args = (inp["x"], inp["dt"], None, None, inp["alpha"], tau_d)
+    print("chunk states", P, M, io, flush=True)
+    y0, f0 = frac.scan_fwd(*args, return_final_state=True, **kw)
+    cs = frac.chunk_states_like(inp["x"], M)
+    y1, f1 = frac.scan_fwd(*args, return_final_state=True, chunk_states=cs, **kw)
+    g0 = frac.scan_bwd(*args, inp["dy"], d_final_state=inp.get("d_final_state"), all_grads=True, **kw)
+    g1 = frac.scan_bwd(*args, inp["dy"], d_final_state=inp.get("d_final_state"), all_grads=True, chunk_states=cs, **kw)
+    torch.cuda.synchronize()
+    assert torch.equal(y0, y1) and torch.equal(f0, f1)
+    nch = (L + 63) // 64
+    slots = cs.view(2, 2, nch + 1, M, P)
+    assert torch.equal(slots[:, :, nch], f1[:, :, :, 0, :])
+    assert torch.equal(slots[:, :, 0], inp["init_state"][:, :, :, 0, :])
+    for k in (1, 3):
+        pre = {key: (v[:, :64 * k].contiguous() if isinstance(v, torch.Tensor) and v.dim() >= 2 and v.shape[1] == L
+                     else v) for key, v in inp.items()}
+        _, ref = _oracle_fwd(pre, tau64)
+        assert_close("chunk state %d" % k, f64(slots[:, :, k]), ref[:, :, :, 0, :], TOL[io])
+    for name, v in g0.items():
+        if v is None:
+            continue
+        ref, got = f64(v), f64(g1[name])
+        scale = max(float(np.abs(ref).max()), 1e-30)
+        assert float(np.abs(got - ref).max()) <= 1e-6 * scale, name
