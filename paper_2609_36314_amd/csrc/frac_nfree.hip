@@ -342,8 +342,9 @@ __global__ void __launch_bounds__(64 * NW) frac_nfree_fwd_kernel(ScanParams p, f
 // ---------------------------------------------------------------- backward
 //
 // Reverse sweep over the chunks with the adjoint G_m (M x d_h per head, this
-// workgroup's 64 columns) in accumulator registers and each chunk's entering
-// state S0 read from the checkpoint pass.  Per chunk, with H = dY X^T over this
+// workgroup's 128 or 64 columns) in accumulator registers and each chunk's entering
+// state S0 read from the chunk states (the caller's forward kept them, or the
+// checkpoint pass wrote them).  Per chunk, with H = dY X^T over this
 // workgroup's columns (a partial sum over d_h) and l the chunk log-decays:
 //   dx_t = sum_m kappa_{t,m} e^{-(l_Q - l_t)} G_m + sum_{t'>=t} Gamma_{t',t} dy_t' + D dy_t
 //   dc_{t,m} = e^{-l_t} (S0_m . dy_t) + sum_{k<=t} H_{t,k} kappa_{k,m} e^{-(l_t - l_k)}
