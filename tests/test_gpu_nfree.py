@@ -345,3 +345,36 @@ def test_chunk_states_from_the_forward_feed_the_backward(P, M, io):
         ref, got = f64(v), f64(g1[name])
         scale = max(float(np.abs(ref).max()), 1e-30)
         assert float(np.abs(got - ref).max()) <= 1e-6 * scale, name
+
+
+@pytest.mark.parametrize("L", [0, 1, 64, 65])
+def test_chunk_states_at_chunk_boundaries(L):
+    """Sequences of no token, one token, exactly one chunk and one token past it: the kept
+    states hold ceil(L / 64) + 1 slots, the first the initial state and the last the final
+    state, and a backward that reads them matches one that recomputes them."""
+    w = Workload("t", 1, L, 2, 256, 1, 16, bc=False, extras=True, init_state=True, backward=True, final_state=True)
+    inp = device_inputs(w, seed=24)
+    tau_d, _ = _tau(16)
+    kw = {k: inp[k] for k in ("lam", "read_logit", "write_logit", "D", "init_state")}
+    args = (inp["x"], inp["dt"], None, None, inp["alpha"], tau_d)
+    print("chunk states L", L, flush=True)
+    cs = frac.chunk_states_like(inp["x"], 16)
+    nch = (L + 63) // 64
+    assert cs.numel() == 1 * 2 * (nch + 1) * 16 * 256
+    _, fin = frac.scan_fwd(*args, return_final_state=True, chunk_states=cs, **kw)
+    torch.cuda.synchronize()
+    slots = cs.view(1, 2, nch + 1, 16, 256)
+    assert torch.equal(slots[:, :, 0], inp["init_state"][:, :, :, 0, :])
+    assert torch.equal(slots[:, :, nch], fin[:, :, :, 0, :])
+    if L == 0:
+        return
+    g0 = frac.scan_bwd(*args, inp["dy"], d_final_state=inp.get("d_final_state"), all_grads=True, **kw)
+    g1 = frac.scan_bwd(*args, inp["dy"], d_final_state=inp.get("d_final_state"), all_grads=True, chunk_states=cs,
+                       **kw)
+    torch.cuda.synchronize()
+    for name, v in g0.items():
+        if v is None:
+            continue
+        ref, got = f64(v), f64(g1[name])
+        scale = max(float(np.abs(ref).max()), 1e-30)
+        assert float(np.abs(got - ref).max()) <= 1e-6 * scale, name
