@@ -105,7 +105,8 @@ typedef struct {
  *                writes it when non-NULL (frac_chunk_states_size gives its bytes).  In
  *                frac_bwd_args.fwd, when non-NULL, it is read as frac_scan_fwd wrote it
  *                for the same inputs, in place of the backward's own pass that recomputes
- *                these states (the chunked scan's stored chunk states, Sec. 3.2). */
+ *                these states (the cross-chunk state passing of the appendix on the
+ *                efficient implementation, kept from the forward to the backward). */
 typedef struct {
   const void *x;
   const float *dt;
