@@ -55,3 +55,43 @@ def test_noalloc_forward_replays_in_a_graph(name):
         assert torch.equal(y_g, y_e), rep
         assert torch.equal(fin_g, fin_e), rep
         assert torch.isfinite(y_e.float()).all()
+
+
+@pytest.mark.parametrize("name", list(CASES))
+def test_backward_with_a_caller_workspace_replays_in_a_graph(name):
+    """The backward with every gradient, its workspace and outputs allocated before the
+    capture: each replay gives the bits of an eager call on the same inputs."""
+    w = CASES[name].scaled(backward=True)
+    inp = device_inputs(w, seed=42)
+    tau = torch.from_numpy(oracle.default_tau(w.nmodes).astype(np.float32)).cuda()
+    dy = inp["dy"].clone()
+    Bm, Cm = inp.get("Bm"), inp.get("Cm")
+    kw = {k: inp[k] for k in ("lam", "read_logit", "write_logit", "D", "init_state")}
+    shape = frac._shape(inp["x"], Bm, w.nmodes, 0)
+    ws = torch.empty(max(1, frac.scan_workspace_size(shape, True)), dtype=torch.uint8, device="cuda")
+
+    def call():
+        return frac.scan_bwd(inp["x"], inp["dt"], Bm, Cm, inp["alpha"], tau, dy, all_grads=True, workspace=ws,
+                             d_final_state=inp.get("d_final_state"), **kw)
+
+    print("graph bwd", name, flush=True)
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        call()
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        out_g = call()
+    gen = torch.Generator(device="cpu").manual_seed(6)
+    for rep in range(3):
+        dy.copy_(torch.randn(dy.shape, generator=gen).to(dy.dtype))
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        out_e = call()
+        torch.cuda.synchronize()
+        for k, v in out_e.items():
+            if v is not None:
+                assert torch.equal(out_g[k], v), (rep, k)
