@@ -150,7 +150,7 @@ __device__ __forceinline__ int pair_weights(const ChunkCtl& k, int nv, int M, co
       const float E = Ecur[m];
       const float Enew = E * fexp(-lQ);
       const bool ren = !(Enew >= kRescaleFloor);
-      const float upd = ren ? 1.0f : __frcp_rn(Enew);
+      const float upd = ren ? 1.0f : fast_rcp(Enew);
       const float dec = ell_decay(lh + m * kWQ, ll + m * kWQ, kQ - 1, t);
       if constexpr (ROLE == kState) {
         o[2 * SW] = cw * ea * E;

@@ -346,6 +346,10 @@ __device__ __forceinline__ float ell_decay(const float* lh, const float* ll, int
 // e^x through the hardware exp2 (a multiply and one transcendental).
 __device__ __forceinline__ float fexp(float x) { return __expf(x); }
 
+// 1 / x through the hardware reciprocal (one transcendental, about 1 ulp) for a
+// normal, finite x: a softmax normaliser (>= 1) or a state scale (>= 2^-60).
+__device__ __forceinline__ float fast_rcp(float x) { return __builtin_amdgcn_rcpf(x); }
+
 // 1 - e^{-x} for x >= 0 without cancellation: a short Taylor series where the
 // difference is small, the subtraction elsewhere (relative error <= ~4e-6).
 __device__ __forceinline__ float one_minus_exp_neg(float x) {
@@ -366,7 +370,7 @@ __device__ __forceinline__ void softmax_fast(float* z, int M) {
     z[m] = (m < M) ? __expf(z[m] - mx) : 0.0f;
     sum += z[m];
   }
-  const float inv = __frcp_rn(sum);
+  const float inv = fast_rcp(sum);
 #pragma unroll
   for (int m = 0; m < MP; ++m) z[m] *= inv;
 }
@@ -414,7 +418,7 @@ __device__ __forceinline__ float group_softmax(float z) {
   const float mx = group_allreduce<MP>(z, [](float a, float b) { return fmaxf(a, b); });
   const float e = __expf(z - mx);
   const float sum = group_allreduce<MP>(e, [](float a, float b) { return a + b; });
-  return e * __frcp_rn(sum);
+  return e * fast_rcp(sum);
 }
 
 // The thread index behind an empty asm statement: values derived from it inside

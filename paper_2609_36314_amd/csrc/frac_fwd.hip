@@ -387,7 +387,7 @@ __global__ void __launch_bounds__(512, STATE_ONLY ? 4 : 1) frac_fwd_kernel(ScanP
       const float lhQ = P_lh[m * kWQ + kQ - 1];
       const float Enew = Ecur[m] * fexp(-lhQ);
       const bool ren = !(Enew >= kRescaleFloor);
-      const float upd = ren ? 1.0f : __frcp_rn(Enew);
+      const float upd = ren ? 1.0f : fast_rcp(Enew);
       if constexpr (STATE_ONLY) {  // the state update only: the write weights
         float ww;
         if constexpr (BLK) {

@@ -29,6 +29,8 @@ namespace frac {
 
 namespace {
 
+typedef unsigned int i32x4_t __attribute__((ext_vector_type(4)));  // a 16-byte buffer access
+
 constexpr float kNfSafe = 55.0f;
 constexpr float kNfFloor = 0x1p-60f;
 
@@ -37,22 +39,29 @@ constexpr float kNfFloor = 0x1p-60f;
 // ckpt [B H][nchunks + 1][M][P] (the first pass of the backward).  Without CKPT a
 // non-NULL ckpt receives the same states beside the outputs (the caller's chunk
 // states, which its backward then reads instead of running that pass).
-// NW waves per workgroup, 16 NW columns of d_h: with more waves per workgroup the
-// per-chunk work that does not depend on the columns (the log-decays, the weights,
-// the Gamma tiles) is done once for more columns and split over more waves.
-template <typename T, int MP, bool CKPT, int NW = 4>
+// NW waves per workgroup over 16 NW / NH columns of d_h: with more waves per
+// workgroup the per-chunk work that does not depend on the columns (the
+// log-decays, the weights, the Gamma tiles) is done once for more columns and
+// split over more waves.  With NH = 2 two waves share each 16 columns: both keep
+// the state, and each forms the outputs of one half of the chunk's tokens.
+// Inside a chunk, global addresses are a wave-uniform chunk base plus 32-bit
+// per-lane offsets (the host keeps 64 H d_h below 2^31).
+template <typename T, int MP, bool CKPT, int NW = 4, int NH = 1>
 __global__ void __launch_bounds__(64 * NW) frac_nfree_fwd_kernel(ScanParams p, float* __restrict__ ckpt) {
   constexpr bool kBf16 = sizeof(T) == 2;
   constexpr int MB = (MP + 15) / 16;        // 16-row blocks of modes in the state
-  constexpr int NT = 64 * NW, CW = 16 * NW;  // threads, columns of d_h per workgroup
+  constexpr int CG = NW / NH;               // 16-column groups (waves per token half)
+  constexpr int NT = 64 * NW, CW = 16 * CG;  // threads, columns of d_h per workgroup
   constexpr int XS = kBf16 ? CW + 8 : CW + 4;  // [t][p] tile stride
   constexpr int GS = kBf16 ? 64 + 8 : 64 + 4;  // [t][k] tile stride
+  static_assert(NT % MP == 0, "every (token, mode) pair of a thread has the same mode");
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, li = lane & 15, lg = lane >> 4;
+  const int cg = wave % CG, half = wave / CG;  // column group, token half of the readout
   const int L = p.L, H = p.H, P = p.P, M = p.M;
   const int nps = (P + CW - 1) / CW;
   const int ps = blockIdx.x % nps, bh = blockIdx.x / nps, b = bh / H, h = bh - b * H;
-  const int p0 = ps * CW, pc = p0 + wave * 16 + li;  // this lane's column of d_h
-  const bool active = p0 + wave * 16 < P;
+  const int p0 = ps * CW, pc = p0 + cg * 16 + li;  // this lane's column of d_h
+  const bool active = p0 + cg * 16 < P;
   const int nchunks = (L + kQ - 1) / kQ;
 
   __shared__ __align__(16) T Xs[64 * XS];  // x of the chunk [t][p]
@@ -62,24 +71,36 @@ __global__ void __launch_bounds__(64 * NW) frac_nfree_fwd_kernel(ScanParams p, f
   // stores of one wave (4 tokens x 16 modes, or 8 x 8) over distinct LDS banks
   constexpr int WQ = kQ + 4;
   __shared__ __align__(16) float W[8 * MP * WQ];
-  __shared__ float s_rr[MP], s_lnt[MP], s_E2[2][MP];
-  float* P_om = W;                 // [MP][Q] c e^{-rA_t} E_m   (readout)
-  float* P_v = W + MP * WQ;        // [MP][Q] kappa e^{-r(A_Q-A_t)} upd (update)
-  float* P_O = W + 2 * MP * WQ;    // [MP][Q] c e^{-rA_t}        (Gamma rows)
-  float* P_Vt = W + 3 * MP * WQ;   // [MP][Q] kappa e^{rA_t}, safe modes (Gamma columns)
-  float* P_c = W + 4 * MP * WQ;    // [MP][Q] c, kappa (modes past the factorisation bound)
-  float* P_k = W + 5 * MP * WQ;
-  float* P_lh = W + 6 * MP * WQ;   // [MP][Q] chunk log-decays l_{t,m}, hi and lo parts
-  float* P_ll = W + 7 * MP * WQ;
+  float* P_O = W;                  // [MP][Q] c e^{-rA_t}        (Gamma rows)
+  float* P_Vt = W + MP * WQ;       // [MP][Q] kappa e^{rA_t}, safe modes (Gamma columns)
+  float* P_c = W + 2 * MP * WQ;    // [MP][Q] c, kappa (modes past the factorisation bound)
+  float* P_k = W + 3 * MP * WQ;
+  // chunk log-decays l_{t,m} [MP][Q], hi and lo parts, in two buffers: chunk c's in
+  // buffer c & 1, formed while the previous chunk is processed
+  float* P_L = W + 4 * MP * WQ;
+  // the readout and update weights in the operand type, laid out for the operand reads:
+  // Om [t][m] = c e^{-rA_t} E_m (four modes per read), Vm [m][t] = kappa e^{-r(A_Q-A_t)} upd
+  // (eight tokens per read)
+  constexpr int OS = MP + 4, VS = kBf16 ? kQ + 8 : kQ + 4;
+  __shared__ __align__(16) T Om[kQ * OS];
+  __shared__ __align__(16) T Vm[MP * VS];
+  __shared__ __align__(16) float s_ren[MP];  // the state's rescale factor of the chunk (1: none)
+  __shared__ float s_E2[2][MP];
 
   // Gamma tiles above the diagonal that the intra product reads are never written
   for (int i = tid; i < 64 * GS; i += NT) Gs[i] = (T)0.0f;
-  if (tid < MP) {
-    const float tau = (tid < M) ? p.tau[tid] : 1.0f;
-    s_rr[tid] = (tid < M) ? 1.0f / tau : 0.0f;
-    s_lnt[tid] = (tid < M) ? logf(tau) : 0.0f;
-    s_E2[0][tid] = s_E2[1][tid] = 1.0f;
-  }
+  if (tid < MP) s_E2[0][tid] = s_E2[1][tid] = 1.0f;
+  // the mode of this thread's (token, mode) pairs: its rate and log time constant
+  const int wm = tid % MP;
+  const float wtau = (wm < M) ? p.tau[wm] : 1.0f;
+  const float wr = (wm < M) ? 1.0f / wtau : 0.0f, wlnt = (wm < M) ? logf(wtau) : 0.0f;
+  // without logits the scores of a token are -alpha ln tau_m, whose largest lies at the
+  // smallest or the largest ln tau: the value the group reduction would find
+  const float lnt_lo = group_allreduce<MP>(wm < M ? wlnt : INFINITY, [](float a, float b) { return fminf(a, b); });
+  const float lnt_hi = group_allreduce<MP>(wm < M ? wlnt : -INFINITY, [](float a, float b) { return fmaxf(a, b); });
+  // the rates of all modes for the log-decay sums (lane = token)
+  __shared__ float s_rr[MP];
+  if (tid < MP) s_rr[tid] = wr;
   // the state: S[mb] holds modes 16 mb + 4 lg + r, column pc
   const int64_t sbase = ((int64_t)b * H + h) * (int64_t)M * P;
   floatx4 S[MB];
@@ -95,6 +116,7 @@ __global__ void __launch_bounds__(64 * NW) frac_nfree_fwd_kernel(ScanParams p, f
   const T* xg = reinterpret_cast<const T*>(p.x) + (((int64_t)b * L) * H + h) * P + p0;
   T* yg = reinterpret_cast<T*>(p.y) + (((int64_t)b * L) * H + h) * P + p0;
   const int64_t xstride = (int64_t)H * P;
+  const unsigned xs32 = (unsigned)(H * P);
   const float* dt_bh = p.dt + (int64_t)b * L * H + h;
   const float* al_bh = p.alpha + b * p.as0 + h * p.as2;
   const float* lm_bh = p.lambda ? p.lambda + b * p.ls0 + h * p.ls2 : nullptr;
@@ -103,114 +125,182 @@ __global__ void __launch_bounds__(64 * NW) frac_nfree_fwd_kernel(ScanParams p, f
   const int64_t lg_st = (int64_t)H * M;
   constexpr int E16 = 16 / (int)sizeof(T);  // elements per 16-byte vector
   constexpr int CPR = CW / E16;             // 16-byte vectors per row of this workgroup's columns
-  constexpr int XV = 64 * CPR / NT;         // 16-byte vectors of x per thread and chunk
+  constexpr int XV = 64 * CPR / NT;         // 16-byte vectors of x (and y) per thread and chunk
+  static_assert(XV * NT == 64 * CPR, "the x tile splits evenly over the threads");
 
-  // x and the per-token controls of a chunk, loaded one chunk ahead into registers
+  // Per chunk c, three barriers:
+  //   1. x(c) into LDS, the weights of c (from its log-decays), the loads of x(c + 1)
+  //   2. the Gamma tiles of c; the log-decays of c + 1 (the other buffer); the loads of
+  //      the controls of c + 2
+  //   3. readout and state update of c
+  //   4. the output rows of c to global memory (no barrier: the next chunk writes no
+  //      array this phase reads)
+  // x and the logits of a chunk are loaded one chunk ahead into registers, the
+  // per-token controls (step, order, lambda) two chunks ahead.  Every global access
+  // of the loop goes through a buffer resource whose range ends at the chunk's last
+  // valid token, with per-lane offsets fixed for the whole sequence (past d_h, past
+  // the modes: an offset beyond every range): out-of-range loads return zeros and
+  // out-of-range stores are dropped, so the loop issues every access unconditionally
+  // and a register filled by a load is never merged with a default value.
+  constexpr unsigned kOut = 0x80000000u;
+  const unsigned xs_b = xs32 * (unsigned)sizeof(T);  // bytes between consecutive tokens of x, y
+  auto nv_of = [&](int c) { return max(0, min(kQ, L - c * kQ)); };
+  auto span = [](int nv, int64_t stride, int64_t tail) {  // bytes of rows 0 .. nv - 1
+    return nv > 0 ? (int)min(((int64_t)(nv - 1) * stride + tail), (int64_t)kOut - 1) : 0;
+  };
+  auto rsrc = [](const void* base, int bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, bytes, 0x00020000);
+  };
+  unsigned xoff[XV];  // byte offsets of this thread's 16-byte vectors of the x / y tiles
+#pragma unroll
+  for (int j = 0; j < XV; ++j) {
+    const int i = tid + NT * j, t = i / CPR, col = (i - t * CPR) * E16;
+    xoff[j] = (p0 + col < P) ? (unsigned)t * xs_b + (unsigned)(col * (int)sizeof(T)) : kOut;
+  }
+  const int xtail = (P - p0) * (int)sizeof(T);
   int4 xr[XV];
-  float dt_n, al_n, lam_n;
+  float dt_q = 0.0f, al_q = 1.0f, lam_q = 1.0f;  // raw controls of the chunk after the next one in flight
   constexpr int NPR = (kQ * MP + NT - 1) / NT;  // (token, mode) pairs per thread: pair = t MP + m = tid + NT j
   float rlr[NPR], wlr[NPR];           // the read / write logits of this thread's pairs
-  auto prefetch = [&](int c) {
-    const int t0 = c * kQ, nv = min(kQ, L - t0);
+  unsigned loff[NPR];
+#pragma unroll
+  for (int j = 0; j < NPR; ++j) {
+    const int pr = tid + NT * j, t = pr / MP;
+    loff[j] = (pr < kQ * MP && wm < M) ? (unsigned)(t * (H * M) + wm) * 4u : kOut;
+  }
+  const bool own_wl = wl_bh && wl_bh != rl_bh;  // a separate write-logit array
+  auto prefetch_x = [&](int c) {
+    const int t0 = c * kQ, nv = nv_of(c);
+    const auto rx = rsrc(xg + (int64_t)t0 * xstride, span(nv, xs_b, xtail));
+#pragma unroll
+    for (int j = 0; j < XV; ++j) xr[j] = __builtin_bit_cast(int4, __builtin_amdgcn_raw_buffer_load_b128(rx, xoff[j], 0, 0));
+    const int lb = span(nv, (int64_t)H * M * 4, (int64_t)M * 4);
+    const auto rr = rsrc(rl_bh ? rl_bh + (int64_t)t0 * lg_st : p.tau, rl_bh ? lb : 0);
+    const auto rw = rsrc(own_wl ? wl_bh + (int64_t)t0 * lg_st : p.tau, own_wl ? lb : 0);
+#pragma unroll
+    for (int j = 0; j < NPR; ++j) {
+      rlr[j] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rr, loff[j], 0, 0));
+      wlr[j] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rw, loff[j], 0, 0));
+    }
+  };
+  auto load_controls = [&](int c) {  // lane = token; zeros past the sequence
+    const int t0 = c * kQ, nv = nv_of(c);
+    const auto rd = rsrc(dt_bh + (int64_t)t0 * H, span(nv, (int64_t)H * 4, 4));
+    const auto ra = rsrc(al_bh + (int64_t)t0 * p.as1, span(nv, (int64_t)p.as1 * 4, 4));
+    const auto rl = rsrc(lm_bh ? lm_bh + (int64_t)t0 * p.ls1 : p.tau, lm_bh ? span(nv, (int64_t)p.ls1 * 4, 4) : 0);
+    dt_q = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rd, (unsigned)(lane * H) * 4u, 0, 0));
+    al_q = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(ra, (unsigned)(lane * p.as1) * 4u, 0, 0));
+    lam_q = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rl, (unsigned)(lane * p.ls1) * 4u, 0, 0));
+  };
+  // the effective step of this lane's token (0 past the sequence) from the raw controls
+  auto eff_step = [&](int c) {
+    const float s_eff = lm_bh ? step_factor(lam_q, al_q) : 1.0f;
+    return (lane < nv_of(c)) ? dt_q * s_eff : 0.0f;
+  };
+  // the output rows of chunk c from LDS to global memory, 16 bytes per thread
+  auto store_y = [&](int c) {
+    const auto ry = rsrc(yg + (int64_t)c * kQ * xstride, span(nv_of(c), xs_b, xtail));
 #pragma unroll
     for (int j = 0; j < XV; ++j) {
       const int i = tid + NT * j, t = i / CPR, col = (i - t * CPR) * E16;
-      xr[j] = make_int4(0, 0, 0, 0);
-      if (t < nv && p0 + col < P) xr[j] = *reinterpret_cast<const int4*>(xg + (int64_t)(t0 + t) * xstride + col);
-    }
-    const int tg = t0 + lane;
-    const bool tvalid = lane < nv;
-    dt_n = tvalid ? dt_bh[(int64_t)tg * H] : 0.0f;
-    al_n = tvalid ? al_bh[tg * p.as1] : 1.0f;
-    lam_n = (tvalid && lm_bh) ? lm_bh[tg * p.ls1] : 1.0f;
-#pragma unroll
-    for (int j = 0; j < NPR; ++j) {
-      const int pr = tid + NT * j, t = pr / MP, m = pr - t * MP;
-      const bool ok = pr < kQ * MP && t < nv && m < M;
-      const int64_t ith = (int64_t)(t0 + t) * lg_st + m;
-      rlr[j] = (ok && rl_bh) ? rl_bh[ith] : 0.0f;
-      wlr[j] = (ok && wl_bh && wl_bh != rl_bh) ? wl_bh[ith] : 0.0f;  // unused when the two are one array
+      const int4 v = *reinterpret_cast<const int4*>(Ys + t * XS + col);
+      __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(i32x4_t, v), ry, xoff[j], 0, 0);
     }
   };
-  prefetch(0);
+  // the state entering chunk c as stored for the backward (modes past M, columns past
+  // d_h and the second token half store nothing)
+  unsigned ckoff[MB * 4];
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int m = mb * 16 + lg * 4 + r;
+      ckoff[mb * 4 + r] = (active && half == 0 && m < M && pc < P) ? (unsigned)(m * P + pc) * 4u : kOut;
+    }
+  float dtt_c, al_c;  // the effective step and order of the current chunk (lane = token)
+  load_controls(0);
+  dtt_c = eff_step(0);
+  al_c = al_q;
+  load_controls(1);
+  prefetch_x(0);
+  barrier();  // the rates and scales in LDS
+  chunk_log_decays<MP, NW>(dtt_c, s_rr, P_L, P_L + MP * WQ);
+  barrier();  // the log-decays of the first chunk in LDS
 
   for (int c = 0; c < nchunks; ++c) {
     const int t0 = c * kQ, nv = min(kQ, L - t0);
     const float* Ecur = s_E2[c & 1];
     float* Enext = s_E2[(c + 1) & 1];
-    barrier();  // the previous chunk is done with every LDS array
+    const float* P_lh = P_L + (c & 1) * 2 * MP * WQ;
+    const float* P_ll = P_lh + MP * WQ;
     // ---- x of the chunk into LDS (zeros past the sequence and past d_h)
 #pragma unroll
     for (int j = 0; j < XV; ++j) {
       const int i = tid + NT * j, t = i / CPR, col = (i - t * CPR) * E16;
       *reinterpret_cast<int4*>(Xs + t * XS + col) = xr[j];
     }
-    const bool tvalid = lane < nv;
-    const float dtv = dt_n, al_l = al_n, lam = lam_n;
     if (CKPT || ckpt) {  // the state entering this chunk
-      float* ck = ckpt + ((int64_t)bh * (nchunks + 1) + c) * M * P;
+      const auto rk = rsrc(ckpt + ((int64_t)bh * (nchunks + 1) + c) * M * P, M * P * 4);
 #pragma unroll
       for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int m = mb * 16 + lg * 4 + r;
-          if (active && m < M && pc < P) ck[(int64_t)m * P + pc] = S[mb][r] * Ecur[m];
+          const float v = S[mb][r] * Ecur[m < MP ? m : 0];
+          __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(int, v), rk, ckoff[mb * 4 + r], 0, 0);
         }
     }
-    // ---- per-token controls (lane = token, every wave) and the per-mode log-decays
-    const float s_eff = lm_bh ? step_factor(lam, al_l) : 1.0f;
-    const float dtt_l = tvalid ? dtv * s_eff : 0.0f;
-    chunk_log_decays<MP, NW>(dtt_l, s_rr, P_lh, P_ll);
-    barrier();  // log-decays in LDS
     const bool over = lane < MP && lane < M && !(P_lh[(lane < MP ? lane : 0) * WQ + kQ - 1] <= kNfSafe);
     const int unsafe = (int)(__ballot(over) & ((MP >= 32) ? 0xffffffffull : ((1ull << MP) - 1)));
-    // ---- per (token, mode) weights: pair = t MP + m
+    // ---- per (token, mode) weights: pair = t MP + m, m = wm
 #pragma unroll
     for (int j = 0; j < NPR; ++j) {
-      const int pr = tid + NT * j, t = pr / MP, m = pr - t * MP;
+      const int pr = tid + NT * j, t = pr / MP, m = wm;
       if (pr >= kQ * MP) break;  // wave-uniform
-      const float dtt = __shfl(dtt_l, t, 64), al = __shfl(al_l, t, 64);
+      const float dtt = __shfl(dtt_c, t, 64), al = __shfl(al_c, t, 64);
       const bool valid = t < nv;
-      const float r = s_rr[m], prior = -al * s_lnt[m];
+      const float prior = -al * wlnt;
       const float zc = (m < M) ? prior + rlr[j] : -INFINITY;
       const float zw = (m < M) ? prior + wlr[j] : -INFINITY;
-      const float lhQ = P_lh[m * WQ + kQ - 1];
+      const float lhQ = P_lh[m * WQ + kQ - 1], llQ = P_ll[m * WQ + kQ - 1];
       const float Enew = Ecur[m] * fexp(-lhQ);
       const bool ren = !(Enew >= kNfFloor);
-      const float upd = ren ? 1.0f : __frcp_rn(Enew);
+      const float upd = ren ? 1.0f : fast_rcp(Enew);
+      const float lh = P_lh[m * WQ + t], ll = P_ll[m * WQ + t];
+      const float dQ = __expf(-fmaxf(ell_diff(lhQ, llQ, lh, ll), 0.0f));  // e^{-(l_Q - l_t)}
       if constexpr (CKPT) {  // the state update only: the write weights
         const float ww = valid ? group_softmax<MP>((rl_bh == wl_bh) ? zc : zw) : 0.0f;
-        const float kap = one_minus_exp_neg(dtt * r) * ww;
-        P_v[m * WQ + t] = kap * ell_decay(P_lh + m * WQ, P_ll + m * WQ, kQ - 1, t) * upd;
+        const float kap = one_minus_exp_neg(dtt * wr) * ww;
+        Vm[m * VS + t] = (T)(kap * dQ * upd);
       } else {
-        const float cw = valid ? group_softmax<MP>(zc) : 0.0f;
+        float cw;
+        if (!rl_bh) {  // the scores are the priors: their maximum is known
+          const float e = __expf(zc - fmaxf(-al * lnt_lo, -al * lnt_hi));
+          const float sum = group_allreduce<MP>(e, [](float a, float b) { return a + b; });
+          cw = valid ? e * fast_rcp(sum) : 0.0f;
+        } else {
+          cw = valid ? group_softmax<MP>(zc) : 0.0f;
+        }
         const float ww = (rl_bh == wl_bh) ? cw : (valid ? group_softmax<MP>(zw) : 0.0f);
-        const float lh = P_lh[m * WQ + t];
         const bool safe = lhQ <= kNfSafe;
-        const float kap = one_minus_exp_neg(dtt * r) * ww;
+        const float kap = one_minus_exp_neg(dtt * wr) * ww;
         const float om = cw * fexp(-lh);
         P_O[m * WQ + t] = om;
-        P_om[m * WQ + t] = om * Ecur[m];
-        P_v[m * WQ + t] = kap * ell_decay(P_lh + m * WQ, P_ll + m * WQ, kQ - 1, t) * upd;
         P_Vt[m * WQ + t] = safe ? kap * fexp(lh) : 0.0f;
-        P_c[m * WQ + t] = cw;
-        P_k[m * WQ + t] = kap;
+        Om[t * OS + m] = (T)(om * Ecur[m]);
+        Vm[m * VS + t] = (T)(kap * dQ * upd);
+        if (unsafe) {  // wave-uniform
+          P_c[m * WQ + t] = cw;
+          P_k[m * WQ + t] = kap;
+        }
       }
-      if (pr < MP) Enext[m] = ren ? 1.0f : Enew;
+      if (pr < MP) {
+        Enext[m] = ren ? 1.0f : Enew;
+        s_ren[m] = ren ? Enew : 1.0f;
+      }
     }
-    float renf[MB * 4];
-    bool ren_any = false;
-#pragma unroll
-    for (int mb = 0; mb < MB; ++mb)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int m = mb * 16 + lg * 4 + r;
-        const float Enew = (m < MP) ? Ecur[m] * fexp(-P_lh[(m < MP ? m : 0) * WQ + kQ - 1]) : 1.0f;
-        renf[mb * 4 + r] = Enew;
-        ren_any |= !(Enew >= kNfFloor);
-      }
+    prefetch_x(c + 1);  // this chunk's x and logits are consumed (past the end: nothing is read)
     barrier();  // x and the weights in LDS
-    if (c + 1 < nchunks) prefetch(c + 1);  // the registers of this chunk are consumed
 
     if constexpr (!CKPT) {
     // ---- causal Gamma tiles [t][k] (float32 matrix cores, modes as K)
@@ -240,91 +330,78 @@ __global__ void __launch_bounds__(64 * NW) frac_nfree_fwd_kernel(ScanParams p, f
         Gs[t * GS + k] = (T)keep_if_ge(Gm[r], t, k);
       }
     }
-    barrier();  // Gamma in LDS
     }  // !CKPT
+    // ---- the next chunk's per-token controls and log-decays (the other buffer)
+    if (c + 1 < nchunks) {
+      dtt_c = eff_step(c + 1);
+      al_c = al_q;
+      float* N_lh = P_L + ((c + 1) & 1) * 2 * MP * WQ;
+      chunk_log_decays<MP, NW>(dtt_c, s_rr, N_lh, N_lh + MP * WQ);
+    }
+    load_controls(c + 2);
+    barrier();  // Gamma and the next log-decays in LDS
 
     if (active) {
       if constexpr (!CKPT) {
-      // ---- readout, intra-chunk product and skip term, 4 row blocks of 16 tokens
+      // ---- readout, intra-chunk product and skip term, row blocks of 16 tokens
       Frag<T> Sf;  // the state as a B operand: slot s < 4 mode 4 lg + s, s >= 4 mode 16 + 4 lg + s - 4
 #pragma unroll
       for (int s = 0; s < 4; ++s) frag_set(Sf, s, S[0][s]);
 #pragma unroll
       for (int s = 0; s < 4; ++s) frag_set(Sf, 4 + s, MB > 1 ? S[MB - 1][s] : 0.0f);
 #pragma unroll
-      for (int tb = 0; tb < 4; ++tb) {
-        const int t = tb * 16 + li;  // A-operand row
+      for (int tq = 0; tq < 4 / NH; ++tq) {
+        const int tb = half * (4 / NH) + tq;  // row block of 16 tokens
+        const int t = tb * 16 + li;            // this lane's token (Gamma and O row)
+        // the transposed products (operands swapped): lane (li, lg) accumulates the
+        // outputs of token t at columns cg 16 + 4 lg .. + 3, stored as one vector
         floatx4 Y = {0.f, 0.f, 0.f, 0.f};
-        Frag<T> Of;
+        // slots as in Sf; modes past MP (lane groups beyond MP / 4) are zero
+        const Frag<T> Of = (lg * 4 < MP) ? frag_load4x2(Om + t * OS + lg * 4, Om + t * OS + 16 + lg * 4, MB > 1)
+                                         : frag_zero<T>();
+        mma(Y, Sf, Of);
 #pragma unroll
-        for (int s = 0; s < 4; ++s) {
-          const int m0 = lg * 4 + s, m1 = 16 + lg * 4 + s;
-          frag_set(Of, s, (m0 < MP) ? P_om[m0 * WQ + t] : 0.0f);
-          frag_set(Of, 4 + s, (MB > 1 && m1 < MP) ? P_om[m1 * WQ + t] : 0.0f);
-        }
-        mma(Y, Of, Sf);
-#pragma unroll
-        for (int kk = 0; kk <= tb / 2; ++kk) {
+        for (int kk = 0; kk < 2; ++kk) {
+          if (kk > tb / 2) break;  // wave-uniform
           const Frag<T> a = frag_load8(Gs + t * GS + kk * 32 + lg * 8);
-          const Frag<T> bx = frag_load_rows(Xs, XS, kk * 32 + lg * 8, wave * 16);
-          mma(Y, a, bx);
+          const Frag<T> bx = frag_load_rows(Xs, XS, kk * 32 + lg * 8, cg * 16);
+          mma(Y, bx, a);
         }
         float xv[4];
-        col4_rows(Xs, XS, tb * 16 + lg * 4, wave * 16, xv);
+        load4(Xs + t * XS + cg * 16 + lg * 4, xv);
 #pragma unroll
-        for (int r = 0; r < 4; ++r) Ys[(tb * 16 + lg * 4 + r) * XS + wave * 16 + li] = (T)(Y[r] + Dh * xv[r]);
+        for (int r = 0; r < 4; ++r) Y[r] += Dh * xv[r];
+        store4(Ys + t * XS + cg * 16 + lg * 4, Y);
       }
       }  // !CKPT
 
-      // ---- state update S_m <- (rescale) + V^T x, V = kappa e^{-r(A_Q - A_k)} upd
-      if (ren_any) {
+      // ---- state update S_m <- (rescale) S_m + V^T x, V = kappa e^{-r(A_Q - A_k)} upd
 #pragma unroll
-        for (int mb = 0; mb < MB; ++mb)
+      for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
-          for (int r = 0; r < 4; ++r)
-            if (!(renf[mb * 4 + r] >= kNfFloor)) S[mb][r] *= renf[mb * 4 + r];
-      }
+        for (int r = 0; r < 4; ++r) {
+          const int m = mb * 16 + lg * 4 + r;
+          if (m < MP) S[mb][r] *= s_ren[m];
+        }
 #pragma unroll
       for (int kt = 0; kt < 2; ++kt) {
-        const Frag<T> bx = frag_load_rows(Xs, XS, kt * 32 + lg * 8, wave * 16);
+        const Frag<T> bx = frag_load_rows(Xs, XS, kt * 32 + lg * 8, cg * 16);
 #pragma unroll
         for (int mb = 0; mb < MB; ++mb) {
           const int m = mb * 16 + li;  // A-operand row (mode)
-          Frag<T> Vf;
-          if (m < MP) {
-            const float* pv = P_v + m * WQ + kt * 32 + lg * 8;
-            const float4 v0 = *reinterpret_cast<const float4*>(pv);
-            const float4 v1 = *reinterpret_cast<const float4*>(pv + 4);
-            frag_set(Vf, 0, v0.x);
-            frag_set(Vf, 1, v0.y);
-            frag_set(Vf, 2, v0.z);
-            frag_set(Vf, 3, v0.w);
-            frag_set(Vf, 4, v1.x);
-            frag_set(Vf, 5, v1.y);
-            frag_set(Vf, 6, v1.z);
-            frag_set(Vf, 7, v1.w);
-          } else {
-            Vf = frag_zero<T>();
-          }
+          const Frag<T> Vf = (m < MP) ? frag_load8(Vm + m * VS + kt * 32 + lg * 8) : frag_zero<T>();
           mma(S[mb], Vf, bx);
         }
       }
     }
-    if constexpr (CKPT) continue;
-    barrier();  // output rows in LDS
-    // ---- output rows -> global, 16 bytes per thread
-    for (int i = tid; i < 64 * CPR; i += NT) {
-      const int t = i / CPR, ch = i - t * CPR, col = ch * E16;
-      if (t < nv && p0 + col < P)
-        *reinterpret_cast<int4*>(yg + (int64_t)(t0 + t) * xstride + col) = *reinterpret_cast<const int4*>(Ys + t * XS + col);
-    }
+    barrier();  // output rows in LDS; every array of this chunk is consumed
+    if constexpr (!CKPT) store_y(c);
   }
 
   float* fin_ck = ckpt ? ckpt + ((int64_t)bh * (nchunks + 1) + nchunks) * M * P : nullptr;
   float* fin = (!CKPT && p.final_state) ? p.final_state + sbase : nullptr;
-  if ((fin || fin_ck) && active) {
-    __syncthreads();
-    const float* Ef = s_E2[nchunks & 1];
+  if ((fin || fin_ck) && active && half == 0) {
+    const float* Ef = s_E2[nchunks & 1];  // written before the last chunk's weights barrier
 #pragma unroll
     for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
@@ -844,17 +921,25 @@ int nfree_bwd_cols(const ScanParams& p) { return (p.P > 128 && (p.io_bf16 || p.M
 
 // The forward pass (CKPT: the checkpoint pass of the backward) in workgroups of NW
 // waves, 16 NW columns each.
-template <typename T, int MP, bool CKPT, int NW>
+template <typename T, int MP, bool CKPT, int NW, int NH = 1>
 hipError_t launch_nfree_fwd_nw(const ScanParams& p, float* ckpt, hipStream_t stream) {
-  const unsigned blocks = (unsigned)((int64_t)p.Bsz * p.H * ((p.P + 16 * NW - 1) / (16 * NW)));
-  hipLaunchKernelGGL((frac_nfree_fwd_kernel<T, MP, CKPT, NW>), dim3(blocks), dim3(64 * NW), 0, stream, p, ckpt);
+  constexpr int CW = 16 * (NW / NH);
+  const unsigned blocks = (unsigned)((int64_t)p.Bsz * p.H * ((p.P + CW - 1) / CW));
+  hipLaunchKernelGGL((frac_nfree_fwd_kernel<T, MP, CKPT, NW, NH>), dim3(blocks), dim3(64 * NW), 0, stream, p, ckpt);
   return hipGetLastError();
 }
 
+// Head dims above 128: the outputs in 16 waves over 128 columns (two per 16
+// columns, one per half of the chunk's tokens), the checkpoint pass (no outputs)
+// in 8; float32 inputs with 32 modes in 4 over 64 columns (LDS).
 template <typename T, int MP, bool CKPT>
 hipError_t launch_nfree_fwd(const ScanParams& p, float* ckpt, hipStream_t stream) {
-  return nfree_cols(p) == 128 ? launch_nfree_fwd_nw<T, MP, CKPT, 8>(p, ckpt, stream)
-                              : launch_nfree_fwd_nw<T, MP, CKPT, 4>(p, ckpt, stream);
+  if (nfree_cols(p) == 128) {
+    if constexpr (CKPT) return launch_nfree_fwd_nw<T, MP, CKPT, 8>(p, ckpt, stream);
+    else if constexpr (sizeof(T) == 4 && MP > 16) return launch_nfree_fwd_nw<T, MP, CKPT, 4>(p, ckpt, stream);
+    else return launch_nfree_fwd_nw<T, MP, CKPT, 16, 2>(p, ckpt, stream);
+  }
+  return launch_nfree_fwd_nw<T, MP, CKPT, 4>(p, ckpt, stream);
 }
 
 template <typename T>
