@@ -456,7 +456,7 @@ __global__ void __launch_bounds__(64 * NW, NW == 4 ? 2 : 1) frac_nfree_bwd_kerne
   constexpr int KP = CW / 32;                  // 32-column K steps over this workgroup's columns
   constexpr bool kSplit = NW == 8;
   constexpr int WQ = kWQ;
-  constexpr int NWA = 6;
+  constexpr int NWA = 8;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, li = lane & 15, lg = lane >> 4;
   const int L = p.L, H = p.H, P = p.P, M = p.M;
   const int nps = (P + CW - 1) / CW;
@@ -471,7 +471,7 @@ __global__ void __launch_bounds__(64 * NW, NW == 4 ? 2 : 1) frac_nfree_bwd_kerne
   __shared__ __align__(16) T GT[64 * GS];                      // Gamma^T [t][t'], t' >= t
   constexpr int HS = 64 + 4;
   __shared__ __align__(16) float HT[64 * HS];                  // dY X^T [t][k], k <= t (float32)
-  T* const DX = Xs;  // dx rows [t][p] (bfloat16 staging; x is no longer read by then)
+  __shared__ __align__(16) T DX[kBf16 ? 64 * XS : 8];         // dx rows [t][p] (bfloat16 staging)
   __shared__ __align__(16) float Gt[MP * GQ];                  // the adjoint [m][p]
   __shared__ __align__(16) float W[NWA * MP * WQ];
   __shared__ float s_rr[MP], s_lnt[MP];
@@ -489,8 +489,9 @@ __global__ void __launch_bounds__(64 * NW, NW == 4 ? 2 : 1) frac_nfree_bwd_kerne
   float* P_Vt = W + 1 * SW;   // kappa e^{l} (safe modes), kappa (modes past the factorisation bound)
   float* P_vq = W + 2 * SW;   // kappa e^{-(l_Q - l)}
   float* P_c = W + 3 * SW;    // c (modes past the factorisation bound)
-  float* P_lh = W + 4 * SW;   // chunk log-decays, hi and lo parts
-  float* P_ll = W + 5 * SW;
+  // chunk log-decays [MP][Q], hi and lo parts, in two buffers: chunk c's in buffer
+  // c & 1, formed while the chunk after it is processed
+  float* P_L = W + 4 * SW;
 
   for (int i = tid; i < 64 * GS; i += NT) GT[i] = (T)0.0f;
   for (int i = tid; i < 64 * HS; i += NT) HT[i] = 0.0f;
@@ -547,88 +548,155 @@ __global__ void __launch_bounds__(64 * NW, NW == 4 ? 2 : 1) frac_nfree_bwd_kerne
   constexpr int CPR = CW / E16;
   constexpr int XV = 64 * CPR / NT;
 
+  // Per chunk c (in reverse order), three barriers:
+  //   1. x(c), dy(c) into LDS, the weights of c (from its log-decays), the adjoint into
+  //      LDS, the loads of x, dy and the logits of c - 1
+  //   2. the tiles Gamma^T and H, the per-token products, the loads of the state
+  //      entering c - 1, the log-decays of c - 1 (the other buffer), the loads of the
+  //      controls of c - 2
+  //   3. the per-(token, mode) partials, dx and the adjoint update
+  //   4. the dx rows of c to global memory (bfloat16; no barrier: the next chunk
+  //      writes no array this phase reads)
+  // Global accesses go through buffer resources whose range ends at the chunk's last
+  // valid token, with per-lane offsets fixed for the whole sequence (an offset past
+  // every range where a lane has nothing to access): out-of-range loads return
+  // zeros, out-of-range stores are dropped, and no loaded register is merged with a
+  // default value.
+  constexpr unsigned kOut = 0x80000000u;
+  const unsigned xs_b = (unsigned)(H * P) * (unsigned)sizeof(T);  // bytes between tokens of x, dy, dx
+  auto nv_of = [&](int c) { return c >= 0 ? max(0, min(kQ, L - c * kQ)) : 0; };
+  auto span = [](int nv, int64_t stride, int64_t tail) {  // bytes of rows 0 .. nv - 1
+    return nv > 0 ? (int)min(((int64_t)(nv - 1) * stride + tail), (int64_t)kOut - 1) : 0;
+  };
+  auto rsrc = [](const void* base, int bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, bytes, 0x00020000);
+  };
+  const int xtail = (P - p0) * (int)sizeof(T);
+  unsigned xoff[XV];  // byte offsets of this thread's 16-byte vectors of the x / dy / dx tiles
+#pragma unroll
+  for (int j = 0; j < XV; ++j) {
+    const int i = tid + NT * j, t = i / CPR, col = (i - t * CPR) * E16;
+    xoff[j] = (p0 + col < P) ? (unsigned)t * xs_b + (unsigned)(col * (int)sizeof(T)) : kOut;
+  }
+  const int wm = tid % MP;  // the mode of this thread's (token, mode) pairs (NT is a multiple of MP)
+  static_assert(NT % MP == 0, "every (token, mode) pair of a thread has the same mode");
+  const float wr = s_rr[wm], wlnt = s_lnt[wm];
+  // without logits the scores of a token are -alpha ln tau_m, whose largest lies at the
+  // smallest or the largest ln tau: the value the group reduction would find
+  const float lnt_lo = group_allreduce<MP>(wm < M ? wlnt : INFINITY, [](float a, float b) { return fminf(a, b); });
+  const float lnt_hi = group_allreduce<MP>(wm < M ? wlnt : -INFINITY, [](float a, float b) { return fmaxf(a, b); });
+
   int4 xr[XV], yr[XV];
-  float dt_n, al_n, lam_n;
+  float dt_q = 0.0f, al_q = 1.0f, lam_q = 1.0f;  // raw controls two chunks ahead, in flight
   constexpr int NPR = (kQ * MP + NT - 1) / NT;  // (token, mode) pairs per thread: pair = t MP + m = tid + NT j
   float rlr[NPR], wlr[NPR];           // the read / write logits of this thread's pairs
-  auto prefetch = [&](int c) {
-    const int t0 = c * kQ, nv = min(kQ, L - t0);
+  unsigned loff[NPR];
+#pragma unroll
+  for (int j = 0; j < NPR; ++j) {
+    const int pr = tid + NT * j, t = pr / MP;
+    loff[j] = (pr < kQ * MP && wm < M) ? (unsigned)(t * (H * M) + wm) * 4u : kOut;
+  }
+  const bool own_wl = wl_bh && wl_bh != rl_bh;  // a separate write-logit array
+  auto prefetch = [&](int c) {  // x, dy and the logits of chunk c (nothing past either end)
+    const int t0 = c * kQ, nv = nv_of(c);
+    const int xb = span(nv, xs_b, xtail);
+    const auto rx = rsrc(xg + (int64_t)t0 * xstride, xb);
+    const auto ry = rsrc(yg + (int64_t)t0 * xstride, xb);
 #pragma unroll
     for (int j = 0; j < XV; ++j) {
-      const int i = tid + NT * j, t = i / CPR, col = (i - t * CPR) * E16;
-      xr[j] = yr[j] = make_int4(0, 0, 0, 0);
-      if (t < nv && p0 + col < P) {
-        xr[j] = *reinterpret_cast<const int4*>(xg + (int64_t)(t0 + t) * xstride + col);
-        yr[j] = *reinterpret_cast<const int4*>(yg + (int64_t)(t0 + t) * xstride + col);
-      }
+      xr[j] = __builtin_bit_cast(int4, __builtin_amdgcn_raw_buffer_load_b128(rx, xoff[j], 0, 0));
+      yr[j] = __builtin_bit_cast(int4, __builtin_amdgcn_raw_buffer_load_b128(ry, xoff[j], 0, 0));
     }
-    const int tg = t0 + lane;
-    const bool tvalid = lane < nv;
-    dt_n = tvalid ? dt_bh[(int64_t)tg * H] : 0.0f;
-    al_n = tvalid ? al_bh[tg * p.as1] : 1.0f;
-    lam_n = (tvalid && lm_bh) ? lm_bh[tg * p.ls1] : 1.0f;
+    const int lb = span(nv, (int64_t)H * M * 4, (int64_t)M * 4);
+    const auto rr = rsrc(rl_bh ? rl_bh + (int64_t)t0 * lg_st : p.tau, rl_bh ? lb : 0);
+    const auto rw = rsrc(own_wl ? wl_bh + (int64_t)t0 * lg_st : p.tau, own_wl ? lb : 0);
 #pragma unroll
     for (int j = 0; j < NPR; ++j) {
-      const int pr = tid + NT * j, t = pr / MP, m = pr - t * MP;
-      const bool ok = pr < kQ * MP && t < nv && m < M;
-      const int64_t ith = (int64_t)(t0 + t) * lg_st + m;
-      rlr[j] = (ok && rl_bh) ? rl_bh[ith] : 0.0f;
-      wlr[j] = (ok && wl_bh && wl_bh != rl_bh) ? wl_bh[ith] : 0.0f;  // unused when the two are one array
+      rlr[j] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rr, loff[j], 0, 0));
+      wlr[j] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rw, loff[j], 0, 0));
     }
   };
-  // the state entering a chunk (from the checkpoint pass) as U-product operands:
-  // lane row m = 16 mb + lane % 16, 8 columns p0 + 32 kp + 8 (lane / 16) .. + 7
+  auto load_controls = [&](int c) {  // lane = token; zeros outside the sequence
+    const int t0 = c * kQ, nv = nv_of(c);
+    const auto rd = rsrc(dt_bh + (int64_t)t0 * H, span(nv, (int64_t)H * 4, 4));
+    const auto ra = rsrc(al_bh + (int64_t)t0 * p.as1, span(nv, (int64_t)p.as1 * 4, 4));
+    const auto rl = rsrc(lm_bh ? lm_bh + (int64_t)t0 * p.ls1 : p.tau, lm_bh ? span(nv, (int64_t)p.ls1 * 4, 4) : 0);
+    dt_q = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rd, (unsigned)(lane * H) * 4u, 0, 0));
+    al_q = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(ra, (unsigned)(lane * p.as1) * 4u, 0, 0));
+    lam_q = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rl, (unsigned)(lane * p.ls1) * 4u, 0, 0));
+  };
+  auto eff_step = [&](int c) {  // the effective step of this lane's token (0 past the sequence)
+    const float s_eff = lm_bh ? step_factor(lam_q, al_q) : 1.0f;
+    return (lane < nv_of(c)) ? dt_q * s_eff : 0.0f;
+  };
+  // the state entering a chunk (kept by the forward or written by the checkpoint
+  // pass) as U-product operands: lane row m = 16 mb + lane % 16, 8 columns
+  // p0 + 32 kp + 8 (lane / 16) .. + 7 (P is a multiple of 8: all 8 columns or none)
   float4 s0r[MB][KP][2];
+  unsigned s0off[MB][KP];
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+    for (int kp = 0; kp < KP; ++kp) {
+      const int m = mb * 16 + li, pk = p0 + kp * 32 + lg * 8;
+      s0off[mb][kp] = (doU && m < M && pk < P) ? (unsigned)(m * P + pk) * 4u : kOut;
+    }
   auto prefetch_s0 = [&](int c) {
-    const float* ckc = ck_bh + (int64_t)c * M * P;
+    const auto rs = rsrc(ck_bh + (int64_t)max(c, 0) * M * P, c >= 0 ? M * P * 4 : 0);
 #pragma unroll
     for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
       for (int kp = 0; kp < KP; ++kp) {
-        const int m = mb * 16 + li, pk = p0 + kp * 32 + lg * 8;
-        s0r[mb][kp][0] = s0r[mb][kp][1] = make_float4(0.f, 0.f, 0.f, 0.f);
-        if (doU && m < M && pk < P) {  // P is a multiple of 8: all 8 columns or none
-          const float4* q = reinterpret_cast<const float4*>(ckc + (int64_t)m * P + pk);
-          s0r[mb][kp][0] = q[0];
-          s0r[mb][kp][1] = q[1];
-        }
+        s0r[mb][kp][0] = __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(rs, s0off[mb][kp], 0, 0));
+        s0r[mb][kp][1] = __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(rs, s0off[mb][kp] + 16u, 0, 0));
       }
   };
+  // the per-(token, mode) partials of row block tb = wave & 3 (modes past M store nothing)
+  const int64_t part0 = (int64_t)ps * p.Bsz * H * L + (int64_t)bh * L;  // [nps][B H L][M] row of token 0
+  float dtt_c, al_c;  // the effective step and order of the current chunk (lane = token)
+  load_controls(nchunks - 1);
+  dtt_c = eff_step(nchunks - 1);
+  al_c = al_q;
+  load_controls(nchunks - 2);
   prefetch(nchunks - 1);
   prefetch_s0(nchunks - 1);
+  chunk_log_decays<MP, NW>(dtt_c, s_rr, P_L + ((nchunks - 1) & 1) * 2 * SW, P_L + ((nchunks - 1) & 1) * 2 * SW + SW);
+  barrier();  // the log-decays of the last chunk in LDS
 
   for (int c = nchunks - 1; c >= 0; --c) {
     const int t0 = c * kQ, nv = min(kQ, L - t0);
-    barrier();  // the previous chunk is done with every LDS array
+    const float* P_lh = P_L + (c & 1) * 2 * SW;
+    const float* P_ll = P_lh + SW;
 #pragma unroll
     for (int j = 0; j < XV; ++j) {
       const int i = tid + NT * j, t = i / CPR, col = (i - t * CPR) * E16;
       *reinterpret_cast<int4*>(Xs + t * XS + col) = xr[j];
       *reinterpret_cast<int4*>(Ys + t * XS + col) = yr[j];
     }
-    const bool tvalid = lane < nv;
-    const float dtv = dt_n, al_l = al_n, lam = lam_n;
-    const float s_eff = lm_bh ? step_factor(lam, al_l) : 1.0f;
-    const float dtt_l = tvalid ? dtv * s_eff : 0.0f;
-    chunk_log_decays<MP, NW>(dtt_l, s_rr, P_lh, P_ll);
-    barrier();  // log-decays in LDS
     const bool over = lane < MP && lane < M && !(P_lh[(lane < MP ? lane : 0) * WQ + kQ - 1] <= kNfSafe);
     const int unsafe = (int)(__ballot(over) & ((MP >= 32) ? 0xffffffffull : ((1ull << MP) - 1)));
-    // ---- per (token, mode) weights: pair = t MP + m
+    // ---- per (token, mode) weights: pair = t MP + m, m = wm
 #pragma unroll
     for (int j = 0; j < NPR; ++j) {
-      const int pr = tid + NT * j, t = pr / MP, m = pr - t * MP;
+      const int pr = tid + NT * j, t = pr / MP, m = wm;
       if (pr >= kQ * MP) break;  // wave-uniform
-      const float dtt = __shfl(dtt_l, t, 64), al = __shfl(al_l, t, 64);
+      const float dtt = __shfl(dtt_c, t, 64), al = __shfl(al_c, t, 64);
       const bool valid = t < nv;
-      const float r = s_rr[m], prior = -al * s_lnt[m];
+      const float prior = -al * wlnt;
       const float zc = (m < M) ? prior + rlr[j] : -INFINITY;
       const float zw = (m < M) ? prior + wlr[j] : -INFINITY;
-      const float cw = valid ? group_softmax<MP>(zc) : 0.0f;
+      float cw;
+      if (!rl_bh) {  // the scores are the priors: their maximum is known
+        const float e = __expf(zc - fmaxf(-al * lnt_lo, -al * lnt_hi));
+        const float sum = group_allreduce<MP>(e, [](float a, float b) { return a + b; });
+        cw = valid ? e * fast_rcp(sum) : 0.0f;
+      } else {
+        cw = valid ? group_softmax<MP>(zc) : 0.0f;
+      }
       const float ww = (rl_bh == wl_bh) ? cw : (valid ? group_softmax<MP>(zw) : 0.0f);
       const float lh = P_lh[m * WQ + t];
       const bool safe = P_lh[m * WQ + kQ - 1] <= kNfSafe;
-      const float kap = one_minus_exp_neg(dtt * r) * ww;
+      const float kap = one_minus_exp_neg(dtt * wr) * ww;
       float* o = W + m * WQ + t;
       o[0 * SW] = cw * fexp(-lh);
       o[1 * SW] = safe ? kap * fexp(lh) : kap;
@@ -643,8 +711,8 @@ __global__ void __launch_bounds__(64 * NW, NW == 4 ? 2 : 1) frac_nfree_bwd_kerne
         const int m = mb * 16 + lg * 4 + r;
         if (m < MP) Gt[m * GQ + wave * 16 + li] = G[mb][r];
       }
+    prefetch(c - 1);  // this chunk's x, dy and logits are consumed (before the start: nothing is read)
     barrier();  // x, dy, weights and the adjoint in LDS
-
     // ---- causal tiles: Gamma^T and the masked H = dY X^T into LDS
     for (int tile = wave; tile < 10; tile += NW) {
       const int tb = tile_row(tile), kb = tile_col(tile);
@@ -728,11 +796,8 @@ __global__ void __launch_bounds__(64 * NW, NW == 4 ? 2 : 1) frac_nfree_bwd_kerne
         }
       }
     }
-    // the next chunk's inputs, issued once this chunk's copies have been consumed
-    if (c > 0) {
-      prefetch(c - 1);
-      prefetch_s0(c - 1);
-    }
+    // the state entering the chunk before, once this chunk's copy has been consumed
+    prefetch_s0(c - 1);
     // sum(dy . x) of the chunk for dD (columns past d_h and tokens past the sequence are zero)
     if (p.dD) {
       for (int i = tid; i < 64 * CW; i += NT) {
@@ -740,8 +805,15 @@ __global__ void __launch_bounds__(64 * NW, NW == 4 ? 2 : 1) frac_nfree_bwd_kerne
         dd_acc += to_f32(Xs[t * XS + pcol]) * to_f32(Ys[t * XS + pcol]);
       }
     }
-    barrier();  // Gamma^T and H in LDS
-
+    // ---- the previous chunk's per-token controls and log-decays (the other buffer)
+    if (c > 0) {
+      dtt_c = eff_step(c - 1);
+      al_c = al_q;
+      float* N_lh = P_L + ((c - 1) & 1) * 2 * SW;
+      chunk_log_decays<MP, NW>(dtt_c, s_rr, N_lh, N_lh + SW);
+    }
+    load_controls(c - 2);
+    barrier();  // Gamma^T, H and the previous log-decays in LDS
     {
       // ---- per-(token, mode) partials, tokens of row block tb = wave, modes as columns:
       //   dc_{t,m} = e^{-l_t} (S0_m . dy_t) + sum_{k<=t} H_{t,k} kappa_{k,m} e^{-(l_t - l_k)}
@@ -774,17 +846,19 @@ __global__ void __launch_bounds__(64 * NW, NW == 4 ? 2 : 1) frac_nfree_bwd_kerne
         const bool direct = m < M && ((unsafe >> mm) & 1);
         const float* lhm = P_lh + mm * WQ;
         const float* llm = P_ll + mm * WQ;
+        const int pb = span(nv, (int64_t)M * 4, (int64_t)M * 4);
+        const unsigned po = (m < M) ? (unsigned)((tb * 16 + lg * 4) * M + m) * 4u : kOut;
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int t = tb * 16 + lg * 4 + r;
-          const int64_t i = ((int64_t)ps * p.Bsz * H * L + (int64_t)bh * L + t0 + t) * M + m;  // [nps][B H L][M]
+          const unsigned pi = po + (unsigned)(r * M) * 4u;  // token t, mode m of [nps][B H L][M]
           if (doU) {
             const float ea = fexp(-lhm[t]);
             float dc = ea * Uk[mb][r];
             if (!direct) dc += ea * cI[r];
             else
               for (int k = 0; k <= t; ++k) dc += HT[t * HS + k] * P_Vt[mm * WQ + k] * ell_decay(lhm, llm, t, k);
-            if (m < M && t < nv) wk.dcp[i] = dc;
+            __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(int, dc), rsrc(wk.dcp + (part0 + t0) * M, pb), pi, 0, 0);
           }
           if (doZ) {
             const float dk = ell_decay(lhm, llm, kQ - 1, t) * Zk[mb][r];
@@ -792,10 +866,8 @@ __global__ void __launch_bounds__(64 * NW, NW == 4 ? 2 : 1) frac_nfree_bwd_kerne
             if (!direct) dki = fexp(lhm[t]) * kI[r];
             else
               for (int t2 = t; t2 < 64; ++t2) dki += HT[t2 * HS + t] * P_c[mm * WQ + t2] * ell_decay(lhm, llm, t2, t);
-            if (m < M && t < nv) {
-              wk.dkp[i] = dk;
-              wk.dkip[i] = dki;
-            }
+            __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(int, dk), rsrc(wk.dkp + (part0 + t0) * M, pb), pi, 0, 0);
+            __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(int, dki), rsrc(wk.dkip + (part0 + t0) * M, pb), pi, 0, 0);
           }
         }
       }
@@ -832,7 +904,8 @@ __global__ void __launch_bounds__(64 * NW, NW == 4 ? 2 : 1) frac_nfree_bwd_kerne
           if constexpr (kBf16) {
             DX[tr * XS + wave * 16 + li] = (T)v;
           } else {
-            if (tr < nv && pc < P) dxg[(int64_t)(t0 + tr) * xstride + wave * 16 + li] = (T)v;
+            __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(int, (float)v), rsrc(dxg + (int64_t)t0 * xstride, span(nv, xs_b, xtail)),
+                                                  pc < P ? (unsigned)tr * xs_b + (unsigned)(wave * 16 + li) * 4u : kOut, 0, 0);
           }
         }
       }
@@ -870,12 +943,14 @@ __global__ void __launch_bounds__(64 * NW, NW == 4 ? 2 : 1) frac_nfree_bwd_kerne
         }
       }
     }
-    barrier();  // dx rows in LDS
+    barrier();  // dx rows in LDS; every array of this chunk is consumed
     if constexpr (kBf16) {
-      for (int i = tid; i < 64 * CPR; i += NT) {
-        const int t = i / CPR, col = (i - t * CPR) * E16;
-        if (t < nv && p0 + col < P)
-          *reinterpret_cast<int4*>(dxg + (int64_t)(t0 + t) * xstride + col) = *reinterpret_cast<const int4*>(DX + t * XS + col);
+      const auto rdx = rsrc(dxg + (int64_t)t0 * xstride, span(nv, xs_b, xtail));
+#pragma unroll
+      for (int j = 0; j < XV; ++j) {
+        const int i = tid + NT * j, t = i / CPR, col = (i - t * CPR) * E16;
+        const int4 v = *reinterpret_cast<const int4*>(DX + t * XS + col);
+        __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(i32x4_t, v), rdx, xoff[j], 0, 0);
       }
     }
   }
@@ -914,10 +989,10 @@ __global__ void __launch_bounds__(64 * NW, NW == 4 ? 2 : 1) frac_nfree_bwd_kerne
   }
 }
 
-// Columns of d_h per workgroup: 128 (8 waves) for head dims above 128, else 64 (4
-// waves); the backward of float32 inputs with 32 modes keeps 64 (LDS).
+// Columns of d_h per workgroup: 128 for head dims above 128, else 64; the backward
+// with 32 modes keeps 64 (LDS).
 int nfree_cols(const ScanParams& p) { return p.P > 128 ? 128 : 64; }
-int nfree_bwd_cols(const ScanParams& p) { return (p.P > 128 && (p.io_bf16 || p.M <= 16)) ? 128 : 64; }
+int nfree_bwd_cols(const ScanParams& p) { return (p.P > 128 && p.M <= 16) ? 128 : 64; }
 
 // The forward pass (CKPT: the checkpoint pass of the backward) in workgroups of NW
 // waves, 16 NW columns each.
@@ -989,7 +1064,7 @@ hipError_t launch_nfree_bwd_mp(const ScanParams& p, void* ws, hipStream_t stream
   if (!p.chunk_states && (e = launch_nfree_fwd<T, MP, true>(p, ck, stream)) != hipSuccess) return e;
   const int cw = nfree_bwd_cols(p), nps = (p.P + cw - 1) / cw;
   const unsigned blocks = (unsigned)((int64_t)p.Bsz * p.H * nps);
-  constexpr bool kWide = sizeof(T) == 2 || MP <= 16;  // an 8-wave instance fits the LDS
+  constexpr bool kWide = MP <= 16;  // an 8-wave instance fits the LDS
   if constexpr (kWide) {
     if (cw == 128) hipLaunchKernelGGL((frac_nfree_bwd_kernel<T, MP, 8>), dim3(blocks), dim3(512), 0, stream, p, wk);
     else hipLaunchKernelGGL((frac_nfree_bwd_kernel<T, MP, 4>), dim3(blocks), dim3(256), 0, stream, p, wk);
