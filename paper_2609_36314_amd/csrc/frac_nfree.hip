@@ -452,7 +452,7 @@ __global__ void __launch_bounds__(64 * NW, NW == 4 ? 2 : 1) frac_nfree_bwd_kerne
   constexpr int NT = 64 * NW, CW = 16 * NW;    // threads, columns of d_h per workgroup
   constexpr int XS = kBf16 ? CW + 8 : CW + 4;  // [t][p] tile stride
   constexpr int GS = kBf16 ? 64 + 8 : 64 + 4;  // [t][t'] tile stride
-  constexpr int GQ = CW + 4;                   // row stride of the adjoint [m][p]
+  constexpr int GQ = kBf16 ? CW + 8 : CW + 4;  // row stride of the adjoint [m][p]
   constexpr int KP = CW / 32;                  // 32-column K steps over this workgroup's columns
   constexpr bool kSplit = NW == 8;
   constexpr int WQ = kWQ;
@@ -472,7 +472,13 @@ __global__ void __launch_bounds__(64 * NW, NW == 4 ? 2 : 1) frac_nfree_bwd_kerne
   constexpr int HS = 64 + 4;
   __shared__ __align__(16) float HT[64 * HS];                  // dY X^T [t][k], k <= t (float32)
   __shared__ __align__(16) T DX[kBf16 ? 64 * XS : 8];         // dx rows [t][p] (bfloat16 staging)
-  __shared__ __align__(16) float Gt[MP * GQ];                  // the adjoint [m][p]
+  // the adjoint [m][p] in the operand type: for bfloat16 a rounded value (GtH) and its
+  // rounded remainder (GtL), formed once by the wave that owns the columns
+  __shared__ __align__(16) T GtH[MP * GQ];
+  __shared__ __align__(16) T GtL[kBf16 ? MP * GQ : 8];
+  // the state entering the chunk [m][p], likewise (loaded by all threads, four columns each)
+  __shared__ __align__(16) T S0H[MP * GQ];
+  __shared__ __align__(16) T S0L[kBf16 ? MP * GQ : 8];
   __shared__ __align__(16) float W[NWA * MP * WQ];
   __shared__ float s_rr[MP], s_lnt[MP];
   __shared__ float red[NW][MP > 64 ? MP : 64];
@@ -630,26 +636,21 @@ __global__ void __launch_bounds__(64 * NW, NW == 4 ? 2 : 1) frac_nfree_bwd_kerne
     return (lane < nv_of(c)) ? dt_q * s_eff : 0.0f;
   };
   // the state entering a chunk (kept by the forward or written by the checkpoint
-  // pass) as U-product operands: lane row m = 16 mb + lane % 16, 8 columns
-  // p0 + 32 kp + 8 (lane / 16) .. + 7 (P is a multiple of 8: all 8 columns or none)
-  float4 s0r[MB][KP][2];
-  unsigned s0off[MB][KP];
+  // pass), four consecutive columns per thread: element e = 4 (tid + NT q) of the
+  // [MP][CW] tile, staged into LDS (rounded value and remainder) for the U products
+  constexpr int S4 = (MP * CW / 4 + NT - 1) / NT;
+  float4 s0q[S4];
+  unsigned s0off[S4];
 #pragma unroll
-  for (int mb = 0; mb < MB; ++mb)
-#pragma unroll
-    for (int kp = 0; kp < KP; ++kp) {
-      const int m = mb * 16 + li, pk = p0 + kp * 32 + lg * 8;
-      s0off[mb][kp] = (doU && m < M && pk < P) ? (unsigned)(m * P + pk) * 4u : kOut;
-    }
+  for (int q = 0; q < S4; ++q) {
+    const int e = 4 * (tid + NT * q), m = e / CW, col = e - m * CW;
+    s0off[q] = (e < MP * CW && m < M && p0 + col < P) ? (unsigned)(m * P + p0 + col) * 4u : kOut;
+  }
   auto prefetch_s0 = [&](int c) {
     const auto rs = rsrc(ck_bh + (int64_t)max(c, 0) * M * P, c >= 0 ? M * P * 4 : 0);
 #pragma unroll
-    for (int mb = 0; mb < MB; ++mb)
-#pragma unroll
-      for (int kp = 0; kp < KP; ++kp) {
-        s0r[mb][kp][0] = __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(rs, s0off[mb][kp], 0, 0));
-        s0r[mb][kp][1] = __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(rs, s0off[mb][kp] + 16u, 0, 0));
-      }
+    for (int q = 0; q < S4; ++q)
+      s0q[q] = __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(rs, s0off[q], 0, 0));
   };
   // the per-(token, mode) partials of row block tb = wave & 3 (modes past M store nothing)
   const int64_t part0 = (int64_t)ps * p.Bsz * H * L + (int64_t)bh * L;  // [nps][B H L][M] row of token 0
@@ -672,6 +673,20 @@ __global__ void __launch_bounds__(64 * NW, NW == 4 ? 2 : 1) frac_nfree_bwd_kerne
       const int i = tid + NT * j, t = i / CPR, col = (i - t * CPR) * E16;
       *reinterpret_cast<int4*>(Xs + t * XS + col) = xr[j];
       *reinterpret_cast<int4*>(Ys + t * XS + col) = yr[j];
+    }
+#pragma unroll
+    for (int q = 0; q < S4; ++q) {
+      const int e = 4 * (tid + NT * q), m = e / CW, col = e - m * CW;
+      if (e < MP * CW) {
+        const floatx4 v = {s0q[q].x, s0q[q].y, s0q[q].z, s0q[q].w};
+        store4(S0H + m * GQ + col, v);
+        if constexpr (kBf16) {
+          floatx4 lo;
+#pragma unroll
+          for (int i = 0; i < 4; ++i) lo[i] = v[i] - to_f32((T)v[i]);
+          store4(S0L + m * GQ + col, lo);
+        }
+      }
     }
     const bool over = lane < MP && lane < M && !(P_lh[(lane < MP ? lane : 0) * WQ + kQ - 1] <= kNfSafe);
     const int unsafe = (int)(__ballot(over) & ((MP >= 32) ? 0xffffffffull : ((1ull << MP) - 1)));
@@ -709,9 +724,14 @@ __global__ void __launch_bounds__(64 * NW, NW == 4 ? 2 : 1) frac_nfree_bwd_kerne
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int m = mb * 16 + lg * 4 + r;
-        if (m < MP) Gt[m * GQ + wave * 16 + li] = G[mb][r];
+        if (m < MP) {
+          const T g = (T)G[mb][r];
+          GtH[m * GQ + wave * 16 + li] = g;
+          if constexpr (kBf16) GtL[m * GQ + wave * 16 + li] = (T)(G[mb][r] - to_f32(g));
+        }
       }
     prefetch(c - 1);  // this chunk's x, dy and logits are consumed (before the start: nothing is read)
+    prefetch_s0(c - 1);  // and its entering state
     barrier();  // x, dy, weights and the adjoint in LDS
     // ---- causal tiles: Gamma^T and the masked H = dY X^T into LDS
     for (int tile = wave; tile < 10; tile += NW) {
@@ -765,39 +785,26 @@ __global__ void __launch_bounds__(64 * NW, NW == 4 ? 2 : 1) frac_nfree_bwd_kerne
 #pragma unroll
         for (int kp = 0; kp < KP; ++kp) {
           if (doU) {
-            const float4 a0 = s0r[mb][kp][0], a1 = s0r[mb][kp][1];
-            const float sv[8] = {a0.x, a0.y, a0.z, a0.w, a1.x, a1.y, a1.z, a1.w};
-            Frag<T> S0f;
-#pragma unroll
-            for (int s = 0; s < 8; ++s) frag_set(S0f, s, sv[s]);
             const Frag<T> yf = frag_load8(Ys + (tb * 16 + li) * XS + kp * 32 + lg * 8);
+            const Frag<T> S0f = (m < MP) ? frag_load8(S0H + m * GQ + kp * 32 + lg * 8) : frag_zero<T>();
             mma(U, yf, S0f);
             if constexpr (kBf16) {  // the remainder
-#pragma unroll
-              for (int s = 0; s < 8; ++s) frag_set(S0f, s, sv[s] - to_f32((T)sv[s]));
-              mma(U, yf, S0f);
+              const Frag<T> S0l = (m < MP) ? frag_load8(S0L + m * GQ + kp * 32 + lg * 8) : frag_zero<T>();
+              mma(U, yf, S0l);
             }
           }
           if (doZ) {
-            float gv[8];
-#pragma unroll
-            for (int s = 0; s < 8; ++s) gv[s] = (m < MP) ? Gt[m * GQ + kp * 32 + lg * 8 + s] : 0.0f;
-            Frag<T> Gf;
-#pragma unroll
-            for (int s = 0; s < 8; ++s) frag_set(Gf, s, gv[s]);
             const Frag<T> xf = frag_load8(Xs + (tb * 16 + li) * XS + kp * 32 + lg * 8);
+            const Frag<T> Gf = (m < MP) ? frag_load8(GtH + m * GQ + kp * 32 + lg * 8) : frag_zero<T>();
             mma(Z, xf, Gf);
             if constexpr (kBf16) {  // the remainder
-#pragma unroll
-              for (int s = 0; s < 8; ++s) frag_set(Gf, s, gv[s] - to_f32((T)gv[s]));
-              mma(Z, xf, Gf);
+              const Frag<T> Gl = (m < MP) ? frag_load8(GtL + m * GQ + kp * 32 + lg * 8) : frag_zero<T>();
+              mma(Z, xf, Gl);
             }
           }
         }
       }
     }
-    // the state entering the chunk before, once this chunk's copy has been consumed
-    prefetch_s0(c - 1);
     // sum(dy . x) of the chunk for dD (columns past d_h and tokens past the sequence are zero)
     if (p.dD) {
       for (int i = tid; i < 64 * CW; i += NT) {
@@ -827,21 +834,42 @@ __global__ void __launch_bounds__(64 * NW, NW == 4 ? 2 : 1) frac_nfree_bwd_kerne
         const int mm = m < MP ? m : 0;
         const bool fac = m < MP && !((unsafe >> mm) & 1);
         floatx4 cI = {0.f, 0.f, 0.f, 0.f}, kI = {0.f, 0.f, 0.f, 0.f};
+        // 16 tokens of K per step: four reads issued together, two accumulators
         if (doU) {
-          for (int kq = 0; kq < (tb + 1) * 4; ++kq) {
-            const int k = kq * 4 + lg;
-            const float a = HT[(tb * 16 + li) * HS + k];
-            const float bb = fac ? P_Vt[mm * WQ + k] : 0.0f;
-            cI = __builtin_amdgcn_mfma_f32_16x16x4f32(a, bb, cI, 0, 0, 0);
+          floatx4 c1 = {0.f, 0.f, 0.f, 0.f};
+          for (int k4 = 0; k4 <= tb; ++k4) {
+            float a[4], bb[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+              const int k = (k4 * 4 + u) * 4 + lg;
+              a[u] = HT[(tb * 16 + li) * HS + k];
+              bb[u] = fac ? P_Vt[mm * WQ + k] : 0.0f;
+            }
+#pragma unroll
+            for (int u = 0; u < 4; u += 2) {
+              cI = __builtin_amdgcn_mfma_f32_16x16x4f32(a[u], bb[u], cI, 0, 0, 0);
+              c1 = __builtin_amdgcn_mfma_f32_16x16x4f32(a[u + 1], bb[u + 1], c1, 0, 0, 0);
+            }
           }
+          cI += c1;
         }
         if (doZ) {
-          for (int tq = tb * 4; tq < 16; ++tq) {
-            const int t = tq * 4 + lg;
-            const float a = HT[t * HS + tb * 16 + li];
-            const float bb = fac ? P_O[mm * WQ + t] : 0.0f;
-            kI = __builtin_amdgcn_mfma_f32_16x16x4f32(a, bb, kI, 0, 0, 0);
+          floatx4 k1 = {0.f, 0.f, 0.f, 0.f};
+          for (int t4 = tb; t4 < 4; ++t4) {
+            float a[4], bb[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+              const int t = (t4 * 4 + u) * 4 + lg;
+              a[u] = HT[t * HS + tb * 16 + li];
+              bb[u] = fac ? P_O[mm * WQ + t] : 0.0f;
+            }
+#pragma unroll
+            for (int u = 0; u < 4; u += 2) {
+              kI = __builtin_amdgcn_mfma_f32_16x16x4f32(a[u], bb[u], kI, 0, 0, 0);
+              k1 = __builtin_amdgcn_mfma_f32_16x16x4f32(a[u + 1], bb[u + 1], k1, 0, 0, 0);
+            }
           }
+          kI += k1;
         }
         const bool direct = m < M && ((unsafe >> mm) & 1);
         const float* lhm = P_lh + mm * WQ;
