@@ -30,6 +30,7 @@ namespace frac {
 namespace {
 
 typedef unsigned int i32x4_t __attribute__((ext_vector_type(4)));  // a 16-byte buffer access
+typedef unsigned int u32x2_t __attribute__((ext_vector_type(2)));  // an 8-byte buffer access
 
 constexpr float kNfSafe = 55.0f;
 constexpr float kNfFloor = 0x1p-60f;
@@ -402,6 +403,399 @@ __global__ void __launch_bounds__(64 * NW) frac_nfree_fwd_kernel(ScanParams p, f
   float* fin = (!CKPT && p.final_state) ? p.final_state + sbase : nullptr;
   if ((fin || fin_ck) && active && half == 0) {
     const float* Ef = s_E2[nchunks & 1];  // written before the last chunk's weights barrier
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int m = mb * 16 + lg * 4 + r;
+        if (m < M && pc < P) {
+          const float v = S[mb][r] * Ef[m];
+          if (fin) fin[(int64_t)m * P + pc] = v;
+          if (fin_ck) fin_ck[(int64_t)m * P + pc] = v;
+        }
+      }
+  }
+}
+
+// ------------------------------------------------ forward, split waves
+//
+// Head dims above 128: one workgroup of 16 waves per (batch, head, 128 columns),
+// in two roles with one barrier per iteration.  Producer waves 8 .. 15 form, in
+// iteration i, the log-decays of chunk i + 2, the weights of chunk i + 1 (from the
+// log-decays formed one iteration earlier) and the Gamma tiles of chunk i (from the
+// weights formed one iteration earlier).  Consumer waves 0 .. 7 each own 16 columns
+// and, in iteration i, run chunk i - 1: x into their own columns of LDS, readout,
+// intra-chunk product and skip term (outputs stored from registers), the state
+// update.  The per-chunk work that does not depend on the state thus overlaps the
+// recurrence; buffers are kept for as many chunks as are in flight (log-decays,
+// readout and update weights: three; Gamma and its factors: two).
+template <typename T, int MP>
+__global__ void __launch_bounds__(1024) frac_nfree_fwd_split_kernel(ScanParams p, float* __restrict__ ckpt) {
+  constexpr bool kBf16 = sizeof(T) == 2;
+  constexpr int MB = (MP + 15) / 16;
+  constexpr int CW = 128, NPW = 8, NPT = 64 * NPW;  // columns, producer waves, producer threads
+  constexpr int XS = kBf16 ? CW + 8 : CW + 4;
+  constexpr int GS = kBf16 ? 64 + 8 : 64 + 4;
+  constexpr int WQ = kQ + 4;
+  constexpr int OS = MP + 4, VS = kBf16 ? kQ + 8 : kQ + 4;
+  constexpr int ES = (int)sizeof(T);
+  static_assert(NPT % MP == 0, "every (token, mode) pair of a producer thread has the same mode");
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, li = lane & 15, lg = lane >> 4;
+  const bool producer = wave >= 8;
+  const int pt = tid - NPT, pw = wave - 8;  // producer thread and wave (when producer)
+  const int L = p.L, H = p.H, P = p.P, M = p.M;
+  const int nps = (P + CW - 1) / CW;
+  const int ps = blockIdx.x % nps, bh = blockIdx.x / nps, b = bh / H, h = bh - b * H;
+  const int p0 = ps * CW;
+  const int cg = wave & 7, pc = p0 + cg * 16 + li;  // consumer column group and lane column
+  const bool active = !producer && p0 + cg * 16 < P;
+  const int nchunks = (L + kQ - 1) / kQ;
+
+  __shared__ __align__(16) T Xs[64 * XS];          // x of the consumers' chunk [t][p]
+  __shared__ __align__(16) T Gb[2][64 * GS];       // Gamma [t][k] of chunk j in Gb[j & 1]
+  __shared__ __align__(16) float LDb[3][2 * MP * WQ];  // log-decays (hi, lo) [MP][Q] of chunk j in LDb[j % 3]
+  __shared__ __align__(16) float Wb[2][4 * MP * WQ];   // Gamma factors c e^{-l}, kappa e^{l}; c, kappa (unsafe modes)
+  __shared__ __align__(16) T Omb[3][kQ * OS];      // readout weights [t][m] of chunk j in slot j % 3
+  __shared__ __align__(16) T Vmb[3][MP * VS];      // update weights [m][t]
+  __shared__ __align__(16) float s_ren[3][MP];     // the state's rescale factor of chunk j
+  __shared__ float s_Ein[3][MP];                   // the state scale entering chunk j
+  __shared__ float s_E[2][MP];                     // the running state scale (producers)
+  __shared__ float s_rr[MP];
+
+  for (int i = tid; i < 2 * 64 * GS; i += 1024) (&Gb[0][0])[i] = (T)0.0f;  // tiles above the diagonal stay zero
+  const int wm = (producer ? pt : tid) % MP;
+  const float wtau = (wm < M) ? p.tau[wm] : 1.0f;
+  const float wr = (wm < M) ? 1.0f / wtau : 0.0f, wlnt = (wm < M) ? logf(wtau) : 0.0f;
+  const float lnt_lo = group_allreduce<MP>(wm < M ? wlnt : INFINITY, [](float a, float b) { return fminf(a, b); });
+  const float lnt_hi = group_allreduce<MP>(wm < M ? wlnt : -INFINITY, [](float a, float b) { return fmaxf(a, b); });
+  if (tid < MP) {
+    s_rr[tid] = wr;
+    s_E[0][tid] = 1.0f;
+  }
+
+  constexpr unsigned kOut = 0x80000000u;
+  const int64_t xstride = (int64_t)H * P;
+  const unsigned xs_b = (unsigned)(H * P) * (unsigned)ES;
+  const T* xg = reinterpret_cast<const T*>(p.x) + (((int64_t)b * L) * H + h) * P + p0;
+  T* yg = reinterpret_cast<T*>(p.y) + (((int64_t)b * L) * H + h) * P + p0;
+  const float* dt_bh = p.dt + (int64_t)b * L * H + h;
+  const float* al_bh = p.alpha + b * p.as0 + h * p.as2;
+  const float* lm_bh = p.lambda ? p.lambda + b * p.ls0 + h * p.ls2 : nullptr;
+  const float* rl_bh = p.read_logit ? p.read_logit + ((int64_t)b * L * H + h) * M : nullptr;
+  const float* wl_bh = p.write_logit ? p.write_logit + ((int64_t)b * L * H + h) * M : nullptr;
+  const bool own_wl = wl_bh && wl_bh != rl_bh;
+  const int64_t lg_st = (int64_t)H * M;
+  const int xtail = (P - p0) * ES;
+  auto nv_of = [&](int c) { return (c >= 0 && c < nchunks) ? min(kQ, L - c * kQ) : 0; };
+  auto span = [](int nv, int64_t stride, int64_t tail) {
+    return nv > 0 ? (int)min(((int64_t)(nv - 1) * stride + tail), (int64_t)kOut - 1) : 0;
+  };
+  auto rsrc = [](const void* base, int bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, bytes, 0x00020000);
+  };
+
+  // ---- producer state: raw controls two chunks ahead (lane = token), the effective
+  // step and order of the chunk whose weights come next, the logits of those weights
+  constexpr int NPR = (kQ * MP + NPT - 1) / NPT;
+  float dt_q = 0.0f, al_q = 1.0f, lam_q = 1.0f;
+  float w_dtt = 0.0f, w_al = 1.0f;
+  float rlr[NPR], wlr[NPR];
+  unsigned loff[NPR];
+#pragma unroll
+  for (int j = 0; j < NPR; ++j) {
+    const int pr = pt + NPT * j, t = pr / MP;
+    loff[j] = (producer && pr < kQ * MP && wm < M) ? (unsigned)(t * (H * M) + wm) * 4u : kOut;
+  }
+  auto load_controls = [&](int c) {
+    const int t0 = c * kQ, nv = nv_of(c);
+    const auto rd = rsrc(dt_bh + (int64_t)t0 * H, span(nv, (int64_t)H * 4, 4));
+    const auto ra = rsrc(al_bh + (int64_t)t0 * p.as1, span(nv, (int64_t)p.as1 * 4, 4));
+    const auto rl = rsrc(lm_bh ? lm_bh + (int64_t)t0 * p.ls1 : p.tau, lm_bh ? span(nv, (int64_t)p.ls1 * 4, 4) : 0);
+    dt_q = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rd, (unsigned)(lane * H) * 4u, 0, 0));
+    al_q = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(ra, (unsigned)(lane * p.as1) * 4u, 0, 0));
+    lam_q = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rl, (unsigned)(lane * p.ls1) * 4u, 0, 0));
+  };
+  auto eff_step = [&](int c) {
+    const float s_eff = lm_bh ? step_factor(lam_q, al_q) : 1.0f;
+    return (lane < nv_of(c)) ? dt_q * s_eff : 0.0f;
+  };
+  auto load_logits = [&](int c) {
+    const int t0 = c * kQ, nv = nv_of(c);
+    const int lb = span(nv, (int64_t)H * M * 4, (int64_t)M * 4);
+    const auto rr = rsrc(rl_bh ? rl_bh + (int64_t)t0 * lg_st : p.tau, rl_bh ? lb : 0);
+    const auto rw = rsrc(own_wl ? wl_bh + (int64_t)t0 * lg_st : p.tau, own_wl ? lb : 0);
+#pragma unroll
+    for (int j = 0; j < NPR; ++j) {
+      rlr[j] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rr, loff[j], 0, 0));
+      wlr[j] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rw, loff[j], 0, 0));
+    }
+  };
+  // the per-mode log-decays of chunk c from this lane's effective step (producer wave pw: modes pw, pw + 8, ..)
+  auto log_decays = [&](int c, float dtt) {
+    float* lh = LDb[c % 3];
+#pragma unroll
+    for (int m0 = 0; m0 < MP; m0 += NPW) {
+      const int m = m0 + pw;
+      if (m0 + NPW > MP && m >= MP) break;  // wave-uniform
+      const double v = wave_inclusive_sum_f64((double)capped_exponent(s_rr[m], dtt));
+      const float hi = (float)v;
+      lh[m * WQ + lane] = hi;
+      lh[MP * WQ + m * WQ + lane] = (float)(v - (double)hi);
+    }
+  };
+  auto unsafe_of = [&](int c) {
+    const float* lh = LDb[c % 3];
+    const bool over = lane < MP && lane < M && !(lh[(lane < MP ? lane : 0) * WQ + kQ - 1] <= kNfSafe);
+    return (int)(__ballot(over) & ((MP >= 32) ? 0xffffffffull : ((1ull << MP) - 1)));
+  };
+  // the weights of chunk c: the Gamma factors, the readout and update weights, the
+  // state scale and rescale
+  auto weights = [&](int c) {
+    const float* P_lh = LDb[c % 3];
+    const float* P_ll = P_lh + MP * WQ;
+    float* W = Wb[c & 1];
+    T* Om = Omb[c % 3];
+    T* Vm = Vmb[c % 3];
+    const float* Ecur = s_E[c & 1];
+    float* Enext = s_E[(c + 1) & 1];
+    const int nv = nv_of(c), unsafe = unsafe_of(c);
+#pragma unroll
+    for (int j = 0; j < NPR; ++j) {
+      const int pr = pt + NPT * j, t = pr / MP, m = wm;
+      if (pr >= kQ * MP) break;  // wave-uniform
+      const float dtt = __shfl(w_dtt, t, 64), al = __shfl(w_al, t, 64);
+      const bool valid = t < nv;
+      const float prior = -al * wlnt;
+      const float zc = (m < M) ? prior + rlr[j] : -INFINITY;
+      const float zw = (m < M) ? prior + wlr[j] : -INFINITY;
+      const float lhQ = P_lh[m * WQ + kQ - 1], llQ = P_ll[m * WQ + kQ - 1];
+      const float Ec = Ecur[m];
+      const float Enew = Ec * fexp(-lhQ);
+      const bool ren = !(Enew >= kNfFloor);
+      const float upd = ren ? 1.0f : fast_rcp(Enew);
+      const float lh = P_lh[m * WQ + t], ll = P_ll[m * WQ + t];
+      const float dQ = __expf(-fmaxf(ell_diff(lhQ, llQ, lh, ll), 0.0f));  // e^{-(l_Q - l_t)}
+      float cw;
+      if (!rl_bh) {  // the scores are the priors: their maximum is known
+        const float e = __expf(zc - fmaxf(-al * lnt_lo, -al * lnt_hi));
+        const float sum = group_allreduce<MP>(e, [](float a, float b) { return a + b; });
+        cw = valid ? e * fast_rcp(sum) : 0.0f;
+      } else {
+        cw = valid ? group_softmax<MP>(zc) : 0.0f;
+      }
+      const float ww = (rl_bh == wl_bh) ? cw : (valid ? group_softmax<MP>(zw) : 0.0f);
+      const bool safe = lhQ <= kNfSafe;
+      const float kap = one_minus_exp_neg(dtt * wr) * ww;
+      const float om = cw * fexp(-lh);
+      W[m * WQ + t] = om;
+      W[MP * WQ + m * WQ + t] = safe ? kap * fexp(lh) : 0.0f;
+      Om[t * OS + m] = (T)(om * Ec);
+      Vm[m * VS + t] = (T)(kap * dQ * upd);
+      if (unsafe) {  // wave-uniform
+        W[2 * MP * WQ + m * WQ + t] = cw;
+        W[3 * MP * WQ + m * WQ + t] = kap;
+      }
+      if (pr < MP) {
+        Enext[m] = ren ? 1.0f : Enew;
+        s_ren[c % 3][m] = ren ? Enew : 1.0f;
+        s_Ein[c % 3][m] = Ec;
+      }
+    }
+  };
+  // causal Gamma tile `tile` of chunk c (modes as K; one exponential per pair for the
+  // modes past the factorisation bound)
+  auto gamma = [&](int c, int tile) {
+    const float* P_lh = LDb[c % 3];
+    const float* P_ll = P_lh + MP * WQ;
+    const float* W = Wb[c & 1];
+    T* Gs = Gb[c & 1];
+    const int unsafe = unsafe_of(c);
+    {
+      const int tb = tile_row(tile), kb = tile_col(tile);
+      floatx4 Gm = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int q = 0; q < (MP + 3) / 4; ++q) {
+        const int m = q * 4 + lg;
+        const float av = (m < MP) ? W[m * WQ + tb * 16 + li] : 0.0f;
+        const float bv = (m < MP) ? W[MP * WQ + m * WQ + kb * 16 + li] : 0.0f;
+        Gm = __builtin_amdgcn_mfma_f32_16x16x4f32(av, bv, Gm, 0, 0, 0);
+      }
+      if (unsafe) {
+        for (int m = 0; m < MP; ++m) {
+          if (!((unsafe >> m) & 1)) continue;
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int t = tb * 16 + lg * 4 + r, k = kb * 16 + li;
+            if (t >= k)
+              Gm[r] += W[2 * MP * WQ + m * WQ + t] * W[3 * MP * WQ + m * WQ + k] * ell_decay(P_lh + m * WQ, P_ll + m * WQ, t, k);
+          }
+        }
+      }
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int t = tb * 16 + lg * 4 + r, k = kb * 16 + li;
+        Gs[t * GS + k] = (T)keep_if_ge(Gm[r], t, k);
+      }
+    }
+  };
+
+  // ---- consumer state: the state slice, x of the next chunk (lane = token, two
+  // 16-byte vectors of this wave's 16 columns)
+  const int64_t sbase = ((int64_t)b * H + h) * (int64_t)M * P;
+  floatx4 S[MB];
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int m = mb * 16 + lg * 4 + r;
+      S[mb][r] = (p.init_state && active && m < M && pc < P) ? p.init_state[sbase + (int64_t)m * P + pc] : 0.0f;
+    }
+  const float Dh = p.D ? p.D[h] : 0.0f;
+  constexpr int XV = 16 * ES / 16;  // 16-byte vectors per row of a wave's 16 columns
+  int4 xr[XV];
+  unsigned xoff[XV];
+#pragma unroll
+  for (int v = 0; v < XV; ++v) {
+    const int col = cg * 16 + v * (16 / ES);
+    xoff[v] = (active && p0 + col < P) ? (unsigned)lane * xs_b + (unsigned)(col * ES) : kOut;
+  }
+  auto load_x = [&](int c) {
+    const auto rx = rsrc(xg + (int64_t)max(c, 0) * kQ * xstride, span(nv_of(c), xs_b, xtail));
+#pragma unroll
+    for (int v = 0; v < XV; ++v) xr[v] = __builtin_bit_cast(int4, __builtin_amdgcn_raw_buffer_load_b128(rx, xoff[v], 0, 0));
+  };
+  unsigned ckoff[MB * 4];
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int m = mb * 16 + lg * 4 + r;
+      ckoff[mb * 4 + r] = (active && m < M && pc < P) ? (unsigned)(m * P + pc) * 4u : kOut;
+    }
+  // the outputs of a row block: lane (li, lg) holds token 16 tb + li, columns cg 16 + 4 lg .. + 3
+  unsigned yoff[4];
+#pragma unroll
+  for (int tb = 0; tb < 4; ++tb) {
+    const int col = cg * 16 + lg * 4;
+    yoff[tb] = (active && p0 + col < P) ? (unsigned)(tb * 16 + li) * xs_b + (unsigned)(col * ES) : kOut;
+  }
+
+  // ---- prologue: the log-decays of chunks 0 and 1, then the weights of chunk 0
+  float d1 = 0.0f, a1 = 1.0f;
+  if (producer) {
+    load_controls(0);
+    w_dtt = eff_step(0);
+    w_al = al_q;
+    load_controls(1);
+    load_logits(0);
+  } else {
+    load_x(0);
+  }
+  __syncthreads();  // the rates and scales in LDS
+  if (producer) {
+    log_decays(0, w_dtt);
+    d1 = eff_step(1);
+    a1 = al_q;
+    log_decays(1, d1);
+    load_controls(2);
+  }
+  __syncthreads();  // the first log-decays in LDS
+  if (producer) {
+    weights(0);
+    w_dtt = d1;
+    w_al = a1;
+    load_logits(1);
+  }
+  __syncthreads();  // the weights of chunk 0 in LDS
+
+  for (int it = 0; it <= nchunks; ++it) {
+    if (producer) {
+      // log-decays of chunk it + 2 from the controls loaded one iteration ago
+      const float ld_dtt = eff_step(it + 2), ld_al = al_q;
+      if (it + 2 < nchunks) log_decays(it + 2, ld_dtt);
+      if (it + 1 < nchunks) weights(it + 1);
+      if (it < nchunks)
+        for (int tile = pw; tile < 10; tile += NPW) gamma(it, tile);
+      w_dtt = ld_dtt;
+      w_al = ld_al;
+      load_controls(it + 3);
+      load_logits(it + 2);
+    } else {
+      if (it >= 1) {
+      const int c = it - 1, slot = c % 3;
+      const int nv = nv_of(c);
+      const T* Gs = Gb[c & 1];
+      const T* Om = Omb[slot];
+      const T* Vm = Vmb[slot];
+      // x of the chunk into this wave's columns of LDS (lane = token)
+#pragma unroll
+      for (int v = 0; v < XV; ++v) *reinterpret_cast<int4*>(Xs + lane * XS + cg * 16 + v * (16 / ES)) = xr[v];
+      load_x(c + 1);
+      if (ckpt) {  // the state entering this chunk
+        const auto rk = rsrc(ckpt + ((int64_t)bh * (nchunks + 1) + c) * M * P, M * P * 4);
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int m = mb * 16 + lg * 4 + r;
+            const float v = S[mb][r] * s_Ein[slot][m < MP ? m : 0];
+            __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(int, v), rk, ckoff[mb * 4 + r], 0, 0);
+          }
+      }
+      Frag<T> Sf;  // the state as a B operand: slot s < 4 mode 4 lg + s, s >= 4 mode 16 + 4 lg + s - 4
+#pragma unroll
+      for (int s = 0; s < 4; ++s) frag_set(Sf, s, S[0][s]);
+#pragma unroll
+      for (int s = 0; s < 4; ++s) frag_set(Sf, 4 + s, MB > 1 ? S[MB - 1][s] : 0.0f);
+      const auto ry = rsrc(yg + (int64_t)c * kQ * xstride, span(nv, xs_b, xtail));
+#pragma unroll
+      for (int tb = 0; tb < 4; ++tb) {
+        const int t = tb * 16 + li;
+        floatx4 Y = {0.f, 0.f, 0.f, 0.f};  // transposed products: token t, columns cg 16 + 4 lg .. + 3
+        const Frag<T> Of = (lg * 4 < MP) ? frag_load4x2(Om + t * OS + lg * 4, Om + t * OS + 16 + lg * 4, MB > 1)
+                                         : frag_zero<T>();
+        mma(Y, Sf, Of);
+#pragma unroll
+        for (int kk = 0; kk <= tb / 2; ++kk)
+          mma(Y, frag_load_rows(Xs, XS, kk * 32 + lg * 8, cg * 16), frag_load8(Gs + t * GS + kk * 32 + lg * 8));
+        float xv[4];
+        load4(Xs + t * XS + cg * 16 + lg * 4, xv);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) Y[r] += Dh * xv[r];
+        if constexpr (kBf16) {
+          const bf16x4 o = bf16x4{(bf16)Y[0], (bf16)Y[1], (bf16)Y[2], (bf16)Y[3]};
+          __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(u32x2_t, o), ry, yoff[tb], 0, 0);
+        } else {
+          __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(i32x4_t, Y), ry, yoff[tb], 0, 0);
+        }
+      }
+      // ---- state update S_m <- (rescale) S_m + V^T x
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int m = mb * 16 + lg * 4 + r;
+          if (m < MP) S[mb][r] *= s_ren[slot][m];
+        }
+#pragma unroll
+      for (int kt = 0; kt < 2; ++kt) {
+        const Frag<T> bx = frag_load_rows(Xs, XS, kt * 32 + lg * 8, cg * 16);
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb) {
+          const int m = mb * 16 + li;
+          const Frag<T> Vf = (m < MP) ? frag_load8(Vm + m * VS + kt * 32 + lg * 8) : frag_zero<T>();
+          mma(S[mb], Vf, bx);
+        }
+      }
+      }  // it >= 1
+    }
+    __syncthreads();  // this iteration's log-decays, weights and Gamma in LDS
+  }
+
+  float* fin_ck = ckpt ? ckpt + ((int64_t)bh * (nchunks + 1) + nchunks) * M * P : nullptr;
+  float* fin = p.final_state ? p.final_state + sbase : nullptr;
+  if ((fin || fin_ck) && active) {
+    const float* Ef = s_E[nchunks & 1];  // the scale after the last chunk (written by its weights)
 #pragma unroll
     for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
@@ -1038,9 +1432,17 @@ hipError_t launch_nfree_fwd_nw(const ScanParams& p, float* ckpt, hipStream_t str
 template <typename T, int MP, bool CKPT>
 hipError_t launch_nfree_fwd(const ScanParams& p, float* ckpt, hipStream_t stream) {
   if (nfree_cols(p) == 128) {
-    if constexpr (CKPT) return launch_nfree_fwd_nw<T, MP, CKPT, 8>(p, ckpt, stream);
-    else if constexpr (sizeof(T) == 4 && MP > 16) return launch_nfree_fwd_nw<T, MP, CKPT, 4>(p, ckpt, stream);
-    else return launch_nfree_fwd_nw<T, MP, CKPT, 16, 2>(p, ckpt, stream);
+    if constexpr (CKPT) {
+      return launch_nfree_fwd_nw<T, MP, CKPT, 8>(p, ckpt, stream);
+    } else if constexpr (MP <= 16) {
+      const unsigned blocks = (unsigned)((int64_t)p.Bsz * p.H * ((p.P + 127) / 128));
+      hipLaunchKernelGGL((frac_nfree_fwd_split_kernel<T, MP>), dim3(blocks), dim3(1024), 0, stream, p, ckpt);
+      return hipGetLastError();
+    } else if constexpr (sizeof(T) == 4) {
+      return launch_nfree_fwd_nw<T, MP, CKPT, 4>(p, ckpt, stream);
+    } else {
+      return launch_nfree_fwd_nw<T, MP, CKPT, 16, 2>(p, ckpt, stream);
+    }
   }
   return launch_nfree_fwd_nw<T, MP, CKPT, 4>(p, ckpt, stream);
 }
