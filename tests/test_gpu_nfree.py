@@ -62,6 +62,13 @@ SMALL = {
     "bf16 M32 P256": Workload("t", 1, 150, 2, 256, 1, 32, bc=False, final_state=True, init_state=True),
     "f32 M16 P256 extras": Workload("t", 1, 130, 2, 256, 1, 16, bc=False, io_dtype="f32", extras=True,
                                     final_state=True),
+    # the forward whose weights run ahead of the state: one chunk, two, and a ragged
+    # last group of columns (a single 16-column group with outputs)
+    "bf16 M16 P256 L64 extras": Workload("t", 2, 64, 2, 256, 1, 16, bc=False, extras=True, init_state=True,
+                                         final_state=True),
+    "bf16 M8 P256 L65": Workload("t", 1, 65, 2, 256, 1, 8, bc=False, init_state=True, final_state=True),
+    "f32 M4 P136 ragged extras": Workload("t", 1, 129, 2, 136, 1, 4, bc=False, io_dtype="f32", extras=True,
+                                          init_state=True, final_state=True),
 }
 
 
