@@ -499,7 +499,7 @@ __global__ void __launch_bounds__(1024) frac_nfree_fwd_split_kernel(ScanParams p
   constexpr int NPR = (kQ * MP + NPT - 1) / NPT;
   float dt_q = 0.0f, al_q = 1.0f, lam_q = 1.0f;
   float w_dtt = 0.0f, w_al = 1.0f;
-  float rlr[NPR], wlr[NPR];
+  float rlr[NPR] = {}, wlr[NPR] = {};
   unsigned loff[NPR];
 #pragma unroll
   for (int j = 0; j < NPR; ++j) {
@@ -510,24 +510,29 @@ __global__ void __launch_bounds__(1024) frac_nfree_fwd_split_kernel(ScanParams p
     const int t0 = c * kQ, nv = nv_of(c);
     const auto rd = rsrc(dt_bh + (int64_t)t0 * H, span(nv, (int64_t)H * 4, 4));
     const auto ra = rsrc(al_bh + (int64_t)t0 * p.as1, span(nv, (int64_t)p.as1 * 4, 4));
-    const auto rl = rsrc(lm_bh ? lm_bh + (int64_t)t0 * p.ls1 : p.tau, lm_bh ? span(nv, (int64_t)p.ls1 * 4, 4) : 0);
     dt_q = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rd, (unsigned)(lane * H) * 4u, 0, 0));
     al_q = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(ra, (unsigned)(lane * p.as1) * 4u, 0, 0));
-    lam_q = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rl, (unsigned)(lane * p.ls1) * 4u, 0, 0));
+    if (lm_bh) {  // read only where lambda is given (the value is used only then)
+      const auto rl = rsrc(lm_bh + (int64_t)t0 * p.ls1, span(nv, (int64_t)p.ls1 * 4, 4));
+      lam_q = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rl, (unsigned)(lane * p.ls1) * 4u, 0, 0));
+    }
   };
   auto eff_step = [&](int c) {
     const float s_eff = lm_bh ? step_factor(lam_q, al_q) : 1.0f;
     return (lane < nv_of(c)) ? dt_q * s_eff : 0.0f;
   };
-  auto load_logits = [&](int c) {
+  auto load_logits = [&](int c) {  // read only where given (the values are used only then)
     const int t0 = c * kQ, nv = nv_of(c);
     const int lb = span(nv, (int64_t)H * M * 4, (int64_t)M * 4);
-    const auto rr = rsrc(rl_bh ? rl_bh + (int64_t)t0 * lg_st : p.tau, rl_bh ? lb : 0);
-    const auto rw = rsrc(own_wl ? wl_bh + (int64_t)t0 * lg_st : p.tau, own_wl ? lb : 0);
+    if (rl_bh) {
+      const auto rr = rsrc(rl_bh + (int64_t)t0 * lg_st, lb);
 #pragma unroll
-    for (int j = 0; j < NPR; ++j) {
-      rlr[j] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rr, loff[j], 0, 0));
-      wlr[j] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rw, loff[j], 0, 0));
+      for (int j = 0; j < NPR; ++j) rlr[j] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rr, loff[j], 0, 0));
+    }
+    if (own_wl) {
+      const auto rw = rsrc(wl_bh + (int64_t)t0 * lg_st, lb);
+#pragma unroll
+      for (int j = 0; j < NPR; ++j) wlr[j] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rw, loff[j], 0, 0));
     }
   };
   // the per-mode log-decays of chunk c from this lane's effective step (producer wave pw: modes pw, pw + 8, ..)
@@ -566,8 +571,8 @@ __global__ void __launch_bounds__(1024) frac_nfree_fwd_split_kernel(ScanParams p
       const float dtt = __shfl(w_dtt, t, 64), al = __shfl(w_al, t, 64);
       const bool valid = t < nv;
       const float prior = -al * wlnt;
-      const float zc = (m < M) ? prior + rlr[j] : -INFINITY;
-      const float zw = (m < M) ? prior + wlr[j] : -INFINITY;
+      const float zc = (m < M) ? prior + (rl_bh ? rlr[j] : 0.0f) : -INFINITY;
+      const float zw = (m < M) ? prior + (own_wl ? wlr[j] : 0.0f) : -INFINITY;
       const float lhQ = P_lh[m * WQ + kQ - 1], llQ = P_ll[m * WQ + kQ - 1];
       const float Ec = Ecur[m];
       const float Enew = Ec * fexp(-lhQ);
