@@ -421,12 +421,12 @@ __global__ void __launch_bounds__(64 * NW) frac_nfree_fwd_kernel(ScanParams p, f
 //
 // Head dims above 128: one workgroup of 16 waves per (batch, head, 128 columns),
 // in two roles with one barrier per iteration.  Producer waves 8 .. 15 form, in
-// iteration i, the log-decays of chunk i + 2, the weights of chunk i + 1 (from the
-// log-decays formed one iteration earlier) and the Gamma tiles of chunk i (from the
-// weights formed one iteration earlier).  Consumer waves 0 .. 7 each own 16 columns
-// and, in iteration i, run chunk i - 1: x into their own columns of LDS, readout,
-// intra-chunk product and skip term (outputs stored from registers), the state
-// update.  The per-chunk work that does not depend on the state thus overlaps the
+// iteration i, the weights of chunk i + 1 (from the log-decays formed one iteration
+// earlier) and the Gamma tiles of chunk i (from the weights formed one iteration
+// earlier).  Consumer waves 0 .. 7 form the log-decays of chunk i + 2 (two modes
+// each), and each owns 16 columns where, in iteration i, it runs chunk i - 1: x
+// into its own columns of LDS, readout, intra-chunk product and skip term (outputs
+// stored from registers), the state update.  The per-chunk work that does not depend on the state thus overlaps the
 // recurrence; buffers are kept for as many chunks as are in flight (log-decays,
 // readout and update weights: three; Gamma and its factors: two).
 template <typename T, int MP>
@@ -461,6 +461,7 @@ __global__ void __launch_bounds__(1024) frac_nfree_fwd_split_kernel(ScanParams p
   __shared__ float s_Ein[3][MP];                   // the state scale entering chunk j
   __shared__ float s_E[2][MP];                     // the running state scale (producers)
   __shared__ float s_rr[MP];
+  __shared__ float s_dtt[3][kQ], s_al[3][kQ];      // effective step and order of chunk j's tokens in slot j % 3
 
   for (int i = tid; i < 2 * 64 * GS; i += 1024) (&Gb[0][0])[i] = (T)0.0f;  // tiles above the diagonal stay zero
   const int wm = (producer ? pt : tid) % MP;
@@ -497,8 +498,7 @@ __global__ void __launch_bounds__(1024) frac_nfree_fwd_split_kernel(ScanParams p
   // ---- producer state: raw controls two chunks ahead (lane = token), the effective
   // step and order of the chunk whose weights come next, the logits of those weights
   constexpr int NPR = (kQ * MP + NPT - 1) / NPT;
-  float dt_q = 0.0f, al_q = 1.0f, lam_q = 1.0f;
-  float w_dtt = 0.0f, w_al = 1.0f;
+  float dt_q = 0.0f, al_q = 1.0f, lam_q = 1.0f;  // raw controls of a chunk two ahead (consumers, lane = token)
   float rlr[NPR] = {}, wlr[NPR] = {};
   unsigned loff[NPR];
 #pragma unroll
@@ -535,12 +535,17 @@ __global__ void __launch_bounds__(1024) frac_nfree_fwd_split_kernel(ScanParams p
       for (int j = 0; j < NPR; ++j) wlr[j] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rw, loff[j], 0, 0));
     }
   };
-  // the per-mode log-decays of chunk c from this lane's effective step (producer wave pw: modes pw, pw + 8, ..)
-  auto log_decays = [&](int c, float dtt) {
+  // the per-mode log-decays of chunk c from this lane's effective step (wave wi of
+  // eight: modes wi, wi + 8, ..), and the token's step and order for the weights
+  auto log_decays = [&](int c, float dtt, float al, int wi) {
     float* lh = LDb[c % 3];
+    if (wi == 0) {
+      s_dtt[c % 3][lane] = dtt;
+      s_al[c % 3][lane] = al;
+    }
 #pragma unroll
     for (int m0 = 0; m0 < MP; m0 += NPW) {
-      const int m = m0 + pw;
+      const int m = m0 + wi;
       if (m0 + NPW > MP && m >= MP) break;  // wave-uniform
       const double v = wave_inclusive_sum_f64((double)capped_exponent(s_rr[m], dtt));
       const float hi = (float)v;
@@ -568,7 +573,7 @@ __global__ void __launch_bounds__(1024) frac_nfree_fwd_split_kernel(ScanParams p
     for (int j = 0; j < NPR; ++j) {
       const int pr = pt + NPT * j, t = pr / MP, m = wm;
       if (pr >= kQ * MP) break;  // wave-uniform
-      const float dtt = __shfl(w_dtt, t, 64), al = __shfl(w_al, t, 64);
+      const float dtt = s_dtt[c % 3][t], al = s_al[c % 3][t];
       const bool valid = t < nv;
       const float prior = -al * wlnt;
       const float zc = (m < M) ? prior + (rl_bh ? rlr[j] : 0.0f) : -INFINITY;
@@ -685,47 +690,37 @@ __global__ void __launch_bounds__(1024) frac_nfree_fwd_split_kernel(ScanParams p
     yoff[tb] = (active && p0 + col < P) ? (unsigned)(tb * 16 + li) * xs_b + (unsigned)(col * ES) : kOut;
   }
 
-  // ---- prologue: the log-decays of chunks 0 and 1, then the weights of chunk 0
-  float d1 = 0.0f, a1 = 1.0f;
+  // ---- prologue: the log-decays of chunks 0 and 1 (consumers), then the weights of chunk 0
   if (producer) {
-    load_controls(0);
-    w_dtt = eff_step(0);
-    w_al = al_q;
-    load_controls(1);
     load_logits(0);
   } else {
     load_x(0);
+    load_controls(0);
   }
   __syncthreads();  // the rates and scales in LDS
-  if (producer) {
-    log_decays(0, w_dtt);
-    d1 = eff_step(1);
-    a1 = al_q;
-    log_decays(1, d1);
+  if (!producer) {
+    log_decays(0, eff_step(0), al_q, cg);
+    load_controls(1);
+    log_decays(1, eff_step(1), al_q, cg);
     load_controls(2);
   }
   __syncthreads();  // the first log-decays in LDS
   if (producer) {
     weights(0);
-    w_dtt = d1;
-    w_al = a1;
     load_logits(1);
   }
   __syncthreads();  // the weights of chunk 0 in LDS
 
   for (int it = 0; it <= nchunks; ++it) {
     if (producer) {
-      // log-decays of chunk it + 2 from the controls loaded one iteration ago
-      const float ld_dtt = eff_step(it + 2), ld_al = al_q;
-      if (it + 2 < nchunks) log_decays(it + 2, ld_dtt);
       if (it + 1 < nchunks) weights(it + 1);
       if (it < nchunks)
         for (int tile = pw; tile < 10; tile += NPW) gamma(it, tile);
-      w_dtt = ld_dtt;
-      w_al = ld_al;
-      load_controls(it + 3);
       load_logits(it + 2);
     } else {
+      // log-decays of chunk it + 2 from the controls loaded one iteration ago
+      if (it + 2 < nchunks) log_decays(it + 2, eff_step(it + 2), al_q, cg);
+      load_controls(it + 3);
       if (it >= 1) {
       const int c = it - 1, slot = c % 3;
       const int nv = nv_of(c);
