@@ -429,8 +429,11 @@ __global__ void __launch_bounds__(64 * NW) frac_nfree_fwd_kernel(ScanParams p, f
 // stored from registers), the state update.  The per-chunk work that does not depend on the state thus overlaps the
 // recurrence; buffers are kept for as many chunks as are in flight (log-decays,
 // readout and update weights: three; Gamma and its factors: two).
-template <typename T, int MP>
-__global__ void __launch_bounds__(1024) frac_nfree_fwd_split_kernel(ScanParams p, float* __restrict__ ckpt) {
+// KEEP: ckpt receives the state entering every chunk and the final state (the
+// caller's kept chunk states); without it ckpt is not read.
+template <typename T, int MP, bool KEEP>
+__global__ void __launch_bounds__(1024) frac_nfree_fwd_split_kernel(ScanParams p, float* __restrict__ ckpt_arg) {
+  float* const ckpt = KEEP ? ckpt_arg : nullptr;
   constexpr bool kBf16 = sizeof(T) == 2;
   constexpr int MB = (MP + 15) / 16;
   constexpr int CW = 128, NPW = 8, NPT = 64 * NPW;  // columns, producer waves, producer threads
@@ -682,6 +685,18 @@ __global__ void __launch_bounds__(1024) frac_nfree_fwd_split_kernel(ScanParams p
       const int m = mb * 16 + lg * 4 + r;
       ckoff[mb * 4 + r] = (active && m < M && pc < P) ? (unsigned)(m * P + pc) * 4u : kOut;
     }
+  // the state scaled by E, as the state entering chunk c (slot c of the kept states)
+  auto store_state = [&](int c, const float* E) {
+    const auto rk = rsrc(ckpt + ((int64_t)bh * (nchunks + 1) + c) * M * P, M * P * 4);
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int m = mb * 16 + lg * 4 + r;
+        const float v = S[mb][r] * E[m < MP ? m : 0];
+        __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(int, v), rk, ckoff[mb * 4 + r], 0, 0);
+      }
+  };
   // the outputs of a row block: lane (li, lg) holds token 16 tb + li, columns cg 16 + 4 lg .. + 3
   unsigned yoff[4];
 #pragma unroll
@@ -710,6 +725,9 @@ __global__ void __launch_bounds__(1024) frac_nfree_fwd_split_kernel(ScanParams p
     load_logits(1);
   }
   __syncthreads();  // the weights of chunk 0 in LDS
+  if constexpr (KEEP) {
+    if (!producer) store_state(0, s_Ein[0]);  // the initial state (scale 1)
+  }
 
   for (int it = 0; it <= nchunks; ++it) {
     if (producer) {
@@ -731,17 +749,6 @@ __global__ void __launch_bounds__(1024) frac_nfree_fwd_split_kernel(ScanParams p
 #pragma unroll
       for (int v = 0; v < XV; ++v) *reinterpret_cast<int4*>(Xs + lane * XS + cg * 16 + v * (16 / ES)) = xr[v];
       load_x(c + 1);
-      if (ckpt) {  // the state entering this chunk
-        const auto rk = rsrc(ckpt + ((int64_t)bh * (nchunks + 1) + c) * M * P, M * P * 4);
-#pragma unroll
-        for (int mb = 0; mb < MB; ++mb)
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const int m = mb * 16 + lg * 4 + r;
-            const float v = S[mb][r] * s_Ein[slot][m < MP ? m : 0];
-            __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(int, v), rk, ckoff[mb * 4 + r], 0, 0);
-          }
-      }
       Frag<T> Sf;  // the state as a B operand: slot s < 4 mode 4 lg + s, s >= 4 mode 16 + 4 lg + s - 4
 #pragma unroll
       for (int s = 0; s < 4; ++s) frag_set(Sf, s, S[0][s]);
@@ -786,6 +793,11 @@ __global__ void __launch_bounds__(1024) frac_nfree_fwd_split_kernel(ScanParams p
           const Frag<T> Vf = (m < MP) ? frag_load8(Vm + m * VS + kt * 32 + lg * 8) : frag_zero<T>();
           mma(S[mb], Vf, bx);
         }
+      }
+      // the state entering the next chunk, stored at the end of this one (a wait for
+      // the loads issued at its start would also wait for these stores)
+      if constexpr (KEEP) {
+        if (c + 1 < nchunks) store_state(c + 1, s_Ein[(c + 1) % 3]);
       }
       }  // it >= 1
     }
@@ -1436,7 +1448,10 @@ hipError_t launch_nfree_fwd(const ScanParams& p, float* ckpt, hipStream_t stream
       return launch_nfree_fwd_nw<T, MP, CKPT, 8>(p, ckpt, stream);
     } else if constexpr (MP <= 16) {
       const unsigned blocks = (unsigned)((int64_t)p.Bsz * p.H * ((p.P + 127) / 128));
-      hipLaunchKernelGGL((frac_nfree_fwd_split_kernel<T, MP>), dim3(blocks), dim3(1024), 0, stream, p, ckpt);
+      if (ckpt)
+        hipLaunchKernelGGL((frac_nfree_fwd_split_kernel<T, MP, true>), dim3(blocks), dim3(1024), 0, stream, p, ckpt);
+      else
+        hipLaunchKernelGGL((frac_nfree_fwd_split_kernel<T, MP, false>), dim3(blocks), dim3(1024), 0, stream, p, ckpt);
       return hipGetLastError();
     } else if constexpr (sizeof(T) == 4) {
       return launch_nfree_fwd_nw<T, MP, CKPT, 4>(p, ckpt, stream);
