@@ -375,7 +375,7 @@ def measured_traffic(entry, workload):
 _ENTRY_KERNELS = {"frac_scan_bwd": ("frac_cb_kernel", "frac_bwd_", "frac_grad_", "frac_nfree_fwd_kernel<bf16,16,1",
                                     "frac_nfree_bwd_"),
                   "frac_scan_fwd": ("frac_cb_kernel", "frac_fwd_", "frac_seg_combine", "frac_mode_lse",
-                                    "frac_nfree_fwd_kernel<bf16,16,0", "frac_nfree_fwd_split_kernel<bf16,16>")}
+                                    "frac_nfree_fwd_kernel<bf16,16,0", "frac_nfree_fwd_split_kernel<bf16,16,")}
 
 
 def measured_mfma_busy(entry, workload):
