@@ -89,6 +89,14 @@ def test_paper_form_paper_range_steps_match_the_oracle(io):
 
 
 @pytest.mark.parametrize("io", ["f32", "bf16"])
+def test_paper_form_paper_range_steps_wide_heads(io):
+    """Head dim 256: the forward whose weights run ahead of the state (and its
+    Gamma tiles with one exponential per pair for the modes past the factorisation
+    bound) and the 128-column backward."""
+    _run_case(io, False, 1, 200, 2, 256, 1, 16, seed=5)
+
+
+@pytest.mark.parametrize("io", ["f32", "bf16"])
 def test_bc_form_paper_range_steps_match_the_oracle(io):
     _run_case(io, True, 1, 160, 2, 32, 16, 8, seed=1)
 

@@ -87,9 +87,10 @@ def test_nfree_fwd_parity(name):
         assert_close("final_state mode %d" % m, f64(fs)[:, :, m], fsr[:, :, m], tol)
 
 
-def test_nfree_large_steps_use_direct_decay():
+@pytest.mark.parametrize("P", [64, 256])
+def test_nfree_large_steps_use_direct_decay(P):
     """Steps large enough that the fast modes pass the factorisation bound."""
-    w = Workload("t", 1, 140, 2, 64, 1, 16, bc=False, final_state=True)
+    w = Workload("t", 1, 140, 2, P, 1, 16, bc=False, final_state=True)
     inp = device_inputs(w, seed=12)
     inp["dt"] = (inp["dt"] * 8.0).contiguous()
     tau_d, tau64 = _tau(16)
