@@ -419,16 +419,17 @@ __global__ void __launch_bounds__(64 * NW) frac_nfree_fwd_kernel(ScanParams p, f
 
 // ------------------------------------------------ forward, split waves
 //
-// Head dims above 128: one workgroup of 16 waves per (batch, head, 128 columns),
-// in two roles with one barrier per iteration.  Producer waves 8 .. 15 form, in
-// iteration i, the weights of chunk i + 1 (from the log-decays formed one iteration
-// earlier) and the Gamma tiles of chunk i (from the weights formed one iteration
-// earlier).  Consumer waves 0 .. 7 form the log-decays of chunk i + 2 (two modes
-// each), and each owns 16 columns where, in iteration i, it runs chunk i - 1: x
-// into its own columns of LDS, readout, intra-chunk product and skip term (outputs
-// stored from registers), the state update.  The per-chunk work that does not depend on the state thus overlaps the
-// recurrence; buffers are kept for as many chunks as are in flight (log-decays,
-// readout and update weights: three; Gamma and its factors: two).
+// Head dims above 128 with up to 16 modes: one workgroup of 16 waves per (batch,
+// head, 128 columns), in two roles with one barrier per iteration.  Producer waves
+// 8 .. 15 form, in iteration i, the weights of chunk i + 1 (from the log-decays
+// formed one iteration earlier) and the Gamma tiles of chunk i (from the weights
+// formed one iteration earlier).  Consumer waves 0 .. 7 form the log-decays of
+// chunk i + 2 (two modes each), and each owns 16 columns where, in iteration i, it
+// runs chunk i - 1: x into its own columns of LDS, readout, intra-chunk product and
+// skip term (outputs stored from registers), the state update.  The per-chunk work
+// that does not depend on the state thus overlaps the recurrence; buffers are kept
+// for as many chunks as are in flight (log-decays, readout and update weights:
+// three; Gamma and its factors: two).
 // KEEP: ckpt receives the state entering every chunk and the final state (the
 // caller's kept chunk states); without it ckpt is not read.
 template <typename T, int MP, bool KEEP>
